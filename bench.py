@@ -1,0 +1,213 @@
+"""Throughput of the exact factored output-layer step on one GPU, with its roofline,
+the naive O(D d) path and the fp64 CPU oracle as baselines.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+
+A step is one pass of the whole factored step (dense contractions, sparse
+gather, loss and grad_H, the m x m Woodbury block, the U / U^{-T} / Q updates
+and the V scatter) over one minibatch already resident in HBM.  Prints one JSON
+line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP32_TFLOPS = 157.3      # MI355X dense fp32 matrix (and vector) peak
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+METRIC = "examples/s exact loss+grad+update, D=200k d=500 m=128; speedup vs naive O(Dd)"
+
+
+def phase_work(w, idx_pool):
+    """Algorithmic work per launch of each phase: (bound, amount, unit-of-amount)."""
+    m, d, K = w.m, w.d, w.K
+    uniq = float(np.mean([len(np.unique(i[i >= 0])) for i in idx_pool]))
+    return {
+        # MACs x 2: H^, H~, X = {Q,U,U^-T} H and H^T H
+        "contract": ("mfma", 2.0 * (3 * m * d * d + m * m * d), "flop"),
+        # V rows of the targets, H, H^, H~ read; G and the scaled H~ written
+        "gather": ("hbm", 4.0 * (m * K * d + 5 * m * d), "byte"),
+        # Z^ = U^T G, H^T H^, H~^T G
+        "zgrad": ("mfma", 2.0 * (m * d * d + 2 * m * m * d), "flop"),
+        # Gauss-Jordan inverse of the m x m Woodbury matrix and the M entries
+        "small": ("alu", 2.0 * m ** 3 + 8.0 * m * m, "flop"),
+        # R X, M H, U update
+        "mid": ("mfma", 2.0 * (m * d * d + 2 * m * m * d), "flop"),
+        # U^-T update, Q update (two products), P
+        "update": ("mfma", 2.0 * (3 * m * d * d + m * m * d), "flop"),
+        # read-modify-write of the distinct target rows and the P rows they use
+        "scatter": ("hbm", 4.0 * (2 * uniq * d + m * d), "byte"),
+    }
+
+
+def roofline_for(phases, work, steps):
+    # dominant phase = largest total time
+    name = max(work, key=lambda p: phases[p][1])
+    cnt, ms = phases[name]
+    avg_s = ms / max(cnt, 1) / 1e3
+    bound, amount, _ = work[name]
+    if bound == "hbm":
+        achieved = amount / avg_s / 1e9
+        peak, unit = PEAK_HBM_GBS, "GB/s"
+    else:
+        achieved = amount / avg_s / 1e12
+        peak, unit = PEAK_FP32_TFLOPS, "TFLOP/s"
+    return {"kernel_phase": name, "bound": bound, "achieved": round(achieved, 4), "peak": peak,
+            "unit": unit, "frac": round(achieved / peak, 5), "traffic": None,
+            "avg_launch_us": round(avg_s * 1e6, 3), "algorithmic_per_launch": amount}
+
+
+def cpu_baseline(w, V0, pool, seconds):
+    from threadpoolctl import threadpool_info
+
+    from oracle import dense_step
+
+    W = V0.astype(np.float64)
+    H, idx, val = pool[0]
+    dense_step(W, H, idx, val, np.float32(w.lr), w.loss, np.float32(w.eps))  # warm-up
+    n = 0
+    t0 = time.perf_counter()
+    while True:
+        H, idx, val = pool[(n + 1) % len(pool)]
+        W = dense_step(W, H, idx, val, np.float32(w.lr), w.loss, np.float32(w.eps)).W_new
+        n += 1
+        el = time.perf_counter() - t0
+        if (el >= seconds and n >= 2) or n >= 200:
+            break
+    blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+    cores = int(blas[0]["num_threads"]) if blas else 1
+    return {"value": round(w.m * n / el, 3), "unit": "examples/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"{n} dense fp64 steps of {w.name} (D={w.D}, d={w.d}, m={w.m}) after 1 "
+                      f"warm-up step, {el:.1f} s; nproc={os.cpu_count()}, "
+                      f"affinity={len(os.sched_getaffinity(0))}"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="sq_D200k_d500_m128_K5")
+    ap.add_argument("--pool", type=int, default=64, help="distinct minibatches cycled through")
+    ap.add_argument("--naive-steps", type=int, default=20)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-naive", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on exactly one GPU: the factored step is measured on one GPU's "
+              "share (multi-GPU sharding of V by rows is described but not built)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_1606_08061_amd as lst
+    from workloads import WORKLOADS, Stream
+
+    if not torch.cuda.is_available():
+        raise RuntimeError("no GPU visible")
+    lst.lib()  # fails loudly when the HIP library is not built
+    w = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+
+    print(f"[bench] generating {w.name}", file=sys.stderr, flush=True)
+    s = Stream(w)
+    pool = [s.batch() for _ in range(args.pool)]
+    gpool = [[torch.from_numpy(a).to(dev) for a in b] for b in pool]
+    V0 = torch.from_numpy(s.V0).to(dev)
+
+    # ---- factored path ----
+    f = lst.Factored(w.D, w.d, w.m, w.K, w.loss, float(np.float32(w.eps)), device=dev)
+    f.init(V0)
+    for t in range(args.warmup):
+        f.step(*gpool[t % len(gpool)], w.lr, want_grad=False)
+    grad = torch.empty((w.m, w.d), dtype=torch.float32, device=dev)
+    f.check("warm-up")
+    print("[bench] factored timed region", file=sys.stderr, flush=True)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for t in range(args.steps):
+        f.step(*gpool[t % len(gpool)], w.lr, grad_H=grad)
+    e1.record()
+    torch.cuda.synchronize()
+    ms_total = e0.elapsed_time(e1)
+    f.check("timed steps")
+    ms_step = ms_total / args.steps
+    value = w.m * args.steps / (ms_total / 1e3)
+
+    # per-phase HIP events over a second region of the same length
+    f.profile(True)
+    for t in range(args.steps):
+        f.step(*gpool[t % len(gpool)], w.lr, grad_H=grad)
+    phases = f.profile_read()
+    f.profile(False)
+    f.check("profiled steps")
+    work = phase_work(w, [b[1] for b in pool])
+    roof = roofline_for(phases, work, args.steps)
+    f.close()
+    del f
+
+    # ---- naive O(D d) path on the same batches ----
+    naive = None
+    if not args.no_naive:
+        print("[bench] naive timed region", file=sys.stderr, flush=True)
+        n = lst.Naive(w.D, w.d, w.m, w.K, w.loss, float(np.float32(w.eps)), device=dev)
+        n.init(V0)
+        for t in range(2):
+            n.step(*gpool[t % len(gpool)], w.lr, grad_H=grad)
+        torch.cuda.synchronize()
+        e0.record()
+        for t in range(args.naive_steps):
+            n.step(*gpool[t % len(gpool)], w.lr, grad_H=grad)
+        e1.record()
+        torch.cuda.synchronize()
+        n.check("naive steps")
+        nms = e0.elapsed_time(e1) / args.naive_steps
+        n.profile(True)
+        for t in range(args.naive_steps):
+            n.step(*gpool[t % len(gpool)], w.lr, grad_H=grad)
+        nph = n.profile_read()
+        n.close()
+        del n
+        naive = {"value": round(w.m / (nms / 1e3), 2), "unit": "examples/s",
+                 "ms_per_step": round(nms, 4),
+                 "phases_us": {k: round(v[1] / max(v[0], 1) * 1e3, 2)
+                               for k, v in nph.items() if v[0] and k.startswith("naive")}}
+
+    del V0, gpool
+    torch.cuda.empty_cache()
+    cpu = None
+    if not args.no_cpu:
+        print("[bench] cpu baseline (fp64 oracle)", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(w, s.V0, pool, args.cpu_seconds)
+
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "examples/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "loss": w.loss, "D": w.D, "d": w.d, "m": w.m, "K": w.K,
+                   "index_dist": w.index_dist, "lr": w.lr, "distinct_batches": args.pool},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "naive": naive,
+        "speedup_vs_naive": round(value / naive["value"], 2) if naive else None,
+        "speedup_model_D_over_4d": round(w.D / (4 * w.d), 1),
+        "phases_us": {k: round(v[1] / max(v[0], 1) * 1e3, 2) for k, v in phases.items() if v[0]},
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

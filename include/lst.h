@@ -1,0 +1,200 @@
+/*
+ * lst.h -- exact output-layer training step for very large sparse targets on gfx950.
+ *
+ * Method: Vincent, de Brebisson, Bouthillier, "Exact gradient updates in time
+ * independent of output size for the spherical loss family" (arXiv 1606.08061).
+ * The D x d output weights are kept factored as W = V U (section 3.2), with the
+ * bookkeeping matrices Q = W^T W (section 3.4) and U^{-T} (eq. updateU-T,
+ * Woodbury for minibatches, section 3.6 / 4.7).  One step (Algorithm 3 for
+ * squared error, Algorithm 4 for the spherical family) computes the exact
+ * minibatch loss, its gradient with respect to the hidden layer H and the full
+ * gradient update of the implicit W in O(m d^2 + m^2 d + m^3 + m K d), touching
+ * only the m*K target rows of V.  A naive O(D d) path with the same step
+ * contract (sections 2.3 and 4.3) is provided for comparison.
+ *
+ * Conventions shared by every entry point
+ *   - Memory: every float / int pointer is a DEVICE pointer owned by the caller
+ *     (allocated with the HIP runtime, e.g. through PyTorch), except where a
+ *     parameter says "host".  The library never frees caller memory.  A context
+ *     allocates its own device workspace in lst_create / lst_naive_create and
+ *     frees it in lst_destroy.
+ *   - Layout: row-major.  A minibatch H is m x d, one example per row (the same
+ *     bytes as the paper's d x m H with one example per column).  V and W are
+ *     D x d with row stride ldv / ldw >= d (floats); U, U^{-T} and Q are d x d
+ *     with row stride ldd >= d.
+ *   - Targets: idx and val are m x K (row stride K).  idx holds 0-based row
+ *     indices in [0, D); -1 marks an empty slot (the paper's "at most K"
+ *     non-zeros).  An index repeated inside one example adds its values
+ *     (y = sum_k val_k onehot(idx_k)); repeated indices across examples are
+ *     allowed and their V updates are summed in a fixed order.
+ *   - Streams: every call is enqueued on the stream given at creation (a
+ *     hipStream_t passed as void*; NULL = the null stream) and returns without
+ *     synchronising, except lst_sync_status and lst_init_factored.  A context
+ *     must not be used from two host threads at once.
+ *   - Errors: every call returns an lst_status.  Argument errors detectable on
+ *     the host are returned at once and nothing is enqueued.  Data-dependent
+ *     errors found on the device (an index outside [-1, D), a Woodbury matrix
+ *     that is not positive definite, a non-finite loss) set a sticky device
+ *     flag: all later state writes of that step and of every following step
+ *     are skipped, so V, U, U^{-T} and Q keep the values they had before the
+ *     failing step.  lst_sync_status reports and clears the flag.
+ */
+#ifndef LST_H
+#define LST_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct lst_ctx lst_ctx;
+
+/* Loss functions of the spherical family (section 4) implemented by the step. */
+enum lst_loss {
+  /* l = ||o - y||^2 (section 2.1); as a spherical loss q - 2 a.t + ||y||^2. */
+  LST_LOSS_SQUARED = 0,
+  /* l = -sum_k t_k log((o_{c_k}^2 + eps) / sum_i (o_i^2 + eps)), the spherical
+     softmax named in section 4 (no definition is printed there; this is the
+     reading used by the library, independent of sum(o)). */
+  LST_LOSS_SPHERICAL_SOFTMAX = 1
+};
+
+enum lst_status {
+  LST_OK = 0,
+  LST_E_ARG = -1,       /* null pointer, bad enum, lr <= 0 or not finite, ... */
+  LST_E_SHAPE = -2,     /* m > m_max, K > K_max, ld < d, D or d out of range   */
+  LST_E_INDEX = -3,     /* (device) a target index outside [-1, D)             */
+  LST_E_NOT_SPD = -4,   /* (device) the m x m Woodbury matrix is not positive
+                           definite: the step is too large for the batch
+                           (m = 1: 1 - 2 eta ||h||^2 <= 0, eq. updateU-T)       */
+  LST_E_NONFINITE = -5, /* (device) the loss is NaN or infinite                */
+  LST_E_HIP = -6,       /* a HIP runtime call failed                           */
+  LST_E_STATE = -7      /* wrong context kind for this call                    */
+};
+
+/* Limits of one context. */
+#define LST_MAX_D ((int64_t)2147483647)
+#define LST_MAX_d 4096
+#define LST_MAX_M 1024
+#define LST_MAX_K 64
+
+/*
+ * lst_create -- context for the factored step (Algorithm 3 / Algorithm 4).
+ *   D, d         output size and hidden size (1 <= d <= LST_MAX_d, 1 <= D <= LST_MAX_D).
+ *   m_max, K_max largest minibatch and largest number of target slots per
+ *                example that lst_step will be given (<= LST_MAX_M, LST_MAX_K).
+ *   loss         an lst_loss value.
+ *   eps          spherical softmax epsilon (> 0); ignored for squared error.
+ *   V            D x ldv device buffer holding V (updated in place by lst_step).
+ *   U, UinvT, Q  d x ldd device buffers (updated in place by lst_step).
+ *   stream       hipStream_t as void*; every call is enqueued on it.
+ * The buffers are borrowed: they must stay allocated until lst_destroy.  The
+ * state they hold is not read here; call lst_init_factored before the first
+ * step.  On success *out receives the context.
+ */
+int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss,
+               float eps, float *V, int64_t ldv, float *U, float *UinvT, float *Q, int32_t ldd,
+               void *stream);
+
+/*
+ * lst_init_factored -- Algorithm 1 (and the general initialisation of section 4.8).
+ *   V0 (D x ldv0, device) is copied into V when not NULL; NULL keeps V as it is.
+ *   U0 (d x ldu0, device) is copied into U when not NULL; NULL sets U = I.
+ * Then U^{-T} = inv(U)^T and Q = (V U)^T (V U) are computed (Q = V^T V when
+ * U = I), and the sticky error flag is cleared.  With U0 given, U is inverted
+ * in fp64 on the host (LST_E_NOT_SPD if it is singular).  Synchronises the
+ * stream.  Passing the current (V, U) re-derives the bookkeeping from scratch,
+ * which is also how a run resumes from a (V, U) checkpoint.
+ */
+int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0, int32_t ldu0);
+
+/*
+ * lst_step -- one minibatch step (Algorithm 3 for squared error, Algorithm 4
+ * with dl/ds = 0 and omega = 0 for the spherical softmax).
+ *   H        m x d device buffer, row stride d (one example per row).
+ *   m        number of examples, 0 <= m <= m_max (m = 0 writes loss 0).
+ *   idx, val m x K device buffers (int32 indices, float values), see above.
+ *   K        slots per example, 0 <= K <= K_max.
+ *   lr       learning rate eta > 0: W <- W - eta dL/dW.
+ *   loss_dev device float receiving L = sum over the m examples.
+ *   grad_H   m x d device buffer receiving dL/dH (row stride d); may be NULL.
+ * State V, U, U^{-T}, Q is updated in place so that V U equals
+ * W - eta dL/dW (eq. updateU / updateV, eq. gen-updateU / gen-updateV), Q equals
+ * the new W^T W (eq. updateQ / gen-Qnew) and U^{-T} the new inverse transpose.
+ * Returns once the work is enqueued; device-side errors surface at the next
+ * lst_sync_status.
+ */
+int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val,
+             int32_t K, float lr, float *loss_dev, float *grad_H);
+
+/*
+ * lst_materialize_W -- W = V U into a D x ldw device buffer (section 5.1: the
+ * explicit weights, an O(D d^2) product).  For a naive context, copies its W.
+ */
+int lst_materialize_W(lst_ctx *c, float *W, int64_t ldw);
+
+/*
+ * lst_sync_status -- synchronises the context's stream, returns the sticky
+ * device error (LST_OK if none) and clears it.  Also returns LST_E_HIP if a
+ * kernel launch or the synchronisation failed.
+ */
+int lst_sync_status(lst_ctx *c);
+
+/* lst_status_string -- static, human-readable name of a status code. */
+const char *lst_status_string(int status);
+
+/* lst_destroy -- frees the context and its workspace (after synchronising). */
+void lst_destroy(lst_ctx *c);
+
+/*
+ * lst_naive_create -- context for the naive O(D d) step of sections 2.3 / 4.3:
+ * O = W H^T (D x m) on MFMA, the loss over the full output, grad_H = W^T grad_O
+ * and W <- W - eta grad_O H, with W held explicitly.
+ *   W      D x ldw device buffer, updated in place by lst_naive_step.
+ *   Other arguments as in lst_create.  The workspace holds the D x m output.
+ */
+int lst_naive_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max,
+                     int32_t loss, float eps, float *W, int64_t ldw, void *stream);
+
+/* lst_naive_step -- same contract as lst_step, on a naive context. */
+int lst_naive_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val,
+                   int32_t K, float lr, float *loss_dev, float *grad_H);
+
+/* Phases of a step, as timed by the profiling hook below. */
+enum lst_phase {
+  LST_PHASE_CONTRACT = 0,     /* H^ = Q H, H~ = U H, X = U^{-T} H, H^T H (matrix cores)    */
+  LST_PHASE_GATHER = 1,       /* gather of the K target rows of V, loss epilogue, G         */
+  LST_PHASE_ZGRAD = 2,        /* Z^ = U^T G, grad_H, H^T H^, H~^T G (matrix cores)          */
+  LST_PHASE_SMALL = 3,        /* loss sum, M, Woodbury inverse, scatter keys (one CU)       */
+  LST_PHASE_MID = 4,          /* R X, (eta^2/2) M H - eta grad_H, U update (matrix cores)   */
+  LST_PHASE_UPDATE = 5,       /* U^{-T} and Q updates, P = U_new^{-T} H (matrix cores)      */
+  LST_PHASE_SCATTER = 6,      /* conflict-free update of the target rows of V               */
+  LST_PHASE_NAIVE_FWD = 7,    /* naive: O = W H^T                                           */
+  LST_PHASE_NAIVE_LOSS = 8,   /* naive: column norms of O, loss, grad_O                     */
+  LST_PHASE_NAIVE_GRAD = 9,   /* naive: grad_H = grad_O^T W                                 */
+  LST_PHASE_NAIVE_UPDATE = 10,/* naive: W <- W - eta grad_O H                               */
+  LST_NUM_PHASES = 11
+};
+
+/*
+ * lst_profile_enable -- tracing hook.  While on (on != 0), every step records a
+ * pair of HIP events around each of its phases on the context's stream (this
+ * adds a few microseconds per phase).  Turning it on clears earlier records.
+ */
+int lst_profile_enable(lst_ctx *c, int32_t on);
+
+/*
+ * lst_profile_read -- synchronises the stream and, for phases 0..n-1 (n <=
+ * LST_NUM_PHASES), writes to host arrays counts[p] = number of timed launches
+ * and ms[p] = their summed duration in milliseconds since the last enable/read;
+ * then clears the records.  At most 65536 launches per phase are recorded.
+ */
+int lst_profile_read(lst_ctx *c, int32_t *counts, double *ms, int32_t n);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LST_H */

@@ -1,0 +1,292 @@
+"""ctypes binding of liblst (include/lst.h): argument marshalling only.
+
+Every step of the method runs in the HIP kernels of liblst.so.  PyTorch
+provides device memory and the stream; tensors are passed as raw device
+pointers.  There is no fallback: if the library is not built, or no GPU is
+visible, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+import torch  # loaded before liblst so both share one HIP runtime
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "liblst.so")
+
+LST_LOSS_SQUARED = 0
+LST_LOSS_SPHERICAL_SOFTMAX = 1
+LOSSES = {"squared": LST_LOSS_SQUARED, "spherical_softmax": LST_LOSS_SPHERICAL_SOFTMAX}
+
+LST_OK = 0
+LST_E_ARG = -1
+LST_E_SHAPE = -2
+LST_E_INDEX = -3
+LST_E_NOT_SPD = -4
+LST_E_NONFINITE = -5
+LST_E_HIP = -6
+LST_E_STATE = -7
+
+# Exported C symbols and their signatures (kept in step with include/lst.h).
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_F = ctypes.c_float
+SIGNATURES = {
+    "lst_create": (_I32, [ctypes.POINTER(_P), _I64, _I32, _I32, _I32, _I32, _F, _P, _I64, _P, _P,
+                          _P, _I32, _P]),
+    "lst_init_factored": (_I32, [_P, _P, _I64, _P, _I32]),
+    "lst_step": (_I32, [_P, _P, _I32, _P, _P, _I32, _F, _P, _P]),
+    "lst_materialize_W": (_I32, [_P, _P, _I64]),
+    "lst_sync_status": (_I32, [_P]),
+    "lst_status_string": (ctypes.c_char_p, [_I32]),
+    "lst_destroy": (None, [_P]),
+    "lst_naive_create": (_I32, [ctypes.POINTER(_P), _I64, _I32, _I32, _I32, _I32, _F, _P, _I64,
+                                _P]),
+    "lst_naive_step": (_I32, [_P, _P, _I32, _P, _P, _I32, _F, _P, _P]),
+    "lst_profile_enable": (_I32, [_P, _I32]),
+    "lst_profile_read": (_I32, [_P, ctypes.POINTER(_I32), ctypes.POINTER(ctypes.c_double), _I32]),
+}
+
+PHASES = ["contract", "gather", "zgrad", "small", "mid", "update", "scatter",
+          "naive_fwd", "naive_loss", "naive_grad", "naive_update"]
+
+_lib = None
+_lock = threading.Lock()
+
+
+def library_path() -> str:
+    return LIB_PATH
+
+
+def lib() -> ctypes.CDLL:
+    """Load liblst.so (raises if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(
+                    f"{LIB_PATH} is missing: build it with paper_1606_08061_amd.build.build()")
+            L = ctypes.CDLL(LIB_PATH)
+            for name, (res, args) in SIGNATURES.items():
+                fn = getattr(L, name)
+                fn.restype = res
+                fn.argtypes = args
+            _lib = L
+        return _lib
+
+
+class LstError(RuntimeError):
+    def __init__(self, status: int, where: str = ""):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+
+
+def status_string(status: int) -> str:
+    return lib().lst_status_string(status).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != LST_OK:
+        raise LstError(status, where)
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else t.data_ptr()
+
+
+def _stream_handle(stream) -> int:
+    return stream.cuda_stream if stream is not None else torch.cuda.current_stream().cuda_stream
+
+
+# ---- C entry points under their own names (raw pointers and sizes) ----
+
+def lst_create(D, d, m_max, K_max, loss, eps, V, ldv, U, UinvT, Q, ldd, stream) -> tuple[int, int]:
+    ctx = _P()
+    st = lib().lst_create(ctypes.byref(ctx), D, d, m_max, K_max, loss, eps, V, ldv, U, UinvT, Q,
+                          ldd, stream)
+    return st, (ctx.value or 0)
+
+
+def lst_naive_create(D, d, m_max, K_max, loss, eps, W, ldw, stream) -> tuple[int, int]:
+    ctx = _P()
+    st = lib().lst_naive_create(ctypes.byref(ctx), D, d, m_max, K_max, loss, eps, W, ldw, stream)
+    return st, (ctx.value or 0)
+
+
+def lst_init_factored(ctx, V0, ldv0, U0, ldu0) -> int:
+    return lib().lst_init_factored(ctx, V0, ldv0, U0, ldu0)
+
+
+def lst_step(ctx, H, m, idx, val, K, lr, loss_dev, grad_H) -> int:
+    return lib().lst_step(ctx, H, m, idx, val, K, lr, loss_dev, grad_H)
+
+
+def lst_naive_step(ctx, H, m, idx, val, K, lr, loss_dev, grad_H) -> int:
+    return lib().lst_naive_step(ctx, H, m, idx, val, K, lr, loss_dev, grad_H)
+
+
+def lst_materialize_W(ctx, W, ldw) -> int:
+    return lib().lst_materialize_W(ctx, W, ldw)
+
+
+def lst_sync_status(ctx) -> int:
+    return lib().lst_sync_status(ctx)
+
+
+def lst_destroy(ctx) -> None:
+    lib().lst_destroy(ctx)
+
+
+def lst_profile_enable(ctx, on) -> int:
+    return lib().lst_profile_enable(ctx, on)
+
+
+def lst_profile_read(ctx) -> tuple[int, dict]:
+    n = len(PHASES)
+    counts = (_I32 * n)()
+    ms = (ctypes.c_double * n)()
+    st = lib().lst_profile_read(ctx, counts, ms, n)
+    return st, {PHASES[p]: (int(counts[p]), float(ms[p])) for p in range(n)}
+
+
+# ---- tensor-level wrappers ----
+
+def _need(t, dtype, shape, name):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+class _Ctx:
+    def __init__(self, D, d, m_max, K_max, loss, eps, device, stream):
+        if not torch.cuda.is_available():
+            raise RuntimeError("liblst needs a GPU; none is visible")
+        self.D, self.d, self.m_max, self.K_max = int(D), int(d), int(m_max), int(K_max)
+        self.loss_name = loss
+        self.loss = LOSSES[loss]
+        self.eps = float(eps)
+        self.device = torch.device(device) if device is not None else torch.device("cuda")
+        self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
+        self.ctx = 0
+        self.loss_buf = torch.zeros((), dtype=torch.float32, device=self.device)
+
+    def _batch(self, H, idx, val):
+        m = H.shape[0]
+        K = idx.shape[1] if idx.dim() == 2 else 0
+        _need(H, torch.float32, (m, self.d), "H")
+        _need(idx, torch.int32, (m, K), "idx")
+        _need(val, torch.float32, (m, K), "val")
+        return m, K
+
+    def sync_status(self) -> int:
+        return lst_sync_status(self.ctx)
+
+    def check(self, where="lst_sync_status") -> None:
+        _check(self.sync_status(), where)
+
+    def profile(self, on: bool = True) -> None:
+        _check(lst_profile_enable(self.ctx, 1 if on else 0), "lst_profile_enable")
+
+    def profile_read(self) -> dict:
+        """{phase: (launches, total ms)} since the last enable / read."""
+        st, res = lst_profile_read(self.ctx)
+        _check(st, "lst_profile_read")
+        return res
+
+    def close(self) -> None:
+        if self.ctx:
+            lst_destroy(self.ctx)
+            self.ctx = 0
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class Factored(_Ctx):
+    """The factored output layer W = V U with Q and U^{-T} (device tensors V, U, UinvT, Q)."""
+
+    def __init__(self, D, d, m_max, K_max, loss="squared", eps=1e-3, device=None, stream=None):
+        super().__init__(D, d, m_max, K_max, loss, eps, device, stream)
+        kw = dict(dtype=torch.float32, device=self.device)
+        self.V = torch.zeros((self.D, self.d), **kw)
+        self.U = torch.zeros((self.d, self.d), **kw)
+        self.UinvT = torch.zeros((self.d, self.d), **kw)
+        self.Q = torch.zeros((self.d, self.d), **kw)
+        st, self.ctx = lst_create(self.D, self.d, self.m_max, self.K_max, self.loss, self.eps,
+                                  _ptr(self.V), self.d, _ptr(self.U), _ptr(self.UinvT),
+                                  _ptr(self.Q), self.d, _stream_handle(self.stream))
+        _check(st, "lst_create")
+
+    def init(self, V0=None, U0=None) -> None:
+        if V0 is not None:
+            _need(V0, torch.float32, (self.D, self.d), "V0")
+        if U0 is not None:
+            _need(U0, torch.float32, (self.d, self.d), "U0")
+        _check(lst_init_factored(self.ctx, _ptr(V0), self.d, _ptr(U0), self.d),
+               "lst_init_factored")
+
+    def step(self, H, idx, val, lr, grad_H=None, loss_out=None, want_grad=True):
+        m, K = self._batch(H, idx, val)
+        if grad_H is None and want_grad:
+            grad_H = torch.empty((m, self.d), dtype=torch.float32, device=self.device)
+        if grad_H is not None:
+            _need(grad_H, torch.float32, (m, self.d), "grad_H")
+        loss_out = self.loss_buf if loss_out is None else loss_out
+        _check(lst_step(self.ctx, _ptr(H), m, _ptr(idx), _ptr(val), K, float(lr), _ptr(loss_out),
+                        _ptr(grad_H)), "lst_step")
+        return loss_out, grad_H
+
+    def materialize_W(self, out=None):
+        if out is None:
+            out = torch.empty((self.D, self.d), dtype=torch.float32, device=self.device)
+        _need(out, torch.float32, (self.D, self.d), "W")
+        _check(lst_materialize_W(self.ctx, _ptr(out), self.d), "lst_materialize_W")
+        return out
+
+
+class Naive(_Ctx):
+    """The naive O(D d) output layer with an explicit W (device tensor)."""
+
+    def __init__(self, D, d, m_max, K_max, loss="squared", eps=1e-3, device=None, stream=None):
+        super().__init__(D, d, m_max, K_max, loss, eps, device, stream)
+        self.W = torch.zeros((self.D, self.d), dtype=torch.float32, device=self.device)
+        st, self.ctx = lst_naive_create(self.D, self.d, self.m_max, self.K_max, self.loss,
+                                        self.eps, _ptr(self.W), self.d,
+                                        _stream_handle(self.stream))
+        _check(st, "lst_naive_create")
+
+    def init(self, W0) -> None:
+        _need(W0, torch.float32, (self.D, self.d), "W0")
+        with torch.cuda.stream(self.stream):
+            self.W.copy_(W0)
+
+    def step(self, H, idx, val, lr, grad_H=None, loss_out=None, want_grad=True):
+        m, K = self._batch(H, idx, val)
+        if grad_H is None and want_grad:
+            grad_H = torch.empty((m, self.d), dtype=torch.float32, device=self.device)
+        if grad_H is not None:
+            _need(grad_H, torch.float32, (m, self.d), "grad_H")
+        loss_out = self.loss_buf if loss_out is None else loss_out
+        _check(lst_naive_step(self.ctx, _ptr(H), m, _ptr(idx), _ptr(val), K, float(lr),
+                              _ptr(loss_out), _ptr(grad_H)), "lst_naive_step")
+        return loss_out, grad_H
+
+    def materialize_W(self, out=None):
+        if out is None:
+            out = torch.empty((self.D, self.d), dtype=torch.float32, device=self.device)
+        _need(out, torch.float32, (self.D, self.d), "W")
+        _check(lst_materialize_W(self.ctx, _ptr(out), self.d), "lst_materialize_W")
+        return out

@@ -1,0 +1,580 @@
+// C ABI of liblst: argument validation, workspace carving and the enqueue order
+// of the factored step (Algorithm 3 / Algorithm 4) and of the naive step.
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "lst_internal.h"
+
+using namespace lst;
+
+namespace {
+
+enum : int { KIND_FACTORED = 1, KIND_NAIVE = 2 };
+constexpr int kTargetWGs = 1024;   // workgroups a split-k GEMM aims for
+constexpr int kColnormBlocks = 1024;
+
+// Device workspace carved in 256-byte aligned pieces.
+struct Carver {
+  char *base;
+  size_t off = 0;
+  template <class T>
+  T *take(size_t n) {
+    off = (off + 255) & ~size_t(255);
+    T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+    off += n * sizeof(T);
+    return p;
+  }
+};
+
+}  // namespace
+
+struct lst_ctx {
+  int kind;
+  int64_t D;
+  int d, m_max, K_max, loss;
+  float eps;
+  hipStream_t stream;
+  // factored state (borrowed)
+  float *V;
+  int64_t ldv;
+  float *U, *UinvT, *Q;
+  int ldd;
+  // naive state (borrowed)
+  float *W;
+  int64_t ldw;
+  // workspace (owned)
+  void *ws;
+  size_t ws_bytes;
+  float *Hhat, *Htil, *X, *G, *Atil, *Zhat, *gradH, *Yw, *Zq, *P;
+  float *N, *Mhat, *HZ, *M, *R, *Cwork;
+  float *dq, *lvec, *dA;
+  int *srow, *sslot, *nvalid, *flag;
+  float *O, *colpart, *splitpart;
+  hipError_t last_err;
+  // tracing: event pairs per phase
+  bool prof_on;
+  std::vector<hipEvent_t> prof_ev[LST_NUM_PHASES];
+  int prof_used[LST_NUM_PHASES];
+};
+
+namespace {
+
+bool finite_pos(float x) { return std::isfinite(x) && x > 0.f; }
+
+void carve_factored(lst_ctx *c, Carver &cv) {
+  const size_t md = (size_t)c->m_max * c->d, mm = (size_t)c->m_max * c->m_max;
+  const size_t mk = (size_t)c->m_max * (c->K_max > 0 ? c->K_max : 1);
+  c->Hhat = cv.take<float>(md);
+  c->Htil = cv.take<float>(md);
+  c->X = cv.take<float>(md);
+  c->G = cv.take<float>(md);
+  c->Atil = cv.take<float>(md);
+  c->Zhat = cv.take<float>(md);
+  c->gradH = cv.take<float>(md);
+  c->Yw = cv.take<float>(md);
+  c->Zq = cv.take<float>(md);
+  c->P = cv.take<float>(md);
+  c->N = cv.take<float>(mm);
+  c->Mhat = cv.take<float>(mm);
+  c->HZ = cv.take<float>(mm);
+  c->M = cv.take<float>(mm);
+  c->R = cv.take<float>(mm);
+  c->Cwork = cv.take<float>(mm);
+  c->dq = cv.take<float>(c->m_max);
+  c->lvec = cv.take<float>(c->m_max);
+  c->dA = cv.take<float>(mk);
+  c->srow = cv.take<int>(mk);
+  c->sslot = cv.take<int>(mk);
+  c->nvalid = cv.take<int>(1);
+  c->flag = cv.take<int>(1);
+}
+
+// Upper bound of the split-k partial buffer of grad_H = grad_O^T W for any m <= m_max:
+// gemm_plan_split keeps splits <= ceil(kTargetWGs / tiles), and m * d <= tiles * 1024.
+size_t naive_split_floats(const lst_ctx *c) {
+  const size_t tiles = (size_t)((c->m_max + 31) / 32) * ((c->d + 31) / 32);
+  return (kTargetWGs + tiles) * 1024;
+}
+
+void carve_naive(lst_ctx *c, Carver &cv) {
+  const size_t md = (size_t)c->m_max * c->d;
+  const size_t mk = (size_t)c->m_max * (c->K_max > 0 ? c->K_max : 1);
+  c->O = cv.take<float>((size_t)c->D * c->m_max);
+  c->colpart = cv.take<float>((size_t)kColnormBlocks * c->m_max);
+  c->splitpart = cv.take<float>(naive_split_floats(c));
+  c->gradH = cv.take<float>(md);
+  c->dq = cv.take<float>(c->m_max);
+  c->dA = cv.take<float>(mk);
+  c->flag = cv.take<int>(1);
+}
+
+int common_args(int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss, float eps) {
+  if (loss != LST_LOSS_SQUARED && loss != LST_LOSS_SPHERICAL_SOFTMAX) return LST_E_ARG;
+  if (loss == LST_LOSS_SPHERICAL_SOFTMAX && !finite_pos(eps)) return LST_E_ARG;
+  if (D < 1 || D > LST_MAX_D || d < 1 || d > LST_MAX_d) return LST_E_SHAPE;
+  if (m_max < 1 || m_max > LST_MAX_M || K_max < 0 || K_max > LST_MAX_K) return LST_E_SHAPE;
+  if ((int64_t)m_max * K_max > 8192) return LST_E_SHAPE;
+  return LST_OK;
+}
+
+int alloc_ws(lst_ctx *c, void (*carve)(lst_ctx *, Carver &)) {
+  Carver probe{nullptr};
+  carve(c, probe);
+  c->ws_bytes = probe.off + 256;
+  if (hipMalloc(&c->ws, c->ws_bytes) != hipSuccess) return LST_E_HIP;
+  Carver real{static_cast<char *>(c->ws)};
+  carve(c, real);
+  if (hipMemsetAsync(c->ws, 0, c->ws_bytes, c->stream) != hipSuccess) return LST_E_HIP;
+  if (hipStreamSynchronize(c->stream) != hipSuccess) return LST_E_HIP;
+  return LST_OK;
+}
+
+int step_args(const lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val,
+              int32_t K, float lr, const float *loss_dev) {
+  if (!loss_dev) return LST_E_ARG;
+  if (m < 0 || m > c->m_max || K < 0 || K > c->K_max) return LST_E_SHAPE;
+  if (m > 0 && !H) return LST_E_ARG;
+  if (m > 0 && K > 0 && (!idx || !val)) return LST_E_ARG;
+  if (!finite_pos(lr)) return LST_E_ARG;
+  return LST_OK;
+}
+
+int record(lst_ctx *c, hipError_t e) {
+  if (e != hipSuccess) {
+    c->last_err = e;
+    return LST_E_HIP;
+  }
+  return LST_OK;
+}
+
+constexpr int kProfCap = 65536;
+
+// Records the start (begin=true) or the end of a phase when profiling is on.
+void prof(lst_ctx *c, int phase, bool begin) {
+  if (!c->prof_on) return;
+  int &used = c->prof_used[phase];
+  if (used >= kProfCap) return;
+  std::vector<hipEvent_t> &ev = c->prof_ev[phase];
+  const size_t slot = 2 * (size_t)used + (begin ? 0 : 1);
+  while (ev.size() <= slot) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) {
+      c->prof_on = false;
+      return;
+    }
+    ev.push_back(e);
+  }
+  (void)hipEventRecord(ev[slot], c->stream);
+  if (!begin) ++used;
+}
+
+void prof_free(lst_ctx *c) {
+  for (int p = 0; p < LST_NUM_PHASES; ++p) {
+    for (hipEvent_t e : c->prof_ev[p]) (void)hipEventDestroy(e);
+    c->prof_ev[p].clear();
+    c->prof_used[p] = 0;
+  }
+}
+
+// fp64 Gauss-Jordan with partial pivoting (init only): returns false if singular.
+bool invert_host(std::vector<double> &a, int n, std::vector<double> &inv) {
+  inv.assign((size_t)n * n, 0.0);
+  for (int i = 0; i < n; ++i) inv[(size_t)i * n + i] = 1.0;
+  for (int k = 0; k < n; ++k) {
+    int p = k;
+    double best = std::fabs(a[(size_t)k * n + k]);
+    for (int i = k + 1; i < n; ++i)
+      if (std::fabs(a[(size_t)i * n + k]) > best) {
+        best = std::fabs(a[(size_t)i * n + k]);
+        p = i;
+      }
+    if (!(best > 0.0) || !std::isfinite(best)) return false;
+    if (p != k)
+      for (int j = 0; j < n; ++j) {
+        std::swap(a[(size_t)k * n + j], a[(size_t)p * n + j]);
+        std::swap(inv[(size_t)k * n + j], inv[(size_t)p * n + j]);
+      }
+    const double ip = 1.0 / a[(size_t)k * n + k];
+    for (int j = 0; j < n; ++j) {
+      a[(size_t)k * n + j] *= ip;
+      inv[(size_t)k * n + j] *= ip;
+    }
+    for (int i = 0; i < n; ++i) {
+      if (i == k) continue;
+      const double f = a[(size_t)i * n + k];
+      if (f == 0.0) continue;
+      for (int j = 0; j < n; ++j) {
+        a[(size_t)i * n + j] -= f * a[(size_t)k * n + j];
+        inv[(size_t)i * n + j] -= f * inv[(size_t)k * n + j];
+      }
+    }
+  }
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *lst_status_string(int status) {
+  switch (status) {
+    case LST_OK: return "LST_OK";
+    case LST_E_ARG: return "LST_E_ARG";
+    case LST_E_SHAPE: return "LST_E_SHAPE";
+    case LST_E_INDEX: return "LST_E_INDEX";
+    case LST_E_NOT_SPD: return "LST_E_NOT_SPD";
+    case LST_E_NONFINITE: return "LST_E_NONFINITE";
+    case LST_E_HIP: return "LST_E_HIP";
+    case LST_E_STATE: return "LST_E_STATE";
+    default: return "LST_E_UNKNOWN";
+  }
+}
+
+int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss,
+               float eps, float *V, int64_t ldv, float *U, float *UinvT, float *Q, int32_t ldd,
+               void *stream) {
+  if (!out) return LST_E_ARG;
+  *out = nullptr;
+  int st = common_args(D, d, m_max, K_max, loss, eps);
+  if (st != LST_OK) return st;
+  if (!V || !U || !UinvT || !Q) return LST_E_ARG;
+  if (ldv < d || ldd < d) return LST_E_SHAPE;
+  lst_ctx *c = new (std::nothrow) lst_ctx{};
+  if (!c) return LST_E_ARG;
+  c->kind = KIND_FACTORED;
+  c->D = D;
+  c->d = d;
+  c->m_max = m_max;
+  c->K_max = K_max;
+  c->loss = loss;
+  c->eps = eps;
+  c->stream = static_cast<hipStream_t>(stream);
+  c->V = V;
+  c->ldv = ldv;
+  c->U = U;
+  c->UinvT = UinvT;
+  c->Q = Q;
+  c->ldd = ldd;
+  c->last_err = hipSuccess;
+  st = alloc_ws(c, carve_factored);
+  if (st != LST_OK) {
+    lst_destroy(c);
+    return st;
+  }
+  *out = c;
+  return LST_OK;
+}
+
+int lst_naive_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max,
+                     int32_t loss, float eps, float *W, int64_t ldw, void *stream) {
+  if (!out) return LST_E_ARG;
+  *out = nullptr;
+  int st = common_args(D, d, m_max, K_max, loss, eps);
+  if (st != LST_OK) return st;
+  if (!W) return LST_E_ARG;
+  if (ldw < d) return LST_E_SHAPE;
+  lst_ctx *c = new (std::nothrow) lst_ctx{};
+  if (!c) return LST_E_ARG;
+  c->kind = KIND_NAIVE;
+  c->D = D;
+  c->d = d;
+  c->m_max = m_max;
+  c->K_max = K_max;
+  c->loss = loss;
+  c->eps = eps;
+  c->stream = static_cast<hipStream_t>(stream);
+  c->W = W;
+  c->ldw = ldw;
+  c->last_err = hipSuccess;
+  st = alloc_ws(c, carve_naive);
+  if (st != LST_OK) {
+    lst_destroy(c);
+    return st;
+  }
+  *out = c;
+  return LST_OK;
+}
+
+void lst_destroy(lst_ctx *c) {
+  if (!c) return;
+  if (c->ws) {
+    (void)hipStreamSynchronize(c->stream);
+    (void)hipFree(c->ws);
+  }
+  prof_free(c);
+  delete c;
+}
+
+int lst_profile_enable(lst_ctx *c, int32_t on) {
+  if (!c) return LST_E_ARG;
+  if (record(c, hipStreamSynchronize(c->stream))) return LST_E_HIP;
+  for (int p = 0; p < LST_NUM_PHASES; ++p) c->prof_used[p] = 0;
+  c->prof_on = on != 0;
+  return LST_OK;
+}
+
+int lst_profile_read(lst_ctx *c, int32_t *counts, double *ms, int32_t n) {
+  if (!c || !counts || !ms || n < 0 || n > LST_NUM_PHASES) return LST_E_ARG;
+  if (record(c, hipStreamSynchronize(c->stream))) return LST_E_HIP;
+  for (int p = 0; p < n; ++p) {
+    double tot = 0.0;
+    for (int i = 0; i < c->prof_used[p]; ++i) {
+      float t = 0.f;
+      if (record(c, hipEventElapsedTime(&t, c->prof_ev[p][2 * i], c->prof_ev[p][2 * i + 1])))
+        return LST_E_HIP;
+      tot += t;
+    }
+    counts[p] = c->prof_used[p];
+    ms[p] = tot;
+  }
+  for (int p = 0; p < LST_NUM_PHASES; ++p) c->prof_used[p] = 0;
+  return LST_OK;
+}
+
+int lst_sync_status(lst_ctx *c) {
+  if (!c) return LST_E_ARG;
+  if (hipStreamSynchronize(c->stream) != hipSuccess) return LST_E_HIP;
+  if (c->last_err != hipSuccess) {
+    c->last_err = hipSuccess;
+    return LST_E_HIP;
+  }
+  int f = 0;
+  if (hipMemcpy(&f, c->flag, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess) return LST_E_HIP;
+  if (f != 0) {
+    const int zero = 0;
+    if (hipMemcpy(c->flag, &zero, sizeof(int), hipMemcpyHostToDevice) != hipSuccess)
+      return LST_E_HIP;
+  }
+  if (f & FLAG_INDEX) return LST_E_INDEX;
+  if (f & FLAG_NONFINITE) return LST_E_NONFINITE;
+  if (f & FLAG_NOT_SPD) return LST_E_NOT_SPD;
+  return LST_OK;
+}
+
+int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0, int32_t ldu0) {
+  if (!c) return LST_E_ARG;
+  if (c->kind != KIND_FACTORED) return LST_E_STATE;
+  if ((V0 && ldv0 < c->d) || (U0 && ldu0 < c->d)) return LST_E_SHAPE;
+  hipStream_t s = c->stream;
+  const int d = c->d;
+  const size_t row = (size_t)d * sizeof(float);
+  if (V0 && V0 != c->V) {
+    if (record(c, hipMemcpy2DAsync(c->V, c->ldv * sizeof(float), V0, ldv0 * sizeof(float), row,
+                                   (size_t)c->D, hipMemcpyDeviceToDevice, s)))
+      return LST_E_HIP;
+  }
+  if (U0) {
+    if (U0 != c->U &&
+        record(c, hipMemcpy2DAsync(c->U, c->ldd * sizeof(float), U0, ldu0 * sizeof(float), row,
+                                   (size_t)d, hipMemcpyDeviceToDevice, s)))
+      return LST_E_HIP;
+    std::vector<float> hu((size_t)d * d);
+    if (record(c, hipMemcpy2DAsync(hu.data(), row, c->U, c->ldd * sizeof(float), row, (size_t)d,
+                                   hipMemcpyDeviceToHost, s)) ||
+        record(c, hipStreamSynchronize(s)))
+      return LST_E_HIP;
+    std::vector<double> a(hu.begin(), hu.end()), inv;
+    if (!invert_host(a, d, inv)) return LST_E_NOT_SPD;
+    std::vector<float> hut((size_t)d * d);
+    for (int i = 0; i < d; ++i)
+      for (int j = 0; j < d; ++j) hut[(size_t)i * d + j] = (float)inv[(size_t)j * d + i];
+    if (record(c, hipMemcpy2DAsync(c->UinvT, c->ldd * sizeof(float), hut.data(), row, row,
+                                   (size_t)d, hipMemcpyHostToDevice, s)) ||
+        record(c, hipStreamSynchronize(s)))
+      return LST_E_HIP;
+  } else {
+    if (record(c, launch_identity(s, c->U, d, c->ldd)) ||
+        record(c, launch_identity(s, c->UinvT, d, c->ldd)))
+      return LST_E_HIP;
+  }
+  // Q = U^T (V^T V) U  (Q = V^T V when U = I), V^T V split over D.
+  GemmDesc g = gemm_desc(d, d, (int)c->D, c->V, c->ldv, 1, c->V, c->ldv, 1, nullptr, d);
+  const size_t pf = gemm_plan_split(g, kTargetWGs, nullptr);
+  float *tmp = nullptr;
+  const size_t tmp_floats = pf + 2 * (size_t)d * d + 64;
+  if (record(c, hipMalloc(&tmp, tmp_floats * sizeof(float)))) return LST_E_HIP;
+  float *part = tmp, *Gm = tmp + ((pf + 63) / 64) * 64, *Tm = Gm + (size_t)d * d;
+  gemm_plan_split(g, kTargetWGs, part);
+  GemmBatch b{};
+  int st = LST_OK;
+  if (!U0) {
+    g.C = c->Q;
+    g.ldc = c->ldd;
+    b.d[0] = g;
+    b.n = 1;
+    if (record(c, gemm_launch(b, nullptr, s))) st = LST_E_HIP;
+  } else {
+    g.C = Gm;
+    g.ldc = d;
+    b.d[0] = g;
+    b.n = 1;
+    if (record(c, gemm_launch(b, nullptr, s))) st = LST_E_HIP;
+    GemmBatch b2{};
+    b2.d[0] = gemm_desc(d, d, d, Gm, d, 0, c->U, c->ldd, 1, Tm, d);  // T = G U
+    b2.n = 1;
+    if (st == LST_OK && record(c, gemm_launch(b2, nullptr, s))) st = LST_E_HIP;
+    GemmBatch b3{};
+    b3.d[0] = gemm_desc(d, d, d, c->U, c->ldd, 1, Tm, d, 1, c->Q, c->ldd);  // Q = U^T T
+    b3.n = 1;
+    if (st == LST_OK && record(c, gemm_launch(b3, nullptr, s))) st = LST_E_HIP;
+  }
+  const int zero = 0;
+  if (record(c, hipStreamSynchronize(s))) st = LST_E_HIP;
+  (void)hipFree(tmp);
+  if (record(c, hipMemcpy(c->flag, &zero, sizeof(int), hipMemcpyHostToDevice))) st = LST_E_HIP;
+  return st;
+}
+
+int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val, int32_t K,
+             float lr, float *loss_dev, float *grad_H) {
+  if (!c) return LST_E_ARG;
+  if (c->kind != KIND_FACTORED) return LST_E_STATE;
+  int st = step_args(c, H, m, idx, val, K, lr, loss_dev);
+  if (st != LST_OK) return st;
+  hipStream_t s = c->stream;
+  if (m == 0) return record(c, launch_fill(s, loss_dev, 0.f));
+  const int d = c->d, ldd = c->ldd;
+  float *gH = grad_H ? grad_H : c->gradH;
+
+  // H^ = Q H, H~ = U H, X = U^{-T} H (Algorithm 3 steps 1, 5, 6; Algorithm 4 rows 1, 5),
+  // and N = H^T H for the Woodbury matrix.
+  GemmBatch b1{};
+  b1.d[0] = gemm_desc(m, d, d, H, d, 0, c->Q, ldd, 0, c->Hhat, d);
+  b1.d[1] = gemm_desc(m, d, d, H, d, 0, c->U, ldd, 0, c->Htil, d);
+  b1.d[2] = gemm_desc(m, d, d, H, d, 0, c->UinvT, ldd, 0, c->X, d);
+  b1.d[3] = gemm_desc(m, m, d, H, d, 0, H, d, 0, c->N, m);
+  b1.n = 4;
+  prof(c, LST_PHASE_CONTRACT, true);
+  if (record(c, gemm_launch(b1, nullptr, s, GEMM_CONTRACT))) return LST_E_HIP;
+  prof(c, LST_PHASE_CONTRACT, false);
+
+  // Sparse gather of the K target rows of the pre-update V and the loss epilogue.
+  prof(c, LST_PHASE_GATHER, true);
+  if (record(c, launch_gather(s, m, K, d, c->D, H, c->Hhat, c->Htil, idx, val, c->V, c->ldv,
+                              c->loss, c->eps, lr, c->G, c->Atil, c->dq, c->dA, c->lvec, c->flag)))
+    return LST_E_HIP;
+  prof(c, LST_PHASE_GATHER, false);
+
+  // Z^ = U^T G with grad_H = 2 H^ diag(dl/dq) + Z^; M^ = H^T H^; H^T Z^ = H~^T G.
+  GemmBatch b2{};
+  GemmDesc z = gemm_desc(m, d, d, c->G, d, 0, c->U, ldd, 1, c->Zhat, d);
+  z.epi = EPI_GRADH;
+  z.rs = c->dq;
+  z.E = c->Hhat;
+  z.lde = d;
+  z.C2 = gH;
+  z.ldc2 = d;
+  b2.d[0] = z;
+  b2.d[1] = gemm_desc(m, m, d, H, d, 0, c->Hhat, d, 0, c->Mhat, m);
+  b2.d[2] = gemm_desc(m, m, d, c->Htil, d, 0, c->G, d, 0, c->HZ, m);
+  b2.n = 3;
+  prof(c, LST_PHASE_ZGRAD, true);
+  if (record(c, gemm_launch(b2, nullptr, s, GEMM_ZGRAD))) return LST_E_HIP;
+  prof(c, LST_PHASE_ZGRAD, false);
+
+  // Loss, M, Woodbury inverse, sorted scatter keys; sets the error flag.
+  prof(c, LST_PHASE_SMALL, true);
+  if (record(c, launch_small(s, m, K, lr, idx, c->lvec, c->dq, c->dA, c->N, c->Mhat, c->HZ, c->M,
+                             c->R, c->Cwork, c->srow, c->sslot, c->nvalid, loss_dev, c->flag)))
+    return LST_E_HIP;
+  prof(c, LST_PHASE_SMALL, false);
+
+  // Gated state updates.  Yw = R X; Zq = (eta^2/2) M H - eta grad_H;
+  // U <- U - 2 eta H~ diag(dl/dq) H^T (eq. updateU / gen-updateU).
+  GemmBatch b3{};
+  b3.d[0] = gemm_desc(m, d, m, c->R, m, 0, c->X, d, 1, c->Yw, d);
+  b3.d[1] = gemm_desc(m, d, m, c->M, m, 0, H, d, 1, c->Zq, d, 0.5f * lr * lr, gH, d, -lr);
+  b3.d[2] = gemm_desc(d, d, m, c->Atil, d, 1, H, d, 1, c->U, ldd, -1.f, c->U, ldd, 1.f);
+  b3.n = 3;
+  prof(c, LST_PHASE_MID, true);
+  if (record(c, gemm_launch(b3, c->flag, s, GEMM_MID))) return LST_E_HIP;
+  prof(c, LST_PHASE_MID, false);
+
+  // U^{-T} += (2 eta X S C^{-1} S) H^T (Woodbury); Q += H Zq^T + Zq H^T (eq. updateQ /
+  // gen-Qnew); P = U_new^{-T} H = X + (2 eta X S C^{-1} S)(H^T H).
+  GemmBatch b4{};
+  b4.d[0] = gemm_desc(d, d, m, c->Yw, d, 1, H, d, 1, c->UinvT, ldd, 1.f, c->UinvT, ldd, 1.f);
+  GemmDesc qd = gemm_desc(d, d, m, H, d, 1, c->Zq, d, 1, c->Q, ldd, 1.f, c->Q, ldd, 1.f);
+  qd.A2 = c->Zq;
+  qd.lda2 = d;
+  qd.B2 = H;
+  qd.ldb2 = d;
+  qd.K2 = m;
+  b4.d[1] = qd;
+  b4.d[2] = gemm_desc(m, d, m, c->N, m, 0, c->Yw, d, 1, c->P, d, 1.f, c->X, d, 1.f);
+  b4.n = 3;
+  prof(c, LST_PHASE_UPDATE, true);
+  if (record(c, gemm_launch(b4, c->flag, s, GEMM_UPDATE))) return LST_E_HIP;
+  prof(c, LST_PHASE_UPDATE, false);
+
+  // V_r -= eta sum dl/dA P_j over the slots of each distinct target row (eq. updateV).
+  prof(c, LST_PHASE_SCATTER, true);
+  if (record(c, launch_scatter(s, m, K, d, lr, c->srow, c->sslot, c->nvalid, c->dA, c->P, c->V,
+                               c->ldv, c->flag)))
+    return LST_E_HIP;
+  prof(c, LST_PHASE_SCATTER, false);
+  return LST_OK;
+}
+
+int lst_materialize_W(lst_ctx *c, float *W, int64_t ldw) {
+  if (!c || !W) return LST_E_ARG;
+  if (ldw < c->d) return LST_E_SHAPE;
+  if (c->kind == KIND_NAIVE) {
+    return record(c, hipMemcpy2DAsync(W, ldw * sizeof(float), c->W, c->ldw * sizeof(float),
+                                      (size_t)c->d * sizeof(float), (size_t)c->D,
+                                      hipMemcpyDeviceToDevice, c->stream));
+  }
+  GemmBatch b{};
+  b.d[0] = gemm_desc((int)c->D, c->d, c->d, c->V, c->ldv, 0, c->U, c->ldd, 1, W, ldw);
+  b.n = 1;
+  return record(c, gemm_launch(b, nullptr, c->stream));
+}
+
+int lst_naive_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val,
+                   int32_t K, float lr, float *loss_dev, float *grad_H) {
+  if (!c) return LST_E_ARG;
+  if (c->kind != KIND_NAIVE) return LST_E_STATE;
+  int st = step_args(c, H, m, idx, val, K, lr, loss_dev);
+  if (st != LST_OK) return st;
+  hipStream_t s = c->stream;
+  if (m == 0) return record(c, launch_fill(s, loss_dev, 0.f));
+  const int d = c->d;
+  const int64_t D = c->D;
+  float *gH = grad_H ? grad_H : c->gradH;
+  // O = W H^T  (D x m), the O(D d) forward product of section 2.3.
+  GemmBatch b1{};
+  b1.d[0] = gemm_desc((int)D, m, d, c->W, c->ldw, 0, H, d, 0, c->O, m);
+  b1.n = 1;
+  prof(c, LST_PHASE_NAIVE_FWD, true);
+  if (record(c, gemm_launch(b1, nullptr, s, GEMM_NAIVE_FWD))) return LST_E_HIP;
+  prof(c, LST_PHASE_NAIVE_FWD, false);
+  // q_j = ||o_j||^2 over all D outputs, the loss and dl/dq, dl/da from the explicit O.
+  prof(c, LST_PHASE_NAIVE_LOSS, true);
+  if (record(c, launch_colnorm(s, c->O, D, m, c->colpart, kColnormBlocks)) ||
+      record(c, launch_naive_epilogue(s, m, K, D, kColnormBlocks, c->colpart, c->O, idx, val,
+                                      c->loss, c->eps, c->dq, c->dA, loss_dev, c->flag)))
+    return LST_E_HIP;
+  // grad_O = 2 O diag(dl/dq) + Yring, in place over O.
+  if (record(c, launch_grad_o(s, c->O, D, m, K, c->dq, idx, c->dA))) return LST_E_HIP;
+  prof(c, LST_PHASE_NAIVE_LOSS, false);
+  // grad_H = grad_O^T W (split over D), then W <- W - eta grad_O H.
+  GemmBatch b2{};
+  b2.d[0] = gemm_desc(m, d, (int)D, c->O, m, 1, c->W, c->ldw, 1, gH, d);
+  gemm_plan_split(b2.d[0], kTargetWGs, c->splitpart);
+  b2.n = 1;
+  prof(c, LST_PHASE_NAIVE_GRAD, true);
+  if (record(c, gemm_launch(b2, nullptr, s, GEMM_NAIVE_GRAD))) return LST_E_HIP;
+  prof(c, LST_PHASE_NAIVE_GRAD, false);
+  GemmBatch b3{};
+  b3.d[0] = gemm_desc((int)D, d, m, c->O, m, 0, H, d, 1, c->W, c->ldw, -lr, c->W, c->ldw, 1.f);
+  b3.n = 1;
+  prof(c, LST_PHASE_NAIVE_UPDATE, true);
+  if (record(c, gemm_launch(b3, c->flag, s, GEMM_NAIVE_UPDATE))) return LST_E_HIP;
+  prof(c, LST_PHASE_NAIVE_UPDATE, false);
+  return LST_OK;
+}
+
+}  // extern "C"

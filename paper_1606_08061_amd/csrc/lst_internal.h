@@ -1,0 +1,113 @@
+// Internal declarations shared by the HIP sources of liblst (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "lst.h"
+
+namespace lst {
+
+// Sticky device error bits (mapped to lst_status by lst_sync_status).
+enum : int { FLAG_INDEX = 1, FLAG_NOT_SPD = 2, FLAG_NONFINITE = 4 };
+
+// ---------------------------------------------------------------------------
+// Batched fp32 MFMA GEMM.
+//
+// One descriptor computes  C[i,j] = alpha * sum_k opA(i,k) opB(k,j) + beta * Cin[i,j]
+// for i < M, j < N, with the k sum running over one or two segments
+// (k in [0,K) with A,B then k in [0,K2) with A2,B2).  Operand layouts:
+//   tA = 0: opA(i,k) = A[i*lda + k]      tA = 1: opA(i,k) = A[k*lda + i]
+//   tB = 0: opB(k,j) = B[j*ldb + k]      tB = 1: opB(k,j) = B[k*ldb + j]
+// Epilogue EPI_GRADH additionally writes C2[i,j] = 2 rs[i] E[i,j] + C[i,j].
+// splits > 1 splits the single segment's k range across workgroups; partial
+// sums go to `partial` ([splits][M][N]) and a second kernel reduces them in a
+// fixed order before applying the epilogue.
+// ---------------------------------------------------------------------------
+enum : int { EPI_NONE = 0, EPI_GRADH = 1 };
+
+struct GemmDesc {
+  const float *A, *B, *A2, *B2;
+  float *C;
+  const float *Cin;
+  const float *rs;
+  const float *E;
+  float *C2;
+  float *partial;
+  int64_t lda, ldb, lda2, ldb2, ldc, ldcin, lde, ldc2;
+  int M, N, K, K2;
+  int tA, tB;
+  float alpha, beta;
+  int epi;
+  int splits;
+  int kchunk;  // k per split (multiple of 8) when splits > 1
+  int tiles_m, tiles_n;
+  int tile_begin;
+};
+
+constexpr int kMaxBatch = 6;
+
+struct GemmBatch {
+  GemmDesc d[kMaxBatch];
+  int n;
+  int total_tiles;
+};
+
+GemmDesc gemm_desc(int M, int N, int K, const float *A, int64_t lda, int tA, const float *B,
+                   int64_t ldb, int tB, float *C, int64_t ldc, float alpha = 1.f,
+                   const float *Cin = nullptr, int64_t ldcin = 0, float beta = 0.f);
+
+// Kernel instantiations (distinct symbols per step phase for profilers).
+enum : int {
+  GEMM_OTHER = 0,
+  GEMM_CONTRACT = 1,
+  GEMM_ZGRAD = 2,
+  GEMM_MID = 3,
+  GEMM_UPDATE = 4,
+  GEMM_NAIVE_FWD = 5,
+  GEMM_NAIVE_GRAD = 6,
+  GEMM_NAIVE_UPDATE = 7
+};
+
+// Enqueue every descriptor of the batch (one main launch plus one reduce launch
+// per split descriptor).  When gate is not null the kernels skip all writes if
+// *gate != 0 at kernel start.
+hipError_t gemm_launch(GemmBatch &b, const int *gate, hipStream_t s, int phase = GEMM_OTHER);
+
+// Choose a split count for a long-k descriptor and attach its partial buffer.
+// Returns the number of floats the partial buffer needs.
+size_t gemm_plan_split(GemmDesc &g, int target_wgs, float *partial);
+
+// ---------------------------------------------------------------------------
+// Step kernels (step_kernels.hip)
+// ---------------------------------------------------------------------------
+hipError_t launch_gather(hipStream_t s, int m, int K, int d, int64_t D, const float *H,
+                         const float *Hhat, const float *Htil, const int *idx, const float *val,
+                         const float *V, int64_t ldv, int loss, float eps, float lr, float *G,
+                         float *Atil, float *dq, float *dA, float *lvec, int *flag);
+
+hipError_t launch_small(hipStream_t s, int m, int K, float lr, const int *idx, const float *lvec,
+                        const float *dq, const float *dA, const float *N, const float *Mhat,
+                        const float *HZ, float *M, float *R, float *Cwork, int *srow,
+                        int *sslot, int *nvalid, float *loss_out, int *flag);
+
+hipError_t launch_scatter(hipStream_t s, int m, int K, int d, float lr, const int *srow,
+                          const int *sslot, const int *nvalid, const float *dA, const float *P,
+                          float *V, int64_t ldv, const int *flag);
+
+hipError_t launch_identity(hipStream_t s, float *A, int d, int64_t ld);
+hipError_t launch_fill(hipStream_t s, float *p, float v);
+
+// Naive-path kernels.
+hipError_t launch_colnorm(hipStream_t s, const float *O, int64_t D, int m, float *partial,
+                          int nblk);
+hipError_t launch_naive_epilogue(hipStream_t s, int m, int K, int64_t D, int nblk,
+                                 const float *partial, const float *O, const int *idx,
+                                 const float *val, int loss, float eps, float *dq, float *dA,
+                                 float *loss_out, int *flag);
+hipError_t launch_grad_o(hipStream_t s, float *O, int64_t D, int m, int K, const float *dq,
+                         const int *idx, const float *dA);
+
+}  // namespace lst

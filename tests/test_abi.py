@@ -1,0 +1,76 @@
+"""The C-ABI library loads, exports every symbol include/lst.h declares, and rejects bad
+arguments on the host (no GPU call is made by any of these)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_1606_08061_amd as lst
+from paper_1606_08061_amd import build as lst_build
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "lst.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(lst_\w+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(lst.LIB_PATH):
+        lst_build.build()
+    return lst.lib()
+
+
+def test_header_and_binding_agree():
+    assert _declared() == sorted(lst.SIGNATURES)
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in _declared():
+        assert hasattr(L, name), name
+        assert ctypes.cast(getattr(L, name), ctypes.c_void_p).value
+
+
+def test_status_strings(L):
+    for code, name in [(0, "LST_OK"), (-1, "LST_E_ARG"), (-3, "LST_E_INDEX"),
+                       (-4, "LST_E_NOT_SPD"), (-5, "LST_E_NONFINITE"), (7, "LST_E_UNKNOWN")]:
+        assert lst.status_string(code) == name
+
+
+def test_host_argument_errors(L):
+    # shape and argument checks run before any device call
+    P = 0x1000  # a non-null placeholder; never dereferenced on these paths
+    st, ctx = lst.lst_create(0, 8, 4, 2, 0, 1e-3, P, 8, P, P, P, 8, 0)
+    assert st == lst.LST_E_SHAPE and ctx == 0
+    st, _ = lst.lst_create(10, 8, 4, 2, 5, 1e-3, P, 8, P, P, P, 8, 0)
+    assert st == lst.LST_E_ARG
+    st, _ = lst.lst_create(10, 8, 4, 2, 1, 0.0, P, 8, P, P, P, 8, 0)
+    assert st == lst.LST_E_ARG
+    st, _ = lst.lst_create(10, 8, 4, 2, 0, 1e-3, 0, 8, P, P, P, 8, 0)
+    assert st == lst.LST_E_ARG
+    st, _ = lst.lst_create(10, 8, 4, 2, 0, 1e-3, P, 7, P, P, P, 8, 0)
+    assert st == lst.LST_E_SHAPE
+    st, _ = lst.lst_create(10, 8, 2048, 2, 0, 1e-3, P, 8, P, P, P, 8, 0)
+    assert st == lst.LST_E_SHAPE
+    st, _ = lst.lst_create(10, 8, 512, 64, 0, 1e-3, P, 8, P, P, P, 8, 0)
+    assert st == lst.LST_E_SHAPE
+    st, _ = lst.lst_naive_create(10, 0, 4, 2, 0, 1e-3, P, 8, 0)
+    assert st == lst.LST_E_SHAPE
+    assert lst.lst_step(0, P, 1, P, P, 1, 0.1, P, P) == lst.LST_E_ARG
+    assert lst.lst_sync_status(0) == lst.LST_E_ARG
+    assert lst.lst_materialize_W(0, P, 8) == lst.LST_E_ARG
+    lst.lst_destroy(0)
+
+
+def test_product_path_does_not_import_the_oracle():
+    pkg = os.path.join(ROOT, "paper_1606_08061_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"^\s*(from|import)\s+oracle\b", text, re.M), f
+                assert "oracle/" not in text, f

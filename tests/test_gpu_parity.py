@@ -1,0 +1,184 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 dense oracle.
+
+Tolerances: relative error <= 1e-4 on the loss and on grad_H (Frobenius) for a
+single step; <= 1e-3 on V U after 100 steps; integer/index results bit exact
+(rows of V outside a step's targets are unchanged bit for bit).
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_common import DEV, Compare, make_factored, oracle_step, rel, to_dev
+from workloads import LOSS_SPHERICAL_SOFTMAX, LOSS_SQUARED, WORKLOADS, Stream, Workload
+
+pytestmark = pytest.mark.gpu
+
+TOL1 = 1e-4
+TOL100 = 1e-3
+
+
+def _check_step(st, loss, grad, ref, tol=TOL1):
+    assert st == 0
+    assert abs(loss - ref.loss) <= tol * abs(ref.loss), (loss, ref.loss)
+    assert rel(grad, ref.grad_H) <= tol
+
+
+def test_small_config_single_step_and_invariants():
+    w = WORKLOADS["sq_D2k_d32_m16_K3"]
+    c = Compare(w)
+    st, loss, grad, ref = c.step()
+    _check_step(st, loss, grad, ref)
+    Wg = c.W_gpu()
+    assert rel(Wg, ref.W_new) <= TOL1
+    f = c.ctx
+    Q = f.Q.cpu().numpy().astype(np.float64)
+    U = f.U.cpu().numpy().astype(np.float64)
+    UinvT = f.UinvT.cpu().numpy().astype(np.float64)
+    assert rel(Q, ref.W_new.T @ ref.W_new) <= TOL1
+    assert np.abs(U @ UinvT.T - np.eye(w.d)).max() <= 1e-5
+    c.close()
+
+
+def test_small_config_100_steps():
+    w = WORKLOADS["sq_D2k_d32_m16_K3"]
+    c = Compare(w)
+    for t in range(w.steps):
+        st, loss, grad, ref = c.step()
+        _check_step(st, loss, grad, ref, TOL1 if t == 0 else TOL100)
+    assert rel(c.W_gpu(), c.W) <= TOL100
+    c.close()
+
+
+@pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX])
+@pytest.mark.parametrize("D,d,m,K", [
+    (50, 1, 1, 1), (300, 31, 2, 3), (1000, 33, 17, 2), (777, 65, 33, 1), (2000, 40, 70, 3),
+    (1500, 47, 130, 2), (3000, 24, 300, 1), (400, 64, 5, 0),
+])
+def test_awkward_shapes(loss, D, d, m, K):
+    w = Workload("t", loss, D, d, m, K, index_dist="uniform",
+                 value_dist="normal" if loss == LOSS_SQUARED else "ones", lr=0.01)
+    c = Compare(w, seed=D + d + m + K)
+    for t in range(4):
+        st, l, g, ref = c.step()
+        _check_step(st, l, g, ref, TOL1 if t == 0 else TOL100)
+    assert rel(c.W_gpu(), c.W) <= TOL100
+    c.close()
+
+
+def test_spherical_softmax_zipf_steps():
+    w = Workload("t", LOSS_SPHERICAL_SOFTMAX, 5000, 48, 32, 1, index_dist="zipf",
+                 value_dist="ones", steps=30)
+    c = Compare(w)
+    for t in range(w.steps):
+        st, l, g, ref = c.step()
+        _check_step(st, l, g, ref, TOL1 if t == 0 else TOL100)
+    assert rel(c.W_gpu(), c.W) <= TOL100
+    c.close()
+
+
+@pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX])
+def test_duplicates_and_empty_slots(loss):
+    # tiny D under Zipf: rows repeat across examples; some examples repeat an index or have -1
+    w = Workload("t", loss, 9, 8, 24, 3, index_dist="zipf",
+                 value_dist="normal" if loss == LOSS_SQUARED else "ones")
+    c = Compare(w)
+    for t in range(10):
+        H, idx, val = c.s.batch()
+        idx[0, 1] = idx[0, 0]
+        idx[1, 2] = -1
+        if t % 3 == 0:
+            idx[2, :] = -1
+        st, l, g, ref = c.step((H, idx, val))
+        _check_step(st, l, g, ref, TOL1 if t == 0 else TOL100)
+    assert rel(c.W_gpu(), c.W) <= TOL100
+    c.close()
+
+
+def test_all_slots_same_row():
+    w = Workload("t", LOSS_SQUARED, 100, 16, 40, 4)
+    c = Compare(w)
+    for _ in range(3):
+        H, idx, val = c.s.batch()
+        idx[:, :] = 7
+        st, l, g, ref = c.step((H, idx, val))
+        _check_step(st, l, g, ref, 1e-3)
+    assert rel(c.W_gpu(), c.W) <= TOL100
+    c.close()
+
+
+def test_general_U0():
+    rng = np.random.default_rng(3)
+    w = Workload("t", LOSS_SQUARED, 1200, 24, 10, 2)
+    U0 = (np.eye(24) + 0.2 * rng.standard_normal((24, 24))).astype(np.float32)
+    c = Compare(w, U0=U0)
+    for t in range(5):
+        st, l, g, ref = c.step()
+        _check_step(st, l, g, ref, 1e-4 if t == 0 else 1e-3)
+    assert rel(c.W_gpu(), c.W) <= 1e-3
+    c.close()
+
+
+def test_naive_path_matches_oracle():
+    for w in (WORKLOADS["sq_D2k_d32_m16_K3"],
+              Workload("t", LOSS_SPHERICAL_SOFTMAX, 3000, 40, 20, 1, index_dist="zipf",
+                       value_dist="ones")):
+        c = Compare(w, path="naive")
+        for t in range(10):
+            st, l, g, ref = c.step()
+            _check_step(st, l, g, ref, TOL1 if t == 0 else TOL100)
+        assert rel(c.W_gpu(), c.W) <= TOL100
+        c.close()
+
+
+def test_factored_and_naive_agree_over_steps():
+    w = Workload("t", LOSS_SQUARED, 4000, 64, 32, 3)
+    s = Stream(w)
+    f = make_factored(w, s.V0)
+    import paper_1606_08061_amd as lst
+    n = lst.Naive(w.D, w.d, w.m, w.K, w.loss, device=DEV)
+    n.init(to_dev(s.V0)[0])
+    for _ in range(20):
+        b = to_dev(*s.batch())
+        lf, gf = f.step(*b, w.lr)
+        ln, gn = n.step(*b, w.lr)
+        assert abs(lf.item() - ln.item()) <= 1e-3 * abs(ln.item())
+    f.check()
+    n.check()
+    assert rel(f.materialize_W().cpu().numpy(), n.W.cpu().numpy()) <= 1e-3
+    f.close()
+    n.close()
+
+
+def test_zero_batch_and_no_targets():
+    w = Workload("t", LOSS_SQUARED, 500, 16, 8, 2)
+    c = Compare(w)
+    V = c.ctx.V.clone()
+    H, idx, val = c.s.batch()
+    loss, _ = c.ctx.step(*to_dev(H[:0], idx[:0], val[:0]), w.lr)
+    assert c.ctx.sync_status() == 0 and loss.item() == 0.0
+    assert torch.equal(V, c.ctx.V)
+    # K = 0: no targets, y = 0
+    st, l, g, ref = c.step((H, idx[:, :0].copy(), val[:, :0].copy()))
+    _check_step(st, l, g, ref)
+    c.close()
+
+
+def test_untouched_rows_bit_identical_and_deterministic():
+    w = Workload("t", LOSS_SQUARED, 20000, 96, 64, 4, index_dist="zipf")
+    s = Stream(w)
+    batches = [s.batch() for _ in range(5)]
+    outs = []
+    for rep in range(2):
+        f = make_factored(w, s.V0)
+        for H, idx, val in batches:
+            V_before = f.V.clone()
+            loss, g = f.step(*to_dev(H, idx, val), w.lr)
+            f.check()
+            touched = torch.zeros(w.D, dtype=torch.bool, device=DEV)
+            touched[torch.from_numpy(idx.reshape(-1).astype(np.int64)).to(DEV)] = True
+            assert torch.equal(f.V[~touched], V_before[~touched])
+            assert not torch.equal(f.V[touched], V_before[touched])
+        outs.append([t.clone() for t in (f.V, f.U, f.UinvT, f.Q, loss, g)])
+        f.close()
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
