@@ -37,8 +37,12 @@ def phase_work(w, idx_pool):
         "gather": ("hbm", 4.0 * (m * K * d + 5 * m * d), "byte"),
         # Z^ = U^T G, H^T H^, H~^T G
         "zgrad": ("mfma", 2.0 * (m * d * d + 2 * m * m * d), "flop"),
-        # Gauss-Jordan inverse of the m x m Woodbury matrix and the M entries
-        "small": ("alu", 2.0 * m ** 3 + 8.0 * m * m, "flop"),
+        # Gauss-Jordan inverse of the m x m Woodbury matrix (m^3 multiply-adds)
+        "woodbury": ("alu", 2.0 * m ** 3, "flop"),
+        # loss sum and the m x m entries of M
+        "mblock": ("alu", 8.0 * m * m, "flop"),
+        # bitonic sort of the m*K (row, slot) keys: n log2(n)^2 / 2 compare-exchanges
+        "sort": ("alu", 0.5 * (m * K) * max(np.log2(max(m * K, 2)), 1.0) ** 2, "flop"),
         # R X, M H, U update
         "mid": ("mfma", 2.0 * (m * d * d + 2 * m * m * d), "flop"),
         # U^-T update, Q update (two products), P
@@ -95,7 +99,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=128)
     ap.add_argument("--workload", default="sq_D200k_d500_m128_K5")
     ap.add_argument("--pool", type=int, default=64, help="distinct minibatches cycled through")
     ap.add_argument("--naive-steps", type=int, default=20)
@@ -137,8 +141,10 @@ def main():
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     e0.record()
+    h0 = time.perf_counter()
     for t in range(args.steps):
         f.step(*gpool[t % len(gpool)], w.lr, grad_H=grad)
+    host_us = (time.perf_counter() - h0) / args.steps * 1e6
     e1.record()
     torch.cuda.synchronize()
     ms_total = e0.elapsed_time(e1)
@@ -204,6 +210,7 @@ def main():
         "naive": naive,
         "speedup_vs_naive": round(value / naive["value"], 2) if naive else None,
         "speedup_model_D_over_4d": round(w.D / (4 * w.d), 1),
+        "host_enqueue_us_per_step": round(host_us, 2),
         "phases_us": {k: round(v[1] / max(v[0], 1) * 1e3, 2) for k, v in phases.items() if v[0]},
     }
     print(json.dumps(out), flush=True)

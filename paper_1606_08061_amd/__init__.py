@@ -9,5 +9,6 @@ from ._binding import (  # noqa: F401
     LST_E_SHAPE, LST_E_STATE, LST_LOSS_SPHERICAL_SOFTMAX, LST_LOSS_SQUARED, LST_OK, SIGNATURES,
     Factored, LstError, Naive, lib, library_path, lst_create, lst_destroy, lst_init_factored,
     lst_materialize_W, lst_naive_create, lst_naive_step, lst_profile_enable, lst_profile_read,
+    lst_use_graphs,
     lst_step, lst_sync_status, status_string, PHASES,
 )

@@ -46,11 +46,12 @@ SIGNATURES = {
     "lst_naive_create": (_I32, [ctypes.POINTER(_P), _I64, _I32, _I32, _I32, _I32, _F, _P, _I64,
                                 _P]),
     "lst_naive_step": (_I32, [_P, _P, _I32, _P, _P, _I32, _F, _P, _P]),
+    "lst_use_graphs": (_I32, [_P, _I32]),
     "lst_profile_enable": (_I32, [_P, _I32]),
     "lst_profile_read": (_I32, [_P, ctypes.POINTER(_I32), ctypes.POINTER(ctypes.c_double), _I32]),
 }
 
-PHASES = ["contract", "gather", "zgrad", "small", "mid", "update", "scatter",
+PHASES = ["contract", "gather", "zgrad", "mblock", "woodbury", "sort", "mid", "update", "scatter",
           "naive_fwd", "naive_loss", "naive_grad", "naive_update"]
 
 _lib = None
@@ -138,6 +139,10 @@ def lst_sync_status(ctx) -> int:
 
 def lst_destroy(ctx) -> None:
     lib().lst_destroy(ctx)
+
+
+def lst_use_graphs(ctx, on) -> int:
+    return lib().lst_use_graphs(ctx, on)
 
 
 def lst_profile_enable(ctx, on) -> int:
@@ -255,6 +260,9 @@ class Factored(_Ctx):
         _need(out, torch.float32, (self.D, self.d), "W")
         _check(lst_materialize_W(self.ctx, _ptr(out), self.d), "lst_materialize_W")
         return out
+
+    def use_graphs(self, on: bool = True) -> None:
+        _check(lst_use_graphs(self.ctx, 1 if on else 0), "lst_use_graphs")
 
 
 class Naive(_Ctx):

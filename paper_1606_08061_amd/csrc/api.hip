@@ -29,6 +29,17 @@ struct Carver {
   }
 };
 
+// A factored step recorded as a HIP graph, replayed when the same arguments recur.
+struct GraphEntry {
+  const void *H, *idx, *val;
+  void *loss, *grad;
+  int m, K;
+  uint32_t lr_bits;
+  hipGraphExec_t exec;
+  uint64_t last_use;
+};
+constexpr size_t kGraphCap = 256;
+
 }  // namespace
 
 struct lst_ctx {
@@ -54,10 +65,20 @@ struct lst_ctx {
   int *srow, *sslot, *nvalid, *flag;
   float *O, *colpart, *splitpart;
   hipError_t last_err;
+  // side streams of a factored step (sort; Woodbury inverse) and their fork/join events;
+  // cap is the stream a step is captured on when it is recorded as a HIP graph
+  hipStream_t side[2];
+  hipStream_t cap;
+  hipEvent_t ev_fork, ev_wood_ready, ev_wood_done, ev_sort_done;
+  bool have_side;
   // tracing: event pairs per phase
   bool prof_on;
   std::vector<hipEvent_t> prof_ev[LST_NUM_PHASES];
   int prof_used[LST_NUM_PHASES];
+  // captured steps, one per distinct (inputs, m, K, lr)
+  bool use_graphs;
+  std::vector<GraphEntry> graphs;
+  uint64_t graph_tick;
 };
 
 namespace {
@@ -153,7 +174,7 @@ int record(lst_ctx *c, hipError_t e) {
 constexpr int kProfCap = 65536;
 
 // Records the start (begin=true) or the end of a phase when profiling is on.
-void prof(lst_ctx *c, int phase, bool begin) {
+void prof(lst_ctx *c, int phase, bool begin, hipStream_t st = nullptr) {
   if (!c->prof_on) return;
   int &used = c->prof_used[phase];
   if (used >= kProfCap) return;
@@ -167,8 +188,32 @@ void prof(lst_ctx *c, int phase, bool begin) {
     }
     ev.push_back(e);
   }
-  (void)hipEventRecord(ev[slot], c->stream);
+  (void)hipEventRecord(ev[slot], st ? st : c->stream);
   if (!begin) ++used;
+}
+
+int side_create(lst_ctx *c) {
+  for (int i = 0; i < 2; ++i)
+    if (hipStreamCreateWithFlags(&c->side[i], hipStreamNonBlocking) != hipSuccess) return LST_E_HIP;
+  if (hipStreamCreateWithFlags(&c->cap, hipStreamNonBlocking) != hipSuccess) return LST_E_HIP;
+  hipEvent_t *evs[4] = {&c->ev_fork, &c->ev_wood_ready, &c->ev_wood_done, &c->ev_sort_done};
+  for (hipEvent_t *e : evs)
+    if (hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) return LST_E_HIP;
+  c->have_side = true;
+  return LST_OK;
+}
+
+void side_free(lst_ctx *c) {
+  if (!c->have_side) return;
+  for (int i = 0; i < 2; ++i)
+    if (c->side[i]) (void)hipStreamDestroy(c->side[i]);
+  if (c->cap) (void)hipStreamDestroy(c->cap);
+  for (GraphEntry &g : c->graphs) (void)hipGraphExecDestroy(g.exec);
+  c->graphs.clear();
+  hipEvent_t evs[4] = {c->ev_fork, c->ev_wood_ready, c->ev_wood_done, c->ev_sort_done};
+  for (hipEvent_t e : evs)
+    if (e) (void)hipEventDestroy(e);
+  c->have_side = false;
 }
 
 void prof_free(lst_ctx *c) {
@@ -259,7 +304,9 @@ int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max
   c->Q = Q;
   c->ldd = ldd;
   c->last_err = hipSuccess;
+  c->use_graphs = true;
   st = alloc_ws(c, carve_factored);
+  if (st == LST_OK) st = side_create(c);
   if (st != LST_OK) {
     lst_destroy(c);
     return st;
@@ -304,6 +351,9 @@ void lst_destroy(lst_ctx *c) {
     (void)hipStreamSynchronize(c->stream);
     (void)hipFree(c->ws);
   }
+  if (c->have_side)
+    for (int i = 0; i < 2; ++i) (void)hipStreamSynchronize(c->side[i]);
+  side_free(c);
   prof_free(c);
   delete c;
 }
@@ -337,6 +387,9 @@ int lst_profile_read(lst_ctx *c, int32_t *counts, double *ms, int32_t n) {
 int lst_sync_status(lst_ctx *c) {
   if (!c) return LST_E_ARG;
   if (hipStreamSynchronize(c->stream) != hipSuccess) return LST_E_HIP;
+  if (c->have_side)
+    for (int i = 0; i < 2; ++i)
+      if (hipStreamSynchronize(c->side[i]) != hipSuccess) return LST_E_HIP;
   if (c->last_err != hipSuccess) {
     c->last_err = hipSuccess;
     return LST_E_HIP;
@@ -428,25 +481,51 @@ int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0
   return st;
 }
 
-int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val, int32_t K,
-             float lr, float *loss_dev, float *grad_H) {
-  if (!c) return LST_E_ARG;
-  if (c->kind != KIND_FACTORED) return LST_E_STATE;
-  int st = step_args(c, H, m, idx, val, K, lr, loss_dev);
-  if (st != LST_OK) return st;
-  hipStream_t s = c->stream;
-  if (m == 0) return record(c, launch_fill(s, loss_dev, 0.f));
+}  // extern "C"
+
+namespace {
+
+// Enqueues one factored step on stream s (and the context's side streams).
+int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, const int32_t *idx,
+                          const float *val, int32_t K, float lr, float *loss_dev,
+                          float *grad_H) {
   const int d = c->d, ldd = c->ldd;
   float *gH = grad_H ? grad_H : c->gradH;
 
-  // H^ = Q H, H~ = U H, X = U^{-T} H (Algorithm 3 steps 1, 5, 6; Algorithm 4 rows 1, 5),
-  // and N = H^T H for the Woodbury matrix.
+  hipStream_t s_wood = c->side[0], s_sort = c->side[1];
+  // Fork.  The sort of the target keys only needs idx.
+  if (record(c, hipEventRecord(c->ev_fork, s)) || record(c, hipStreamWaitEvent(s_sort, c->ev_fork, 0)))
+    return LST_E_HIP;
+  prof(c, LST_PHASE_SORT, true, s_sort);
+  if (record(c, launch_sort(s_sort, m * K, idx, c->srow, c->sslot, c->nvalid))) return LST_E_HIP;
+  prof(c, LST_PHASE_SORT, false, s_sort);
+  if (record(c, hipEventRecord(c->ev_sort_done, s_sort))) return LST_E_HIP;
+
+  // Woodbury branch: N = H^T H, then C = I - 2 eta S N S and its inverse.  For
+  // squared error dl/dq = 1 and the branch needs nothing else; the spherical
+  // softmax waits for dl/dq = T / (q + D eps) from the gather.
+  const bool unit_dq = (c->loss == LST_LOSS_SQUARED);
+  if (record(c, hipStreamWaitEvent(s_wood, c->ev_fork, 0))) return LST_E_HIP;
+  prof(c, LST_PHASE_WOODBURY, true, s_wood);
+  GemmBatch bn{};
+  bn.d[0] = gemm_desc(m, m, d, H, d, 0, H, d, 0, c->N, m);
+  bn.n = 1;
+  if (record(c, gemm_launch(bn, nullptr, s_wood))) return LST_E_HIP;
+  auto woodbury = [&]() -> int {
+    if (record(c, launch_woodbury(s_wood, m, lr, unit_dq ? 1 : 0, c->dq, c->N, c->R, c->Cwork,
+                                  c->flag)))
+      return LST_E_HIP;
+    prof(c, LST_PHASE_WOODBURY, false, s_wood);
+    return record(c, hipEventRecord(c->ev_wood_done, s_wood));
+  };
+  if (unit_dq && woodbury() != LST_OK) return LST_E_HIP;
+
+  // H^ = Q H, H~ = U H, X = U^{-T} H (Algorithm 3 steps 1, 5, 6; Algorithm 4 rows 1, 5).
   GemmBatch b1{};
   b1.d[0] = gemm_desc(m, d, d, H, d, 0, c->Q, ldd, 0, c->Hhat, d);
   b1.d[1] = gemm_desc(m, d, d, H, d, 0, c->U, ldd, 0, c->Htil, d);
   b1.d[2] = gemm_desc(m, d, d, H, d, 0, c->UinvT, ldd, 0, c->X, d);
-  b1.d[3] = gemm_desc(m, m, d, H, d, 0, H, d, 0, c->N, m);
-  b1.n = 4;
+  b1.n = 3;
   prof(c, LST_PHASE_CONTRACT, true);
   if (record(c, gemm_launch(b1, nullptr, s, GEMM_CONTRACT))) return LST_E_HIP;
   prof(c, LST_PHASE_CONTRACT, false);
@@ -457,6 +536,11 @@ int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const fl
                               c->loss, c->eps, lr, c->G, c->Atil, c->dq, c->dA, c->lvec, c->flag)))
     return LST_E_HIP;
   prof(c, LST_PHASE_GATHER, false);
+  if (!unit_dq) {
+    if (record(c, hipEventRecord(c->ev_wood_ready, s)) ||
+        record(c, hipStreamWaitEvent(s_wood, c->ev_wood_ready, 0)) || woodbury() != LST_OK)
+      return LST_E_HIP;
+  }
 
   // Z^ = U^T G with grad_H = 2 H^ diag(dl/dq) + Z^; M^ = H^T H^; H^T Z^ = H~^T G.
   GemmBatch b2{};
@@ -475,12 +559,15 @@ int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const fl
   if (record(c, gemm_launch(b2, nullptr, s, GEMM_ZGRAD))) return LST_E_HIP;
   prof(c, LST_PHASE_ZGRAD, false);
 
-  // Loss, M, Woodbury inverse, sorted scatter keys; sets the error flag.
-  prof(c, LST_PHASE_SMALL, true);
-  if (record(c, launch_small(s, m, K, lr, idx, c->lvec, c->dq, c->dA, c->N, c->Mhat, c->HZ, c->M,
-                             c->R, c->Cwork, c->srow, c->sslot, c->nvalid, loss_dev, c->flag)))
+  // Loss and M; sets the error flag on a non-finite loss.
+  prof(c, LST_PHASE_MBLOCK, true);
+  if (record(c, launch_mblock(s, m, K, idx, c->lvec, c->dq, c->dA, c->Mhat, c->HZ, c->M, loss_dev,
+                              c->flag)))
     return LST_E_HIP;
-  prof(c, LST_PHASE_SMALL, false);
+  prof(c, LST_PHASE_MBLOCK, false);
+
+  // Join the Woodbury branch before its result (and its error flag) is used.
+  if (record(c, hipStreamWaitEvent(s, c->ev_wood_done, 0))) return LST_E_HIP;
 
   // Gated state updates.  Yw = R X; Zq = (eta^2/2) M H - eta grad_H;
   // U <- U - 2 eta H~ diag(dl/dq) H^T (eq. updateU / gen-updateU).
@@ -511,11 +598,76 @@ int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const fl
   prof(c, LST_PHASE_UPDATE, false);
 
   // V_r -= eta sum dl/dA P_j over the slots of each distinct target row (eq. updateV).
+  if (record(c, hipStreamWaitEvent(s, c->ev_sort_done, 0))) return LST_E_HIP;
   prof(c, LST_PHASE_SCATTER, true);
   if (record(c, launch_scatter(s, m, K, d, lr, c->srow, c->sslot, c->nvalid, c->dA, c->P, c->V,
                                c->ldv, c->flag)))
     return LST_E_HIP;
   prof(c, LST_PHASE_SCATTER, false);
+  return LST_OK;
+}
+
+// Replays (capturing first if needed) the graph of a step with these arguments.
+int graph_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val,
+               int32_t K, float lr, float *loss_dev, float *grad_H) {
+  uint32_t lr_bits;
+  std::memcpy(&lr_bits, &lr, sizeof(lr_bits));
+  GraphEntry *hit = nullptr;
+  for (GraphEntry &g : c->graphs)
+    if (g.H == H && g.idx == idx && g.val == val && g.loss == loss_dev && g.grad == grad_H &&
+        g.m == m && g.K == K && g.lr_bits == lr_bits) {
+      hit = &g;
+      break;
+    }
+  if (!hit) {
+    if (c->graphs.size() >= kGraphCap) {  // evict the least recently used graph
+      size_t v = 0;
+      for (size_t i = 1; i < c->graphs.size(); ++i)
+        if (c->graphs[i].last_use < c->graphs[v].last_use) v = i;
+      if (record(c, hipStreamSynchronize(c->stream))) return LST_E_HIP;
+      (void)hipGraphExecDestroy(c->graphs[v].exec);
+      c->graphs.erase(c->graphs.begin() + v);
+    }
+    if (record(c, hipStreamBeginCapture(c->cap, hipStreamCaptureModeThreadLocal))) return LST_E_HIP;
+    const int st = enqueue_factored_step(c, c->cap, H, m, idx, val, K, lr, loss_dev, grad_H);
+    hipGraph_t graph = nullptr;
+    const hipError_t ec = hipStreamEndCapture(c->cap, &graph);
+    if (st != LST_OK || ec != hipSuccess || !graph) {
+      if (graph) (void)hipGraphDestroy(graph);
+      if (ec != hipSuccess) c->last_err = ec;
+      return st != LST_OK ? st : LST_E_HIP;
+    }
+    GraphEntry e{H, idx, val, loss_dev, grad_H, m, K, lr_bits, nullptr, 0};
+    const hipError_t ei = hipGraphInstantiate(&e.exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (record(c, ei)) return LST_E_HIP;
+    c->graphs.push_back(e);
+    hit = &c->graphs.back();
+  }
+  hit->last_use = ++c->graph_tick;
+  return record(c, hipGraphLaunch(hit->exec, c->stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val, int32_t K,
+             float lr, float *loss_dev, float *grad_H) {
+  if (!c) return LST_E_ARG;
+  if (c->kind != KIND_FACTORED) return LST_E_STATE;
+  int st = step_args(c, H, m, idx, val, K, lr, loss_dev);
+  if (st != LST_OK) return st;
+  if (m == 0) return record(c, launch_fill(c->stream, loss_dev, 0.f));
+  if (c->use_graphs && !c->prof_on)
+    return graph_step(c, H, m, idx, val, K, lr, loss_dev, grad_H);
+  return enqueue_factored_step(c, c->stream, H, m, idx, val, K, lr, loss_dev, grad_H);
+}
+
+int lst_use_graphs(lst_ctx *c, int32_t on) {
+  if (!c) return LST_E_ARG;
+  if (c->kind != KIND_FACTORED) return LST_E_STATE;
+  c->use_graphs = on != 0;
   return LST_OK;
 }
 

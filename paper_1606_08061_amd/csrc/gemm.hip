@@ -3,9 +3,9 @@
 // Every d x d and d x m contraction of the factored step (Algorithm 3 steps
 // 1, 2, 5, 6, 8 and the matching rows of Algorithm 4), the m x m products
 // (H^T H, H^T H^, H~^T G) and the naive path's D x d products go through this
-// one kernel.  A workgroup owns a 32 x 32 output tile; its four wavefronts
-// split the k range and their accumulators are summed through LDS in a fixed
-// order, so results do not depend on scheduling.
+// one kernel template.  A workgroup owns a 32 x 32 output tile; its NW
+// wavefronts split the k range and their accumulators are summed through LDS
+// in a fixed order, so results do not depend on scheduling.
 //
 // MFMA operand mapping (one 32x32x2 instruction, 64 lanes): lane l supplies
 // A[i = l%32][kk = l/32] and B[kk = l/32][j = l%32]; the 16 accumulator values
@@ -13,6 +13,11 @@
 // is consumed by four instructions; in instruction s lane-half h feeds
 // k = kb + 4h + s for both operands, so each lane reads 4 consecutive k values
 // of its row (one 16-byte load when k is the contiguous dimension).
+//
+// Loads are branch free: a lane whose output row (column) lies beyond M (N)
+// reads the last valid row instead, since that output is never stored; only
+// the ragged end of the k range is masked.  Operands are fetched kStage
+// k-blocks ahead of the matrix cores.
 #include "lst_internal.h"
 
 namespace lst {
@@ -21,66 +26,114 @@ namespace {
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
+constexpr int kStage = 4;
 
-// Loads opX(idx, k0..k0+3) for one lane.  kcontig: element = p[idx*ld + k];
-// otherwise element = p[k*ld + idx].  Out-of-range elements read as 0.
-__device__ __forceinline__ void load4(const float *__restrict__ p, int64_t ld, bool kcontig,
-                                      bool vec_ok, int idx, int idx_lim, int k0, int k_lim,
-                                      float out[4]) {
-  out[0] = out[1] = out[2] = out[3] = 0.f;
-  if (idx >= idx_lim) return;
-  if (kcontig) {
-    const float *q = p + (int64_t)idx * ld + k0;
-    if (vec_ok && k0 + 3 < k_lim) {
-      const float4 v = *reinterpret_cast<const float4 *>(q);
-      out[0] = v.x;
-      out[1] = v.y;
-      out[2] = v.z;
-      out[3] = v.w;
-    } else {
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-        if (k0 + s < k_lim) out[s] = q[s];
-    }
+// Operand access modes.  VEC: k contiguous and 16-byte aligned, one float4 per
+// lane; STRIDED: four scalars at p[idx*si + (k0+s)*sk] (k contiguous with an
+// unaligned stride, or the index contiguous).
+enum : int { VEC = 0, STRIDED = 1 };
+
+template <int MODE>
+__device__ __forceinline__ void ld4(const float *__restrict__ p, int64_t si, int64_t sk, int idx,
+                                    int k0, float (&o)[4]) {
+  if constexpr (MODE == VEC) {
+    const float4 v = *reinterpret_cast<const float4 *>(p + (int64_t)idx * si + k0);
+    o[0] = v.x;
+    o[1] = v.y;
+    o[2] = v.z;
+    o[3] = v.w;
   } else {
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-      if (k0 + s < k_lim) out[s] = p[(int64_t)(k0 + s) * ld + idx];
+    const float *q = p + (int64_t)idx * si + (int64_t)k0 * sk;
+    o[0] = q[0];
+    o[1] = q[sk];
+    o[2] = q[2 * sk];
+    o[3] = q[3 * sk];
   }
 }
 
-__device__ __forceinline__ bool aligned16(const float *p, int64_t ld) {
+// Ragged end of the k range: k >= kend reads as zero (address clamped).
+__device__ __forceinline__ void ld4_tail(const float *__restrict__ p, int64_t si, int64_t sk,
+                                         int idx, int k0, int kend, float (&o)[4]) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const int kk = k0 + s;
+    const float v = p[(int64_t)idx * si + (int64_t)min(kk, kend - 1) * sk];
+    o[s] = (kk < kend) ? v : 0.f;
+  }
+}
+
+// One wavefront's share of the k range [kbeg, kend): full blocks of 8 with
+// index wave, wave + NW, ...; the ragged tail block goes to wave NW-1.
+template <int NW, int AM, int BM>
+__device__ __forceinline__ void kloop(floatx16 &acc, const float *A, int64_t asi, int64_t ask,
+                                      const float *B, int64_t bsi, int64_t bsk, int ia, int jb,
+                                      int kbeg, int kend, int wave, int lh) {
+  const int nfull = (kend - kbeg) >> 3;
+  const int nw = nfull > wave ? (nfull - wave + NW - 1) / NW : 0;
+  if (nw > 0) {
+    auto kof = [&](int s) { return kbeg + 8 * (wave + NW * min(s, nw - 1)) + 4 * lh; };
+    float a[kStage][4], b[kStage][4];
+#pragma unroll
+    for (int u = 0; u < kStage; ++u) {
+      ld4<AM>(A, asi, ask, ia, kof(u), a[u]);
+      ld4<BM>(B, bsi, bsk, jb, kof(u), b[u]);
+    }
+    for (int s0 = 0; s0 < nw; s0 += kStage) {
+      float an[kStage][4], bn[kStage][4];
+#pragma unroll
+      for (int u = 0; u < kStage; ++u) {
+        ld4<AM>(A, asi, ask, ia, kof(s0 + kStage + u), an[u]);
+        ld4<BM>(B, bsi, bsk, jb, kof(s0 + kStage + u), bn[u]);
+      }
+#pragma unroll
+      for (int u = 0; u < kStage; ++u) {
+        if (s0 + u < nw) {
+#pragma unroll
+          for (int s = 0; s < 4; ++s)
+            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[u][s], b[u][s], acc, 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kStage; ++u)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          a[u][s] = an[u][s];
+          b[u][s] = bn[u][s];
+        }
+    }
+  }
+  if (((kend - kbeg) & 7) && wave == NW - 1) {
+    const int k0 = kbeg + 8 * nfull + 4 * lh;
+    float a[4], b[4];
+    ld4_tail(A, asi, ask, ia, k0, kend, a);
+    ld4_tail(B, bsi, bsk, jb, k0, kend, b);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], b[s], acc, 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ bool vec_ok(const float *p, int64_t ld) {
   return ((reinterpret_cast<uintptr_t>(p) & 15) == 0) && ((ld & 3) == 0);
 }
 
-// k-loop of one wavefront over [kbeg, kend) in blocks of 8 strided by kWaves*8.
-__device__ __forceinline__ void kloop(floatx16 &acc, const float *A, int64_t lda, int tA,
-                                      const float *B, int64_t ldb, int tB, int i, int M, int j,
-                                      int N, int kbeg, int kend, int wave, int lh) {
-  const bool ak = (tA == 0), bk = (tB == 0);
-  const bool av = ak && aligned16(A, lda);
-  const bool bv = bk && aligned16(B, ldb);
-  int kb = kbeg + 8 * wave;
-  if (kb >= kend) return;
-  float a[4], b[4], an[4], bn[4];
-  load4(A, lda, ak, av, i, M, kb + 4 * lh, kend, a);
-  load4(B, ldb, bk, bv, j, N, kb + 4 * lh, kend, b);
-  for (; kb < kend; kb += 8 * kWaves) {
-    const int kn = kb + 8 * kWaves;
-    if (kn < kend) {
-      load4(A, lda, ak, av, i, M, kn + 4 * lh, kend, an);
-      load4(B, ldb, bk, bv, j, N, kn + 4 * lh, kend, bn);
-    }
-#pragma unroll
-    for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], b[s], acc, 0, 0, 0);
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      a[s] = an[s];
-      b[s] = bn[s];
-    }
-  }
+// opA(i,k): tA = 0 -> A[i*lda + k] (index stride lda, k stride 1); tA = 1 -> A[k*lda + i].
+// opB(k,j): tB = 0 -> B[j*ldb + k];                                 tB = 1 -> B[k*ldb + j].
+template <int NW>
+__device__ __forceinline__ void segment(floatx16 &acc, const float *A, int64_t lda, int tA,
+                                        const float *B, int64_t ldb, int tB, int ia, int jb,
+                                        int kbeg, int kend, int wave, int lh) {
+  const int64_t asi = tA ? 1 : lda, ask = tA ? lda : 1;
+  const int64_t bsi = tB ? 1 : ldb, bsk = tB ? ldb : 1;
+  const bool av = !tA && vec_ok(A, lda);
+  const bool bv = !tB && vec_ok(B, ldb);
+  if (av && bv)
+    kloop<NW, VEC, VEC>(acc, A, asi, ask, B, bsi, bsk, ia, jb, kbeg, kend, wave, lh);
+  else if (av)
+    kloop<NW, VEC, STRIDED>(acc, A, asi, ask, B, bsi, bsk, ia, jb, kbeg, kend, wave, lh);
+  else if (bv)
+    kloop<NW, STRIDED, VEC>(acc, A, asi, ask, B, bsi, bsk, ia, jb, kbeg, kend, wave, lh);
+  else
+    kloop<NW, STRIDED, STRIDED>(acc, A, asi, ask, B, bsi, bsk, ia, jb, kbeg, kend, wave, lh);
 }
 
 __device__ __forceinline__ void finish(const GemmDesc &g, int i, int j, float v) {
@@ -90,11 +143,19 @@ __device__ __forceinline__ void finish(const GemmDesc &g, int i, int j, float v)
   if (g.epi == EPI_GRADH) g.C2[(int64_t)i * g.ldc2 + j] = 2.f * g.rs[i] * g.E[(int64_t)i * g.lde + j] + out;
 }
 
+// Workgroup w runs on XCD w % 8; consecutive logical tiles are given to the same
+// XCD so that tiles sharing an operand panel share that XCD's L2.
+__device__ __forceinline__ int xcd_tile(int wg, int T) {
+  const int q = T >> 3, r = T & 7;
+  const int x = wg & 7, slot = wg >> 3;
+  return x < r ? x * (q + 1) + slot : r * (q + 1) + (x - r) * q + slot;
+}
+
 // PHASE only names the instantiation, so profilers report each step phase separately.
-template <int PHASE>
-__global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatch bt, const int *__restrict__ gate) {
+template <int PHASE, int NW>
+__global__ __launch_bounds__(64 * NW) void gemm_kernel(const GemmBatch bt, const int *__restrict__ gate) {
   if (gate && *gate != 0) return;
-  const int tile = blockIdx.x;
+  const int tile = xcd_tile(blockIdx.x, bt.total_tiles);
   int di = 0;
 #pragma unroll
   for (int q = 1; q < kMaxBatch; ++q)
@@ -111,6 +172,7 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatch bt, cons
   const int tm = t2 / g.tiles_n;
   const int tn = t2 - tm * g.tiles_n;
   const int i0 = tm * 32, j0 = tn * 32;
+  const int ia = min(i0 + li, g.M - 1), jb = min(j0 + li, g.N - 1);
 
   floatx16 acc;
 #pragma unroll
@@ -119,22 +181,21 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(const GemmBatch bt, cons
   if (g.splits > 1) {
     const int kbeg = split * g.kchunk;
     const int kend = min(g.K, kbeg + g.kchunk);
-    kloop(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, i0 + li, g.M, j0 + li, g.N, kbeg, kend, wave, lh);
+    segment<NW>(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, ia, jb, kbeg, kend, wave, lh);
   } else {
-    kloop(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, i0 + li, g.M, j0 + li, g.N, 0, g.K, wave, lh);
-    if (g.K2 > 0)
-      kloop(acc, g.A2, g.lda2, g.tA, g.B2, g.ldb2, g.tB, i0 + li, g.M, j0 + li, g.N, 0, g.K2, wave, lh);
+    segment<NW>(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, ia, jb, 0, g.K, wave, lh);
+    if (g.K2 > 0) segment<NW>(acc, g.A2, g.lda2, g.tA, g.B2, g.ldb2, g.tB, ia, jb, 0, g.K2, wave, lh);
   }
 
-  __shared__ float red[kWaves][16][64];
+  __shared__ float red[NW][16][64];
 #pragma unroll
   for (int r = 0; r < 16; ++r) red[wave][r][lane] = acc[r];
   __syncthreads();
-  for (int o = threadIdx.x; o < 1024; o += kThreads) {
+  for (int o = threadIdx.x; o < 1024; o += 64 * NW) {
     const int r = o >> 6, ln = o & 63;
     float v = 0.f;
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) v += red[w][r][ln];
+    for (int w = 0; w < NW; ++w) v += red[w][r][ln];
     const int i = i0 + (r >> 2) * 8 + (ln >> 5) * 4 + (r & 3);
     const int j = j0 + (ln & 31);
     if (i < g.M && j < g.N) {
@@ -156,6 +217,11 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const GemmDesc g, co
     const int i = (int)(e / g.N), j = (int)(e % g.N);
     finish(g, i, j, v);
   }
+}
+
+template <int P, int NW>
+void launch_phase(int total, hipStream_t s, const GemmBatch &b, const int *gate) {
+  hipLaunchKernelGGL((gemm_kernel<P, NW>), dim3(total), dim3(64 * NW), 0, s, b, gate);
 }
 
 }  // namespace
@@ -207,22 +273,32 @@ size_t gemm_plan_split(GemmDesc &g, int target_wgs, float *partial) {
 
 hipError_t gemm_launch(GemmBatch &b, const int *gate, hipStream_t s, int phase) {
   int total = 0;
+  int kmax = 0;
   for (int q = 0; q < b.n; ++q) {
     GemmDesc &g = b.d[q];
     g.tiles_m = (g.M + 31) / 32;
     g.tiles_n = (g.N + 31) / 32;
     g.tile_begin = total;
-    if (g.M > 0 && g.N > 0) total += g.tiles_m * g.tiles_n * (g.splits > 1 ? g.splits : 1);
+    if (g.M > 0 && g.N > 0) {
+      total += g.tiles_m * g.tiles_n * (g.splits > 1 ? g.splits : 1);
+      const int kk = g.splits > 1 ? g.kchunk : g.K + g.K2;
+      if (kk > kmax) kmax = kk;
+    }
   }
   b.total_tiles = total;
   if (total == 0) return hipSuccess;
   // Empty descriptors (M or N == 0) own no tiles; give them tile_begin past the end.
   for (int q = 0; q < b.n; ++q)
     if (b.d[q].M <= 0 || b.d[q].N <= 0) b.d[q].tile_begin = total;
+  // Waves per tile: enough to keep each wave's share of k short.
+  const bool wide = kmax >= 384;
   switch (phase) {
-#define LST_GEMM_CASE(P)                                                              \
-  case P:                                                                             \
-    hipLaunchKernelGGL(gemm_kernel<P>, dim3(total), dim3(kThreads), 0, s, b, gate); \
+#define LST_GEMM_CASE(P)                     \
+  case P:                                    \
+    if (wide)                                \
+      launch_phase<P, 8>(total, s, b, gate); \
+    else                                     \
+      launch_phase<P, 4>(total, s, b, gate); \
     break;
     LST_GEMM_CASE(GEMM_CONTRACT)
     LST_GEMM_CASE(GEMM_ZGRAD)
@@ -233,7 +309,10 @@ hipError_t gemm_launch(GemmBatch &b, const int *gate, hipStream_t s, int phase) 
     LST_GEMM_CASE(GEMM_NAIVE_UPDATE)
 #undef LST_GEMM_CASE
     default:
-      hipLaunchKernelGGL(gemm_kernel<GEMM_OTHER>, dim3(total), dim3(kThreads), 0, s, b, gate);
+      if (wide)
+        launch_phase<GEMM_OTHER, 8>(total, s, b, gate);
+      else
+        launch_phase<GEMM_OTHER, 4>(total, s, b, gate);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;

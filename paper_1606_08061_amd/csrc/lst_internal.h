@@ -47,7 +47,7 @@ struct GemmDesc {
   int tile_begin;
 };
 
-constexpr int kMaxBatch = 6;
+constexpr int kMaxBatch = 4;
 
 struct GemmBatch {
   GemmDesc d[kMaxBatch];
@@ -88,10 +88,14 @@ hipError_t launch_gather(hipStream_t s, int m, int K, int d, int64_t D, const fl
                          const float *V, int64_t ldv, int loss, float eps, float lr, float *G,
                          float *Atil, float *dq, float *dA, float *lvec, int *flag);
 
-hipError_t launch_small(hipStream_t s, int m, int K, float lr, const int *idx, const float *lvec,
-                        const float *dq, const float *dA, const float *N, const float *Mhat,
-                        const float *HZ, float *M, float *R, float *Cwork, int *srow,
-                        int *sslot, int *nvalid, float *loss_out, int *flag);
+hipError_t launch_sort(hipStream_t s, int n, const int *idx, int *srow, int *sslot, int *nvalid);
+
+hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
+                           const float *N, float *R, float *Cwork, int *flag);
+
+hipError_t launch_mblock(hipStream_t s, int m, int K, const int *idx, const float *lvec,
+                         const float *dq, const float *dA, const float *Mhat, const float *HZ,
+                         float *M, float *loss_out, int *flag);
 
 hipError_t launch_scatter(hipStream_t s, int m, int K, int d, float lr, const int *srow,
                           const int *sslot, const int *nvalid, const float *dA, const float *P,

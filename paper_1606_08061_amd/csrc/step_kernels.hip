@@ -4,15 +4,18 @@
 //               gen-A-fact), q_j = h_j . H^_j (eq. qvec), the loss epilogue
 //               (l_j, dl/dq_j, dl/dA_kj) and G_j = sum_k dl/dA_kj V_{K_kj}
 //               (the V^T Yring of eq. gen-Zhat-fact; Algorithm 3 step 2's V^T Y
-//               up to the factor -2).  One wavefront per example.
-//   small    -- the m x m block: L = sum_j l_j, M of eq. gen-M (with the sparse
-//               Yring^T Yring by index equality), the Woodbury matrix
-//               C = I - 2 eta S H^T H S and its inverse (Gauss-Jordan, no
-//               pivoting: C is symmetric positive definite exactly when the
-//               step is admissible), R = 2 eta S C^{-1} S, and the sort of the
-//               (row, slot) keys that makes the V scatter conflict free.
+//               up to the factor -2).
+//   sort     -- (row, slot) keys of the targets sorted, so that the slots of
+//               each V row are contiguous and in a fixed order.
+//   woodbury -- the m x m Woodbury matrix C = I - 2 eta S H^T H S and its
+//               inverse (Gauss-Jordan without pivoting: C is symmetric positive
+//               definite exactly when the step is admissible), giving
+//               R = 2 eta S C^{-1} S for the U^{-T} update (Algorithm 3 step 6,
+//               the Woodbury form of section 4.7).
+//   mblock   -- L = sum_j l_j and the Q-update matrix M of eq. gen-M, with the
+//               sparse Yring^T Yring by index equality.
 //   scatter  -- eq. updateV / gen-updateV: V_r -= eta sum_{slots of row r}
-//               dl/dA P_j, one wavefront per distinct row, slots in a fixed
+//               dl/dA P_j, one workgroup per distinct row, slots in a fixed
 //               order, so repeated rows never race and results are
 //               reproducible bit for bit.
 //   naive    -- column norms of O, the loss epilogue over the explicit output
@@ -64,65 +67,76 @@ __device__ __forceinline__ void loss_epilogue(int loss, float q, int K, const in
   }
 }
 
-__global__ __launch_bounds__(64) void gather_kernel(int K, int d, int64_t D, const float *__restrict__ H,
-                                                    const float *__restrict__ Hhat,
-                                                    const float *__restrict__ Htil,
-                                                    const int *__restrict__ idx,
-                                                    const float *__restrict__ val,
-                                                    const float *__restrict__ V, int64_t ldv, int loss,
-                                                    float eps, float lr, float *__restrict__ G,
-                                                    float *__restrict__ Atil, float *__restrict__ dq,
-                                                    float *__restrict__ dA, float *__restrict__ lvec,
-                                                    int *__restrict__ flag) {
+constexpr int kGatherThreads = 256;
+
+// One workgroup (four wavefronts) per example j.  The K row dot products
+// A_kj = H~_j . V_r are spread over the wavefronts, and G_j = sum_k dl/dA_kj V_r
+// is formed column-parallel, so the loads of the K target rows are in flight
+// together rather than one row after another.
+__global__ __launch_bounds__(kGatherThreads) void gather_kernel(
+    int K, int d, int64_t D, const float *__restrict__ H, const float *__restrict__ Hhat,
+    const float *__restrict__ Htil, const int *__restrict__ idx, const float *__restrict__ val,
+    const float *__restrict__ V, int64_t ldv, int loss, float eps, float lr, float *__restrict__ G,
+    float *__restrict__ Atil, float *__restrict__ dq, float *__restrict__ dA,
+    float *__restrict__ lvec, int *__restrict__ flag) {
   __shared__ int sr[LST_MAX_K];
   __shared__ float sa[LST_MAX_K], st[LST_MAX_K], sg[LST_MAX_K];
+  __shared__ float sred[kGatherThreads / 64];
+  __shared__ float s_gq;
+  __shared__ int s_bad;
   const int j = blockIdx.x;
-  const int lane = threadIdx.x;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const float *h = H + (int64_t)j * d;
   const float *hh = Hhat + (int64_t)j * d;
   const float *ht = Htil + (int64_t)j * d;
 
-  float qs = 0.f;
-  for (int c = lane; c < d; c += 64) qs += h[c] * hh[c];
-  const float q = wave_sum(qs);
-
-  int bad = 0;
-  for (int k = 0; k < K; ++k) {
+  if (t == 0) s_bad = 0;
+  __syncthreads();
+  for (int k = t; k < K; k += kGatherThreads) {
     int r = idx[(int64_t)j * K + k];
     if (r < -1 || (int64_t)r >= D) {
-      bad = 1;
+      atomicOr(&s_bad, 1);
       r = -1;
     }
+    sr[k] = r;
+    st[k] = val[(int64_t)j * K + k];
+  }
+  float qs = 0.f;
+  for (int c = t; c < d; c += kGatherThreads) qs += h[c] * hh[c];
+  qs = wave_sum(qs);
+  if (lane == 0) sred[wave] = qs;
+  __syncthreads();
+  const float q = (sred[0] + sred[1]) + (sred[2] + sred[3]);
+  if (t == 0 && s_bad) atomicOr(flag, FLAG_INDEX);
+
+  for (int k = wave; k < K; k += kGatherThreads / 64) {
+    const int r = sr[k];
     float a = 0.f;
     if (r >= 0) {
       const float *vr = V + (int64_t)r * ldv;
       float s = 0.f;
+#pragma unroll 8
       for (int c = lane; c < d; c += 64) s += ht[c] * vr[c];
       a = wave_sum(s);
     }
-    if (lane == 0) {
-      sr[k] = r;
-      sa[k] = a;
-      st[k] = val[(int64_t)j * K + k];
-    }
+    if (lane == 0) sa[k] = a;
   }
-  if (bad && lane == 0) atomicOr(flag, FLAG_INDEX);
   __syncthreads();
 
-  float l, gq;
-  if (lane == 0) {
+  if (t == 0) {
+    float l, gq;
     loss_epilogue(loss, q, K, sr, st, sa, (float)D * eps, eps, l, gq, sg);
     dq[j] = gq;
     lvec[j] = l;
-    sa[0] = gq;  // broadcast dl/dq (sa no longer needed)
+    s_gq = gq;
   }
   __syncthreads();
-  gq = sa[0];
-  for (int k = lane; k < K; k += 64) dA[(int64_t)j * K + k] = sg[k];
+  for (int k = t; k < K; k += kGatherThreads) dA[(int64_t)j * K + k] = sg[k];
 
-  const float s2 = 2.f * lr * gq;
-  for (int c = lane; c < d; c += 64) {
+  const float s2 = 2.f * lr * s_gq;
+  for (int c = t; c < d; c += kGatherThreads) {
     float s = 0.f;
+#pragma unroll 4
     for (int k = 0; k < K; ++k) {
       const int r = sr[k];
       if (r >= 0) s += sg[k] * V[(int64_t)r * ldv + c];
@@ -132,7 +146,6 @@ __global__ __launch_bounds__(64) void gather_kernel(int K, int d, int64_t D, con
   }
 }
 
-constexpr int kSmallThreads = 1024;
 constexpr int kMaxSortKeys = 8192;
 
 // Bitonic sort of n (power of two) 64-bit keys in LDS, ascending.
@@ -154,51 +167,133 @@ __device__ void bitonic_sort(unsigned long long *key, int n) {
   }
 }
 
-// Gauss-Jordan inversion in place, matrix held in registers: thread (ti, tj)
-// of a 32 x 32 grid owns the B x B block at rows ti*B.., cols tj*B...  Entries
-// outside m x m are the identity and take no part.  Returns false (uniformly)
-// if a pivot is not positive and finite.
-template <int B>
-__device__ bool gj_invert_regs(float (&a)[B][B], int m, float *srow, float *scol) {
+// Sorted (row, slot) keys of the valid target slots: the slots of one V row
+// become contiguous, in ascending slot order, for the conflict-free scatter.
+constexpr int kSortThreads = 1024;
+
+__global__ __launch_bounds__(kSortThreads) void sort_kernel(int n, const int *__restrict__ idx,
+                                                           int *__restrict__ srow_out,
+                                                           int *__restrict__ sslot_out,
+                                                           int *__restrict__ nvalid) {
+  __shared__ unsigned long long skey[kMaxSortKeys];
+  __shared__ int s_cnt;
   const int t = threadIdx.x;
-  const int ti = t >> 5, tj = t & 31;
-  for (int k = 0; k < m; ++k) {
-    float *rowk = srow + (k & 1) * (32 * B);
-    float *colk = scol + (k & 1) * (32 * B);
-    const int kb = k / B, kr = k - kb * B;
-    if (ti == kb) {
-#pragma unroll
-      for (int c = 0; c < B; ++c) rowk[tj * B + c] = a[kr][c];
+  int np = 1;
+  while (np < n) np <<= 1;
+  if (t == 0) s_cnt = 0;
+  for (int e = t; e < np; e += kSortThreads) {
+    unsigned long long key = ~0ull;
+    if (e < n) {
+      const int r = idx[e];
+      if (r >= 0) key = ((unsigned long long)(unsigned)r << 32) | (unsigned)e;
     }
-    if (tj == kb) {
-#pragma unroll
-      for (int r = 0; r < B; ++r) colk[ti * B + r] = a[r][kr];
-    }
-    __syncthreads();
-    const float p = rowk[k];
-    if (!(p > 0.f) || !isfinite(p)) return false;
-    const float ip = 1.f / p;
-    float cr[B], rc[B];
-#pragma unroll
-    for (int r = 0; r < B; ++r) cr[r] = colk[ti * B + r];
-#pragma unroll
-    for (int c = 0; c < B; ++c) rc[c] = rowk[tj * B + c];
-#pragma unroll
-    for (int r = 0; r < B; ++r) {
-      const int i = ti * B + r;
-#pragma unroll
-      for (int c = 0; c < B; ++c) {
-        const int j = tj * B + c;
-        if (i == k) {
-          a[r][c] = (j == k) ? ip : rc[c] * ip;
-        } else if (j == k) {
-          a[r][c] = -cr[r] * ip;
-        } else {
-          a[r][c] -= cr[r] * (rc[c] * ip);
-        }
-      }
+    skey[e] = key;
+  }
+  __syncthreads();
+  bitonic_sort(skey, np);
+  int cnt = 0;
+  for (int e = t; e < n; e += kSortThreads) {
+    const unsigned long long key = skey[e];
+    if (key != ~0ull) {
+      srow_out[e] = (int)(key >> 32);
+      sslot_out[e] = (int)(key & 0xffffffffu);
+      ++cnt;
     }
   }
+  if (cnt) atomicAdd(&s_cnt, cnt);
+  __syncthreads();
+  if (t == 0) *nvalid = s_cnt;
+}
+
+// Gauss-Jordan inversion in place, matrix held in registers: thread (ti, tj)
+// of a T x T grid owns the B x B block at rows ti*B.., cols tj*B...  Entries
+// outside m x m are the identity and take no part.  Returns false (uniformly)
+// if a pivot is not positive and finite.
+//
+// One elimination step on pivot k (p = A_kk) is written as
+//   A' = X - f g^T,  X = A with column k replaced by e_k,
+//   f_i = A_ik (i != k), f_k = p - 1,   g_j = A_kj / p (j != k), g_k = 1 / p,
+// which gives A'_kj = A_kj / p, A'_ik = -A_ik / p, A'_kk = 1 / p and
+// A'_ij = A_ij - A_ik A_kj / p elsewhere.  The pivot's position inside a block
+// (KR) is a compile-time index of the unrolled inner loop, so the register
+// block is never indexed at run time.  Lookahead: right after reading pivot k,
+// the owners of row and column k+1 compute their updated values and publish
+// them, so the one barrier per pivot waits only for the bulk of the update.
+template <int B, int KR>
+__device__ __forceinline__ float gj_new(const float (&a)[B][B], int r, int c, bool own_row,
+                                        bool own_col, const float (&f)[B], const float (&g)[B]) {
+  float x = a[r][c];
+  if (c == KR) x = own_col ? ((r == KR && own_row) ? 1.f : 0.f) : x;
+  return x - f[r] * g[c];
+}
+
+template <int T, int B, int KR>
+__device__ __forceinline__ bool gj_step(float (&a)[B][B], int kb, int m, float *srow, float *scol) {
+  const int t = threadIdx.x;
+  const int ti = t / T, tj = t % T;
+  const int k = kb * B + KR;
+  const float *rowk = srow + (k & 1) * (T * B);
+  const float *colk = scol + (k & 1) * (T * B);
+  __syncthreads();
+  const float p = rowk[k];
+  if (!(p > 0.f) || !isfinite(p)) return false;
+  const float ip = 1.f / p;
+  const bool own_row = (ti == kb), own_col = (tj == kb);
+  float f[B], g[B];
+#pragma unroll
+  for (int r = 0; r < B; ++r) f[r] = colk[ti * B + r];
+#pragma unroll
+  for (int c = 0; c < B; ++c) g[c] = rowk[tj * B + c] * ip;
+  if (own_row) f[KR] = p - 1.f;
+  if (own_col) g[KR] = ip;
+  if (k + 1 < m) {
+    constexpr int KR1 = (KR + 1 < B) ? KR + 1 : 0;
+    const int kb1 = (KR + 1 < B) ? kb : kb + 1;
+    float *rown = srow + ((k + 1) & 1) * (T * B);
+    float *coln = scol + ((k + 1) & 1) * (T * B);
+    if (ti == kb1) {
+#pragma unroll
+      for (int c = 0; c < B; ++c) rown[tj * B + c] = gj_new<B, KR>(a, KR1, c, own_row, own_col, f, g);
+    }
+    if (tj == kb1) {
+#pragma unroll
+      for (int r = 0; r < B; ++r) coln[ti * B + r] = gj_new<B, KR>(a, r, KR1, own_row, own_col, f, g);
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < B; ++r)
+#pragma unroll
+    for (int c = 0; c < B; ++c) a[r][c] = gj_new<B, KR>(a, r, c, own_row, own_col, f, g);
+  return true;
+}
+
+template <int T, int B, int KR>
+__device__ __forceinline__ bool gj_block(float (&a)[B][B], int kb, int m, float *srow, float *scol) {
+  if constexpr (KR < B) {
+    if (kb * B + KR >= m) return true;
+    if (!gj_step<T, B, KR>(a, kb, m, srow, scol)) return false;
+    return gj_block<T, B, KR + 1>(a, kb, m, srow, scol);
+  } else {
+    return true;
+  }
+}
+
+template <int T, int B>
+__device__ bool gj_invert_regs(float (&a)[B][B], int m, float *srow, float *scol) {
+  // publish pivot 0
+  const int t = threadIdx.x;
+  const int ti = t / T, tj = t % T;
+  if (ti == 0) {
+#pragma unroll
+    for (int c = 0; c < B; ++c) srow[tj * B + c] = a[0][c];
+  }
+  if (tj == 0) {
+#pragma unroll
+    for (int r = 0; r < B; ++r) scol[ti * B + r] = a[r][0];
+  }
+  const int nb = (m + B - 1) / B;
+  for (int kb = 0; kb < nb; ++kb)
+    if (!gj_block<T, B, 0>(a, kb, m, srow, scol)) return false;
   return true;
 }
 
@@ -229,151 +324,183 @@ __device__ bool gj_invert_global(float *A, int m, float *srow, float *scol) {
   return true;
 }
 
-// Entry (i, j) of M (eq. gen-M, dl/ds = 0):
-//   4 dq_i M^_ij dq_j + Yring^T Yring_ij + 2 dq_i (H~^T G)_ij + 2 dq_j (H~^T G)_ji
-__device__ __forceinline__ float m_entry(int i, int j, int m, int K, const int *idx,
-                                         const float *dq, const float *dA, const float *Mhat,
-                                         const float *HZ) {
-  float yy = 0.f;
-  for (int k = 0; k < K; ++k) {
-    const int ri = idx[(int64_t)i * K + k];
-    if (ri < 0) continue;
-    const float gi = dA[(int64_t)i * K + k];
-    for (int kk = 0; kk < K; ++kk)
-      if (idx[(int64_t)j * K + kk] == ri) yy += gi * dA[(int64_t)j * K + kk];
-  }
-  return 4.f * dq[i] * Mhat[(int64_t)i * m + j] * dq[j] + yy +
-         2.f * dq[i] * HZ[(int64_t)i * m + j] + 2.f * dq[j] * HZ[(int64_t)j * m + i];
-}
-
-template <int B>
-__global__ __launch_bounds__(kSmallThreads) void small_kernel(
-    int m, int K, float lr, const int *__restrict__ idx, const float *__restrict__ lvec,
-    const float *__restrict__ dq, const float *__restrict__ dA, const float *__restrict__ N,
-    const float *__restrict__ Mhat, const float *__restrict__ HZ, float *__restrict__ M,
-    float *__restrict__ R, float *__restrict__ Cwork, int *__restrict__ srow_out,
-    int *__restrict__ sslot_out, int *__restrict__ nvalid, float *__restrict__ loss_out,
-    int *__restrict__ flag) {
-  __shared__ unsigned long long skey[kMaxSortKeys];
-  __shared__ float red[kSmallThreads];
-  __shared__ int s_abort;
+// Woodbury matrix C = I - 2 eta S N S with S = diag(dl/dq)^{1/2} and N = H^T H,
+// its inverse, and R = 2 eta S C^{-1} S (U_new^{-T} = U^{-T} + (U^{-T} H) R H^T).
+// unit_dq: dl/dq = 1 for every example (squared error), dq is not read.
+template <int T, int B>
+__global__ __launch_bounds__(T *T) void woodbury_kernel(int m, float lr, int unit_dq,
+                                                       const float *__restrict__ dq,
+                                                       const float *__restrict__ N,
+                                                       float *__restrict__ R, float *__restrict__ Cwork,
+                                                       int *__restrict__ flag) {
+  __shared__ float sbuf[4096];
+  __shared__ float sq[LST_MAX_M];
+  __shared__ int s_bad;
   const int t = threadIdx.x;
-
-  // Loss: fixed-order sum of the per-example losses; dl/dq must be >= 0.
-  float ls = 0.f;
-  int neg = 0;
-  for (int j = t; j < m; j += kSmallThreads) {
-    ls += lvec[j];
-    if (!(dq[j] >= 0.f)) neg = 1;
-  }
-  red[t] = ls;
-  if (t == 0) s_abort = *flag;
+  if (t == 0) s_bad = 0;
   __syncthreads();
-  if (neg) atomicOr(&s_abort, FLAG_NOT_SPD);
-  for (int s = kSmallThreads / 2; s > 0; s >>= 1) {
-    if (t < s) red[t] += red[t + s];
-    __syncthreads();
-  }
-  if (t == 0) {
-    const float L = red[0];
-    *loss_out = L;
-    if (!isfinite(L)) s_abort |= FLAG_NONFINITE;
-    if (s_abort) atomicOr(flag, s_abort);
+  for (int i = t; i < m; i += T * T) {
+    const float v = unit_dq ? 1.f : dq[i];
+    if (!(v >= 0.f)) atomicOr(&s_bad, 1);  // negative or NaN dl/dq: no real square root
+    sq[i] = sqrtf(fmaxf(v, 0.f));
   }
   __syncthreads();
-  if (s_abort) return;
-
-  // Sort (row, slot) keys of the valid target slots.
-  const int n = m * K;
-  int np = 1;
-  while (np < n) np <<= 1;
-  for (int e = t; e < np; e += kSmallThreads) {
-    unsigned long long key = ~0ull;
-    if (e < n) {
-      const int r = idx[e];
-      if (r >= 0) key = ((unsigned long long)(unsigned)r << 32) | (unsigned)e;
-    }
-    skey[e] = key;
+  if (s_bad) {
+    if (t == 0) atomicOr(flag, FLAG_NOT_SPD);
+    return;
   }
-  __syncthreads();
-  bitonic_sort(skey, np);
-  int cnt = 0;
-  for (int e = t; e < n; e += kSmallThreads) {
-    const unsigned long long key = skey[e];
-    if (key != ~0ull) {
-      srow_out[e] = (int)(key >> 32);
-      sslot_out[e] = (int)(key & 0xffffffffu);
-      ++cnt;
-    }
-  }
-  red[t] = (float)cnt;
-  __syncthreads();
-  for (int s = kSmallThreads / 2; s > 0; s >>= 1) {
-    if (t < s) red[t] += red[t + s];
-    __syncthreads();
-  }
-  if (t == 0) *nvalid = (int)red[0];
-
-  // M (for the Q update) over all m x m entries.
-  for (int e = t; e < m * m; e += kSmallThreads) {
-    const int i = e / m, j = e - i * m;
-    M[e] = m_entry(i, j, m, K, idx, dq, dA, Mhat, HZ);
-  }
-
-  // C = I - 2 eta S N S, inverted in place; R = 2 eta S C^{-1} S.
-  float *srow = reinterpret_cast<float *>(skey);
-  float *scol = srow + 2048;
   bool ok;
   if constexpr (B > 0) {
     float a[B][B];
-    const int ti = t >> 5, tj = t & 31;
+    const int ti = t / T, tj = t % T;
 #pragma unroll
     for (int r = 0; r < B; ++r)
 #pragma unroll
       for (int c = 0; c < B; ++c) {
         const int i = ti * B + r, j = tj * B + c;
         float v = (i == j) ? 1.f : 0.f;
-        if (i < m && j < m)
-          v -= 2.f * lr * sqrtf(dq[i]) * N[(int64_t)i * m + j] * sqrtf(dq[j]);
+        if (i < m && j < m) v -= 2.f * lr * sq[i] * N[(int64_t)i * m + j] * sq[j];
         a[r][c] = v;
       }
-    __syncthreads();  // skey reuse as srow/scol
-    ok = gj_invert_regs<B>(a, m, srow, scol);
+    ok = gj_invert_regs<T, B>(a, m, sbuf, sbuf + 2048);
     if (ok) {
 #pragma unroll
       for (int r = 0; r < B; ++r)
 #pragma unroll
         for (int c = 0; c < B; ++c) {
           const int i = ti * B + r, j = tj * B + c;
-          if (i < m && j < m) R[(int64_t)i * m + j] = 2.f * lr * sqrtf(dq[i]) * a[r][c] * sqrtf(dq[j]);
+          if (i < m && j < m) R[(int64_t)i * m + j] = 2.f * lr * sq[i] * a[r][c] * sq[j];
         }
     }
   } else {
-    for (int e = t; e < m * m; e += kSmallThreads) {
+    for (int e = t; e < m * m; e += T * T) {
       const int i = e / m, j = e - i * m;
-      Cwork[e] = ((i == j) ? 1.f : 0.f) - 2.f * lr * sqrtf(dq[i]) * N[e] * sqrtf(dq[j]);
+      Cwork[e] = ((i == j) ? 1.f : 0.f) - 2.f * lr * sq[i] * N[e] * sq[j];
     }
     __syncthreads();
-    ok = gj_invert_global(Cwork, m, srow, scol);
+    ok = gj_invert_global(Cwork, m, sbuf, sbuf + 2048);
     if (ok) {
-      for (int e = t; e < m * m; e += kSmallThreads) {
+      for (int e = t; e < m * m; e += T * T) {
         const int i = e / m, j = e - i * m;
-        R[e] = 2.f * lr * sqrtf(dq[i]) * Cwork[e] * sqrtf(dq[j]);
+        R[e] = 2.f * lr * sq[i] * Cwork[e] * sq[j];
       }
     }
   }
   if (!ok && t == 0) atomicOr(flag, FLAG_NOT_SPD);
 }
 
-__global__ __launch_bounds__(256) void scatter_kernel(int K, int d, float lr, const int *__restrict__ srow,
-                                                      const int *__restrict__ sslot,
-                                                      const int *__restrict__ nvalid,
-                                                      const float *__restrict__ dA,
-                                                      const float *__restrict__ P, float *__restrict__ V,
-                                                      int64_t ldv, const int *__restrict__ gate) {
+// Loss L = sum_j l_j (fixed order; non-finite -> error flag) and the Q-update
+// matrix M of eq. gen-M (dl/ds = 0):
+//   M_ij = 4 dq_i M^_ij dq_j + (Yring^T Yring)_ij + 2 dq_i (H~^T G)_ij + 2 dq_j (H~^T G)_ji
+// Column j of the sparse Yring is kept as a sorted list of (row, value) pairs,
+// so (Yring^T Yring)_ij is a merge of two lists in ascending row order.  Each
+// workgroup builds the m lists in LDS and fills kMblockThreads entries of M;
+// workgroup 0 also forms the loss.
+constexpr int kMblockThreads = 256;
+
+__global__ __launch_bounds__(kMblockThreads) void mblock_kernel(
+    int m, int K, const int *__restrict__ idx, const float *__restrict__ lvec,
+    const float *__restrict__ dq, const float *__restrict__ dA, const float *__restrict__ Mhat,
+    const float *__restrict__ HZ, float *__restrict__ M, float *__restrict__ loss_out,
+    int *__restrict__ flag) {
+  __shared__ int lrow[kMaxSortKeys];
+  __shared__ float lval[kMaxSortKeys];
+  __shared__ int lcnt[LST_MAX_M];
+  __shared__ float red[kMblockThreads];
+  const int t = threadIdx.x;
+  const int e = blockIdx.x * kMblockThreads + t;
+
+  // Prefetch this thread's dense terms before building the lists.
+  const bool has = e < m * m;
+  const int i = has ? e / m : 0, j = has ? e - (e / m) * m : 0;
+  float mh = 0.f, hz = 0.f, hzt = 0.f, di = 0.f, dj = 0.f;
+  if (has) {
+    mh = Mhat[e];
+    hz = HZ[e];
+    hzt = HZ[(int64_t)j * m + i];
+    di = dq[i];
+    dj = dq[j];
+  }
+
+  if (blockIdx.x == 0) {
+    float ls = 0.f;
+    for (int q = t; q < m; q += kMblockThreads) ls += lvec[q];
+    red[t] = ls;
+    __syncthreads();
+    for (int s = kMblockThreads / 2; s > 0; s >>= 1) {
+      if (t < s) red[t] += red[t + s];
+      __syncthreads();
+    }
+    if (t == 0) {
+      const float L = red[0];
+      *loss_out = L;
+      if (!isfinite(L)) atomicOr(flag, FLAG_NONFINITE);
+    }
+  }
+
+  for (int q = t; q < m; q += kMblockThreads) {
+    int *lr = lrow + q * K;
+    float *lv = lval + q * K;
+    int c = 0;
+    for (int k = 0; k < K; ++k) {
+      const int r = idx[(int64_t)q * K + k];
+      if (r < 0) continue;
+      const float g = dA[(int64_t)q * K + k];
+      int p = c;
+      while (p > 0 && lr[p - 1] > r) {
+        lr[p] = lr[p - 1];
+        lv[p] = lv[p - 1];
+        --p;
+      }
+      lr[p] = r;
+      lv[p] = g;
+      ++c;
+    }
+    int w = 0;
+    for (int u = 0; u < c; ++u) {
+      if (w > 0 && lr[w - 1] == lr[u]) {
+        lv[w - 1] += lv[u];
+      } else {
+        lr[w] = lr[u];
+        lv[w] = lv[u];
+        ++w;
+      }
+    }
+    lcnt[q] = w;
+  }
+  __syncthreads();
+  if (!has) return;
+
+  const int *ri = lrow + i * K, *rj = lrow + j * K;
+  const float *vi = lval + i * K, *vj = lval + j * K;
+  const int na = lcnt[i], nb = lcnt[j];
+  float yy = 0.f;
+  int a = 0, b = 0;
+  while (a < na && b < nb) {
+    const int ra = ri[a], rb = rj[b];
+    if (ra == rb) {
+      yy += vi[a] * vj[b];
+      ++a;
+      ++b;
+    } else if (ra < rb) {
+      ++a;
+    } else {
+      ++b;
+    }
+  }
+  M[e] = 4.f * di * mh * dj + yy + 2.f * di * hz + 2.f * dj * hzt;
+}
+
+constexpr int kScatterThreads = 256;
+
+// One workgroup per sorted slot position; only the first position of each
+// distinct row does work, over all the slots of that row, column-parallel.
+__global__ __launch_bounds__(kScatterThreads) void scatter_kernel(
+    int K, int d, float lr, const int *__restrict__ srow, const int *__restrict__ sslot,
+    const int *__restrict__ nvalid, const float *__restrict__ dA, const float *__restrict__ P,
+    float *__restrict__ V, int64_t ldv, const int *__restrict__ gate) {
   if (*gate != 0) return;
-  const int p = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
+  const int p = blockIdx.x;
   const int n = *nvalid;
   if (p >= n) return;
   const int r = srow[p];
@@ -381,8 +508,9 @@ __global__ __launch_bounds__(256) void scatter_kernel(int K, int d, float lr, co
   int e = p + 1;
   while (e < n && srow[e] == r) ++e;
   float *vr = V + (int64_t)r * ldv;
-  for (int c = lane; c < d; c += 64) {
+  for (int c = threadIdx.x; c < d; c += kScatterThreads) {
     float acc = 0.f;
+#pragma unroll 4
     for (int s = p; s < e; ++s) {
       const int slot = sslot[s];
       acc += dA[slot] * P[(int64_t)(slot / K) * d + c];
@@ -494,30 +622,42 @@ hipError_t launch_gather(hipStream_t s, int m, int K, int d, int64_t D, const fl
                          const float *Hhat, const float *Htil, const int *idx, const float *val,
                          const float *V, int64_t ldv, int loss, float eps, float lr, float *G,
                          float *Atil, float *dq, float *dA, float *lvec, int *flag) {
-  hipLaunchKernelGGL(gather_kernel, dim3(m), dim3(64), 0, s, K, d, D, H, Hhat, Htil, idx, val, V,
+  hipLaunchKernelGGL(gather_kernel, dim3(m), dim3(kGatherThreads), 0, s, K, d, D, H, Hhat, Htil, idx, val, V,
                      ldv, loss, eps, lr, G, Atil, dq, dA, lvec, flag);
   return hipGetLastError();
 }
 
-hipError_t launch_small(hipStream_t s, int m, int K, float lr, const int *idx, const float *lvec,
-                        const float *dq, const float *dA, const float *N, const float *Mhat,
-                        const float *HZ, float *M, float *R, float *Cwork, int *srow, int *sslot,
-                        int *nvalid, float *loss_out, int *flag) {
+hipError_t launch_sort(hipStream_t s, int n, const int *idx, int *srow, int *sslot, int *nvalid) {
+  hipLaunchKernelGGL(sort_kernel, dim3(1), dim3(kSortThreads), 0, s, n, idx, srow, sslot, nvalid);
+  return hipGetLastError();
+}
+
+hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
+                           const float *N, float *R, float *Cwork, int *flag) {
   if (m <= 32)
-    hipLaunchKernelGGL(small_kernel<1>, dim3(1), dim3(kSmallThreads), 0, s, m, K, lr, idx, lvec,
-                       dq, dA, N, Mhat, HZ, M, R, Cwork, srow, sslot, nvalid, loss_out, flag);
+    hipLaunchKernelGGL((woodbury_kernel<16, 2>), dim3(1), dim3(256), 0, s, m, lr, unit_dq, dq, N, R,
+                       Cwork, flag);
   else if (m <= 64)
-    hipLaunchKernelGGL(small_kernel<2>, dim3(1), dim3(kSmallThreads), 0, s, m, K, lr, idx, lvec,
-                       dq, dA, N, Mhat, HZ, M, R, Cwork, srow, sslot, nvalid, loss_out, flag);
+    hipLaunchKernelGGL((woodbury_kernel<16, 4>), dim3(1), dim3(256), 0, s, m, lr, unit_dq, dq, N, R,
+                       Cwork, flag);
   else if (m <= 128)
-    hipLaunchKernelGGL(small_kernel<4>, dim3(1), dim3(kSmallThreads), 0, s, m, K, lr, idx, lvec,
-                       dq, dA, N, Mhat, HZ, M, R, Cwork, srow, sslot, nvalid, loss_out, flag);
+    hipLaunchKernelGGL((woodbury_kernel<32, 4>), dim3(1), dim3(1024), 0, s, m, lr, unit_dq, dq, N,
+                       R, Cwork, flag);
   else if (m <= 256)
-    hipLaunchKernelGGL(small_kernel<8>, dim3(1), dim3(kSmallThreads), 0, s, m, K, lr, idx, lvec,
-                       dq, dA, N, Mhat, HZ, M, R, Cwork, srow, sslot, nvalid, loss_out, flag);
+    hipLaunchKernelGGL((woodbury_kernel<32, 8>), dim3(1), dim3(1024), 0, s, m, lr, unit_dq, dq, N,
+                       R, Cwork, flag);
   else
-    hipLaunchKernelGGL(small_kernel<0>, dim3(1), dim3(kSmallThreads), 0, s, m, K, lr, idx, lvec,
-                       dq, dA, N, Mhat, HZ, M, R, Cwork, srow, sslot, nvalid, loss_out, flag);
+    hipLaunchKernelGGL((woodbury_kernel<32, 0>), dim3(1), dim3(1024), 0, s, m, lr, unit_dq, dq, N,
+                       R, Cwork, flag);
+  return hipGetLastError();
+}
+
+hipError_t launch_mblock(hipStream_t s, int m, int K, const int *idx, const float *lvec,
+                         const float *dq, const float *dA, const float *Mhat, const float *HZ,
+                         float *M, float *loss_out, int *flag) {
+  const int blocks = (m * m + kMblockThreads - 1) / kMblockThreads;
+  hipLaunchKernelGGL(mblock_kernel, dim3(blocks), dim3(kMblockThreads), 0, s, m, K, idx, lvec, dq,
+                     dA, Mhat, HZ, M, loss_out, flag);
   return hipGetLastError();
 }
 
@@ -526,7 +666,7 @@ hipError_t launch_scatter(hipStream_t s, int m, int K, int d, float lr, const in
                           float *V, int64_t ldv, const int *flag) {
   const int n = m * K;
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(scatter_kernel, dim3((n + 3) / 4), dim3(256), 0, s, K, d, lr, srow, sslot,
+  hipLaunchKernelGGL(scatter_kernel, dim3(n), dim3(kScatterThreads), 0, s, K, d, lr, srow, sslot,
                      nvalid, dA, P, V, ldv, flag);
   return hipGetLastError();
 }

@@ -182,3 +182,34 @@ def test_untouched_rows_bit_identical_and_deterministic():
         f.close()
     for a, b in zip(*outs):
         assert torch.equal(a, b)
+
+
+@pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX])
+def test_graph_replay_matches_eager(loss):
+    # Each step's arguments recur every third step, so the cached graphs are replayed several
+    # times, with eager torch work and host synchronisations between the replays; every replay
+    # must give bit-identical results to kernel-by-kernel enqueueing.
+    w = Workload("t", loss, 5000, 64, 32, 3, value_dist="normal" if loss == LOSS_SQUARED else "ones")
+    s = Stream(w)
+    batches = [to_dev(*s.batch()) for _ in range(3)]
+    outs = []
+    for graphs in (False, True):
+        f = make_factored(w, s.V0)
+        f.use_graphs(graphs)
+        loss_buf = torch.zeros((), device=DEV)
+        grad_buf = torch.empty((w.m, w.d), device=DEV)
+        losses, grads = [], []
+        for t in range(9):
+            f.step(*batches[t % 3], w.lr, grad_H=grad_buf, loss_out=loss_buf)
+            losses.append(loss_buf.item())
+            grads.append(grad_buf.clone())
+            assert torch.ones(7, device=DEV).sum().item() == 7.0
+        f.check()
+        outs.append((losses, grads, [t.clone() for t in (f.V, f.U, f.UinvT, f.Q)]))
+        f.close()
+    (l0, g0, s0), (l1, g1, s1) = outs
+    assert l0 == l1
+    for a, b in zip(g0, g1):
+        assert torch.equal(a, b)
+    for a, b in zip(s0, s1):
+        assert torch.equal(a, b)
