@@ -31,14 +31,14 @@ def phase_work(w, idx_pool):
     m, d, K = w.m, w.d, w.K
     uniq = float(np.mean([len(np.unique(i[i >= 0])) for i in idx_pool]))
     return {
-        # MACs x 2: H^, H~, X = {Q,U,U^-T} H and H^T H
-        "contract": ("mfma", 2.0 * (3 * m * d * d + m * m * d), "flop"),
+        # MACs x 2: H^, H~, X = {Q,U,U^-T} H
+        "contract": ("mfma", 2.0 * 3 * m * d * d, "flop"),
         # V rows of the targets, H, H^, H~ read; G and the scaled H~ written
         "gather": ("hbm", 4.0 * (m * K * d + 5 * m * d), "byte"),
         # Z^ = U^T G, H^T H^, H~^T G
         "zgrad": ("mfma", 2.0 * (m * d * d + 2 * m * m * d), "flop"),
-        # Gauss-Jordan inverse of the m x m Woodbury matrix (m^3 multiply-adds)
-        "woodbury": ("alu", 2.0 * m ** 3, "flop"),
+        # N = H^T H (2 m^2 d) and the Gauss-Jordan inverse of the m x m Woodbury matrix (m^3 FMA)
+        "woodbury": ("alu", 2.0 * m * m * d + 2.0 * m ** 3, "flop"),
         # loss sum and the m x m entries of M
         "mblock": ("alu", 8.0 * m * m, "flop"),
         # bitonic sort of the m*K (row, slot) keys: n log2(n)^2 / 2 compare-exchanges
