@@ -41,8 +41,6 @@ def phase_work(w, idx_pool):
         "woodbury": ("alu", 2.0 * m * m * d + 2.0 * m ** 3, "flop"),
         # loss sum and the m x m entries of M
         "mblock": ("alu", 8.0 * m * m, "flop"),
-        # bitonic sort of the m*K (row, slot) keys: n log2(n)^2 / 2 compare-exchanges
-        "sort": ("alu", 0.5 * (m * K) * max(np.log2(max(m * K, 2)), 1.0) ** 2, "flop"),
         # R X, M H, U update
         "mid": ("mfma", 2.0 * (m * d * d + 2 * m * m * d), "flop"),
         # U^-T update, Q update (two products), P

@@ -173,24 +173,23 @@ int lst_naive_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t
 int lst_naive_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val,
                    int32_t K, float lr, float *loss_dev, float *grad_H);
 
-/* Phases of a step, as timed by the profiling hook below.  The sort and the
-   Woodbury inverse run on side streams of the context, overlapping the main
-   chain; the other phases run in order on the context's stream. */
+/* Phases of a step, as timed by the profiling hook below.  The Woodbury inverse
+   runs on a side stream of the context, overlapping the main chain; the other
+   phases run in order on the context's stream. */
 enum lst_phase {
-  LST_PHASE_CONTRACT = 0,      /* H^ = Q H, H~ = U H, X = U^{-T} H, H^T H (matrix cores)  */
+  LST_PHASE_CONTRACT = 0,      /* H^ = Q H, H~ = U H, X = U^{-T} H (matrix cores)          */
   LST_PHASE_GATHER = 1,        /* gather of the K target rows of V, loss epilogue, G       */
   LST_PHASE_ZGRAD = 2,         /* Z^ = U^T G, grad_H, H^T H^, H~^T G (matrix cores)        */
-  LST_PHASE_MBLOCK = 3,        /* loss sum, M of the Q update (one workgroup)              */
-  LST_PHASE_WOODBURY = 4,      /* m x m Woodbury matrix and its inverse (one workgroup)    */
-  LST_PHASE_SORT = 5,          /* sort of the (row, slot) target keys (one workgroup)      */
-  LST_PHASE_MID = 6,           /* R X, (eta^2/2) M H - eta grad_H, U update (matrix cores) */
-  LST_PHASE_UPDATE = 7,        /* U^{-T} and Q updates, P = U_new^{-T} H (matrix cores)    */
-  LST_PHASE_SCATTER = 8,       /* conflict-free update of the target rows of V             */
-  LST_PHASE_NAIVE_FWD = 9,     /* naive: O = W H^T                                         */
-  LST_PHASE_NAIVE_LOSS = 10,   /* naive: column norms of O, loss, grad_O                   */
-  LST_PHASE_NAIVE_GRAD = 11,   /* naive: grad_H = grad_O^T W                               */
-  LST_PHASE_NAIVE_UPDATE = 12, /* naive: W <- W - eta grad_O H                             */
-  LST_NUM_PHASES = 13
+  LST_PHASE_MBLOCK = 3,        /* loss sum, M of the Q update                              */
+  LST_PHASE_WOODBURY = 4,      /* N = H^T H, the m x m Woodbury matrix and its inverse     */
+  LST_PHASE_MID = 5,           /* R X, (eta^2/2) M H - eta grad_H, U update (matrix cores) */
+  LST_PHASE_UPDATE = 6,        /* U^{-T} and Q updates, P = U_new^{-T} H (matrix cores)    */
+  LST_PHASE_SCATTER = 7,       /* conflict-free update of the target rows of V             */
+  LST_PHASE_NAIVE_FWD = 8,     /* naive: O = W H^T                                         */
+  LST_PHASE_NAIVE_LOSS = 9,    /* naive: column norms of O, loss, grad_O                   */
+  LST_PHASE_NAIVE_GRAD = 10,   /* naive: grad_H = grad_O^T W                               */
+  LST_PHASE_NAIVE_UPDATE = 11, /* naive: W <- W - eta grad_O H                             */
+  LST_NUM_PHASES = 12
 };
 
 /*

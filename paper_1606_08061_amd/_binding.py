@@ -51,7 +51,7 @@ SIGNATURES = {
     "lst_profile_read": (_I32, [_P, ctypes.POINTER(_I32), ctypes.POINTER(ctypes.c_double), _I32]),
 }
 
-PHASES = ["contract", "gather", "zgrad", "mblock", "woodbury", "sort", "mid", "update", "scatter",
+PHASES = ["contract", "gather", "zgrad", "mblock", "woodbury", "mid", "update", "scatter",
           "naive_fwd", "naive_loss", "naive_grad", "naive_update"]
 
 _lib = None
@@ -186,11 +186,17 @@ class _Ctx:
         self.loss_buf = torch.zeros((), dtype=torch.float32, device=self.device)
 
     def _batch(self, H, idx, val):
+        # one cheap combined check on the hot path; the detailed one only to report what failed
         m = H.shape[0]
-        K = idx.shape[1] if idx.dim() == 2 else 0
-        _need(H, torch.float32, (m, self.d), "H")
-        _need(idx, torch.int32, (m, K), "idx")
-        _need(val, torch.float32, (m, K), "val")
+        K = idx.shape[1] if idx.dim() == 2 else -1
+        if not (H.is_cuda and idx.is_cuda and val.is_cuda and H.dtype is torch.float32
+                and idx.dtype is torch.int32 and val.dtype is torch.float32
+                and H.dim() == 2 and H.shape[1] == self.d and idx.shape[0] == m
+                and val.shape == idx.shape and H.is_contiguous() and idx.is_contiguous()
+                and val.is_contiguous()):
+            _need(H, torch.float32, (m, self.d), "H")
+            _need(idx, torch.int32, (m, max(K, 0)), "idx")
+            _need(val, torch.float32, (m, max(K, 0)), "val")
         return m, K
 
     def sync_status(self) -> int:
@@ -234,6 +240,7 @@ class Factored(_Ctx):
                                   _ptr(self.V), self.d, _ptr(self.U), _ptr(self.UinvT),
                                   _ptr(self.Q), self.d, _stream_handle(self.stream))
         _check(st, "lst_create")
+        self._step_fn = lib().lst_step
 
     def init(self, V0=None, U0=None) -> None:
         if V0 is not None:
@@ -247,11 +254,14 @@ class Factored(_Ctx):
         m, K = self._batch(H, idx, val)
         if grad_H is None and want_grad:
             grad_H = torch.empty((m, self.d), dtype=torch.float32, device=self.device)
-        if grad_H is not None:
+        if grad_H is not None and not (grad_H.is_cuda and grad_H.dtype is torch.float32
+                                       and grad_H.shape == H.shape and grad_H.is_contiguous()):
             _need(grad_H, torch.float32, (m, self.d), "grad_H")
         loss_out = self.loss_buf if loss_out is None else loss_out
-        _check(lst_step(self.ctx, _ptr(H), m, _ptr(idx), _ptr(val), K, float(lr), _ptr(loss_out),
-                        _ptr(grad_H)), "lst_step")
+        st = self._step_fn(self.ctx, H.data_ptr(), m, idx.data_ptr(), val.data_ptr(), K, lr,
+                           loss_out.data_ptr(), 0 if grad_H is None else grad_H.data_ptr())
+        if st:
+            _check(st, "lst_step")
         return loss_out, grad_H
 
     def materialize_W(self, out=None):
@@ -275,6 +285,7 @@ class Naive(_Ctx):
                                         self.eps, _ptr(self.W), self.d,
                                         _stream_handle(self.stream))
         _check(st, "lst_naive_create")
+        self._step_fn = lib().lst_naive_step
 
     def init(self, W0) -> None:
         _need(W0, torch.float32, (self.D, self.d), "W0")
@@ -288,8 +299,8 @@ class Naive(_Ctx):
         if grad_H is not None:
             _need(grad_H, torch.float32, (m, self.d), "grad_H")
         loss_out = self.loss_buf if loss_out is None else loss_out
-        _check(lst_naive_step(self.ctx, _ptr(H), m, _ptr(idx), _ptr(val), K, float(lr),
-                              _ptr(loss_out), _ptr(grad_H)), "lst_naive_step")
+        _check(self._step_fn(self.ctx, _ptr(H), m, _ptr(idx), _ptr(val), K, float(lr),
+                             _ptr(loss_out), _ptr(grad_H)), "lst_naive_step")
         return loss_out, grad_H
 
     def materialize_W(self, out=None):

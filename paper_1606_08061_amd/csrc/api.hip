@@ -62,14 +62,14 @@ struct lst_ctx {
   float *Hhat, *Htil, *X, *G, *Atil, *Zhat, *gradH, *Yw, *Zq, *P;
   float *N, *Mhat, *HZ, *M, *R, *Cwork;
   float *dq, *lvec, *dA;
-  int *srow, *sslot, *nvalid, *flag;
+  int *flag;
   float *O, *colpart, *splitpart;
   hipError_t last_err;
-  // side streams of a factored step (sort; Woodbury inverse) and their fork/join events;
+  // side stream of a factored step (Woodbury inverse) and its fork/join events;
   // cap is the stream a step is captured on when it is recorded as a HIP graph
-  hipStream_t side[2];
+  hipStream_t side[1];
   hipStream_t cap;
-  hipEvent_t ev_fork, ev_wood_ready, ev_wood_done, ev_sort_done;
+  hipEvent_t ev_fork, ev_wood_ready, ev_wood_done;
   bool have_side;
   // tracing: event pairs per phase
   bool prof_on;
@@ -107,9 +107,6 @@ void carve_factored(lst_ctx *c, Carver &cv) {
   c->dq = cv.take<float>(c->m_max);
   c->lvec = cv.take<float>(c->m_max);
   c->dA = cv.take<float>(mk);
-  c->srow = cv.take<int>(mk);
-  c->sslot = cv.take<int>(mk);
-  c->nvalid = cv.take<int>(1);
   c->flag = cv.take<int>(1);
 }
 
@@ -193,10 +190,10 @@ void prof(lst_ctx *c, int phase, bool begin, hipStream_t st = nullptr) {
 }
 
 int side_create(lst_ctx *c) {
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 1; ++i)
     if (hipStreamCreateWithFlags(&c->side[i], hipStreamNonBlocking) != hipSuccess) return LST_E_HIP;
   if (hipStreamCreateWithFlags(&c->cap, hipStreamNonBlocking) != hipSuccess) return LST_E_HIP;
-  hipEvent_t *evs[4] = {&c->ev_fork, &c->ev_wood_ready, &c->ev_wood_done, &c->ev_sort_done};
+  hipEvent_t *evs[3] = {&c->ev_fork, &c->ev_wood_ready, &c->ev_wood_done};
   for (hipEvent_t *e : evs)
     if (hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) return LST_E_HIP;
   c->have_side = true;
@@ -205,12 +202,12 @@ int side_create(lst_ctx *c) {
 
 void side_free(lst_ctx *c) {
   if (!c->have_side) return;
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < 1; ++i)
     if (c->side[i]) (void)hipStreamDestroy(c->side[i]);
   if (c->cap) (void)hipStreamDestroy(c->cap);
   for (GraphEntry &g : c->graphs) (void)hipGraphExecDestroy(g.exec);
   c->graphs.clear();
-  hipEvent_t evs[4] = {c->ev_fork, c->ev_wood_ready, c->ev_wood_done, c->ev_sort_done};
+  hipEvent_t evs[3] = {c->ev_fork, c->ev_wood_ready, c->ev_wood_done};
   for (hipEvent_t e : evs)
     if (e) (void)hipEventDestroy(e);
   c->have_side = false;
@@ -352,7 +349,7 @@ void lst_destroy(lst_ctx *c) {
     (void)hipFree(c->ws);
   }
   if (c->have_side)
-    for (int i = 0; i < 2; ++i) (void)hipStreamSynchronize(c->side[i]);
+    for (int i = 0; i < 1; ++i) (void)hipStreamSynchronize(c->side[i]);
   side_free(c);
   prof_free(c);
   delete c;
@@ -388,7 +385,7 @@ int lst_sync_status(lst_ctx *c) {
   if (!c) return LST_E_ARG;
   if (hipStreamSynchronize(c->stream) != hipSuccess) return LST_E_HIP;
   if (c->have_side)
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 1; ++i)
       if (hipStreamSynchronize(c->side[i]) != hipSuccess) return LST_E_HIP;
   if (c->last_err != hipSuccess) {
     c->last_err = hipSuccess;
@@ -486,20 +483,19 @@ int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0
 namespace {
 
 // Enqueues one factored step on stream s (and the context's side streams).
+void gemm_run(GemmBatch &b, const int *gate, hipStream_t s, int phase = GEMM_OTHER) {
+  gemm_prepare(b);
+  gemm_enqueue(b, gate, s, phase);
+}
+
 int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, const int32_t *idx,
                           const float *val, int32_t K, float lr, float *loss_dev,
                           float *grad_H) {
   const int d = c->d, ldd = c->ldd;
   float *gH = grad_H ? grad_H : c->gradH;
 
-  hipStream_t s_wood = c->side[0], s_sort = c->side[1];
-  // Fork.  The sort of the target keys only needs idx.
-  if (record(c, hipEventRecord(c->ev_fork, s)) || record(c, hipStreamWaitEvent(s_sort, c->ev_fork, 0)))
-    return LST_E_HIP;
-  prof(c, LST_PHASE_SORT, true, s_sort);
-  if (record(c, launch_sort(s_sort, m * K, idx, c->srow, c->sslot, c->nvalid))) return LST_E_HIP;
-  prof(c, LST_PHASE_SORT, false, s_sort);
-  if (record(c, hipEventRecord(c->ev_sort_done, s_sort))) return LST_E_HIP;
+  hipStream_t s_wood = c->side[0];
+  if (record(c, hipEventRecord(c->ev_fork, s))) return LST_E_HIP;
 
   // Woodbury branch: N = H^T H, then C = I - 2 eta S N S and its inverse.  For
   // squared error dl/dq = 1 and the branch needs nothing else; the spherical
@@ -510,11 +506,9 @@ int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, 
   GemmBatch bn{};
   bn.d[0] = gemm_desc(m, m, d, H, d, 0, H, d, 0, c->N, m);
   bn.n = 1;
-  if (record(c, gemm_launch(bn, nullptr, s_wood))) return LST_E_HIP;
+  gemm_run(bn, nullptr, s_wood);
   auto woodbury = [&]() -> int {
-    if (record(c, launch_woodbury(s_wood, m, lr, unit_dq ? 1 : 0, c->dq, c->N, c->R, c->Cwork,
-                                  c->flag)))
-      return LST_E_HIP;
+    launch_woodbury(s_wood, m, lr, unit_dq ? 1 : 0, c->dq, c->N, c->R, c->Cwork, c->flag);
     prof(c, LST_PHASE_WOODBURY, false, s_wood);
     return record(c, hipEventRecord(c->ev_wood_done, s_wood));
   };
@@ -527,14 +521,13 @@ int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, 
   b1.d[2] = gemm_desc(m, d, d, H, d, 0, c->UinvT, ldd, 0, c->X, d);
   b1.n = 3;
   prof(c, LST_PHASE_CONTRACT, true);
-  if (record(c, gemm_launch(b1, nullptr, s, GEMM_CONTRACT))) return LST_E_HIP;
+  gemm_run(b1, nullptr, s, GEMM_CONTRACT);
   prof(c, LST_PHASE_CONTRACT, false);
 
   // Sparse gather of the K target rows of the pre-update V and the loss epilogue.
   prof(c, LST_PHASE_GATHER, true);
-  if (record(c, launch_gather(s, m, K, d, c->D, H, c->Hhat, c->Htil, idx, val, c->V, c->ldv,
-                              c->loss, c->eps, lr, c->G, c->Atil, c->dq, c->dA, c->lvec, c->flag)))
-    return LST_E_HIP;
+  launch_gather(s, m, K, d, c->D, H, c->Hhat, c->Htil, idx, val, c->V, c->ldv, c->loss, c->eps, lr,
+                c->G, c->Atil, c->dq, c->dA, c->lvec, c->flag);
   prof(c, LST_PHASE_GATHER, false);
   if (!unit_dq) {
     if (record(c, hipEventRecord(c->ev_wood_ready, s)) ||
@@ -556,14 +549,12 @@ int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, 
   b2.d[2] = gemm_desc(m, m, d, c->Htil, d, 0, c->G, d, 0, c->HZ, m);
   b2.n = 3;
   prof(c, LST_PHASE_ZGRAD, true);
-  if (record(c, gemm_launch(b2, nullptr, s, GEMM_ZGRAD))) return LST_E_HIP;
+  gemm_run(b2, nullptr, s, GEMM_ZGRAD);
   prof(c, LST_PHASE_ZGRAD, false);
 
   // Loss and M; sets the error flag on a non-finite loss.
   prof(c, LST_PHASE_MBLOCK, true);
-  if (record(c, launch_mblock(s, m, K, idx, c->lvec, c->dq, c->dA, c->Mhat, c->HZ, c->M, loss_dev,
-                              c->flag)))
-    return LST_E_HIP;
+  launch_mblock(s, m, K, idx, c->lvec, c->dq, c->dA, c->Mhat, c->HZ, c->M, loss_dev, c->flag);
   prof(c, LST_PHASE_MBLOCK, false);
 
   // Join the Woodbury branch before its result (and its error flag) is used.
@@ -577,7 +568,7 @@ int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, 
   b3.d[2] = gemm_desc(d, d, m, c->Atil, d, 1, H, d, 1, c->U, ldd, -1.f, c->U, ldd, 1.f);
   b3.n = 3;
   prof(c, LST_PHASE_MID, true);
-  if (record(c, gemm_launch(b3, c->flag, s, GEMM_MID))) return LST_E_HIP;
+  gemm_run(b3, c->flag, s, GEMM_MID);
   prof(c, LST_PHASE_MID, false);
 
   // U^{-T} += (2 eta X S C^{-1} S) H^T (Woodbury); Q += H Zq^T + Zq H^T (eq. updateQ /
@@ -594,17 +585,16 @@ int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, 
   b4.d[2] = gemm_desc(m, d, m, c->N, m, 0, c->Yw, d, 1, c->P, d, 1.f, c->X, d, 1.f);
   b4.n = 3;
   prof(c, LST_PHASE_UPDATE, true);
-  if (record(c, gemm_launch(b4, c->flag, s, GEMM_UPDATE))) return LST_E_HIP;
+  gemm_run(b4, c->flag, s, GEMM_UPDATE);
   prof(c, LST_PHASE_UPDATE, false);
 
   // V_r -= eta sum dl/dA P_j over the slots of each distinct target row (eq. updateV).
-  if (record(c, hipStreamWaitEvent(s, c->ev_sort_done, 0))) return LST_E_HIP;
   prof(c, LST_PHASE_SCATTER, true);
-  if (record(c, launch_scatter(s, m, K, d, lr, c->srow, c->sslot, c->nvalid, c->dA, c->P, c->V,
-                               c->ldv, c->flag)))
-    return LST_E_HIP;
+  launch_scatter(s, m, K, d, lr, idx, c->dA, c->P, c->V, c->ldv, c->flag);
   prof(c, LST_PHASE_SCATTER, false);
-  return LST_OK;
+  // Kernel launches above are not checked one by one: a launch error stays pending
+  // and is reported here.
+  return record(c, hipGetLastError()) ? LST_E_HIP : LST_OK;
 }
 
 // Replays (capturing first if needed) the graph of a step with these arguments.

@@ -151,9 +151,8 @@ __device__ __forceinline__ int xcd_tile(int wg, int T) {
   return x < r ? x * (q + 1) + slot : r * (q + 1) + (x - r) * q + slot;
 }
 
-// PHASE only names the instantiation, so profilers report each step phase separately.
-template <int PHASE, int NW>
-__global__ __launch_bounds__(64 * NW) void gemm_kernel(const GemmBatch bt, const int *__restrict__ gate) {
+template <int NW>
+__device__ __forceinline__ void gemm_body(const GemmBatch &bt, const int *__restrict__ gate) {
   if (gate && *gate != 0) return;
   const int tile = xcd_tile(blockIdx.x, bt.total_tiles);
   int di = 0;
@@ -205,6 +204,12 @@ __global__ __launch_bounds__(64 * NW) void gemm_kernel(const GemmBatch bt, const
         finish(g, i, j, v);
     }
   }
+}
+
+// PHASE only names the instantiation, so profilers report each step phase separately.
+template <int PHASE, int NW>
+__global__ __launch_bounds__(64 * NW) void gemm_kernel(const GemmBatch bt, const int *__restrict__ gate) {
+  gemm_body<NW>(bt, gate);
 }
 
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const GemmDesc g, const int *__restrict__ gate) {
@@ -271,7 +276,7 @@ size_t gemm_plan_split(GemmDesc &g, int target_wgs, float *partial) {
   return (size_t)splits * g.M * g.N;
 }
 
-hipError_t gemm_launch(GemmBatch &b, const int *gate, hipStream_t s, int phase) {
+int gemm_prepare(GemmBatch &b) {
   int total = 0;
   int kmax = 0;
   for (int q = 0; q < b.n; ++q) {
@@ -285,19 +290,24 @@ hipError_t gemm_launch(GemmBatch &b, const int *gate, hipStream_t s, int phase) 
       if (kk > kmax) kmax = kk;
     }
   }
-  b.total_tiles = total;
-  if (total == 0) return hipSuccess;
   // Empty descriptors (M or N == 0) own no tiles; give them tile_begin past the end.
   for (int q = 0; q < b.n; ++q)
     if (b.d[q].M <= 0 || b.d[q].N <= 0) b.d[q].tile_begin = total;
-  // Waves per tile: enough to keep each wave's share of k short.
-  const bool wide = kmax >= 384;
+  b.total_tiles = total;
+  b.wide = kmax >= 384 ? 1 : 0;  // waves per tile: enough to keep each wave's share of k short
+  return total;
+}
+
+void gemm_enqueue(const GemmBatch &b, const int *gate, hipStream_t s, int phase) {
+  const int total = b.total_tiles;
+  if (total == 0) return;
+  const bool wide = b.wide != 0;
   switch (phase) {
-#define LST_GEMM_CASE(P)                     \
-  case P:                                    \
-    if (wide)                                \
+#define LST_GEMM_CASE(P)                          \
+  case P:                                         \
+    if (wide)                                     \
       launch_phase<P, 8>(total, s, b, gate); \
-    else                                     \
+    else                                          \
       launch_phase<P, 4>(total, s, b, gate); \
     break;
     LST_GEMM_CASE(GEMM_CONTRACT)
@@ -314,8 +324,6 @@ hipError_t gemm_launch(GemmBatch &b, const int *gate, hipStream_t s, int phase) 
       else
         launch_phase<GEMM_OTHER, 4>(total, s, b, gate);
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
   for (int q = 0; q < b.n; ++q) {
     const GemmDesc &g = b.d[q];
     if (g.splits > 1 && g.M > 0 && g.N > 0) {
@@ -323,11 +331,14 @@ hipError_t gemm_launch(GemmBatch &b, const int *gate, hipStream_t s, int phase) 
       int blocks = (int)((tot + 255) / 256);
       if (blocks > 2048) blocks = 2048;
       hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, g, gate);
-      e = hipGetLastError();
-      if (e != hipSuccess) return e;
     }
   }
-  return hipSuccess;
+}
+
+hipError_t gemm_launch(GemmBatch &b, const int *gate, hipStream_t s, int phase) {
+  gemm_prepare(b);
+  gemm_enqueue(b, gate, s, phase);
+  return hipGetLastError();
 }
 
 }  // namespace lst

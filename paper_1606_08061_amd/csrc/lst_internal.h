@@ -53,6 +53,7 @@ struct GemmBatch {
   GemmDesc d[kMaxBatch];
   int n;
   int total_tiles;
+  int wide;  // 8 wavefronts per tile (long k) instead of 4
 };
 
 GemmDesc gemm_desc(int M, int N, int K, const float *A, int64_t lda, int tA, const float *B,
@@ -76,6 +77,11 @@ enum : int {
 // *gate != 0 at kernel start.
 hipError_t gemm_launch(GemmBatch &b, const int *gate, hipStream_t s, int phase = GEMM_OTHER);
 
+// Two-part form: gemm_prepare fills the tile bookkeeping (returns the tile
+// count); gemm_enqueue launches without checking for errors.
+int gemm_prepare(GemmBatch &b);
+void gemm_enqueue(const GemmBatch &b, const int *gate, hipStream_t s, int phase);
+
 // Choose a split count for a long-k descriptor and attach its partial buffer.
 // Returns the number of floats the partial buffer needs.
 size_t gemm_plan_split(GemmDesc &g, int target_wgs, float *partial);
@@ -88,8 +94,6 @@ hipError_t launch_gather(hipStream_t s, int m, int K, int d, int64_t D, const fl
                          const float *V, int64_t ldv, int loss, float eps, float lr, float *G,
                          float *Atil, float *dq, float *dA, float *lvec, int *flag);
 
-hipError_t launch_sort(hipStream_t s, int n, const int *idx, int *srow, int *sslot, int *nvalid);
-
 hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
                            const float *N, float *R, float *Cwork, int *flag);
 
@@ -97,9 +101,8 @@ hipError_t launch_mblock(hipStream_t s, int m, int K, const int *idx, const floa
                          const float *dq, const float *dA, const float *Mhat, const float *HZ,
                          float *M, float *loss_out, int *flag);
 
-hipError_t launch_scatter(hipStream_t s, int m, int K, int d, float lr, const int *srow,
-                          const int *sslot, const int *nvalid, const float *dA, const float *P,
-                          float *V, int64_t ldv, const int *flag);
+hipError_t launch_scatter(hipStream_t s, int m, int K, int d, float lr, const int *idx,
+                          const float *dA, const float *P, float *V, int64_t ldv, const int *flag);
 
 hipError_t launch_identity(hipStream_t s, float *A, int d, int64_t ld);
 hipError_t launch_fill(hipStream_t s, float *p, float v);

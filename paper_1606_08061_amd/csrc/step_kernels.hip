@@ -5,8 +5,6 @@
 //               (l_j, dl/dq_j, dl/dA_kj) and G_j = sum_k dl/dA_kj V_{K_kj}
 //               (the V^T Yring of eq. gen-Zhat-fact; Algorithm 3 step 2's V^T Y
 //               up to the factor -2).
-//   sort     -- (row, slot) keys of the targets sorted, so that the slots of
-//               each V row are contiguous and in a fixed order.
 //   woodbury -- the m x m Woodbury matrix C = I - 2 eta S H^T H S and its
 //               inverse (Gauss-Jordan without pivoting: C is symmetric positive
 //               definite exactly when the step is admissible), giving
@@ -15,9 +13,9 @@
 //   mblock   -- L = sum_j l_j and the Q-update matrix M of eq. gen-M, with the
 //               sparse Yring^T Yring by index equality.
 //   scatter  -- eq. updateV / gen-updateV: V_r -= eta sum_{slots of row r}
-//               dl/dA P_j, one workgroup per distinct row, slots in a fixed
-//               order, so repeated rows never race and results are
-//               reproducible bit for bit.
+//               dl/dA P_j, one writer per distinct row (its lowest slot), slots
+//               summed in ascending order, so repeated rows never race and
+//               results are reproducible bit for bit.
 //   naive    -- column norms of O, the loss epilogue over the explicit output
 //               and grad_O = 2 O diag(dl/dq) + Yring (eq. gen-grad-O).
 #include "lst_internal.h"
@@ -147,63 +145,6 @@ __global__ __launch_bounds__(kGatherThreads) void gather_kernel(
 }
 
 constexpr int kMaxSortKeys = 8192;
-
-// Bitonic sort of n (power of two) 64-bit keys in LDS, ascending.
-__device__ void bitonic_sort(unsigned long long *key, int n) {
-  for (int size = 2; size <= n; size <<= 1) {
-    for (int stride = size >> 1; stride > 0; stride >>= 1) {
-      for (int t = threadIdx.x; t < (n >> 1); t += blockDim.x) {
-        const int lo = 2 * t - (t & (stride - 1));
-        const int hi = lo + stride;
-        const bool up = ((lo & size) == 0);
-        const unsigned long long a = key[lo], b = key[hi];
-        if ((a > b) == up) {
-          key[lo] = b;
-          key[hi] = a;
-        }
-      }
-      __syncthreads();
-    }
-  }
-}
-
-// Sorted (row, slot) keys of the valid target slots: the slots of one V row
-// become contiguous, in ascending slot order, for the conflict-free scatter.
-constexpr int kSortThreads = 1024;
-
-__global__ __launch_bounds__(kSortThreads) void sort_kernel(int n, const int *__restrict__ idx,
-                                                           int *__restrict__ srow_out,
-                                                           int *__restrict__ sslot_out,
-                                                           int *__restrict__ nvalid) {
-  __shared__ unsigned long long skey[kMaxSortKeys];
-  __shared__ int s_cnt;
-  const int t = threadIdx.x;
-  int np = 1;
-  while (np < n) np <<= 1;
-  if (t == 0) s_cnt = 0;
-  for (int e = t; e < np; e += kSortThreads) {
-    unsigned long long key = ~0ull;
-    if (e < n) {
-      const int r = idx[e];
-      if (r >= 0) key = ((unsigned long long)(unsigned)r << 32) | (unsigned)e;
-    }
-    skey[e] = key;
-  }
-  __syncthreads();
-  bitonic_sort(skey, np);
-  int cnt = 0;
-  for (int e = t; e < n; e += kSortThreads) {
-    const unsigned long long key = skey[e];
-    if (key != ~0ull) {
-      srow_out[e] = (int)(key >> 32);
-      sslot_out[e] = (int)(key & 0xffffffffu);
-      ++cnt;
-    }
-  }
-  if (cnt) atomicAdd(&s_cnt, cnt);
-  __syncthreads();
-  if (t == 0) *nvalid = s_cnt;
-}
 
 // Gauss-Jordan inversion in place, matrix held in registers: thread (ti, tj)
 // of a T x T grid owns the B x B block at rows ti*B.., cols tj*B...  Entries
@@ -493,27 +434,51 @@ __global__ __launch_bounds__(kMblockThreads) void mblock_kernel(
 
 constexpr int kScatterThreads = 256;
 
-// One workgroup per sorted slot position; only the first position of each
-// distinct row does work, over all the slots of that row, column-parallel.
+// One workgroup per target slot s (slot = j*K + k of the m x K index matrix).
+// The lowest slot of each V row does the row's update: it lists, in ascending
+// slot order, every slot with the same row and applies
+//   V_r -= eta sum_{slots s' of row r} dl/dA_s' P_{j(s')},
+// so each distinct row has exactly one writer and a fixed summation order.
 __global__ __launch_bounds__(kScatterThreads) void scatter_kernel(
-    int K, int d, float lr, const int *__restrict__ srow, const int *__restrict__ sslot,
-    const int *__restrict__ nvalid, const float *__restrict__ dA, const float *__restrict__ P,
-    float *__restrict__ V, int64_t ldv, const int *__restrict__ gate) {
+    int n, int K, int d, float lr, const int *__restrict__ idx, const float *__restrict__ dA,
+    const float *__restrict__ P, float *__restrict__ V, int64_t ldv, const int *__restrict__ gate) {
+  extern __shared__ int sh[];
+  int *sidx = sh;        // n target rows
+  int *slist = sh + n;   // slots of this row, ascending
+  __shared__ int swcnt[kScatterThreads / 64];
   if (*gate != 0) return;
-  const int p = blockIdx.x;
-  const int n = *nvalid;
-  if (p >= n) return;
-  const int r = srow[p];
-  if (p > 0 && srow[p - 1] == r) return;  // not the first slot of its row
-  int e = p + 1;
-  while (e < n && srow[e] == r) ++e;
+  const int s = blockIdx.x;
+  const int r = idx[s];
+  if (r < 0) return;
+  int dup = 0;
+  for (int q = threadIdx.x; q < n; q += kScatterThreads) {
+    const int v = idx[q];
+    sidx[q] = v;
+    dup |= (q < s && v == r);
+  }
+  if (__syncthreads_or(dup)) return;  // an earlier slot owns this row
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  int total = 0;
+  for (int base = s; base < n; base += kScatterThreads) {
+    const int q = base + threadIdx.x;
+    const bool match = q < n && sidx[q] == r;
+    const unsigned long long mask = __ballot(match);
+    if (lane == 0) swcnt[w] = __popcll(mask);
+    __syncthreads();
+    int before = total;
+    for (int x = 0; x < w; ++x) before += swcnt[x];
+    if (match) slist[before + __popcll(mask & ((1ull << lane) - 1ull))] = q;
+    for (int x = 0; x < kScatterThreads / 64; ++x) total += swcnt[x];
+    __syncthreads();
+  }
+
   float *vr = V + (int64_t)r * ldv;
   for (int c = threadIdx.x; c < d; c += kScatterThreads) {
     float acc = 0.f;
-#pragma unroll 4
-    for (int s = p; s < e; ++s) {
-      const int slot = sslot[s];
-      acc += dA[slot] * P[(int64_t)(slot / K) * d + c];
+    for (int t = 0; t < total; ++t) {
+      const int q = slist[t];
+      acc += dA[q] * P[(int64_t)(q / K) * d + c];
     }
     vr[c] -= lr * acc;
   }
@@ -624,12 +589,7 @@ hipError_t launch_gather(hipStream_t s, int m, int K, int d, int64_t D, const fl
                          float *Atil, float *dq, float *dA, float *lvec, int *flag) {
   hipLaunchKernelGGL(gather_kernel, dim3(m), dim3(kGatherThreads), 0, s, K, d, D, H, Hhat, Htil, idx, val, V,
                      ldv, loss, eps, lr, G, Atil, dq, dA, lvec, flag);
-  return hipGetLastError();
-}
-
-hipError_t launch_sort(hipStream_t s, int n, const int *idx, int *srow, int *sslot, int *nvalid) {
-  hipLaunchKernelGGL(sort_kernel, dim3(1), dim3(kSortThreads), 0, s, n, idx, srow, sslot, nvalid);
-  return hipGetLastError();
+  return hipSuccess;  // checked once per step by the caller
 }
 
 hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
@@ -649,7 +609,7 @@ hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const fl
   else
     hipLaunchKernelGGL((woodbury_kernel<32, 0>), dim3(1), dim3(1024), 0, s, m, lr, unit_dq, dq, N,
                        R, Cwork, flag);
-  return hipGetLastError();
+  return hipSuccess;  // checked once per step by the caller
 }
 
 hipError_t launch_mblock(hipStream_t s, int m, int K, const int *idx, const float *lvec,
@@ -658,17 +618,16 @@ hipError_t launch_mblock(hipStream_t s, int m, int K, const int *idx, const floa
   const int blocks = (m * m + kMblockThreads - 1) / kMblockThreads;
   hipLaunchKernelGGL(mblock_kernel, dim3(blocks), dim3(kMblockThreads), 0, s, m, K, idx, lvec, dq,
                      dA, Mhat, HZ, M, loss_out, flag);
-  return hipGetLastError();
+  return hipSuccess;  // checked once per step by the caller
 }
 
-hipError_t launch_scatter(hipStream_t s, int m, int K, int d, float lr, const int *srow,
-                          const int *sslot, const int *nvalid, const float *dA, const float *P,
-                          float *V, int64_t ldv, const int *flag) {
+hipError_t launch_scatter(hipStream_t s, int m, int K, int d, float lr, const int *idx,
+                          const float *dA, const float *P, float *V, int64_t ldv, const int *flag) {
   const int n = m * K;
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(scatter_kernel, dim3(n), dim3(kScatterThreads), 0, s, K, d, lr, srow, sslot,
-                     nvalid, dA, P, V, ldv, flag);
-  return hipGetLastError();
+  hipLaunchKernelGGL(scatter_kernel, dim3(n), dim3(kScatterThreads), 2 * n * sizeof(int), s, n, K,
+                     d, lr, idx, dA, P, V, ldv, flag);
+  return hipSuccess;  // checked once per step by the caller
 }
 
 hipError_t launch_identity(hipStream_t s, float *A, int d, int64_t ld) {
