@@ -146,96 +146,152 @@ __global__ __launch_bounds__(kGatherThreads) void gather_kernel(
 
 constexpr int kMaxSortKeys = 8192;
 
-// Gauss-Jordan inversion in place, matrix held in registers: thread (ti, tj)
-// of a T x T grid owns the B x B block at rows ti*B.., cols tj*B...  Entries
-// outside m x m are the identity and take no part.  Returns false (uniformly)
-// if a pivot is not positive and finite.
+// ---------------------------------------------------------------------------
+// Blocked Gauss-Jordan inverse on the matrix cores (m <= 256).
 //
-// One elimination step on pivot k (p = A_kk) is written as
-//   A' = X - f g^T,  X = A with column k replaced by e_k,
-//   f_i = A_ik (i != k), f_k = p - 1,   g_j = A_kj / p (j != k), g_k = 1 / p,
-// which gives A'_kj = A_kj / p, A'_ik = -A_ik / p, A'_kk = 1 / p and
-// A'_ij = A_ij - A_ik A_kj / p elsewhere.  The pivot's position inside a block
-// (KR) is a compile-time index of the unrolled inner loop, so the register
-// block is never indexed at run time.  Lookahead: right after reading pivot k,
-// the owners of row and column k+1 compute their updated values and publish
-// them, so the one barrier per pivot waits only for the bulk of the update.
-template <int B, int KR>
-__device__ __forceinline__ float gj_new(const float (&a)[B][B], int r, int c, bool own_row,
-                                        bool own_col, const float (&f)[B], const float (&g)[B]) {
-  float x = a[r][c];
-  if (c == KR) x = own_col ? ((r == KR && own_row) ? 1.f : 0.f) : x;
-  return x - f[r] * g[c];
+// The mp x mp matrix (mp = 32 NBK >= m, padded with the identity) lives in
+// MFMA accumulator registers as NBK x NBK tiles of 32 x 32, tile t owned by
+// wavefront t % W.  In accumulator layout lane l = j + 32 h holds column j of a
+// tile and register r holds row acc_row(h, r).  Block step kb with pivot block
+// P = A_kb,kb^{-1} is, in place,
+//   A_kb,j <- P A_kb,j,   A_ij <- A_ij - A_i,kb (P A_kb,j),
+//   A_i,kb <- -A_i,kb P,  A_kb,kb <- P                          (i, j != kb),
+// the block form of the scalar step below; after NBK block steps the tiles hold
+// the inverse.  The products run on v_mfma_f32_32x32x2f32 with the k index of
+// instruction r taken as acc_row(h, r) in lane-half h, so a tile held in
+// registers is directly the B operand of a product; the other operands come
+// from LDS copies of the column panel, the new row panel and P.  Since every
+// pivot block is a Schur complement of C, the pivots met inside the 32 x 32
+// inversions are exactly those of unblocked elimination: all are positive iff
+// C is positive definite.
+// ---------------------------------------------------------------------------
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ int acc_row(int h, int r) { return 4 * h + (r & 3) + 8 * (r >> 2); }
+
+constexpr int kTileLd = 36;  // LDS row stride (floats) of a staged 32 x 32 tile: 16-byte rows
+constexpr int kTileSz = 32 * kTileLd;
+
+// One scalar Gauss-Jordan step on pivot K of a 32 x 32 block held by one
+// wavefront in accumulator layout.  With p = A_KK the step is
+//   A' = X - f g^T,  X = A with column K replaced by e_K,
+//   f_i = A_iK (i != K), f_K = p - 1,   g_j = A_Kj / p (j != K), g_K = 1 / p,
+// i.e. A'_Kj = A_Kj / p, A'_iK = -A_iK / p, A'_KK = 1 / p, A'_ij = A_ij - A_iK A_Kj / p.
+// The block is symmetric on entry, so before step K column K is row K up to
+// sign (A_iK = A_Ki for i > K, -A_Ki for i < K) and only row K is exchanged.
+// Column K needs no separate case: there t_i = f_i (and t_K = p), so
+// A' = t - f (1 + 1/p) gives -f_i / p and 1 / p.  All pivots of a positive
+// definite C satisfy 0 < p <= 1 (C <= I), so that form loses nothing.
+//
+// Row K lives in register RK of lane-half HK.  The values on the serial path
+// from one step to the next -- p, row K at the lane's own column, and f for the
+// register that holds row K+1 -- are moved between lanes with readlane and
+// permlane32_swap; the other f values come from row K written to LDS
+// (rowx[K & 1][.]), whose latency the serial part of the step covers.  A bad
+// pivot sets `bad` and ends the elimination; the caller discards the block.
+// Orders LDS writes of some lanes of a wavefront before later LDS reads of other
+// lanes of the same wavefront (the hardware keeps one wavefront's LDS accesses in
+// order; the fence stops the compiler from moving a read above the write).
+__device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
+
+__device__ __forceinline__ float lane_read(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
-template <int T, int B, int KR>
-__device__ __forceinline__ bool gj_step(float (&a)[B][B], int kb, int m, float *srow, float *scol) {
-  const int t = threadIdx.x;
-  const int ti = t / T, tj = t % T;
-  const int k = kb * B + KR;
-  const float *rowk = srow + (k & 1) * (T * B);
-  const float *colk = scol + (k & 1) * (T * B);
-  __syncthreads();
-  const float p = rowk[k];
-  if (!(p > 0.f) || !isfinite(p)) return false;
-  const float ip = 1.f / p;
-  const bool own_row = (ti == kb), own_col = (tj == kb);
-  float f[B], g[B];
+template <int K>
+__device__ __forceinline__ void gj32_step(float (&t)[16], int j, int h, float *rowx, bool &bad) {
+  constexpr int HK = (K >> 2) & 1, RK = (K & 3) + 4 * (K >> 3);
+  const float rk = t[RK];  // row K at column j in lane-half HK
+  if (h == HK) rowx[(K & 1) * 32 + j] = rk;
+  wave_lds_sync();
+  float rv[16];  // row K at columns acc_row(h, r)
 #pragma unroll
-  for (int r = 0; r < B; ++r) f[r] = colk[ti * B + r];
-#pragma unroll
-  for (int c = 0; c < B; ++c) g[c] = rowk[tj * B + c] * ip;
-  if (own_row) f[KR] = p - 1.f;
-  if (own_col) g[KR] = ip;
-  if (k + 1 < m) {
-    constexpr int KR1 = (KR + 1 < B) ? KR + 1 : 0;
-    const int kb1 = (KR + 1 < B) ? kb : kb + 1;
-    float *rown = srow + ((k + 1) & 1) * (T * B);
-    float *coln = scol + ((k + 1) & 1) * (T * B);
-    if (ti == kb1) {
-#pragma unroll
-      for (int c = 0; c < B; ++c) rown[tj * B + c] = gj_new<B, KR>(a, KR1, c, own_row, own_col, f, g);
-    }
-    if (tj == kb1) {
-#pragma unroll
-      for (int r = 0; r < B; ++r) coln[ti * B + r] = gj_new<B, KR>(a, r, KR1, own_row, own_col, f, g);
-    }
+  for (int q = 0; q < 4; ++q) {
+    const float4 v = *reinterpret_cast<const float4 *>(rowx + (K & 1) * 32 + 4 * h + 8 * q);
+    rv[4 * q] = v.x;
+    rv[4 * q + 1] = v.y;
+    rv[4 * q + 2] = v.z;
+    rv[4 * q + 3] = v.w;
+  }
+  const float p = lane_read(rk, K + 32 * HK);
+  bad |= !(p > 0.f && p < INFINITY);
+  if (bad) return;  // uniform; also splits the unrolled steps into separate blocks, which
+                    // keeps the compiler from hoisting (and holding) later steps' values
+  float ip = __builtin_amdgcn_rcpf(p);
+  ip = fmaf(ip, fmaf(-p, ip, 1.f), ip);  // one Newton step on the hardware reciprocal
+  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(rk), __float_as_uint(rk),
+                                                   false, false);
+  const float rkj = __uint_as_float(HK ? sw[1] : sw[0]);  // row K at column j, both halves
+  const float g = (j == K) ? 1.f + ip : rkj * ip;
+  constexpr int K1 = K + 1;
+  if constexpr (K1 < 32) {
+    // Register RK1 holds row K+1 in half HK1 and row K1o in the other half; their
+    // f values (row K at those columns) come from lanes of half HK directly.
+    constexpr int HK1 = (K1 >> 2) & 1, RK1 = (K1 & 3) + 4 * (K1 >> 3);
+    constexpr int K1o = HK1 ? K1 - 4 : K1 + 4;
+    const float f1 = lane_read(rk, K1 + 32 * HK);
+    const float r1o = lane_read(rk, K1o + 32 * HK);
+    const float f1o = (K1o == K) ? p - 1.f : ((K1o < K) ? -r1o : r1o);
+    t[RK1] = fmaf(-(h == HK1 ? f1 : f1o), g, t[RK1]);
   }
 #pragma unroll
-  for (int r = 0; r < B; ++r)
-#pragma unroll
-    for (int c = 0; c < B; ++c) a[r][c] = gj_new<B, KR>(a, r, c, own_row, own_col, f, g);
-  return true;
-}
-
-template <int T, int B, int KR>
-__device__ __forceinline__ bool gj_block(float (&a)[B][B], int kb, int m, float *srow, float *scol) {
-  if constexpr (KR < B) {
-    if (kb * B + KR >= m) return true;
-    if (!gj_step<T, B, KR>(a, kb, m, srow, scol)) return false;
-    return gj_block<T, B, KR + 1>(a, kb, m, srow, scol);
-  } else {
-    return true;
+  for (int r = 0; r < 16; ++r) {
+    if (K1 < 32 && r == ((K1 & 3) + 4 * (K1 >> 3))) continue;
+    const int i = acc_row(h, r);
+    const float f = (i == K) ? p - 1.f : ((i < K) ? -rv[r] : rv[r]);
+    t[r] = fmaf(-f, g, t[r]);
   }
 }
 
-template <int T, int B>
-__device__ bool gj_invert_regs(float (&a)[B][B], int m, float *srow, float *scol) {
-  // publish pivot 0
-  const int t = threadIdx.x;
-  const int ti = t / T, tj = t % T;
-  if (ti == 0) {
-#pragma unroll
-    for (int c = 0; c < B; ++c) srow[tj * B + c] = a[0][c];
+template <int K>
+__device__ __forceinline__ void gj32_from(float (&t)[16], int j, int h, float *rowx, bool &bad) {
+  if constexpr (K < 32) {
+    gj32_step<K>(t, j, h, rowx, bad);
+    gj32_from<K + 1>(t, j, h, rowx, bad);
   }
-  if (tj == 0) {
+}
+
+// Inverts the symmetric positive definite 32 x 32 block t (one wavefront,
+// accumulator layout) in place; false (uniformly) if some pivot is not
+// positive and finite.
+__device__ __forceinline__ bool gj32_invert(float (&t)[16], int j, int h, float *rowx) {
+  bool bad = false;
+  gj32_from<0>(t, j, h, rowx, bad);
+  return !bad;
+}
+
+// Operand fetch of a staged tile: lane (i or j, h) reads its 16 values at
+// column (row) offsets acc_row(h, 0..15), four 16-byte reads.
+__device__ __forceinline__ void lds_operand(const float *tile, int idx, int h, float (&o)[16]) {
 #pragma unroll
-    for (int r = 0; r < B; ++r) scol[ti * B + r] = a[r][0];
+  for (int q = 0; q < 4; ++q) {
+    const float4 v = *reinterpret_cast<const float4 *>(tile + idx * kTileLd + 4 * h + 8 * q);
+    o[4 * q] = v.x;
+    o[4 * q + 1] = v.y;
+    o[4 * q + 2] = v.z;
+    o[4 * q + 3] = v.w;
   }
-  const int nb = (m + B - 1) / B;
-  for (int kb = 0; kb < nb; ++kb)
-    if (!gj_block<T, B, 0>(a, kb, m, srow, scol)) return false;
-  return true;
+}
+
+// Stage a register tile for use as an A operand later (row-major: T[row][col]).
+__device__ __forceinline__ void stage_a(float *tile, const floatx16 &v, int j, int h) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) tile[acc_row(h, r) * kTileLd + j] = v[r];
+}
+
+// Stage a register tile for use as a B operand later (transposed: T[col][row]).
+__device__ __forceinline__ void stage_b(float *tile, const floatx16 &v, int j, int h) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    *reinterpret_cast<float4 *>(tile + j * kTileLd + 4 * h + 8 * q) =
+        make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+}
+
+// acc += A B over one 32-wide k block, k of instruction r = acc_row(h, r).
+__device__ __forceinline__ floatx16 mfma32(const float (&a)[16], const float (&b)[16], floatx16 acc) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[r], b[r], acc, 0, 0, 0);
+  return acc;
 }
 
 // Gauss-Jordan inversion in place of an m x m matrix in global memory (large m).
@@ -268,66 +324,195 @@ __device__ bool gj_invert_global(float *A, int m, float *srow, float *scol) {
 // Woodbury matrix C = I - 2 eta S N S with S = diag(dl/dq)^{1/2} and N = H^T H,
 // its inverse, and R = 2 eta S C^{-1} S (U_new^{-T} = U^{-T} + (U^{-T} H) R H^T).
 // unit_dq: dl/dq = 1 for every example (squared error), dq is not read.
-template <int T, int B>
-__global__ __launch_bounds__(T *T) void woodbury_kernel(int m, float lr, int unit_dq,
-                                                       const float *__restrict__ dq,
-                                                       const float *__restrict__ N,
-                                                       float *__restrict__ R, float *__restrict__ Cwork,
-                                                       int *__restrict__ flag) {
-  __shared__ float sbuf[4096];
-  __shared__ float sq[LST_MAX_M];
-  __shared__ int s_bad;
+// Returns false after raising the error flag when some dl/dq is negative or NaN.
+__device__ __forceinline__ bool woodbury_scales(int m, int unit_dq, const float *__restrict__ dq,
+                                                float *sq, int *s_bad, int *flag) {
   const int t = threadIdx.x;
-  if (t == 0) s_bad = 0;
+  if (t == 0) *s_bad = 0;
   __syncthreads();
-  for (int i = t; i < m; i += T * T) {
+  for (int i = t; i < m; i += blockDim.x) {
     const float v = unit_dq ? 1.f : dq[i];
-    if (!(v >= 0.f)) atomicOr(&s_bad, 1);  // negative or NaN dl/dq: no real square root
+    if (!(v >= 0.f)) atomicOr(s_bad, 1);  // negative or NaN dl/dq: no real square root
     sq[i] = sqrtf(fmaxf(v, 0.f));
   }
   __syncthreads();
-  if (s_bad) {
+  if (__builtin_amdgcn_readfirstlane(*s_bad)) {
+    if (t == 0) atomicOr(flag, FLAG_NOT_SPD);
+    return false;
+  }
+  return true;
+}
+
+template <int NBK>
+constexpr int wb_waves() { return NBK <= 4 ? 4 : 8; }
+
+template <int NBK>
+__global__ __launch_bounds__(64 * wb_waves<NBK>()) void woodbury_blocked_kernel(
+    int m, float lr, int unit_dq, const float *__restrict__ dq, const float *__restrict__ N,
+    float *__restrict__ R, int *__restrict__ flag) {
+  constexpr int W = wb_waves<NBK>();
+  constexpr int NT = NBK * NBK;
+  constexpr int TPW = (NT + W - 1) / W;  // tiles per wavefront
+  // Column panel and P are double-buffered by block-step parity, so a step
+  // needs two barriers: after the pivot block is inverted and the column panel
+  // staged, and after the new row panel is staged.
+  __shared__ __align__(16) float cpan[2][NBK][kTileSz];  // A_i,kb        (A operand)
+  __shared__ __align__(16) float rpan[NBK][kTileSz];     // P A_kb,j      (B operand)
+  __shared__ __align__(16) float pa[2][kTileSz];         // P             (A operand)
+  __shared__ __align__(16) float pb[2][kTileSz];         // P             (B operand)
+  __shared__ __align__(16) float rowx[64];
+  __shared__ __align__(16) float sq[32 * NBK];
+  __shared__ int s_bad;
+  if (!woodbury_scales(m, unit_dq, dq, sq, &s_bad, flag)) return;
+  const int lane = threadIdx.x & 63, j = lane & 31, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const float tl = 2.f * lr;
+
+  // Load C tile by tile: lane (j, h) reads column col of rows acc_row(h, 0..15);
+  // the scales come from LDS, sq[row] as four 16-byte reads.  Entries outside
+  // m x m read a clamped in-range address and are replaced by the identity.
+  floatx16 acc[TPW];
+#pragma unroll
+  for (int s = 0; s < TPW; ++s) {
+    const int t = min(wave + W * s, NT - 1);
+    const int r0 = (t / NBK) * 32, col = (t % NBK) * 32 + j;
+    const float sc = tl * sq[min(col, m - 1)];
+    float sr[16];
+    lds_operand(sq + r0, 0, h, sr);
+    const float *np = N + min(col, m - 1);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = r0 + acc_row(h, r);
+      const float v = np[min(row, m - 1) * m];
+      const float c = (row < m && col < m) ? -(sr[r] * v * sc) : 0.f;
+      acc[s][r] = (row == col) ? 1.f + c : c;
+    }
+  }
+
+  for (int kb = 0; kb < NBK; ++kb) {
+    const int buf = kb & 1;
+    // (a) invert the pivot block (its owner), stage P and the column panel
+    const int td = kb * NBK + kb;
+    if (wave == td % W) {
+      const int sd = td / W;  // slot of the pivot block; copied out by value so that
+      float p[16];            // the register tiles are never indexed at run time
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float v = acc[0][r];
+#pragma unroll
+        for (int s = 1; s < TPW; ++s) v = (s == sd) ? acc[s][r] : v;
+        p[r] = v;
+      }
+      if (gj32_invert(p, j, h, rowx)) {
+        floatx16 pv;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) pv[r] = p[r];
+#pragma unroll
+        for (int s = 0; s < TPW; ++s)
+          if (s == sd) acc[s] = pv;
+        stage_a(pa[buf], pv, j, h);
+        stage_b(pb[buf], pv, j, h);
+      } else if (lane == 0) {
+        s_bad = 1;
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < TPW; ++s) {
+      const int t = wave + W * s;
+      if (t < NT && t % NBK == kb && t / NBK != kb) stage_a(cpan[buf][t / NBK], acc[s], j, h);
+    }
+    __syncthreads();
+    if (__builtin_amdgcn_readfirstlane(s_bad)) break;
+    // (b) row panel A_kb,j <- P A_kb,j, staged for the trailing update
+#pragma unroll
+    for (int s = 0; s < TPW; ++s) {
+      const int t = wave + W * s;
+      if (t >= NT) continue;
+      const int ti = t / NBK, tj = t % NBK;
+      if (ti != kb || tj == kb) continue;
+      float a[16], b[16];
+      lds_operand(pa[buf], j, h, a);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) b[r] = acc[s][r];
+      floatx16 z;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) z[r] = 0.f;
+      acc[s] = mfma32(a, b, z);
+      stage_b(rpan[tj], acc[s], j, h);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+    // (c) trailing tiles and the column panel
+#pragma unroll
+    for (int s = 0; s < TPW; ++s) {
+      const int t = wave + W * s;
+      if (t >= NT) continue;
+      const int ti = t / NBK, tj = t % NBK;
+      if (ti == kb) continue;
+      float a[16], b[16];
+      lds_operand(cpan[buf][ti], j, h, a);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) a[r] = -a[r];
+      if (tj != kb) {
+        lds_operand(rpan[tj], j, h, b);
+        acc[s] = mfma32(a, b, acc[s]);
+      } else {
+        lds_operand(pb[buf], j, h, b);
+        floatx16 z;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) z[r] = 0.f;
+        acc[s] = mfma32(a, b, z);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // one tile's operands live at a time
+    }
+  }
+  if (__builtin_amdgcn_readfirstlane(s_bad)) {
+    if (threadIdx.x == 0) atomicOr(flag, FLAG_NOT_SPD);
+    return;
+  }
+#pragma unroll
+  for (int s = 0; s < TPW; ++s) {
+    const int t = wave + W * s;
+    if (t >= NT) continue;
+    const int r0 = (t / NBK) * 32, col = (t % NBK) * 32 + j;
+    if (col >= m) continue;
+    const float sc = tl * sq[col];
+    float sr[16];
+    lds_operand(sq + r0, 0, h, sr);
+    float *rp = R + col;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = r0 + acc_row(h, r);
+      if (row < m) rp[row * m] = sr[r] * acc[s][r] * sc;
+    }
+  }
+}
+
+// Larger m: the same Woodbury matrix inverted by scalar Gauss-Jordan in global memory.
+__global__ __launch_bounds__(1024) void woodbury_global_kernel(int m, float lr, int unit_dq,
+                                                               const float *__restrict__ dq,
+                                                               const float *__restrict__ N,
+                                                               float *__restrict__ R,
+                                                               float *__restrict__ Cwork,
+                                                               int *__restrict__ flag) {
+  __shared__ float sbuf[2 * LST_MAX_M];
+  __shared__ float sq[LST_MAX_M];
+  __shared__ int s_bad;
+  if (!woodbury_scales(m, unit_dq, dq, sq, &s_bad, flag)) return;
+  const int t = threadIdx.x;
+  for (int e = t; e < m * m; e += blockDim.x) {
+    const int i = e / m, j = e - i * m;
+    Cwork[e] = ((i == j) ? 1.f : 0.f) - 2.f * lr * sq[i] * N[e] * sq[j];
+  }
+  __syncthreads();
+  if (!gj_invert_global(Cwork, m, sbuf, sbuf + LST_MAX_M)) {
     if (t == 0) atomicOr(flag, FLAG_NOT_SPD);
     return;
   }
-  bool ok;
-  if constexpr (B > 0) {
-    float a[B][B];
-    const int ti = t / T, tj = t % T;
-#pragma unroll
-    for (int r = 0; r < B; ++r)
-#pragma unroll
-      for (int c = 0; c < B; ++c) {
-        const int i = ti * B + r, j = tj * B + c;
-        float v = (i == j) ? 1.f : 0.f;
-        if (i < m && j < m) v -= 2.f * lr * sq[i] * N[(int64_t)i * m + j] * sq[j];
-        a[r][c] = v;
-      }
-    ok = gj_invert_regs<T, B>(a, m, sbuf, sbuf + 2048);
-    if (ok) {
-#pragma unroll
-      for (int r = 0; r < B; ++r)
-#pragma unroll
-        for (int c = 0; c < B; ++c) {
-          const int i = ti * B + r, j = tj * B + c;
-          if (i < m && j < m) R[(int64_t)i * m + j] = 2.f * lr * sq[i] * a[r][c] * sq[j];
-        }
-    }
-  } else {
-    for (int e = t; e < m * m; e += T * T) {
-      const int i = e / m, j = e - i * m;
-      Cwork[e] = ((i == j) ? 1.f : 0.f) - 2.f * lr * sq[i] * N[e] * sq[j];
-    }
-    __syncthreads();
-    ok = gj_invert_global(Cwork, m, sbuf, sbuf + 2048);
-    if (ok) {
-      for (int e = t; e < m * m; e += T * T) {
-        const int i = e / m, j = e - i * m;
-        R[e] = 2.f * lr * sq[i] * Cwork[e] * sq[j];
-      }
-    }
+  for (int e = t; e < m * m; e += blockDim.x) {
+    const int i = e / m, j = e - i * m;
+    R[e] = 2.f * lr * sq[i] * Cwork[e] * sq[j];
   }
-  if (!ok && t == 0) atomicOr(flag, FLAG_NOT_SPD);
 }
 
 // Loss L = sum_j l_j (fixed order; non-finite -> error flag) and the Q-update
@@ -594,21 +779,25 @@ hipError_t launch_gather(hipStream_t s, int m, int K, int d, int64_t D, const fl
 
 hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
                            const float *N, float *R, float *Cwork, int *flag) {
-  if (m <= 32)
-    hipLaunchKernelGGL((woodbury_kernel<16, 2>), dim3(1), dim3(256), 0, s, m, lr, unit_dq, dq, N, R,
-                       Cwork, flag);
-  else if (m <= 64)
-    hipLaunchKernelGGL((woodbury_kernel<16, 4>), dim3(1), dim3(256), 0, s, m, lr, unit_dq, dq, N, R,
-                       Cwork, flag);
-  else if (m <= 128)
-    hipLaunchKernelGGL((woodbury_kernel<32, 4>), dim3(1), dim3(1024), 0, s, m, lr, unit_dq, dq, N,
-                       R, Cwork, flag);
-  else if (m <= 256)
-    hipLaunchKernelGGL((woodbury_kernel<32, 8>), dim3(1), dim3(1024), 0, s, m, lr, unit_dq, dq, N,
-                       R, Cwork, flag);
-  else
-    hipLaunchKernelGGL((woodbury_kernel<32, 0>), dim3(1), dim3(1024), 0, s, m, lr, unit_dq, dq, N,
-                       R, Cwork, flag);
+  switch ((m + 31) / 32) {
+#define LST_WB_CASE(NB)                                                                       \
+  case NB:                                                                                    \
+    hipLaunchKernelGGL((woodbury_blocked_kernel<NB>), dim3(1), dim3(64 * wb_waves<NB>()), 0, s, \
+                       m, lr, unit_dq, dq, N, R, flag);                                       \
+    break;
+    LST_WB_CASE(1)
+    LST_WB_CASE(2)
+    LST_WB_CASE(3)
+    LST_WB_CASE(4)
+    LST_WB_CASE(5)
+    LST_WB_CASE(6)
+    LST_WB_CASE(7)
+    LST_WB_CASE(8)
+#undef LST_WB_CASE
+    default:
+      hipLaunchKernelGGL(woodbury_global_kernel, dim3(1), dim3(1024), 0, s, m, lr, unit_dq, dq, N,
+                         R, Cwork, flag);
+  }
   return hipSuccess;  // checked once per step by the caller
 }
 

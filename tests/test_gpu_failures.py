@@ -68,16 +68,21 @@ def test_nonfinite_H():
     f.close()
 
 
-def test_not_positive_definite():
-    # m = 1 and ||h||^2 = 1/eta: the Woodbury (Sherman-Morrison) denominator
-    # 1 - 2 eta ||h||^2 = -1 < 0; the fp64 mirror predicts the same.
-    w = Workload("t", LOSS_SQUARED, 200, 16, 1, 1, lr=0.05)
+@pytest.mark.parametrize("m,bad", [(1, 0), (70, 40), (200, 150), (300, 290)])
+def test_not_positive_definite(m, bad):
+    # Example `bad` gets ||h||^2 = 1/eta, so C = I - 2 eta H H^T has C_bad,bad = -1
+    # and a negative eigenvalue (for m = 1 this is the Sherman-Morrison denominator
+    # 1 - 2 eta ||h||^2 = -1).  Elimination meets the first non-positive pivot at
+    # or before row `bad`, inside a later diagonal block for m > 32.  The fp64
+    # mirror confirms C is indefinite.
+    w = Workload("t", LOSS_SQUARED, 400, 16, m, 1, lr=0.05)
     s = Stream(w)
     H, idx, val = s.batch()
-    H = (H / np.linalg.norm(H) * np.sqrt(1.0 / w.lr)).astype(np.float32)
+    H = (H * 0.05).astype(np.float32)
+    H[bad] = (H[bad] / np.linalg.norm(H[bad]) * np.sqrt(1.0 / w.lr)).astype(np.float32)
     st = factored_init(s.V0)
     _, _, inter = alg4_step(st, H, idx, val, np.float32(w.lr), LOSS_SQUARED)
-    assert inter["C"][0, 0] < 0
+    assert np.linalg.eigvalsh(inter["C"]).min() < 0
     f = make_factored(w, s.V0)
     snap = _state(f)
     f.step(*to_dev(H, idx, val), w.lr)
