@@ -2,6 +2,7 @@
 the naive O(D d) path and the fp64 CPU oracle as baselines.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+    python bench.py --sweep        # factored vs naive over the D x d sweep, JSON lines
 
 A step is one pass of the whole factored step (dense contractions, sparse
 gather, loss and grad_H, the m x m Woodbury block, the U / U^{-T} / Q updates
@@ -27,70 +28,160 @@ METRIC = "examples/s exact loss+grad+update, D=200k d=500 m=128; speedup vs naiv
 
 
 def phase_work(w, idx_pool):
-    """Algorithmic work per launch of each phase: (bound, amount, unit-of-amount)."""
+    """Algorithmic work per launch of each phase: (bound, amount, unit of amount).
+
+    bound "mfma": dense contractions, flops against the fp32 matrix peak; "hbm":
+    sparse V traffic, bytes against HBM bandwidth; "serial": the m x m Woodbury
+    inverse, a dependent chain of m pivots on one compute unit, reported by time.
+    """
     m, d, K = w.m, w.d, w.K
     uniq = float(np.mean([len(np.unique(i[i >= 0])) for i in idx_pool]))
     return {
-        # MACs x 2: H^, H~, X = {Q,U,U^-T} H
+        # H^, H~, X = {Q, U, U^-T} H: three m x d x d products
         "contract": ("mfma", 2.0 * 3 * m * d * d, "flop"),
-        # V rows of the targets, H, H^, H~ read; G and the scaled H~ written
+        # N = H^T H (m x m x d)
+        "gram": ("mfma", 2.0 * m * m * d, "flop"),
+        # the m x K target rows of V plus H, H^, H~ read; G and the scaled H~ written
         "gather": ("hbm", 4.0 * (m * K * d + 5 * m * d), "byte"),
-        # Z^ = U^T G, H^T H^, H~^T G
+        # Z^ = U^T G (m d^2), H^T H^ and H~^T G (m^2 d each)
         "zgrad": ("mfma", 2.0 * (m * d * d + 2 * m * m * d), "flop"),
-        # N = H^T H (2 m^2 d) and the Gauss-Jordan inverse of the m x m Woodbury matrix (m^3 FMA)
-        "woodbury": ("alu", 2.0 * m * m * d + 2.0 * m ** 3, "flop"),
+        # Gauss-Jordan inverse of the m x m Woodbury matrix: m^3 multiply-adds
+        "woodbury": ("serial", 2.0 * m ** 3, "flop"),
         # loss sum and the m x m entries of M
-        "mblock": ("alu", 8.0 * m * m, "flop"),
-        # R X, M H, U update
+        "mblock": ("serial", 8.0 * m * m, "flop"),
+        # R X, M H (m^2 d each) and the U update (m d^2)
         "mid": ("mfma", 2.0 * (m * d * d + 2 * m * m * d), "flop"),
-        # U^-T update, Q update (two products), P
+        # U^-T update (m d^2), Q update (2 m d^2), P = X + N Yw (m^2 d)
         "update": ("mfma", 2.0 * (3 * m * d * d + m * m * d), "flop"),
         # read-modify-write of the distinct target rows and the P rows they use
         "scatter": ("hbm", 4.0 * (2 * uniq * d + m * d), "byte"),
     }
 
 
-def roofline_for(phases, work, steps):
-    # dominant phase = largest total time
-    name = max(work, key=lambda p: phases[p][1])
-    cnt, ms = phases[name]
-    avg_s = ms / max(cnt, 1) / 1e3
-    bound, amount, _ = work[name]
-    if bound == "hbm":
-        achieved = amount / avg_s / 1e9
-        peak, unit = PEAK_HBM_GBS, "GB/s"
-    else:
-        achieved = amount / avg_s / 1e12
-        peak, unit = PEAK_FP32_TFLOPS, "TFLOP/s"
-    return {"kernel_phase": name, "bound": bound, "achieved": round(achieved, 4), "peak": peak,
-            "unit": unit, "frac": round(achieved / peak, 5), "traffic": None,
-            "avg_launch_us": round(avg_s * 1e6, 3), "algorithmic_per_launch": amount}
+def kernel_table(phases, work):
+    """Per-phase average duration and, where a roofline applies, its fraction."""
+    out = {}
+    for name, (bound, amount, unit) in work.items():
+        cnt, ms = phases.get(name, (0, 0.0))
+        if not cnt:
+            continue
+        avg_s = ms / cnt / 1e3
+        row = {"bound": bound, "avg_us": round(avg_s * 1e6, 3), "work_per_launch": amount,
+               "work_unit": unit}
+        if bound == "mfma":
+            row.update(achieved=round(amount / avg_s / 1e12, 4), peak=PEAK_FP32_TFLOPS,
+                       unit="TFLOP/s", frac=round(amount / avg_s / 1e12 / PEAK_FP32_TFLOPS, 5))
+        elif bound == "hbm":
+            row.update(achieved=round(amount / avg_s / 1e9, 2), peak=PEAK_HBM_GBS, unit="GB/s",
+                       frac=round(amount / avg_s / 1e9 / PEAK_HBM_GBS, 5))
+        out[name] = row
+    return out
 
 
-def cpu_baseline(w, V0, pool, seconds):
-    from threadpoolctl import threadpool_info
+def roofline_for(table, traffic=None):
+    """The dominant kernel: the longest of the kernels a roofline applies to (the
+    dense contractions and the sparse V passes).  The serial m x m inverse runs on
+    a side stream and is reported by its time only."""
+    name = max((k for k in table if table[k]["bound"] in ("mfma", "hbm")),
+               key=lambda k: table[k]["avg_us"])
+    r = table[name]
+    return {"kernel_phase": name, "bound": r["bound"], "achieved": r["achieved"], "peak": r["peak"],
+            "unit": r["unit"], "frac": r["frac"], "traffic": traffic,
+            "avg_launch_us": r["avg_us"], "algorithmic_per_launch": r["work_per_launch"]}
+
+
+def cpu_baseline(w, V0, pool, seconds, threads=None):
+    """The fp64 dense oracle on the host: examples/s over a bounded sample."""
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import dense_step
 
-    W = V0.astype(np.float64)
-    H, idx, val = pool[0]
-    dense_step(W, H, idx, val, np.float32(w.lr), w.loss, np.float32(w.eps))  # warm-up
-    n = 0
-    t0 = time.perf_counter()
-    while True:
-        H, idx, val = pool[(n + 1) % len(pool)]
-        W = dense_step(W, H, idx, val, np.float32(w.lr), w.loss, np.float32(w.eps)).W_new
-        n += 1
-        el = time.perf_counter() - t0
-        if (el >= seconds and n >= 2) or n >= 200:
-            break
-    blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
-    cores = int(blas[0]["num_threads"]) if blas else 1
+    with threadpool_limits(limits=threads, user_api="blas"):
+        W = V0.astype(np.float64)
+        H, idx, val = pool[0]
+        dense_step(W, H, idx, val, np.float32(w.lr), w.loss, np.float32(w.eps))  # warm-up
+        n = 0
+        t0 = time.perf_counter()
+        while True:
+            H, idx, val = pool[(n + 1) % len(pool)]
+            W = dense_step(W, H, idx, val, np.float32(w.lr), w.loss, np.float32(w.eps)).W_new
+            n += 1
+            el = time.perf_counter() - t0
+            if (el >= seconds and n >= 2) or n >= 200:
+                break
+        blas = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        cores = int(blas[0]["num_threads"]) if blas else 1
     return {"value": round(w.m * n / el, 3), "unit": "examples/s", "cores": cores,
             "kind": "oracle",
             "sample": f"{n} dense fp64 steps of {w.name} (D={w.D}, d={w.d}, m={w.m}) after 1 "
                       f"warm-up step, {el:.1f} s; nproc={os.cpu_count()}, "
                       f"affinity={len(os.sched_getaffinity(0))}"}
+
+
+def run_sweep(args):
+    """Factored vs naive ms/step over the D x d sweep (squared error, m=512, K=5), one
+    JSON line per config plus a line with the measured crossover per d."""
+    import torch
+
+    import paper_1606_08061_amd as lst
+    from workloads import sweep_workloads
+
+    dev = torch.device("cuda:0")
+    res = []
+    for w in sweep_workloads():
+        g = torch.Generator(device=dev)
+        g.manual_seed(w.D * 7 + w.d)
+        V0 = torch.randn((w.D, w.d), device=dev, generator=g) * (1.0 / np.sqrt(w.d))
+        batches = []
+        for t in range(4):
+            H = torch.randn((w.m, w.d), device=dev, generator=g) * (1.0 / np.sqrt(w.d))
+            idx = torch.randint(0, w.D, (w.m, w.K), device=dev, generator=g, dtype=torch.int32)
+            val = torch.randn((w.m, w.K), device=dev, generator=g)
+            batches.append((H.contiguous(), idx, val))
+        grad = torch.empty((w.m, w.d), device=dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+        def timed(step, n):
+            for t in range(3):
+                step(*batches[t % 4], w.lr, grad_H=grad)
+            torch.cuda.synchronize()
+            e0.record()
+            for t in range(n):
+                step(*batches[t % 4], w.lr, grad_H=grad)
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / n
+
+        f = lst.Factored(w.D, w.d, w.m, w.K, w.loss, float(np.float32(w.eps)), device=dev)
+        f.init(V0)
+        fms = timed(f.step, args.sweep_steps)
+        f.check("sweep factored")
+        f.close()
+        n = lst.Naive(w.D, w.d, w.m, w.K, w.loss, float(np.float32(w.eps)), device=dev)
+        n.init(V0)
+        nms = timed(n.step, max(2, args.sweep_steps // 4))
+        n.check("sweep naive")
+        n.close()
+        del V0, batches
+        torch.cuda.empty_cache()
+        row = {"sweep": w.name, "D": w.D, "d": w.d, "m": w.m, "K": w.K,
+               "factored_ms_per_step": round(fms, 4), "naive_ms_per_step": round(nms, 4),
+               "speedup": round(nms / fms, 3), "D_over_4d": round(w.D / (4 * w.d), 2)}
+        res.append(row)
+        print(json.dumps(row), flush=True)
+    cross = {}
+    for d in sorted({r["d"] for r in res}):
+        pts = sorted((r["D"], r["speedup"]) for r in res if r["d"] == d)
+        c = None
+        for (D0, s0), (D1, s1) in zip(pts, pts[1:]):
+            if s0 < 1.0 <= s1:  # log-linear interpolation of speedup = 1
+                t = (0.0 - np.log(s0)) / (np.log(s1) - np.log(s0))
+                c = float(np.exp(np.log(D0) + t * (np.log(D1) - np.log(D0))))
+                break
+        if c is None and pts and pts[0][1] >= 1.0:
+            c = f"below {pts[0][0]}"
+        cross[str(d)] = c if not isinstance(c, float) else round(c, 1)
+    print(json.dumps({"sweep_crossover_D": cross, "m": 512, "K": 5}), flush=True)
 
 
 def main():
@@ -101,15 +192,25 @@ def main():
     ap.add_argument("--workload", default="sq_D200k_d500_m128_K5")
     ap.add_argument("--pool", type=int, default=64, help="distinct minibatches cycled through")
     ap.add_argument("--naive-steps", type=int, default=20)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-naive", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="factored vs naive over the D x d sweep instead of the default line")
+    ap.add_argument("--sweep-steps", type=int, default=20)
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: the factored step is measured on one GPU's "
               "share (multi-GPU sharding of V by rows is described but not built)",
               file=sys.stderr)
         sys.exit(2)
+    if args.sweep:
+        import torch
+
+        if not torch.cuda.is_available():
+            raise RuntimeError("no GPU visible")
+        run_sweep(args)
+        return
 
     import torch
 
@@ -131,9 +232,11 @@ def main():
     # ---- factored path ----
     f = lst.Factored(w.D, w.d, w.m, w.K, w.loss, float(np.float32(w.eps)), device=dev)
     f.init(V0)
-    for t in range(args.warmup):
-        f.step(*gpool[t % len(gpool)], w.lr, want_grad=False)
     grad = torch.empty((w.m, w.d), dtype=torch.float32, device=dev)
+    # Warm-up with exactly the timed calls: every (batch, output) argument set is
+    # recorded as a HIP graph here, so the timed region only replays graphs.
+    for t in range(max(args.warmup, len(gpool))):
+        f.step(*gpool[t % len(gpool)], w.lr, grad_H=grad)
     f.check("warm-up")
     print("[bench] factored timed region", file=sys.stderr, flush=True)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -158,7 +261,8 @@ def main():
     f.profile(False)
     f.check("profiled steps")
     work = phase_work(w, [b[1] for b in pool])
-    roof = roofline_for(phases, work, args.steps)
+    table = kernel_table(phases, work)
+    roof = roofline_for(table)
     f.close()
     del f
 
@@ -191,10 +295,11 @@ def main():
 
     del V0, gpool
     torch.cuda.empty_cache()
-    cpu = None
+    cpu = cpu1 = None
     if not args.no_cpu:
         print("[bench] cpu baseline (fp64 oracle)", file=sys.stderr, flush=True)
         cpu = cpu_baseline(w, s.V0, pool, args.cpu_seconds)
+        cpu1 = cpu_baseline(w, s.V0, pool, args.cpu_seconds / 2, threads=1)
 
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "examples/s", "n_gpus": 1,
@@ -205,11 +310,13 @@ def main():
                    "index_dist": w.index_dist, "lr": w.lr, "distinct_batches": args.pool},
         "roofline": roof,
         "cpu_baseline": cpu,
+        "cpu_baseline_1core": cpu1,
         "naive": naive,
         "speedup_vs_naive": round(value / naive["value"], 2) if naive else None,
         "speedup_model_D_over_4d": round(w.D / (4 * w.d), 1),
         "host_enqueue_us_per_step": round(host_us, 2),
-        "phases_us": {k: round(v[1] / max(v[0], 1) * 1e3, 2) for k, v in phases.items() if v[0]},
+        "kernels": table,
+        "serial_inverse_us": table.get("woodbury", {}).get("avg_us"),
     }
     print(json.dumps(out), flush=True)
 

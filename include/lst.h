@@ -173,15 +173,15 @@ int lst_naive_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t
 int lst_naive_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val,
                    int32_t K, float lr, float *loss_dev, float *grad_H);
 
-/* Phases of a step, as timed by the profiling hook below.  The Woodbury inverse
-   runs on a side stream of the context, overlapping the main chain; the other
-   phases run in order on the context's stream. */
+/* Phases of a step, as timed by the profiling hook below.  The Gram product and
+   the Woodbury inverse run on a side stream of the context, overlapping the main
+   chain; the other phases run in order on the context's stream. */
 enum lst_phase {
   LST_PHASE_CONTRACT = 0,      /* H^ = Q H, H~ = U H, X = U^{-T} H (matrix cores)          */
   LST_PHASE_GATHER = 1,        /* gather of the K target rows of V, loss epilogue, G       */
   LST_PHASE_ZGRAD = 2,         /* Z^ = U^T G, grad_H, H^T H^, H~^T G (matrix cores)        */
   LST_PHASE_MBLOCK = 3,        /* loss sum, M of the Q update                              */
-  LST_PHASE_WOODBURY = 4,      /* N = H^T H, the m x m Woodbury matrix and its inverse     */
+  LST_PHASE_WOODBURY = 4,      /* the m x m Woodbury matrix and its inverse                */
   LST_PHASE_MID = 5,           /* R X, (eta^2/2) M H - eta grad_H, U update (matrix cores) */
   LST_PHASE_UPDATE = 6,        /* U^{-T} and Q updates, P = U_new^{-T} H (matrix cores)    */
   LST_PHASE_SCATTER = 7,       /* conflict-free update of the target rows of V             */
@@ -189,13 +189,16 @@ enum lst_phase {
   LST_PHASE_NAIVE_LOSS = 9,    /* naive: column norms of O, loss, grad_O                   */
   LST_PHASE_NAIVE_GRAD = 10,   /* naive: grad_H = grad_O^T W                               */
   LST_PHASE_NAIVE_UPDATE = 11, /* naive: W <- W - eta grad_O H                             */
-  LST_NUM_PHASES = 12
+  LST_PHASE_GRAM = 12,         /* N = H^T H, the Gram matrix of the minibatch (matrix cores) */
+  LST_NUM_PHASES = 13
 };
 
 /*
- * lst_profile_enable -- tracing hook.  While on (on != 0), every step records a
- * pair of HIP events around each of its phases on the context's stream (this
- * adds a few microseconds per phase).  Turning it on clears earlier records.
+ * lst_profile_enable -- tracing hook.  While on (on != 0), steps are enqueued
+ * without HIP graphs and each phase's kernels are launched with a pair of HIP
+ * events attached to the launches themselves (start of the phase's first kernel,
+ * end of its last kernel), so the recorded time is the phases' GPU execution time
+ * without launch gaps.  Turning it on clears earlier records.
  */
 int lst_profile_enable(lst_ctx *c, int32_t on);
 

@@ -52,7 +52,7 @@ SIGNATURES = {
 }
 
 PHASES = ["contract", "gather", "zgrad", "mblock", "woodbury", "mid", "update", "scatter",
-          "naive_fwd", "naive_loss", "naive_grad", "naive_update"]
+          "naive_fwd", "naive_loss", "naive_grad", "naive_update", "gram"]
 
 _lib = None
 _lock = threading.Lock()

@@ -10,6 +10,10 @@
 
 using namespace lst;
 
+namespace lst {
+thread_local ProfHook g_prof;
+}  // namespace lst
+
 namespace {
 
 enum : int { KIND_FACTORED = 1, KIND_NAIVE = 2 };
@@ -61,6 +65,7 @@ struct lst_ctx {
   size_t ws_bytes;
   float *Hhat, *Htil, *X, *G, *Atil, *Zhat, *gradH, *Yw, *Zq, *P;
   float *N, *Mhat, *HZ, *M, *R, *Cwork;
+  float *Pbig, *Cp, *Rp;  // blocked Woodbury inverse for m > 256
   float *dq, *lvec, *dA;
   int *flag;
   float *O, *colpart, *splitpart;
@@ -104,6 +109,10 @@ void carve_factored(lst_ctx *c, Carver &cv) {
   c->M = cv.take<float>(mm);
   c->R = cv.take<float>(mm);
   c->Cwork = cv.take<float>(mm);
+  const size_t big = c->m_max > kWoodburyOneWG ? kBigBlock : 0;
+  c->Pbig = cv.take<float>(2 * big * big);  // P and P + I
+  c->Cp = cv.take<float>((size_t)c->m_max * big);
+  c->Rp = cv.take<float>(big * c->m_max);
   c->dq = cv.take<float>(c->m_max);
   c->lvec = cv.take<float>(c->m_max);
   c->dA = cv.take<float>(mk);
@@ -171,13 +180,21 @@ int record(lst_ctx *c, hipError_t e) {
 constexpr int kProfCap = 65536;
 
 // Records the start (begin=true) or the end of a phase when profiling is on.
-void prof(lst_ctx *c, int phase, bool begin, hipStream_t st = nullptr) {
+// Phase timing: begin hands a fresh event pair to the launch hook (see
+// LST_LAUNCH); end withdraws it and keeps the pair if a kernel consumed it.
+void prof(lst_ctx *c, int phase, bool begin) {
   if (!c->prof_on) return;
   int &used = c->prof_used[phase];
+  if (!begin) {
+    const bool launched = g_prof.stop != nullptr && g_prof.start == nullptr;
+    g_prof = ProfHook{};
+    if (launched) ++used;
+    return;
+  }
+  g_prof = ProfHook{};
   if (used >= kProfCap) return;
   std::vector<hipEvent_t> &ev = c->prof_ev[phase];
-  const size_t slot = 2 * (size_t)used + (begin ? 0 : 1);
-  while (ev.size() <= slot) {
+  while (ev.size() < 2 * (size_t)used + 2) {
     hipEvent_t e;
     if (hipEventCreate(&e) != hipSuccess) {
       c->prof_on = false;
@@ -185,8 +202,8 @@ void prof(lst_ctx *c, int phase, bool begin, hipStream_t st = nullptr) {
     }
     ev.push_back(e);
   }
-  (void)hipEventRecord(ev[slot], st ? st : c->stream);
-  if (!begin) ++used;
+  g_prof.start = ev[2 * (size_t)used];
+  g_prof.stop = ev[2 * (size_t)used + 1];
 }
 
 int side_create(lst_ctx *c) {
@@ -502,14 +519,17 @@ int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, 
   // softmax waits for dl/dq = T / (q + D eps) from the gather.
   const bool unit_dq = (c->loss == LST_LOSS_SQUARED);
   if (record(c, hipStreamWaitEvent(s_wood, c->ev_fork, 0))) return LST_E_HIP;
-  prof(c, LST_PHASE_WOODBURY, true, s_wood);
+  prof(c, LST_PHASE_GRAM, true);
   GemmBatch bn{};
   bn.d[0] = gemm_desc(m, m, d, H, d, 0, H, d, 0, c->N, m);
   bn.n = 1;
   gemm_run(bn, nullptr, s_wood);
+  prof(c, LST_PHASE_GRAM, false);
   auto woodbury = [&]() -> int {
-    launch_woodbury(s_wood, m, lr, unit_dq ? 1 : 0, c->dq, c->N, c->R, c->Cwork, c->flag);
-    prof(c, LST_PHASE_WOODBURY, false, s_wood);
+    prof(c, LST_PHASE_WOODBURY, true);
+    launch_woodbury(s_wood, m, lr, unit_dq ? 1 : 0, c->dq, c->N, c->R, c->Cwork, c->Pbig, c->Cp,
+                    c->Rp, c->flag);
+    prof(c, LST_PHASE_WOODBURY, false);
     return record(c, hipEventRecord(c->ev_wood_done, s_wood));
   };
   if (unit_dq && woodbury() != LST_OK) return LST_E_HIP;

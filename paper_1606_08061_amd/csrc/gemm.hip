@@ -153,7 +153,8 @@ __device__ __forceinline__ int xcd_tile(int wg, int T) {
 
 template <int NW>
 __device__ __forceinline__ void gemm_body(const GemmBatch &bt, const int *__restrict__ gate) {
-  if (gate && *gate != 0) return;
+  // The gate only suppresses writes, so its load is waited for at the end.
+  const int closed = gate ? *gate : 0;
   const int tile = xcd_tile(blockIdx.x, bt.total_tiles);
   int di = 0;
 #pragma unroll
@@ -173,6 +174,23 @@ __device__ __forceinline__ void gemm_body(const GemmBatch &bt, const int *__rest
   const int i0 = tm * 32, j0 = tn * 32;
   const int ia = min(i0 + li, g.M - 1), jb = min(j0 + li, g.N - 1);
 
+  // Epilogue operands (C_in, and E of the grad_H epilogue) are fetched before the
+  // k loop so that their latency overlaps it.  Thread o of the tile's 1024
+  // outputs holds output (r, ln) = (o / 64, o % 64) after the reduction below.
+  constexpr int kPer = 1024 / (64 * NW);
+  float cin[kPer], ein[kPer];
+  const bool use_cin = g.Cin != nullptr && g.splits == 1;
+  const bool use_e = g.epi == EPI_GRADH && g.splits == 1;
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int o = threadIdx.x + u * 64 * NW;
+    const int r = o >> 6, ln = o & 63;
+    const int i = min(i0 + (r >> 2) * 8 + (ln >> 5) * 4 + (r & 3), g.M - 1);
+    const int j = min(j0 + (ln & 31), g.N - 1);
+    cin[u] = use_cin ? g.Cin[(int64_t)i * g.ldcin + j] : 0.f;
+    ein[u] = use_e ? g.E[(int64_t)i * g.lde + j] : 0.f;
+  }
+
   floatx16 acc;
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc[r] = 0.f;
@@ -190,7 +208,10 @@ __device__ __forceinline__ void gemm_body(const GemmBatch &bt, const int *__rest
 #pragma unroll
   for (int r = 0; r < 16; ++r) red[wave][r][lane] = acc[r];
   __syncthreads();
-  for (int o = threadIdx.x; o < 1024; o += 64 * NW) {
+  if (closed) return;  // after the last barrier
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int o = threadIdx.x + u * 64 * NW;
     const int r = o >> 6, ln = o & 63;
     float v = 0.f;
 #pragma unroll
@@ -198,10 +219,13 @@ __device__ __forceinline__ void gemm_body(const GemmBatch &bt, const int *__rest
     const int i = i0 + (r >> 2) * 8 + (ln >> 5) * 4 + (r & 3);
     const int j = j0 + (ln & 31);
     if (i < g.M && j < g.N) {
-      if (g.splits > 1)
+      if (g.splits > 1) {
         g.partial[((int64_t)split * g.M + i) * g.N + j] = v;
-      else
-        finish(g, i, j, v);
+      } else {
+        const float out = g.alpha * v + g.beta * cin[u];
+        g.C[(int64_t)i * g.ldc + j] = out;
+        if (use_e) g.C2[(int64_t)i * g.ldc2 + j] = 2.f * g.rs[i] * ein[u] + out;
+      }
     }
   }
 }
@@ -226,7 +250,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const GemmDesc g, co
 
 template <int P, int NW>
 void launch_phase(int total, hipStream_t s, const GemmBatch &b, const int *gate) {
-  hipLaunchKernelGGL((gemm_kernel<P, NW>), dim3(total), dim3(64 * NW), 0, s, b, gate);
+  LST_LAUNCH((gemm_kernel<P, NW>), dim3(total), dim3(64 * NW), 0, s, b, gate);
 }
 
 }  // namespace
@@ -330,7 +354,7 @@ void gemm_enqueue(const GemmBatch &b, const int *gate, hipStream_t s, int phase)
       const int64_t tot = (int64_t)g.M * g.N;
       int blocks = (int)((tot + 255) / 256);
       if (blocks > 2048) blocks = 2048;
-      hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, g, gate);
+      LST_LAUNCH(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, g, gate);
     }
   }
 }

@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 
 #include <cstddef>
 #include <cstdint>
@@ -9,6 +10,26 @@
 #include "lst.h"
 
 namespace lst {
+
+// Kernel timing hook.  While a phase is being timed, the launch macro attaches
+// g_prof.start to the next kernel launched (the phase's first) and g_prof.stop
+// to every launch (the last one records the phase's end).
+struct ProfHook {
+  hipEvent_t start = nullptr, stop = nullptr;
+};
+extern thread_local ProfHook g_prof;
+
+#define LST_LAUNCH(KERNEL, GRID, BLOCK, SHMEM, STREAM, ...)                                     \
+  do {                                                                                          \
+    hipEvent_t lst_ev_a_ = ::lst::g_prof.start;                                                \
+    ::lst::g_prof.start = nullptr;                                                             \
+    if (lst_ev_a_ || ::lst::g_prof.stop)                                                       \
+      hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, lst_ev_a_, ::lst::g_prof.stop, \
+                            0, __VA_ARGS__);                                                   \
+    else                                                                                       \
+      hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__);                     \
+  } while (0)
+
 
 // Sticky device error bits (mapped to lst_status by lst_sync_status).
 enum : int { FLAG_INDEX = 1, FLAG_NOT_SPD = 2, FLAG_NONFINITE = 4 };
@@ -94,8 +115,13 @@ hipError_t launch_gather(hipStream_t s, int m, int K, int d, int64_t D, const fl
                          const float *V, int64_t ldv, int loss, float eps, float lr, float *G,
                          float *Atil, float *dq, float *dA, float *lvec, int *flag);
 
+// m <= kWoodburyOneWG: one workgroup.  Larger m: blocked in kBigBlock-row steps
+// through Cwork (m x m), Pbig (2 kBigBlock^2), Cp (m x kBigBlock) and Rp (kBigBlock x m).
+constexpr int kWoodburyOneWG = 128;
+constexpr int kBigBlock = 128;
 hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
-                           const float *N, float *R, float *Cwork, int *flag);
+                           const float *N, float *R, float *Cwork, float *Pbig, float *Cp,
+                           float *Rp, int *flag);
 
 hipError_t launch_mblock(hipStream_t s, int m, int K, const int *idx, const float *lvec,
                          const float *dq, const float *dA, const float *Mhat, const float *HZ,

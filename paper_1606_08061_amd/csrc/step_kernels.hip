@@ -18,6 +18,8 @@
 //               results are reproducible bit for bit.
 //   naive    -- column norms of O, the loss epilogue over the explicit output
 //               and grad_O = 2 O diag(dl/dq) + Yring (eq. gen-grad-O).
+#include <algorithm>
+
 #include "lst_internal.h"
 
 namespace lst {
@@ -147,7 +149,7 @@ __global__ __launch_bounds__(kGatherThreads) void gather_kernel(
 constexpr int kMaxSortKeys = 8192;
 
 // ---------------------------------------------------------------------------
-// Blocked Gauss-Jordan inverse on the matrix cores (m <= 256).
+// Blocked Gauss-Jordan inverse on the matrix cores.
 //
 // The mp x mp matrix (mp = 32 NBK >= m, padded with the identity) lives in
 // MFMA accumulator registers as NBK x NBK tiles of 32 x 32, tile t owned by
@@ -294,32 +296,6 @@ __device__ __forceinline__ floatx16 mfma32(const float (&a)[16], const float (&b
   return acc;
 }
 
-// Gauss-Jordan inversion in place of an m x m matrix in global memory (large m).
-__device__ bool gj_invert_global(float *A, int m, float *srow, float *scol) {
-  for (int k = 0; k < m; ++k) {
-    for (int t = threadIdx.x; t < m; t += blockDim.x) {
-      srow[t] = A[(int64_t)k * m + t];
-      scol[t] = A[(int64_t)t * m + k];
-    }
-    __syncthreads();
-    const float p = srow[k];
-    if (!(p > 0.f) || !isfinite(p)) return false;
-    const float ip = 1.f / p;
-    for (int e = threadIdx.x; e < m * m; e += blockDim.x) {
-      const int i = e / m, j = e - i * m;
-      float v;
-      if (i == k)
-        v = (j == k) ? ip : srow[j] * ip;
-      else if (j == k)
-        v = -scol[i] * ip;
-      else
-        v = A[e] - scol[i] * (srow[j] * ip);
-      A[e] = v;
-    }
-    __syncthreads();
-  }
-  return true;
-}
 
 // Woodbury matrix C = I - 2 eta S N S with S = diag(dl/dq)^{1/2} and N = H^T H,
 // its inverse, and R = 2 eta S C^{-1} S (U_new^{-T} = U^{-T} + (U^{-T} H) R H^T).
@@ -344,7 +320,108 @@ __device__ __forceinline__ bool woodbury_scales(int m, int unit_dq, const float 
 }
 
 template <int NBK>
-constexpr int wb_waves() { return NBK <= 4 ? 4 : 8; }
+constexpr int wb_waves() { return 4; }  // NBK <= 4: at most 4 tiles per wavefront
+
+// LDS of the blocked elimination.  Column panel and P are double-buffered by
+// block-step parity, so a block step needs two barriers: after the pivot block
+// is inverted and the column panel staged, and after the new row panel is staged.
+template <int NBK>
+struct alignas(16) GjLds {
+  float cpan[2][NBK][kTileSz];  // A_i,kb        (A operand)
+  float rpan[NBK][kTileSz];     // P A_kb,j      (B operand)
+  float pa[2][kTileSz];         // P             (A operand)
+  float pb[2][kTileSz];         // P             (B operand)
+  float rowx[64];               // row exchange of the 32 x 32 inversions
+  int bad;
+};
+
+// The NBK block steps on the register-resident tiles (tile t = wave + W s).
+// sh.bad must be 0 on entry.  Returns false (uniformly) if a pivot is not
+// positive and finite; the tiles are then meaningless.
+template <int NBK, int W, int TPW>
+__device__ __forceinline__ bool blocked_gj(floatx16 (&acc)[TPW], GjLds<NBK> &sh, int wave,
+                                           int lane) {
+  constexpr int NT = NBK * NBK;
+  const int j = lane & 31, h = lane >> 5;
+  for (int kb = 0; kb < NBK; ++kb) {
+    const int buf = kb & 1;
+    // (a) invert the pivot block (its owner), stage P and the column panel
+    const int td = kb * NBK + kb;
+    if (wave == td % W) {
+      const int sd = td / W;  // slot of the pivot block; copied out by value so that
+      float p[16];            // the register tiles are never indexed at run time
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        float v = acc[0][r];
+#pragma unroll
+        for (int s = 1; s < TPW; ++s) v = (s == sd) ? acc[s][r] : v;
+        p[r] = v;
+      }
+      if (gj32_invert(p, j, h, sh.rowx)) {
+        floatx16 pv;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) pv[r] = p[r];
+#pragma unroll
+        for (int s = 0; s < TPW; ++s)
+          if (s == sd) acc[s] = pv;
+        stage_a(sh.pa[buf], pv, j, h);
+        stage_b(sh.pb[buf], pv, j, h);
+      } else if (lane == 0) {
+        sh.bad = 1;
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < TPW; ++s) {
+      const int t = wave + W * s;
+      if (t < NT && t % NBK == kb && t / NBK != kb) stage_a(sh.cpan[buf][t / NBK], acc[s], j, h);
+    }
+    __syncthreads();
+    if (__builtin_amdgcn_readfirstlane(sh.bad)) return false;
+    // (b) row panel A_kb,j <- P A_kb,j, staged for the trailing update
+#pragma unroll
+    for (int s = 0; s < TPW; ++s) {
+      const int t = wave + W * s;
+      if (t >= NT) continue;
+      const int ti = t / NBK, tj = t % NBK;
+      if (ti != kb || tj == kb) continue;
+      float a[16], b[16];
+      lds_operand(sh.pa[buf], j, h, a);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) b[r] = acc[s][r];
+      floatx16 z;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) z[r] = 0.f;
+      acc[s] = mfma32(a, b, z);
+      stage_b(sh.rpan[tj], acc[s], j, h);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+    // (c) trailing tiles and the column panel
+#pragma unroll
+    for (int s = 0; s < TPW; ++s) {
+      const int t = wave + W * s;
+      if (t >= NT) continue;
+      const int ti = t / NBK, tj = t % NBK;
+      if (ti == kb) continue;
+      float a[16], b[16];
+      lds_operand(sh.cpan[buf][ti], j, h, a);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) a[r] = -a[r];
+      if (tj != kb) {
+        lds_operand(sh.rpan[tj], j, h, b);
+        acc[s] = mfma32(a, b, acc[s]);
+      } else {
+        lds_operand(sh.pb[buf], j, h, b);
+        floatx16 z;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) z[r] = 0.f;
+        acc[s] = mfma32(a, b, z);
+      }
+      __builtin_amdgcn_sched_barrier(0);  // one tile's operands live at a time
+    }
+  }
+  return true;
+}
 
 template <int NBK>
 __global__ __launch_bounds__(64 * wb_waves<NBK>()) void woodbury_blocked_kernel(
@@ -353,17 +430,9 @@ __global__ __launch_bounds__(64 * wb_waves<NBK>()) void woodbury_blocked_kernel(
   constexpr int W = wb_waves<NBK>();
   constexpr int NT = NBK * NBK;
   constexpr int TPW = (NT + W - 1) / W;  // tiles per wavefront
-  // Column panel and P are double-buffered by block-step parity, so a step
-  // needs two barriers: after the pivot block is inverted and the column panel
-  // staged, and after the new row panel is staged.
-  __shared__ __align__(16) float cpan[2][NBK][kTileSz];  // A_i,kb        (A operand)
-  __shared__ __align__(16) float rpan[NBK][kTileSz];     // P A_kb,j      (B operand)
-  __shared__ __align__(16) float pa[2][kTileSz];         // P             (A operand)
-  __shared__ __align__(16) float pb[2][kTileSz];         // P             (B operand)
-  __shared__ __align__(16) float rowx[64];
+  __shared__ GjLds<NBK> sh;
   __shared__ __align__(16) float sq[32 * NBK];
-  __shared__ int s_bad;
-  if (!woodbury_scales(m, unit_dq, dq, sq, &s_bad, flag)) return;
+  if (!woodbury_scales(m, unit_dq, dq, sq, &sh.bad, flag)) return;
   const int lane = threadIdx.x & 63, j = lane & 31, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const float tl = 2.f * lr;
@@ -389,84 +458,7 @@ __global__ __launch_bounds__(64 * wb_waves<NBK>()) void woodbury_blocked_kernel(
     }
   }
 
-  for (int kb = 0; kb < NBK; ++kb) {
-    const int buf = kb & 1;
-    // (a) invert the pivot block (its owner), stage P and the column panel
-    const int td = kb * NBK + kb;
-    if (wave == td % W) {
-      const int sd = td / W;  // slot of the pivot block; copied out by value so that
-      float p[16];            // the register tiles are never indexed at run time
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float v = acc[0][r];
-#pragma unroll
-        for (int s = 1; s < TPW; ++s) v = (s == sd) ? acc[s][r] : v;
-        p[r] = v;
-      }
-      if (gj32_invert(p, j, h, rowx)) {
-        floatx16 pv;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) pv[r] = p[r];
-#pragma unroll
-        for (int s = 0; s < TPW; ++s)
-          if (s == sd) acc[s] = pv;
-        stage_a(pa[buf], pv, j, h);
-        stage_b(pb[buf], pv, j, h);
-      } else if (lane == 0) {
-        s_bad = 1;
-      }
-    }
-#pragma unroll
-    for (int s = 0; s < TPW; ++s) {
-      const int t = wave + W * s;
-      if (t < NT && t % NBK == kb && t / NBK != kb) stage_a(cpan[buf][t / NBK], acc[s], j, h);
-    }
-    __syncthreads();
-    if (__builtin_amdgcn_readfirstlane(s_bad)) break;
-    // (b) row panel A_kb,j <- P A_kb,j, staged for the trailing update
-#pragma unroll
-    for (int s = 0; s < TPW; ++s) {
-      const int t = wave + W * s;
-      if (t >= NT) continue;
-      const int ti = t / NBK, tj = t % NBK;
-      if (ti != kb || tj == kb) continue;
-      float a[16], b[16];
-      lds_operand(pa[buf], j, h, a);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) b[r] = acc[s][r];
-      floatx16 z;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) z[r] = 0.f;
-      acc[s] = mfma32(a, b, z);
-      stage_b(rpan[tj], acc[s], j, h);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    __syncthreads();
-    // (c) trailing tiles and the column panel
-#pragma unroll
-    for (int s = 0; s < TPW; ++s) {
-      const int t = wave + W * s;
-      if (t >= NT) continue;
-      const int ti = t / NBK, tj = t % NBK;
-      if (ti == kb) continue;
-      float a[16], b[16];
-      lds_operand(cpan[buf][ti], j, h, a);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) a[r] = -a[r];
-      if (tj != kb) {
-        lds_operand(rpan[tj], j, h, b);
-        acc[s] = mfma32(a, b, acc[s]);
-      } else {
-        lds_operand(pb[buf], j, h, b);
-        floatx16 z;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) z[r] = 0.f;
-        acc[s] = mfma32(a, b, z);
-      }
-      __builtin_amdgcn_sched_barrier(0);  // one tile's operands live at a time
-    }
-  }
-  if (__builtin_amdgcn_readfirstlane(s_bad)) {
+  if (!blocked_gj<NBK, W, TPW>(acc, sh, wave, lane)) {
     if (threadIdx.x == 0) atomicOr(flag, FLAG_NOT_SPD);
     return;
   }
@@ -488,30 +480,89 @@ __global__ __launch_bounds__(64 * wb_waves<NBK>()) void woodbury_blocked_kernel(
   }
 }
 
-// Larger m: the same Woodbury matrix inverted by scalar Gauss-Jordan in global memory.
-__global__ __launch_bounds__(1024) void woodbury_global_kernel(int m, float lr, int unit_dq,
-                                                               const float *__restrict__ dq,
-                                                               const float *__restrict__ N,
-                                                               float *__restrict__ R,
-                                                               float *__restrict__ Cwork,
-                                                               int *__restrict__ flag) {
-  __shared__ float sbuf[2 * LST_MAX_M];
-  __shared__ float sq[LST_MAX_M];
-  __shared__ int s_bad;
-  if (!woodbury_scales(m, unit_dq, dq, sq, &s_bad, flag)) return;
-  const int t = threadIdx.x;
-  for (int e = t; e < m * m; e += blockDim.x) {
-    const int i = e / m, j = e - i * m;
-    Cwork[e] = ((i == j) ? 1.f : 0.f) - 2.f * lr * sq[i] * N[e] * sq[j];
+// ---------------------------------------------------------------------------
+// Larger m: the same block step with kBigBlock-row pivot blocks on the m x m
+// matrix A (= C) in global memory, three launches per block b:
+//   pivot kernel   P = A_bb^{-1} (blocked_gj on one workgroup), PI = P + I;
+//   row launch     Rp_:,j = P A_b,j for the columns j outside b, Rp_:,b = P + I,
+//                  and the column panel copy Cp = A_:,b;
+//   trailing launch A_i,: += -Cp_i Rp for the rows i outside b, A_b,: = Rp.
+// Column b of a row outside b becomes A_ib - A_ib (P + I) = -A_ib P, as the block
+// step requires; the diagonal block becomes P + I, and the next pivot kernel (or
+// the final scaling) subtracts the I.
+// ---------------------------------------------------------------------------
+
+// A = C = I - 2 eta S N S (m x m); a negative or NaN dl/dq raises the error flag.
+__global__ void form_c_kernel(int m, float lr, int unit_dq, const float *__restrict__ dq,
+                              const float *__restrict__ N, float *__restrict__ A,
+                              int *__restrict__ flag) {
+  const int64_t total = (int64_t)m * m;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int i = (int)(e / m), j = (int)(e - (int64_t)i * m);
+    const float qi = unit_dq ? 1.f : dq[i], qj = unit_dq ? 1.f : dq[j];
+    if (i == j && !(qi >= 0.f)) atomicOr(flag, FLAG_NOT_SPD);
+    const float si = sqrtf(fmaxf(qi, 0.f)), sj = sqrtf(fmaxf(qj, 0.f));
+    A[e] = ((i == j) ? 1.f : 0.f) - 2.f * lr * si * N[e] * sj;
   }
+}
+
+// R = 2 eta S A S from the inverse held in A, less the I left on the last
+// diagonal block (rows lb0 .. m-1).
+__global__ void scale_r_kernel(int m, int lb0, float lr, int unit_dq, const float *__restrict__ dq,
+                               const float *__restrict__ A, float *__restrict__ R) {
+  const int64_t total = (int64_t)m * m;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int i = (int)(e / m), j = (int)(e - (int64_t)i * m);
+    const float qi = unit_dq ? 1.f : dq[i], qj = unit_dq ? 1.f : dq[j];
+    const float a = A[e] - ((i == j && i >= lb0) ? 1.f : 0.f);
+    R[e] = 2.f * lr * sqrtf(fmaxf(qi, 0.f)) * a * sqrtf(fmaxf(qj, 0.f));
+  }
+}
+
+// Pivot block b0 .. b0+nb-1 (nb <= kBigBlock) of A: P and PI = P + I
+// (kBigBlock^2 each, identity-padded).  First removes the I left on the
+// previous diagonal block (rows pb0 .. pb0+pnb-1; pnb = 0 for none).
+__global__ __launch_bounds__(256) void pivot_block_kernel(int m, int b0, int nb, int pb0, int pnb,
+                                                          float *__restrict__ A,
+                                                          float *__restrict__ P,
+                                                          float *__restrict__ PI,
+                                                          int *__restrict__ flag) {
+  constexpr int NBK = kBigBlock / 32, W = 4, TPW = NBK * NBK / W;
+  __shared__ GjLds<NBK> sh;
+  if (threadIdx.x == 0) sh.bad = 0;
+  for (int i = threadIdx.x; i < pnb; i += blockDim.x) A[(int64_t)(pb0 + i) * m + pb0 + i] -= 1.f;
   __syncthreads();
-  if (!gj_invert_global(Cwork, m, sbuf, sbuf + LST_MAX_M)) {
-    if (t == 0) atomicOr(flag, FLAG_NOT_SPD);
+  const int lane = threadIdx.x & 63, j = lane & 31, h = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  floatx16 acc[TPW];
+#pragma unroll
+  for (int s = 0; s < TPW; ++s) {
+    const int t = wave + W * s;
+    const int col = (t % NBK) * 32 + j;
+    const float *ap = A + (int64_t)b0 * m + b0 + min(col, nb - 1);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = (t / NBK) * 32 + acc_row(h, r);
+      const float v = ap[(int64_t)min(row, nb - 1) * m];
+      acc[s][r] = (row < nb && col < nb) ? v : ((row == col) ? 1.f : 0.f);
+    }
+  }
+  if (!blocked_gj<NBK, W, TPW>(acc, sh, wave, lane)) {
+    if (threadIdx.x == 0) atomicOr(flag, FLAG_NOT_SPD);
     return;
   }
-  for (int e = t; e < m * m; e += blockDim.x) {
-    const int i = e / m, j = e - i * m;
-    R[e] = 2.f * lr * sq[i] * Cwork[e] * sq[j];
+#pragma unroll
+  for (int s = 0; s < TPW; ++s) {
+    const int t = wave + W * s;
+    const int col = (t % NBK) * 32 + j;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int row = (t / NBK) * 32 + acc_row(h, r);
+      P[row * kBigBlock + col] = acc[s][r];
+      PI[row * kBigBlock + col] = acc[s][r] + ((row == col) ? 1.f : 0.f);
+    }
   }
 }
 
@@ -772,31 +823,65 @@ hipError_t launch_gather(hipStream_t s, int m, int K, int d, int64_t D, const fl
                          const float *Hhat, const float *Htil, const int *idx, const float *val,
                          const float *V, int64_t ldv, int loss, float eps, float lr, float *G,
                          float *Atil, float *dq, float *dA, float *lvec, int *flag) {
-  hipLaunchKernelGGL(gather_kernel, dim3(m), dim3(kGatherThreads), 0, s, K, d, D, H, Hhat, Htil, idx, val, V,
+  LST_LAUNCH(gather_kernel, dim3(m), dim3(kGatherThreads), 0, s, K, d, D, H, Hhat, Htil, idx, val, V,
                      ldv, loss, eps, lr, G, Atil, dq, dA, lvec, flag);
   return hipSuccess;  // checked once per step by the caller
 }
 
 hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
-                           const float *N, float *R, float *Cwork, int *flag) {
-  switch ((m + 31) / 32) {
+                           const float *N, float *R, float *Cwork, float *Pbig, float *Cp,
+                           float *Rp, int *flag) {
+  switch (m <= kWoodburyOneWG ? (m + 31) / 32 : 0) {
 #define LST_WB_CASE(NB)                                                                       \
   case NB:                                                                                    \
-    hipLaunchKernelGGL((woodbury_blocked_kernel<NB>), dim3(1), dim3(64 * wb_waves<NB>()), 0, s, \
-                       m, lr, unit_dq, dq, N, R, flag);                                       \
+    LST_LAUNCH((woodbury_blocked_kernel<NB>), dim3(1), dim3(64 * wb_waves<NB>()), 0, s, m, lr, \
+               unit_dq, dq, N, R, flag);                                                      \
     break;
     LST_WB_CASE(1)
     LST_WB_CASE(2)
     LST_WB_CASE(3)
     LST_WB_CASE(4)
-    LST_WB_CASE(5)
-    LST_WB_CASE(6)
-    LST_WB_CASE(7)
-    LST_WB_CASE(8)
 #undef LST_WB_CASE
-    default:
-      hipLaunchKernelGGL(woodbury_global_kernel, dim3(1), dim3(1024), 0, s, m, lr, unit_dq, dq, N,
-                         R, Cwork, flag);
+    default: {
+      const int blocks = (int)std::min<int64_t>(((int64_t)m * m + 255) / 256, 2048);
+      float *PI = Pbig + kBigBlock * kBigBlock;
+      LST_LAUNCH(form_c_kernel, dim3(blocks), dim3(256), 0, s, m, lr, unit_dq, dq, N, Cwork, flag);
+      int pb0 = 0, pnb = 0;
+      for (int b0 = 0; b0 < m; b0 += kBigBlock) {
+        const int nb = std::min(kBigBlock, m - b0), e0 = b0 + nb;
+        LST_LAUNCH(pivot_block_kernel, dim3(1), dim3(256), 0, s, m, b0, nb, pb0, pnb, Cwork, Pbig,
+                   PI, flag);
+        float *Ab = Cwork + (int64_t)b0 * m;
+        GemmBatch r{};
+        int n = 0;
+        if (b0 > 0) r.d[n++] = gemm_desc(nb, b0, nb, Pbig, kBigBlock, 0, Ab, m, 1, Rp, m);
+        if (e0 < m)
+          r.d[n++] = gemm_desc(nb, m - e0, nb, Pbig, kBigBlock, 0, Ab + e0, m, 1, Rp + e0, m);
+        r.d[n++] = gemm_desc(nb, nb, 0, PI, kBigBlock, 0, PI, kBigBlock, 1, Rp + b0, m, 0.f, PI,
+                             kBigBlock, 1.f);  // Rp_:,b = P + I
+        r.d[n++] = gemm_desc(m, nb, 0, Cp, kBigBlock, 0, Cp, kBigBlock, 1, Cp, kBigBlock, 0.f,
+                             Cwork + b0, m, 1.f);  // Cp = A_:,b
+        r.n = n;
+        gemm_prepare(r);
+        gemm_enqueue(r, nullptr, s, GEMM_OTHER);
+        GemmBatch t{};
+        n = 0;
+        if (b0 > 0)
+          t.d[n++] = gemm_desc(b0, m, nb, Cp, kBigBlock, 0, Rp, m, 1, Cwork, m, -1.f, Cwork, m, 1.f);
+        if (e0 < m) {
+          float *Al = Cwork + (int64_t)e0 * m;
+          t.d[n++] = gemm_desc(m - e0, m, nb, Cp + (int64_t)e0 * kBigBlock, kBigBlock, 0, Rp, m, 1,
+                               Al, m, -1.f, Al, m, 1.f);
+        }
+        t.d[n++] = gemm_desc(nb, m, 0, Rp, m, 0, Rp, m, 1, Ab, m, 0.f, Rp, m, 1.f);  // A_b,: = Rp
+        t.n = n;
+        gemm_prepare(t);
+        gemm_enqueue(t, nullptr, s, GEMM_OTHER);
+        pb0 = b0;
+        pnb = nb;
+      }
+      LST_LAUNCH(scale_r_kernel, dim3(blocks), dim3(256), 0, s, m, pb0, lr, unit_dq, dq, Cwork, R);
+    }
   }
   return hipSuccess;  // checked once per step by the caller
 }
@@ -805,7 +890,7 @@ hipError_t launch_mblock(hipStream_t s, int m, int K, const int *idx, const floa
                          const float *dq, const float *dA, const float *Mhat, const float *HZ,
                          float *M, float *loss_out, int *flag) {
   const int blocks = (m * m + kMblockThreads - 1) / kMblockThreads;
-  hipLaunchKernelGGL(mblock_kernel, dim3(blocks), dim3(kMblockThreads), 0, s, m, K, idx, lvec, dq,
+  LST_LAUNCH(mblock_kernel, dim3(blocks), dim3(kMblockThreads), 0, s, m, K, idx, lvec, dq,
                      dA, Mhat, HZ, M, loss_out, flag);
   return hipSuccess;  // checked once per step by the caller
 }
@@ -814,7 +899,7 @@ hipError_t launch_scatter(hipStream_t s, int m, int K, int d, float lr, const in
                           const float *dA, const float *P, float *V, int64_t ldv, const int *flag) {
   const int n = m * K;
   if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(scatter_kernel, dim3(n), dim3(kScatterThreads), 2 * n * sizeof(int), s, n, K,
+  LST_LAUNCH(scatter_kernel, dim3(n), dim3(kScatterThreads), 2 * n * sizeof(int), s, n, K,
                      d, lr, idx, dA, P, V, ldv, flag);
   return hipSuccess;  // checked once per step by the caller
 }
@@ -822,18 +907,18 @@ hipError_t launch_scatter(hipStream_t s, int m, int K, int d, float lr, const in
 hipError_t launch_identity(hipStream_t s, float *A, int d, int64_t ld) {
   int blocks = (int)(((int64_t)d * d + 255) / 256);
   if (blocks > 4096) blocks = 4096;
-  hipLaunchKernelGGL(identity_kernel, dim3(blocks), dim3(256), 0, s, A, d, ld);
+  LST_LAUNCH(identity_kernel, dim3(blocks), dim3(256), 0, s, A, d, ld);
   return hipGetLastError();
 }
 
 hipError_t launch_fill(hipStream_t s, float *p, float v) {
-  hipLaunchKernelGGL(fill_kernel, dim3(1), dim3(1), 0, s, p, v);
+  LST_LAUNCH(fill_kernel, dim3(1), dim3(1), 0, s, p, v);
   return hipGetLastError();
 }
 
 hipError_t launch_colnorm(hipStream_t s, const float *O, int64_t D, int m, float *partial,
                           int nblk) {
-  hipLaunchKernelGGL(colnorm_kernel, dim3(nblk), dim3(256), 0, s, O, D, m, partial);
+  LST_LAUNCH(colnorm_kernel, dim3(nblk), dim3(256), 0, s, O, D, m, partial);
   return hipGetLastError();
 }
 
@@ -841,7 +926,7 @@ hipError_t launch_naive_epilogue(hipStream_t s, int m, int K, int64_t D, int nbl
                                  const float *partial, const float *O, const int *idx,
                                  const float *val, int loss, float eps, float *dq, float *dA,
                                  float *loss_out, int *flag) {
-  hipLaunchKernelGGL(naive_epilogue_kernel, dim3(1), dim3(1024), 0, s, m, K, D, nblk, partial, O,
+  LST_LAUNCH(naive_epilogue_kernel, dim3(1), dim3(1024), 0, s, m, K, D, nblk, partial, O,
                      idx, val, loss, eps, dq, dA, loss_out, flag);
   return hipGetLastError();
 }
@@ -851,10 +936,10 @@ hipError_t launch_grad_o(hipStream_t s, float *O, int64_t D, int m, int K, const
   const int64_t total = D * m;
   int blocks = (int)((total + 255) / 256);
   if (blocks > 8192) blocks = 8192;
-  hipLaunchKernelGGL(scale_cols_kernel, dim3(blocks), dim3(256), 0, s, O, total, m, dq);
+  LST_LAUNCH(scale_cols_kernel, dim3(blocks), dim3(256), 0, s, O, total, m, dq);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(sparse_add_kernel, dim3((m + 255) / 256), dim3(256), 0, s, O, D, m, K, idx,
+  LST_LAUNCH(sparse_add_kernel, dim3((m + 255) / 256), dim3(256), 0, s, O, D, m, K, idx,
                      dA);
   return hipGetLastError();
 }

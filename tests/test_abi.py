@@ -29,6 +29,15 @@ def test_header_and_binding_agree():
     assert _declared() == sorted(lst.SIGNATURES)
 
 
+def test_phase_names_follow_the_header_enum():
+    src = open(os.path.join(ROOT, "include", "lst.h")).read()
+    vals = {name: int(v) for name, v in re.findall(r"\bLST_PHASE_(\w+)\s*=\s*(\d+)", src)}
+    n = int(re.search(r"\bLST_NUM_PHASES\s*=\s*(\d+)", src).group(1))
+    assert sorted(vals.values()) == list(range(n)) == list(range(len(lst.PHASES)))
+    for name, v in vals.items():
+        assert lst.PHASES[v] == name.lower()
+
+
 def test_every_declared_symbol_is_exported(L):
     for name in _declared():
         assert hasattr(L, name), name

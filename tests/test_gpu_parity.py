@@ -52,7 +52,7 @@ def test_small_config_100_steps():
 @pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX])
 @pytest.mark.parametrize("D,d,m,K", [
     (50, 1, 1, 1), (300, 31, 2, 3), (1000, 33, 17, 2), (777, 65, 33, 1), (2000, 40, 70, 3),
-    (1500, 47, 130, 2), (3000, 24, 300, 1), (400, 64, 5, 0),
+    (1500, 47, 130, 2), (3000, 24, 300, 1), (2500, 20, 520, 1), (400, 64, 5, 0),
 ])
 def test_awkward_shapes(loss, D, d, m, K):
     w = Workload("t", loss, D, d, m, K, index_dist="uniform",

@@ -68,9 +68,13 @@ WORKLOADS = {
 
 
 def sweep_workloads(m: int = 512, K: int = 5) -> list[Workload]:
-    """The D x d sweep comparing the factored and naive paths (squared error)."""
+    """The D x d sweep comparing the factored and naive paths (squared error).
+
+    D runs from 2k (below the flop crossover D ~ (10 d^2 + 3 m d + m^2) / (3 d),
+    about 1.7k at d = 256) up to 1M, so that the measured crossover is bracketed.
+    """
     out = []
-    for D in (50_000, 200_000, 1_000_000):
+    for D in (2_000, 5_000, 10_000, 20_000, 50_000, 200_000, 1_000_000):
         for d in (256, 512, 1024):
             out.append(Workload(f"sq_sweep_D{D}_d{d}_m{m}", LOSS_SQUARED, D, d, m, K,
                                 steps=50))
