@@ -44,6 +44,17 @@ struct GraphEntry {
 };
 constexpr size_t kGraphCap = 256;
 
+// The five GEMM batches of a factored step for one m: Gram product, contractions,
+// Z^/grad_H, mid and state updates.
+constexpr int kPlanBatches = 5;
+constexpr size_t kPlanCap = 16;
+struct PlanEntry {
+  int m;
+  GemmBatch b[kPlanBatches];
+  GemmBatch *dev;
+  uint64_t last_use;
+};
+
 }  // namespace
 
 struct lst_ctx {
@@ -80,6 +91,11 @@ struct lst_ctx {
   bool prof_on;
   std::vector<hipEvent_t> prof_ev[LST_NUM_PHASES];
   int prof_used[LST_NUM_PHASES];
+  // GEMM plans of the factored step, one per minibatch size m (host copies and
+  // their device slots in plan_pool)
+  std::vector<PlanEntry> plans;
+  GemmBatch *plan_pool;
+  uint64_t plan_tick;
   // captured steps, one per distinct (inputs, m, K, lr)
   bool use_graphs;
   std::vector<GraphEntry> graphs;
@@ -117,6 +133,7 @@ void carve_factored(lst_ctx *c, Carver &cv) {
   c->lvec = cv.take<float>(c->m_max);
   c->dA = cv.take<float>(mk);
   c->flag = cv.take<int>(1);
+  c->plan_pool = cv.take<GemmBatch>(kPlanCap * kPlanBatches);
 }
 
 // Upper bound of the split-k partial buffer of grad_H = grad_O^T W for any m <= m_max:
@@ -505,11 +522,104 @@ void gemm_run(GemmBatch &b, const int *gate, hipStream_t s, int phase = GEMM_OTH
   gemm_enqueue(b, gate, s, phase);
 }
 
-int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, const int32_t *idx,
-                          const float *val, int32_t K, float lr, float *loss_dev,
-                          float *grad_H) {
+// The step's GEMM batches for minibatch size m, with H and grad_H as placeholders.
+void build_plan(const lst_ctx *c, int m, GemmBatch (&b)[kPlanBatches]) {
   const int d = c->d, ldd = c->ldd;
+  const float *H = sym_H();
+  float *gH = sym_gradH();
+  for (GemmBatch &x : b) x = GemmBatch{};
+  // N = H^T H (Woodbury branch)
+  b[0].d[0] = gemm_desc(m, m, d, H, d, 0, H, d, 0, c->N, m);
+  b[0].n = 1;
+  // H^ = Q H, H~ = U H, X = U^{-T} H (Algorithm 3 steps 1, 5, 6; Algorithm 4 rows 1, 5)
+  b[1].d[0] = gemm_desc(m, d, d, H, d, 0, c->Q, ldd, 0, c->Hhat, d);
+  b[1].d[1] = gemm_desc(m, d, d, H, d, 0, c->U, ldd, 0, c->Htil, d);
+  b[1].d[2] = gemm_desc(m, d, d, H, d, 0, c->UinvT, ldd, 0, c->X, d);
+  b[1].n = 3;
+  // Z^ = U^T G with grad_H = 2 H^ diag(dl/dq) + Z^; M^ = H^T H^; H^T Z^ = H~^T G
+  GemmDesc z = gemm_desc(m, d, d, c->G, d, 0, c->U, ldd, 1, c->Zhat, d);
+  z.epi = EPI_GRADH;
+  z.rs = c->dq;
+  z.E = c->Hhat;
+  z.lde = d;
+  z.C2 = gH;
+  z.ldc2 = d;
+  b[2].d[0] = z;
+  b[2].d[1] = gemm_desc(m, m, d, H, d, 0, c->Hhat, d, 0, c->Mhat, m);
+  b[2].d[2] = gemm_desc(m, m, d, c->Htil, d, 0, c->G, d, 0, c->HZ, m);
+  b[2].n = 3;
+  // Yw = R X; Zq = (eta^2/2) M H - eta grad_H; U <- U - 2 eta H~ diag(dl/dq) H^T
+  // (eq. updateU / gen-updateU).  Zq's alpha and beta scale with eta at launch.
+  b[3].d[0] = gemm_desc(m, d, m, c->R, m, 0, c->X, d, 1, c->Yw, d);
+  GemmDesc zq = gemm_desc(m, d, m, c->M, m, 0, H, d, 1, c->Zq, d, 0.5f, gH, d, -1.f);
+  zq.lr_scaled = 1;
+  b[3].d[1] = zq;
+  b[3].d[2] = gemm_desc(d, d, m, c->Atil, d, 1, H, d, 1, c->U, ldd, -1.f, c->U, ldd, 1.f);
+  b[3].n = 3;
+  // U^{-T} += (2 eta X S C^{-1} S) H^T (Woodbury); Q += H Zq^T + Zq H^T (eq. updateQ /
+  // gen-Qnew); P = U_new^{-T} H = X + (2 eta X S C^{-1} S)(H^T H).
+  b[4].d[0] = gemm_desc(d, d, m, c->Yw, d, 1, H, d, 1, c->UinvT, ldd, 1.f, c->UinvT, ldd, 1.f);
+  GemmDesc qd = gemm_desc(d, d, m, H, d, 1, c->Zq, d, 1, c->Q, ldd, 1.f, c->Q, ldd, 1.f);
+  qd.A2 = c->Zq;
+  qd.lda2 = d;
+  qd.B2 = H;
+  qd.ldb2 = d;
+  qd.K2 = m;
+  b[4].d[1] = qd;
+  b[4].d[2] = gemm_desc(m, d, m, c->N, m, 0, c->Yw, d, 1, c->P, d, 1.f, c->X, d, 1.f);
+  b[4].n = 3;
+  for (GemmBatch &x : b) gemm_prepare(x);
+}
+
+// The plan for m, built and copied to its device slot on first use.  Replacing
+// the least recently used plan first drains the streams and drops the recorded
+// graphs that launch it.
+PlanEntry *get_plan(lst_ctx *c, int m) {
+  for (PlanEntry &e : c->plans)
+    if (e.m == m) {
+      e.last_use = ++c->plan_tick;
+      return &e;
+    }
+  GemmBatch *slot;
+  if (c->plans.size() < kPlanCap) {
+    slot = c->plan_pool + c->plans.size() * kPlanBatches;
+    c->plans.push_back(PlanEntry{});
+  } else {
+    size_t v = 0;
+    for (size_t i = 1; i < c->plans.size(); ++i)
+      if (c->plans[i].last_use < c->plans[v].last_use) v = i;
+    if (record(c, hipStreamSynchronize(c->stream)) || record(c, hipStreamSynchronize(c->side[0])))
+      return nullptr;
+    const int old_m = c->plans[v].m;
+    for (size_t i = c->graphs.size(); i-- > 0;)
+      if (c->graphs[i].m == old_m) {
+        (void)hipGraphExecDestroy(c->graphs[i].exec);
+        c->graphs.erase(c->graphs.begin() + i);
+      }
+    slot = c->plans[v].dev;
+    c->plans.erase(c->plans.begin() + v);
+    c->plans.push_back(PlanEntry{});
+  }
+  PlanEntry &e = c->plans.back();
+  e.m = m;
+  e.dev = slot;
+  build_plan(c, m, e.b);
+  if (record(c, hipMemcpy(e.dev, e.b, sizeof(e.b), hipMemcpyHostToDevice))) {
+    c->plans.pop_back();
+    return nullptr;
+  }
+  e.last_use = ++c->plan_tick;
+  return &e;
+}
+
+int enqueue_factored_step(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *H,
+                          int32_t m, const int32_t *idx, const float *val, int32_t K, float lr,
+                          float *loss_dev, float *grad_H) {
+  const int d = c->d;
   float *gH = grad_H ? grad_H : c->gradH;
+  auto gemm = [&](int i, const int *gate, hipStream_t st, int phase) {
+    gemm_enqueue_plan(pl.b[i], pl.dev + i, H, gH, lr, gate, st, phase);
+  };
 
   hipStream_t s_wood = c->side[0];
   if (record(c, hipEventRecord(c->ev_fork, s))) return LST_E_HIP;
@@ -520,10 +630,7 @@ int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, 
   const bool unit_dq = (c->loss == LST_LOSS_SQUARED);
   if (record(c, hipStreamWaitEvent(s_wood, c->ev_fork, 0))) return LST_E_HIP;
   prof(c, LST_PHASE_GRAM, true);
-  GemmBatch bn{};
-  bn.d[0] = gemm_desc(m, m, d, H, d, 0, H, d, 0, c->N, m);
-  bn.n = 1;
-  gemm_run(bn, nullptr, s_wood);
+  gemm(0, nullptr, s_wood, GEMM_OTHER);
   prof(c, LST_PHASE_GRAM, false);
   auto woodbury = [&]() -> int {
     prof(c, LST_PHASE_WOODBURY, true);
@@ -534,14 +641,8 @@ int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, 
   };
   if (unit_dq && woodbury() != LST_OK) return LST_E_HIP;
 
-  // H^ = Q H, H~ = U H, X = U^{-T} H (Algorithm 3 steps 1, 5, 6; Algorithm 4 rows 1, 5).
-  GemmBatch b1{};
-  b1.d[0] = gemm_desc(m, d, d, H, d, 0, c->Q, ldd, 0, c->Hhat, d);
-  b1.d[1] = gemm_desc(m, d, d, H, d, 0, c->U, ldd, 0, c->Htil, d);
-  b1.d[2] = gemm_desc(m, d, d, H, d, 0, c->UinvT, ldd, 0, c->X, d);
-  b1.n = 3;
   prof(c, LST_PHASE_CONTRACT, true);
-  gemm_run(b1, nullptr, s, GEMM_CONTRACT);
+  gemm(1, nullptr, s, GEMM_CONTRACT);
   prof(c, LST_PHASE_CONTRACT, false);
 
   // Sparse gather of the K target rows of the pre-update V and the loss epilogue.
@@ -555,21 +656,8 @@ int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, 
       return LST_E_HIP;
   }
 
-  // Z^ = U^T G with grad_H = 2 H^ diag(dl/dq) + Z^; M^ = H^T H^; H^T Z^ = H~^T G.
-  GemmBatch b2{};
-  GemmDesc z = gemm_desc(m, d, d, c->G, d, 0, c->U, ldd, 1, c->Zhat, d);
-  z.epi = EPI_GRADH;
-  z.rs = c->dq;
-  z.E = c->Hhat;
-  z.lde = d;
-  z.C2 = gH;
-  z.ldc2 = d;
-  b2.d[0] = z;
-  b2.d[1] = gemm_desc(m, m, d, H, d, 0, c->Hhat, d, 0, c->Mhat, m);
-  b2.d[2] = gemm_desc(m, m, d, c->Htil, d, 0, c->G, d, 0, c->HZ, m);
-  b2.n = 3;
   prof(c, LST_PHASE_ZGRAD, true);
-  gemm_run(b2, nullptr, s, GEMM_ZGRAD);
+  gemm(2, nullptr, s, GEMM_ZGRAD);
   prof(c, LST_PHASE_ZGRAD, false);
 
   // Loss and M; sets the error flag on a non-finite loss.
@@ -580,32 +668,12 @@ int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, 
   // Join the Woodbury branch before its result (and its error flag) is used.
   if (record(c, hipStreamWaitEvent(s, c->ev_wood_done, 0))) return LST_E_HIP;
 
-  // Gated state updates.  Yw = R X; Zq = (eta^2/2) M H - eta grad_H;
-  // U <- U - 2 eta H~ diag(dl/dq) H^T (eq. updateU / gen-updateU).
-  GemmBatch b3{};
-  b3.d[0] = gemm_desc(m, d, m, c->R, m, 0, c->X, d, 1, c->Yw, d);
-  b3.d[1] = gemm_desc(m, d, m, c->M, m, 0, H, d, 1, c->Zq, d, 0.5f * lr * lr, gH, d, -lr);
-  b3.d[2] = gemm_desc(d, d, m, c->Atil, d, 1, H, d, 1, c->U, ldd, -1.f, c->U, ldd, 1.f);
-  b3.n = 3;
+  // Gated state updates (see build_plan).
   prof(c, LST_PHASE_MID, true);
-  gemm_run(b3, c->flag, s, GEMM_MID);
+  gemm(3, c->flag, s, GEMM_MID);
   prof(c, LST_PHASE_MID, false);
-
-  // U^{-T} += (2 eta X S C^{-1} S) H^T (Woodbury); Q += H Zq^T + Zq H^T (eq. updateQ /
-  // gen-Qnew); P = U_new^{-T} H = X + (2 eta X S C^{-1} S)(H^T H).
-  GemmBatch b4{};
-  b4.d[0] = gemm_desc(d, d, m, c->Yw, d, 1, H, d, 1, c->UinvT, ldd, 1.f, c->UinvT, ldd, 1.f);
-  GemmDesc qd = gemm_desc(d, d, m, H, d, 1, c->Zq, d, 1, c->Q, ldd, 1.f, c->Q, ldd, 1.f);
-  qd.A2 = c->Zq;
-  qd.lda2 = d;
-  qd.B2 = H;
-  qd.ldb2 = d;
-  qd.K2 = m;
-  b4.d[1] = qd;
-  b4.d[2] = gemm_desc(m, d, m, c->N, m, 0, c->Yw, d, 1, c->P, d, 1.f, c->X, d, 1.f);
-  b4.n = 3;
   prof(c, LST_PHASE_UPDATE, true);
-  gemm_run(b4, c->flag, s, GEMM_UPDATE);
+  gemm(4, c->flag, s, GEMM_UPDATE);
   prof(c, LST_PHASE_UPDATE, false);
 
   // V_r -= eta sum dl/dA P_j over the slots of each distinct target row (eq. updateV).
@@ -618,8 +686,8 @@ int enqueue_factored_step(lst_ctx *c, hipStream_t s, const float *H, int32_t m, 
 }
 
 // Replays (capturing first if needed) the graph of a step with these arguments.
-int graph_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val,
-               int32_t K, float lr, float *loss_dev, float *grad_H) {
+int graph_step(lst_ctx *c, const PlanEntry &pl, const float *H, int32_t m, const int32_t *idx,
+               const float *val, int32_t K, float lr, float *loss_dev, float *grad_H) {
   uint32_t lr_bits;
   std::memcpy(&lr_bits, &lr, sizeof(lr_bits));
   GraphEntry *hit = nullptr;
@@ -639,7 +707,7 @@ int graph_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const 
       c->graphs.erase(c->graphs.begin() + v);
     }
     if (record(c, hipStreamBeginCapture(c->cap, hipStreamCaptureModeThreadLocal))) return LST_E_HIP;
-    const int st = enqueue_factored_step(c, c->cap, H, m, idx, val, K, lr, loss_dev, grad_H);
+    const int st = enqueue_factored_step(c, c->cap, pl, H, m, idx, val, K, lr, loss_dev, grad_H);
     hipGraph_t graph = nullptr;
     const hipError_t ec = hipStreamEndCapture(c->cap, &graph);
     if (st != LST_OK || ec != hipSuccess || !graph) {
@@ -669,9 +737,11 @@ int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const fl
   int st = step_args(c, H, m, idx, val, K, lr, loss_dev);
   if (st != LST_OK) return st;
   if (m == 0) return record(c, launch_fill(c->stream, loss_dev, 0.f));
+  const PlanEntry *pl = get_plan(c, m);
+  if (!pl) return LST_E_HIP;
   if (c->use_graphs && !c->prof_on)
-    return graph_step(c, H, m, idx, val, K, lr, loss_dev, grad_H);
-  return enqueue_factored_step(c, c->stream, H, m, idx, val, K, lr, loss_dev, grad_H);
+    return graph_step(c, *pl, H, m, idx, val, K, lr, loss_dev, grad_H);
+  return enqueue_factored_step(c, c->stream, *pl, H, m, idx, val, K, lr, loss_dev, grad_H);
 }
 
 int lst_use_graphs(lst_ctx *c, int32_t on) {

@@ -151,8 +151,14 @@ __device__ __forceinline__ int xcd_tile(int wg, int T) {
   return x < r ? x * (q + 1) + slot : r * (q + 1) + (x - r) * q + slot;
 }
 
+__device__ __forceinline__ const float *resolve(const float *p, const float *H, float *gH) {
+  const uintptr_t v = reinterpret_cast<uintptr_t>(p);
+  return v == 16 ? H : (v == 32 ? gH : p);
+}
+
 template <int NW>
-__device__ __forceinline__ void gemm_body(const GemmBatch &bt, const int *__restrict__ gate) {
+__device__ __forceinline__ void gemm_body(const GemmBatch &bt, const float *H, float *gH, float lr,
+                                          const int *__restrict__ gate) {
   // The gate only suppresses writes, so its load is waited for at the end.
   const int closed = gate ? *gate : 0;
   const int tile = xcd_tile(blockIdx.x, bt.total_tiles);
@@ -160,7 +166,17 @@ __device__ __forceinline__ void gemm_body(const GemmBatch &bt, const int *__rest
 #pragma unroll
   for (int q = 1; q < kMaxBatch; ++q)
     if (q < bt.n && tile >= bt.d[q].tile_begin) di = q;
-  const GemmDesc &g = bt.d[di];
+  GemmDesc g = bt.d[di];
+  g.A = resolve(g.A, H, gH);
+  g.B = resolve(g.B, H, gH);
+  g.A2 = resolve(g.A2, H, gH);
+  g.B2 = resolve(g.B2, H, gH);
+  g.Cin = resolve(g.Cin, H, gH);
+  g.C2 = const_cast<float *>(resolve(g.C2, H, gH));
+  if (g.lr_scaled) {
+    g.alpha *= lr * lr;
+    g.beta *= lr;
+  }
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -233,7 +249,15 @@ __device__ __forceinline__ void gemm_body(const GemmBatch &bt, const int *__rest
 // PHASE only names the instantiation, so profilers report each step phase separately.
 template <int PHASE, int NW>
 __global__ __launch_bounds__(64 * NW) void gemm_kernel(const GemmBatch bt, const int *__restrict__ gate) {
-  gemm_body<NW>(bt, gate);
+  gemm_body<NW>(bt, nullptr, nullptr, 1.f, gate);
+}
+
+// The batch read from device memory (a plan), with the step's H, grad_H and lr.
+template <int PHASE, int NW>
+__global__ __launch_bounds__(64 * NW) void gemm_plan_kernel(const GemmBatch *__restrict__ bt,
+                                                            const float *H, float *gH, float lr,
+                                                            const int *__restrict__ gate) {
+  gemm_body<NW>(*bt, H, gH, lr, gate);
 }
 
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const GemmDesc g, const int *__restrict__ gate) {
@@ -356,6 +380,36 @@ void gemm_enqueue(const GemmBatch &b, const int *gate, hipStream_t s, int phase)
       if (blocks > 2048) blocks = 2048;
       LST_LAUNCH(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, g, gate);
     }
+  }
+}
+
+void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float *H,
+                       float *gradH, float lr, const int *gate, hipStream_t s, int phase) {
+  const int total = host.total_tiles;
+  if (total == 0) return;
+  const bool wide = host.wide != 0;
+  switch (phase) {
+#define LST_PLAN_CASE(P)                                                                       \
+  case P:                                                                                      \
+    if (wide)                                                                                  \
+      LST_LAUNCH((gemm_plan_kernel<P, 8>), dim3(total), dim3(512), 0, s, dev, H, gradH, lr,     \
+                 gate);                                                                        \
+    else                                                                                       \
+      LST_LAUNCH((gemm_plan_kernel<P, 4>), dim3(total), dim3(256), 0, s, dev, H, gradH, lr,     \
+                 gate);                                                                        \
+    break;
+    LST_PLAN_CASE(GEMM_CONTRACT)
+    LST_PLAN_CASE(GEMM_ZGRAD)
+    LST_PLAN_CASE(GEMM_MID)
+    LST_PLAN_CASE(GEMM_UPDATE)
+#undef LST_PLAN_CASE
+    default:
+      if (wide)
+        LST_LAUNCH((gemm_plan_kernel<GEMM_OTHER, 8>), dim3(total), dim3(512), 0, s, dev, H, gradH,
+                   lr, gate);
+      else
+        LST_LAUNCH((gemm_plan_kernel<GEMM_OTHER, 4>), dim3(total), dim3(256), 0, s, dev, H, gradH,
+                   lr, gate);
   }
 }
 

@@ -66,7 +66,14 @@ struct GemmDesc {
   int kchunk;  // k per split (multiple of 8) when splits > 1
   int tiles_m, tiles_n;
   int tile_begin;
+  int lr_scaled;  // alpha *= lr^2 and beta *= lr at launch (plans shared across lr)
 };
+
+// Operand placeholders of plans kept in device memory: a plan is built once per
+// minibatch size m and refers to the step's H and grad_H through these values,
+// which the kernel replaces by the pointers passed at launch.
+inline const float *sym_H() { return reinterpret_cast<const float *>(uintptr_t{16}); }
+inline float *sym_gradH() { return reinterpret_cast<float *>(uintptr_t{32}); }
 
 constexpr int kMaxBatch = 4;
 
@@ -102,6 +109,13 @@ hipError_t gemm_launch(GemmBatch &b, const int *gate, hipStream_t s, int phase =
 // count); gemm_enqueue launches without checking for errors.
 int gemm_prepare(GemmBatch &b);
 void gemm_enqueue(const GemmBatch &b, const int *gate, hipStream_t s, int phase);
+
+// Launch of a prepared batch whose identical copy `dev` lives in device memory
+// (no split-k): the kernel reads its descriptors from there and takes H, grad_H
+// and lr for the placeholders, so the launch carries a few dozen bytes of
+// arguments instead of the whole batch.
+void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float *H,
+                       float *gradH, float lr, const int *gate, hipStream_t s, int phase);
 
 // Choose a split count for a long-k descriptor and attach its partial buffer.
 // Returns the number of floats the partial buffer needs.

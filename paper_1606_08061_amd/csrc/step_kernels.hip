@@ -179,42 +179,28 @@ constexpr int kTileSz = 32 * kTileLd;
 //   A' = X - f g^T,  X = A with column K replaced by e_K,
 //   f_i = A_iK (i != K), f_K = p - 1,   g_j = A_Kj / p (j != K), g_K = 1 / p,
 // i.e. A'_Kj = A_Kj / p, A'_iK = -A_iK / p, A'_KK = 1 / p, A'_ij = A_ij - A_iK A_Kj / p.
-// The block is symmetric on entry, so before step K column K is row K up to
-// sign (A_iK = A_Ki for i > K, -A_Ki for i < K) and only row K is exchanged.
-// Column K needs no separate case: there t_i = f_i (and t_K = p), so
-// A' = t - f (1 + 1/p) gives -f_i / p and 1 / p.  All pivots of a positive
-// definite C satisfy 0 < p <= 1 (C <= I), so that form loses nothing.
-//
-// Row K lives in register RK of lane-half HK.  The values on the serial path
-// from one step to the next -- p, row K at the lane's own column, and f for the
-// register that holds row K+1 -- are moved between lanes with readlane and
-// permlane32_swap; the other f values come from row K written to LDS
-// (rowx[K & 1][.]), whose latency the serial part of the step covers.  A bad
-// pivot sets `bad` and ends the elimination; the caller discards the block.
-// Orders LDS writes of some lanes of a wavefront before later LDS reads of other
-// lanes of the same wavefront (the hardware keeps one wavefront's LDS accesses in
-// order; the fence stops the compiler from moving a read above the write).
-__device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
-
+// Lane K + 32 h holds column K at exactly the rows lane-half h holds, so f is a
+// broadcast of that lane's registers within each half (ds_swizzle); p and row K
+// at the lane's own column come from readlane and permlane32_swap.  Column K
+// needs no separate case: there t_i = f_i (and t_K = p), so A' = t - f (1 + 1/p)
+// gives -f_i / p and 1 / p.  A bad pivot sets `bad` and ends the elimination;
+// the caller discards the block.
 __device__ __forceinline__ float lane_read(float v, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
+template <int L>
+__device__ __forceinline__ float half_broadcast(float v) {  // lane L of each 32-lane half
+  return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), L << 5));
+}
+
 template <int K>
-__device__ __forceinline__ void gj32_step(float (&t)[16], int j, int h, float *rowx, bool &bad) {
+__device__ __forceinline__ void gj32_step(float (&t)[16], int j, int h, bool &bad) {
   constexpr int HK = (K >> 2) & 1, RK = (K & 3) + 4 * (K >> 3);
-  const float rk = t[RK];  // row K at column j in lane-half HK
-  if (h == HK) rowx[(K & 1) * 32 + j] = rk;
-  wave_lds_sync();
-  float rv[16];  // row K at columns acc_row(h, r)
+  float f[16];  // column K at rows acc_row(h, r)
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const float4 v = *reinterpret_cast<const float4 *>(rowx + (K & 1) * 32 + 4 * h + 8 * q);
-    rv[4 * q] = v.x;
-    rv[4 * q + 1] = v.y;
-    rv[4 * q + 2] = v.z;
-    rv[4 * q + 3] = v.w;
-  }
+  for (int r = 0; r < 16; ++r) f[r] = half_broadcast<K>(t[r]);
+  const float rk = t[RK];  // row K at column j in lane-half HK
   const float p = lane_read(rk, K + 32 * HK);
   bad |= !(p > 0.f && p < INFINITY);
   if (bad) return;  // uniform; also splits the unrolled steps into separate blocks, which
@@ -225,40 +211,26 @@ __device__ __forceinline__ void gj32_step(float (&t)[16], int j, int h, float *r
                                                    false, false);
   const float rkj = __uint_as_float(HK ? sw[1] : sw[0]);  // row K at column j, both halves
   const float g = (j == K) ? 1.f + ip : rkj * ip;
-  constexpr int K1 = K + 1;
-  if constexpr (K1 < 32) {
-    // Register RK1 holds row K+1 in half HK1 and row K1o in the other half; their
-    // f values (row K at those columns) come from lanes of half HK directly.
-    constexpr int HK1 = (K1 >> 2) & 1, RK1 = (K1 & 3) + 4 * (K1 >> 3);
-    constexpr int K1o = HK1 ? K1 - 4 : K1 + 4;
-    const float f1 = lane_read(rk, K1 + 32 * HK);
-    const float r1o = lane_read(rk, K1o + 32 * HK);
-    const float f1o = (K1o == K) ? p - 1.f : ((K1o < K) ? -r1o : r1o);
-    t[RK1] = fmaf(-(h == HK1 ? f1 : f1o), g, t[RK1]);
-  }
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
-    if (K1 < 32 && r == ((K1 & 3) + 4 * (K1 >> 3))) continue;
-    const int i = acc_row(h, r);
-    const float f = (i == K) ? p - 1.f : ((i < K) ? -rv[r] : rv[r]);
-    t[r] = fmaf(-f, g, t[r]);
+    const float fr = (acc_row(h, r) == K) ? p - 1.f : f[r];
+    t[r] = fmaf(-fr, g, t[r]);
   }
 }
 
 template <int K>
-__device__ __forceinline__ void gj32_from(float (&t)[16], int j, int h, float *rowx, bool &bad) {
+__device__ __forceinline__ void gj32_from(float (&t)[16], int j, int h, bool &bad) {
   if constexpr (K < 32) {
-    gj32_step<K>(t, j, h, rowx, bad);
-    gj32_from<K + 1>(t, j, h, rowx, bad);
+    gj32_step<K>(t, j, h, bad);
+    gj32_from<K + 1>(t, j, h, bad);
   }
 }
 
-// Inverts the symmetric positive definite 32 x 32 block t (one wavefront,
-// accumulator layout) in place; false (uniformly) if some pivot is not
-// positive and finite.
-__device__ __forceinline__ bool gj32_invert(float (&t)[16], int j, int h, float *rowx) {
+// Inverts the 32 x 32 block t (one wavefront, accumulator layout) in place;
+// false (uniformly) if some pivot is not positive and finite.
+__device__ __forceinline__ bool gj32_invert(float (&t)[16], int j, int h) {
   bool bad = false;
-  gj32_from<0>(t, j, h, rowx, bad);
+  gj32_from<0>(t, j, h, bad);
   return !bad;
 }
 
@@ -331,7 +303,6 @@ struct alignas(16) GjLds {
   float rpan[NBK][kTileSz];     // P A_kb,j      (B operand)
   float pa[2][kTileSz];         // P             (A operand)
   float pb[2][kTileSz];         // P             (B operand)
-  float rowx[64];               // row exchange of the 32 x 32 inversions
   int bad;
 };
 
@@ -357,7 +328,7 @@ __device__ __forceinline__ bool blocked_gj(floatx16 (&acc)[TPW], GjLds<NBK> &sh,
         for (int s = 1; s < TPW; ++s) v = (s == sd) ? acc[s][r] : v;
         p[r] = v;
       }
-      if (gj32_invert(p, j, h, sh.rowx)) {
+      if (gj32_invert(p, j, h)) {
         floatx16 pv;
 #pragma unroll
         for (int r = 0; r < 16; ++r) pv[r] = p[r];
