@@ -198,6 +198,8 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="factored vs naive over the D x d sweep instead of the default line")
     ap.add_argument("--sweep-steps", type=int, default=20)
+    ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
+                    help="also run one plain device copy of MIB MiB (hardware-counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: the factored step is measured on one GPU's "
@@ -265,6 +267,16 @@ def main():
     roof = roofline_for(table)
     f.close()
     del f
+
+    if args.copy_calib:
+        # A copy of known size: its FETCH_SIZE / WRITE_SIZE counters scale the
+        # counters of the step's kernels to bytes.
+        src = torch.ones(args.copy_calib << 18, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ---- naive O(D d) path on the same batches ----
     naive = None

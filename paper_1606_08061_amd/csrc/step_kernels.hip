@@ -146,6 +146,122 @@ __global__ __launch_bounds__(kGatherThreads) void gather_kernel(
   }
 }
 
+// Register-resident variant for K <= 4 KPW and d <= 64 NV: wavefront w keeps the
+// target rows k = w, w + 4, ... (64 NV columns per row) in registers from the
+// dot products A_kj to the G sum, so V is read once and the index loads lead
+// straight into the row loads.  G_j is summed per wavefront, then over the four
+// wavefronts in a fixed order.
+template <int KPW, int NV>
+__global__ __launch_bounds__(kGatherThreads) void gather_reg_kernel(
+    int K, int d, int64_t D, const float *__restrict__ H, const float *__restrict__ Hhat,
+    const float *__restrict__ Htil, const int *__restrict__ idx, const float *__restrict__ val,
+    const float *__restrict__ V, int64_t ldv, int loss, float eps, float lr, float *__restrict__ G,
+    float *__restrict__ Atil, float *__restrict__ dq, float *__restrict__ dA,
+    float *__restrict__ lvec, int *__restrict__ flag) {
+  constexpr int W = kGatherThreads / 64;
+  __shared__ int sr[W * KPW];
+  __shared__ float sa[W * KPW], st[W * KPW], sg[W * KPW];
+  __shared__ float sred[W];
+  __shared__ float s_gq;
+  __shared__ int s_bad;
+  __shared__ float gpart[W][64 * NV];
+  const int j = blockIdx.x;
+  const int t = threadIdx.x, lane = t & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
+  if (t == 0) s_bad = 0;
+
+  // Target rows of this wavefront (uniform loads), then the rows themselves.
+  int r[KPW];
+  bool bad = false;
+#pragma unroll
+  for (int i = 0; i < KPW; ++i) {
+    const int k = wave + W * i;
+    int v = -1;
+    if (k < K) {
+      v = idx[(int64_t)j * K + k];
+      if (v < -1 || (int64_t)v >= D) {
+        bad = true;
+        v = -1;
+      }
+    }
+    r[i] = v;
+  }
+  float vr[KPW][NV];
+#pragma unroll
+  for (int i = 0; i < KPW; ++i) {
+    const float *row = V + (int64_t)max(r[i], 0) * ldv;
+#pragma unroll
+    for (int n = 0; n < NV; ++n) {
+      const int c = lane + 64 * n;
+      const float x = row[min(c, d - 1)];
+      vr[i][n] = (r[i] >= 0 && c < d) ? x : 0.f;
+    }
+  }
+  float ht[NV];
+  const float *htp = Htil + (int64_t)j * d;
+#pragma unroll
+  for (int n = 0; n < NV; ++n) {
+    const int c = lane + 64 * n;
+    ht[n] = (c < d) ? htp[c] : 0.f;
+  }
+  // q_j = h_j . H^_j over all threads
+  float qs = 0.f;
+  for (int c = t; c < d; c += kGatherThreads) qs += H[(int64_t)j * d + c] * Hhat[(int64_t)j * d + c];
+  qs = wave_sum(qs);
+  // A_kj = H~_j . V_r for this wavefront's rows
+  float a[KPW];
+#pragma unroll
+  for (int i = 0; i < KPW; ++i) {
+    float sacc = 0.f;
+#pragma unroll
+    for (int n = 0; n < NV; ++n) sacc += ht[n] * vr[i][n];
+    a[i] = wave_sum(sacc);
+  }
+  __syncthreads();  // s_bad initialised
+  if (lane == 0) {
+    sred[wave] = qs;
+#pragma unroll
+    for (int i = 0; i < KPW; ++i) {
+      const int k = wave + W * i;
+      if (k < K) {
+        sr[k] = r[i];
+        sa[k] = a[i];
+        st[k] = val[(int64_t)j * K + k];
+      }
+    }
+    if (bad) atomicOr(&s_bad, 1);
+  }
+  __syncthreads();
+  if (t == 0) {
+    if (s_bad) atomicOr(flag, FLAG_INDEX);
+    const float q = (sred[0] + sred[1]) + (sred[2] + sred[3]);
+    float l, gq;
+    loss_epilogue(loss, q, K, sr, st, sa, (float)D * eps, eps, l, gq, sg);
+    dq[j] = gq;
+    lvec[j] = l;
+    s_gq = gq;
+  }
+  __syncthreads();
+  for (int k = t; k < K; k += kGatherThreads) dA[(int64_t)j * K + k] = sg[k];
+  // G_j = sum_k dl/dA_kj V_r: this wavefront's rows, then the four partials in order
+#pragma unroll
+  for (int n = 0; n < NV; ++n) {
+    float g = 0.f;
+#pragma unroll
+    for (int i = 0; i < KPW; ++i) {
+      const int k = wave + W * i;
+      if (k < K) g += sg[k] * vr[i][n];
+    }
+    gpart[wave][lane + 64 * n] = g;
+  }
+  __syncthreads();
+  const float s2 = 2.f * lr * s_gq;
+  for (int c = t; c < d; c += kGatherThreads) {
+    G[(int64_t)j * d + c] = (gpart[0][c] + gpart[1][c]) + (gpart[2][c] + gpart[3][c]);
+    Atil[(int64_t)j * d + c] = s2 * htp[c];
+  }
+}
+
 constexpr int kMaxSortKeys = 8192;
 
 // ---------------------------------------------------------------------------
@@ -794,8 +910,21 @@ hipError_t launch_gather(hipStream_t s, int m, int K, int d, int64_t D, const fl
                          const float *Hhat, const float *Htil, const int *idx, const float *val,
                          const float *V, int64_t ldv, int loss, float eps, float lr, float *G,
                          float *Atil, float *dq, float *dA, float *lvec, int *flag) {
+  const int kpw = (K + 3) / 4;
+#define LST_GATHER_REG(KPW, NV)                                                               \
+  if (kpw <= KPW && d <= 64 * NV) {                                                           \
+    LST_LAUNCH((gather_reg_kernel<KPW, NV>), dim3(m), dim3(kGatherThreads), 0, s, K, d, D, H, \
+               Hhat, Htil, idx, val, V, ldv, loss, eps, lr, G, Atil, dq, dA, lvec, flag);     \
+    return hipSuccess;                                                                        \
+  }
+  LST_GATHER_REG(1, 8)
+  LST_GATHER_REG(2, 8)
+  LST_GATHER_REG(4, 8)
+  LST_GATHER_REG(1, 16)
+  LST_GATHER_REG(2, 16)
+#undef LST_GATHER_REG
   LST_LAUNCH(gather_kernel, dim3(m), dim3(kGatherThreads), 0, s, K, d, D, H, Hhat, Htil, idx, val, V,
-                     ldv, loss, eps, lr, G, Atil, dq, dA, lvec, flag);
+             ldv, loss, eps, lr, G, Atil, dq, dA, lvec, flag);
   return hipSuccess;  // checked once per step by the caller
 }
 
