@@ -78,6 +78,24 @@ def kernel_table(phases, work):
     return out
 
 
+def load_traffic():
+    """Per-launch HBM bytes measured by hardware counters (traffic.json, written by
+    paper_1606_08061_amd.traffic_from_pmc), per phase, kept only while the kernel's
+    source file is unchanged since the counters were taken."""
+    import hashlib
+
+    pkg = os.path.join(ROOT, "paper_1606_08061_amd")
+    path = os.path.join(pkg, "traffic.json")
+    if not os.path.exists(path):
+        return {}
+    out = {}
+    for phase, r in json.load(open(path)).get("phases", {}).items():
+        src = os.path.join(pkg, "csrc", r["source"])
+        if os.path.exists(src) and hashlib.sha256(open(src, "rb").read()).hexdigest() == r["source_sha256"]:
+            out[phase] = int(r["fetch_bytes"]) + int(r["write_bytes"])
+    return out
+
+
 def roofline_for(table, traffic=None):
     """The dominant kernel: the longest of the kernels a roofline applies to (the
     dense contractions and the sparse V passes).  The serial m x m inverse runs on
@@ -86,7 +104,7 @@ def roofline_for(table, traffic=None):
                key=lambda k: table[k]["avg_us"])
     r = table[name]
     return {"kernel_phase": name, "bound": r["bound"], "achieved": r["achieved"], "peak": r["peak"],
-            "unit": r["unit"], "frac": r["frac"], "traffic": traffic,
+            "unit": r["unit"], "frac": r["frac"], "traffic": (traffic or {}).get(name),
             "avg_launch_us": r["avg_us"], "algorithmic_per_launch": r["work_per_launch"]}
 
 
@@ -264,7 +282,11 @@ def main():
     f.check("profiled steps")
     work = phase_work(w, [b[1] for b in pool])
     table = kernel_table(phases, work)
-    roof = roofline_for(table)
+    traffic = load_traffic()
+    for k, v in traffic.items():
+        if k in table:
+            table[k]["traffic_bytes"] = v
+    roof = roofline_for(table, traffic)
     f.close()
     del f
 
