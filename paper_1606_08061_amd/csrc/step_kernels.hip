@@ -290,64 +290,94 @@ __device__ __forceinline__ int acc_row(int h, int r) { return 4 * h + (r & 3) + 
 constexpr int kTileLd = 36;  // LDS row stride (floats) of a staged 32 x 32 tile: 16-byte rows
 constexpr int kTileSz = 32 * kTileLd;
 
-// One scalar Gauss-Jordan step on pivot K of a 32 x 32 block held by one
-// wavefront in accumulator layout.  With p = A_KK the step is
+// One scalar Gauss-Jordan step on pivot K (p = A_KK) of a 32 x 32 block:
 //   A' = X - f g^T,  X = A with column K replaced by e_K,
 //   f_i = A_iK (i != K), f_K = p - 1,   g_j = A_Kj / p (j != K), g_K = 1 / p,
 // i.e. A'_Kj = A_Kj / p, A'_iK = -A_iK / p, A'_KK = 1 / p, A'_ij = A_ij - A_iK A_Kj / p.
-// Lane K + 32 h holds column K at exactly the rows lane-half h holds, so f is a
-// broadcast of that lane's registers within each half (ds_swizzle); p and row K
-// at the lane's own column come from readlane and permlane32_swap.  Column K
-// needs no separate case: there t_i = f_i (and t_K = p), so A' = t - f (1 + 1/p)
-// gives -f_i / p and 1 / p.  A bad pivot sets `bad` and ends the elimination;
-// the caller discards the block.
+// Column K needs no separate case: there t_i = f_i (and t_K = p), so
+// A' = t - f (1 + 1/p) gives -f_i / p and 1 / p.  A bad pivot sets `bad`; the
+// caller discards the block.
 __device__ __forceinline__ float lane_read(float v, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
 
-template <int L>
-__device__ __forceinline__ float half_broadcast(float v) {  // lane L of each 32-lane half
-  return __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), L << 5));
+// Orders LDS writes of some lanes of a wavefront before later LDS reads of other
+// lanes of the same wavefront (the hardware keeps one wavefront's LDS accesses in
+// order; the fence stops the compiler from moving a read above the write).
+__device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
+
+// The pivot-block inversion runs in the layout the cross-lane moves favour:
+// lane 16 q + c holds rows 8q .. 8q+7 of columns 2c and 2c+1, t[8e + r] = T[8q + r][2c + e].
+// Column K at the lane's rows sits in lane c = K/2 of the lane's own 16-lane row
+// (DPP row_newbcast); row K at the lane's columns sits in 16-lane row K/8 (two
+// permlane swaps broadcast it to all four rows); the pivot comes from readlane.
+// No LDS round trip is on the serial path.
+template <int N>
+__device__ __forceinline__ float row_newbcast(float v) {  // lane N of each 16-lane row
+  return __int_as_float(
+      __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x150 + N, 0xF, 0xF, false));
+}
+
+template <int Q>
+__device__ __forceinline__ float row16_broadcast(float v) {  // 16-lane row Q to all four rows
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false,
+                                                  false);
+  const unsigned y = (Q >> 1) ? a[1] : a[0];  // rows (2(Q>>1), 2(Q>>1)+1) in both halves
+  const auto b = __builtin_amdgcn_permlane16_swap(y, y, false, false);
+  return __uint_as_float((Q & 1) ? b[1] : b[0]);
 }
 
 template <int K>
-__device__ __forceinline__ void gj32_step(float (&t)[16], int j, int h, bool &bad) {
-  constexpr int HK = (K >> 2) & 1, RK = (K & 3) + 4 * (K >> 3);
-  float f[16];  // column K at rows acc_row(h, r)
+__device__ __forceinline__ void gjr_step(float (&t)[16], int q, int c, bool &bad) {
+  constexpr int QK = K >> 3, RK = K & 7, CK = K >> 1, EK = K & 1;
+  const float p = lane_read(t[8 * EK + RK], 16 * QK + CK);
+  bad |= !(p > 0.f && p < INFINITY);  // checked once after the 32 steps
+  float f[8];                          // column K at rows 8q + r
 #pragma unroll
-  for (int r = 0; r < 16; ++r) f[r] = half_broadcast<K>(t[r]);
-  const float rk = t[RK];  // row K at column j in lane-half HK
-  const float p = lane_read(rk, K + 32 * HK);
-  bad |= !(p > 0.f && p < INFINITY);
-  if (bad) return;  // uniform; also splits the unrolled steps into separate blocks, which
-                    // keeps the compiler from hoisting (and holding) later steps' values
+  for (int r = 0; r < 8; ++r) f[r] = row_newbcast<CK>(t[8 * EK + r]);
+  float rw[2];  // row K at columns 2c + e
+#pragma unroll
+  for (int e = 0; e < 2; ++e) rw[e] = row16_broadcast<QK>(t[8 * e + RK]);
   float ip = __builtin_amdgcn_rcpf(p);
   ip = fmaf(ip, fmaf(-p, ip, 1.f), ip);  // one Newton step on the hardware reciprocal
-  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(rk), __float_as_uint(rk),
-                                                   false, false);
-  const float rkj = __uint_as_float(HK ? sw[1] : sw[0]);  // row K at column j, both halves
-  const float g = (j == K) ? 1.f + ip : rkj * ip;
+  float g[2];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
-    const float fr = (acc_row(h, r) == K) ? p - 1.f : f[r];
-    t[r] = fmaf(-fr, g, t[r]);
-  }
+  for (int e = 0; e < 2; ++e) g[e] = (e == EK && c == CK) ? 1.f + ip : rw[e] * ip;
+#pragma unroll
+  for (int e = 0; e < 2; ++e)
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const float fr = (r == RK && q == QK) ? p - 1.f : f[r];
+      t[8 * e + r] = fmaf(-fr, g[e], t[8 * e + r]);
+    }
 }
 
 template <int K>
-__device__ __forceinline__ void gj32_from(float (&t)[16], int j, int h, bool &bad) {
+__device__ __forceinline__ void gjr_from(float (&t)[16], int q, int c, bool &bad) {
   if constexpr (K < 32) {
-    gj32_step<K>(t, j, h, bad);
-    gj32_from<K + 1>(t, j, h, bad);
+    gjr_step<K>(t, q, c, bad);
+    gjr_from<K + 1>(t, q, c, bad);
   }
 }
 
-// Inverts the 32 x 32 block t (one wavefront, accumulator layout) in place;
-// false (uniformly) if some pivot is not positive and finite.
-__device__ __forceinline__ bool gj32_invert(float (&t)[16], int j, int h) {
+// Inverts the 32 x 32 block staged row-major (stride kTileLd) in `tile` by one
+// wavefront and leaves the inverse there; false (uniformly) on a bad pivot.
+__device__ __forceinline__ bool gj32_invert_staged(float *tile, int lane) {
+  const int q = lane >> 4, c = lane & 15;
+  float t[16];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const float2 v = *reinterpret_cast<const float2 *>(tile + (8 * q + r) * kTileLd + 2 * c);
+    t[r] = v.x;
+    t[8 + r] = v.y;
+  }
   bool bad = false;
-  gj32_from<0>(t, j, h, bad);
-  return !bad;
+  gjr_from<0>(t, q, c, bad);
+  if (bad) return false;
+#pragma unroll
+  for (int r = 0; r < 8; ++r)
+    *reinterpret_cast<float2 *>(tile + (8 * q + r) * kTileLd + 2 * c) = make_float2(t[r], t[8 + r]);
+  return true;
 }
 
 // Operand fetch of a staged tile: lane (i or j, h) reads its 16 values at
@@ -444,14 +474,18 @@ __device__ __forceinline__ bool blocked_gj(floatx16 (&acc)[TPW], GjLds<NBK> &sh,
         for (int s = 1; s < TPW; ++s) v = (s == sd) ? acc[s][r] : v;
         p[r] = v;
       }
-      if (gj32_invert(p, j, h)) {
-        floatx16 pv;
+      floatx16 pv;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) pv[r] = p[r];
+      for (int r = 0; r < 16; ++r) pv[r] = p[r];
+      stage_a(sh.pa[buf], pv, j, h);  // the pivot block, row-major
+      wave_lds_sync();
+      if (gj32_invert_staged(sh.pa[buf], lane)) {  // P replaces it (A-operand layout)
+        wave_lds_sync();
+#pragma unroll
+        for (int r = 0; r < 16; ++r) pv[r] = sh.pa[buf][acc_row(h, r) * kTileLd + j];
 #pragma unroll
         for (int s = 0; s < TPW; ++s)
           if (s == sd) acc[s] = pv;
-        stage_a(sh.pa[buf], pv, j, h);
         stage_b(sh.pb[buf], pv, j, h);
       } else if (lane == 0) {
         sh.bad = 1;
