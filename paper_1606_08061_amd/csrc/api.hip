@@ -568,7 +568,13 @@ void build_plan(const lst_ctx *c, int m, GemmBatch (&b)[kPlanBatches]) {
   b[4].d[1] = qd;
   b[4].d[2] = gemm_desc(m, d, m, c->N, m, 0, c->Yw, d, 1, c->P, d, 1.f, c->X, d, 1.f);
   b[4].n = 3;
-  for (GemmBatch &x : b) gemm_prepare(x);
+  // 16 x 16 tiles where the outputs are m x m or m x d with long k (Gram product,
+  // contractions, Z^): four times the workgroups of 32 x 32 tiles.  The d x d
+  // updates (short k = m, read-modify-write of the state) keep 32 x 32 tiles.
+  for (int i = 0; i < kPlanBatches; ++i) {
+    b[i].t16 = i <= 2 ? 1 : 0;
+    gemm_prepare(b[i]);
+  }
 }
 
 // The plan for m, built and copied to its device slot on first use.  Replacing

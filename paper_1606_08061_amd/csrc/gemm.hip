@@ -272,6 +272,123 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const GemmDesc g, co
   }
 }
 
+// ---------------------------------------------------------------------------
+// 16 x 16 output tiles (v_mfma_f32_16x16x4f32) for the step's plans: four times
+// the workgroups of the 32 x 32 form on these small products, and each
+// wavefront's share of k loaded in one round.  Lane l = c + 16 g supplies
+// A[i = c][k] and B[k][j = c] for k = kb + 4g + s in instruction s of a k-block
+// of 16 (four consecutive k of its row: one 16-byte load when k is contiguous);
+// accumulator register r holds C[4g + r][c].  The four wavefronts take the
+// k-blocks w, w + 4, ...; their sums are added through LDS in a fixed order.
+// ---------------------------------------------------------------------------
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kT16Group = 8;  // k-blocks of 16 loaded per round
+
+template <int AM, int BM>
+__device__ __forceinline__ void kloop16(floatx4 &acc, const float *A, int64_t asi, int64_t ask,
+                                        const float *B, int64_t bsi, int64_t bsk, int ia, int jb,
+                                        int K, int wave, int g) {
+  const int nfull = K >> 4;
+  const int nw = nfull > wave ? (nfull - wave + 3) / 4 : 0;
+  for (int b0 = 0; b0 < nw; b0 += kT16Group) {
+    float a[kT16Group][4], b[kT16Group][4];
+#pragma unroll
+    for (int u = 0; u < kT16Group; ++u) {
+      const int kb = 16 * (wave + 4 * min(b0 + u, nw - 1)) + 4 * g;
+      ld4<AM>(A, asi, ask, ia, kb, a[u]);
+      ld4<BM>(B, bsi, bsk, jb, kb, b[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < kT16Group; ++u)
+      if (b0 + u < nw) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][s], b[u][s], acc, 0, 0, 0);
+      }
+  }
+  if ((K & 15) && wave == 3) {
+    const int k0 = 16 * nfull + 4 * g;
+    float a[4], b[4];
+    ld4_tail(A, asi, ask, ia, k0, K, a);
+    ld4_tail(B, bsi, bsk, jb, k0, K, b);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s], acc, 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void segment16(floatx4 &acc, const float *A, int64_t lda, int tA,
+                                          const float *B, int64_t ldb, int tB, int ia, int jb,
+                                          int K, int wave, int g) {
+  const int64_t asi = tA ? 1 : lda, ask = tA ? lda : 1;
+  const int64_t bsi = tB ? 1 : ldb, bsk = tB ? ldb : 1;
+  const bool av = !tA && vec_ok(A, lda);
+  const bool bv = !tB && vec_ok(B, ldb);
+  if (av && bv)
+    kloop16<VEC, VEC>(acc, A, asi, ask, B, bsi, bsk, ia, jb, K, wave, g);
+  else if (av)
+    kloop16<VEC, STRIDED>(acc, A, asi, ask, B, bsi, bsk, ia, jb, K, wave, g);
+  else if (bv)
+    kloop16<STRIDED, VEC>(acc, A, asi, ask, B, bsi, bsk, ia, jb, K, wave, g);
+  else
+    kloop16<STRIDED, STRIDED>(acc, A, asi, ask, B, bsi, bsk, ia, jb, K, wave, g);
+}
+
+// One 16 x 16 tile per workgroup of 256 threads; thread t finishes output
+// (4 (t / 16 % 4) + ..., see below) after the reduction.  No split-k.
+template <int PHASE>
+__global__ __launch_bounds__(256) void gemm16_plan_kernel(const GemmBatch *__restrict__ bt,
+                                                           const float *H, float *gH, float lr,
+                                                           const int *__restrict__ gate) {
+  const int closed = gate ? *gate : 0;  // waited for at the end: it only suppresses writes
+  const int tile = xcd_tile(blockIdx.x, bt->total_tiles);
+  int di = 0;
+#pragma unroll
+  for (int q = 1; q < kMaxBatch; ++q)
+    if (q < bt->n && tile >= bt->d[q].tile_begin) di = q;
+  GemmDesc g = bt->d[di];
+  g.A = resolve(g.A, H, gH);
+  g.B = resolve(g.B, H, gH);
+  g.A2 = resolve(g.A2, H, gH);
+  g.B2 = resolve(g.B2, H, gH);
+  g.Cin = resolve(g.Cin, H, gH);
+  g.C2 = const_cast<float *>(resolve(g.C2, H, gH));
+  if (g.lr_scaled) {
+    g.alpha *= lr * lr;
+    g.beta *= lr;
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = lane & 15, lg = lane >> 4;
+  const int local = tile - g.tile_begin;
+  const int tm = local / g.tiles_n, tn = local - tm * g.tiles_n;
+  const int i0 = tm * 16, j0 = tn * 16;
+  const int ia = min(i0 + c, g.M - 1), jb = min(j0 + c, g.N - 1);
+
+  // Output of thread t after the reduction: accumulator register r = wave of
+  // lane lane: row 4 lg + wave, column c (each wavefront finishes one register).
+  const int oi = i0 + 4 * lg + wave, oj = j0 + c;
+  const int ci = min(oi, g.M - 1), cj = min(oj, g.N - 1);
+  const bool use_e = g.epi == EPI_GRADH;
+  const float cin = g.Cin ? g.Cin[(int64_t)ci * g.ldcin + cj] : 0.f;
+  const float ein = use_e ? g.E[(int64_t)ci * g.lde + cj] : 0.f;
+
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  segment16(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, ia, jb, g.K, wave, lg);
+  if (g.K2 > 0) segment16(acc, g.A2, g.lda2, g.tA, g.B2, g.ldb2, g.tB, ia, jb, g.K2, wave, lg);
+
+  __shared__ float red[4][4][64];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) red[wave][r][lane] = acc[r];
+  __syncthreads();
+  if (closed) return;  // after the last barrier
+  const float v = (red[0][wave][lane] + red[1][wave][lane]) + (red[2][wave][lane] + red[3][wave][lane]);
+  if (oi < g.M && oj < g.N) {
+    const float out = g.alpha * v + g.beta * cin;
+    g.C[(int64_t)oi * g.ldc + oj] = out;
+    if (use_e) g.C2[(int64_t)oi * g.ldc2 + oj] = 2.f * g.rs[oi] * ein + out;
+  }
+}
+
 template <int P, int NW>
 void launch_phase(int total, hipStream_t s, const GemmBatch &b, const int *gate) {
   LST_LAUNCH((gemm_kernel<P, NW>), dim3(total), dim3(64 * NW), 0, s, b, gate);
@@ -327,10 +444,11 @@ size_t gemm_plan_split(GemmDesc &g, int target_wgs, float *partial) {
 int gemm_prepare(GemmBatch &b) {
   int total = 0;
   int kmax = 0;
+  const int ts = b.t16 ? 16 : 32;
   for (int q = 0; q < b.n; ++q) {
     GemmDesc &g = b.d[q];
-    g.tiles_m = (g.M + 31) / 32;
-    g.tiles_n = (g.N + 31) / 32;
+    g.tiles_m = (g.M + ts - 1) / ts;
+    g.tiles_n = (g.N + ts - 1) / ts;
     g.tile_begin = total;
     if (g.M > 0 && g.N > 0) {
       total += g.tiles_m * g.tiles_n * (g.splits > 1 ? g.splits : 1);
@@ -387,6 +505,23 @@ void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float 
                        float *gradH, float lr, const int *gate, hipStream_t s, int phase) {
   const int total = host.total_tiles;
   if (total == 0) return;
+  if (host.t16) {
+    switch (phase) {
+#define LST_PLAN16_CASE(P)                                                                      \
+  case P:                                                                                       \
+    LST_LAUNCH((gemm16_plan_kernel<P>), dim3(total), dim3(256), 0, s, dev, H, gradH, lr, gate); \
+    break;
+      LST_PLAN16_CASE(GEMM_CONTRACT)
+      LST_PLAN16_CASE(GEMM_ZGRAD)
+      LST_PLAN16_CASE(GEMM_MID)
+      LST_PLAN16_CASE(GEMM_UPDATE)
+#undef LST_PLAN16_CASE
+      default:
+        LST_LAUNCH((gemm16_plan_kernel<GEMM_OTHER>), dim3(total), dim3(256), 0, s, dev, H, gradH,
+                   lr, gate);
+    }
+    return;
+  }
   const bool wide = host.wide != 0;
   switch (phase) {
 #define LST_PLAN_CASE(P)                                                                       \

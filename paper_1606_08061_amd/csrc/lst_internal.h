@@ -82,6 +82,7 @@ struct GemmBatch {
   int n;
   int total_tiles;
   int wide;  // 8 wavefronts per tile (long k) instead of 4
+  int t16;   // 16 x 16 output tiles (plans): set before gemm_prepare
 };
 
 GemmDesc gemm_desc(int M, int N, int K, const float *A, int64_t lda, int tA, const float *B,
