@@ -575,6 +575,14 @@ void build_plan(const lst_ctx *c, int m, GemmBatch (&b)[kPlanBatches]) {
     b[i].t16 = i <= 2 ? 1 : 0;
     gemm_prepare(b[i]);
   }
+  // The contraction launch also reads the step's target rows of V into the caches
+  // (one workgroup per example, on the XCD of that example's gather workgroup).
+  b[1].pf_V = c->V;
+  b[1].pf_D = c->D;
+  b[1].pf_ldv = c->ldv;
+  b[1].pf_d = d;
+  b[1].pf_m = m;
+  b[1].pf_base = (b[1].total_tiles + 7) / 8 * 8;
 }
 
 // The plan for m, built and copied to its device slot on first use.  Replacing
@@ -624,7 +632,8 @@ int enqueue_factored_step(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const 
   const int d = c->d;
   float *gH = grad_H ? grad_H : c->gradH;
   auto gemm = [&](int i, const int *gate, hipStream_t st, int phase) {
-    gemm_enqueue_plan(pl.b[i], pl.dev + i, H, gH, lr, gate, st, phase);
+    gemm_enqueue_plan(pl.b[i], pl.dev + i, H, gH, lr, gate, st, phase, i == 1 ? idx : nullptr,
+                      K);
   };
 
   hipStream_t s_wood = c->side[0];

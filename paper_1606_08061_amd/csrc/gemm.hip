@@ -339,7 +339,23 @@ __device__ __forceinline__ void segment16(floatx4 &acc, const float *A, int64_t 
 template <int PHASE>
 __global__ __launch_bounds__(256) void gemm16_plan_kernel(const GemmBatch *__restrict__ bt,
                                                            const float *H, float *gH, float lr,
-                                                           const int *__restrict__ gate) {
+                                                           const int *__restrict__ gate,
+                                                           const int *__restrict__ pf_idx,
+                                                           int pf_K) {
+  if ((int)blockIdx.x >= bt->total_tiles) {
+    // Prefetch workgroup: the target rows of example j (indices outside [0, D) skipped).
+    const int j = (int)blockIdx.x - bt->pf_base;
+    if (j < 0 || j >= bt->pf_m) return;
+    float sink = 0.f;
+    for (int k = 0; k < pf_K; ++k) {
+      const int r = pf_idx[(int64_t)j * pf_K + k];
+      if (r < 0 || (int64_t)r >= bt->pf_D) continue;
+      const float *row = bt->pf_V + (int64_t)r * bt->pf_ldv;
+      for (int c = threadIdx.x; c < bt->pf_d; c += 256) sink += row[c];
+    }
+    asm volatile("" ::"v"(sink));
+    return;
+  }
   const int closed = gate ? *gate : 0;  // waited for at the end: it only suppresses writes
   const int tile = xcd_tile(blockIdx.x, bt->total_tiles);
   int di = 0;
@@ -502,14 +518,17 @@ void gemm_enqueue(const GemmBatch &b, const int *gate, hipStream_t s, int phase)
 }
 
 void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float *H,
-                       float *gradH, float lr, const int *gate, hipStream_t s, int phase) {
+                       float *gradH, float lr, const int *gate, hipStream_t s, int phase,
+                       const int *pf_idx, int pf_K) {
   const int total = host.total_tiles;
   if (total == 0) return;
   if (host.t16) {
+    const int grid = (pf_idx && host.pf_m > 0) ? host.pf_base + host.pf_m : total;
     switch (phase) {
-#define LST_PLAN16_CASE(P)                                                                      \
-  case P:                                                                                       \
-    LST_LAUNCH((gemm16_plan_kernel<P>), dim3(total), dim3(256), 0, s, dev, H, gradH, lr, gate); \
+#define LST_PLAN16_CASE(P)                                                                     \
+  case P:                                                                                      \
+    LST_LAUNCH((gemm16_plan_kernel<P>), dim3(grid), dim3(256), 0, s, dev, H, gradH, lr, gate, \
+               pf_idx, pf_K);                                                                  \
     break;
       LST_PLAN16_CASE(GEMM_CONTRACT)
       LST_PLAN16_CASE(GEMM_ZGRAD)
@@ -517,8 +536,8 @@ void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float 
       LST_PLAN16_CASE(GEMM_UPDATE)
 #undef LST_PLAN16_CASE
       default:
-        LST_LAUNCH((gemm16_plan_kernel<GEMM_OTHER>), dim3(total), dim3(256), 0, s, dev, H, gradH,
-                   lr, gate);
+        LST_LAUNCH((gemm16_plan_kernel<GEMM_OTHER>), dim3(grid), dim3(256), 0, s, dev, H, gradH,
+                   lr, gate, pf_idx, pf_K);
     }
     return;
   }

@@ -83,6 +83,13 @@ struct GemmBatch {
   int total_tiles;
   int wide;  // 8 wavefronts per tile (long k) instead of 4
   int t16;   // 16 x 16 output tiles (plans): set before gemm_prepare
+  // Optional prefetch (16 x 16 plans): pf_m extra workgroups after the tiles
+  // (whose count is padded to pf_base, a multiple of 8, so that workgroup
+  // pf_base + j shares an XCD with workgroup j of the next launch) read the K
+  // target rows of example j of V (D x ldv) into the caches.
+  const float *pf_V;
+  int64_t pf_D, pf_ldv;
+  int pf_m, pf_d, pf_base;
 };
 
 GemmDesc gemm_desc(int M, int N, int K, const float *A, int64_t lda, int tA, const float *B,
@@ -116,7 +123,8 @@ void gemm_enqueue(const GemmBatch &b, const int *gate, hipStream_t s, int phase)
 // and lr for the placeholders, so the launch carries a few dozen bytes of
 // arguments instead of the whole batch.
 void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float *H,
-                       float *gradH, float lr, const int *gate, hipStream_t s, int phase);
+                       float *gradH, float lr, const int *gate, hipStream_t s, int phase,
+                       const int *pf_idx = nullptr, int pf_K = 0);
 
 // Choose a split count for a long-k descriptor and attach its partial buffer.
 // Returns the number of floats the partial buffer needs.

@@ -67,6 +67,44 @@ __device__ __forceinline__ void loss_epilogue(int loss, float q, int K, const in
   }
 }
 
+// The same epilogue on register arrays (K <= KMAX slots, fully unrolled), so the
+// serial part of a gather workgroup does no dependent LDS reads.
+template <int KMAX>
+__device__ __forceinline__ void loss_epilogue_reg(int loss, float q, int K, const int (&r)[KMAX],
+                                                  const float (&t)[KMAX], const float (&a)[KMAX],
+                                                  float Deps, float eps, float &l, float &gq,
+                                                  float (&g)[KMAX]) {
+  l = 0.f;
+  gq = 0.f;
+  if (loss == LST_LOSS_SQUARED) {
+    float at = 0.f, yy = 0.f;
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      const bool ok = k < K && r[k] >= 0;
+      g[k] = ok ? -2.f * t[k] : 0.f;
+      if (!ok) continue;
+      at += t[k] * a[k];
+#pragma unroll
+      for (int kk = 0; kk < KMAX; ++kk)
+        if (kk < K && r[kk] == r[k]) yy += t[k] * t[kk];
+    }
+    l = q - 2.f * at + yy;
+    gq = 1.f;
+  } else {
+    const float z = q + Deps;
+    const float lz = logf(z);
+#pragma unroll
+    for (int k = 0; k < KMAX; ++k) {
+      g[k] = 0.f;
+      if (k >= K || r[k] < 0) continue;
+      const float den = a[k] * a[k] + eps;
+      l += t[k] * (lz - logf(den));
+      gq += t[k] / z;
+      g[k] = -2.f * t[k] * a[k] / den;
+    }
+  }
+}
+
 constexpr int kGatherThreads = 256;
 
 // One workgroup (four wavefronts) per example j.  The K row dot products
@@ -235,8 +273,20 @@ __global__ __launch_bounds__(kGatherThreads) void gather_reg_kernel(
   if (t == 0) {
     if (s_bad) atomicOr(flag, FLAG_INDEX);
     const float q = (sred[0] + sred[1]) + (sred[2] + sred[3]);
+    constexpr int KM = W * KPW;
+    int rr[KM];
+    float tt[KM], aa[KM], gg[KM];
+#pragma unroll
+    for (int k = 0; k < KM; ++k) {
+      rr[k] = k < K ? sr[k] : -1;
+      tt[k] = k < K ? st[k] : 0.f;
+      aa[k] = k < K ? sa[k] : 0.f;
+    }
     float l, gq;
-    loss_epilogue(loss, q, K, sr, st, sa, (float)D * eps, eps, l, gq, sg);
+    loss_epilogue_reg<KM>(loss, q, K, rr, tt, aa, (float)D * eps, eps, l, gq, gg);
+#pragma unroll
+    for (int k = 0; k < KM; ++k)
+      if (k < K) sg[k] = gg[k];
     dq[j] = gq;
     lvec[j] = l;
     s_gq = gq;
