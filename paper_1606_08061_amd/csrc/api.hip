@@ -229,7 +229,9 @@ int side_create(lst_ctx *c) {
   if (hipStreamCreateWithFlags(&c->cap, hipStreamNonBlocking) != hipSuccess) return LST_E_HIP;
   hipEvent_t *evs[3] = {&c->ev_fork, &c->ev_wood_ready, &c->ev_wood_done};
   for (hipEvent_t *e : evs)
-    if (hipEventCreateWithFlags(e, hipEventDisableTiming) != hipSuccess) return LST_E_HIP;
+    // device-scope release: only kernels on this device consume the fork/join events
+    if (hipEventCreateWithFlags(e, hipEventDisableTiming | hipEventReleaseToDevice) != hipSuccess)
+      return LST_E_HIP;
   c->have_side = true;
   return LST_OK;
 }
