@@ -138,19 +138,39 @@ void carve_factored(lst_ctx *c, Carver &cv) {
 
 // Upper bound of the split-k partial buffer of grad_H = grad_O^T W for any m <= m_max:
 // gemm_plan_split keeps splits <= ceil(kTargetWGs / tiles), and m * d <= tiles * 1024.
+// The 128 x 128-tile kernel's bound is the same with 128^2 floats per tile.
 size_t naive_split_floats(const lst_ctx *c) {
   const size_t tiles = (size_t)((c->m_max + 31) / 32) * ((c->d + 31) / 32);
-  return (kTargetWGs + tiles) * 1024;
+  const size_t tiles128 = (size_t)((c->m_max + 127) / 128) * ((c->d + 127) / 128);
+  const size_t a = (kTargetWGs + tiles) * 1024, b = (kTargetWGs + tiles128) * 16384;
+  return a > b ? a : b;
+}
+
+// One naive-path product: the 128 x 128-tile kernel when the operands allow it,
+// else the general one.  split: spread k over workgroups (grad_H's k = D).
+hipError_t naive_gemm(lst_ctx *c, GemmDesc g, bool split, const int *gate, hipStream_t s,
+                      int phase) {
+  if (gemm_big_ok(g)) {
+    gemm_big_plan(g, kTargetWGs, split ? naive_split_floats(c) : 0, split ? c->splitpart : nullptr);
+    return gemm_big_launch(g, gate, s, phase);
+  }
+  if (split) gemm_plan_split(g, kTargetWGs, c->splitpart);
+  GemmBatch b{};
+  b.d[0] = g;
+  b.n = 1;
+  return gemm_launch(b, gate, s, phase);
 }
 
 void carve_naive(lst_ctx *c, Carver &cv) {
   const size_t md = (size_t)c->m_max * c->d;
   const size_t mk = (size_t)c->m_max * (c->K_max > 0 ? c->K_max : 1);
   c->O = cv.take<float>((size_t)c->D * c->m_max);
-  c->colpart = cv.take<float>((size_t)kColnormBlocks * c->m_max);
+  const size_t parts128 = (size_t)kBigColsqRows * ((c->D + 127) / 128);
+  c->colpart = cv.take<float>((parts128 > kColnormBlocks ? parts128 : kColnormBlocks) * c->m_max);
   c->splitpart = cv.take<float>(naive_split_floats(c));
   c->gradH = cv.take<float>(md);
   c->dq = cv.take<float>(c->m_max);
+  c->lvec = cv.take<float>(c->m_max);
   c->dA = cv.take<float>(mk);
   c->flag = cv.take<int>(1);
 }
@@ -793,35 +813,43 @@ int lst_naive_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, co
   const int d = c->d;
   const int64_t D = c->D;
   float *gH = grad_H ? grad_H : c->gradH;
-  // O = W H^T  (D x m), the O(D d) forward product of section 2.3.
-  GemmBatch b1{};
-  b1.d[0] = gemm_desc((int)D, m, d, c->W, c->ldw, 0, H, d, 0, c->O, m);
-  b1.n = 1;
+  // O = W H^T  (D x m), the O(D d) forward product of section 2.3, with the
+  // partial column sums of squares for q_j = ||o_j||^2 when the tiled kernel runs.
   prof(c, LST_PHASE_NAIVE_FWD, true);
-  if (record(c, gemm_launch(b1, nullptr, s, GEMM_NAIVE_FWD))) return LST_E_HIP;
+  GemmDesc fwd = gemm_desc((int)D, m, d, c->W, c->ldw, 0, H, d, 0, c->O, m);
+  int nparts = kColnormBlocks;
+  if (gemm_big_ok(fwd)) {
+    fwd.colsq = c->colpart;
+    gemm_big_plan(fwd, kTargetWGs, 0, nullptr);
+    nparts = kBigColsqRows * fwd.tiles_m;
+    if (record(c, gemm_big_launch(fwd, nullptr, s, GEMM_NAIVE_FWD))) return LST_E_HIP;
+  } else {
+    if (record(c, naive_gemm(c, fwd, false, nullptr, s, GEMM_NAIVE_FWD)) ||
+        record(c, launch_colnorm(s, c->O, D, m, c->colpart, kColnormBlocks)))
+      return LST_E_HIP;
+  }
   prof(c, LST_PHASE_NAIVE_FWD, false);
-  // q_j = ||o_j||^2 over all D outputs, the loss and dl/dq, dl/da from the explicit O.
+  // The loss and dl/dq, dl/da from the explicit O.
   prof(c, LST_PHASE_NAIVE_LOSS, true);
-  if (record(c, launch_colnorm(s, c->O, D, m, c->colpart, kColnormBlocks)) ||
-      record(c, launch_naive_epilogue(s, m, K, D, kColnormBlocks, c->colpart, c->O, idx, val,
-                                      c->loss, c->eps, c->dq, c->dA, loss_dev, c->flag)))
+  if (record(c, launch_naive_epilogue(s, m, K, D, nparts, c->colpart, c->O, idx, val, c->loss,
+                                      c->eps, c->dq, c->dA, c->lvec, c->flag)))
     return LST_E_HIP;
   // grad_O = 2 O diag(dl/dq) + Yring, in place over O.
-  if (record(c, launch_grad_o(s, c->O, D, m, K, c->dq, idx, c->dA))) return LST_E_HIP;
+  if (record(c, launch_grad_o(s, c->O, D, m, K, c->dq, idx, c->dA, c->lvec, loss_dev, c->flag)))
+    return LST_E_HIP;
   prof(c, LST_PHASE_NAIVE_LOSS, false);
   // grad_H = grad_O^T W (split over D), then W <- W - eta grad_O H.
-  GemmBatch b2{};
-  b2.d[0] = gemm_desc(m, d, (int)D, c->O, m, 1, c->W, c->ldw, 1, gH, d);
-  gemm_plan_split(b2.d[0], kTargetWGs, c->splitpart);
-  b2.n = 1;
   prof(c, LST_PHASE_NAIVE_GRAD, true);
-  if (record(c, gemm_launch(b2, nullptr, s, GEMM_NAIVE_GRAD))) return LST_E_HIP;
+  if (record(c, naive_gemm(c, gemm_desc(m, d, (int)D, c->O, m, 1, c->W, c->ldw, 1, gH, d), true,
+                           nullptr, s, GEMM_NAIVE_GRAD)))
+    return LST_E_HIP;
   prof(c, LST_PHASE_NAIVE_GRAD, false);
-  GemmBatch b3{};
-  b3.d[0] = gemm_desc((int)D, d, m, c->O, m, 0, H, d, 1, c->W, c->ldw, -lr, c->W, c->ldw, 1.f);
-  b3.n = 1;
   prof(c, LST_PHASE_NAIVE_UPDATE, true);
-  if (record(c, gemm_launch(b3, c->flag, s, GEMM_NAIVE_UPDATE))) return LST_E_HIP;
+  if (record(c, naive_gemm(c,
+                           gemm_desc((int)D, d, m, c->O, m, 0, H, d, 1, c->W, c->ldw, -lr, c->W,
+                                     c->ldw, 1.f),
+                           false, c->flag, s, GEMM_NAIVE_UPDATE)))
+    return LST_E_HIP;
   prof(c, LST_PHASE_NAIVE_UPDATE, false);
   return LST_OK;
 }

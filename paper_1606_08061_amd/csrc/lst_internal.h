@@ -67,6 +67,10 @@ struct GemmDesc {
   int tiles_m, tiles_n;
   int tile_begin;
   int lr_scaled;  // alpha *= lr^2 and beta *= lr at launch (plans shared across lr)
+  // 128 x 128-tile kernel without split: when set, also writes per-column partial
+  // sums of squares of the product, colsq[p][j] for p < 4 * tiles_m (each the sum
+  // over 32 of the tile's rows of C[i,j]^2 before alpha/beta).
+  float *colsq;
 };
 
 // Operand placeholders of plans kept in device memory: a plan is built once per
@@ -126,6 +130,15 @@ void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float 
                        float *gradH, float lr, const int *gate, hipStream_t s, int phase,
                        const int *pf_idx = nullptr, int pf_K = 0);
 
+// Large single products on 128 x 128 tiles (the naive path).  gemm_big_ok: the
+// operands meet the kernel's alignment needs (else use gemm_launch).  gemm_big_plan
+// fills the tile counts and splits k over workgroups when the tiles are few, with
+// at most partial_floats of partial sums.  gemm_big_launch also runs the reduce.
+bool gemm_big_ok(const GemmDesc &g);
+constexpr int kBigColsqRows = 4;  // colsq rows per 128-row tile
+size_t gemm_big_plan(GemmDesc &g, int target_wgs, size_t partial_floats, float *partial);
+hipError_t gemm_big_launch(GemmDesc g, const int *gate, hipStream_t s, int phase);
+
 // Choose a split count for a long-k descriptor and attach its partial buffer.
 // Returns the number of floats the partial buffer needs.
 size_t gemm_plan_split(GemmDesc &g, int target_wgs, float *partial);
@@ -156,14 +169,18 @@ hipError_t launch_scatter(hipStream_t s, int m, int K, int d, float lr, const in
 hipError_t launch_identity(hipStream_t s, float *A, int d, int64_t ld);
 hipError_t launch_fill(hipStream_t s, float *p, float v);
 
-// Naive-path kernels.
+// Naive-path kernels.  Column norms come as nparts partial sums partial[p][j]
+// (from the forward product's epilogue, or from launch_colnorm).
 hipError_t launch_colnorm(hipStream_t s, const float *O, int64_t D, int m, float *partial,
                           int nblk);
-hipError_t launch_naive_epilogue(hipStream_t s, int m, int K, int64_t D, int nblk,
+hipError_t launch_naive_epilogue(hipStream_t s, int m, int K, int64_t D, int nparts,
                                  const float *partial, const float *O, const int *idx,
                                  const float *val, int loss, float eps, float *dq, float *dA,
-                                 float *loss_out, int *flag);
+                                 float *lvec, int *flag);
+// grad_O = 2 O diag(dq) + sum of dA at the targets, in place over O; also
+// loss_out = sum_j lvec[j].
 hipError_t launch_grad_o(hipStream_t s, float *O, int64_t D, int m, int K, const float *dq,
-                         const int *idx, const float *dA);
+                         const int *idx, const float *dA, const float *lvec, float *loss_out,
+                         int *flag);
 
 }  // namespace lst

@@ -119,9 +119,12 @@ def test_general_U0():
 
 
 def test_naive_path_matches_oracle():
+    # the first two run the 128 x 128-tile products (split over D for grad_H, with a
+    # ragged last split); m = 13, d = 30 takes the general GEMM and column-norm kernels
     for w in (WORKLOADS["sq_D2k_d32_m16_K3"],
               Workload("t", LOSS_SPHERICAL_SOFTMAX, 3000, 40, 20, 1, index_dist="zipf",
-                       value_dist="ones")):
+                       value_dist="ones"),
+              Workload("t", LOSS_SQUARED, 2500, 30, 13, 2)):
         c = Compare(w, path="naive")
         for t in range(10):
             st, l, g, ref = c.step()
