@@ -202,6 +202,37 @@ def run_sweep(args):
     print(json.dumps({"sweep_crossover_D": cross, "m": 512, "K": 5}), flush=True)
 
 
+def vendor_gemms(w, dev, H) -> dict:
+    """The naive path's three fp32 products through torch (the ROCm BLAS libraries),
+    as context for the naive path's own GEMM kernels: O = W H^T, grad_H = O^T W and
+    W += -lr O H, each timed over 10 calls on torch's current stream."""
+    import torch
+
+    torch.backends.cuda.matmul.allow_tf32 = False
+    W = torch.randn(w.D, w.d, device=dev) * 0.1
+    O = torch.randn(w.D, w.m, device=dev)
+    out = {}
+    calls = {
+        "naive_fwd": lambda: torch.mm(W, H.t()),
+        "naive_grad": lambda: torch.mm(O.t(), W),
+        "naive_update": lambda: W.addmm_(O, H, alpha=-w.lr),
+    }
+    for name, fn in calls.items():
+        for _ in range(2):
+            fn()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(10):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        out[name] = round(a.elapsed_time(b) / 10 * 1e3, 2)
+    del W, O
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -325,7 +356,8 @@ def main():
         naive = {"value": round(w.m / (nms / 1e3), 2), "unit": "examples/s",
                  "ms_per_step": round(nms, 4),
                  "phases_us": {k: round(v[1] / max(v[0], 1) * 1e3, 2)
-                               for k, v in nph.items() if v[0] and k.startswith("naive")}}
+                               for k, v in nph.items() if v[0] and k.startswith("naive")},
+                 "vendor_gemm_us": vendor_gemms(w, dev, gpool[0][0])}
 
     del V0, gpool
     torch.cuda.empty_cache()

@@ -62,53 +62,65 @@ __device__ __forceinline__ void ld4_tail(const float *__restrict__ p, int64_t si
   }
 }
 
-// One wavefront's share of the k range [kbeg, kend): full blocks of 8 with
-// index wave, wave + NW, ...; the ragged tail block goes to wave NW-1.
+// One wavefront's share of the k blocks of 8: blocks wave, wave + NW, ... of
+// the first segment (k in [kbeg, kbeg + len1)) followed by the second (k in
+// [0, len2) of A2, B2), so that the loads of both are in flight together.  The
+// last block of a segment may be ragged (masked loads).
 template <int NW, int AM, int BM>
 __device__ __forceinline__ void kloop(floatx16 &acc, const float *A, int64_t asi, int64_t ask,
-                                      const float *B, int64_t bsi, int64_t bsk, int ia, int jb,
-                                      int kbeg, int kend, int wave, int lh) {
-  const int nfull = (kend - kbeg) >> 3;
-  const int nw = nfull > wave ? (nfull - wave + NW - 1) / NW : 0;
-  if (nw > 0) {
-    auto kof = [&](int s) { return kbeg + 8 * (wave + NW * min(s, nw - 1)) + 4 * lh; };
-    float a[kStage][4], b[kStage][4];
+                                      const float *B, int64_t bsi, int64_t bsk, int len1,
+                                      const float *A2, int64_t asi2, int64_t ask2, const float *B2,
+                                      int64_t bsi2, int64_t bsk2, int len2, int ia, int jb,
+                                      int kbeg, int wave, int lh) {
+  const int nb1 = (len1 + 7) >> 3;
+  const int nb = nb1 + ((len2 + 7) >> 3);
+  const int nw = nb > wave ? (nb - wave + NW - 1) / NW : 0;
+  auto load = [&](int s, float(&a)[4], float(&b)[4]) {
+    const int bi = wave + NW * min(s, nw - 1);
+    if (bi < nb1) {
+      const int k0 = kbeg + 8 * bi + 4 * lh;
+      if (8 * bi + 8 <= len1) {
+        ld4<AM>(A, asi, ask, ia, k0, a);
+        ld4<BM>(B, bsi, bsk, jb, k0, b);
+      } else {
+        ld4_tail(A, asi, ask, ia, k0, kbeg + len1, a);
+        ld4_tail(B, bsi, bsk, jb, k0, kbeg + len1, b);
+      }
+    } else {
+      const int k0 = 8 * (bi - nb1) + 4 * lh;
+      if (8 * (bi - nb1) + 8 <= len2) {
+        ld4<AM>(A2, asi2, ask2, ia, k0, a);
+        ld4<BM>(B2, bsi2, bsk2, jb, k0, b);
+      } else {
+        ld4_tail(A2, asi2, ask2, ia, k0, len2, a);
+        ld4_tail(B2, bsi2, bsk2, jb, k0, len2, b);
+      }
+    }
+  };
+  if (nw == 0) return;
+  float a[kStage][4], b[kStage][4];
+#pragma unroll
+  for (int u = 0; u < kStage; ++u) load(u, a[u], b[u]);
+  for (int s0 = 0; s0 < nw; s0 += kStage) {
+    float an[kStage][4], bn[kStage][4];
+#pragma unroll
+    for (int u = 0; u < kStage; ++u)
+      if (s0 + kStage + u < nw) load(s0 + kStage + u, an[u], bn[u]);
 #pragma unroll
     for (int u = 0; u < kStage; ++u) {
-      ld4<AM>(A, asi, ask, ia, kof(u), a[u]);
-      ld4<BM>(B, bsi, bsk, jb, kof(u), b[u]);
-    }
-    for (int s0 = 0; s0 < nw; s0 += kStage) {
-      float an[kStage][4], bn[kStage][4];
+      if (s0 + u < nw) {
 #pragma unroll
-      for (int u = 0; u < kStage; ++u) {
-        ld4<AM>(A, asi, ask, ia, kof(s0 + kStage + u), an[u]);
-        ld4<BM>(B, bsi, bsk, jb, kof(s0 + kStage + u), bn[u]);
+        for (int s = 0; s < 4; ++s)
+          acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[u][s], b[u][s], acc, 0, 0, 0);
       }
-#pragma unroll
-      for (int u = 0; u < kStage; ++u) {
-        if (s0 + u < nw) {
-#pragma unroll
-          for (int s = 0; s < 4; ++s)
-            acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[u][s], b[u][s], acc, 0, 0, 0);
-        }
-      }
-#pragma unroll
-      for (int u = 0; u < kStage; ++u)
-#pragma unroll
-        for (int s = 0; s < 4; ++s) {
-          a[u][s] = an[u][s];
-          b[u][s] = bn[u][s];
-        }
     }
-  }
-  if (((kend - kbeg) & 7) && wave == NW - 1) {
-    const int k0 = kbeg + 8 * nfull + 4 * lh;
-    float a[4], b[4];
-    ld4_tail(A, asi, ask, ia, k0, kend, a);
-    ld4_tail(B, bsi, bsk, jb, k0, kend, b);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x2f32(a[s], b[s], acc, 0, 0, 0);
+    for (int u = 0; u < kStage; ++u)
+#pragma unroll
+      for (int s = 0; s < 4; ++s) {
+        a[u][s] = an[u][s];
+        b[u][s] = bn[u][s];
+      }
   }
 }
 
@@ -118,22 +130,30 @@ __device__ __forceinline__ bool vec_ok(const float *p, int64_t ld) {
 
 // opA(i,k): tA = 0 -> A[i*lda + k] (index stride lda, k stride 1); tA = 1 -> A[k*lda + i].
 // opB(k,j): tB = 0 -> B[j*ldb + k];                                 tB = 1 -> B[k*ldb + j].
+// k runs over [kbeg, kend) of (A, B) and then over [0, K2) of (A2, B2).
 template <int NW>
 __device__ __forceinline__ void segment(floatx16 &acc, const float *A, int64_t lda, int tA,
-                                        const float *B, int64_t ldb, int tB, int ia, int jb,
-                                        int kbeg, int kend, int wave, int lh) {
+                                        const float *B, int64_t ldb, int tB, const float *A2,
+                                        int64_t lda2, const float *B2, int64_t ldb2, int K2,
+                                        int ia, int jb, int kbeg, int kend, int wave, int lh) {
   const int64_t asi = tA ? 1 : lda, ask = tA ? lda : 1;
   const int64_t bsi = tB ? 1 : ldb, bsk = tB ? ldb : 1;
-  const bool av = !tA && vec_ok(A, lda);
-  const bool bv = !tB && vec_ok(B, ldb);
+  const int64_t asi2 = tA ? 1 : lda2, ask2 = tA ? lda2 : 1;
+  const int64_t bsi2 = tB ? 1 : ldb2, bsk2 = tB ? ldb2 : 1;
+  const bool av = !tA && vec_ok(A, lda) && (K2 == 0 || vec_ok(A2, lda2));
+  const bool bv = !tB && vec_ok(B, ldb) && (K2 == 0 || vec_ok(B2, ldb2));
+#define LST_KLOOP(AMODE, BMODE)                                                                    \
+  kloop<NW, AMODE, BMODE>(acc, A, asi, ask, B, bsi, bsk, kend - kbeg, A2, asi2, ask2, B2, bsi2, \
+                          bsk2, K2, ia, jb, kbeg, wave, lh)
   if (av && bv)
-    kloop<NW, VEC, VEC>(acc, A, asi, ask, B, bsi, bsk, ia, jb, kbeg, kend, wave, lh);
+    LST_KLOOP(VEC, VEC);
   else if (av)
-    kloop<NW, VEC, STRIDED>(acc, A, asi, ask, B, bsi, bsk, ia, jb, kbeg, kend, wave, lh);
+    LST_KLOOP(VEC, STRIDED);
   else if (bv)
-    kloop<NW, STRIDED, VEC>(acc, A, asi, ask, B, bsi, bsk, ia, jb, kbeg, kend, wave, lh);
+    LST_KLOOP(STRIDED, VEC);
   else
-    kloop<NW, STRIDED, STRIDED>(acc, A, asi, ask, B, bsi, bsk, ia, jb, kbeg, kend, wave, lh);
+    LST_KLOOP(STRIDED, STRIDED);
+#undef LST_KLOOP
 }
 
 __device__ __forceinline__ void finish(const GemmDesc &g, int i, int j, float v) {
@@ -214,10 +234,11 @@ __device__ __forceinline__ void gemm_body(const GemmBatch &bt, const float *H, f
   if (g.splits > 1) {
     const int kbeg = split * g.kchunk;
     const int kend = min(g.K, kbeg + g.kchunk);
-    segment<NW>(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, ia, jb, kbeg, kend, wave, lh);
+    segment<NW>(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, nullptr, 0, nullptr, 0, 0, ia, jb, kbeg,
+                kend, wave, lh);
   } else {
-    segment<NW>(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, ia, jb, 0, g.K, wave, lh);
-    if (g.K2 > 0) segment<NW>(acc, g.A2, g.lda2, g.tA, g.B2, g.ldb2, g.tB, ia, jb, 0, g.K2, wave, lh);
+    segment<NW>(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, g.A2, g.lda2, g.B2, g.ldb2, g.K2, ia, jb,
+                0, g.K, wave, lh);
   }
 
   __shared__ float red[NW][16][64];
@@ -248,13 +269,13 @@ __device__ __forceinline__ void gemm_body(const GemmBatch &bt, const float *H, f
 
 // PHASE only names the instantiation, so profilers report each step phase separately.
 template <int PHASE, int NW>
-__global__ __launch_bounds__(64 * NW) void gemm_kernel(const GemmBatch bt, const int *__restrict__ gate) {
+__global__ __launch_bounds__(64 * NW, 12 / NW) void gemm_kernel(const GemmBatch bt, const int *__restrict__ gate) {
   gemm_body<NW>(bt, nullptr, nullptr, 1.f, gate);
 }
 
 // The batch read from device memory (a plan), with the step's H, grad_H and lr.
 template <int PHASE, int NW>
-__global__ __launch_bounds__(64 * NW) void gemm_plan_kernel(const GemmBatch *__restrict__ bt,
+__global__ __launch_bounds__(64 * NW, 12 / NW) void gemm_plan_kernel(const GemmBatch *__restrict__ bt,
                                                             const float *H, float *gH, float lr,
                                                             const int *__restrict__ gate) {
   gemm_body<NW>(*bt, H, gH, lr, gate);
