@@ -839,7 +839,7 @@ __global__ __launch_bounds__(kMblockThreads) void mblock_kernel(
   M[e] = 4.f * di * mh * dj + yy + 2.f * di * hz + 2.f * dj * hzt;
 }
 
-constexpr int kScatterThreads = 256;
+constexpr int kScatterThreads = 512;
 
 // One workgroup per target slot s (slot = j*K + k of the m x K index matrix).
 // The lowest slot of each V row does the row's update: it lists, in ascending
@@ -880,14 +880,94 @@ __global__ __launch_bounds__(kScatterThreads) void scatter_kernel(
     __syncthreads();
   }
 
+  // The row's sum over its `total` slots: columns in groups of four where the
+  // layout allows; the slots split into np interleaved parts (np a power of two,
+  // as many as the threads left over by the columns allow), each part's sum
+  // carried in kIlp independent partial sums, the parts then added in a fixed
+  // order through LDS.  Rows with many slots (frequent targets) are so spread
+  // over the workgroup instead of running one slot after another.
   float *vr = V + (int64_t)r * ldv;
-  for (int c = threadIdx.x; c < d; c += kScatterThreads) {
-    float acc = 0.f;
-    for (int t = 0; t < total; ++t) {
-      const int q = slist[t];
-      acc += dA[q] * P[(int64_t)(q / K) * d + c];
+  const bool v4 = (d & 3) == 0 && (ldv & 3) == 0 && (reinterpret_cast<uintptr_t>(V) & 15) == 0 &&
+                  (reinterpret_cast<uintptr_t>(P) & 15) == 0;
+  const int width = v4 ? 4 : 1;
+  const int ng = (d + width - 1) / width;  // column groups
+  int np = 1;
+  while (np < 16 && 2 * np * ng <= kScatterThreads) np *= 2;
+  __shared__ float4 spart[kScatterThreads];
+  for (int g0 = 0; g0 < ng; g0 += kScatterThreads / np) {
+    const int gl = threadIdx.x % (kScatterThreads / np), part = threadIdx.x / (kScatterThreads / np);
+    const int g = g0 + gl;
+    const bool active = g < ng;
+    constexpr int kIlp = 8;
+    float4 a[kIlp];
+#pragma unroll
+    for (int u = 0; u < kIlp; ++u) a[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (active) {
+      int t = part;
+      for (; t + (kIlp - 1) * np < total; t += kIlp * np) {
+#pragma unroll
+        for (int u = 0; u < kIlp; ++u) {
+          const int q = slist[t + u * np];
+          const float w = dA[q];
+          const float *pr = P + (int64_t)(q / K) * d + g * width;
+          if (v4) {
+            const float4 x = *reinterpret_cast<const float4 *>(pr);
+            a[u].x += w * x.x;
+            a[u].y += w * x.y;
+            a[u].z += w * x.z;
+            a[u].w += w * x.w;
+          } else {
+            a[u].x += w * pr[0];
+          }
+        }
+      }
+      for (; t < total; t += np) {  // fewer than kIlp left
+        const int q = slist[t];
+        const float w = dA[q];
+        const float *pr = P + (int64_t)(q / K) * d + g * width;
+        if (v4) {
+          const float4 x = *reinterpret_cast<const float4 *>(pr);
+          a[0].x += w * x.x;
+          a[0].y += w * x.y;
+          a[0].z += w * x.z;
+          a[0].w += w * x.w;
+        } else {
+          a[0].x += w * pr[0];
+        }
+      }
     }
-    vr[c] -= lr * acc;
+    float4 sum = a[0];
+#pragma unroll
+    for (int u = 1; u < kIlp; ++u) {
+      sum.x += a[u].x;
+      sum.y += a[u].y;
+      sum.z += a[u].z;
+      sum.w += a[u].w;
+    }
+    spart[threadIdx.x] = sum;
+    __syncthreads();
+    if (part == 0 && active) {
+      float4 tot = spart[gl];
+      for (int p2 = 1; p2 < np; ++p2) {
+        const float4 x = spart[gl + p2 * (kScatterThreads / np)];
+        tot.x += x.x;
+        tot.y += x.y;
+        tot.z += x.z;
+        tot.w += x.w;
+      }
+      if (v4) {
+        float4 *dst = reinterpret_cast<float4 *>(vr) + g;
+        float4 v = *dst;
+        v.x -= lr * tot.x;
+        v.y -= lr * tot.y;
+        v.z -= lr * tot.z;
+        v.w -= lr * tot.w;
+        *dst = v;
+      } else {
+        vr[g] -= lr * tot.x;
+      }
+    }
+    __syncthreads();
   }
 }
 
