@@ -357,26 +357,10 @@ __device__ __forceinline__ void segment16(floatx4 &acc, const float *A, int64_t 
 
 // One 16 x 16 tile per workgroup of 256 threads; thread t finishes output
 // (4 (t / 16 % 4) + ..., see below) after the reduction.  No split-k.
-template <int PHASE>
-__global__ __launch_bounds__(256) void gemm16_plan_kernel(const GemmBatch *__restrict__ bt,
-                                                           const float *H, float *gH, float lr,
-                                                           const int *__restrict__ gate,
-                                                           const int *__restrict__ pf_idx,
-                                                           int pf_K) {
-  if ((int)blockIdx.x >= bt->total_tiles) {
-    // Prefetch workgroup: the target rows of example j (indices outside [0, D) skipped).
-    const int j = (int)blockIdx.x - bt->pf_base;
-    if (j < 0 || j >= bt->pf_m) return;
-    float sink = 0.f;
-    for (int k = 0; k < pf_K; ++k) {
-      const int r = pf_idx[(int64_t)j * pf_K + k];
-      if (r < 0 || (int64_t)r >= bt->pf_D) continue;
-      const float *row = bt->pf_V + (int64_t)r * bt->pf_ldv;
-      for (int c = threadIdx.x; c < bt->pf_d; c += 256) sink += row[c];
-    }
-    asm volatile("" ::"v"(sink));
-    return;
-  }
+// One 16 x 16 output tile of a plan batch (workgroup blockIdx.x).
+__device__ __forceinline__ void gemm16_tile(const GemmBatch &bt_, const float *H, float *gH,
+                                            float lr, const int *__restrict__ gate) {
+  const GemmBatch *bt = &bt_;
   const int closed = gate ? *gate : 0;  // waited for at the end: it only suppresses writes
   const int tile = xcd_tile(blockIdx.x, bt->total_tiles);
   int di = 0;
@@ -424,6 +408,29 @@ __global__ __launch_bounds__(256) void gemm16_plan_kernel(const GemmBatch *__res
     g.C[(int64_t)oi * g.ldc + oj] = out;
     if (use_e) g.C2[(int64_t)oi * g.ldc2 + oj] = 2.f * g.rs[oi] * ein + out;
   }
+}
+
+template <int PHASE>
+__global__ __launch_bounds__(256) void gemm16_plan_kernel(const GemmBatch *__restrict__ bt,
+                                                           const float *H, float *gH, float lr,
+                                                           const int *__restrict__ gate,
+                                                           const int *__restrict__ pf_idx,
+                                                           int pf_K) {
+  if ((int)blockIdx.x >= bt->total_tiles) {
+    // Prefetch workgroup: the target rows of example j (indices outside [0, D) skipped).
+    const int j = (int)blockIdx.x - bt->pf_base;
+    if (j < 0 || j >= bt->pf_m) return;
+    float sink = 0.f;
+    for (int k = 0; k < pf_K; ++k) {
+      const int r = pf_idx[(int64_t)j * pf_K + k];
+      if (r < 0 || (int64_t)r >= bt->pf_D) continue;
+      const float *row = bt->pf_V + (int64_t)r * bt->pf_ldv;
+      for (int c = threadIdx.x; c < bt->pf_d; c += 256) sink += row[c];
+    }
+    asm volatile("" ::"v"(sink));
+    return;
+  }
+  gemm16_tile(*bt, H, gH, lr, gate);
 }
 
 // ---------------------------------------------------------------------------
