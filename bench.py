@@ -82,16 +82,18 @@ def load_traffic():
     """Per-launch HBM bytes measured by hardware counters (traffic.json, written by
     paper_1606_08061_amd.traffic_from_pmc), per phase, kept only while the kernel's
     source file is unchanged since the counters were taken."""
-    import hashlib
+    from paper_1606_08061_amd.traffic_from_pmc import source_sha
 
-    pkg = os.path.join(ROOT, "paper_1606_08061_amd")
-    path = os.path.join(pkg, "traffic.json")
+    path = os.path.join(ROOT, "paper_1606_08061_amd", "traffic.json")
     if not os.path.exists(path):
         return {}
     out = {}
     for phase, r in json.load(open(path)).get("phases", {}).items():
-        src = os.path.join(pkg, "csrc", r["source"])
-        if os.path.exists(src) and hashlib.sha256(open(src, "rb").read()).hexdigest() == r["source_sha256"]:
+        try:
+            same = source_sha(r["source"]) == r["source_sha256"]
+        except OSError:
+            same = False
+        if same:
             out[phase] = int(r["fetch_bytes"]) + int(r["write_bytes"])
     return out
 

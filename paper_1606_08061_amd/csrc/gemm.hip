@@ -286,10 +286,16 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const GemmDesc g, co
   const int64_t total = (int64_t)g.M * g.N;
   for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
        e += (int64_t)gridDim.x * blockDim.x) {
-    float v = 0.f;
-    for (int s = 0; s < g.splits; ++s) v += g.partial[(int64_t)s * total + e];
+    // eight interleaved partial sums (loads in flight together), added in a fixed order
+    float v[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    int s = 0;
+    for (; s + 8 <= g.splits; s += 8)
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] += g.partial[(int64_t)(s + u) * total + e];
+    for (; s < g.splits; ++s) v[0] += g.partial[(int64_t)s * total + e];
+    const float sum = ((v[0] + v[1]) + (v[2] + v[3])) + ((v[4] + v[5]) + (v[6] + v[7]));
     const int i = (int)(e / g.N), j = (int)(e % g.N);
-    finish(g, i, j, v);
+    finish(g, i, j, sum);
   }
 }
 

@@ -23,8 +23,11 @@ import os
 PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 
-# kernel name prefix -> (phase, defining source file)
+# kernel name prefix -> (phase, source files that define the kernel's code)
 KERNELS = [
+    ("gemm16_plan_kernel<0>", "gram", "gemm.hip"),
+    ("gemm16_plan_kernel<1>", "contract", "gemm.hip"),
+    ("gemm16_plan_kernel<2>", "zgrad", "gemm.hip"),
     ("gemm_plan_kernel<0,", "gram", "gemm.hip"),
     ("gemm_plan_kernel<1,", "contract", "gemm.hip"),
     ("gemm_plan_kernel<2,", "zgrad", "gemm.hip"),
@@ -33,13 +36,17 @@ KERNELS = [
     ("gather_reg_kernel", "gather", "step_kernels.hip"),
     ("gather_kernel", "gather", "step_kernels.hip"),
     ("mblock_kernel", "mblock", "step_kernels.hip"),
-    ("woodbury_blocked_kernel", "woodbury", "step_kernels.hip"),
+    ("woodbury_blocked_kernel", "woodbury", "step_kernels.hip+woodbury_gj.h"),
     ("scatter_kernel", "scatter", "step_kernels.hip"),
 ]
 
 
-def source_sha(name: str) -> str:
-    return hashlib.sha256(open(os.path.join(CSRC, name), "rb").read()).hexdigest()
+def source_sha(names: str) -> str:
+    """SHA-256 of the named sources ("a+b": their bytes in that order)."""
+    h = hashlib.sha256()
+    for n in names.split("+"):
+        h.update(open(os.path.join(CSRC, n), "rb").read())
+    return h.hexdigest()
 
 
 def _short(name: str) -> str:
