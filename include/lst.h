@@ -71,7 +71,10 @@ enum lst_status {
                            (m = 1: 1 - 2 eta ||h||^2 <= 0, eq. updateU-T)       */
   LST_E_NONFINITE = -5, /* (device) the loss is NaN or infinite                */
   LST_E_HIP = -6,       /* a HIP runtime call failed                           */
-  LST_E_STATE = -7      /* wrong context kind for this call                    */
+  LST_E_STATE = -7,     /* wrong context kind for this call                    */
+  LST_E_SYNC = -8       /* (device) a step's two streams lost their ordering: a
+                           bounded wait of one on the other's progress counter
+                           expired; the state updates of that step were skipped */
 };
 
 /* Limits of one context. */

@@ -28,6 +28,7 @@ LST_E_NOT_SPD = -4
 LST_E_NONFINITE = -5
 LST_E_HIP = -6
 LST_E_STATE = -7
+LST_E_SYNC = -8
 
 # Exported C symbols and their signatures (kept in step with include/lst.h).
 _P = ctypes.c_void_p

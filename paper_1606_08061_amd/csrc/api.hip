@@ -39,7 +39,9 @@ struct GraphEntry {
   void *loss, *grad;
   int m, K;
   uint32_t lr_bits;
-  hipGraphExec_t exec;
+  // the step's parts in launch order: main stream up to M, side stream (Woodbury
+  // branch), main stream state updates
+  hipGraphExec_t exec_a, exec_side, exec_b;
   uint64_t last_use;
 };
 constexpr size_t kGraphCap = 256;
@@ -79,13 +81,15 @@ struct lst_ctx {
   float *Pbig, *Cp, *Rp;  // blocked Woodbury inverse for m > 256
   float *dq, *lvec, *dA;
   int *flag;
+  // progress counters ordering the two streams of a factored step: [0] contraction
+  // launches started, [1] Woodbury inverses completed, [2] Z^ launches started
+  int *cnt;
   float *O, *colpart, *splitpart;
   hipError_t last_err;
-  // side stream of a factored step (Woodbury inverse) and its fork/join events;
-  // cap is the stream a step is captured on when it is recorded as a HIP graph
+  // side stream of a factored step (Woodbury inverse); cap is the stream a step
+  // is captured on when it is recorded as HIP graphs
   hipStream_t side[1];
   hipStream_t cap;
-  hipEvent_t ev_fork, ev_wood_ready, ev_wood_done;
   bool have_side;
   // tracing: event pairs per phase
   bool prof_on;
@@ -98,6 +102,10 @@ struct lst_ctx {
   uint64_t plan_tick;
   // captured steps, one per distinct (inputs, m, K, lr)
   bool use_graphs;
+  // test hook (environment variable LST_TEST_WITHHOLD_WOODBURY_RELEASE at creation):
+  // the Woodbury branch never releases its counter, so the state-update wait of
+  // every step expires (bounded) and reports LST_E_SYNC
+  bool withhold_release;
   std::vector<GraphEntry> graphs;
   uint64_t graph_tick;
 };
@@ -133,6 +141,7 @@ void carve_factored(lst_ctx *c, Carver &cv) {
   c->lvec = cv.take<float>(c->m_max);
   c->dA = cv.take<float>(mk);
   c->flag = cv.take<int>(1);
+  c->cnt = cv.take<int>(3);
   c->plan_pool = cv.take<GemmBatch>(kPlanCap * kPlanBatches);
 }
 
@@ -243,15 +252,16 @@ void prof(lst_ctx *c, int phase, bool begin) {
   g_prof.stop = ev[2 * (size_t)used + 1];
 }
 
+void graph_entry_free(GraphEntry &g) {
+  hipGraphExec_t ex[3] = {g.exec_a, g.exec_side, g.exec_b};
+  for (hipGraphExec_t e : ex)
+    if (e) (void)hipGraphExecDestroy(e);
+}
+
 int side_create(lst_ctx *c) {
   for (int i = 0; i < 1; ++i)
     if (hipStreamCreateWithFlags(&c->side[i], hipStreamNonBlocking) != hipSuccess) return LST_E_HIP;
   if (hipStreamCreateWithFlags(&c->cap, hipStreamNonBlocking) != hipSuccess) return LST_E_HIP;
-  hipEvent_t *evs[3] = {&c->ev_fork, &c->ev_wood_ready, &c->ev_wood_done};
-  for (hipEvent_t *e : evs)
-    // device-scope release: only kernels on this device consume the fork/join events
-    if (hipEventCreateWithFlags(e, hipEventDisableTiming | hipEventReleaseToDevice) != hipSuccess)
-      return LST_E_HIP;
   c->have_side = true;
   return LST_OK;
 }
@@ -261,11 +271,8 @@ void side_free(lst_ctx *c) {
   for (int i = 0; i < 1; ++i)
     if (c->side[i]) (void)hipStreamDestroy(c->side[i]);
   if (c->cap) (void)hipStreamDestroy(c->cap);
-  for (GraphEntry &g : c->graphs) (void)hipGraphExecDestroy(g.exec);
+  for (GraphEntry &g : c->graphs) graph_entry_free(g);
   c->graphs.clear();
-  hipEvent_t evs[3] = {c->ev_fork, c->ev_wood_ready, c->ev_wood_done};
-  for (hipEvent_t e : evs)
-    if (e) (void)hipEventDestroy(e);
   c->have_side = false;
 }
 
@@ -327,6 +334,7 @@ const char *lst_status_string(int status) {
     case LST_E_NONFINITE: return "LST_E_NONFINITE";
     case LST_E_HIP: return "LST_E_HIP";
     case LST_E_STATE: return "LST_E_STATE";
+    case LST_E_SYNC: return "LST_E_SYNC";
     default: return "LST_E_UNKNOWN";
   }
 }
@@ -358,6 +366,7 @@ int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max
   c->ldd = ldd;
   c->last_err = hipSuccess;
   c->use_graphs = true;
+  c->withhold_release = std::getenv("LST_TEST_WITHHOLD_WOODBURY_RELEASE") != nullptr;
   st = alloc_ws(c, carve_factored);
   if (st == LST_OK) st = side_create(c);
   if (st != LST_OK) {
@@ -457,6 +466,11 @@ int lst_sync_status(lst_ctx *c) {
   if (f & FLAG_INDEX) return LST_E_INDEX;
   if (f & FLAG_NONFINITE) return LST_E_NONFINITE;
   if (f & FLAG_NOT_SPD) return LST_E_NOT_SPD;
+  if (f & FLAG_SYNC) {
+    // Both streams are idle: restart the progress counters from a consistent state.
+    if (c->cnt && hipMemset(c->cnt, 0, 3 * sizeof(int)) != hipSuccess) return LST_E_HIP;
+    return LST_E_SYNC;
+  }
   return LST_OK;
 }
 
@@ -629,7 +643,7 @@ PlanEntry *get_plan(lst_ctx *c, int m) {
     const int old_m = c->plans[v].m;
     for (size_t i = c->graphs.size(); i-- > 0;)
       if (c->graphs[i].m == old_m) {
-        (void)hipGraphExecDestroy(c->graphs[i].exec);
+        graph_entry_free(c->graphs[i]);
         c->graphs.erase(c->graphs.begin() + i);
       }
     slot = c->plans[v].dev;
@@ -648,78 +662,113 @@ PlanEntry *get_plan(lst_ctx *c, int m) {
   return &e;
 }
 
-int enqueue_factored_step(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *H,
-                          int32_t m, const int32_t *idx, const float *val, int32_t K, float lr,
-                          float *loss_dev, float *grad_H) {
-  const int d = c->d;
-  float *gH = grad_H ? grad_H : c->gradH;
-  auto gemm = [&](int i, const int *gate, hipStream_t st, int phase) {
-    gemm_enqueue_plan(pl.b[i], pl.dev + i, H, gH, lr, gate, st, phase, i == 1 ? idx : nullptr,
-                      K);
-  };
+// A step runs on two streams ordered by the progress counters c->cnt (no host
+// events): the main stream signals when its contraction launch starts (the
+// step's inputs are ready and the previous step has consumed N and R); the side
+// stream then forms N = H^T H and the Woodbury inverse and releases R; the main
+// stream waits for that before the state updates.  Each wait is a kernel of one
+// workgroup (many polling workgroups slow the step down).
+// The parts are launched in the order main (to M), side, main (updates), so that
+// every wait's producer is launched before it even where the two streams share
+// a hardware queue.
 
-  hipStream_t s_wood = c->side[0];
-  if (record(c, hipEventRecord(c->ev_fork, s))) return LST_E_HIP;
-
-  // Woodbury branch: N = H^T H, then C = I - 2 eta S N S and its inverse.  For
-  // squared error dl/dq = 1 and the branch needs nothing else; the spherical
-  // softmax waits for dl/dq = T / (q + D eps) from the gather.
+// Main stream up to M: contractions, gather and loss epilogue, Z^ and grad_H, M.
+int enqueue_main_a(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *H, int32_t m,
+                   const int32_t *idx, const float *val, int32_t K, float lr, float *loss_dev,
+                   float *gH) {
   const bool unit_dq = (c->loss == LST_LOSS_SQUARED);
-  if (record(c, hipStreamWaitEvent(s_wood, c->ev_fork, 0))) return LST_E_HIP;
-  prof(c, LST_PHASE_GRAM, true);
-  gemm(0, nullptr, s_wood, GEMM_OTHER);
-  prof(c, LST_PHASE_GRAM, false);
-  auto woodbury = [&]() -> int {
-    prof(c, LST_PHASE_WOODBURY, true);
-    launch_woodbury(s_wood, m, lr, unit_dq ? 1 : 0, c->dq, c->N, c->R, c->Cwork, c->Pbig, c->Cp,
-                    c->Rp, c->flag);
-    prof(c, LST_PHASE_WOODBURY, false);
-    return record(c, hipEventRecord(c->ev_wood_done, s_wood));
+  auto gemm = [&](int i, int phase, int *sig) {
+    StepSync sy;
+    sy.sig = sig;
+    gemm_enqueue_plan(pl.b[i], pl.dev + i, H, gH, lr, nullptr, s, phase, i == 1 ? idx : nullptr,
+                      K, sy);
   };
-  if (unit_dq && woodbury() != LST_OK) return LST_E_HIP;
-
   prof(c, LST_PHASE_CONTRACT, true);
-  gemm(1, nullptr, s, GEMM_CONTRACT);
+  gemm(1, GEMM_CONTRACT, c->cnt + 0);
   prof(c, LST_PHASE_CONTRACT, false);
 
   // Sparse gather of the K target rows of the pre-update V and the loss epilogue.
   prof(c, LST_PHASE_GATHER, true);
-  launch_gather(s, m, K, d, c->D, H, c->Hhat, c->Htil, idx, val, c->V, c->ldv, c->loss, c->eps, lr,
-                c->G, c->Atil, c->dq, c->dA, c->lvec, c->flag);
+  launch_gather(s, m, K, c->d, c->D, H, c->Hhat, c->Htil, idx, val, c->V, c->ldv, c->loss, c->eps,
+                lr, c->G, c->Atil, c->dq, c->dA, c->lvec, c->flag);
   prof(c, LST_PHASE_GATHER, false);
-  if (!unit_dq) {
-    if (record(c, hipEventRecord(c->ev_wood_ready, s)) ||
-        record(c, hipStreamWaitEvent(s_wood, c->ev_wood_ready, 0)) || woodbury() != LST_OK)
-      return LST_E_HIP;
-  }
 
+  // Z^ and grad_H; its start tells the spherical softmax's Woodbury branch that
+  // dl/dq is ready.
   prof(c, LST_PHASE_ZGRAD, true);
-  gemm(2, nullptr, s, GEMM_ZGRAD);
+  gemm(2, GEMM_ZGRAD, unit_dq ? nullptr : c->cnt + 2);
   prof(c, LST_PHASE_ZGRAD, false);
 
   // Loss and M; sets the error flag on a non-finite loss.
   prof(c, LST_PHASE_MBLOCK, true);
   launch_mblock(s, m, K, idx, c->lvec, c->dq, c->dA, c->Mhat, c->HZ, c->M, loss_dev, c->flag);
   prof(c, LST_PHASE_MBLOCK, false);
+  return record(c, hipGetLastError()) ? LST_E_HIP : LST_OK;
+}
 
-  // Join the Woodbury branch before its result (and its error flag) is used.
-  if (record(c, hipStreamWaitEvent(s, c->ev_wood_done, 0))) return LST_E_HIP;
+// Side stream: N = H^T H, then C = I - 2 eta S N S and R = 2 eta S C^{-1} S.
+// For squared error dl/dq = 1; the spherical softmax waits for the gather's
+// dl/dq = T / (q + D eps).
+int enqueue_side(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *H, int32_t m,
+                 float lr, float *gH) {
+  const bool unit_dq = (c->loss == LST_LOSS_SQUARED);
+  StepSync started;  // the main stream has reached this step's contraction
+  started.wx = c->cnt + 0;
+  started.wy = c->cnt + 1;
+  started.wd = 1;
+  started.flag = c->flag;
+  prof(c, LST_PHASE_GRAM, true);
+  launch_step_sync(s, started, nullptr);
+  gemm_enqueue_plan(pl.b[0], pl.dev + 0, H, gH, lr, nullptr, s, GEMM_OTHER);
+  prof(c, LST_PHASE_GRAM, false);
+  StepSync gathered;
+  if (!unit_dq) {
+    gathered.wx = c->cnt + 2;
+    gathered.wy = c->cnt + 1;
+    gathered.wd = 1;
+    gathered.flag = c->flag;
+  }
+  prof(c, LST_PHASE_WOODBURY, true);
+  launch_woodbury(s, m, lr, unit_dq ? 1 : 0, c->dq, c->N, c->R, c->Cwork, c->Pbig, c->Cp, c->Rp,
+                  c->flag, gathered, c->withhold_release ? nullptr : c->cnt + 1);
+  prof(c, LST_PHASE_WOODBURY, false);
+  return record(c, hipGetLastError()) ? LST_E_HIP : LST_OK;
+}
 
-  // Gated state updates (see build_plan).
+// Main stream: the gated state updates (see build_plan) once the side stream has
+// released this step's R (and its error flag), then the scatter into V.
+int enqueue_main_b(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *H, int32_t m,
+                   const int32_t *idx, int32_t K, float lr, float *gH) {
+  StepSync joined;
+  joined.wx = c->cnt + 1;
+  joined.wy = c->cnt + 0;
+  joined.wd = 0;
+  joined.flag = c->flag;
   prof(c, LST_PHASE_MID, true);
-  gemm(3, c->flag, s, GEMM_MID);
+  launch_step_sync(s, joined, nullptr);
+  gemm_enqueue_plan(pl.b[3], pl.dev + 3, H, gH, lr, c->flag, s, GEMM_MID);
   prof(c, LST_PHASE_MID, false);
   prof(c, LST_PHASE_UPDATE, true);
-  gemm(4, c->flag, s, GEMM_UPDATE);
+  gemm_enqueue_plan(pl.b[4], pl.dev + 4, H, gH, lr, c->flag, s, GEMM_UPDATE);
   prof(c, LST_PHASE_UPDATE, false);
 
   // V_r -= eta sum dl/dA P_j over the slots of each distinct target row (eq. updateV).
   prof(c, LST_PHASE_SCATTER, true);
-  launch_scatter(s, m, K, d, lr, idx, c->dA, c->P, c->V, c->ldv, c->flag);
+  launch_scatter(s, m, K, c->d, lr, idx, c->dA, c->P, c->V, c->ldv, c->flag);
   prof(c, LST_PHASE_SCATTER, false);
   // Kernel launches above are not checked one by one: a launch error stays pending
   // and is reported here.
   return record(c, hipGetLastError()) ? LST_E_HIP : LST_OK;
+}
+
+int enqueue_factored_step(lst_ctx *c, const PlanEntry &pl, const float *H, int32_t m,
+                          const int32_t *idx, const float *val, int32_t K, float lr,
+                          float *loss_dev, float *grad_H) {
+  float *gH = grad_H ? grad_H : c->gradH;
+  int st = enqueue_main_a(c, c->stream, pl, H, m, idx, val, K, lr, loss_dev, gH);
+  if (st == LST_OK) st = enqueue_side(c, c->side[0], pl, H, m, lr, gH);
+  if (st == LST_OK) st = enqueue_main_b(c, c->stream, pl, H, m, idx, K, lr, gH);
+  return st;
 }
 
 // Replays (capturing first if needed) the graph of a step with these arguments.
@@ -739,28 +788,47 @@ int graph_step(lst_ctx *c, const PlanEntry &pl, const float *H, int32_t m, const
       size_t v = 0;
       for (size_t i = 1; i < c->graphs.size(); ++i)
         if (c->graphs[i].last_use < c->graphs[v].last_use) v = i;
-      if (record(c, hipStreamSynchronize(c->stream))) return LST_E_HIP;
-      (void)hipGraphExecDestroy(c->graphs[v].exec);
+      if (record(c, hipStreamSynchronize(c->stream)) || record(c, hipStreamSynchronize(c->side[0])))
+        return LST_E_HIP;
+      graph_entry_free(c->graphs[v]);
       c->graphs.erase(c->graphs.begin() + v);
     }
-    if (record(c, hipStreamBeginCapture(c->cap, hipStreamCaptureModeThreadLocal))) return LST_E_HIP;
-    const int st = enqueue_factored_step(c, c->cap, pl, H, m, idx, val, K, lr, loss_dev, grad_H);
-    hipGraph_t graph = nullptr;
-    const hipError_t ec = hipStreamEndCapture(c->cap, &graph);
-    if (st != LST_OK || ec != hipSuccess || !graph) {
-      if (graph) (void)hipGraphDestroy(graph);
-      if (ec != hipSuccess) c->last_err = ec;
-      return st != LST_OK ? st : LST_E_HIP;
+    float *gH = grad_H ? grad_H : c->gradH;
+    // The step's three parts are captured one after the other on the capture stream.
+    auto capture = [&](int part, hipGraphExec_t *exec) -> int {
+      if (record(c, hipStreamBeginCapture(c->cap, hipStreamCaptureModeThreadLocal)))
+        return LST_E_HIP;
+      const int st =
+          part == 0   ? enqueue_main_a(c, c->cap, pl, H, m, idx, val, K, lr, loss_dev, gH)
+          : part == 1 ? enqueue_side(c, c->cap, pl, H, m, lr, gH)
+                      : enqueue_main_b(c, c->cap, pl, H, m, idx, K, lr, gH);
+      hipGraph_t graph = nullptr;
+      const hipError_t ec = hipStreamEndCapture(c->cap, &graph);
+      if (st != LST_OK || ec != hipSuccess || !graph) {
+        if (graph) (void)hipGraphDestroy(graph);
+        if (ec != hipSuccess) c->last_err = ec;
+        return st != LST_OK ? st : LST_E_HIP;
+      }
+      const hipError_t ei = hipGraphInstantiate(exec, graph, nullptr, nullptr, 0);
+      (void)hipGraphDestroy(graph);
+      return record(c, ei) ? LST_E_HIP : LST_OK;
+    };
+    GraphEntry e{H, idx, val, loss_dev, grad_H, m, K, lr_bits, nullptr, nullptr, nullptr, 0};
+    int st = capture(0, &e.exec_a);
+    if (st == LST_OK) st = capture(1, &e.exec_side);
+    if (st == LST_OK) st = capture(2, &e.exec_b);
+    if (st != LST_OK) {
+      graph_entry_free(e);
+      return st;
     }
-    GraphEntry e{H, idx, val, loss_dev, grad_H, m, K, lr_bits, nullptr, 0};
-    const hipError_t ei = hipGraphInstantiate(&e.exec, graph, nullptr, nullptr, 0);
-    (void)hipGraphDestroy(graph);
-    if (record(c, ei)) return LST_E_HIP;
     c->graphs.push_back(e);
     hit = &c->graphs.back();
   }
   hit->last_use = ++c->graph_tick;
-  return record(c, hipGraphLaunch(hit->exec, c->stream));
+  if (record(c, hipGraphLaunch(hit->exec_a, c->stream)) ||
+      record(c, hipGraphLaunch(hit->exec_side, c->side[0])))
+    return LST_E_HIP;
+  return record(c, hipGraphLaunch(hit->exec_b, c->stream));
 }
 
 }  // namespace
@@ -778,7 +846,7 @@ int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const fl
   if (!pl) return LST_E_HIP;
   if (c->use_graphs && !c->prof_on)
     return graph_step(c, *pl, H, m, idx, val, K, lr, loss_dev, grad_H);
-  return enqueue_factored_step(c, c->stream, *pl, H, m, idx, val, K, lr, loss_dev, grad_H);
+  return enqueue_factored_step(c, *pl, H, m, idx, val, K, lr, loss_dev, grad_H);
 }
 
 int lst_use_graphs(lst_ctx *c, int32_t on) {

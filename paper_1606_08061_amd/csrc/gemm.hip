@@ -277,7 +277,9 @@ __global__ __launch_bounds__(64 * NW, 12 / NW) void gemm_kernel(const GemmBatch 
 template <int PHASE, int NW>
 __global__ __launch_bounds__(64 * NW, 12 / NW) void gemm_plan_kernel(const GemmBatch *__restrict__ bt,
                                                             const float *H, float *gH, float lr,
-                                                            const int *__restrict__ gate) {
+                                                            const int *__restrict__ gate,
+                                                            const StepSync sync) {
+  step_sync_begin(sync);
   gemm_body<NW>(*bt, H, gH, lr, gate);
 }
 
@@ -421,7 +423,8 @@ __global__ __launch_bounds__(256) void gemm16_plan_kernel(const GemmBatch *__res
                                                            const float *H, float *gH, float lr,
                                                            const int *__restrict__ gate,
                                                            const int *__restrict__ pf_idx,
-                                                           int pf_K) {
+                                                           int pf_K, const StepSync sync) {
+  step_sync_begin(sync);
   if ((int)blockIdx.x >= bt->total_tiles) {
     // Prefetch workgroup: the target rows of example j (indices outside [0, D) skipped).
     const int j = (int)blockIdx.x - bt->pf_base;
@@ -746,7 +749,7 @@ void gemm_enqueue(const GemmBatch &b, const int *gate, hipStream_t s, int phase)
 
 void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float *H,
                        float *gradH, float lr, const int *gate, hipStream_t s, int phase,
-                       const int *pf_idx, int pf_K) {
+                       const int *pf_idx, int pf_K, const StepSync &sync) {
   const int total = host.total_tiles;
   if (total == 0) return;
   if (host.t16) {
@@ -755,7 +758,7 @@ void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float 
 #define LST_PLAN16_CASE(P)                                                                     \
   case P:                                                                                      \
     LST_LAUNCH((gemm16_plan_kernel<P>), dim3(grid), dim3(256), 0, s, dev, H, gradH, lr, gate, \
-               pf_idx, pf_K);                                                                  \
+               pf_idx, pf_K, sync);                                                             \
     break;
       LST_PLAN16_CASE(GEMM_CONTRACT)
       LST_PLAN16_CASE(GEMM_ZGRAD)
@@ -764,7 +767,7 @@ void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float 
 #undef LST_PLAN16_CASE
       default:
         LST_LAUNCH((gemm16_plan_kernel<GEMM_OTHER>), dim3(grid), dim3(256), 0, s, dev, H, gradH,
-                   lr, gate, pf_idx, pf_K);
+                   lr, gate, pf_idx, pf_K, sync);
     }
     return;
   }
@@ -774,10 +777,10 @@ void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float 
   case P:                                                                                      \
     if (wide)                                                                                  \
       LST_LAUNCH((gemm_plan_kernel<P, 8>), dim3(total), dim3(512), 0, s, dev, H, gradH, lr,     \
-                 gate);                                                                        \
+                 gate, sync);                                                                   \
     else                                                                                       \
       LST_LAUNCH((gemm_plan_kernel<P, 4>), dim3(total), dim3(256), 0, s, dev, H, gradH, lr,     \
-                 gate);                                                                        \
+                 gate, sync);                                                                   \
     break;
     LST_PLAN_CASE(GEMM_CONTRACT)
     LST_PLAN_CASE(GEMM_ZGRAD)
@@ -787,10 +790,10 @@ void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float 
     default:
       if (wide)
         LST_LAUNCH((gemm_plan_kernel<GEMM_OTHER, 8>), dim3(total), dim3(512), 0, s, dev, H, gradH,
-                   lr, gate);
+                   lr, gate, sync);
       else
         LST_LAUNCH((gemm_plan_kernel<GEMM_OTHER, 4>), dim3(total), dim3(256), 0, s, dev, H, gradH,
-                   lr, gate);
+                   lr, gate, sync);
   }
 }
 

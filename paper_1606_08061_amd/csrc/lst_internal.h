@@ -32,7 +32,55 @@ extern thread_local ProfHook g_prof;
 
 
 // Sticky device error bits (mapped to lst_status by lst_sync_status).
-enum : int { FLAG_INDEX = 1, FLAG_NOT_SPD = 2, FLAG_NONFINITE = 4 };
+enum : int { FLAG_INDEX = 1, FLAG_NOT_SPD = 2, FLAG_NONFINITE = 4, FLAG_SYNC = 8 };
+
+// ---------------------------------------------------------------------------
+// Ordering between the step's two streams without host events: monotone
+// progress counters in device memory.  A kernel given a StepSync adds 1 to
+// *sig from its workgroup 0 on entry ("every kernel before me on my stream has
+// completed") and, if wx is set, waits until *wx - *wy >= wd (thread 0 polls,
+// then the workgroup acquires).  Waits are placed in single-workgroup kernels
+// only.  A producer publishes its results with release_count at its end.
+// The wait is bounded (a few tenths of a second); when it expires it sets
+// FLAG_SYNC, which also closes the gated state updates, and the kernel goes on,
+// so no wave waits forever.
+// ---------------------------------------------------------------------------
+struct StepSync {
+  const int *wx = nullptr, *wy = nullptr;
+  int wd = 0;
+  int *sig = nullptr;
+  int *flag = nullptr;
+};
+
+constexpr int kSyncSpinLimit = 1 << 18;
+
+__device__ inline void step_sync_begin(const StepSync &s) {
+  if (s.sig && blockIdx.x == 0 && threadIdx.x == 0)
+    __hip_atomic_fetch_add(s.sig, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  if (!s.wx) return;
+  if (threadIdx.x == 0) {
+    // relaxed polls (coherent loads, no cache invalidation per poll), one acquire after
+    for (int it = 0;; ++it) {
+      const int x = __hip_atomic_load(s.wx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      const int y = __hip_atomic_load(s.wy, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if ((int)((unsigned)x - (unsigned)y) >= s.wd) break;
+      if (it >= kSyncSpinLimit) {
+        atomicOr(s.flag, FLAG_SYNC);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+  }
+  __syncthreads();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+}
+
+// Called by every thread of the (single) producing workgroup after its last write.
+__device__ inline void release_count(int *cnt) {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // ---------------------------------------------------------------------------
 // Batched fp32 MFMA GEMM.
@@ -128,7 +176,7 @@ void gemm_enqueue(const GemmBatch &b, const int *gate, hipStream_t s, int phase)
 // arguments instead of the whole batch.
 void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float *H,
                        float *gradH, float lr, const int *gate, hipStream_t s, int phase,
-                       const int *pf_idx = nullptr, int pf_K = 0);
+                       const int *pf_idx = nullptr, int pf_K = 0, const StepSync &sync = {});
 
 // Large single products on 128 x 128 tiles (the naive path).  gemm_big_ok: the
 // operands meet the kernel's alignment needs (else use gemm_launch).  gemm_big_plan
@@ -155,9 +203,14 @@ hipError_t launch_gather(hipStream_t s, int m, int K, int d, int64_t D, const fl
 // through Cwork (m x m), Pbig (2 kBigBlock^2), Cp (m x kBigBlock) and Rp (kBigBlock x m).
 constexpr int kWoodburyOneWG = 128;
 constexpr int kBigBlock = 128;
+// wait: ordering before the first kernel reads dq; done: counter released after
+// R is written (also when the matrix was rejected).
 hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
                            const float *N, float *R, float *Cwork, float *Pbig, float *Cp,
-                           float *Rp, int *flag);
+                           float *Rp, int *flag, const StepSync &wait, int *done);
+
+// One workgroup: waits as `wait` says, then releases *done (if not null).
+hipError_t launch_step_sync(hipStream_t s, const StepSync &wait, int *done);
 
 hipError_t launch_mblock(hipStream_t s, int m, int K, const int *idx, const float *lvec,
                          const float *dq, const float *dA, const float *Mhat, const float *HZ,

@@ -315,11 +315,20 @@ __global__ __launch_bounds__(kGatherThreads) void gather_reg_kernel(
 
 constexpr int kMaxSortKeys = 8192;
 
+// The whole inverse on one workgroup (m <= 32 NBK); releases *done at the end,
+// whether or not the matrix was accepted.
 template <int NBK>
 __global__ __launch_bounds__(64 * wb_waves<NBK>()) void woodbury_blocked_kernel(
     int m, float lr, int unit_dq, const float *__restrict__ dq, const float *__restrict__ N,
-    float *__restrict__ R, int *__restrict__ flag) {
+    float *__restrict__ R, int *__restrict__ flag, const StepSync wait, int *__restrict__ done) {
+  step_sync_begin(wait);
   woodbury_blocked<NBK>(m, lr, unit_dq, dq, N, R, flag);
+  if (done) release_count(done);
+}
+
+__global__ void step_sync_kernel(const StepSync wait, int *__restrict__ done) {
+  step_sync_begin(wait);
+  if (done) release_count(done);
 }
 
 // ---------------------------------------------------------------------------
@@ -797,14 +806,19 @@ hipError_t launch_gather(hipStream_t s, int m, int K, int d, int64_t D, const fl
   return hipSuccess;  // checked once per step by the caller
 }
 
+hipError_t launch_step_sync(hipStream_t s, const StepSync &wait, int *done) {
+  LST_LAUNCH(step_sync_kernel, dim3(1), dim3(64), 0, s, wait, done);
+  return hipGetLastError();
+}
+
 hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
                            const float *N, float *R, float *Cwork, float *Pbig, float *Cp,
-                           float *Rp, int *flag) {
+                           float *Rp, int *flag, const StepSync &wait, int *done) {
   switch (m <= kWoodburyOneWG ? (m + 31) / 32 : 0) {
 #define LST_WB_CASE(NB)                                                                       \
   case NB:                                                                                    \
     LST_LAUNCH((woodbury_blocked_kernel<NB>), dim3(1), dim3(64 * wb_waves<NB>()), 0, s, m, lr, \
-               unit_dq, dq, N, R, flag);                                                      \
+               unit_dq, dq, N, R, flag, wait, done);                                          \
     break;
     LST_WB_CASE(1)
     LST_WB_CASE(2)
@@ -812,6 +826,7 @@ hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const fl
     LST_WB_CASE(4)
 #undef LST_WB_CASE
     default: {
+      if (wait.wx) LST_LAUNCH(step_sync_kernel, dim3(1), dim3(64), 0, s, wait, nullptr);
       const int blocks = (int)std::min<int64_t>(((int64_t)m * m + 255) / 256, 2048);
       float *PI = Pbig + kBigBlock * kBigBlock;
       LST_LAUNCH(form_c_kernel, dim3(blocks), dim3(256), 0, s, m, lr, unit_dq, dq, N, Cwork, flag);
@@ -850,6 +865,7 @@ hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const fl
         pnb = nb;
       }
       LST_LAUNCH(scale_r_kernel, dim3(blocks), dim3(256), 0, s, m, pb0, lr, unit_dq, dq, Cwork, R);
+      if (done) LST_LAUNCH(step_sync_kernel, dim3(1), dim3(64), 0, s, StepSync{}, done);
     }
   }
   return hipSuccess;  // checked once per step by the caller

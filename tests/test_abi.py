@@ -46,7 +46,8 @@ def test_every_declared_symbol_is_exported(L):
 
 def test_status_strings(L):
     for code, name in [(0, "LST_OK"), (-1, "LST_E_ARG"), (-3, "LST_E_INDEX"),
-                       (-4, "LST_E_NOT_SPD"), (-5, "LST_E_NONFINITE"), (7, "LST_E_UNKNOWN")]:
+                       (-4, "LST_E_NOT_SPD"), (-5, "LST_E_NONFINITE"), (-8, "LST_E_SYNC"),
+                       (7, "LST_E_UNKNOWN")]:
         assert lst.status_string(code) == name
 
 

@@ -143,3 +143,29 @@ def test_naive_index_error_keeps_W():
     assert n.sync_status() == lst.LST_E_INDEX
     assert torch.equal(n.W, W0)
     n.close()
+
+
+@pytest.mark.parametrize("m", [8, 200])
+def test_woodbury_release_withheld(monkeypatch, m):
+    """The two streams of a step are ordered by device progress counters.  With the
+    Woodbury branch's release withheld (a test hook read at creation), the state
+    updates' bounded wait must expire: the step reports LST_E_SYNC, writes no state,
+    and the kernels all finish (the wait, not the GPU, gives up)."""
+    w = Workload("t", LOSS_SQUARED, 1000, 32, m, 2)
+    s = Stream(w)
+    monkeypatch.setenv("LST_TEST_WITHHOLD_WOODBURY_RELEASE", "1")
+    f = make_factored(w, s.V0)
+    monkeypatch.delenv("LST_TEST_WITHHOLD_WOODBURY_RELEASE")
+    snap = _state(f)
+    H, idx, val = s.batch()
+    f.step(*to_dev(H, idx, val), w.lr)
+    assert f.sync_status() == lst.LST_E_SYNC
+    assert _same(f, snap)
+    f.close()
+    # a context created without the hook is unaffected
+    g = make_factored(w, s.V0)
+    ref = oracle_step(s.V0.astype(np.float64), H, idx, val, w)
+    loss, grad = g.step(*to_dev(H, idx, val), w.lr)
+    assert g.sync_status() == lst.LST_OK
+    assert abs(loss.item() - ref.loss) <= 1e-4 * abs(ref.loss)
+    g.close()
