@@ -29,8 +29,13 @@
  *     allowed and their V updates are summed in a fixed order.
  *   - Streams: every call is enqueued on the stream given at creation (a
  *     hipStream_t passed as void*; NULL = the null stream) and returns without
- *     synchronising, except lst_sync_status and lst_init_factored.  A context
- *     must not be used from two host threads at once.
+ *     synchronising, except lst_sync_status and lst_init_factored.  A factored
+ *     step also uses a side stream of the context (the Woodbury inverse); the
+ *     two are ordered by progress counters in device memory (the side stream
+ *     starts once the step has started on the given stream, the state updates
+ *     wait for the side stream's result), so the caller only orders work against
+ *     the given stream.  A context must not be used from two host threads at
+ *     once.
  *   - Errors: every call returns an lst_status.  Argument errors detectable on
  *     the host are returned at once and nothing is enqueued.  Data-dependent
  *     errors found on the device (an index outside [-1, D), a Woodbury matrix
@@ -134,9 +139,9 @@ int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const fl
 
 /*
  * lst_use_graphs -- on (default) or off.  When on, lst_step records the work of
- * a step as a HIP graph the first time it sees a given (H, idx, val, loss_dev,
- * grad_H, m, K, lr) and replays that graph, with one launch, whenever the same
- * arguments recur (up to 256 graphs per context, least recently used evicted);
+ * a step as HIP graphs (one per stream part) the first time it sees a given (H,
+ * idx, val, loss_dev, grad_H, m, K, lr) and replays them, three graph launches,
+ * whenever the same arguments recur (up to 256 per context, least recently used evicted);
  * the kernels and results are the same as without graphs.  Callers that reuse
  * their input buffers from step to step get one graph.  While the profiling
  * hook is on, steps are enqueued kernel by kernel.
@@ -150,9 +155,10 @@ int lst_use_graphs(lst_ctx *c, int32_t on);
 int lst_materialize_W(lst_ctx *c, float *W, int64_t ldw);
 
 /*
- * lst_sync_status -- synchronises the context's stream, returns the sticky
+ * lst_sync_status -- synchronises the context's streams, returns the sticky
  * device error (LST_OK if none) and clears it.  Also returns LST_E_HIP if a
- * kernel launch or the synchronisation failed.
+ * kernel launch or the synchronisation failed.  After LST_E_SYNC it also resets
+ * the progress counters that order the two streams.
  */
 int lst_sync_status(lst_ctx *c);
 
@@ -178,7 +184,8 @@ int lst_naive_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, co
 
 /* Phases of a step, as timed by the profiling hook below.  The Gram product and
    the Woodbury inverse run on a side stream of the context, overlapping the main
-   chain; the other phases run in order on the context's stream. */
+   chain; the other phases run in order on the context's stream.  GRAM includes
+   the wait for the step's start and MID the wait for the inverse. */
 enum lst_phase {
   LST_PHASE_CONTRACT = 0,      /* H^ = Q H, H~ = U H, X = U^{-T} H (matrix cores)          */
   LST_PHASE_GATHER = 1,        /* gather of the K target rows of V, loss epilogue, G       */
