@@ -138,13 +138,15 @@ int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const fl
              int32_t K, float lr, float *loss_dev, float *grad_H);
 
 /*
- * lst_use_graphs -- on (default) or off.  When on, lst_step records the work of
+ * lst_use_graphs -- off (default) or on.  When on, lst_step records the work of
  * a step as HIP graphs (one per stream part) the first time it sees a given (H,
  * idx, val, loss_dev, grad_H, m, K, lr) and replays them, three graph launches,
- * whenever the same arguments recur (up to 256 per context, least recently used evicted);
- * the kernels and results are the same as without graphs.  Callers that reuse
- * their input buffers from step to step get one graph.  While the profiling
- * hook is on, steps are enqueued kernel by kernel.
+ * whenever the same arguments recur (up to 256 per context, least recently used
+ * evicted); the kernels and results are the same as without graphs.  Off by
+ * default: with the streams ordered by device counters, direct launches cost
+ * the host less than the graph launches and leave shorter gaps between kernels
+ * on the GPU.  While the profiling hook is on, steps are enqueued kernel by
+ * kernel.
  */
 int lst_use_graphs(lst_ctx *c, int32_t on);
 

@@ -365,7 +365,7 @@ int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max
   c->Q = Q;
   c->ldd = ldd;
   c->last_err = hipSuccess;
-  c->use_graphs = true;
+  c->use_graphs = false;
   c->withhold_release = std::getenv("LST_TEST_WITHHOLD_WOODBURY_RELEASE") != nullptr;
   st = alloc_ws(c, carve_factored);
   if (st == LST_OK) st = side_create(c);
