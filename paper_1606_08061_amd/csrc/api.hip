@@ -78,7 +78,7 @@ struct lst_ctx {
   size_t ws_bytes;
   float *Hhat, *Htil, *X, *G, *Atil, *Zhat, *gradH, *Yw, *Zq, *P;
   float *N, *Mhat, *HZ, *M, *R, *Cwork;
-  float *Pbig, *Cp, *Rp;  // blocked Woodbury inverse for m > 256
+  float *Pbig, *Cp, *Rp;  // blocked Woodbury inverse for m > kWoodburyOneWG
   float *dq, *lvec, *dA;
   int *flag;
   // progress counters ordering the two streams of a factored step: [0] contraction

@@ -387,17 +387,30 @@ __global__ __launch_bounds__(256) void pivot_block_kernel(int m, int b0, int nb,
   __syncthreads();
   const int lane = threadIdx.x & 63, j = lane & 31, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  floatx16 acc[TPW];
+  // All loads issued first and pinned (none moved under the padding conditions).
+  float raw[TPW][16];
 #pragma unroll
   for (int s = 0; s < TPW; ++s) {
     const int t = wave + W * s;
     const int col = (t % NBK) * 32 + j;
     const float *ap = A + (int64_t)b0 * m + b0 + min(col, nb - 1);
 #pragma unroll
+    for (int r = 0; r < 16; ++r)
+      raw[s][r] = ap[(int64_t)min((t / NBK) * 32 + acc_row(h, r), nb - 1) * m];
+  }
+#pragma unroll
+  for (int s = 0; s < TPW; ++s)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) asm volatile("" : "+v"(raw[s][r]));
+  floatx16 acc[TPW];
+#pragma unroll
+  for (int s = 0; s < TPW; ++s) {
+    const int t = wave + W * s;
+    const int col = (t % NBK) * 32 + j;
+#pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int row = (t / NBK) * 32 + acc_row(h, r);
-      const float v = ap[(int64_t)min(row, nb - 1) * m];
-      acc[s][r] = (row < nb && col < nb) ? v : ((row == col) ? 1.f : 0.f);
+      acc[s][r] = (row < nb && col < nb) ? raw[s][r] : ((row == col) ? 1.f : 0.f);
     }
   }
   if (!blocked_gj<NBK, W, TPW>(acc, sh, wave, lane)) {
