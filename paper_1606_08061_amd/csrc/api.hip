@@ -602,8 +602,11 @@ void build_plan(const lst_ctx *c, int m, GemmBatch (&b)[kPlanBatches]) {
   qd.ldb2 = d;
   qd.K2 = m;
   b[4].d[1] = qd;
+  // P is needed for the spherical softmax only: for squared error S = I, and with
+  // 2 eta N = I - C one has I + N R = I + (I - C) C^{-1} = C^{-1}, so P = C^{-1} X
+  // = Yw / (2 eta) and the V update (eq. updateV) uses Yw with the factor 1/2.
   b[4].d[2] = gemm_desc(m, d, m, c->N, m, 0, c->Yw, d, 1, c->P, d, 1.f, c->X, d, 1.f);
-  b[4].n = 3;
+  b[4].n = c->loss == LST_LOSS_SQUARED ? 2 : 3;
   // 16 x 16 tiles where the outputs are m x m or m x d with long k (Gram product,
   // contractions, Z^): four times the workgroups of 32 x 32 tiles.  The d x d
   // updates (short k = m, read-modify-write of the state) keep 32 x 32 tiles.
@@ -754,7 +757,10 @@ int enqueue_main_b(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *
 
   // V_r -= eta sum dl/dA P_j over the slots of each distinct target row (eq. updateV).
   prof(c, LST_PHASE_SCATTER, true);
-  launch_scatter(s, m, K, c->d, lr, idx, c->dA, c->P, c->V, c->ldv, c->flag);
+  if (c->loss == LST_LOSS_SQUARED)  // eta P = Yw / 2 (see build_plan)
+    launch_scatter(s, m, K, c->d, 0.5f, idx, c->dA, c->Yw, c->V, c->ldv, c->flag);
+  else
+    launch_scatter(s, m, K, c->d, lr, idx, c->dA, c->P, c->V, c->ldv, c->flag);
   prof(c, LST_PHASE_SCATTER, false);
   // Kernel launches above are not checked one by one: a launch error stays pending
   // and is reported here.
