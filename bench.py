@@ -249,9 +249,14 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="factored vs naive over the D x d sweep instead of the default line")
     ap.add_argument("--sweep-steps", type=int, default=20)
+    ap.add_argument("--one-stream", action="store_true",
+                    help="enqueue the whole step on one stream (for hardware counter "
+                         "collection, which runs one dispatch at a time)")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                     help="also run one plain device copy of MIB MiB (hardware-counter calibration)")
     args = ap.parse_args()
+    if args.one_stream:
+        os.environ["LST_ONE_STREAM"] = "1"  # read by the library when a context is created
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: the factored step is measured on one GPU's "
               "share (multi-GPU sharding of V by rows is described but not built)",

@@ -36,6 +36,9 @@
  *     wait for the side stream's result), so the caller only orders work against
  *     the given stream.  A context must not be used from two host threads at
  *     once.
+ *     With the environment variable LST_ONE_STREAM set when the context is
+ *     created, the side stream's work goes on the given stream too (for tools
+ *     that run one dispatch at a time, e.g. hardware counter collection).
  *   - Errors: every call returns an lst_status.  Argument errors detectable on
  *     the host are returned at once and nothing is enqueued.  Data-dependent
  *     errors found on the device (an index outside [-1, D), a Woodbury matrix
@@ -186,8 +189,8 @@ int lst_naive_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, co
 
 /* Phases of a step, as timed by the profiling hook below.  The Gram product and
    the Woodbury inverse run on a side stream of the context, overlapping the main
-   chain; the other phases run in order on the context's stream.  GRAM includes
-   the wait for the step's start and MID the wait for the inverse. */
+   chain; the other phases run in order on the context's stream.  The waits
+   between the streams are not part of any phase. */
 enum lst_phase {
   LST_PHASE_CONTRACT = 0,      /* H^ = Q H, H~ = U H, X = U^{-T} H (matrix cores)          */
   LST_PHASE_GATHER = 1,        /* gather of the K target rows of V, loss epilogue, G       */

@@ -106,6 +106,12 @@ struct lst_ctx {
   // the Woodbury branch never releases its counter, so the state-update wait of
   // every step expires (bounded) and reports LST_E_SYNC
   bool withhold_release;
+  // environment variable LST_ONE_STREAM at creation: the side stream's work is
+  // enqueued on the context's stream instead, after the main chain up to M (the
+  // waits are then met on arrival).  For tools that run one dispatch at a time,
+  // such as hardware counter collection, under which a wait on another stream's
+  // progress could not be met.
+  bool one_stream;
   std::vector<GraphEntry> graphs;
   uint64_t graph_tick;
 };
@@ -367,6 +373,7 @@ int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max
   c->last_err = hipSuccess;
   c->use_graphs = false;
   c->withhold_release = std::getenv("LST_TEST_WITHHOLD_WOODBURY_RELEASE") != nullptr;
+  c->one_stream = std::getenv("LST_ONE_STREAM") != nullptr;
   st = alloc_ws(c, carve_factored);
   if (st == LST_OK) st = side_create(c);
   if (st != LST_OK) {
@@ -720,8 +727,8 @@ int enqueue_side(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *H,
   started.wy = c->cnt + 1;
   started.wd = 1;
   started.flag = c->flag;
-  prof(c, LST_PHASE_GRAM, true);
   launch_step_sync(s, started, nullptr);
+  prof(c, LST_PHASE_GRAM, true);
   gemm_enqueue_plan(pl.b[0], pl.dev + 0, H, gH, lr, nullptr, s, GEMM_OTHER);
   prof(c, LST_PHASE_GRAM, false);
   StepSync gathered;
@@ -747,8 +754,8 @@ int enqueue_main_b(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *
   joined.wy = c->cnt + 0;
   joined.wd = 0;
   joined.flag = c->flag;
-  prof(c, LST_PHASE_MID, true);
   launch_step_sync(s, joined, nullptr);
+  prof(c, LST_PHASE_MID, true);
   gemm_enqueue_plan(pl.b[3], pl.dev + 3, H, gH, lr, c->flag, s, GEMM_MID);
   prof(c, LST_PHASE_MID, false);
   prof(c, LST_PHASE_UPDATE, true);
@@ -772,7 +779,7 @@ int enqueue_factored_step(lst_ctx *c, const PlanEntry &pl, const float *H, int32
                           float *loss_dev, float *grad_H) {
   float *gH = grad_H ? grad_H : c->gradH;
   int st = enqueue_main_a(c, c->stream, pl, H, m, idx, val, K, lr, loss_dev, gH);
-  if (st == LST_OK) st = enqueue_side(c, c->side[0], pl, H, m, lr, gH);
+  if (st == LST_OK) st = enqueue_side(c, c->one_stream ? c->stream : c->side[0], pl, H, m, lr, gH);
   if (st == LST_OK) st = enqueue_main_b(c, c->stream, pl, H, m, idx, K, lr, gH);
   return st;
 }
@@ -832,7 +839,7 @@ int graph_step(lst_ctx *c, const PlanEntry &pl, const float *H, int32_t m, const
   }
   hit->last_use = ++c->graph_tick;
   if (record(c, hipGraphLaunch(hit->exec_a, c->stream)) ||
-      record(c, hipGraphLaunch(hit->exec_side, c->side[0])))
+      record(c, hipGraphLaunch(hit->exec_side, c->one_stream ? c->stream : c->side[0])))
     return LST_E_HIP;
   return record(c, hipGraphLaunch(hit->exec_b, c->stream));
 }
