@@ -124,6 +124,110 @@ __device__ __forceinline__ bool gj32_invert_staged(float *tile, int lane) {
   return true;
 }
 
+// The same inversion as four 16 x 16 blocks, [A11 A12; A21 A22]^{-1} by the
+// Schur complement S = A22 - A21 A11^{-1} A12: two 16 x 16 Gauss-Jordan
+// inversions (the first 16 pivots, then the 16 pivots of S: exactly the 32
+// pivots of the unblocked elimination) and six 16 x 16 products on
+// v_mfma_f32_16x16x4_f32.  A 16 x 16 block sits in the accumulator layout of that
+// instruction: lane c + 16 g holds rows 4g .. 4g+3 of column c, so a pivot step
+// costs four multiply-adds per lane instead of sixteen.  Column K reaches the
+// lane's 16-lane row by DPP row_newbcast, row K the whole wavefront by two
+// permlane swaps, the pivot by readlane.  `scr` holds three staged 16 x 16
+// matrices (row stride kS16) for the products' left operands.
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+constexpr int kS16 = 20;  // LDS row stride (floats) of a staged 16 x 16 matrix: 16-byte rows
+
+template <int K>
+__device__ __forceinline__ void gj16_step(float (&t)[4], int g, int c, bool &bad) {
+  constexpr int QK = K >> 2, RK = K & 3;
+  const float p = lane_read(t[RK], 16 * QK + K);
+  bad |= !(p > 0.f && p < INFINITY);  // checked once after the 16 steps
+  float f[4];                          // column K at rows 4g + r
+#pragma unroll
+  for (int r = 0; r < 4; ++r) f[r] = row_newbcast<K>(t[r]);
+  const float rw = row16_broadcast<QK>(t[RK]);  // row K at column c
+  float ip = __builtin_amdgcn_rcpf(p);
+  ip = fmaf(ip, fmaf(-p, ip, 1.f), ip);  // one Newton step on the hardware reciprocal
+  const float gc = (c == K) ? 1.f + ip : rw * ip;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float fr = (r == RK && g == QK) ? p - 1.f : f[r];
+    t[r] = fmaf(-fr, gc, t[r]);
+  }
+}
+
+template <int K>
+__device__ __forceinline__ void gj16_from(float (&t)[4], int g, int c, bool &bad) {
+  if constexpr (K < 16) {
+    gj16_step<K>(t, g, c, bad);
+    gj16_from<K + 1>(t, g, c, bad);
+  }
+}
+
+// Row-major 16 x 16 (stride ld) <-> accumulator layout.
+__device__ __forceinline__ void ld16(const float *m, int ld, float (&x)[4], int g, int c) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) x[r] = m[(4 * g + r) * ld + c];
+}
+__device__ __forceinline__ void st16(float *m, int ld, const float (&x)[4], int g, int c) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) m[(4 * g + r) * ld + c] = x[r];
+}
+
+// x (accumulator layout) += sgn * A B, A row-major in LDS (stride lda, a multiple
+// of 4), B in accumulator layout: k = 4g + s in instruction s.
+__device__ __forceinline__ void mm16(float (&x)[4], const float *A, int lda, const float (&b)[4],
+                                     int g, int c, float sgn) {
+  const float4 a = *reinterpret_cast<const float4 *>(A + c * lda + 4 * g);
+  floatx4 acc = {x[0], x[1], x[2], x[3]};
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(sgn * a.x, b[0], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(sgn * a.y, b[1], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(sgn * a.z, b[2], acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(sgn * a.w, b[3], acc, 0, 0, 0);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) x[r] = acc[r];
+}
+
+// Inverts the 32 x 32 block staged row-major (stride kTileLd) in `tile` by one
+// wavefront and leaves the inverse there; false (uniformly) on a bad pivot.
+__device__ __forceinline__ bool gj32_invert_schur(float *tile, float *scr, int lane) {
+  const int c = lane & 15, g = lane >> 4;
+  float *s0 = scr, *s1 = scr + 16 * kS16, *s2 = scr + 32 * kS16;
+  bool bad = false;
+  float x11[4], a12[4], t1[4], x22[4];
+  ld16(tile, kTileLd, x11, g, c);                        // A11
+  ld16(tile + 16, kTileLd, a12, g, c);                   // A12
+  ld16(tile + 16 * kTileLd + 16, kTileLd, x22, g, c);    // A22
+  gj16_from<0>(x11, g, c, bad);                          // X11 = A11^{-1}
+#pragma unroll
+  for (int r = 0; r < 4; ++r) t1[r] = 0.f;
+  mm16(t1, tile + 16 * kTileLd, kTileLd, x11, g, c, 1.f);  // T1 = A21 X11
+  st16(s0, kS16, t1, g, c);
+  st16(s1, kS16, x11, g, c);
+  wave_lds_sync();
+  mm16(x22, s0, kS16, a12, g, c, -1.f);                 // S = A22 - T1 A12
+  gj16_from<0>(x22, g, c, bad);                          // X22 = S^{-1}
+  float t2[4] = {0.f, 0.f, 0.f, 0.f};
+  mm16(t2, s1, kS16, a12, g, c, 1.f);                    // T2 = X11 A12
+  st16(s2, kS16, t2, g, c);
+  wave_lds_sync();
+  float x12[4] = {0.f, 0.f, 0.f, 0.f};
+  mm16(x12, s2, kS16, x22, g, c, -1.f);                  // X12 = -T2 X22
+  st16(s1, kS16, x22, g, c);                             // (X11 staged copy no longer needed)
+  st16(s0, kS16, x12, g, c);
+  wave_lds_sync();
+  float x21[4] = {0.f, 0.f, 0.f, 0.f};
+  mm16(x21, s1, kS16, t1, g, c, -1.f);                   // X21 = -X22 T1
+  mm16(x11, s0, kS16, t1, g, c, -1.f);                   // X11' = X11 - X12 T1
+  if (bad) return false;
+  wave_lds_sync();
+  st16(tile, kTileLd, x11, g, c);
+  st16(tile + 16, kTileLd, x12, g, c);
+  st16(tile + 16 * kTileLd, kTileLd, x21, g, c);
+  st16(tile + 16 * kTileLd + 16, kTileLd, x22, g, c);
+  return true;
+}
+
 // Operand fetch of a staged tile: lane (i or j, h) reads its 16 values at
 // column (row) offsets acc_row(h, 0..15), four 16-byte reads.
 __device__ __forceinline__ void lds_operand(const float *tile, int idx, int h, float (&o)[16]) {
@@ -223,7 +327,7 @@ __device__ __forceinline__ bool blocked_gj(floatx16 (&acc)[TPW], GjLds<NBK> &sh,
       for (int r = 0; r < 16; ++r) pv[r] = p[r];
       stage_a(sh.pa[buf], pv, j, h);  // the pivot block, row-major
       wave_lds_sync();
-      if (gj32_invert_staged(sh.pa[buf], lane)) {  // P replaces it (A-operand layout)
+      if (gj32_invert_schur(sh.pa[buf], sh.pb[buf], lane)) {  // P replaces it (A-operand layout)
         wave_lds_sync();
 #pragma unroll
         for (int r = 0; r < 16; ++r) pv[r] = sh.pa[buf][acc_row(h, r) * kTileLd + j];
