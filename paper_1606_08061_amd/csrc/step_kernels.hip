@@ -334,7 +334,7 @@ __global__ void step_sync_kernel(const StepSync wait, int *__restrict__ done) {
 // ---------------------------------------------------------------------------
 // Larger m: the same block step with kBigBlock-row pivot blocks on the m x m
 // matrix A (= C) in global memory, three launches per block b:
-//   pivot kernel   P = A_bb^{-1} (blocked_gj on one workgroup), PI = P + I;
+//   pivot kernel   P = A_bb^{-1} (the blocked elimination on one workgroup), PI = P + I;
 //   row launch     Rp_:,j = P A_b,j for the columns j outside b, Rp_:,b = P + I,
 //                  and the column panel copy Cp = A_:,b;
 //   trailing launch A_i,: += -Cp_i Rp for the rows i outside b, A_b,: = Rp.
@@ -375,58 +375,83 @@ __global__ void scale_r_kernel(int m, int lb0, float lr, int unit_dq, const floa
 // Pivot block b0 .. b0+nb-1 (nb <= kBigBlock) of A: P and PI = P + I
 // (kBigBlock^2 each, identity-padded).  First removes the I left on the
 // previous diagonal block (rows pb0 .. pb0+pnb-1; pnb = 0 for none).
-__global__ __launch_bounds__(256) void pivot_block_kernel(int m, int b0, int nb, int pb0, int pnb,
-                                                          float *__restrict__ A,
-                                                          float *__restrict__ P,
-                                                          float *__restrict__ PI,
-                                                          int *__restrict__ flag) {
-  constexpr int NBK = kBigBlock / 32, W = 4, TPW = NBK * NBK / W;
+constexpr int kPivotNbk = kBigBlock / 32;
+
+__global__ __launch_bounds__(64 * wb_waves<kPivotNbk>()) void pivot_block_kernel(
+    int m, int b0, int nb, int pb0, int pnb, float *__restrict__ A, float *__restrict__ P,
+    float *__restrict__ PI, int *__restrict__ flag) {
+  constexpr int NBK = kPivotNbk;
   __shared__ GjLds<NBK> sh;
-  if (threadIdx.x == 0) sh.bad = 0;
+  if (threadIdx.x == 0) sh.bad[0] = sh.bad[1] = 0;
   for (int i = threadIdx.x; i < pnb; i += blockDim.x) A[(int64_t)(pb0 + i) * m + pb0 + i] -= 1.f;
   __syncthreads();
   const int lane = threadIdx.x & 63, j = lane & 31, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   // All loads issued first and pinned (none moved under the padding conditions).
-  float raw[TPW][16];
+  constexpr int NW = wb_workers<NBK>(), NS = wb_sets<NBK>();
+  const float *ab = A + (int64_t)b0 * m + b0;
+  if (wave == NW) {  // the inverting wavefront: the pivot block A_00
+    float raw[16];
 #pragma unroll
-  for (int s = 0; s < TPW; ++s) {
-    const int t = wave + W * s;
-    const int col = (t % NBK) * 32 + j;
-    const float *ap = A + (int64_t)b0 * m + b0 + min(col, nb - 1);
+    for (int r = 0; r < 16; ++r) raw[r] = ab[(int64_t)min(acc_row(h, r), nb - 1) * m + min(j, nb - 1)];
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      raw[s][r] = ap[(int64_t)min((t / NBK) * 32 + acc_row(h, r), nb - 1) * m];
-  }
-#pragma unroll
-  for (int s = 0; s < TPW; ++s)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) asm volatile("" : "+v"(raw[s][r]));
-  floatx16 acc[TPW];
-#pragma unroll
-  for (int s = 0; s < TPW; ++s) {
-    const int t = wave + W * s;
-    const int col = (t % NBK) * 32 + j;
+    for (int r = 0; r < 16; ++r) asm volatile("" : "+v"(raw[r]));
+    floatx16 a00;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int row = (t / NBK) * 32 + acc_row(h, r);
-      acc[s][r] = (row < nb && col < nb) ? raw[s][r] : ((row == col) ? 1.f : 0.f);
+      const int row = acc_row(h, r);
+      a00[r] = (row < nb && j < nb) ? raw[r] : ((row == j) ? 1.f : 0.f);
+    }
+    gj_inverter<NBK>(a00, sh, lane);
+    return;
+  }
+  floatx16 acc[NS][NBK];
+  {
+    float raw[NS][NBK][16];
+#pragma unroll
+    for (int t = 0; t < NS; ++t) {
+      if (wave + NW * t >= NBK) continue;  // no such tile column
+      const float *ap = ab + min(32 * (wave + NW * t) + j, nb - 1);
+#pragma unroll
+      for (int s = 0; s < NBK; ++s)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          raw[t][s][r] = ap[(int64_t)min(32 * s + acc_row(h, r), nb - 1) * m];
+    }
+#pragma unroll
+    for (int t = 0; t < NS; ++t)
+#pragma unroll
+      for (int s = 0; s < NBK; ++s)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) asm volatile("" : "+v"(raw[t][s][r]));
+#pragma unroll
+    for (int t = 0; t < NS; ++t) {
+      const int col = 32 * (wave + NW * t) + j;
+#pragma unroll
+      for (int s = 0; s < NBK; ++s)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = 32 * s + acc_row(h, r);
+          acc[t][s][r] = (row < nb && col < nb) ? raw[t][s][r] : ((row == col) ? 1.f : 0.f);
+        }
     }
   }
-  if (!blocked_gj<NBK, W, TPW>(acc, sh, wave, lane)) {
+  if (!gj_workers<NBK>(acc, sh, wave, lane)) {
     if (threadIdx.x == 0) atomicOr(flag, FLAG_NOT_SPD);
     return;
   }
 #pragma unroll
-  for (int s = 0; s < TPW; ++s) {
-    const int t = wave + W * s;
-    const int col = (t % NBK) * 32 + j;
+  for (int t = 0; t < NS; ++t) {
+    if (wave + NW * t >= NBK) continue;
+    const int col = 32 * (wave + NW * t) + j;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = (t / NBK) * 32 + acc_row(h, r);
-      P[row * kBigBlock + col] = acc[s][r];
-      PI[row * kBigBlock + col] = acc[s][r] + ((row == col) ? 1.f : 0.f);
-    }
+    for (int s = 0; s < NBK; ++s)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 32 * s + acc_row(h, r);
+        P[row * kBigBlock + col] = acc[t][s][r];
+        PI[row * kBigBlock + col] = acc[t][s][r] + ((row == col) ? 1.f : 0.f);
+      }
   }
 }
 
@@ -846,8 +871,8 @@ hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const fl
       int pb0 = 0, pnb = 0;
       for (int b0 = 0; b0 < m; b0 += kBigBlock) {
         const int nb = std::min(kBigBlock, m - b0), e0 = b0 + nb;
-        LST_LAUNCH(pivot_block_kernel, dim3(1), dim3(256), 0, s, m, b0, nb, pb0, pnb, Cwork, Pbig,
-                   PI, flag);
+        LST_LAUNCH(pivot_block_kernel, dim3(1), dim3(64 * wb_waves<kPivotNbk>()), 0, s, m, b0, nb,
+                   pb0, pnb, Cwork, Pbig, PI, flag);
         float *Ab = Cwork + (int64_t)b0 * m;
         GemmBatch r{};
         int n = 0;

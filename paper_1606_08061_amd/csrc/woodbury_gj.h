@@ -12,8 +12,9 @@ namespace {
 // Blocked Gauss-Jordan inverse on the matrix cores.
 //
 // The mp x mp matrix (mp = 32 NBK >= m, padded with the identity) lives in
-// MFMA accumulator registers as NBK x NBK tiles of 32 x 32, tile t owned by
-// wavefront t % W.  In accumulator layout lane l = j + 32 h holds column j of a
+// MFMA accumulator registers as NBK x NBK tiles of 32 x 32: wavefront w < NBK
+// holds tile column w (acc[i] = tile (i, w)) and wavefront NBK inverts the
+// pivot blocks.  In accumulator layout lane l = j + 32 h holds column j of a
 // tile and register r holds row acc_row(h, r).  Block step kb with pivot block
 // P = A_kb,kb^{-1} is, in place,
 //   A_kb,j <- P A_kb,j,   A_ij <- A_ij - A_i,kb (P A_kb,j),
@@ -21,11 +22,10 @@ namespace {
 // the block form of the scalar step below; after NBK block steps the tiles hold
 // the inverse.  The products run on v_mfma_f32_32x32x2f32 with the k index of
 // instruction r taken as acc_row(h, r) in lane-half h, so a tile held in
-// registers is directly the B operand of a product; the other operands come
-// from LDS copies of the column panel, the new row panel and P.  Since every
-// pivot block is a Schur complement of C, the pivots met inside the 32 x 32
-// inversions are exactly those of unblocked elimination: all are positive iff
-// C is positive definite.
+// registers is directly the B operand of a product: a column owner needs from
+// LDS only P and the column panel -A_i,kb.  Since every pivot block is a Schur
+// complement of C, the pivots met inside the 32 x 32 inversions are exactly
+// those of unblocked elimination: all are positive iff C is positive definite.
 // ---------------------------------------------------------------------------
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
@@ -34,7 +34,7 @@ __device__ __forceinline__ int acc_row(int h, int r) { return 4 * h + (r & 3) + 
 constexpr int kTileLd = 36;  // LDS row stride (floats) of a staged 32 x 32 tile: 16-byte rows
 constexpr int kTileSz = 32 * kTileLd;
 
-// One scalar Gauss-Jordan step on pivot K (p = A_KK) of a 32 x 32 block:
+// One scalar Gauss-Jordan step on pivot K (p = A_KK) of a 16 x 16 block:
 //   A' = X - f g^T,  X = A with column K replaced by e_K,
 //   f_i = A_iK (i != K), f_K = p - 1,   g_j = A_Kj / p (j != K), g_K = 1 / p,
 // i.e. A'_Kj = A_Kj / p, A'_iK = -A_iK / p, A'_KK = 1 / p, A'_ij = A_ij - A_iK A_Kj / p.
@@ -50,12 +50,9 @@ __device__ __forceinline__ float lane_read(float v, int lane) {
 // order; the fence stops the compiler from moving a read above the write).
 __device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "wavefront"); }
 
-// The pivot-block inversion runs in the layout the cross-lane moves favour:
-// lane 16 q + c holds rows 8q .. 8q+7 of columns 2c and 2c+1, t[8e + r] = T[8q + r][2c + e].
-// Column K at the lane's rows sits in lane c = K/2 of the lane's own 16-lane row
-// (DPP row_newbcast); row K at the lane's columns sits in 16-lane row K/8 (two
-// permlane swaps broadcast it to all four rows); the pivot comes from readlane.
-// No LDS round trip is on the serial path.
+// Cross-lane moves of the 16 x 16 Gauss-Jordan steps below: DPP row_newbcast
+// (one lane of each 16-lane row to the whole row) and two permlane swaps (one
+// 16-lane row to all four).
 template <int N>
 __device__ __forceinline__ float row_newbcast(float v) {  // lane N of each 16-lane row
   return __int_as_float(
@@ -71,61 +68,8 @@ __device__ __forceinline__ float row16_broadcast(float v) {  // 16-lane row Q to
   return __uint_as_float((Q & 1) ? b[1] : b[0]);
 }
 
-template <int K>
-__device__ __forceinline__ void gjr_step(float (&t)[16], int q, int c, bool &bad) {
-  constexpr int QK = K >> 3, RK = K & 7, CK = K >> 1, EK = K & 1;
-  const float p = lane_read(t[8 * EK + RK], 16 * QK + CK);
-  bad |= !(p > 0.f && p < INFINITY);  // checked once after the 32 steps
-  float f[8];                          // column K at rows 8q + r
-#pragma unroll
-  for (int r = 0; r < 8; ++r) f[r] = row_newbcast<CK>(t[8 * EK + r]);
-  float rw[2];  // row K at columns 2c + e
-#pragma unroll
-  for (int e = 0; e < 2; ++e) rw[e] = row16_broadcast<QK>(t[8 * e + RK]);
-  float ip = __builtin_amdgcn_rcpf(p);
-  ip = fmaf(ip, fmaf(-p, ip, 1.f), ip);  // one Newton step on the hardware reciprocal
-  float g[2];
-#pragma unroll
-  for (int e = 0; e < 2; ++e) g[e] = (e == EK && c == CK) ? 1.f + ip : rw[e] * ip;
-#pragma unroll
-  for (int e = 0; e < 2; ++e)
-#pragma unroll
-    for (int r = 0; r < 8; ++r) {
-      const float fr = (r == RK && q == QK) ? p - 1.f : f[r];
-      t[8 * e + r] = fmaf(-fr, g[e], t[8 * e + r]);
-    }
-}
-
-template <int K>
-__device__ __forceinline__ void gjr_from(float (&t)[16], int q, int c, bool &bad) {
-  if constexpr (K < 32) {
-    gjr_step<K>(t, q, c, bad);
-    gjr_from<K + 1>(t, q, c, bad);
-  }
-}
-
-// Inverts the 32 x 32 block staged row-major (stride kTileLd) in `tile` by one
-// wavefront and leaves the inverse there; false (uniformly) on a bad pivot.
-__device__ __forceinline__ bool gj32_invert_staged(float *tile, int lane) {
-  const int q = lane >> 4, c = lane & 15;
-  float t[16];
-#pragma unroll
-  for (int r = 0; r < 8; ++r) {
-    const float2 v = *reinterpret_cast<const float2 *>(tile + (8 * q + r) * kTileLd + 2 * c);
-    t[r] = v.x;
-    t[8 + r] = v.y;
-  }
-  bool bad = false;
-  gjr_from<0>(t, q, c, bad);
-  if (bad) return false;
-#pragma unroll
-  for (int r = 0; r < 8; ++r)
-    *reinterpret_cast<float2 *>(tile + (8 * q + r) * kTileLd + 2 * c) = make_float2(t[r], t[8 + r]);
-  return true;
-}
-
-// The same inversion as four 16 x 16 blocks, [A11 A12; A21 A22]^{-1} by the
-// Schur complement S = A22 - A21 A11^{-1} A12: two 16 x 16 Gauss-Jordan
+// Inversion of a 32 x 32 pivot block as four 16 x 16 blocks, [A11 A12; A21 A22]^{-1}
+// by the Schur complement S = A22 - A21 A11^{-1} A12: two 16 x 16 Gauss-Jordan
 // inversions (the first 16 pivots, then the 16 pivots of S: exactly the 32
 // pivots of the unblocked elimination) and six 16 x 16 products on
 // v_mfma_f32_16x16x4_f32.  A 16 x 16 block sits in the accumulator layout of that
@@ -188,43 +132,51 @@ __device__ __forceinline__ void mm16(float (&x)[4], const float *A, int lda, con
   for (int r = 0; r < 4; ++r) x[r] = acc[r];
 }
 
-// Inverts the 32 x 32 block staged row-major (stride kTileLd) in `tile` by one
-// wavefront and leaves the inverse there; false (uniformly) on a bad pivot.
-__device__ __forceinline__ bool gj32_invert_schur(float *tile, float *scr, int lane) {
+// Transposed store of a block in accumulator layout: T[c][4g + r] = x[r].
+__device__ __forceinline__ void st16t(float *m, int ld, const float (&x)[4], int g, int c) {
+  *reinterpret_cast<float4 *>(m + c * ld + 4 * g) = make_float4(x[0], x[1], x[2], x[3]);
+}
+
+// Inverts the 32 x 32 block staged row-major (stride kTileLd) in `in` by one
+// wavefront: X11 = A11^{-1}, T1 = A21 X11, T2 = X11 A12, X22 = (A22 - T1 A12)^{-1},
+// X12 = -T2 X22, X21 = -X22 T1, X11' = X11 - T2 X21 (= X11 + T2 X22 T1).  Writes
+// the inverse row-major to pa and transposed to pb (both stride kTileLd); false
+// (uniformly, nothing written) on a bad pivot.
+__device__ __forceinline__ bool gj32_invert(const float *in, float *pa, float *pb, float *scr,
+                                            int lane) {
   const int c = lane & 15, g = lane >> 4;
   float *s0 = scr, *s1 = scr + 16 * kS16, *s2 = scr + 32 * kS16;
   bool bad = false;
-  float x11[4], a12[4], t1[4], x22[4];
-  ld16(tile, kTileLd, x11, g, c);                        // A11
-  ld16(tile + 16, kTileLd, a12, g, c);                   // A12
-  ld16(tile + 16 * kTileLd + 16, kTileLd, x22, g, c);    // A22
-  gj16_from<0>(x11, g, c, bad);                          // X11 = A11^{-1}
-#pragma unroll
-  for (int r = 0; r < 4; ++r) t1[r] = 0.f;
-  mm16(t1, tile + 16 * kTileLd, kTileLd, x11, g, c, 1.f);  // T1 = A21 X11
+  float x11[4], a12[4], x22[4];
+  ld16(in, kTileLd, x11, g, c);                      // A11
+  ld16(in + 16, kTileLd, a12, g, c);                 // A12
+  ld16(in + 16 * kTileLd + 16, kTileLd, x22, g, c);  // A22
+  gj16_from<0>(x11, g, c, bad);                      // X11 = A11^{-1}
+  float t1[4] = {0.f, 0.f, 0.f, 0.f}, t2[4] = {0.f, 0.f, 0.f, 0.f};
+  mm16(t1, in + 16 * kTileLd, kTileLd, x11, g, c, 1.f);  // T1 = A21 X11
   st16(s0, kS16, t1, g, c);
   st16(s1, kS16, x11, g, c);
   wave_lds_sync();
-  mm16(x22, s0, kS16, a12, g, c, -1.f);                 // S = A22 - T1 A12
-  gj16_from<0>(x22, g, c, bad);                          // X22 = S^{-1}
-  float t2[4] = {0.f, 0.f, 0.f, 0.f};
-  mm16(t2, s1, kS16, a12, g, c, 1.f);                    // T2 = X11 A12
+  mm16(x22, s0, kS16, a12, g, c, -1.f);  // S = A22 - T1 A12
+  mm16(t2, s1, kS16, a12, g, c, 1.f);    // T2 = X11 A12
   st16(s2, kS16, t2, g, c);
+  gj16_from<0>(x22, g, c, bad);          // X22 = S^{-1}
   wave_lds_sync();
-  float x12[4] = {0.f, 0.f, 0.f, 0.f};
-  mm16(x12, s2, kS16, x22, g, c, -1.f);                  // X12 = -T2 X22
-  st16(s1, kS16, x22, g, c);                             // (X11 staged copy no longer needed)
-  st16(s0, kS16, x12, g, c);
+  st16(s1, kS16, x22, g, c);
+  float x12[4] = {0.f, 0.f, 0.f, 0.f}, x21[4] = {0.f, 0.f, 0.f, 0.f};
+  mm16(x12, s2, kS16, x22, g, c, -1.f);  // X12 = -T2 X22
   wave_lds_sync();
-  float x21[4] = {0.f, 0.f, 0.f, 0.f};
-  mm16(x21, s1, kS16, t1, g, c, -1.f);                   // X21 = -X22 T1
-  mm16(x11, s0, kS16, t1, g, c, -1.f);                   // X11' = X11 - X12 T1
+  mm16(x21, s1, kS16, t1, g, c, -1.f);   // X21 = -X22 T1
+  mm16(x11, s2, kS16, x21, g, c, -1.f);  // X11' = X11 - T2 X21
   if (bad) return false;
-  wave_lds_sync();
-  st16(tile, kTileLd, x11, g, c);
-  st16(tile + 16, kTileLd, x12, g, c);
-  st16(tile + 16 * kTileLd, kTileLd, x21, g, c);
-  st16(tile + 16 * kTileLd + 16, kTileLd, x22, g, c);
+  st16(pa, kTileLd, x11, g, c);
+  st16(pa + 16, kTileLd, x12, g, c);
+  st16(pa + 16 * kTileLd, kTileLd, x21, g, c);
+  st16(pa + 16 * kTileLd + 16, kTileLd, x22, g, c);
+  st16t(pb, kTileLd, x11, g, c);
+  st16t(pb + 16 * kTileLd, kTileLd, x12, g, c);
+  st16t(pb + 16, kTileLd, x21, g, c);
+  st16t(pb + 16 * kTileLd + 16, kTileLd, x22, g, c);
   return true;
 }
 
@@ -247,12 +199,10 @@ __device__ __forceinline__ void stage_a(float *tile, const floatx16 &v, int j, i
   for (int r = 0; r < 16; ++r) tile[acc_row(h, r) * kTileLd + j] = v[r];
 }
 
-// Stage a register tile for use as a B operand later (transposed: T[col][row]).
-__device__ __forceinline__ void stage_b(float *tile, const floatx16 &v, int j, int h) {
+// The same, negated.
+__device__ __forceinline__ void stage_a_neg(float *tile, const floatx16 &v, int j, int h) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q)
-    *reinterpret_cast<float4 *>(tile + j * kTileLd + 4 * h + 8 * q) =
-        make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  for (int r = 0; r < 16; ++r) tile[acc_row(h, r) * kTileLd + j] = -v[r];
 }
 
 // acc += A B over one 32-wide k block, k of instruction r = acc_row(h, r).
@@ -285,111 +235,184 @@ __device__ __forceinline__ bool woodbury_scales(int m, int unit_dq, const float 
   return true;
 }
 
-template <int NBK>
-constexpr int wb_waves() { return 4; }  // NBK <= 4: at most 4 tiles per wavefront
+// Stage a register tile for use as a B operand later (transposed: T[col][row]);
+// lds_operand of the copy gives the tile back in accumulator layout.
+__device__ __forceinline__ void stage_b(float *tile, const floatx16 &v, int j, int h) {
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    *reinterpret_cast<float4 *>(tile + j * kTileLd + 4 * h + 8 * q) =
+        make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+}
 
-// LDS of the blocked elimination.  Column panel and P are double-buffered by
-// block-step parity, so a block step needs two barriers: after the pivot block
-// is inverted and the column panel staged, and after the new row panel is staged.
+// Wavefronts of the elimination: wb_workers own the tile columns (column c
+// belongs to wavefront c % wb_workers, as its tile set c / wb_workers) and one
+// more inverts the pivot blocks, one wavefront per SIMD: the inversion is a
+// chain of dependent vector instructions that slows down several times over
+// beside a wavefront issuing matrix instructions on the same SIMD.
+template <int NBK>
+constexpr int wb_workers() { return NBK < 3 ? NBK : 3; }
+template <int NBK>
+constexpr int wb_waves() { return wb_workers<NBK>() + 1; }
+template <int NBK>
+constexpr int wb_sets() { return (NBK + wb_workers<NBK>() - 1) / wb_workers<NBK>(); }
+
+// LDS of the blocked elimination.  Everything a block step reads is written in
+// the step before it (or before the first), so it is double-buffered by
+// block-step parity.
 template <int NBK>
 struct alignas(16) GjLds {
-  float cpan[2][NBK][kTileSz];  // A_i,kb        (A operand)
-  float rpan[NBK][kTileSz];     // P A_kb,j      (B operand)
-  float pa[2][kTileSz];         // P             (A operand)
-  float pb[2][kTileSz];         // P             (B operand)
-  int bad;
+  float cpan[2][NBK][kTileSz];  // -A_i,kb (row-major: A operand)
+  float pa[2][kTileSz];         // P_kb row-major (A operand)
+  float pb[2][kTileSz];         // P_kb transposed (B operand, accumulator-layout reads)
+  float nb[2][kTileSz];         // A_kb,kb+1 transposed
+  float nd[2][kTileSz];         // A_kb+1,kb+1 transposed
+  float pin[kTileSz];           // the pivot block being inverted, row-major
+  float scr[3 * 16 * kS16];     // left operands of the inversion's 16 x 16 products
+  int bad[2];                   // bad pivot block, by block-step parity (0 on entry)
 };
 
-// The NBK block steps on the register-resident tiles (tile t = wave + W s).
-// sh.bad must be 0 on entry.  Returns false (uniformly) if a pivot is not
-// positive and finite; the tiles are then meaningless.
-template <int NBK, int W, int TPW>
-__device__ __forceinline__ bool blocked_gj(floatx16 (&acc)[TPW], GjLds<NBK> &sh, int wave,
-                                           int lane) {
-  constexpr int NT = NBK * NBK;
-  const int j = lane & 31, h = lane >> 5;
-  for (int kb = 0; kb < NBK; ++kb) {
-    const int buf = kb & 1;
-    // (a) invert the pivot block (its owner), stage P and the column panel
-    const int td = kb * NBK + kb;
-    if (wave == td % W) {
-      const int sd = td / W;  // slot of the pivot block; copied out by value so that
-      float p[16];            // the register tiles are never indexed at run time
+// Block step kb on tile column col (acc[i] = tile (i, col)); see gj_workers.
+template <int NBK>
+__device__ __forceinline__ void column_step(floatx16 (&acc)[NBK], GjLds<NBK> &sh, int col, int kb,
+                                            int j, int h) {
+  const int buf = kb & 1;
+  if (col == kb) {
+    float b[16];
+    lds_operand(sh.pb[buf], j, h, b);  // P at (acc_row(h, r), j): B operand and own layout
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float v = acc[0][r];
-#pragma unroll
-        for (int s = 1; s < TPW; ++s) v = (s == sd) ? acc[s][r] : v;
-        p[r] = v;
-      }
-      floatx16 pv;
-#pragma unroll
-      for (int r = 0; r < 16; ++r) pv[r] = p[r];
-      stage_a(sh.pa[buf], pv, j, h);  // the pivot block, row-major
-      wave_lds_sync();
-      if (gj32_invert_schur(sh.pa[buf], sh.pb[buf], lane)) {  // P replaces it (A-operand layout)
-        wave_lds_sync();
-#pragma unroll
-        for (int r = 0; r < 16; ++r) pv[r] = sh.pa[buf][acc_row(h, r) * kTileLd + j];
-#pragma unroll
-        for (int s = 0; s < TPW; ++s)
-          if (s == sd) acc[s] = pv;
-        stage_b(sh.pb[buf], pv, j, h);
-      } else if (lane == 0) {
-        sh.bad = 1;
-      }
-    }
-#pragma unroll
-    for (int s = 0; s < TPW; ++s) {
-      const int t = wave + W * s;
-      if (t < NT && t % NBK == kb && t / NBK != kb) stage_a(sh.cpan[buf][t / NBK], acc[s], j, h);
-    }
-    __syncthreads();
-    if (__builtin_amdgcn_readfirstlane(sh.bad)) return false;
-    // (b) row panel A_kb,j <- P A_kb,j, staged for the trailing update
-#pragma unroll
-    for (int s = 0; s < TPW; ++s) {
-      const int t = wave + W * s;
-      if (t >= NT) continue;
-      const int ti = t / NBK, tj = t % NBK;
-      if (ti != kb || tj == kb) continue;
-      float a[16], b[16];
-      lds_operand(sh.pa[buf], j, h, a);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) b[r] = acc[s][r];
+    for (int s = 0; s < NBK; ++s) {
+      if (s == kb) continue;
+      float a[16];
+      lds_operand(sh.cpan[buf][s], j, h, a);
       floatx16 z;
 #pragma unroll
       for (int r = 0; r < 16; ++r) z[r] = 0.f;
       acc[s] = mfma32(a, b, z);
-      stage_b(sh.rpan[tj], acc[s], j, h);
       __builtin_amdgcn_sched_barrier(0);
     }
+#pragma unroll
+    for (int s = 0; s < NBK; ++s)
+      if (s == kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[s][r] = b[r];
+    return;
+  }
+  float rp[16];  // P A_kb,col: the B operand of the column's trailing products
+#pragma unroll
+  for (int s = 0; s < NBK; ++s) {
+    if (s != kb) continue;
+    float a[16], b[16];
+    lds_operand(sh.pa[buf], j, h, a);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) b[r] = acc[s][r];
+    floatx16 z;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) z[r] = 0.f;
+    acc[s] = mfma32(a, b, z);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) rp[r] = acc[s][r];
+  }
+  const bool next = col == kb + 1;
+#pragma unroll
+  for (int s = 0; s < NBK; ++s) {
+    if (s == kb || (next && s == kb + 1)) continue;
+    float a[16];
+    lds_operand(sh.cpan[buf][s], j, h, a);
+    acc[s] = mfma32(a, rp, acc[s]);
+    __builtin_amdgcn_sched_barrier(0);  // one tile's operands live at a time
+  }
+  if (next) {
+#pragma unroll
+    for (int s = 0; s < NBK; ++s)
+      if (s != kb + 1) stage_a_neg(sh.cpan[buf ^ 1][s], acc[s], j, h);
+  } else if (col == kb + 2) {
+#pragma unroll
+    for (int s = 0; s < NBK; ++s) {
+      if (s == kb + 1) stage_b(sh.nb[buf ^ 1], acc[s], j, h);
+      if (s == kb + 2) stage_b(sh.nd[buf ^ 1], acc[s], j, h);
+    }
+  }
+}
+
+// The NBK block steps with look-ahead, split by role: gj_workers runs on the
+// wb_workers column owners, gj_inverter on the one inverting wavefront; both
+// pass the same barriers (one per block step).  Each step kb opens with a
+// barrier after which P_kb is in pa/pb[kb & 1], -A_i,kb (i != kb) in
+// cpan[kb & 1] and the tiles A_kb,kb+1 and A_kb+1,kb+1 in nb/nd[kb & 1] (values
+// after step kb - 1).  Each tile column is updated by its owner: column kb
+// gives A_i,kb <- -A_i,kb P and A_kb,kb <- P; any other column c the row-panel
+// tile P A_kb,c and the trailing tiles A_i,c - A_i,kb (P A_kb,c).  Meanwhile the
+// inverting wavefront forms the next pivot block, A_kb+1,kb+1 - A_kb+1,kb
+// (P A_kb,kb+1), from the staged tiles and inverts it, so the inversion of
+// P_kb+1 runs beside the rest of step kb (the owner of column kb + 1 skips that
+// tile, which P_kb+1 replaces).  The owners of columns kb + 1 and kb + 2 stage
+// the next step's column panel and nb/nd.  A bad pivot block is flagged in
+// bad[its step's parity], which no wavefront writes between the barrier that
+// opens that step and the next one, so every wavefront reads the same value
+// and all leave at the same step.
+
+// acc[t][i] is tile (i, wave + wb_workers t).  Returns false (uniformly) if a
+// pivot is not positive and finite; the tiles are then meaningless.
+template <int NBK>
+__device__ __forceinline__ bool gj_workers(floatx16 (&acc)[wb_sets<NBK>()][NBK], GjLds<NBK> &sh,
+                                           int wave, int lane) {
+  constexpr int NW = wb_workers<NBK>(), NS = wb_sets<NBK>();
+  const int j = lane & 31, h = lane >> 5;
+#pragma unroll
+  for (int t = 0; t < NS; ++t) {
+    const int col = wave + NW * t;
+    if (col == 0) {
+#pragma unroll
+      for (int s = 1; s < NBK; ++s) stage_a_neg(sh.cpan[0][s], acc[t][s], j, h);
+    } else if (col == 1) {
+      stage_b(sh.nb[0], acc[t][0], j, h);
+      stage_b(sh.nd[0], acc[t][1], j, h);
+    }
+  }
+  for (int kb = 0; kb < NBK; ++kb) {
     __syncthreads();
-    // (c) trailing tiles and the column panel
+    if (__builtin_amdgcn_readfirstlane(sh.bad[kb & 1])) return false;
 #pragma unroll
-    for (int s = 0; s < TPW; ++s) {
-      const int t = wave + W * s;
-      if (t >= NT) continue;
-      const int ti = t / NBK, tj = t % NBK;
-      if (ti == kb) continue;
-      float a[16], b[16];
-      lds_operand(sh.cpan[buf][ti], j, h, a);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) a[r] = -a[r];
-      if (tj != kb) {
-        lds_operand(sh.rpan[tj], j, h, b);
-        acc[s] = mfma32(a, b, acc[s]);
-      } else {
-        lds_operand(sh.pb[buf], j, h, b);
-        floatx16 z;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) z[r] = 0.f;
-        acc[s] = mfma32(a, b, z);
-      }
-      __builtin_amdgcn_sched_barrier(0);  // one tile's operands live at a time
+    for (int t = 0; t < NS; ++t) {
+      const int col = wave + NW * t;
+      if (col < NBK) column_step<NBK>(acc[t], sh, col, kb, j, h);
     }
   }
   return true;
+}
+
+// a00: the pivot block A_00 in accumulator layout.
+template <int NBK>
+__device__ __forceinline__ void gj_inverter(const floatx16 &a00, GjLds<NBK> &sh, int lane) {
+  const int j = lane & 31, h = lane >> 5;
+  stage_a(sh.pin, a00, j, h);
+  wave_lds_sync();
+  if (!gj32_invert(sh.pin, sh.pa[0], sh.pb[0], sh.scr, lane) && lane == 0) sh.bad[0] = 1;
+  for (int kb = 0; kb < NBK; ++kb) {
+    const int buf = kb & 1;
+    __syncthreads();
+    if (__builtin_amdgcn_readfirstlane(sh.bad[buf])) return;
+    if (kb + 1 == NBK) continue;
+    float a[16], b[16];
+    lds_operand(sh.pa[buf], j, h, a);
+    lds_operand(sh.nb[buf], j, h, b);
+    floatx16 z;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) z[r] = 0.f;
+    const floatx16 t = mfma32(a, b, z);  // P A_kb,kb+1
+    float d[16];
+    lds_operand(sh.cpan[buf][kb + 1], j, h, a);
+    lds_operand(sh.nd[buf], j, h, d);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      b[r] = t[r];
+      z[r] = d[r];
+    }
+    stage_a(sh.pin, mfma32(a, b, z), j, h);
+    wave_lds_sync();
+    if (!gj32_invert(sh.pin, sh.pa[buf ^ 1], sh.pb[buf ^ 1], sh.scr, lane) && lane == 0)
+      sh.bad[buf ^ 1] = 1;
+  }
 }
 
 // The whole inverse on one workgroup of 64 wb_waves threads (m <= 32 NBK):
@@ -400,68 +423,101 @@ __device__ __forceinline__ void woodbury_blocked(int m, float lr, int unit_dq,
                                                  const float *__restrict__ dq,
                                                  const float *__restrict__ N,
                                                  float *__restrict__ R, int *__restrict__ flag) {
-  constexpr int W = wb_waves<NBK>();
-  constexpr int NT = NBK * NBK;
-  constexpr int TPW = (NT + W - 1) / W;  // tiles per wavefront
   __shared__ GjLds<NBK> sh;
   __shared__ __align__(16) float sq[32 * NBK];
-  if (!woodbury_scales(m, unit_dq, dq, sq, &sh.bad, flag)) return;
+  if (threadIdx.x == 0) sh.bad[1] = 0;  // published by the barriers in woodbury_scales
+  if (!woodbury_scales(m, unit_dq, dq, sq, &sh.bad[0], flag)) return;
   const int lane = threadIdx.x & 63, j = lane & 31, h = lane >> 5;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const float tl = 2.f * lr;
-
-  // Load C tile by tile: lane (j, h) reads column col of rows acc_row(h, 0..15);
-  // the scales come from LDS, sq[row] as four 16-byte reads.  Entries outside
-  // m x m read a clamped in-range address and are replaced by the identity.
-  // All loads are issued first and pinned by empty asm statements, so that none
-  // is moved under the (row, col) < m conditions and they overlap in flight.
-  float raw[TPW][16];
+  // Load C: lane (j, h) reads column col of rows 32 s + acc_row(h, 0..15); the
+  // scales come from LDS, sq[row] as four 16-byte reads.  Entries outside m x m
+  // read a clamped in-range address and are replaced by the identity.  All loads
+  // are issued first and pinned by empty asm statements, so that none is moved
+  // under the (row, col) < m conditions and they overlap in flight.
+  constexpr int NW = wb_workers<NBK>(), NS = wb_sets<NBK>();
+  if (wave == NW) {  // the inverting wavefront: the pivot block A_00
+    float raw[16];
+    const float *np = N + min(j, m - 1);
 #pragma unroll
-  for (int s = 0; s < TPW; ++s) {
-    const int t = min(wave + W * s, NT - 1);
-    const int col = (t % NBK) * 32 + j, r0 = (t / NBK) * 32;
-    const float *np = N + min(col, m - 1);
+    for (int r = 0; r < 16; ++r) raw[r] = np[min(acc_row(h, r), m - 1) * m];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) raw[s][r] = np[min(r0 + acc_row(h, r), m - 1) * m];
-  }
-#pragma unroll
-  for (int s = 0; s < TPW; ++s)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) asm volatile("" : "+v"(raw[s][r]));
-  floatx16 acc[TPW];
-#pragma unroll
-  for (int s = 0; s < TPW; ++s) {
-    const int t = min(wave + W * s, NT - 1);
-    const int r0 = (t / NBK) * 32, col = (t % NBK) * 32 + j;
-    const float sc = tl * sq[min(col, m - 1)];
+    for (int r = 0; r < 16; ++r) asm volatile("" : "+v"(raw[r]));
+    const float sc = tl * sq[min(j, m - 1)];
     float sr[16];
-    lds_operand(sq + r0, 0, h, sr);
+    lds_operand(sq, 0, h, sr);
+    floatx16 a00;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int row = r0 + acc_row(h, r);
-      const float c = (row < m && col < m) ? -(sr[r] * raw[s][r] * sc) : 0.f;
-      acc[s][r] = (row == col) ? 1.f + c : c;
+      const int row = acc_row(h, r);
+      const float c = (row < m && j < m) ? -(sr[r] * raw[r] * sc) : 0.f;
+      a00[r] = (row == j) ? 1.f + c : c;
+    }
+    gj_inverter<NBK>(a00, sh, lane);
+    return;
+  }
+  floatx16 acc[NS][NBK];
+  {
+    float raw[NS][NBK][16];
+#pragma unroll
+    for (int t = 0; t < NS; ++t) {
+      if (wave + NW * t >= NBK) continue;  // no such tile column
+      const float *np = N + min(32 * (wave + NW * t) + j, m - 1);
+#pragma unroll
+      for (int s = 0; s < NBK; ++s)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) raw[t][s][r] = np[min(32 * s + acc_row(h, r), m - 1) * m];
+    }
+#pragma unroll
+    for (int t = 0; t < NS; ++t)
+#pragma unroll
+      for (int s = 0; s < NBK; ++s)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) asm volatile("" : "+v"(raw[t][s][r]));
+#pragma unroll
+    for (int t = 0; t < NS; ++t) {
+      const int col = 32 * (wave + NW * t) + j;
+      const float sc = tl * sq[min(col, m - 1)];
+#pragma unroll
+      for (int s = 0; s < NBK; ++s) {
+        float sr[16];
+        lds_operand(sq + 32 * s, 0, h, sr);
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = 32 * s + acc_row(h, r);
+          const float c = (row < m && col < m) ? -(sr[r] * raw[t][s][r] * sc) : 0.f;
+          acc[t][s][r] = (row == col) ? 1.f + c : c;
+        }
+      }
     }
   }
 
-  if (!blocked_gj<NBK, W, TPW>(acc, sh, wave, lane)) {
+  if (!gj_workers<NBK>(acc, sh, wave, lane)) {
     if (threadIdx.x == 0) atomicOr(flag, FLAG_NOT_SPD);
     return;
   }
+  // R row-major; tiles inside m x m (all of them when m is a multiple of 32)
+  // store without per-row checks, at 32-bit offsets from R.
 #pragma unroll
-  for (int s = 0; s < TPW; ++s) {
-    const int t = wave + W * s;
-    if (t >= NT) continue;
-    const int r0 = (t / NBK) * 32, col = (t % NBK) * 32 + j;
-    if (col >= m) continue;
+  for (int t = 0; t < NS; ++t) {
+    const int col = 32 * (wave + NW * t) + j;
+    if (wave + NW * t >= NBK || col >= m) continue;
     const float sc = tl * sq[col];
-    float sr[16];
-    lds_operand(sq + r0, 0, h, sr);
-    float *rp = R + col;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = r0 + acc_row(h, r);
-      if (row < m) rp[row * m] = sr[r] * acc[s][r] * sc;
+    for (int s = 0; s < NBK; ++s) {
+      float sr[16];
+      lds_operand(sq + 32 * s, 0, h, sr);
+      const int base = (32 * s + 4 * h) * m + col;
+      if (32 * s + 32 <= m) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          R[base + ((r & 3) + 8 * (r >> 2)) * m] = sr[r] * acc[t][s][r] * sc;
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (32 * s + acc_row(h, r) < m)
+            R[base + ((r & 3) + 8 * (r >> 2)) * m] = sr[r] * acc[t][s][r] * sc;
+      }
     }
   }
 }
