@@ -849,14 +849,37 @@ hipError_t launch_step_sync(hipStream_t s, const StepSync &wait, int *done) {
   return hipGetLastError();
 }
 
+// Dynamic LDS that brings a one-workgroup kernel's allocation to the whole
+// per-workgroup limit, so that no workgroup of another kernel that uses LDS is
+// placed on its compute unit: the elimination keeps all four SIMDs busy, and a
+// workgroup sharing the unit (a gather or GEMM tile of the main stream) ran
+// more than twice as long, holding up its whole launch.  0 if the sizes cannot
+// be queried.
+size_t exclusive_lds_pad(const void *kernel) {
+  int dev = 0, limit = 0;
+  hipFuncAttributes fa{};
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&limit, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess ||
+      hipFuncGetAttributes(&fa, kernel) != hipSuccess || (size_t)limit <= fa.sharedSizeBytes)
+    return 0;
+  return (size_t)limit - fa.sharedSizeBytes;
+}
+
+template <auto Kernel>
+size_t exclusive_lds_pad_cached() {  // one value per kernel
+  static const size_t pad = exclusive_lds_pad(reinterpret_cast<const void *>(Kernel));
+  return pad;
+}
+
 hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
                            const float *N, float *R, float *Cwork, float *Pbig, float *Cp,
                            float *Rp, int *flag, const StepSync &wait, int *done) {
   switch (m <= kWoodburyOneWG ? (m + 31) / 32 : 0) {
 #define LST_WB_CASE(NB)                                                                       \
   case NB:                                                                                    \
-    LST_LAUNCH((woodbury_blocked_kernel<NB>), dim3(1), dim3(64 * wb_waves<NB>()), 0, s, m, lr, \
-               unit_dq, dq, N, R, flag, wait, done);                                          \
+    LST_LAUNCH((woodbury_blocked_kernel<NB>), dim3(1), dim3(64 * wb_waves<NB>()),             \
+               exclusive_lds_pad_cached<woodbury_blocked_kernel<NB>>(), s, m, lr, unit_dq, dq, N, R, \
+               flag, wait, done);                                                             \
     break;
     LST_WB_CASE(1)
     LST_WB_CASE(2)
@@ -871,8 +894,9 @@ hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const fl
       int pb0 = 0, pnb = 0;
       for (int b0 = 0; b0 < m; b0 += kBigBlock) {
         const int nb = std::min(kBigBlock, m - b0), e0 = b0 + nb;
-        LST_LAUNCH(pivot_block_kernel, dim3(1), dim3(64 * wb_waves<kPivotNbk>()), 0, s, m, b0, nb,
-                   pb0, pnb, Cwork, Pbig, PI, flag);
+        LST_LAUNCH(pivot_block_kernel, dim3(1), dim3(64 * wb_waves<kPivotNbk>()),
+                   exclusive_lds_pad_cached<pivot_block_kernel>(), s, m, b0, nb, pb0, pnb, Cwork,
+                   Pbig, PI, flag);
         float *Ab = Cwork + (int64_t)b0 * m;
         GemmBatch r{};
         int n = 0;
