@@ -35,12 +35,13 @@ constexpr int kTileLd = 36;  // LDS row stride (floats) of a staged 32 x 32 tile
 constexpr int kTileSz = 32 * kTileLd;
 
 // One scalar Gauss-Jordan step on pivot K (p = A_KK) of a 16 x 16 block:
-//   A' = X - f g^T,  X = A with column K replaced by e_K,
-//   f_i = A_iK (i != K), f_K = p - 1,   g_j = A_Kj / p (j != K), g_K = 1 / p,
+//   A' = A - (f - e_K) g^T,   f = A_:K (column K),
+//   g_j = A_Kj / p (j != K), g_K = 1 + 1/p,
 // i.e. A'_Kj = A_Kj / p, A'_iK = -A_iK / p, A'_KK = 1 / p, A'_ij = A_ij - A_iK A_Kj / p.
-// Column K needs no separate case: there t_i = f_i (and t_K = p), so
-// A' = t - f (1 + 1/p) gives -f_i / p and 1 / p.  A bad pivot sets `bad`; the
-// caller discards the block.
+// Since A_KK = p, g_j = (A_Kj + [j = K]) / p needs no separate case.  A lane
+// applies -f g_c to its rows with the column-K value taken straight from the
+// lane of its 16-lane row that holds column K (a DPP operand of the multiply-add),
+// then adds g_c on row K.  A bad pivot sets `bad`; the caller discards the block.
 __device__ __forceinline__ float lane_read(float v, int lane) {
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
 }
@@ -55,8 +56,7 @@ __device__ __forceinline__ void wave_lds_sync() { __builtin_amdgcn_fence(__ATOMI
 // 16-lane row to all four).
 template <int N>
 __device__ __forceinline__ float row_newbcast(float v) {  // lane N of each 16-lane row
-  return __int_as_float(
-      __builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x150 + N, 0xF, 0xF, false));
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x150 + N, 0xF, 0xF, false));
 }
 
 template <int Q>
@@ -81,30 +81,24 @@ __device__ __forceinline__ float row16_broadcast(float v) {  // 16-lane row Q to
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 constexpr int kS16 = 20;  // LDS row stride (floats) of a staged 16 x 16 matrix: 16-byte rows
 
+// eg[q] = 1 in the lanes of 16-lane row q, else 0.
 template <int K>
-__device__ __forceinline__ void gj16_step(float (&t)[4], int g, int c, bool &bad) {
+__device__ __forceinline__ void gj16_step(float (&t)[4], int c, const float (&eg)[4], bool &bad) {
   constexpr int QK = K >> 2, RK = K & 3;
   const float p = lane_read(t[RK], 16 * QK + K);
-  bad |= !(p > 0.f && p < INFINITY);  // checked once after the 16 steps
-  float f[4];                          // column K at rows 4g + r
+  bad |= !(p > 0.f && p < INFINITY);              // checked once after the 16 steps
+  const float rw = row16_broadcast<QK>(t[RK]);    // row K at column c (p at c = K)
+  const float ng = -((c == K ? rw + 1.f : rw) * __builtin_amdgcn_rcpf(p));  // -g_c
 #pragma unroll
-  for (int r = 0; r < 4; ++r) f[r] = row_newbcast<K>(t[r]);
-  const float rw = row16_broadcast<QK>(t[RK]);  // row K at column c
-  float ip = __builtin_amdgcn_rcpf(p);
-  ip = fmaf(ip, fmaf(-p, ip, 1.f), ip);  // one Newton step on the hardware reciprocal
-  const float gc = (c == K) ? 1.f + ip : rw * ip;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const float fr = (r == RK && g == QK) ? p - 1.f : f[r];
-    t[r] = fmaf(-fr, gc, t[r]);
-  }
+  for (int r = 0; r < 4; ++r) t[r] = fmaf(row_newbcast<K>(t[r]), ng, t[r]);  // rows 4g + r
+  t[RK] = fmaf(-eg[QK], ng, t[RK]);               // + g_c on row K
 }
 
 template <int K>
-__device__ __forceinline__ void gj16_from(float (&t)[4], int g, int c, bool &bad) {
+__device__ __forceinline__ void gj16_from(float (&t)[4], int c, const float (&eg)[4], bool &bad) {
   if constexpr (K < 16) {
-    gj16_step<K>(t, g, c, bad);
-    gj16_from<K + 1>(t, g, c, bad);
+    gj16_step<K>(t, c, eg, bad);
+    gj16_from<K + 1>(t, c, eg, bad);
   }
 }
 
@@ -147,11 +141,14 @@ __device__ __forceinline__ bool gj32_invert(const float *in, float *pa, float *p
   const int c = lane & 15, g = lane >> 4;
   float *s0 = scr, *s1 = scr + 16 * kS16, *s2 = scr + 32 * kS16;
   bool bad = false;
+  float eg[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) eg[q] = g == q ? 1.f : 0.f;
   float x11[4], a12[4], x22[4];
   ld16(in, kTileLd, x11, g, c);                      // A11
   ld16(in + 16, kTileLd, a12, g, c);                 // A12
   ld16(in + 16 * kTileLd + 16, kTileLd, x22, g, c);  // A22
-  gj16_from<0>(x11, g, c, bad);                      // X11 = A11^{-1}
+  gj16_from<0>(x11, c, eg, bad);                      // X11 = A11^{-1}
   float t1[4] = {0.f, 0.f, 0.f, 0.f}, t2[4] = {0.f, 0.f, 0.f, 0.f};
   mm16(t1, in + 16 * kTileLd, kTileLd, x11, g, c, 1.f);  // T1 = A21 X11
   st16(s0, kS16, t1, g, c);
@@ -160,7 +157,7 @@ __device__ __forceinline__ bool gj32_invert(const float *in, float *pa, float *p
   mm16(x22, s0, kS16, a12, g, c, -1.f);  // S = A22 - T1 A12
   mm16(t2, s1, kS16, a12, g, c, 1.f);    // T2 = X11 A12
   st16(s2, kS16, t2, g, c);
-  gj16_from<0>(x22, g, c, bad);          // X22 = S^{-1}
+  gj16_from<0>(x22, c, eg, bad);          // X22 = S^{-1}
   wave_lds_sync();
   st16(s1, kS16, x22, g, c);
   float x12[4] = {0.f, 0.f, 0.f, 0.f}, x21[4] = {0.f, 0.f, 0.f, 0.f};
