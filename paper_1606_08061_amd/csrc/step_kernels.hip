@@ -504,14 +504,21 @@ __global__ __launch_bounds__(kMblockThreads) void mblock_kernel(
     }
   }
 
+  // Index and value matrices into LDS with all loads in flight at once; each list
+  // is then sorted in place (entry k is read before any insertion reaches it).
+  for (int q = t; q < m * K; q += kMblockThreads) {
+    lrow[q] = idx[q];
+    lval[q] = dA[q];
+  }
+  __syncthreads();
   for (int q = t; q < m; q += kMblockThreads) {
     int *lr = lrow + q * K;
     float *lv = lval + q * K;
     int c = 0;
     for (int k = 0; k < K; ++k) {
-      const int r = idx[(int64_t)q * K + k];
+      const int r = lr[k];
       if (r < 0) continue;
-      const float g = dA[(int64_t)q * K + k];
+      const float g = lv[k];
       int p = c;
       while (p > 0 && lr[p - 1] > r) {
         lr[p] = lr[p - 1];
