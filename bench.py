@@ -51,8 +51,10 @@ def phase_work(w, idx_pool):
         "mblock": ("serial", 8.0 * m * m, "flop"),
         # R X, M H (m^2 d each) and the U update (m d^2)
         "mid": ("mfma", 2.0 * (m * d * d + 2 * m * m * d), "flop"),
-        # U^-T update (m d^2), Q update (2 m d^2), P = X + N Yw (m^2 d)
-        "update": ("mfma", 2.0 * (3 * m * d * d + m * m * d), "flop"),
+        # U^-T update (m d^2), Q update (2 m d^2), and for the spherical softmax P = X + N Yw
+        # (m^2 d); for squared error the same launch also carries the V scatter
+        "update": ("mfma", 2.0 * (3 * m * d * d + (m * m * d if w.loss != "squared" else 0)),
+                   "flop"),
         # read-modify-write of the distinct target rows and the P rows they use
         "scatter": ("hbm", 4.0 * (2 * uniq * d + m * d), "byte"),
     }

@@ -758,17 +758,23 @@ int enqueue_main_b(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *
   prof(c, LST_PHASE_MID, true);
   gemm_enqueue_plan(pl.b[3], pl.dev + 3, H, gH, lr, c->flag, s, GEMM_MID);
   prof(c, LST_PHASE_MID, false);
-  prof(c, LST_PHASE_UPDATE, true);
-  gemm_enqueue_plan(pl.b[4], pl.dev + 4, H, gH, lr, c->flag, s, GEMM_UPDATE);
-  prof(c, LST_PHASE_UPDATE, false);
-
   // V_r -= eta sum dl/dA P_j over the slots of each distinct target row (eq. updateV).
-  prof(c, LST_PHASE_SCATTER, true);
-  if (c->loss == LST_LOSS_SQUARED)  // eta P = Yw / 2 (see build_plan)
-    launch_scatter(s, m, K, c->d, 0.5f, idx, c->dA, c->Yw, c->V, c->ldv, c->flag);
-  else
-    launch_scatter(s, m, K, c->d, lr, idx, c->dA, c->P, c->V, c->ldv, c->flag);
-  prof(c, LST_PHASE_SCATTER, false);
+  // For squared error eta P = Yw / 2 (see build_plan): the scatter needs nothing
+  // from the update launch and runs in it; the spherical softmax's P comes from it.
+  const bool squared = c->loss == LST_LOSS_SQUARED;
+  prof(c, LST_PHASE_UPDATE, true);
+  const bool fused =
+      squared && m * K > 0 &&
+      gemm_enqueue_plan_scatter(pl.b[4], pl.dev + 4, H, gH, lr, c->flag, s, m * K, K, c->d, 0.5f,
+                                idx, c->dA, c->Yw, c->V, c->ldv);
+  if (!fused) gemm_enqueue_plan(pl.b[4], pl.dev + 4, H, gH, lr, c->flag, s, GEMM_UPDATE);
+  prof(c, LST_PHASE_UPDATE, false);
+  if (!fused) {
+    prof(c, LST_PHASE_SCATTER, true);
+    launch_scatter(s, m, K, c->d, squared ? 0.5f : lr, idx, c->dA, squared ? c->Yw : c->P, c->V,
+                   c->ldv, c->flag);
+    prof(c, LST_PHASE_SCATTER, false);
+  }
   // Kernel launches above are not checked one by one: a launch error stays pending
   // and is reported here.
   return record(c, hipGetLastError()) ? LST_E_HIP : LST_OK;

@@ -19,6 +19,7 @@
 // the ragged end of the k range is masked.  Operands are fetched kStage
 // k-blocks ahead of the matrix cores.
 #include "lst_internal.h"
+#include "scatter.h"
 
 namespace lst {
 
@@ -281,6 +282,25 @@ __global__ __launch_bounds__(64 * NW, 12 / NW) void gemm_plan_kernel(const GemmB
                                                             const StepSync sync) {
   step_sync_begin(sync);
   gemm_body<NW>(*bt, H, gH, lr, gate);
+}
+
+// The squared-error update launch with the V update in it: workgroups below
+// ntiles run the update plan's tiles, each of the others one target slot of the
+// scatter (256 threads).  Both only read the mid launch's outputs (Yw, dl/dA),
+// and they write disjoint state (U^-T and Q; the target rows of V), so the
+// scatter needs no launch of its own after the update.
+__global__ __launch_bounds__(256, 4) void update_scatter_kernel(
+    const GemmBatch *__restrict__ bt, int ntiles, const float *H, float *gH, float lr,
+    const int *__restrict__ gate, int n, int K, int d, float slr, const int *__restrict__ idx,
+    const float *__restrict__ dA, const float *__restrict__ P, float *__restrict__ V,
+    int64_t ldv) {
+  if ((int)blockIdx.x < ntiles) {
+    gemm_body<4>(*bt, H, gH, lr, gate);
+    return;
+  }
+  extern __shared__ int sh[];
+  if (*gate != 0) return;
+  scatter_slot<256>((int)blockIdx.x - ntiles, n, K, d, slr, idx, dA, P, V, ldv, sh);
 }
 
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const GemmDesc g, const int *__restrict__ gate) {
@@ -795,6 +815,18 @@ void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float 
         LST_LAUNCH((gemm_plan_kernel<GEMM_OTHER, 4>), dim3(total), dim3(256), 0, s, dev, H, gradH,
                    lr, gate, sync);
   }
+}
+
+bool gemm_enqueue_plan_scatter(const GemmBatch &host, const GemmBatch *dev, const float *H,
+                               float *gradH, float lr, const int *gate, hipStream_t s, int n,
+                               int K, int d, float slr, const int *idx, const float *dA,
+                               const float *P, float *V, int64_t ldv) {
+  if (host.wide || host.t16) return false;
+  for (int i = 0; i < host.n; ++i)
+    if (host.d[i].splits > 1) return false;
+  LST_LAUNCH(update_scatter_kernel, dim3(host.total_tiles + n), dim3(256), 2 * n * sizeof(int), s,
+             dev, host.total_tiles, H, gradH, lr, gate, n, K, d, slr, idx, dA, P, V, ldv);
+  return true;
 }
 
 bool gemm_big_ok(const GemmDesc &g) {

@@ -178,6 +178,15 @@ void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float 
                        float *gradH, float lr, const int *gate, hipStream_t s, int phase,
                        const int *pf_idx = nullptr, int pf_K = 0, const StepSync &sync = {});
 
+// The same launch for a plan of 32 x 32 tiles without split-k, with n more
+// workgroups that each run one target slot of the V scatter (V_r -= slr sum
+// dl/dA P_j over the row's slots).  Returns false, launching nothing, if the
+// plan does not qualify.
+bool gemm_enqueue_plan_scatter(const GemmBatch &host, const GemmBatch *dev, const float *H,
+                               float *gradH, float lr, const int *gate, hipStream_t s, int n,
+                               int K, int d, float slr, const int *idx, const float *dA,
+                               const float *P, float *V, int64_t ldv);
+
 // Large single products on 128 x 128 tiles (the naive path).  gemm_big_ok: the
 // operands meet the kernel's alignment needs (else use gemm_launch).  gemm_big_plan
 // fills the tile counts and splits k over workgroups when the tiles are few, with

@@ -21,6 +21,7 @@
 #include <algorithm>
 
 #include "lst_internal.h"
+#include "scatter.h"
 #include "woodbury_gj.h"
 
 namespace lst {
@@ -566,134 +567,13 @@ __global__ __launch_bounds__(kMblockThreads) void mblock_kernel(
 
 constexpr int kScatterThreads = 512;
 
-// One workgroup per target slot s (slot = j*K + k of the m x K index matrix).
-// The lowest slot of each V row does the row's update: it lists, in ascending
-// slot order, every slot with the same row and applies
-//   V_r -= eta sum_{slots s' of row r} dl/dA_s' P_{j(s')},
-// so each distinct row has exactly one writer and a fixed summation order.
+// The V update: one workgroup per target slot (scatter_slot).
 __global__ __launch_bounds__(kScatterThreads) void scatter_kernel(
     int n, int K, int d, float lr, const int *__restrict__ idx, const float *__restrict__ dA,
     const float *__restrict__ P, float *__restrict__ V, int64_t ldv, const int *__restrict__ gate) {
   extern __shared__ int sh[];
-  int *sidx = sh;        // n target rows
-  int *slist = sh + n;   // slots of this row, ascending
-  __shared__ int swcnt[kScatterThreads / 64];
   if (*gate != 0) return;
-  const int s = blockIdx.x;
-  const int r = idx[s];
-  if (r < 0) return;
-  int dup = 0;
-  for (int q = threadIdx.x; q < n; q += kScatterThreads) {
-    const int v = idx[q];
-    sidx[q] = v;
-    dup |= (q < s && v == r);
-  }
-  if (__syncthreads_or(dup)) return;  // an earlier slot owns this row
-
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  int total = 0;
-  for (int base = s; base < n; base += kScatterThreads) {
-    const int q = base + threadIdx.x;
-    const bool match = q < n && sidx[q] == r;
-    const unsigned long long mask = __ballot(match);
-    if (lane == 0) swcnt[w] = __popcll(mask);
-    __syncthreads();
-    int before = total;
-    for (int x = 0; x < w; ++x) before += swcnt[x];
-    if (match) slist[before + __popcll(mask & ((1ull << lane) - 1ull))] = q;
-    for (int x = 0; x < kScatterThreads / 64; ++x) total += swcnt[x];
-    __syncthreads();
-  }
-
-  // The row's sum over its `total` slots: columns in groups of four where the
-  // layout allows; the slots split into np interleaved parts (np a power of two,
-  // as many as the threads left over by the columns allow), each part's sum
-  // carried in kIlp independent partial sums, the parts then added in a fixed
-  // order through LDS.  Rows with many slots (frequent targets) are so spread
-  // over the workgroup instead of running one slot after another.
-  float *vr = V + (int64_t)r * ldv;
-  const bool v4 = (d & 3) == 0 && (ldv & 3) == 0 && (reinterpret_cast<uintptr_t>(V) & 15) == 0 &&
-                  (reinterpret_cast<uintptr_t>(P) & 15) == 0;
-  const int width = v4 ? 4 : 1;
-  const int ng = (d + width - 1) / width;  // column groups
-  int np = 1;
-  while (np < 16 && 2 * np * ng <= kScatterThreads) np *= 2;
-  __shared__ float4 spart[kScatterThreads];
-  for (int g0 = 0; g0 < ng; g0 += kScatterThreads / np) {
-    const int gl = threadIdx.x % (kScatterThreads / np), part = threadIdx.x / (kScatterThreads / np);
-    const int g = g0 + gl;
-    const bool active = g < ng;
-    constexpr int kIlp = 8;
-    float4 a[kIlp];
-#pragma unroll
-    for (int u = 0; u < kIlp; ++u) a[u] = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (active) {
-      int t = part;
-      for (; t + (kIlp - 1) * np < total; t += kIlp * np) {
-#pragma unroll
-        for (int u = 0; u < kIlp; ++u) {
-          const int q = slist[t + u * np];
-          const float w = dA[q];
-          const float *pr = P + (int64_t)(q / K) * d + g * width;
-          if (v4) {
-            const float4 x = *reinterpret_cast<const float4 *>(pr);
-            a[u].x += w * x.x;
-            a[u].y += w * x.y;
-            a[u].z += w * x.z;
-            a[u].w += w * x.w;
-          } else {
-            a[u].x += w * pr[0];
-          }
-        }
-      }
-      for (; t < total; t += np) {  // fewer than kIlp left
-        const int q = slist[t];
-        const float w = dA[q];
-        const float *pr = P + (int64_t)(q / K) * d + g * width;
-        if (v4) {
-          const float4 x = *reinterpret_cast<const float4 *>(pr);
-          a[0].x += w * x.x;
-          a[0].y += w * x.y;
-          a[0].z += w * x.z;
-          a[0].w += w * x.w;
-        } else {
-          a[0].x += w * pr[0];
-        }
-      }
-    }
-    float4 sum = a[0];
-#pragma unroll
-    for (int u = 1; u < kIlp; ++u) {
-      sum.x += a[u].x;
-      sum.y += a[u].y;
-      sum.z += a[u].z;
-      sum.w += a[u].w;
-    }
-    spart[threadIdx.x] = sum;
-    __syncthreads();
-    if (part == 0 && active) {
-      float4 tot = spart[gl];
-      for (int p2 = 1; p2 < np; ++p2) {
-        const float4 x = spart[gl + p2 * (kScatterThreads / np)];
-        tot.x += x.x;
-        tot.y += x.y;
-        tot.z += x.z;
-        tot.w += x.w;
-      }
-      if (v4) {
-        float4 *dst = reinterpret_cast<float4 *>(vr) + g;
-        float4 v = *dst;
-        v.x -= lr * tot.x;
-        v.y -= lr * tot.y;
-        v.z -= lr * tot.z;
-        v.w -= lr * tot.w;
-        *dst = v;
-      } else {
-        vr[g] -= lr * tot.x;
-      }
-    }
-    __syncthreads();
-  }
+  scatter_slot<kScatterThreads>(blockIdx.x, n, K, d, lr, idx, dA, P, V, ldv, sh);
 }
 
 __global__ void identity_kernel(float *A, int d, int64_t ld) {

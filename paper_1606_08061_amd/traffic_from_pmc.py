@@ -37,7 +37,8 @@ KERNELS = [
     ("gather_kernel", "gather", "step_kernels.hip"),
     ("mblock_kernel", "mblock", "step_kernels.hip"),
     ("woodbury_blocked_kernel", "woodbury", "step_kernels.hip+woodbury_gj.h"),
-    ("scatter_kernel", "scatter", "step_kernels.hip"),
+    ("scatter_kernel", "scatter", "step_kernels.hip+scatter.h"),
+    ("update_scatter_kernel", "update", "gemm.hip+scatter.h"),
 ]
 
 
