@@ -198,8 +198,10 @@ enum lst_phase {
   LST_PHASE_MBLOCK = 3,        /* loss sum, M of the Q update                              */
   LST_PHASE_WOODBURY = 4,      /* the m x m Woodbury matrix and its inverse                */
   LST_PHASE_MID = 5,           /* R X, (eta^2/2) M H - eta grad_H, U update (matrix cores) */
-  LST_PHASE_UPDATE = 6,        /* U^{-T} and Q updates, P = U_new^{-T} H (matrix cores)    */
-  LST_PHASE_SCATTER = 7,       /* conflict-free update of the target rows of V             */
+  LST_PHASE_UPDATE = 6,        /* U^{-T} and Q updates, P = U_new^{-T} H (matrix cores);
+                                  for squared error also the V update of SCATTER           */
+  LST_PHASE_SCATTER = 7,       /* conflict-free update of the target rows of V (spherical
+                                  softmax; for squared error it runs inside UPDATE)        */
   LST_PHASE_NAIVE_FWD = 8,     /* naive: O = W H^T                                         */
   LST_PHASE_NAIVE_LOSS = 9,    /* naive: column norms of O, loss, grad_O                   */
   LST_PHASE_NAIVE_GRAD = 10,   /* naive: grad_H = grad_O^T W                               */
