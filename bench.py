@@ -112,6 +112,40 @@ def roofline_for(table, traffic=None):
             "avg_launch_us": r["avg_us"], "algorithmic_per_launch": r["work_per_launch"]}
 
 
+def attainable_peaks(dev):
+    """Measured ceilings on this GPU beside the spec peaks: a 1 GiB device-to-device
+    copy (bytes read + written per second) and a 8192^3 fp32 matmul through torch's
+    BLAS (fp32 matrix cores; TF32 is off in torch by default)."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(10):
+        dst.copy_(src)
+    ev[1].record()
+    torch.cuda.synchronize()
+    hbm = 10 * 2 * src.numel() * 4 / (ev[0].elapsed_time(ev[1]) / 1e3) / 1e9
+    del src, dst
+    n = 8192
+    a_ = torch.randn(n, n, device=dev)
+    b_ = torch.randn(n, n, device=dev)
+    torch.matmul(a_, b_)
+    torch.cuda.synchronize()
+    ev[0].record()
+    for _ in range(5):
+        torch.matmul(a_, b_)
+    ev[1].record()
+    torch.cuda.synchronize()
+    mm = 5 * 2.0 * n ** 3 / (ev[0].elapsed_time(ev[1]) / 1e3) / 1e12
+    del a_, b_
+    torch.cuda.empty_cache()
+    return {"hbm_GBs": round(hbm, 1), "fp32_matrix_TFLOPs": round(mm, 2),
+            "how": "1 GiB device copy x10 (read+write bytes); 8192^3 fp32 torch.matmul x5"}
+
+
 def cpu_baseline(w, V0, pool, seconds, threads=None):
     """The fp64 dense oracle on the host: examples/s over a bounded sample."""
     from threadpoolctl import threadpool_info, threadpool_limits
@@ -248,6 +282,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-naive", action="store_true")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the measured copy and matmul ceilings (also skipped with --copy-calib)")
     ap.add_argument("--sweep", action="store_true",
                     help="factored vs naive over the D x d sweep instead of the default line")
     ap.add_argument("--sweep-steps", type=int, default=20)
@@ -370,6 +406,12 @@ def main():
 
     del V0, gpool
     torch.cuda.empty_cache()
+    att = None
+    if not (args.no_peaks or args.copy_calib):  # counter runs take the copy as their scale
+        att = attainable_peaks(dev)
+        roof["attainable_peak"] = (att["hbm_GBs"] if roof["bound"] == "hbm"
+                                   else att["fp32_matrix_TFLOPs"])
+        roof["frac_attainable"] = round(roof["achieved"] / roof["attainable_peak"], 5)
     cpu = cpu1 = None
     if not args.no_cpu:
         print("[bench] cpu baseline (fp64 oracle)", file=sys.stderr, flush=True)
@@ -392,6 +434,7 @@ def main():
         "host_enqueue_us_per_step": round(host_us, 2),
         "kernels": table,
         "serial_inverse_us": table.get("woodbury", {}).get("avg_us"),
+        "attainable": att,
     }
     print(json.dumps(out), flush=True)
 
