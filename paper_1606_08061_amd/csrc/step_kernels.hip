@@ -459,11 +459,14 @@ __global__ __launch_bounds__(64 * wb_waves<kPivotNbk>()) void pivot_block_kernel
 // Loss L = sum_j l_j (fixed order; non-finite -> error flag) and the Q-update
 // matrix M of eq. gen-M (dl/ds = 0):
 //   M_ij = 4 dq_i M^_ij dq_j + (Yring^T Yring)_ij + 2 dq_i (H~^T G)_ij + 2 dq_j (H~^T G)_ji
-// Column j of the sparse Yring is kept as a sorted list of (row, value) pairs,
-// so (Yring^T Yring)_ij is a merge of two lists in ascending row order.  Each
-// workgroup builds the m lists in LDS and fills kMblockThreads entries of M;
-// workgroup 0 also forms the loss.
+// Each workgroup stages the m x K targets in LDS and fills kMblockThreads
+// entries of M; workgroup 0 also forms the loss.  For K <= kMblockDirectK the
+// sparse term compares the two examples' targets directly (K^2 compares); for
+// larger K column j of the sparse Yring is kept as a sorted list of (row,
+// value) pairs and (Yring^T Yring)_ij is a merge of two lists in ascending row
+// order.
 constexpr int kMblockThreads = 256;
+constexpr int kMblockDirectK = 16;  // K up to this: direct K x K compare, else sorted lists
 
 __global__ __launch_bounds__(kMblockThreads) void mblock_kernel(
     int m, int K, const int *__restrict__ idx, const float *__restrict__ lvec,
@@ -512,6 +515,31 @@ __global__ __launch_bounds__(kMblockThreads) void mblock_kernel(
     lval[q] = dA[q];
   }
   __syncthreads();
+  if (K <= kMblockDirectK) {
+    // (Yring^T Yring)_ij = sum_a sum_b [idx_ia = idx_jb >= 0] dl/dA_ia dl/dA_jb: the
+    // same bilinear sum as the merge of the two lists below (repeated rows add up
+    // either way), straight from the staged rows, K^2 compares in registers.
+    if (!has) return;
+    int rj[kMblockDirectK];
+    float vj[kMblockDirectK];
+#pragma unroll
+    for (int b = 0; b < kMblockDirectK; ++b) {
+      rj[b] = b < K ? lrow[j * K + b] : -1;
+      vj[b] = b < K ? lval[j * K + b] : 0.f;
+    }
+    float yy = 0.f;
+#pragma unroll
+    for (int a = 0; a < kMblockDirectK; ++a) {
+      if (a >= K) break;
+      const int r = lrow[i * K + a];
+      float sb = 0.f;
+#pragma unroll
+      for (int b = 0; b < kMblockDirectK; ++b) sb += (rj[b] == r) ? vj[b] : 0.f;
+      yy += (r >= 0) ? lval[i * K + a] * sb : 0.f;
+    }
+    M[e] = 4.f * di * mh * dj + yy + 2.f * di * hz + 2.f * dj * hzt;
+    return;
+  }
   for (int q = t; q < m; q += kMblockThreads) {
     int *lr = lrow + q * K;
     float *lv = lval + q * K;
