@@ -403,7 +403,16 @@ __global__ __launch_bounds__(64 * wb_waves<kPivotNbk>()) void pivot_block_kernel
       const int row = acc_row(h, r);
       a00[r] = (row < nb && j < nb) ? raw[r] : ((row == j) ? 1.f : 0.f);
     }
-    gj_inverter<NBK>(a00, sh, lane);
+    if (!gj_inverter<NBK>(a00, sh, lane)) return;
+    const int col = 32 * (NBK - 1) + j;
+    last_column<NBK>(sh, lane, [&](int s, const floatx16 &v) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = 32 * s + acc_row(h, r);
+        P[row * kBigBlock + col] = v[r];
+        PI[row * kBigBlock + col] = v[r] + ((row == col) ? 1.f : 0.f);
+      }
+    });
     return;
   }
   floatx16 acc[NS][NBK];
@@ -443,7 +452,7 @@ __global__ __launch_bounds__(64 * wb_waves<kPivotNbk>()) void pivot_block_kernel
   }
 #pragma unroll
   for (int t = 0; t < NS; ++t) {
-    if (wave + NW * t >= NBK) continue;
+    if (wave + NW * t >= NBK - 1) continue;  // column NBK - 1: the inverting wavefront's
     const int col = 32 * (wave + NW * t) + j;
 #pragma unroll
     for (int s = 0; s < NBK; ++s)

@@ -349,7 +349,9 @@ __device__ __forceinline__ void column_step(floatx16 (&acc)[NBK], GjLds<NBK> &sh
 // and all leave at the same step.
 
 // acc[t][i] is tile (i, wave + wb_workers t).  Returns false (uniformly) if a
-// pivot is not positive and finite; the tiles are then meaningless.
+// pivot is not positive and finite; the tiles are then meaningless.  Column
+// NBK - 1 is left at its values before the last block step: the inverting
+// wavefront finishes it (last_column).
 template <int NBK>
 __device__ __forceinline__ bool gj_workers(floatx16 (&acc)[wb_sets<NBK>()][NBK], GjLds<NBK> &sh,
                                            int wave, int lane) {
@@ -372,15 +374,17 @@ __device__ __forceinline__ bool gj_workers(floatx16 (&acc)[wb_sets<NBK>()][NBK],
 #pragma unroll
     for (int t = 0; t < NS; ++t) {
       const int col = wave + NW * t;
-      if (col < NBK) column_step<NBK>(acc[t], sh, col, kb, j, h);
+      // the last pivot column is the inverting wavefront's (last_column)
+      if (col < NBK && !(kb == NBK - 1 && col == kb)) column_step<NBK>(acc[t], sh, col, kb, j, h);
     }
   }
   return true;
 }
 
-// a00: the pivot block A_00 in accumulator layout.
+// a00: the pivot block A_00 in accumulator layout.  Returns false (uniformly,
+// at the same step as gj_workers) if a pivot is not positive and finite.
 template <int NBK>
-__device__ __forceinline__ void gj_inverter(const floatx16 &a00, GjLds<NBK> &sh, int lane) {
+__device__ __forceinline__ bool gj_inverter(const floatx16 &a00, GjLds<NBK> &sh, int lane) {
   const int j = lane & 31, h = lane >> 5;
   stage_a(sh.pin, a00, j, h);
   wave_lds_sync();
@@ -388,7 +392,7 @@ __device__ __forceinline__ void gj_inverter(const floatx16 &a00, GjLds<NBK> &sh,
   for (int kb = 0; kb < NBK; ++kb) {
     const int buf = kb & 1;
     __syncthreads();
-    if (__builtin_amdgcn_readfirstlane(sh.bad[buf])) return;
+    if (__builtin_amdgcn_readfirstlane(sh.bad[buf])) return false;
     if (kb + 1 == NBK) continue;
     float a[16], b[16];
     lds_operand(sh.pa[buf], j, h, a);
@@ -409,6 +413,39 @@ __device__ __forceinline__ void gj_inverter(const floatx16 &a00, GjLds<NBK> &sh,
     wave_lds_sync();
     if (!gj32_invert(sh.pin, sh.pa[buf ^ 1], sh.pb[buf ^ 1], sh.scr, lane) && lane == 0)
       sh.bad[buf ^ 1] = 1;
+  }
+  return true;
+}
+
+// The last block step's pivot column (kb = NBK - 1), by the inverting wavefront
+// after gj_inverter: tile (i, kb) of the inverse is -A_i,kb P = cpan[kb & 1][i] P
+// for i != kb and P itself for i = kb, all from LDS the last step left in place
+// (nothing writes those buffers after its opening barrier).  This takes the
+// column's three products and its stores off its owner, which in the last step
+// would otherwise hold two columns.  out(i, tile) receives each tile.  Every lane
+// of the wavefront must call it (the products read all lanes' operands).
+template <int NBK, typename Out>
+__device__ __forceinline__ void last_column(const GjLds<NBK> &sh, int lane, Out out) {
+  constexpr int kb = NBK - 1, buf = kb & 1;
+  const int j = lane & 31, h = lane >> 5;
+  float b[16];
+  lds_operand(sh.pb[buf], j, h, b);  // P at (acc_row(h, r), j)
+#pragma unroll
+  for (int s = 0; s < NBK; ++s) {
+    floatx16 v;
+    if (s == kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) v[r] = b[r];
+    } else {
+      float a[16];
+      lds_operand(sh.cpan[buf][s], j, h, a);
+      floatx16 z;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) z[r] = 0.f;
+      v = mfma32(a, b, z);
+    }
+    out(s, v);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -450,7 +487,24 @@ __device__ __forceinline__ void woodbury_blocked(int m, float lr, int unit_dq,
       const float c = (row < m && j < m) ? -(sr[r] * raw[r] * sc) : 0.f;
       a00[r] = (row == j) ? 1.f + c : c;
     }
-    gj_inverter<NBK>(a00, sh, lane);
+    if (!gj_inverter<NBK>(a00, sh, lane)) return;
+    // the whole wavefront takes part in the products; only the stores are masked
+    const int lcol = 32 * (NBK - 1) + j;
+    const float lsc = tl * sq[min(lcol, m - 1)];
+    last_column<NBK>(sh, lane, [&](int s, const floatx16 &v) {
+      if (lcol >= m) return;
+      float sr[16];
+      lds_operand(sq + 32 * s, 0, h, sr);
+      const int base = (32 * s + 4 * h) * m + lcol;
+      if (32 * s + 32 <= m) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) R[base + ((r & 3) + 8 * (r >> 2)) * m] = sr[r] * v[r] * lsc;
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (32 * s + acc_row(h, r) < m) R[base + ((r & 3) + 8 * (r >> 2)) * m] = sr[r] * v[r] * lsc;
+      }
+    });
     return;
   }
   floatx16 acc[NS][NBK];
@@ -498,7 +552,7 @@ __device__ __forceinline__ void woodbury_blocked(int m, float lr, int unit_dq,
 #pragma unroll
   for (int t = 0; t < NS; ++t) {
     const int col = 32 * (wave + NW * t) + j;
-    if (wave + NW * t >= NBK || col >= m) continue;
+    if (wave + NW * t >= NBK - 1 || col >= m) continue;  // column NBK - 1: the inverting wavefront's
     const float sc = tl * sq[col];
 #pragma unroll
     for (int s = 0; s < NBK; ++s) {
