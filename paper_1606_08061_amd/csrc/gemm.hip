@@ -447,14 +447,21 @@ __global__ __launch_bounds__(256) void gemm16_plan_kernel(const GemmBatch *__res
   step_sync_begin(sync);
   if ((int)blockIdx.x >= bt->total_tiles) {
     // Prefetch workgroup: the target rows of example j (indices outside [0, D) skipped).
+    // The indices first (one load each, through LDS), then one load per 128-byte
+    // line of every row, all at once.
     const int j = (int)blockIdx.x - bt->pf_base;
     if (j < 0 || j >= bt->pf_m) return;
-    float sink = 0.f;
-    for (int k = 0; k < pf_K; ++k) {
+    __shared__ int prow[LST_MAX_K];
+    for (int k = threadIdx.x; k < pf_K; k += 256) {
       const int r = pf_idx[(int64_t)j * pf_K + k];
-      if (r < 0 || (int64_t)r >= bt->pf_D) continue;
-      const float *row = bt->pf_V + (int64_t)r * bt->pf_ldv;
-      for (int c = threadIdx.x; c < bt->pf_d; c += 256) sink += row[c];
+      prow[k] = (r < 0 || (int64_t)r >= bt->pf_D) ? -1 : r;
+    }
+    __syncthreads();
+    const int nl = (bt->pf_d + 31) >> 5;  // 128-byte lines per row (one load touches each)
+    float sink = 0.f;
+    for (int e = threadIdx.x; e < pf_K * nl; e += 256) {
+      const int k = e / nl, r = prow[k];
+      if (r >= 0) sink += bt->pf_V[(int64_t)r * bt->pf_ldv + 32 * (e - k * nl)];
     }
     asm volatile("" ::"v"(sink));
     return;
