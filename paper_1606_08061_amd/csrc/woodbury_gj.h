@@ -387,34 +387,36 @@ template <int NBK>
 __device__ __forceinline__ bool gj_inverter(const floatx16 &a00, GjLds<NBK> &sh, int lane) {
   const int j = lane & 31, h = lane >> 5;
   stage_a(sh.pin, a00, j, h);
-  wave_lds_sync();
-  if (!gj32_invert(sh.pin, sh.pa[0], sh.pb[0], sh.scr, lane) && lane == 0) sh.bad[0] = 1;
-  for (int kb = 0; kb < NBK; ++kb) {
-    const int buf = kb & 1;
-    __syncthreads();
-    if (__builtin_amdgcn_readfirstlane(sh.bad[buf])) return false;
-    if (kb + 1 == NBK) continue;
-    float a[16], b[16];
-    lds_operand(sh.pa[buf], j, h, a);
-    lds_operand(sh.nb[buf], j, h, b);
-    floatx16 z;
+  // kb = -1 inverts A_00 into buffer 0; block step kb >= 0 forms and inverts the next
+  // pivot block.  One call site of the inversion: a single copy of its code.
+  for (int kb = -1; kb < NBK - 1; ++kb) {
+    const int dst = (kb + 1) & 1;
+    if (kb >= 0) {
+      const int buf = kb & 1;
+      __syncthreads();
+      if (__builtin_amdgcn_readfirstlane(sh.bad[buf])) return false;
+      float a[16], b[16];
+      lds_operand(sh.pa[buf], j, h, a);
+      lds_operand(sh.nb[buf], j, h, b);
+      floatx16 z;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) z[r] = 0.f;
-    const floatx16 t = mfma32(a, b, z);  // P A_kb,kb+1
-    float d[16];
-    lds_operand(sh.cpan[buf][kb + 1], j, h, a);
-    lds_operand(sh.nd[buf], j, h, d);
+      for (int r = 0; r < 16; ++r) z[r] = 0.f;
+      const floatx16 t = mfma32(a, b, z);  // P A_kb,kb+1
+      float d[16];
+      lds_operand(sh.cpan[buf][kb + 1], j, h, a);
+      lds_operand(sh.nd[buf], j, h, d);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      b[r] = t[r];
-      z[r] = d[r];
+      for (int r = 0; r < 16; ++r) {
+        b[r] = t[r];
+        z[r] = d[r];
+      }
+      stage_a(sh.pin, mfma32(a, b, z), j, h);
     }
-    stage_a(sh.pin, mfma32(a, b, z), j, h);
     wave_lds_sync();
-    if (!gj32_invert(sh.pin, sh.pa[buf ^ 1], sh.pb[buf ^ 1], sh.scr, lane) && lane == 0)
-      sh.bad[buf ^ 1] = 1;
+    if (!gj32_invert(sh.pin, sh.pa[dst], sh.pb[dst], sh.scr, lane) && lane == 0) sh.bad[dst] = 1;
   }
-  return true;
+  __syncthreads();  // the barrier that opens the last block step
+  return !__builtin_amdgcn_readfirstlane(sh.bad[(NBK - 1) & 1]);
 }
 
 // The last block step's pivot column (kb = NBK - 1), by the inverting wavefront
