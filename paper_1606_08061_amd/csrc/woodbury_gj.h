@@ -12,10 +12,12 @@ namespace {
 // Blocked Gauss-Jordan inverse on the matrix cores.
 //
 // The mp x mp matrix (mp = 32 NBK >= m, padded with the identity) lives in
-// MFMA accumulator registers as NBK x NBK tiles of 32 x 32: wavefront w < NBK
-// holds tile column w (acc[i] = tile (i, w)) and wavefront NBK inverts the
-// pivot blocks.  In accumulator layout lane l = j + 32 h holds column j of a
-// tile and register r holds row acc_row(h, r).  Block step kb with pivot block
+// MFMA accumulator registers as NBK x NBK tiles of 32 x 32, each tile column
+// held by one column wavefront (acc[i] = tile (i, c); at most three of them,
+// so one holds two columns when NBK = 4), and one more wavefront forms and
+// inverts the pivot blocks (see gj_workers).  In accumulator layout lane
+// l = j + 32 h holds column j of a tile and register r holds row acc_row(h, r).
+// Block step kb with pivot block
 // P = A_kb,kb^{-1} is, in place,
 //   A_kb,j <- P A_kb,j,   A_ij <- A_ij - A_i,kb (P A_kb,j),
 //   A_i,kb <- -A_i,kb P,  A_kb,kb <- P                          (i, j != kb),
@@ -451,7 +453,7 @@ __device__ __forceinline__ void last_column(const GjLds<NBK> &sh, int lane, Out 
   }
 }
 
-// The whole inverse on one workgroup of 64 wb_waves threads (m <= 32 NBK):
+// The whole inverse on one workgroup of 64 wb_waves<NBK>() threads (m <= 32 NBK):
 // C = I - 2 eta S N S from N, its inverse, R = 2 eta S C^{-1} S.  A rejected
 // matrix (non-positive pivot, negative or NaN dl/dq) raises FLAG_NOT_SPD.
 template <int NBK>
