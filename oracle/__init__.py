@@ -13,6 +13,9 @@ oracle shares no code, table or helper with that path.
                against the dense definition and to expose the intermediates
                (H^, G, Z^, M, the Woodbury matrices, P) when a GPU kernel has to
                be examined step by step.
+  stabilize -- section 5: the pristine restore, the recomputed U^{-T}, power
+               iteration for the extreme singular values of U, Algorithm 5's
+               fix-singular-value and the stabilisation loop around them.
 
 All inputs are float64 upcasts of the float32 arrays the GPU receives.
 """
