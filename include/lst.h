@@ -76,8 +76,11 @@ enum lst_status {
   LST_E_INDEX = -3,     /* (device) a target index outside [-1, D)             */
   LST_E_NOT_SPD = -4,   /* (device) the m x m Woodbury matrix is not positive
                            definite: the step is too large for the batch
-                           (m = 1: 1 - 2 eta ||h||^2 <= 0, eq. updateU-T)       */
-  LST_E_NONFINITE = -5, /* (device) the loss is NaN or infinite                */
+                           (m = 1: 1 - 2 eta ||h||^2 <= 0, eq. updateU-T);
+                           (host) U is numerically singular (section 5)       */
+  LST_E_NONFINITE = -5, /* (device) the loss is NaN or infinite, or a singular
+                           value given to fix-singular-value is not positive
+                           and finite                                          */
   LST_E_HIP = -6,       /* a HIP runtime call failed                           */
   LST_E_STATE = -7,     /* wrong context kind for this call                    */
   LST_E_SYNC = -8       /* (device) a step's two streams lost their ordering: a
@@ -158,6 +161,73 @@ int lst_use_graphs(lst_ctx *c, int32_t on);
  * explicit weights, an O(D d^2) product).  For a naive context, copies its W.
  */
 int lst_materialize_W(lst_ctx *c, float *W, int64_t ldw);
+
+/*
+ * Numerical stabilisation (section 5), on a factored context, between steps.
+ * Each call is enqueued on the context's stream after the steps before it
+ * (lst_singular_stabilize synchronises it); none changes W = V U or Q = W^T W
+ * beyond fp32 rounding.  Device-side errors surface at lst_sync_status.
+ *
+ * lst_restore_pristine -- section 5.1: V <- V U (in place, an O(D d^2) product on
+ * the matrix cores), then U <- I and U^{-T} <- I.  Needs d <= 1024 (LST_E_SHAPE
+ * otherwise).
+ */
+int lst_restore_pristine(lst_ctx *c);
+
+/*
+ * lst_refresh_uinvt -- section 5.3: U^{-T} recomputed from U, so that the drift
+ * the rank-m updates accumulate in it is discarded.  Runs iters (1..100) rounds of
+ * the Newton-Schulz iteration Y <- Y + E Y, E = I - Y U^T, with E accumulated in
+ * fp64 and E Y an fp32 product on the matrix cores (mixed-precision refinement: the
+ * result is the fp32 rounding of U^{-T} while cond(U) is below about 1e7).  Starts
+ * from the carried U^{-T} (from_scratch = 0; converges if max |E| < 1, then each
+ * round squares the error) or from U / (||U||_1 ||U||_inf) (from_scratch = 1:
+ * converges for any invertible U, in about 2 log2(cond U) + 5 rounds).  resid_dev:
+ * one device float receiving max_ij |(I - U^{-T} U^T)_ij| after the last round, or
+ * NULL.  The paper recomputes by Gaussian elimination; the result is the same
+ * inverse.
+ */
+int lst_refresh_uinvt(lst_ctx *c, int32_t iters, int32_t from_scratch, float *resid_dev);
+
+/*
+ * lst_power_iteration -- section 5.3: an extreme singular value of U and its left
+ * singular vector by 2^log2_iters (0..30) power iterations u <- A A^T u / ||A A^T u||
+ * from u0: A = U for the largest (which = 0), A = U^{-T} for the smallest (which =
+ * 1; sigma = 1 / ||U^{-1} u||).  The iterations are carried out as log2_iters
+ * squarings of A A^T on the matrix cores.  u0, u_out: d device floats (may alias);
+ * u_out receives the unit vector, sigma_out (one device float) the singular value.
+ * which = 1 uses the carried U^{-T}: refresh it first if it may have drifted.
+ */
+int lst_power_iteration(lst_ctx *c, int32_t which, int32_t log2_iters, const float *u0,
+                        float *u_out, float *sigma_out);
+
+/*
+ * lst_fix_singular_value -- Algorithm 5, fix-singular-value: the singular value
+ * s = *sigma_dev (device float) of U along its left singular vector u (d device
+ * floats, unit norm) becomes target (> 0): with a = (target - s) / s and
+ * b = -a / (1 + a), U <- U + a u (U^T u)^T, V <- V + b (V u) u^T (one pass over V)
+ * and U^{-T} <- U^{-T} + b u (U^{-1} u)^T.  If *sigma_dev is not positive and
+ * finite, nothing changes and lst_sync_status reports LST_E_NONFINITE.
+ */
+int lst_fix_singular_value(lst_ctx *c, const float *u, const float *sigma_dev, float target);
+
+/*
+ * lst_singular_stabilize -- the procedure of section 5.3 around Algorithm 5:
+ * U^{-T} recomputed first (lst_refresh_uinvt: two rounds from the carried value if
+ * its residual max |I - U^{-T} U^T| is below 1/4, else rounds from scratch until it
+ * is, then two more; LST_E_NOT_SPD if 96 rounds do not get there, U being
+ * numerically singular), then, while the smallest singular value of U
+ * (lst_power_iteration, which = 1) is below lo and fewer than max_fixes corrections
+ * have been made, it is set to 1; then the same for the largest (which = 0) above
+ * hi.  Every search starts from u0 (d device floats) with 2^log2_iters iterations.
+ * Host outputs: n_fixed[0], n_fixed[1] the corrections of the smallest and of the
+ * largest; sigmas[0], sigmas[1] the last smallest and largest singular values
+ * found.  Synchronises the stream after each search; LST_E_NONFINITE if a search
+ * returns a value that is not positive and finite.  The paper suggests a safe
+ * range of [0.001, 100] checked every 100 steps.
+ */
+int lst_singular_stabilize(lst_ctx *c, float lo, float hi, int32_t log2_iters, const float *u0,
+                           int32_t max_fixes, int32_t *n_fixed, float *sigmas);
 
 /*
  * lst_sync_status -- synchronises the context's streams, returns the sticky

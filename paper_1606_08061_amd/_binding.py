@@ -50,6 +50,12 @@ SIGNATURES = {
     "lst_use_graphs": (_I32, [_P, _I32]),
     "lst_profile_enable": (_I32, [_P, _I32]),
     "lst_profile_read": (_I32, [_P, ctypes.POINTER(_I32), ctypes.POINTER(ctypes.c_double), _I32]),
+    "lst_restore_pristine": (_I32, [_P]),
+    "lst_refresh_uinvt": (_I32, [_P, _I32, _I32, _P]),
+    "lst_power_iteration": (_I32, [_P, _I32, _I32, _P, _P, _P]),
+    "lst_fix_singular_value": (_I32, [_P, _P, _P, _F]),
+    "lst_singular_stabilize": (_I32, [_P, _F, _F, _I32, _P, _I32, ctypes.POINTER(_I32),
+                                      ctypes.POINTER(_F)]),
 }
 
 PHASES = ["contract", "gather", "zgrad", "mblock", "woodbury", "mid", "update", "scatter",
@@ -156,6 +162,29 @@ def lst_profile_read(ctx) -> tuple[int, dict]:
     ms = (ctypes.c_double * n)()
     st = lib().lst_profile_read(ctx, counts, ms, n)
     return st, {PHASES[p]: (int(counts[p]), float(ms[p])) for p in range(n)}
+
+
+def lst_restore_pristine(ctx) -> int:
+    return lib().lst_restore_pristine(ctx)
+
+
+def lst_refresh_uinvt(ctx, iters, from_scratch, resid_dev) -> int:
+    return lib().lst_refresh_uinvt(ctx, iters, from_scratch, resid_dev)
+
+
+def lst_power_iteration(ctx, which, log2_iters, u0, u_out, sigma_out) -> int:
+    return lib().lst_power_iteration(ctx, which, log2_iters, u0, u_out, sigma_out)
+
+
+def lst_fix_singular_value(ctx, u, sigma_dev, target) -> int:
+    return lib().lst_fix_singular_value(ctx, u, sigma_dev, target)
+
+
+def lst_singular_stabilize(ctx, lo, hi, log2_iters, u0, max_fixes) -> tuple[int, tuple, tuple]:
+    n = (_I32 * 2)()
+    sig = (_F * 2)()
+    st = lib().lst_singular_stabilize(ctx, lo, hi, log2_iters, u0, max_fixes, n, sig)
+    return st, (int(n[0]), int(n[1])), (float(sig[0]), float(sig[1]))
 
 
 # ---- tensor-level wrappers ----
@@ -274,6 +303,51 @@ class Factored(_Ctx):
 
     def use_graphs(self, on: bool = True) -> None:
         _check(lst_use_graphs(self.ctx, 1 if on else 0), "lst_use_graphs")
+
+    # ---- section 5: numerical stabilisation between steps ----
+
+    def restore_pristine(self) -> None:
+        """V <- V U, U <- I, U^{-T} <- I (in place; d <= 1024)."""
+        _check(lst_restore_pristine(self.ctx), "lst_restore_pristine")
+
+    def refresh_uinvt(self, iters=2, from_scratch=False, resid=None):
+        """Recompute U^{-T} from U (Newton-Schulz rounds); resid: optional 0-d device tensor
+        receiving max |I - U^{-T} U^T|."""
+        if resid is not None:
+            _need(resid, torch.float32, (), "resid")
+        _check(lst_refresh_uinvt(self.ctx, int(iters), 1 if from_scratch else 0, _ptr(resid)),
+               "lst_refresh_uinvt")
+        return resid
+
+    def power_iteration(self, which, log2_iters, u0, u_out=None, sigma_out=None):
+        """which = "largest" or "smallest" singular value of U; returns (u, sigma) device tensors."""
+        w = {"largest": 0, "smallest": 1}[which]
+        _need(u0, torch.float32, (self.d,), "u0")
+        if u_out is None:
+            u_out = torch.empty(self.d, dtype=torch.float32, device=self.device)
+        if sigma_out is None:
+            sigma_out = torch.empty((), dtype=torch.float32, device=self.device)
+        _need(u_out, torch.float32, (self.d,), "u_out")
+        _need(sigma_out, torch.float32, (), "sigma_out")
+        _check(lst_power_iteration(self.ctx, w, int(log2_iters), _ptr(u0), _ptr(u_out),
+                                   _ptr(sigma_out)), "lst_power_iteration")
+        return u_out, sigma_out
+
+    def fix_singular_value(self, u, sigma, target=1.0) -> None:
+        """Algorithm 5 fix-singular-value with device tensors u (d) and sigma (0-d)."""
+        _need(u, torch.float32, (self.d,), "u")
+        _need(sigma, torch.float32, (), "sigma")
+        _check(lst_fix_singular_value(self.ctx, _ptr(u), _ptr(sigma), float(target)),
+               "lst_fix_singular_value")
+
+    def singular_stabilize(self, u0, lo=1e-3, hi=100.0, log2_iters=7, max_fixes=8):
+        """Section 5.3's loop; returns ((fixes of the smallest, of the largest),
+        (last smallest, last largest singular value))."""
+        _need(u0, torch.float32, (self.d,), "u0")
+        st, n, sig = lst_singular_stabilize(self.ctx, float(lo), float(hi), int(log2_iters),
+                                            _ptr(u0), int(max_fixes))
+        _check(st, "lst_singular_stabilize")
+        return n, sig
 
 
 class Naive(_Ctx):

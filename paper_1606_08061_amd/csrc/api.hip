@@ -80,6 +80,9 @@ struct lst_ctx {
   float *N, *Mhat, *HZ, *M, *R, *Cwork;
   float *Pbig, *Cp, *Rp;  // blocked Woodbury inverse for m > kWoodburyOneWG
   float *dq, *lvec, *dA;
+  // section 5 stabilisation: two d x d scratch matrices (row stride d), four
+  // d-vectors and eight scalars
+  float *Sd0, *Sd1, *svec, *sscal;
   int *flag;
   // progress counters ordering the two streams of a factored step: [0] contraction
   // launches started, [1] Woodbury inverses completed, [2] Z^ launches started
@@ -146,6 +149,10 @@ void carve_factored(lst_ctx *c, Carver &cv) {
   c->dq = cv.take<float>(c->m_max);
   c->lvec = cv.take<float>(c->m_max);
   c->dA = cv.take<float>(mk);
+  c->Sd0 = cv.take<float>((size_t)c->d * c->d);
+  c->Sd1 = cv.take<float>((size_t)c->d * c->d);
+  c->svec = cv.take<float>(4 * (size_t)c->d);
+  c->sscal = cv.take<float>(8);
   c->flag = cv.take<int>(1);
   c->cnt = cv.take<int>(3);
   c->plan_pool = cv.take<GemmBatch>(kPlanCap * kPlanBatches);
@@ -938,6 +945,189 @@ int lst_naive_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, co
                            false, c->flag, s, GEMM_NAIVE_UPDATE)))
     return LST_E_HIP;
   prof(c, LST_PHASE_NAIVE_UPDATE, false);
+  return LST_OK;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Section 5: numerical stabilisation between steps.
+// ---------------------------------------------------------------------------
+namespace {
+
+int factored_ctx(const lst_ctx *c) {
+  if (!c) return LST_E_ARG;
+  return c->kind == KIND_FACTORED ? LST_OK : LST_E_STATE;
+}
+
+hipError_t square_gemm(lst_ctx *c, const float *A, int lda, int tA, const float *B, int ldb,
+                       int tB, float *C, int ldc, float alpha = 1.f, const float *Cin = nullptr,
+                       int ldcin = 0, float beta = 0.f) {
+  const int d = c->d;
+  GemmBatch b{};
+  b.d[0] = gemm_desc(d, d, d, A, lda, tA, B, ldb, tB, C, ldc, alpha, Cin, ldcin, beta);
+  b.n = 1;
+  return gemm_launch(b, nullptr, c->stream);
+}
+
+// Newton-Schulz rounds Y <- Y + (I - Y U^T) Y ending in U^{-T}; see lst_refresh_uinvt.
+int refresh_uinvt(lst_ctx *c, int iters, bool from_scratch, float *resid) {
+  const int d = c->d, ldd = c->ldd;
+  hipStream_t s = c->stream;
+  float *Y = c->UinvT;
+  int ldy = ldd;
+  if (from_scratch) {
+    if (record(c, launch_ns_start(s, c->U, ldd, d, c->sscal, c->Sd0, d))) return LST_E_HIP;
+    Y = c->Sd0;
+    ldy = d;
+  }
+  for (int it = 0; it < iters; ++it) {
+    float *Yn = Y == c->UinvT ? c->Sd0 : c->UinvT;
+    const int ldn = Yn == c->UinvT ? ldd : d;
+    if (record(c, launch_residual64(s, Y, ldy, c->U, ldd, d, c->Sd1)) ||            // E = I - Y U^T
+        record(c, square_gemm(c, c->Sd1, d, 0, Y, ldy, 1, Yn, ldn, 1.f, Y, ldy, 1.f)))  // Y + E Y
+      return LST_E_HIP;
+    Y = Yn;
+    ldy = ldn;
+  }
+  if (Y != c->UinvT &&
+      record(c, hipMemcpy2DAsync(c->UinvT, (size_t)ldd * sizeof(float), Y, (size_t)d * sizeof(float),
+                                 (size_t)d * sizeof(float), (size_t)d, hipMemcpyDeviceToDevice, s)))
+    return LST_E_HIP;
+  if (resid && (record(c, launch_residual64(s, c->UinvT, ldd, c->U, ldd, d, c->Sd1)) ||
+                record(c, launch_fill(s, resid, 0.f)) || record(c, launch_absmax(s, c->Sd1, d, resid))))
+    return LST_E_HIP;
+  return LST_OK;
+}
+
+// max |I - U^{-T} U^T| of the current U^{-T}, on the host (synchronises the stream).
+int uinvt_residual(lst_ctx *c, float *r) {
+  float *dev = c->sscal + 2;
+  if (record(c, launch_residual64(c->stream, c->UinvT, c->ldd, c->U, c->ldd, c->d, c->Sd1)) ||
+      record(c, launch_fill(c->stream, dev, 0.f)) ||
+      record(c, launch_absmax(c->stream, c->Sd1, c->d, dev)) ||
+      record(c, hipMemcpyAsync(r, dev, sizeof(float), hipMemcpyDeviceToHost, c->stream)) ||
+      record(c, hipStreamSynchronize(c->stream)))
+    return LST_E_HIP;
+  return LST_OK;
+}
+
+// U^{-T} recomputed before a stabilisation check: two rounds from the carried value
+// when its residual is small enough for the iteration to converge from it, else from
+// scratch in groups of eight rounds until the residual is small, then two more.
+constexpr float kWarmResidual = 0.25f;
+int refresh_for_check(lst_ctx *c) {
+  float r = 0.f;
+  int st = uinvt_residual(c, &r);
+  if (st != LST_OK) return st;
+  if (!(r < kWarmResidual)) {
+    bool scratch = true;
+    for (int rounds = 0; !(r < kWarmResidual); rounds += 8) {
+      if (rounds >= 96) return LST_E_NOT_SPD;  // U is numerically singular
+      if ((st = refresh_uinvt(c, 8, scratch, nullptr)) != LST_OK ||
+          (st = uinvt_residual(c, &r)) != LST_OK)
+        return st;
+      scratch = false;
+    }
+  }
+  return refresh_uinvt(c, 2, false, nullptr);
+}
+
+int power_iteration(lst_ctx *c, int which, int log2_iters, const float *u0, float *u_out,
+                    float *sigma_out) {
+  const int d = c->d, ldd = c->ldd;
+  hipStream_t s = c->stream;
+  const float *A = which ? c->UinvT : c->U;
+  if (record(c, square_gemm(c, A, ldd, 0, A, ldd, 0, c->Sd0, d))) return LST_E_HIP;  // G = A A^T
+  for (int it = 0; it < log2_iters; ++it)
+    if (record(c, launch_trace_scale(s, c->Sd0, d, c->Sd1)) ||
+        record(c, square_gemm(c, c->Sd1, d, 0, c->Sd1, d, 1, c->Sd0, d)))
+      return LST_E_HIP;
+  return record(c, launch_power_finish(s, c->Sd0, d, u0, A, ldd, which, u_out, sigma_out));
+}
+
+int fix_singular_value(lst_ctx *c, const float *u, const float *sigma, float target) {
+  const int d = c->d, ldd = c->ldd;
+  hipStream_t s = c->stream;
+  float *a = c->svec, *b = c->svec + d;
+  if (record(c, launch_tmatvec(s, c->U, ldd, d, u, a)) ||
+      record(c, launch_tmatvec(s, c->UinvT, ldd, d, u, b)) ||
+      record(c, launch_fix_state(s, c->U, c->UinvT, ldd, d, u, a, b, sigma, target, c->flag)) ||
+      record(c, launch_fix_v(s, c->V, c->ldv, c->D, d, u, sigma, target)))
+    return LST_E_HIP;
+  return LST_OK;
+}
+
+bool in_svec(const lst_ctx *c, const float *p) {
+  return p >= c->svec && p < c->svec + 4 * (size_t)c->d;
+}
+
+}  // namespace
+
+extern "C" {
+
+int lst_restore_pristine(lst_ctx *c) {
+  int st = factored_ctx(c);
+  if (st != LST_OK) return st;
+  if (c->d > 1024) return LST_E_SHAPE;
+  hipStream_t s = c->stream;
+  if (record(c, launch_restore(s, c->V, c->ldv, c->D, c->U, c->ldd, c->d)) ||
+      record(c, launch_identity(s, c->U, c->d, c->ldd)) ||
+      record(c, launch_identity(s, c->UinvT, c->d, c->ldd)))
+    return LST_E_HIP;
+  return LST_OK;
+}
+
+int lst_refresh_uinvt(lst_ctx *c, int32_t iters, int32_t from_scratch, float *resid_dev) {
+  int st = factored_ctx(c);
+  if (st != LST_OK) return st;
+  if (iters < 1 || iters > 100) return LST_E_ARG;
+  return refresh_uinvt(c, iters, from_scratch != 0, resid_dev);
+}
+
+int lst_power_iteration(lst_ctx *c, int32_t which, int32_t log2_iters, const float *u0,
+                        float *u_out, float *sigma_out) {
+  int st = factored_ctx(c);
+  if (st != LST_OK) return st;
+  if ((which != 0 && which != 1) || log2_iters < 0 || log2_iters > 30 || !u0 || !u_out ||
+      !sigma_out)
+    return LST_E_ARG;
+  return power_iteration(c, which, log2_iters, u0, u_out, sigma_out);
+}
+
+int lst_fix_singular_value(lst_ctx *c, const float *u, const float *sigma_dev, float target) {
+  int st = factored_ctx(c);
+  if (st != LST_OK) return st;
+  if (!u || !sigma_dev || !finite_pos(target) || in_svec(c, u)) return LST_E_ARG;
+  return fix_singular_value(c, u, sigma_dev, target);
+}
+
+int lst_singular_stabilize(lst_ctx *c, float lo, float hi, int32_t log2_iters, const float *u0,
+                           int32_t max_fixes, int32_t *n_fixed, float *sigmas) {
+  int st = factored_ctx(c);
+  if (st != LST_OK) return st;
+  if (!finite_pos(lo) || !finite_pos(hi) || hi < lo || log2_iters < 0 || log2_iters > 30 || !u0 ||
+      max_fixes < 0 || !n_fixed || !sigmas)
+    return LST_E_ARG;
+  hipStream_t s = c->stream;
+  if ((st = refresh_for_check(c)) != LST_OK) return st;
+  float *u = c->svec + 2 * (size_t)c->d, *sig = c->sscal + 1;
+  for (int which = 1; which >= 0; --which) {  // the smallest singular value first
+    int n = 0;
+    float sv = 0.f;
+    for (;;) {
+      if ((st = power_iteration(c, which, log2_iters, u0, u, sig)) != LST_OK) return st;
+      if (record(c, hipMemcpyAsync(&sv, sig, sizeof(float), hipMemcpyDeviceToHost, s)) ||
+          record(c, hipStreamSynchronize(s)))
+        return LST_E_HIP;
+      if (!std::isfinite(sv) || !(sv > 0.f)) return LST_E_NONFINITE;
+      if ((which ? sv >= lo : sv <= hi) || n >= max_fixes) break;
+      if ((st = fix_singular_value(c, u, sig, 1.f)) != LST_OK) return st;
+      ++n;
+    }
+    n_fixed[1 - which] = n;
+    sigmas[1 - which] = sv;
+  }
   return LST_OK;
 }
 

@@ -245,4 +245,36 @@ hipError_t launch_grad_o(hipStream_t s, float *O, int64_t D, int m, int K, const
                          const int *idx, const float *dA, const float *lvec, float *loss_out,
                          int *flag);
 
+// ---------------------------------------------------------------------------
+// Numerical stabilisation kernels (stabilize.hip), enqueued between steps.
+// ---------------------------------------------------------------------------
+// V <- V U in place (d <= 1024, else hipErrorInvalidValue).
+hipError_t launch_restore(hipStream_t s, float *V, int64_t ldv, int64_t D, const float *U, int ldd,
+                          int d);
+// y = A^T x for a d x d row-major A (y must not alias x).
+hipError_t launch_tmatvec(hipStream_t s, const float *A, int lda, int d, const float *x, float *y);
+// Algorithm 5's rank-one updates of U and U^{-T} (a = U^T u, b = (U^{-T})^T u) and
+// of V, with the coefficients formed from the device scalar *sigma; a sigma that
+// is not positive and finite skips both and sets FLAG_NONFINITE.
+hipError_t launch_fix_state(hipStream_t s, float *U, float *UinvT, int ldd, int d, const float *u,
+                            const float *a, const float *b, const float *sigma, float target,
+                            int *flag);
+hipError_t launch_fix_v(hipStream_t s, float *V, int64_t ldv, int64_t D, int d, const float *u,
+                        const float *sigma, float target);
+// out = S / trace(S) for a d x d S (row stride d); out must not alias S.
+hipError_t launch_trace_scale(hipStream_t s, const float *S, int d, float *out);
+// u_out = S u0 / ||S u0||, *sigma_out = ||A^T u_out|| (which = 0) or its inverse.
+hipError_t launch_power_finish(hipStream_t s, const float *S, int d, const float *u0,
+                               const float *A, int lda, int which, float *u_out,
+                               float *sigma_out);
+// Y = U / (||U||_1 ||U||_inf), the from-scratch start of the Newton-Schulz
+// iteration (*c receives the factor).
+hipError_t launch_ns_start(hipStream_t s, const float *U, int ldd, int d, float *c, float *Y,
+                           int ldy);
+// E = I - Y U^T (d x d, row stride d) with fp64 accumulation.
+hipError_t launch_residual64(hipStream_t s, const float *Y, int ldy, const float *U, int ldu, int d,
+                             float *E);
+// *amax = max_ij |E_ij| (E d x d, row stride d); *amax must be 0 on entry.
+hipError_t launch_absmax(hipStream_t s, const float *E, int d, float *amax);
+
 }  // namespace lst

@@ -73,6 +73,12 @@ def test_host_argument_errors(L):
     assert lst.lst_step(0, P, 1, P, P, 1, 0.1, P, P) == lst.LST_E_ARG
     assert lst.lst_sync_status(0) == lst.LST_E_ARG
     assert lst.lst_materialize_W(0, P, 8) == lst.LST_E_ARG
+    # section 5 entry points: a null context is rejected before anything else
+    assert lst.lst_restore_pristine(0) == lst.LST_E_ARG
+    assert lst.lst_refresh_uinvt(0, 2, 0, 0) == lst.LST_E_ARG
+    assert lst.lst_power_iteration(0, 0, 7, P, P, P) == lst.LST_E_ARG
+    assert lst.lst_fix_singular_value(0, P, P, 1.0) == lst.LST_E_ARG
+    assert lst.lst_singular_stabilize(0, 1e-3, 100.0, 7, P, 8)[0] == lst.LST_E_ARG
     lst.lst_destroy(0)
 
 
