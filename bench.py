@@ -271,6 +271,54 @@ def vendor_gemms(w, dev, H) -> dict:
     return out
 
 
+def stabilize_leg(f, w, dev, reps=5):
+    """Section 5 operations on the benchmark's state after its steps (V of D x d): each
+    timed with HIP events on the context's stream over reps calls.  The pristine restore
+    is an O(D d^2) product (2 D d^2 flops, bound by the matrix cores); the fix of one
+    singular value passes once over V (2 D d 4 bytes read and written, bound by HBM)."""
+    import torch
+
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(fn, n=reps):
+        fn()  # warm-up call
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        f.check("stabilize leg")
+        return e0.elapsed_time(e1) / n * 1e3  # us per call
+
+    g = torch.Generator(device=dev).manual_seed(17)
+    u0 = torch.randn(w.d, generator=g, device=dev)
+    u = u0 / u0.norm()
+    sig = torch.tensor(0.5, device=dev)
+    out = {}
+    out["fix_us"] = timed(lambda: f.fix_singular_value(u, sig, 1.0))
+    out["power_iteration_us"] = timed(lambda: f.power_iteration("smallest", 7, u0))
+    out["refresh_us"] = timed(lambda: f.refresh_uinvt(2))
+    out["restore_us"] = timed(lambda: f.restore_pristine())
+    h0 = time.perf_counter()
+    n_fix, sigmas = f.singular_stabilize(u0, 1e-3, 100.0, 7, 8)
+    out["check_ms_wall"] = (time.perf_counter() - h0) * 1e3
+    out["check_result"] = {"fixes": list(n_fix), "sigma_min": sigmas[0], "sigma_max": sigmas[1]}
+    restore_flops = 2.0 * w.D * w.d * w.d
+    fix_bytes = 2.0 * w.D * w.d * 4
+    out["restore_roofline"] = {"bound": "mfma", "achieved": round(restore_flops / out["restore_us"] / 1e6, 2),
+                               "peak": PEAK_FP32_TFLOPS, "unit": "TFLOP/s",
+                               "frac": round(restore_flops / out["restore_us"] / 1e6 / PEAK_FP32_TFLOPS, 4),
+                               "algorithmic_per_launch": restore_flops}
+    out["fix_roofline"] = {"bound": "hbm", "achieved": round(fix_bytes / out["fix_us"] / 1e3, 1),
+                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                           "frac": round(fix_bytes / out["fix_us"] / 1e3 / PEAK_HBM_GBS, 4),
+                           "algorithmic_per_launch": fix_bytes}
+    for k in ("fix_us", "power_iteration_us", "refresh_us", "restore_us", "check_ms_wall"):
+        out[k] = round(out[k], 2)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -282,6 +330,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-naive", action="store_true")
+    ap.add_argument("--no-stabilize", action="store_true",
+                    help="skip the timing of the section 5 stabilisation operations")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip the measured copy and matmul ceilings (also skipped with --copy-calib)")
     ap.add_argument("--sweep", action="store_true",
@@ -363,6 +413,12 @@ def main():
         if k in table:
             table[k]["traffic_bytes"] = v
     roof = roofline_for(table, traffic)
+    stab = None
+    if not args.no_stabilize:
+        print("[bench] stabilisation operations", file=sys.stderr, flush=True)
+        stab = stabilize_leg(f, w, dev)
+        stab["restore_roofline"]["traffic"] = traffic.get("restore")
+        stab["fix_roofline"]["traffic"] = traffic.get("fix_v")
     f.close()
     del f
 
@@ -435,6 +491,7 @@ def main():
         "kernels": table,
         "serial_inverse_us": table.get("woodbury", {}).get("avg_us"),
         "attainable": att,
+        "stabilize": stab,
     }
     print(json.dumps(out), flush=True)
 

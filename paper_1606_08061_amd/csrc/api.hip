@@ -81,8 +81,8 @@ struct lst_ctx {
   float *Pbig, *Cp, *Rp;  // blocked Woodbury inverse for m > kWoodburyOneWG
   float *dq, *lvec, *dA;
   // section 5 stabilisation: two d x d scratch matrices (row stride d), four
-  // d-vectors and eight scalars
-  float *Sd0, *Sd1, *svec, *sscal;
+  // d-vectors, the partial sums of two matrix-vector products (32 d) and eight scalars
+  float *Sd0, *Sd1, *svec, *spart, *sscal;
   int *flag;
   // progress counters ordering the two streams of a factored step: [0] contraction
   // launches started, [1] Woodbury inverses completed, [2] Z^ launches started
@@ -152,6 +152,7 @@ void carve_factored(lst_ctx *c, Carver &cv) {
   c->Sd0 = cv.take<float>((size_t)c->d * c->d);
   c->Sd1 = cv.take<float>((size_t)c->d * c->d);
   c->svec = cv.take<float>(4 * (size_t)c->d);
+  c->spart = cv.take<float>(32 * (size_t)c->d);
   c->sscal = cv.take<float>(8);
   c->flag = cv.take<int>(1);
   c->cnt = cv.take<int>(3);
@@ -1043,15 +1044,14 @@ int power_iteration(lst_ctx *c, int which, int log2_iters, const float *u0, floa
     if (record(c, launch_trace_scale(s, c->Sd0, d, c->Sd1)) ||
         record(c, square_gemm(c, c->Sd1, d, 0, c->Sd1, d, 1, c->Sd0, d)))
       return LST_E_HIP;
-  return record(c, launch_power_finish(s, c->Sd0, d, u0, A, ldd, which, u_out, sigma_out));
+  return record(c, launch_power_finish(s, c->Sd0, d, u0, A, ldd, which, u_out, sigma_out, c->spart));
 }
 
 int fix_singular_value(lst_ctx *c, const float *u, const float *sigma, float target) {
   const int d = c->d, ldd = c->ldd;
   hipStream_t s = c->stream;
   float *a = c->svec, *b = c->svec + d;
-  if (record(c, launch_tmatvec(s, c->U, ldd, d, u, a)) ||
-      record(c, launch_tmatvec(s, c->UinvT, ldd, d, u, b)) ||
+  if (record(c, launch_tmatvec2(s, c->U, c->UinvT, ldd, d, u, u, a, b, c->spart)) ||
       record(c, launch_fix_state(s, c->U, c->UinvT, ldd, d, u, a, b, sigma, target, c->flag)) ||
       record(c, launch_fix_v(s, c->V, c->ldv, c->D, d, u, sigma, target)))
     return LST_E_HIP;

@@ -251,8 +251,10 @@ hipError_t launch_grad_o(hipStream_t s, float *O, int64_t D, int m, int K, const
 // V <- V U in place (d <= 1024, else hipErrorInvalidValue).
 hipError_t launch_restore(hipStream_t s, float *V, int64_t ldv, int64_t D, const float *U, int ldd,
                           int d);
-// y = A^T x for a d x d row-major A (y must not alias x).
-hipError_t launch_tmatvec(hipStream_t s, const float *A, int lda, int d, const float *x, float *y);
+// y0 = A0^T x0 and, if A1 is not null, y1 = A1^T x1, for d x d row-major matrices
+// with row stride lda; part: 2 * 16 * d floats of partial sums.  y must not alias x.
+hipError_t launch_tmatvec2(hipStream_t s, const float *A0, const float *A1, int lda, int d,
+                           const float *x0, const float *x1, float *y0, float *y1, float *part);
 // Algorithm 5's rank-one updates of U and U^{-T} (a = U^T u, b = (U^{-T})^T u) and
 // of V, with the coefficients formed from the device scalar *sigma; a sigma that
 // is not positive and finite skips both and sets FLAG_NONFINITE.
@@ -263,10 +265,11 @@ hipError_t launch_fix_v(hipStream_t s, float *V, int64_t ldv, int64_t D, int d, 
                         const float *sigma, float target);
 // out = S / trace(S) for a d x d S (row stride d); out must not alias S.
 hipError_t launch_trace_scale(hipStream_t s, const float *S, int d, float *out);
-// u_out = S u0 / ||S u0||, *sigma_out = ||A^T u_out|| (which = 0) or its inverse.
+// u_out = S u0 / ||S u0|| (S symmetric, row stride d), *sigma_out = ||A^T u_out||
+// (which = 0) or its inverse; part: 16 * d floats.  u_out may alias u0.
 hipError_t launch_power_finish(hipStream_t s, const float *S, int d, const float *u0,
                                const float *A, int lda, int which, float *u_out,
-                               float *sigma_out);
+                               float *sigma_out, float *part);
 // Y = U / (||U||_1 ||U||_inf), the from-scratch start of the Newton-Schulz
 // iteration (*c receives the factor).
 hipError_t launch_ns_start(hipStream_t s, const float *U, int ldd, int d, float *c, float *Y,

@@ -106,27 +106,52 @@ __global__ __launch_bounds__(256) void restore_kernel(float *__restrict__ V, int
 }
 
 // ---------------------------------------------------------------------------
-// y[j] = sum_i A[i, j] x[i] (y = A^T x) for a d x d row-major A: workgroup of four
-// wavefronts per 64 columns, wave w summing the rows i = w (mod 4), lane j.
+// y = A^T x for d x d row-major matrices, spread over the chip: workgroup
+// (column block cb of 64, row slice r of kMvSlices, matrix z) sums its slice's rows
+// (wave w of four takes the rows = w mod 4, lane j = 64 cb + lane) and writes the
+// partial sums part[z][r][j]; a second kernel adds the slices in a fixed order, so
+// the result does not depend on scheduling.  Two products (z = 0, 1) share a launch.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void tmatvec_kernel(const float *__restrict__ A, int lda, int d,
-                                                      const float *__restrict__ x,
-                                                      float *__restrict__ y) {
-  __shared__ float part[4][64];
+constexpr int kMvSlices = 16;
+
+__global__ __launch_bounds__(256) void tmatvec_part_kernel(const float *__restrict__ A0,
+                                                           const float *__restrict__ A1, int lda,
+                                                           int d, const float *__restrict__ x0,
+                                                           const float *__restrict__ x1,
+                                                           float *__restrict__ part) {
+  __shared__ float red[4][64];
+  const float *A = blockIdx.z ? A1 : A0;
+  const float *x = blockIdx.z ? x1 : x0;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int j = blockIdx.x * 64 + lane;
+  const int rows = (d + kMvSlices - 1) / kMvSlices;
+  const int i0 = blockIdx.y * rows, i1 = min(d, i0 + rows);
   float s0 = 0.f, s1 = 0.f;
   if (j < d) {
-    int i = wave;
-    for (; i + 4 < d; i += 8) {
+    int i = i0 + wave;
+    for (; i + 4 < i1; i += 8) {
       s0 = fmaf(A[(int64_t)i * lda + j], x[i], s0);
       s1 = fmaf(A[(int64_t)(i + 4) * lda + j], x[i + 4], s1);
     }
-    if (i < d) s0 = fmaf(A[(int64_t)i * lda + j], x[i], s0);
+    if (i < i1) s0 = fmaf(A[(int64_t)i * lda + j], x[i], s0);
   }
-  part[wave][lane] = s0 + s1;
+  red[wave][lane] = s0 + s1;
   __syncthreads();
-  if (wave == 0 && j < d) y[j] = (part[0][lane] + part[1][lane]) + (part[2][lane] + part[3][lane]);
+  if (wave == 0 && j < d)
+    part[((int64_t)blockIdx.z * kMvSlices + blockIdx.y) * d + j] =
+        (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+}
+
+// y_z[j] = sum over the slices of part[z][r][j], in slice order.
+__global__ __launch_bounds__(256) void tmatvec_sum_kernel(const float *__restrict__ part, int d,
+                                                          float *__restrict__ y0,
+                                                          float *__restrict__ y1) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= d) return;
+  const float *p = part + (int64_t)blockIdx.y * kMvSlices * d;
+  float s = 0.f;
+  for (int r = 0; r < kMvSlices; ++r) s += p[(int64_t)r * d + j];
+  (blockIdx.y ? y1 : y0)[j] = s;
 }
 
 // Sum over the workgroup (1024 threads) of v; every thread gets the result.
@@ -238,46 +263,29 @@ __global__ __launch_bounds__(256) void trace_scale_kernel(const float *__restric
     out[e] = S[e] * inv;
 }
 
-// One workgroup of 1024: v = S u0 (S symmetric, read by columns), u = v / ||v||,
-// w = A^T u, sigma = ||w|| (which = 0) or 1 / ||w|| (which = 1).
-__global__ __launch_bounds__(1024) void power_finish_kernel(const float *__restrict__ S, int d,
-                                                            const float *__restrict__ u0,
-                                                            const float *__restrict__ A, int lda,
-                                                            int which, float *__restrict__ u_out,
-                                                            float *__restrict__ sigma_out) {
-  extern __shared__ float su[];  // d floats
+// One workgroup of 1024 adding the slices of an A^T x product (tmatvec_part_kernel),
+// then: mode 0 -- u = y / ||y|| into u_out; mode 1 -- *sigma_out = ||y|| (which = 0)
+// or 1 / ||y|| (which = 1).
+__global__ __launch_bounds__(1024) void power_norm_kernel(const float *__restrict__ part, int d,
+                                                          int mode, int which,
+                                                          float *__restrict__ u_out,
+                                                          float *__restrict__ sigma_out) {
+  extern __shared__ float sy[];  // d floats
   __shared__ float red[16];
   float sq = 0.f;
   for (int j = threadIdx.x; j < d; j += 1024) {
-    float s0 = 0.f, s1 = 0.f;
-    int i = 0;
-    for (; i + 1 < d; i += 2) {
-      s0 = fmaf(S[(int64_t)i * d + j], u0[i], s0);
-      s1 = fmaf(S[(int64_t)(i + 1) * d + j], u0[i + 1], s1);
-    }
-    if (i < d) s0 = fmaf(S[(int64_t)i * d + j], u0[i], s0);
-    su[j] = s0 + s1;
-    sq = fmaf(s0 + s1, s0 + s1, sq);
+    float s = 0.f;
+    for (int r = 0; r < kMvSlices; ++r) s += part[(int64_t)r * d + j];
+    sy[j] = s;
+    sq = fmaf(s, s, sq);
   }
-  const float inv = 1.f / sqrtf(block_sum_1024(sq, red));
-  for (int j = threadIdx.x; j < d; j += 1024) {
-    su[j] *= inv;
-    u_out[j] = su[j];
+  const float n = sqrtf(block_sum_1024(sq, red));
+  if (mode == 0) {
+    const float inv = 1.f / n;
+    for (int j = threadIdx.x; j < d; j += 1024) u_out[j] = sy[j] * inv;
+  } else if (threadIdx.x == 0) {
+    *sigma_out = which ? 1.f / n : n;
   }
-  __syncthreads();
-  sq = 0.f;
-  for (int j = threadIdx.x; j < d; j += 1024) {
-    float s0 = 0.f, s1 = 0.f;
-    int i = 0;
-    for (; i + 1 < d; i += 2) {
-      s0 = fmaf(A[(int64_t)i * lda + j], su[i], s0);
-      s1 = fmaf(A[(int64_t)(i + 1) * lda + j], su[i + 1], s1);
-    }
-    if (i < d) s0 = fmaf(A[(int64_t)i * lda + j], su[i], s0);
-    sq = fmaf(s0 + s1, s0 + s1, sq);
-  }
-  const float nw = sqrtf(block_sum_1024(sq, red));
-  if (threadIdx.x == 0) *sigma_out = which ? 1.f / nw : nw;
 }
 
 // ---------------------------------------------------------------------------
@@ -367,9 +375,11 @@ __global__ __launch_bounds__(256) void scaled_copy_kernel(const float *__restric
 }
 
 // *amax = max_ij |E_ij| (non-negative floats compare as their bit patterns, NaN counting
-// as infinite; *amax starts at 0).
+// as infinite; *amax starts at 0).  One atomic per workgroup.
+constexpr int kAbsmaxBlocks = 64;
 __global__ __launch_bounds__(256) void absmax_kernel(const float *__restrict__ E, int d,
                                                      float *__restrict__ amax) {
+  __shared__ float red[4];
   float m = 0.f;
   const int64_t n = (int64_t)d * d;
   for (int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x; e < n; e += (int64_t)gridDim.x * 256) {
@@ -377,7 +387,11 @@ __global__ __launch_bounds__(256) void absmax_kernel(const float *__restrict__ E
     m = fmaxf(m, a == a ? a : INFINITY);
   }
   for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
-  if ((threadIdx.x & 63) == 0) atomicMax(reinterpret_cast<int *>(amax), __float_as_int(m));
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0)
+    atomicMax(reinterpret_cast<int *>(amax),
+              __float_as_int(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]))));
 }
 
 int elementwise_blocks(int d) {
@@ -402,8 +416,12 @@ hipError_t launch_restore(hipStream_t s, float *V, int64_t ldv, int64_t D, const
   return hipGetLastError();
 }
 
-hipError_t launch_tmatvec(hipStream_t s, const float *A, int lda, int d, const float *x, float *y) {
-  LST_LAUNCH(tmatvec_kernel, dim3((d + 63) / 64), dim3(256), 0, s, A, lda, d, x, y);
+hipError_t launch_tmatvec2(hipStream_t s, const float *A0, const float *A1, int lda, int d,
+                           const float *x0, const float *x1, float *y0, float *y1, float *part) {
+  const int nz = A1 ? 2 : 1;
+  LST_LAUNCH(tmatvec_part_kernel, dim3((d + 63) / 64, kMvSlices, nz), dim3(256), 0, s, A0, A1, lda,
+             d, x0, x1, part);
+  LST_LAUNCH(tmatvec_sum_kernel, dim3((d + 255) / 256, nz), dim3(256), 0, s, part, d, y0, y1);
   return hipGetLastError();
 }
 
@@ -438,9 +456,15 @@ hipError_t launch_trace_scale(hipStream_t s, const float *S, int d, float *out) 
 
 hipError_t launch_power_finish(hipStream_t s, const float *S, int d, const float *u0,
                                const float *A, int lda, int which, float *u_out,
-                               float *sigma_out) {
-  LST_LAUNCH(power_finish_kernel, dim3(1), dim3(1024), (size_t)d * sizeof(float), s, S, d, u0, A,
-             lda, which, u_out, sigma_out);
+                               float *sigma_out, float *part) {
+  const dim3 grid((d + 63) / 64, kMvSlices, 1);
+  const size_t lds = (size_t)d * sizeof(float);
+  // u = S u0 / ||S u0|| (S symmetric: S u0 = S^T u0)
+  LST_LAUNCH(tmatvec_part_kernel, grid, dim3(256), 0, s, S, S, d, d, u0, u0, part);
+  LST_LAUNCH(power_norm_kernel, dim3(1), dim3(1024), lds, s, part, d, 0, which, u_out, sigma_out);
+  // sigma from ||A^T u||
+  LST_LAUNCH(tmatvec_part_kernel, grid, dim3(256), 0, s, A, A, lda, d, u_out, u_out, part);
+  LST_LAUNCH(power_norm_kernel, dim3(1), dim3(1024), lds, s, part, d, 1, which, u_out, sigma_out);
   return hipGetLastError();
 }
 
@@ -460,7 +484,8 @@ hipError_t launch_residual64(hipStream_t s, const float *Y, int ldy, const float
 }
 
 hipError_t launch_absmax(hipStream_t s, const float *E, int d, float *amax) {
-  LST_LAUNCH(absmax_kernel, dim3(elementwise_blocks(d)), dim3(256), 0, s, E, d, amax);
+  LST_LAUNCH(absmax_kernel, dim3(std::min(elementwise_blocks(d), kAbsmaxBlocks)), dim3(256), 0, s, E,
+             d, amax);
   return hipGetLastError();
 }
 

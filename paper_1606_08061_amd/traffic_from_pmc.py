@@ -4,7 +4,9 @@
 
 FETCH.csv and WRITE.csv are the counter_collection files of
 `rocprofv3 --pmc FETCH_SIZE` and `rocprofv3 --pmc WRITE_SIZE` over
-`bench.py --no-cpu --no-naive --copy-calib 256`.  Both counters read KiB per
+`bench.py --no-cpu --no-naive --copy-calib 256` (the step's kernels and, from the
+bench's stabilisation leg, the pristine restore and the fix-singular-value pass
+over V).  Both counters read KiB per
 dispatch; the bench's plain device copy of a known size (the largest
 __amd_rocclr_copyBuffer dispatch) gives the factor that turns each counter into
 bytes.  Writes traffic.json next to this file: per phase, the kernel, the source
@@ -39,6 +41,8 @@ KERNELS = [
     ("woodbury_blocked_kernel", "woodbury", "step_kernels.hip+woodbury_gj.h"),
     ("scatter_kernel", "scatter", "step_kernels.hip+scatter.h"),
     ("update_scatter_kernel", "update", "gemm.hip+scatter.h"),
+    ("restore_kernel", "restore", "stabilize.hip"),
+    ("fix_v_kernel", "fix_v", "stabilize.hip"),
 ]
 
 
