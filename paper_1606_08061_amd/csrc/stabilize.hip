@@ -218,24 +218,36 @@ __global__ __launch_bounds__(256) void fix_v_kernel(float *__restrict__ V, int64
     const int k = lane + 64 * p;
     uu[p] = k < d ? u[k] : 0.f;
   }
+  // two rows per wave per iteration (r and r + waves), so that 2 NPL loads are in flight
   const int64_t waves = (int64_t)gridDim.x * 4;
-  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < D; r += waves) {
-    float *row = V + r * ldv;
-    float v[NPL];
-    float s = 0.f;
+  for (int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); r < D; r += 2 * waves) {
+    const bool two = r + waves < D;
+    float *row0 = V + r * ldv, *row1 = V + (two ? r + waves : r) * ldv;
+    float v0[NPL], v1[NPL];
 #pragma unroll
     for (int p = 0; p < NPL; ++p) {
       const int k = lane + 64 * p;
-      v[p] = k < d ? row[k] : 0.f;
+      v0[p] = k < d ? row0[k] : 0.f;
+      v1[p] = (two && k < d) ? row1[k] : 0.f;
     }
+    float s0 = 0.f, s1 = 0.f;
 #pragma unroll
-    for (int p = 0; p < NPL; ++p) s = fmaf(v[p], uu[p], s);
-    for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
-    const float bs = beta * s;
+    for (int p = 0; p < NPL; ++p) {
+      s0 = fmaf(v0[p], uu[p], s0);
+      s1 = fmaf(v1[p], uu[p], s1);
+    }
+    for (int o = 32; o > 0; o >>= 1) {
+      s0 += __shfl_xor(s0, o);
+      s1 += __shfl_xor(s1, o);
+    }
+    const float b0 = beta * s0, b1 = beta * s1;
 #pragma unroll
     for (int p = 0; p < NPL; ++p) {
       const int k = lane + 64 * p;
-      if (k < d) row[k] = fmaf(bs, uu[p], v[p]);
+      if (k < d) {
+        row0[k] = fmaf(b0, uu[p], v0[p]);
+        if (two) row1[k] = fmaf(b1, uu[p], v1[p]);
+      }
     }
   }
 }
