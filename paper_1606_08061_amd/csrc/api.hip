@@ -724,9 +724,10 @@ int enqueue_main_a(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *
   return record(c, hipGetLastError()) ? LST_E_HIP : LST_OK;
 }
 
-// Side stream: N = H^T H, then C = I - 2 eta S N S and R = 2 eta S C^{-1} S.
-// For squared error dl/dq = 1; the spherical softmax waits for the gather's
-// dl/dq = T / (q + D eps).
+// Side stream: N = H^T H, then C = I - 2 eta S N S and R = 2 eta S C^{-1} S (for
+// m > d, through the d x d inverse of I - 2 eta (SH)^T (SH): the m >= d variant the
+// paper suggests after Algorithm 3, here as the same Woodbury R).  For squared error
+// dl/dq = 1; the spherical softmax waits for the gather's dl/dq = T / (q + D eps).
 int enqueue_side(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *H, int32_t m,
                  float lr, float *gH) {
   const bool unit_dq = (c->loss == LST_LOSS_SQUARED);
@@ -747,8 +748,37 @@ int enqueue_side(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *H,
     gathered.flag = c->flag;
   }
   prof(c, LST_PHASE_WOODBURY, true);
-  launch_woodbury(s, m, lr, unit_dq ? 1 : 0, c->dq, c->N, c->R, c->Cwork, c->Pbig, c->Cp, c->Rp,
-                  c->flag, gathered, c->withhold_release ? nullptr : c->cnt + 1);
+  int *done = c->withhold_release ? nullptr : c->cnt + 1;
+  const int d = c->d;
+  if (m > kWoodburyOneWG && d < m) {
+    // m > d: the d x d inverse of B = I - 2 eta Hs^T Hs instead of the m x m one (see
+    // push_through_r_kernel): R' = 2 eta B^{-1} into Sd0, then R = 2 eta S (I + Hs R' Hs^T) S.
+    const float *Hs = H;
+    if (!unit_dq) {
+      launch_step_sync(s, gathered, nullptr);
+      launch_scale_rows_sqrt(s, m, d, H, c->dq, c->P, c->flag);
+      Hs = c->P;
+    }
+    GemmBatch b{};
+    b.d[0] = gemm_desc(d, d, m, Hs, d, 1, Hs, d, 1, c->Sd1, d);  // Hs^T Hs
+    b.n = 1;
+    gemm_run(b, nullptr, s);
+    launch_woodbury(s, d, lr, 1, c->dq, c->Sd1, c->Sd0, c->Cwork, c->Pbig, c->Cp, c->Rp, c->flag,
+                    StepSync{}, nullptr);
+    b = GemmBatch{};
+    b.d[0] = gemm_desc(m, d, d, Hs, d, 0, c->Sd0, d, 1, c->Zq, d);  // T = Hs R'
+    b.n = 1;
+    gemm_run(b, nullptr, s);
+    b = GemmBatch{};
+    b.d[0] = gemm_desc(m, m, d, c->Zq, d, 0, Hs, d, 0, c->R, m);  // R0 = T Hs^T
+    b.n = 1;
+    gemm_run(b, nullptr, s);
+    launch_push_through_r(s, m, lr, unit_dq ? 1 : 0, c->dq, c->R);
+    if (done) launch_step_sync(s, StepSync{}, done);
+  } else {
+    launch_woodbury(s, m, lr, unit_dq ? 1 : 0, c->dq, c->N, c->R, c->Cwork, c->Pbig, c->Cp, c->Rp,
+                    c->flag, gathered, done);
+  }
   prof(c, LST_PHASE_WOODBURY, false);
   return record(c, hipGetLastError()) ? LST_E_HIP : LST_OK;
 }

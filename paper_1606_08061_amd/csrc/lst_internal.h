@@ -218,6 +218,13 @@ hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const fl
                            const float *N, float *R, float *Cwork, float *Pbig, float *Cp,
                            float *Rp, int *flag, const StepSync &wait, int *done);
 
+// The m > d form of the branch (push-through identity): Hs = diag(dq)^(1/2) H (m x d,
+// flagging dq < 0), and R = 2 eta S (R0 + I) S in place over R0 = Hs R' Hs^T (m x m).
+hipError_t launch_scale_rows_sqrt(hipStream_t s, int m, int d, const float *H, const float *dq,
+                                  float *Hs, int *flag);
+hipError_t launch_push_through_r(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
+                                 float *R);
+
 // One workgroup: waits as `wait` says, then releases *done (if not null).
 hipError_t launch_step_sync(hipStream_t s, const StepSync &wait, int *done);
 

@@ -373,6 +373,38 @@ __global__ void scale_r_kernel(int m, int lb0, float lr, int unit_dq, const floa
   }
 }
 
+// For m > d the branch inverts the d x d matrix B = I - 2 eta Hs^T Hs instead of the
+// m x m C = I - 2 eta Hs Hs^T (Hs = S H, rows of H scaled by (dl/dq)^(1/2)): by the
+// push-through identity C^{-1} = I + Hs R' Hs^T with R' = 2 eta B^{-1}, so
+// R = 2 eta S C^{-1} S = 2 eta S (I + Hs R' Hs^T) S.  B and C share their nonzero
+// eigenvalues, so B's pivots answer the same positive-definiteness question.
+// Hs = S H; dl/dq < 0 has no real square root: flagged as not positive definite.
+__global__ void scale_rows_sqrt_kernel(int m, int d, const float *__restrict__ H,
+                                       const float *__restrict__ dq, float *__restrict__ Hs,
+                                       int *__restrict__ flag) {
+  const int64_t total = (int64_t)m * d;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int i = (int)(e / d);
+    const float q = dq[i];
+    if (e - (int64_t)i * d == 0 && !(q >= 0.f)) atomicOr(flag, FLAG_NOT_SPD);
+    Hs[e] = sqrtf(fmaxf(q, 0.f)) * H[e];
+  }
+}
+
+// R = 2 eta S (R0 + I) S in place, R0 = Hs R' Hs^T.
+__global__ void push_through_r_kernel(int m, float lr, int unit_dq, const float *__restrict__ dq,
+                                      float *__restrict__ R) {
+  const int64_t total = (int64_t)m * m;
+  for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int i = (int)(e / m), j = (int)(e - (int64_t)i * m);
+    const float si = unit_dq ? 1.f : sqrtf(fmaxf(dq[i], 0.f));
+    const float sj = unit_dq ? 1.f : sqrtf(fmaxf(dq[j], 0.f));
+    R[e] = 2.f * lr * si * (R[e] + (i == j ? 1.f : 0.f)) * sj;
+  }
+}
+
 // Pivot block b0 .. b0+nb-1 (nb <= kBigBlock) of A: P and PI = P + I
 // (kBigBlock^2 each, identity-padded).  First removes the I left on the
 // previous diagonal block (rows pb0 .. pb0+pnb-1; pnb = 0 for none).
@@ -854,6 +886,20 @@ hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const fl
       if (done) LST_LAUNCH(step_sync_kernel, dim3(1), dim3(64), 0, s, StepSync{}, done);
     }
   }
+  return hipSuccess;  // checked once per step by the caller
+}
+
+hipError_t launch_scale_rows_sqrt(hipStream_t s, int m, int d, const float *H, const float *dq,
+                                  float *Hs, int *flag) {
+  const int blocks = (int)std::min<int64_t>(((int64_t)m * d + 255) / 256, 2048);
+  LST_LAUNCH(scale_rows_sqrt_kernel, dim3(blocks), dim3(256), 0, s, m, d, H, dq, Hs, flag);
+  return hipSuccess;  // checked once per step by the caller
+}
+
+hipError_t launch_push_through_r(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
+                                 float *R) {
+  const int blocks = (int)std::min<int64_t>(((int64_t)m * m + 255) / 256, 2048);
+  LST_LAUNCH(push_through_r_kernel, dim3(blocks), dim3(256), 0, s, m, lr, unit_dq, dq, R);
   return hipSuccess;  // checked once per step by the caller
 }
 

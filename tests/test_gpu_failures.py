@@ -68,14 +68,16 @@ def test_nonfinite_H():
     f.close()
 
 
-@pytest.mark.parametrize("m,bad", [(1, 0), (70, 40), (200, 150), (300, 290)])
-def test_not_positive_definite(m, bad):
+@pytest.mark.parametrize("m,bad,d", [(1, 0, 16), (70, 40, 16), (200, 150, 16), (300, 290, 16),
+                                     (200, 150, 256), (300, 290, 320)])
+def test_not_positive_definite(m, bad, d):
     # Example `bad` gets ||h||^2 = 1/eta, so C = I - 2 eta H H^T has C_bad,bad = -1
     # and a negative eigenvalue (for m = 1 this is the Sherman-Morrison denominator
-    # 1 - 2 eta ||h||^2 = -1).  Elimination meets the first non-positive pivot at
-    # or before row `bad`, inside a later diagonal block for m > 32.  The fp64
-    # mirror confirms C is indefinite.
-    w = Workload("t", LOSS_SQUARED, 400, 16, m, 1, lr=0.05)
+    # 1 - 2 eta ||h||^2 = -1).  With d >= m, elimination of C meets the first
+    # non-positive pivot at or before row `bad`, inside a later diagonal block for
+    # m > 32; with m > 128 and d < m the branch eliminates the d x d I - 2 eta H^T H,
+    # which shares C's negative eigenvalue.  The fp64 mirror confirms C is indefinite.
+    w = Workload("t", LOSS_SQUARED, 400, d, m, 1, lr=0.05)
     s = Stream(w)
     H, idx, val = s.batch()
     H = (H * 0.05).astype(np.float32)

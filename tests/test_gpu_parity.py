@@ -53,6 +53,9 @@ def test_small_config_100_steps():
 @pytest.mark.parametrize("D,d,m,K", [
     (50, 1, 1, 1), (300, 31, 2, 3), (1000, 33, 17, 2), (777, 65, 33, 1), (2000, 40, 70, 3),
     (1500, 47, 130, 2), (3000, 24, 300, 1), (2500, 20, 520, 1), (400, 64, 5, 0),
+    # m > 128 with d >= m: the m x m blocked inverse (the cases above with d < m take the d x d
+    # push-through form); d = 200 < m = 260: the push-through form with a blocked d x d inverse
+    (2000, 160, 150, 2), (1200, 300, 260, 1), (1800, 200, 260, 2),
 ])
 def test_awkward_shapes(loss, D, d, m, K):
     w = Workload("t", loss, D, d, m, K, index_dist="uniform",
