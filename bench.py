@@ -319,6 +319,60 @@ def stabilize_leg(f, w, dev, reps=5):
     return out
 
 
+def online_leg(w, dev, V0, gpool, steps=2000, general_steps=300):
+    """The online step (m = 1, squared error, Algorithm 2) on the benchmark's V: the first
+    example of each pooled minibatch, through the single cooperative launch and through the
+    general step path (LST_ONLINE_KERNEL=0).  Algorithmic bytes per step: Q, U, U^{-T} read
+    and written once (6 d^2 floats; the K target rows of V add 8 K d)."""
+    import torch
+
+    import paper_1606_08061_amd as lst
+
+    ex = [[t[:1].contiguous() for t in b] for b in gpool]
+    grad = torch.empty((1, w.d), dtype=torch.float32, device=dev)
+    out = {}
+    for name, n, env in (("fused", steps, None), ("general", general_steps, "0")):
+        if env is not None:
+            os.environ["LST_ONLINE_KERNEL"] = env
+        f = lst.Factored(w.D, w.d, 1, w.K, "squared", device=dev)
+        os.environ.pop("LST_ONLINE_KERNEL", None)
+        f.init(V0)
+        for t in range(64):
+            f.step(*ex[t % len(ex)], w.lr, grad_H=grad)
+        f.check("online warm-up")
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for t in range(n):
+            f.step(*ex[t % len(ex)], w.lr, grad_H=grad)
+        e1.record()
+        torch.cuda.synchronize()
+        f.check("online steps")
+        us = e0.elapsed_time(e1) / n * 1e3
+        h0 = time.perf_counter()
+        for t in range(n):
+            f.step(*ex[t % len(ex)], w.lr, grad_H=grad)
+        host_us = (time.perf_counter() - h0) / n * 1e6
+        torch.cuda.synchronize()
+        # GPU time of the step's kernels (launch-attached HIP events per phase)
+        f.profile(True)
+        for t in range(n):
+            f.step(*ex[t % len(ex)], w.lr, grad_H=grad)
+        ph = f.profile_read()
+        f.profile(False)
+        kern_us = sum(v[1] for v in ph.values()) / n * 1e3
+        out[name] = {"us_per_example": round(us, 2), "examples_per_s": round(1e6 / us, 1),
+                     "host_enqueue_us": round(host_us, 2), "kernel_us": round(kern_us, 2)}
+        f.close()
+    byt = 6.0 * w.d * w.d * 4 + 8.0 * w.K * w.d
+    us = out["fused"]["us_per_example"]
+    out["roofline"] = {"bound": "hbm", "achieved": round(byt / us / 1e3, 1), "peak": PEAK_HBM_GBS,
+                       "unit": "GB/s", "frac": round(byt / us / 1e3 / PEAK_HBM_GBS, 4),
+                       "algorithmic_per_launch": byt}
+    out["speedup_fused_vs_general"] = round(out["general"]["us_per_example"] / us, 2)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -330,6 +384,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-naive", action="store_true")
+    ap.add_argument("--no-online", action="store_true",
+                    help="skip the timing of the one-example (m = 1) online step")
     ap.add_argument("--no-stabilize", action="store_true",
                     help="skip the timing of the section 5 stabilisation operations")
     ap.add_argument("--no-peaks", action="store_true",
@@ -432,6 +488,11 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    online = None
+    if not args.no_online and w.loss == "squared":
+        print("[bench] online (m = 1) steps", file=sys.stderr, flush=True)
+        online = online_leg(w, dev, V0, gpool)
+
     # ---- naive O(D d) path on the same batches ----
     naive = None
     if not args.no_naive:
@@ -492,6 +553,7 @@ def main():
         "serial_inverse_us": table.get("woodbury", {}).get("avg_us"),
         "attainable": att,
         "stabilize": stab,
+        "online": online,
     }
     print(json.dumps(out), flush=True)
 

@@ -139,6 +139,12 @@ int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0
  * the new W^T W (eq. updateQ / gen-Qnew) and U^{-T} the new inverse transpose.
  * Returns once the work is enqueued; device-side errors surface at the next
  * lst_sync_status.
+ * With m = 1 and squared error (the online case, Algorithm 2) the step runs as
+ * one cooperative launch of 64 workgroups (its products read the old Q, U, U^{-T},
+ * one grid-wide barrier, then the rank-one updates), unless graphs are on, the
+ * device lacks cooperative launches, or the environment variable
+ * LST_ONLINE_KERNEL=0 was set when the context was created; same results to
+ * fp32 rounding.
  */
 int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val,
              int32_t K, float lr, float *loss_dev, float *grad_H);
@@ -277,7 +283,8 @@ enum lst_phase {
   LST_PHASE_NAIVE_GRAD = 10,   /* naive: grad_H = grad_O^T W                               */
   LST_PHASE_NAIVE_UPDATE = 11, /* naive: W <- W - eta grad_O H                             */
   LST_PHASE_GRAM = 12,         /* N = H^T H, the Gram matrix of the minibatch (matrix cores) */
-  LST_NUM_PHASES = 13
+  LST_PHASE_ONLINE = 13,       /* m = 1, squared error: the whole step in one launch       */
+  LST_NUM_PHASES = 14
 };
 
 /*

@@ -59,7 +59,7 @@ SIGNATURES = {
 }
 
 PHASES = ["contract", "gather", "zgrad", "mblock", "woodbury", "mid", "update", "scatter",
-          "naive_fwd", "naive_loss", "naive_grad", "naive_update", "gram"]
+          "naive_fwd", "naive_loss", "naive_grad", "naive_update", "gram", "online"]
 
 _lib = None
 _lock = threading.Lock()

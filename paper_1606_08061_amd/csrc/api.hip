@@ -1,5 +1,6 @@
 // C ABI of liblst: argument validation, workspace carving and the enqueue order
 // of the factored step (Algorithm 3 / Algorithm 4) and of the naive step.
+#include <algorithm>
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
@@ -85,7 +86,8 @@ struct lst_ctx {
   float *Sd0, *Sd1, *svec, *spart, *sscal;
   int *flag;
   // progress counters ordering the two streams of a factored step: [0] contraction
-  // launches started, [1] Woodbury inverses completed, [2] Z^ launches started
+  // launches started, [1] Woodbury inverses completed, [2] Z^ launches started; [3]
+  // the grid barrier of the online step's single launch
   int *cnt;
   float *O, *colpart, *splitpart;
   hipError_t last_err;
@@ -115,6 +117,8 @@ struct lst_ctx {
   // such as hardware counter collection, under which a wait on another stream's
   // progress could not be met.
   bool one_stream;
+  // m = 1 squared-error steps as one cooperative launch (see lst_step)
+  bool online;
   std::vector<GraphEntry> graphs;
   uint64_t graph_tick;
 };
@@ -152,10 +156,10 @@ void carve_factored(lst_ctx *c, Carver &cv) {
   c->Sd0 = cv.take<float>((size_t)c->d * c->d);
   c->Sd1 = cv.take<float>((size_t)c->d * c->d);
   c->svec = cv.take<float>(4 * (size_t)c->d);
-  c->spart = cv.take<float>(32 * (size_t)c->d);
+  c->spart = cv.take<float>(std::max<size_t>(32 * (size_t)c->d, online_work_floats(c->d)));
   c->sscal = cv.take<float>(8);
   c->flag = cv.take<int>(1);
-  c->cnt = cv.take<int>(3);
+  c->cnt = cv.take<int>(4);
   c->plan_pool = cv.take<GemmBatch>(kPlanCap * kPlanBatches);
 }
 
@@ -382,6 +386,15 @@ int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max
   c->use_graphs = false;
   c->withhold_release = std::getenv("LST_TEST_WITHHOLD_WOODBURY_RELEASE") != nullptr;
   c->one_stream = std::getenv("LST_ONE_STREAM") != nullptr;
+  {
+    int dev = 0, coop = 0;
+    const char *ok = std::getenv("LST_ONLINE_KERNEL");
+    c->online = loss == LST_LOSS_SQUARED && !(ok && std::strcmp(ok, "0") == 0) &&
+                hipGetDevice(&dev) == hipSuccess &&
+                hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) ==
+                    hipSuccess &&
+                coop != 0;
+  }
   st = alloc_ws(c, carve_factored);
   if (st == LST_OK) st = side_create(c);
   if (st != LST_OK) {
@@ -483,7 +496,7 @@ int lst_sync_status(lst_ctx *c) {
   if (f & FLAG_NOT_SPD) return LST_E_NOT_SPD;
   if (f & FLAG_SYNC) {
     // Both streams are idle: restart the progress counters from a consistent state.
-    if (c->cnt && hipMemset(c->cnt, 0, 3 * sizeof(int)) != hipSuccess) return LST_E_HIP;
+    if (c->cnt && hipMemset(c->cnt, 0, 4 * sizeof(int)) != hipSuccess) return LST_E_HIP;
     return LST_E_SYNC;
   }
   return LST_OK;
@@ -899,10 +912,20 @@ int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const fl
   int st = step_args(c, H, m, idx, val, K, lr, loss_dev);
   if (st != LST_OK) return st;
   if (m == 0) return record(c, launch_fill(c->stream, loss_dev, 0.f));
+  const bool graphs = c->use_graphs && !c->prof_on;
+  if (m == 1 && c->online && !graphs) {
+    // the online step of Algorithm 2 in one launch (its work vectors share the section 5
+    // scratch, which is only used between steps on this stream)
+    prof(c, LST_PHASE_ONLINE, true);
+    const hipError_t e = launch_online_step(
+        c->stream, c->D, c->d, K, H, idx, val, lr, c->V, c->ldv, c->U, c->UinvT, c->Q, c->ldd,
+        loss_dev, grad_H, c->spart, reinterpret_cast<unsigned *>(c->cnt + 3), c->flag);
+    prof(c, LST_PHASE_ONLINE, false);
+    return record(c, e);
+  }
   const PlanEntry *pl = get_plan(c, m);
   if (!pl) return LST_E_HIP;
-  if (c->use_graphs && !c->prof_on)
-    return graph_step(c, *pl, H, m, idx, val, K, lr, loss_dev, grad_H);
+  if (graphs) return graph_step(c, *pl, H, m, idx, val, K, lr, loss_dev, grad_H);
   return enqueue_factored_step(c, *pl, H, m, idx, val, K, lr, loss_dev, grad_H);
 }
 

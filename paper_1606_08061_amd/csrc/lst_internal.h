@@ -253,6 +253,17 @@ hipError_t launch_grad_o(hipStream_t s, float *O, int64_t D, int m, int K, const
                          int *flag);
 
 // ---------------------------------------------------------------------------
+// The online step (m = 1, squared error; Algorithm 2) as one cooperative launch
+// (online.hip).  work: online_work_floats(d) floats; bar: a grid-barrier counter
+// that starts at 0 and is reset together with the step's progress counters.
+// ---------------------------------------------------------------------------
+size_t online_work_floats(int d);
+hipError_t launch_online_step(hipStream_t s, int64_t D, int d, int K, const float *h,
+                              const int *idx, const float *val, float lr, float *V, int64_t ldv,
+                              float *U, float *UinvT, float *Q, int ldd, float *loss_out,
+                              float *grad_h, float *work, unsigned *bar, int *flag);
+
+// ---------------------------------------------------------------------------
 // Numerical stabilisation kernels (stabilize.hip), enqueued between steps.
 // ---------------------------------------------------------------------------
 // V <- V U in place (d <= 1024, else hipErrorInvalidValue).
