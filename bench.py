@@ -373,6 +373,47 @@ def online_leg(w, dev, V0, gpool, steps=2000, general_steps=300):
     return out
 
 
+def input_layer_leg(w, dev, D_in=200_000, K_in=4, reps=200):
+    """The sparse input layer of section 2.2 at the benchmark's d and m: K_in-sparse inputs
+    over D_in rows (Zipf, seeded), forward A = X W1 and update W1 -= eta X^T grad_A, each
+    timed with HIP events over reps calls.  Bytes: forward m K_in d 4 read + m d 4 written;
+    update: the distinct named rows read and written, grad_A read."""
+    import torch
+
+    import paper_1606_08061_amd as lst
+
+    rng = np.random.default_rng(23)
+    W1 = torch.from_numpy((rng.standard_normal((D_in, w.d)) / np.sqrt(w.d * K_in))
+                          .astype(np.float32)).to(dev)
+    p = 1.0 / np.arange(1, D_in + 1) ** 1.1
+    idx = rng.choice(D_in, size=(w.m, K_in), p=p / p.sum()).astype(np.int32)
+    val = rng.standard_normal((w.m, K_in)).astype(np.float32)
+    gA = torch.from_numpy(rng.standard_normal((w.m, w.d)).astype(np.float32) * 1e-3).to(dev)
+    idx_d, val_d = torch.from_numpy(idx).to(dev), torch.from_numpy(val).to(dev)
+    layer = lst.SparseInput(W1)
+    A = torch.empty((w.m, w.d), dtype=torch.float32, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    out = {"D_in": D_in, "K_in": K_in}
+    for name, fn in (("forward", lambda: layer.forward(idx_d, val_d, out=A)),
+                     ("update", lambda: layer.update(idx_d, val_d, gA, 1e-3))):
+        fn()
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        out[name + "_us"] = round(e0.elapsed_time(e1) / reps * 1e3, 2)
+    layer.check()
+    u = len(np.unique(idx))
+    fb = 4.0 * w.m * w.d * (K_in + 1)
+    ub = 4.0 * (2 * u * w.d + w.m * w.d)
+    out["forward_GBs"] = round(fb / out["forward_us"] / 1e3, 1)
+    out["update_GBs"] = round(ub / out["update_us"] / 1e3, 1)
+    out["distinct_rows"] = u
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -488,6 +529,10 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
+    inp = None
+    if not args.no_online:
+        print("[bench] sparse input layer", file=sys.stderr, flush=True)
+        inp = input_layer_leg(w, dev)
     online = None
     if not args.no_online and w.loss == "squared":
         print("[bench] online (m = 1) steps", file=sys.stderr, flush=True)
@@ -554,6 +599,7 @@ def main():
         "attainable": att,
         "stabilize": stab,
         "online": online,
+        "input_layer": inp,
     }
     print(json.dumps(out), flush=True)
 

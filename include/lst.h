@@ -169,6 +169,31 @@ int lst_use_graphs(lst_ctx *c, int32_t on);
 int lst_materialize_W(lst_ctx *c, float *W, int64_t ldw);
 
 /*
+ * The sparse input layer (section 2.2), no context needed.  A minibatch of m inputs,
+ * each K-sparse: idx, val are m x K device arrays (index -1 = empty slot; repeated
+ * indices add their values), W1 is D_in x ldw (device, row-major), status_dev one
+ * device int32 that the caller sets to 0 and the calls OR with LST_E_INDEX's device
+ * bit (1) when an index lies outside [-1, D_in).  Both are enqueued on stream.
+ *
+ * lst_input_forward -- A = X W1: row j of A (m x d, row stride d) is
+ * sum_k val[j,k] W1[idx[j,k]], an O(K d) gather per example; an invalid slot adds
+ * nothing.
+ */
+int lst_input_forward(const float *W1, int64_t ldw, int64_t D_in, int32_t d, const int32_t *idx,
+                      const float *val, int32_t m, int32_t K, float *A, int32_t *status_dev,
+                      void *stream);
+
+/*
+ * lst_input_update -- W1 <- W1 - lr X^T grad_A (grad_A m x d, row stride d): only the
+ * rows the inputs name change, each by one writer that sums its slots in slot order
+ * (bit-reproducible).  Writes nothing if *status_dev is non-zero after the index
+ * check (an invalid index in this call, or an error left in it by an earlier call).
+ */
+int lst_input_update(float *W1, int64_t ldw, int64_t D_in, int32_t d, const int32_t *idx,
+                     const float *val, int32_t m, int32_t K, const float *grad_A, float lr,
+                     int32_t *status_dev, void *stream);
+
+/*
  * Numerical stabilisation (section 5), on a factored context, between steps.
  * Each call is enqueued on the context's stream after the steps before it
  * (lst_singular_stabilize synchronises it); none changes W = V U or Q = W^T W

@@ -50,6 +50,8 @@ SIGNATURES = {
     "lst_use_graphs": (_I32, [_P, _I32]),
     "lst_profile_enable": (_I32, [_P, _I32]),
     "lst_profile_read": (_I32, [_P, ctypes.POINTER(_I32), ctypes.POINTER(ctypes.c_double), _I32]),
+    "lst_input_forward": (_I32, [_P, _I64, _I64, _I32, _P, _P, _I32, _I32, _P, _P, _P]),
+    "lst_input_update": (_I32, [_P, _I64, _I64, _I32, _P, _P, _I32, _I32, _P, _F, _P, _P]),
     "lst_restore_pristine": (_I32, [_P]),
     "lst_refresh_uinvt": (_I32, [_P, _I32, _I32, _P]),
     "lst_power_iteration": (_I32, [_P, _I32, _I32, _P, _P, _P]),
@@ -162,6 +164,57 @@ def lst_profile_read(ctx) -> tuple[int, dict]:
     ms = (ctypes.c_double * n)()
     st = lib().lst_profile_read(ctx, counts, ms, n)
     return st, {PHASES[p]: (int(counts[p]), float(ms[p])) for p in range(n)}
+
+
+def lst_input_forward(W1, ldw, D_in, d, idx, val, m, K, A, status, stream) -> int:
+    return lib().lst_input_forward(W1, ldw, D_in, d, idx, val, m, K, A, status, stream)
+
+
+def lst_input_update(W1, ldw, D_in, d, idx, val, m, K, grad_A, lr, status, stream) -> int:
+    return lib().lst_input_update(W1, ldw, D_in, d, idx, val, m, K, grad_A, lr, status, stream)
+
+
+class SparseInput:
+    """The sparse input layer of section 2.2 over a D_in x d device tensor W1."""
+
+    def __init__(self, W1, stream=None):
+        _need(W1, torch.float32, tuple(W1.shape), "W1")
+        if W1.dim() != 2:
+            raise ValueError("W1 must be D_in x d")
+        self.W1 = W1
+        self.D_in, self.d = int(W1.shape[0]), int(W1.shape[1])
+        self.stream = stream if stream is not None else torch.cuda.current_stream(W1.device)
+        self.status = torch.zeros((), dtype=torch.int32, device=W1.device)
+
+    def _slots(self, idx, val):
+        m, K = int(idx.shape[0]), int(idx.shape[1])
+        _need(idx, torch.int32, (m, K), "idx")
+        _need(val, torch.float32, (m, K), "val")
+        return m, K
+
+    def forward(self, idx, val, out=None):
+        m, K = self._slots(idx, val)
+        if out is None:
+            out = torch.empty((m, self.d), dtype=torch.float32, device=self.W1.device)
+        _need(out, torch.float32, (m, self.d), "A")
+        _check(lst_input_forward(_ptr(self.W1), self.d, self.D_in, self.d, _ptr(idx), _ptr(val), m,
+                                 K, _ptr(out), _ptr(self.status), _stream_handle(self.stream)),
+               "lst_input_forward")
+        return out
+
+    def update(self, idx, val, grad_A, lr) -> None:
+        m, K = self._slots(idx, val)
+        _need(grad_A, torch.float32, (m, self.d), "grad_A")
+        _check(lst_input_update(_ptr(self.W1), self.d, self.D_in, self.d, _ptr(idx), _ptr(val), m,
+                                K, _ptr(grad_A), float(lr), _ptr(self.status),
+                                _stream_handle(self.stream)), "lst_input_update")
+
+    def check(self) -> None:
+        """Raises LstError(LST_E_INDEX) if an index was out of range (and clears the status)."""
+        st = int(self.status.item())
+        if st:
+            self.status.zero_()
+            raise LstError(LST_E_INDEX, "sparse input layer")
 
 
 def lst_restore_pristine(ctx) -> int:

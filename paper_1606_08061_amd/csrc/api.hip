@@ -1185,3 +1185,44 @@ int lst_singular_stabilize(lst_ctx *c, float lo, float hi, int32_t log2_iters, c
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------------------
+// Section 2.2: the sparse input layer (no context).
+// ---------------------------------------------------------------------------
+namespace {
+int input_args(int64_t D_in, int32_t d, int64_t ldw, const void *W1, const int32_t *idx,
+               const float *val, int32_t m, int32_t K, const int32_t *status) {
+  if (!W1 || !status) return LST_E_ARG;
+  if (D_in < 1 || D_in > LST_MAX_D || d < 1 || d > LST_MAX_d || ldw < d) return LST_E_SHAPE;
+  if (m < 0 || K < 0 || K > LST_MAX_K || (int64_t)m * K > 8192) return LST_E_SHAPE;
+  if (m > 0 && K > 0 && (!idx || !val)) return LST_E_ARG;
+  return LST_OK;
+}
+}  // namespace
+
+extern "C" {
+
+int lst_input_forward(const float *W1, int64_t ldw, int64_t D_in, int32_t d, const int32_t *idx,
+                      const float *val, int32_t m, int32_t K, float *A, int32_t *status_dev,
+                      void *stream) {
+  int st = input_args(D_in, d, ldw, W1, idx, val, m, K, status_dev);
+  if (st != LST_OK) return st;
+  if (m > 0 && !A) return LST_E_ARG;
+  const hipError_t e = launch_input_forward(static_cast<hipStream_t>(stream), W1, ldw, D_in, d, idx,
+                                            val, m, K, A, status_dev);
+  return e == hipSuccess ? LST_OK : LST_E_HIP;
+}
+
+int lst_input_update(float *W1, int64_t ldw, int64_t D_in, int32_t d, const int32_t *idx,
+                     const float *val, int32_t m, int32_t K, const float *grad_A, float lr,
+                     int32_t *status_dev, void *stream) {
+  int st = input_args(D_in, d, ldw, W1, idx, val, m, K, status_dev);
+  if (st != LST_OK) return st;
+  if (m > 0 && K > 0 && !grad_A) return LST_E_ARG;
+  if (!finite_pos(lr)) return LST_E_ARG;
+  const hipError_t e = launch_input_update(static_cast<hipStream_t>(stream), W1, ldw, D_in, d, idx,
+                                           val, m, K, grad_A, lr, status_dev);
+  return e == hipSuccess ? LST_OK : LST_E_HIP;
+}
+
+}  // extern "C"

@@ -253,6 +253,18 @@ hipError_t launch_grad_o(hipStream_t s, float *O, int64_t D, int m, int K, const
                          int *flag);
 
 // ---------------------------------------------------------------------------
+// The sparse input layer of section 2.2 (input_layer.hip): A = X W1 and
+// W1 -= eta X^T grad_A for m examples of K slots; status: a device int whose bit
+// FLAG_INDEX is set for an index outside [-1, D_in) (the update then writes nothing).
+// ---------------------------------------------------------------------------
+hipError_t launch_input_forward(hipStream_t s, const float *W1, int64_t ldw, int64_t D_in, int d,
+                                const int *idx, const float *val, int m, int K, float *A,
+                                int *status);
+hipError_t launch_input_update(hipStream_t s, float *W1, int64_t ldw, int64_t D_in, int d,
+                               const int *idx, const float *val, int m, int K, const float *gA,
+                               float lr, int *status);
+
+// ---------------------------------------------------------------------------
 // The online step (m = 1, squared error; Algorithm 2) as one cooperative launch
 // (online.hip).  work: online_work_floats(d) floats; bar: a grid-barrier counter
 // that starts at 0 and is reset together with the step's progress counters.

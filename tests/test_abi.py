@@ -79,6 +79,12 @@ def test_host_argument_errors(L):
     assert lst.lst_power_iteration(0, 0, 7, P, P, P) == lst.LST_E_ARG
     assert lst.lst_fix_singular_value(0, P, P, 1.0) == lst.LST_E_ARG
     assert lst.lst_singular_stabilize(0, 1e-3, 100.0, 7, P, 8)[0] == lst.LST_E_ARG
+    # the sparse input layer: null W1 or status, bad shapes
+    assert lst.lst_input_forward(0, 8, 10, 8, P, P, 1, 1, P, P, 0) == lst.LST_E_ARG
+    assert lst.lst_input_forward(P, 8, 10, 8, P, P, 1, 1, P, 0, 0) == lst.LST_E_ARG
+    assert lst.lst_input_forward(P, 7, 10, 8, P, P, 1, 1, P, P, 0) == lst.LST_E_SHAPE
+    assert lst.lst_input_update(P, 8, 10, 8, P, P, 1, 65, P, 0.1, P, 0) == lst.LST_E_SHAPE
+    assert lst.lst_input_update(P, 8, 10, 8, P, P, 1, 1, P, -1.0, P, 0) == lst.LST_E_ARG
     lst.lst_destroy(0)
 
 

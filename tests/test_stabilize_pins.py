@@ -147,3 +147,37 @@ def test_singular_stabilize_cap_and_no_op():
     assert (n_lo, n_hi) == (0, 0)
     np.testing.assert_array_equal(out.V, st2.V)
     np.testing.assert_array_equal(out.U, st2.U)
+
+
+# ---- the sparse input layer of section 2.2 ----
+
+def test_input_layer_brute_force_and_autograd():
+    import torch
+
+    from oracle.input_layer import input_forward, input_update
+    rng = np.random.default_rng(12)
+    D_in, d, m, K = 9, 4, 3, 3
+    W1 = rng.standard_normal((D_in, d))
+    idx = np.array([[2, 5, 2], [0, -1, 8], [7, 7, 7]], dtype=np.int32)
+    val = rng.standard_normal((m, K))
+    A = input_forward(W1, idx, val)
+    for j in range(m):  # the paper's sum over the K slots, written as loops
+        want = np.zeros(d)
+        for k in range(K):
+            if idx[j, k] >= 0:
+                want += val[j, k] * W1[idx[j, k]]
+        np.testing.assert_allclose(A[j], want, rtol=0, atol=1e-14)
+    G = rng.standard_normal((m, d))
+    W1_new = input_update(W1, idx, val, G, 0.3)
+    # autograd of sum(A * G) with respect to W1 is the update's direction
+    Wt = torch.tensor(W1, dtype=torch.float64, requires_grad=True)
+    X = torch.zeros((m, D_in), dtype=torch.float64)
+    for j in range(m):
+        for k in range(K):
+            if idx[j, k] >= 0:
+                X[j, idx[j, k]] += val[j, k]
+    ((X @ Wt) * torch.tensor(G)).sum().backward()
+    np.testing.assert_allclose(W1_new, W1 - 0.3 * Wt.grad.numpy(), rtol=0, atol=1e-13)
+    # rows no slot names are unchanged
+    for r in (1, 3, 4, 6):
+        assert np.array_equal(W1_new[r], W1[r])
