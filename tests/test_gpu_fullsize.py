@@ -64,3 +64,72 @@ def test_full_size_ten_steps():
         print(f"step {t} ok", flush=True)
     assert rel(f.materialize_W().cpu().numpy(), W) <= 1e-3
     f.close()
+
+
+def test_full_size_m_above_d():
+    # the m = 512 sweep shape with d = 256 < m: the Woodbury branch through the d x d
+    # push-through inverse, one step at D = 200k against the oracle (the whole updated W)
+    from workloads import LOSS_SQUARED, Workload
+    w = Workload("sq_D200k_d256_m512_K5", LOSS_SQUARED, 200_000, 256, 512, 5)
+    s = Stream(w)
+    H, idx, val = s.batch()
+    print("[m > d] oracle step", flush=True)
+    ref = oracle_step(s.V0, H, idx, val, w)
+    f = make_factored(w, s.V0)
+    loss, grad = f.step(*to_dev(H, idx, val), w.lr)
+    assert f.sync_status() == 0
+    assert abs(loss.item() - ref.loss) <= 1e-4 * abs(ref.loss)
+    assert rel(grad.cpu().numpy(), ref.grad_H) <= 1e-4
+    assert rel(f.materialize_W().cpu().numpy(), ref.W_new) <= 1e-4
+    f.close()
+
+
+def test_full_size_online_steps():
+    # the one-launch online step on the benchmark's V (D = 200k, d = 500, K = 5): the first
+    # example of five minibatches, against the oracle step by step and the whole W after
+    w = WORKLOADS["sq_D200k_d500_m128_K5"]
+    s = Stream(w)
+    W = s.V0.astype(np.float64)
+    from workloads import Workload
+    w1 = Workload("sq_D200k_d500_m1_K5", w.loss, w.D, w.d, 1, w.K, lr=w.lr)
+    f = make_factored(w1, s.V0)
+    f.profile(True)
+    for t in range(5):
+        H, idx, val = (a[:1].copy() for a in s.batch())
+        ref = oracle_step(W, H, idx, val, w1)
+        loss, grad = f.step(*to_dev(H, idx, val), w.lr)
+        assert f.sync_status() == 0
+        tol = 1e-4 if t == 0 else 1e-3
+        assert abs(loss.item() - ref.loss) <= tol * abs(ref.loss)
+        assert rel(grad.cpu().numpy(), ref.grad_H) <= tol
+        W = ref.W_new
+    assert f.profile_read()["online"][0] == 5
+    assert rel(f.materialize_W().cpu().numpy(), W) <= 1e-3
+    f.close()
+
+
+def test_full_size_fix_singular_value_sampled_rows():
+    # Algorithm 5's V pass over the benchmark's V (D = 200k, d = 500): 1024 sampled rows
+    # against V_r + b (V_r . u) u^T in fp64, every row of W = V U unchanged (sampled)
+    w = WORKLOADS["sq_D200k_d500_m128_K5"]
+    s = Stream(w)
+    f = make_factored(w, s.V0)
+    rng = np.random.default_rng(31)
+    u = rng.standard_normal(w.d)
+    u = (u / np.linalg.norm(u)).astype(np.float32)
+    sigma = np.float32(0.25)
+    rows = np.sort(rng.choice(w.D, 1024, replace=False))
+    rows[-1] = w.D - 1
+    rt = torch.from_numpy(rows).to(DEV)
+    W_before = (f.V[rt] @ f.U).cpu().numpy().astype(np.float64)
+    f.fix_singular_value(to_dev(u)[0], torch.tensor(sigma, device=DEV), 1.0)
+    f.check("fix")
+    a = (1.0 - float(sigma)) / float(sigma)
+    b = -a / (1.0 + a)
+    V0 = s.V0[rows].astype(np.float64)
+    u64 = u.astype(np.float64)
+    want = V0 + b * np.outer(V0 @ u64, u64)
+    assert rel(f.V[rt].cpu().numpy(), want) <= 1e-4
+    W_after = (f.V[rt] @ f.U).cpu().numpy().astype(np.float64)
+    assert rel(W_after, W_before) <= 1e-4
+    f.close()
