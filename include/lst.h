@@ -140,11 +140,13 @@ int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0
  * Returns once the work is enqueued; device-side errors surface at the next
  * lst_sync_status.
  * With m = 1 and squared error (the online case, Algorithm 2) the step runs as
- * one cooperative launch of 64 workgroups (its products read the old Q, U, U^{-T},
- * one grid-wide barrier, then the rank-one updates), unless graphs are on, the
- * device lacks cooperative launches, or the environment variable
- * LST_ONLINE_KERNEL=0 was set when the context was created; same results to
- * fp32 rounding.
+ * one launch of 128 workgroups (its products read the old Q, U, U^{-T}, one
+ * bounded grid-wide barrier, then the rank-one updates; 128 workgroups of 256
+ * threads fit on the GPU at once), unless graphs are on or the environment
+ * variable LST_ONLINE_KERNEL=0 was set when the context was created; same results
+ * to fp32 rounding.  Should the barrier ever expire (workgroups kept from running
+ * by other work on the GPU), the step writes nothing and lst_sync_status reports
+ * LST_E_SYNC.
  */
 int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val,
              int32_t K, float lr, float *loss_dev, float *grad_H);

@@ -117,7 +117,7 @@ struct lst_ctx {
   // such as hardware counter collection, under which a wait on another stream's
   // progress could not be met.
   bool one_stream;
-  // m = 1 squared-error steps as one cooperative launch (see lst_step)
+  // m = 1 squared-error steps as one launch (see lst_step)
   bool online;
   std::vector<GraphEntry> graphs;
   uint64_t graph_tick;
@@ -387,13 +387,8 @@ int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max
   c->withhold_release = std::getenv("LST_TEST_WITHHOLD_WOODBURY_RELEASE") != nullptr;
   c->one_stream = std::getenv("LST_ONE_STREAM") != nullptr;
   {
-    int dev = 0, coop = 0;
     const char *ok = std::getenv("LST_ONLINE_KERNEL");
-    c->online = loss == LST_LOSS_SQUARED && !(ok && std::strcmp(ok, "0") == 0) &&
-                hipGetDevice(&dev) == hipSuccess &&
-                hipDeviceGetAttribute(&coop, hipDeviceAttributeCooperativeLaunch, dev) ==
-                    hipSuccess &&
-                coop != 0;
+    c->online = loss == LST_LOSS_SQUARED && !(ok && std::strcmp(ok, "0") == 0);
   }
   st = alloc_ws(c, carve_factored);
   if (st == LST_OK) st = side_create(c);

@@ -265,7 +265,7 @@ hipError_t launch_input_update(hipStream_t s, float *W1, int64_t ldw, int64_t D_
                                float lr, int *status);
 
 // ---------------------------------------------------------------------------
-// The online step (m = 1, squared error; Algorithm 2) as one cooperative launch
+// The online step (m = 1, squared error; Algorithm 2) as one launch
 // (online.hip).  work: online_work_floats(d) floats; bar: a grid-barrier counter
 // that starts at 0 and is reset together with the step's progress counters.
 // ---------------------------------------------------------------------------

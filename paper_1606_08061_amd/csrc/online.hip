@@ -1,5 +1,5 @@
-// The online step (one example, squared error; Algorithm 2) as one cooperative
-// kernel.  Every product reads the pre-update Q, U, U^{-T} (Algorithm 2 steps 1, 2,
+// The online step (one example, squared error; Algorithm 2) as one kernel
+// launch.  Every product reads the pre-update Q, U, U^{-T} (Algorithm 2 steps 1, 2,
 // 5, 6) before any of them is written (steps 5, 6, 8), so the whole step is two
 // phases around a single grid-wide barrier:
 //   A. rows r of Q, U, U^{-T} (one wavefront per row): h^ = Q h, U h and X = U^{-T} h;
@@ -20,7 +20,7 @@
 namespace lst {
 namespace {
 
-constexpr int kOnlineWGs = 128;   // workgroups (all resident: cooperative launch)
+constexpr int kOnlineWGs = 128;   // workgroups: 128 x 256 threads fit on the GPU at once
 constexpr int kOnlineSlices = 8;  // row slices of the y^ = U^T g partial sums
 constexpr int kBarrierSpin = 1 << 20;
 
