@@ -311,15 +311,24 @@ __global__ __launch_bounds__(1024) void power_norm_kernel(const float *__restric
 // cond(U) = 4e6).  With E exact to fp32 rounding the fp32 correction converges to
 // the fp32 rounding of U^{-T} while cond(U) eps32 < 1 (mixed-precision refinement).
 // ---------------------------------------------------------------------------
-// 32 x 32 entries of E per workgroup of 256 (four per thread), k in chunks of 32
-// staged in LDS as doubles (rows of Y and rows of U: both k-contiguous).
+// 32 x 32 entries of E per workgroup of four wavefronts, each a 16 x 16 block on the
+// fp64 matrix cores (v_mfma_f64_16x16x4_f64: lane l holds A[l % 16][l / 16] and
+// B[l / 16][l % 16] of a k-step of 4, and register r of the result is row
+// l / 16 + 4 r, column l % 16 of the block -- rows interleaved, unlike the fp32
+// 16 x 16 x 4 form; checked on the device); k in chunks of 32 staged in LDS as
+// doubles (rows of Y and rows of U, both k-contiguous).
+typedef double doublex4 __attribute__((ext_vector_type(4)));
+
 __global__ __launch_bounds__(256) void residual64_kernel(const float *__restrict__ Y, int ldy,
                                                          const float *__restrict__ U, int ldu,
                                                          int d, float *__restrict__ E) {
   __shared__ double Ys[32][33], Us[32][33];
   const int i0 = blockIdx.y * 32, j0 = blockIdx.x * 32;
   const int ti = threadIdx.x >> 5, tj = threadIdx.x & 31;
-  double acc[4] = {0.0, 0.0, 0.0, 0.0};  // rows ti + 8 q, column tj
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int bi = 16 * (wave >> 1), bj = 16 * (wave & 1);
+  const int li = lane & 15, lk = lane >> 4;
+  doublex4 acc = {0.0, 0.0, 0.0, 0.0};
   for (int k0 = 0; k0 < d; k0 += 32) {
     const int k = k0 + tj;
 #pragma unroll
@@ -329,18 +338,16 @@ __global__ __launch_bounds__(256) void residual64_kernel(const float *__restrict
       Us[r][tj] = (j0 + r < d && k < d) ? (double)U[(int64_t)(j0 + r) * ldu + k] : 0.0;
     }
     __syncthreads();
-#pragma unroll 8
-    for (int kk = 0; kk < 32; ++kk) {
-      const double u = Us[tj][kk];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) acc[q] = fma(Ys[ti + 8 * q][kk], u, acc[q]);
-    }
+    for (int kk = 0; kk < 32; kk += 4)
+      acc = __builtin_amdgcn_mfma_f64_16x16x4f64(Ys[bi + li][kk + lk], Us[bj + li][kk + lk], acc,
+                                                 0, 0, 0);
     __syncthreads();
   }
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int i = i0 + ti + 8 * q, j = j0 + tj;
-    if (i < d && j < d) E[(int64_t)i * d + j] = (float)((i == j ? 1.0 : 0.0) - acc[q]);
+  for (int r = 0; r < 4; ++r) {
+    const int i = i0 + bi + lk + 4 * r, j = j0 + bj + li;
+    if (i < d && j < d) E[(int64_t)i * d + j] = (float)((i == j ? 1.0 : 0.0) - acc[r]);
   }
 }
 
