@@ -15,9 +15,11 @@
  * Conventions shared by every entry point
  *   - Memory: every float / int pointer is a DEVICE pointer owned by the caller
  *     (allocated with the HIP runtime, e.g. through PyTorch), except where a
- *     parameter says "host".  The library never frees caller memory.  A context
- *     allocates its own device workspace in lst_create / lst_naive_create and
- *     frees it in lst_destroy.
+ *     parameter says "host".  The library never allocates or frees device
+ *     memory: a context works in a caller-owned workspace of
+ *     lst_workspace_bytes (lst_naive_workspace_bytes) bytes, 256-byte aligned,
+ *     that must stay allocated and untouched by the caller until lst_destroy.
+ *     The context itself is a small host object.
  *   - Layout: row-major.  A minibatch H is m x d, one example per row (the same
  *     bytes as the paper's d x m H with one example per column).  V and W are
  *     D x d with row stride ldv / ldw >= d (floats); U, U^{-T} and Q are d x d
@@ -29,16 +31,8 @@
  *     allowed and their V updates are summed in a fixed order.
  *   - Streams: every call is enqueued on the stream given at creation (a
  *     hipStream_t passed as void*; NULL = the null stream) and returns without
- *     synchronising, except lst_sync_status and lst_init_factored.  A factored
- *     step also uses a side stream of the context (the Woodbury inverse); the
- *     two are ordered by progress counters in device memory (the side stream
- *     starts once the step has started on the given stream, the state updates
- *     wait for the side stream's result), so the caller only orders work against
- *     the given stream.  A context must not be used from two host threads at
- *     once.
- *     With the environment variable LST_ONE_STREAM set when the context is
- *     created, the side stream's work goes on the given stream too (for tools
- *     that run one dispatch at a time, e.g. hardware counter collection).
+ *     synchronising, except lst_sync_status and lst_init_factored.  A context
+ *     must not be used from two host threads at once.
  *   - Errors: every call returns an lst_status.  Argument errors detectable on
  *     the host are returned at once and nothing is enqueued.  Data-dependent
  *     errors found on the device (an index outside [-1, D), a Woodbury matrix
@@ -83,9 +77,9 @@ enum lst_status {
                            and finite                                          */
   LST_E_HIP = -6,       /* a HIP runtime call failed                           */
   LST_E_STATE = -7,     /* wrong context kind for this call                    */
-  LST_E_SYNC = -8       /* (device) a step's two streams lost their ordering: a
-                           bounded wait of one on the other's progress counter
-                           expired; the state updates of that step were skipped */
+  LST_E_SYNC = -8       /* (device) the online step's bounded grid barrier
+                           expired (its workgroups were not all resident); the
+                           step wrote nothing                                  */
 };
 
 /* Limits of one context. */
@@ -95,14 +89,27 @@ enum lst_status {
 #define LST_MAX_K 64
 
 /*
+ * lst_workspace_bytes -- size in bytes of the device workspace lst_create needs for
+ * these dimensions (the step's m x d, m x m and per-example intermediates, the
+ * products' descriptors for up to 16 minibatch sizes, the section 5 scratch and the
+ * split-k partial sums of the initial Q = V^T V).  0 if the arguments are invalid
+ * (the checks of lst_create).
+ */
+size_t lst_workspace_bytes(int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss);
+
+/*
  * lst_create -- context for the factored step (Algorithm 3 / Algorithm 4).
  *   D, d         output size and hidden size (1 <= d <= LST_MAX_d, 1 <= D <= LST_MAX_D).
  *   m_max, K_max largest minibatch and largest number of target slots per
- *                example that lst_step will be given (<= LST_MAX_M, LST_MAX_K).
+ *                example that lst_step will be given (<= LST_MAX_M, LST_MAX_K,
+ *                m_max * K_max <= 8192).
  *   loss         an lst_loss value.
  *   eps          spherical softmax epsilon (> 0); ignored for squared error.
  *   V            D x ldv device buffer holding V (updated in place by lst_step).
  *   U, UinvT, Q  d x ldd device buffers (updated in place by lst_step).
+ *   workspace    device buffer of ws_bytes >= lst_workspace_bytes(D, d, m_max,
+ *                K_max, loss) bytes, 256-byte aligned (LST_E_ARG if NULL or
+ *                misaligned, LST_E_SHAPE if too small); cleared on the stream here.
  *   stream       hipStream_t as void*; every call is enqueued on it.
  * The buffers are borrowed: they must stay allocated until lst_destroy.  The
  * state they hold is not read here; call lst_init_factored before the first
@@ -110,7 +117,21 @@ enum lst_status {
  */
 int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss,
                float eps, float *V, int64_t ldv, float *U, float *UinvT, float *Q, int32_t ldd,
-               void *stream);
+               void *workspace, size_t ws_bytes, void *stream);
+
+/* Options of a context (lst_set_option). */
+enum lst_option {
+  /* 1 (default for squared error): m = 1 squared-error steps run as the one-launch
+     online step of Algorithm 2; 0: they take the general minibatch path. */
+  LST_OPT_ONLINE_KERNEL = 0,
+  /* Polls (0 .. 2^30, default 2^20) a workgroup of the online step waits at its
+     grid barrier before the step is abandoned (nothing written, LST_E_SYNC at the
+     next lst_sync_status).  Small values force that outcome, for testing it. */
+  LST_OPT_SPIN_LIMIT = 1
+};
+
+/* lst_set_option -- sets an lst_option; LST_E_ARG for an unknown option or value. */
+int lst_set_option(lst_ctx *c, int32_t option, int64_t value);
 
 /*
  * lst_init_factored -- Algorithm 1 (and the general initialisation of section 4.8).
@@ -118,8 +139,8 @@ int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max
  *   U0 (d x ldu0, device) is copied into U when not NULL; NULL sets U = I.
  * Then U^{-T} = inv(U)^T and Q = (V U)^T (V U) are computed (Q = V^T V when
  * U = I), and the sticky error flag is cleared.  With U0 given, U is inverted
- * in fp64 on the host (LST_E_NOT_SPD if it is singular).  Synchronises the
- * stream.  Passing the current (V, U) re-derives the bookkeeping from scratch,
+ * in fp64 on the host (LST_E_NOT_SPD if it is singular).  V^T V is split over D
+ * into the workspace's partial sums.  Synchronises the stream.  Passing the current (V, U) re-derives the bookkeeping from scratch,
  * which is also how a run resumes from a (V, U) checkpoint.
  */
 int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0, int32_t ldu0);
@@ -136,31 +157,32 @@ int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0
  *   grad_H   m x d device buffer receiving dL/dH (row stride d); may be NULL.
  * State V, U, U^{-T}, Q is updated in place so that V U equals
  * W - eta dL/dW (eq. updateU / updateV, eq. gen-updateU / gen-updateV), Q equals
- * the new W^T W (eq. updateQ / gen-Qnew) and U^{-T} the new inverse transpose.
- * Returns once the work is enqueued; device-side errors surface at the next
- * lst_sync_status.
+ * the new W^T W (eq. updateQ / gen-Qnew) and U^{-T} the new inverse transpose
+ * (Woodbury, section 4.7: C = I - 2 eta S H^T H S is inverted as a certified
+ * degree-7 Chebyshev polynomial in 2 eta S H^T H S on the matrix cores when the
+ * bound ||(2 eta S H^T H S)^2||_inf^(1/2) proves it exact to below fp32 rounding,
+ * else by exact elimination, whose pivots decide LST_E_NOT_SPD).  Five kernel
+ * launches on the stream; returns once they are enqueued (the first call with a
+ * new m also copies that m's product descriptors into the workspace, ordered on
+ * the stream); device-side errors surface at the next lst_sync_status.
  * With m = 1 and squared error (the online case, Algorithm 2) the step runs as
  * one launch of 128 workgroups (its products read the old Q, U, U^{-T}, one
- * bounded grid-wide barrier, then the rank-one updates; 128 workgroups of 256
- * threads fit on the GPU at once), unless graphs are on or the environment
- * variable LST_ONLINE_KERNEL=0 was set when the context was created; same results
- * to fp32 rounding.  Should the barrier ever expire (workgroups kept from running
- * by other work on the GPU), the step writes nothing and lst_sync_status reports
- * LST_E_SYNC.
+ * bounded grid-wide barrier with a single go/abort decision, then the rank-one
+ * updates; 128 workgroups of 256 threads fit on the GPU at once), unless graphs
+ * are on or LST_OPT_ONLINE_KERNEL is 0; same results to fp32 rounding.  Should the
+ * barrier ever expire (workgroups kept from running by other work on the GPU),
+ * the step writes nothing and lst_sync_status reports LST_E_SYNC.
  */
 int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val,
              int32_t K, float lr, float *loss_dev, float *grad_H);
 
 /*
- * lst_use_graphs -- off (default) or on.  When on, lst_step records the work of
- * a step as HIP graphs (one per stream part) the first time it sees a given (H,
- * idx, val, loss_dev, grad_H, m, K, lr) and replays them, three graph launches,
- * whenever the same arguments recur (up to 256 per context, least recently used
- * evicted); the kernels and results are the same as without graphs.  Off by
- * default: with the streams ordered by device counters, direct launches cost
- * the host less than the graph launches and leave shorter gaps between kernels
- * on the GPU.  While the profiling hook is on, steps are enqueued kernel by
- * kernel.
+ * lst_use_graphs -- off (default) or on.  When on, lst_step records the five
+ * launches of a step as one HIP graph the first time it sees a given (H, idx,
+ * val, loss_dev, grad_H, m, K, lr) and replays it whenever the same arguments
+ * recur (up to 256 per context, least recently used evicted); the kernels and
+ * results are the same as without graphs.  While the profiling hook is on, steps
+ * are enqueued kernel by kernel.
  */
 int lst_use_graphs(lst_ctx *c, int32_t on);
 
@@ -263,55 +285,57 @@ int lst_singular_stabilize(lst_ctx *c, float lo, float hi, int32_t log2_iters, c
                            int32_t max_fixes, int32_t *n_fixed, float *sigmas);
 
 /*
- * lst_sync_status -- synchronises the context's streams, returns the sticky
+ * lst_sync_status -- synchronises the context's stream, returns the sticky
  * device error (LST_OK if none) and clears it.  Also returns LST_E_HIP if a
  * kernel launch or the synchronisation failed.  After LST_E_SYNC it also resets
- * the progress counters that order the two streams.
+ * the online step's barrier counter.
  */
 int lst_sync_status(lst_ctx *c);
 
 /* lst_status_string -- static, human-readable name of a status code. */
 const char *lst_status_string(int status);
 
-/* lst_destroy -- frees the context and its workspace (after synchronising). */
+/* lst_destroy -- synchronises the stream and frees the context (the caller then
+   owns its workspace again). */
 void lst_destroy(lst_ctx *c);
+
+/* lst_naive_workspace_bytes -- workspace bytes of lst_naive_create (the D x m
+   output and its column-norm and split-k partial sums); 0 for invalid arguments. */
+size_t lst_naive_workspace_bytes(int64_t D, int32_t d, int32_t m_max, int32_t K_max,
+                                 int32_t loss);
 
 /*
  * lst_naive_create -- context for the naive O(D d) step of sections 2.3 / 4.3:
  * O = W H^T (D x m) on MFMA, the loss over the full output, grad_H = W^T grad_O
  * and W <- W - eta grad_O H, with W held explicitly.
  *   W      D x ldw device buffer, updated in place by lst_naive_step.
- *   Other arguments as in lst_create.  The workspace holds the D x m output.
+ *   workspace, ws_bytes  as in lst_create, sized by lst_naive_workspace_bytes.
+ *   Other arguments as in lst_create.
  */
 int lst_naive_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max,
-                     int32_t loss, float eps, float *W, int64_t ldw, void *stream);
+                     int32_t loss, float eps, float *W, int64_t ldw, void *workspace,
+                     size_t ws_bytes, void *stream);
 
 /* lst_naive_step -- same contract as lst_step, on a naive context. */
 int lst_naive_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const float *val,
                    int32_t K, float lr, float *loss_dev, float *grad_H);
 
-/* Phases of a step, as timed by the profiling hook below.  The Gram product and
-   the Woodbury inverse run on a side stream of the context, overlapping the main
-   chain; the other phases run in order on the context's stream.  The waits
-   between the streams are not part of any phase. */
+/* Phases of a step, as timed by the profiling hook below: the five launches of a
+   factored step, the naive step's parts and the online step. */
 enum lst_phase {
-  LST_PHASE_CONTRACT = 0,      /* H^ = Q H, H~ = U H, X = U^{-T} H (matrix cores)          */
-  LST_PHASE_GATHER = 1,        /* gather of the K target rows of V, loss epilogue, G       */
-  LST_PHASE_ZGRAD = 2,         /* Z^ = U^T G, grad_H, H^T H^, H~^T G (matrix cores)        */
-  LST_PHASE_MBLOCK = 3,        /* loss sum, M of the Q update                              */
-  LST_PHASE_WOODBURY = 4,      /* the m x m Woodbury matrix and its inverse                */
-  LST_PHASE_MID = 5,           /* R X, (eta^2/2) M H - eta grad_H, U update (matrix cores) */
-  LST_PHASE_UPDATE = 6,        /* U^{-T} and Q updates, P = U_new^{-T} H (matrix cores);
-                                  for squared error also the V update of SCATTER           */
-  LST_PHASE_SCATTER = 7,       /* conflict-free update of the target rows of V (spherical
-                                  softmax; for squared error it runs inside UPDATE)        */
-  LST_PHASE_NAIVE_FWD = 8,     /* naive: O = W H^T                                         */
-  LST_PHASE_NAIVE_LOSS = 9,    /* naive: column norms of O, loss, grad_O                   */
-  LST_PHASE_NAIVE_GRAD = 10,   /* naive: grad_H = grad_O^T W                               */
-  LST_PHASE_NAIVE_UPDATE = 11, /* naive: W <- W - eta grad_O H                             */
-  LST_PHASE_GRAM = 12,         /* N = H^T H, the Gram matrix of the minibatch (matrix cores) */
-  LST_PHASE_ONLINE = 13,       /* m = 1, squared error: the whole step in one launch       */
-  LST_NUM_PHASES = 14
+  LST_PHASE_CONTRACT = 0,      /* H^ = Q H, H~ = U H, X = U^{-T} H, N = H^T H (matrix cores)  */
+  LST_PHASE_GATHER = 1,        /* gather of the K target rows of V, loss epilogue, G; H^T H^,
+                                  E^2 and E Xs of the Woodbury polynomial                    */
+  LST_PHASE_ZGRAD = 2,         /* Z^ = U^T G, grad_H, H~^T G, E^2 Xs, E^3 Xs, E^4, Yring^T
+                                  Yring, the loss sum, the certificate (or exact inverse)    */
+  LST_PHASE_MID = 3,           /* (eta^2/2) M H - eta grad_H, R X, the U update              */
+  LST_PHASE_UPDATE = 4,        /* the U^{-T} and Q updates and the V scatter                 */
+  LST_PHASE_NAIVE_FWD = 5,     /* naive: O = W H^T                                           */
+  LST_PHASE_NAIVE_LOSS = 6,    /* naive: column norms of O, loss, grad_O                     */
+  LST_PHASE_NAIVE_GRAD = 7,    /* naive: grad_H = grad_O^T W                                 */
+  LST_PHASE_NAIVE_UPDATE = 8,  /* naive: W <- W - eta grad_O H                               */
+  LST_PHASE_ONLINE = 9,        /* m = 1, squared error: the whole step in one launch         */
+  LST_NUM_PHASES = 10
 };
 
 /*

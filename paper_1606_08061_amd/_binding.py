@@ -36,8 +36,11 @@ _I32 = ctypes.c_int32
 _I64 = ctypes.c_int64
 _F = ctypes.c_float
 SIGNATURES = {
+    "lst_workspace_bytes": (ctypes.c_size_t, [_I64, _I32, _I32, _I32, _I32]),
+    "lst_naive_workspace_bytes": (ctypes.c_size_t, [_I64, _I32, _I32, _I32, _I32]),
     "lst_create": (_I32, [ctypes.POINTER(_P), _I64, _I32, _I32, _I32, _I32, _F, _P, _I64, _P, _P,
-                          _P, _I32, _P]),
+                          _P, _I32, _P, ctypes.c_size_t, _P]),
+    "lst_set_option": (_I32, [_P, _I32, _I64]),
     "lst_init_factored": (_I32, [_P, _P, _I64, _P, _I32]),
     "lst_step": (_I32, [_P, _P, _I32, _P, _P, _I32, _F, _P, _P]),
     "lst_materialize_W": (_I32, [_P, _P, _I64]),
@@ -45,7 +48,7 @@ SIGNATURES = {
     "lst_status_string": (ctypes.c_char_p, [_I32]),
     "lst_destroy": (None, [_P]),
     "lst_naive_create": (_I32, [ctypes.POINTER(_P), _I64, _I32, _I32, _I32, _I32, _F, _P, _I64,
-                                _P]),
+                                _P, ctypes.c_size_t, _P]),
     "lst_naive_step": (_I32, [_P, _P, _I32, _P, _P, _I32, _F, _P, _P]),
     "lst_use_graphs": (_I32, [_P, _I32]),
     "lst_profile_enable": (_I32, [_P, _I32]),
@@ -60,8 +63,11 @@ SIGNATURES = {
                                       ctypes.POINTER(_F)]),
 }
 
-PHASES = ["contract", "gather", "zgrad", "mblock", "woodbury", "mid", "update", "scatter",
-          "naive_fwd", "naive_loss", "naive_grad", "naive_update", "gram", "online"]
+PHASES = ["contract", "gather", "zgrad", "mid", "update", "naive_fwd", "naive_loss", "naive_grad",
+          "naive_update", "online"]
+
+LST_OPT_ONLINE_KERNEL = 0
+LST_OPT_SPIN_LIMIT = 1
 
 _lib = None
 _lock = threading.Lock()
@@ -113,17 +119,32 @@ def _stream_handle(stream) -> int:
 
 # ---- C entry points under their own names (raw pointers and sizes) ----
 
-def lst_create(D, d, m_max, K_max, loss, eps, V, ldv, U, UinvT, Q, ldd, stream) -> tuple[int, int]:
+def lst_workspace_bytes(D, d, m_max, K_max, loss) -> int:
+    return int(lib().lst_workspace_bytes(D, d, m_max, K_max, loss))
+
+
+def lst_naive_workspace_bytes(D, d, m_max, K_max, loss) -> int:
+    return int(lib().lst_naive_workspace_bytes(D, d, m_max, K_max, loss))
+
+
+def lst_create(D, d, m_max, K_max, loss, eps, V, ldv, U, UinvT, Q, ldd, ws, ws_bytes,
+               stream) -> tuple[int, int]:
     ctx = _P()
     st = lib().lst_create(ctypes.byref(ctx), D, d, m_max, K_max, loss, eps, V, ldv, U, UinvT, Q,
-                          ldd, stream)
+                          ldd, ws, ws_bytes, stream)
     return st, (ctx.value or 0)
 
 
-def lst_naive_create(D, d, m_max, K_max, loss, eps, W, ldw, stream) -> tuple[int, int]:
+def lst_naive_create(D, d, m_max, K_max, loss, eps, W, ldw, ws, ws_bytes,
+                     stream) -> tuple[int, int]:
     ctx = _P()
-    st = lib().lst_naive_create(ctypes.byref(ctx), D, d, m_max, K_max, loss, eps, W, ldw, stream)
+    st = lib().lst_naive_create(ctypes.byref(ctx), D, d, m_max, K_max, loss, eps, W, ldw, ws,
+                                ws_bytes, stream)
     return st, (ctx.value or 0)
+
+
+def lst_set_option(ctx, option, value) -> int:
+    return lib().lst_set_option(ctx, option, value)
 
 
 def lst_init_factored(ctx, V0, ldv0, U0, ldu0) -> int:
@@ -255,6 +276,14 @@ def _need(t, dtype, shape, name):
         raise ValueError(f"{name} must be contiguous")
 
 
+def _workspace(nbytes: int, device) -> torch.Tensor:
+    """A device workspace of nbytes (torch's allocator returns 256-byte aligned blocks)."""
+    ws = torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+    if ws.data_ptr() % 256:
+        raise RuntimeError("workspace is not 256-byte aligned")
+    return ws
+
+
 class _Ctx:
     def __init__(self, D, d, m_max, K_max, loss, eps, device, stream):
         if not torch.cuda.is_available():
@@ -319,9 +348,14 @@ class Factored(_Ctx):
         self.U = torch.zeros((self.d, self.d), **kw)
         self.UinvT = torch.zeros((self.d, self.d), **kw)
         self.Q = torch.zeros((self.d, self.d), **kw)
+        nb = lst_workspace_bytes(self.D, self.d, self.m_max, self.K_max, self.loss)
+        if nb == 0:
+            raise LstError(LST_E_SHAPE, "lst_workspace_bytes")
+        self.ws = _workspace(nb, self.device)
         st, self.ctx = lst_create(self.D, self.d, self.m_max, self.K_max, self.loss, self.eps,
                                   _ptr(self.V), self.d, _ptr(self.U), _ptr(self.UinvT),
-                                  _ptr(self.Q), self.d, _stream_handle(self.stream))
+                                  _ptr(self.Q), self.d, _ptr(self.ws), nb,
+                                  _stream_handle(self.stream))
         _check(st, "lst_create")
         self._step_fn = lib().lst_step
 
@@ -356,6 +390,9 @@ class Factored(_Ctx):
 
     def use_graphs(self, on: bool = True) -> None:
         _check(lst_use_graphs(self.ctx, 1 if on else 0), "lst_use_graphs")
+
+    def set_option(self, option: int, value: int) -> None:
+        _check(lst_set_option(self.ctx, int(option), int(value)), "lst_set_option")
 
     # ---- section 5: numerical stabilisation between steps ----
 
@@ -409,8 +446,12 @@ class Naive(_Ctx):
     def __init__(self, D, d, m_max, K_max, loss="squared", eps=1e-3, device=None, stream=None):
         super().__init__(D, d, m_max, K_max, loss, eps, device, stream)
         self.W = torch.zeros((self.D, self.d), dtype=torch.float32, device=self.device)
+        nb = lst_naive_workspace_bytes(self.D, self.d, self.m_max, self.K_max, self.loss)
+        if nb == 0:
+            raise LstError(LST_E_SHAPE, "lst_naive_workspace_bytes")
+        self.ws = _workspace(nb, self.device)
         st, self.ctx = lst_naive_create(self.D, self.d, self.m_max, self.K_max, self.loss,
-                                        self.eps, _ptr(self.W), self.d,
+                                        self.eps, _ptr(self.W), self.d, _ptr(self.ws), nb,
                                         _stream_handle(self.stream))
         _check(st, "lst_naive_create")
         self._step_fn = lib().lst_naive_step

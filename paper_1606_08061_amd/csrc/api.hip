@@ -4,6 +4,7 @@
 #include <cmath>
 #include <cstdlib>
 #include <cstring>
+#include <memory>
 #include <new>
 #include <vector>
 
@@ -18,16 +19,19 @@ thread_local ProfHook g_prof;
 namespace {
 
 enum : int { KIND_FACTORED = 1, KIND_NAIVE = 2 };
-constexpr int kTargetWGs = 1024;   // workgroups a split-k GEMM aims for
+constexpr int kTargetWGs = 1024;  // workgroups a split-k GEMM aims for
 constexpr int kColnormBlocks = 1024;
+constexpr size_t kInitPartialCap = size_t(8) << 20;  // floats of split-k partials for Q = V^T V
+constexpr int kDefaultSpin = 1 << 20;               // polls of the online step's barrier
+constexpr size_t kWsAlign = 256;
 
-// Device workspace carved in 256-byte aligned pieces.
+// Device workspace carved in 256-byte aligned pieces (a null base only measures).
 struct Carver {
   char *base;
   size_t off = 0;
   template <class T>
   T *take(size_t n) {
-    off = (off + 255) & ~size_t(255);
+    off = (off + kWsAlign - 1) & ~(kWsAlign - 1);
     T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
     off += n * sizeof(T);
     return p;
@@ -40,21 +44,17 @@ struct GraphEntry {
   void *loss, *grad;
   int m, K;
   uint32_t lr_bits;
-  // the step's parts in launch order: main stream up to M, side stream (Woodbury
-  // branch), main stream state updates
-  hipGraphExec_t exec_a, exec_side, exec_b;
+  hipGraphExec_t exec;
   uint64_t last_use;
 };
 constexpr size_t kGraphCap = 256;
 
-// The five GEMM batches of a factored step for one m: Gram product, contractions,
-// Z^/grad_H, mid and state updates.
-constexpr int kPlanBatches = 5;
+// The step's products for one minibatch size m: host copy and its device slot.
 constexpr size_t kPlanCap = 16;
 struct PlanEntry {
   int m;
-  GemmBatch b[kPlanBatches];
-  GemmBatch *dev;
+  std::unique_ptr<StepPlan> host;
+  StepPlan *dev;
   uint64_t last_use;
 };
 
@@ -74,93 +74,96 @@ struct lst_ctx {
   // naive state (borrowed)
   float *W;
   int64_t ldw;
-  // workspace (owned)
+  // workspace (borrowed from the caller)
   void *ws;
   size_t ws_bytes;
-  float *Hhat, *Htil, *X, *G, *Atil, *Zhat, *gradH, *Yw, *Zq, *P;
-  float *N, *Mhat, *HZ, *M, *R, *Cwork;
-  float *Pbig, *Cp, *Rp;  // blocked Woodbury inverse for m > kWoodburyOneWG
-  float *dq, *lvec, *dA;
+  StepBufs sb;
+  float *gradH;  // grad_H when the caller passes none
   // section 5 stabilisation: two d x d scratch matrices (row stride d), four
-  // d-vectors, the partial sums of two matrix-vector products (32 d) and eight scalars
+  // d-vectors, the partial sums of two matrix-vector products (32 d; also the
+  // online step's work vectors) and eight scalars
   float *Sd0, *Sd1, *svec, *spart, *sscal;
+  float *initpart;  // split-k partial sums of Q = V^T V (lst_init_factored)
+  size_t initpart_floats;
   int *flag;
-  // progress counters ordering the two streams of a factored step: [0] contraction
-  // launches started, [1] Woodbury inverses completed, [2] Z^ launches started; [3]
-  // the grid barrier of the online step's single launch
-  int *cnt;
+  int *cnt;  // [0] the online step's grid-barrier counter, [1] its decision word
   float *O, *colpart, *splitpart;
   hipError_t last_err;
-  // side stream of a factored step (Woodbury inverse); cap is the stream a step
-  // is captured on when it is recorded as HIP graphs
-  hipStream_t side[1];
-  hipStream_t cap;
-  bool have_side;
+  hipStream_t cap;  // stream a step is captured on when it is recorded as a HIP graph
+  bool have_cap;
   // tracing: event pairs per phase
   bool prof_on;
   std::vector<hipEvent_t> prof_ev[LST_NUM_PHASES];
   int prof_used[LST_NUM_PHASES];
-  // GEMM plans of the factored step, one per minibatch size m (host copies and
-  // their device slots in plan_pool)
   std::vector<PlanEntry> plans;
-  GemmBatch *plan_pool;
+  StepPlan *plan_pool;
   uint64_t plan_tick;
-  // captured steps, one per distinct (inputs, m, K, lr)
   bool use_graphs;
-  // test hook (environment variable LST_TEST_WITHHOLD_WOODBURY_RELEASE at creation):
-  // the Woodbury branch never releases its counter, so the state-update wait of
-  // every step expires (bounded) and reports LST_E_SYNC
-  bool withhold_release;
-  // environment variable LST_ONE_STREAM at creation: the side stream's work is
-  // enqueued on the context's stream instead, after the main chain up to M (the
-  // waits are then met on arrival).  For tools that run one dispatch at a time,
-  // such as hardware counter collection, under which a wait on another stream's
-  // progress could not be met.
-  bool one_stream;
-  // m = 1 squared-error steps as one launch (see lst_step)
-  bool online;
   std::vector<GraphEntry> graphs;
   uint64_t graph_tick;
+  // options (lst_set_option)
+  bool online;     // m = 1 squared-error steps as one launch
+  int spin_limit;  // bound of the online step's barrier wait
 };
 
 namespace {
 
 bool finite_pos(float x) { return std::isfinite(x) && x > 0.f; }
 
+// Floats of split-k partials for Q = V^T V: as many splits as the GEMM would take,
+// capped at kInitPartialCap floats (fewer splits beyond it).
+size_t init_partial_floats(int64_t D, int d) {
+  GemmDesc g = gemm_desc(d, d, (int)D, nullptr, d, 1, nullptr, d, 1, nullptr, d);
+  const size_t want = gemm_plan_split(g, kTargetWGs, nullptr);
+  return std::min(want, kInitPartialCap / ((size_t)d * d) * ((size_t)d * d));
+}
+
 void carve_factored(lst_ctx *c, Carver &cv) {
-  const size_t md = (size_t)c->m_max * c->d, mm = (size_t)c->m_max * c->m_max;
-  const size_t mk = (size_t)c->m_max * (c->K_max > 0 ? c->K_max : 1);
-  c->Hhat = cv.take<float>(md);
-  c->Htil = cv.take<float>(md);
-  c->X = cv.take<float>(md);
-  c->G = cv.take<float>(md);
-  c->Atil = cv.take<float>(md);
-  c->Zhat = cv.take<float>(md);
+  const size_t m = (size_t)c->m_max, d = (size_t)c->d;
+  const size_t md = m * d, mm = m * m;
+  const size_t mk = m * (c->K_max > 0 ? c->K_max : 1);
+  StepBufs &b = c->sb;
+  b.Hhat = cv.take<float>(md);
+  b.Htil = cv.take<float>(md);
+  b.X = cv.take<float>(md);
+  b.G = cv.take<float>(md);
+  b.Atil = cv.take<float>(md);
+  b.W1 = cv.take<float>(md);
+  b.P2 = cv.take<float>(md);
+  b.P3 = cv.take<float>(md);
+  b.RX = cv.take<float>(md);
+  b.Zq = cv.take<float>(md);
   c->gradH = cv.take<float>(md);
-  c->Yw = cv.take<float>(md);
-  c->Zq = cv.take<float>(md);
-  c->P = cv.take<float>(md);
-  c->N = cv.take<float>(mm);
-  c->Mhat = cv.take<float>(mm);
-  c->HZ = cv.take<float>(mm);
-  c->M = cv.take<float>(mm);
-  c->R = cv.take<float>(mm);
-  c->Cwork = cv.take<float>(mm);
-  const size_t big = c->m_max > kWoodburyOneWG ? kBigBlock : 0;
-  c->Pbig = cv.take<float>(2 * big * big);  // P and P + I
-  c->Cp = cv.take<float>((size_t)c->m_max * big);
-  c->Rp = cv.take<float>(big * c->m_max);
-  c->dq = cv.take<float>(c->m_max);
-  c->lvec = cv.take<float>(c->m_max);
-  c->dA = cv.take<float>(mk);
-  c->Sd0 = cv.take<float>((size_t)c->d * c->d);
-  c->Sd1 = cv.take<float>((size_t)c->d * c->d);
-  c->svec = cv.take<float>(4 * (size_t)c->d);
-  c->spart = cv.take<float>(std::max<size_t>(32 * (size_t)c->d, online_work_floats(c->d)));
+  b.N = cv.take<float>(mm);
+  b.Mhat = cv.take<float>(mm);
+  b.HZ = cv.take<float>(mm);
+  b.YY = cv.take<float>(mm);
+  b.E2 = cv.take<float>(mm);
+  b.E4 = cv.take<float>(mm);
+  b.R = cv.take<float>(mm);
+  b.Cwork = cv.take<float>(mm);
+  b.qpart = cv.take<float>((d + 15) / 16 * m);
+  b.bpart = cv.take<float>((m + 15) / 16 * m);
+  b.dq = cv.take<float>(m);
+  b.lvec = cv.take<float>(m);
+  b.dA = cv.take<float>(mk);
+  b.wA = cv.take<float>(mk);
+  b.sval = cv.take<float>(mk);
+  b.srow = cv.take<int>(mk);
+  b.scnt = cv.take<int>(m);
+  b.coef = cv.take<float>(8);
+  b.cert = cv.take<int>(1);
+  c->Sd0 = cv.take<float>(d * d);
+  c->Sd1 = cv.take<float>(d * d);
+  c->svec = cv.take<float>(4 * d);
+  c->spart = cv.take<float>(std::max<size_t>(32 * d, online_work_floats(c->d)));
   c->sscal = cv.take<float>(8);
+  c->initpart_floats = init_partial_floats(c->D, c->d);
+  c->initpart = cv.take<float>(c->initpart_floats);
   c->flag = cv.take<int>(1);
   c->cnt = cv.take<int>(4);
-  c->plan_pool = cv.take<GemmBatch>(kPlanCap * kPlanBatches);
+  c->plan_pool = cv.take<StepPlan>(kPlanCap);
+  b.flag = c->flag;
 }
 
 // Upper bound of the split-k partial buffer of grad_H = grad_O^T W for any m <= m_max:
@@ -196,9 +199,9 @@ void carve_naive(lst_ctx *c, Carver &cv) {
   c->colpart = cv.take<float>((parts128 > kColnormBlocks ? parts128 : kColnormBlocks) * c->m_max);
   c->splitpart = cv.take<float>(naive_split_floats(c));
   c->gradH = cv.take<float>(md);
-  c->dq = cv.take<float>(c->m_max);
-  c->lvec = cv.take<float>(c->m_max);
-  c->dA = cv.take<float>(mk);
+  c->sb.dq = cv.take<float>(c->m_max);
+  c->sb.lvec = cv.take<float>(c->m_max);
+  c->sb.dA = cv.take<float>(mk);
   c->flag = cv.take<int>(1);
 }
 
@@ -211,15 +214,35 @@ int common_args(int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss
   return LST_OK;
 }
 
-int alloc_ws(lst_ctx *c, void (*carve)(lst_ctx *, Carver &)) {
-  Carver probe{nullptr};
-  carve(c, probe);
-  c->ws_bytes = probe.off + 256;
-  if (hipMalloc(&c->ws, c->ws_bytes) != hipSuccess) return LST_E_HIP;
-  Carver real{static_cast<char *>(c->ws)};
+// The bytes a context's carve takes (plus alignment slack for an aligned base).
+size_t ws_size(int kind, int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss) {
+  lst_ctx probe{};
+  probe.kind = kind;
+  probe.D = D;
+  probe.d = d;
+  probe.m_max = m_max;
+  probe.K_max = K_max;
+  probe.loss = loss;
+  Carver cv{nullptr};
+  if (kind == KIND_FACTORED)
+    carve_factored(&probe, cv);
+  else
+    carve_naive(&probe, cv);
+  return (cv.off + kWsAlign - 1) & ~(kWsAlign - 1);
+}
+
+// Takes the caller's workspace: checks its size and alignment, carves it and clears
+// it on the stream (the error flag and counters start at zero).
+int take_ws(lst_ctx *c, void *ws, size_t ws_bytes, void (*carve)(lst_ctx *, Carver &)) {
+  const size_t need = ws_size(c->kind, c->D, c->d, c->m_max, c->K_max, c->loss);
+  if (!ws) return LST_E_ARG;
+  if ((reinterpret_cast<uintptr_t>(ws) & (kWsAlign - 1)) != 0) return LST_E_ARG;
+  if (ws_bytes < need) return LST_E_SHAPE;
+  c->ws = ws;
+  c->ws_bytes = need;
+  Carver real{static_cast<char *>(ws)};
   carve(c, real);
-  if (hipMemsetAsync(c->ws, 0, c->ws_bytes, c->stream) != hipSuccess) return LST_E_HIP;
-  if (hipStreamSynchronize(c->stream) != hipSuccess) return LST_E_HIP;
+  if (hipMemsetAsync(ws, 0, need, c->stream) != hipSuccess) return LST_E_HIP;
   return LST_OK;
 }
 
@@ -270,28 +293,10 @@ void prof(lst_ctx *c, int phase, bool begin) {
   g_prof.stop = ev[2 * (size_t)used + 1];
 }
 
-void graph_entry_free(GraphEntry &g) {
-  hipGraphExec_t ex[3] = {g.exec_a, g.exec_side, g.exec_b};
-  for (hipGraphExec_t e : ex)
-    if (e) (void)hipGraphExecDestroy(e);
-}
-
-int side_create(lst_ctx *c) {
-  for (int i = 0; i < 1; ++i)
-    if (hipStreamCreateWithFlags(&c->side[i], hipStreamNonBlocking) != hipSuccess) return LST_E_HIP;
-  if (hipStreamCreateWithFlags(&c->cap, hipStreamNonBlocking) != hipSuccess) return LST_E_HIP;
-  c->have_side = true;
-  return LST_OK;
-}
-
-void side_free(lst_ctx *c) {
-  if (!c->have_side) return;
-  for (int i = 0; i < 1; ++i)
-    if (c->side[i]) (void)hipStreamDestroy(c->side[i]);
-  if (c->cap) (void)hipStreamDestroy(c->cap);
-  for (GraphEntry &g : c->graphs) graph_entry_free(g);
+void graphs_free(lst_ctx *c) {
+  for (GraphEntry &g : c->graphs)
+    if (g.exec) (void)hipGraphExecDestroy(g.exec);
   c->graphs.clear();
-  c->have_side = false;
 }
 
 void prof_free(lst_ctx *c) {
@@ -338,6 +343,24 @@ bool invert_host(std::vector<double> &a, int n, std::vector<double> &inv) {
   return true;
 }
 
+lst_ctx *new_ctx(int kind, int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss,
+                 float eps, void *stream) {
+  lst_ctx *c = new (std::nothrow) lst_ctx{};
+  if (!c) return nullptr;
+  c->kind = kind;
+  c->D = D;
+  c->d = d;
+  c->m_max = m_max;
+  c->K_max = K_max;
+  c->loss = loss;
+  c->eps = eps;
+  c->stream = static_cast<hipStream_t>(stream);
+  c->last_err = hipSuccess;
+  c->online = loss == LST_LOSS_SQUARED;
+  c->spin_limit = kDefaultSpin;
+  return c;
+}
+
 }  // namespace
 
 extern "C" {
@@ -357,41 +380,51 @@ const char *lst_status_string(int status) {
   }
 }
 
+size_t lst_workspace_bytes(int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss) {
+  if (common_args(D, d, m_max, K_max, loss, 1.f) != LST_OK) return 0;
+  return ws_size(KIND_FACTORED, D, d, m_max, K_max, loss);
+}
+
+size_t lst_naive_workspace_bytes(int64_t D, int32_t d, int32_t m_max, int32_t K_max,
+                                 int32_t loss) {
+  if (common_args(D, d, m_max, K_max, loss, 1.f) != LST_OK) return 0;
+  return ws_size(KIND_NAIVE, D, d, m_max, K_max, loss);
+}
+
 int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss,
                float eps, float *V, int64_t ldv, float *U, float *UinvT, float *Q, int32_t ldd,
-               void *stream) {
+               void *workspace, size_t ws_bytes, void *stream) {
   if (!out) return LST_E_ARG;
   *out = nullptr;
   int st = common_args(D, d, m_max, K_max, loss, eps);
   if (st != LST_OK) return st;
   if (!V || !U || !UinvT || !Q) return LST_E_ARG;
   if (ldv < d || ldd < d) return LST_E_SHAPE;
-  lst_ctx *c = new (std::nothrow) lst_ctx{};
+  lst_ctx *c = new_ctx(KIND_FACTORED, D, d, m_max, K_max, loss, eps, stream);
   if (!c) return LST_E_ARG;
-  c->kind = KIND_FACTORED;
-  c->D = D;
-  c->d = d;
-  c->m_max = m_max;
-  c->K_max = K_max;
-  c->loss = loss;
-  c->eps = eps;
-  c->stream = static_cast<hipStream_t>(stream);
   c->V = V;
   c->ldv = ldv;
   c->U = U;
   c->UinvT = UinvT;
   c->Q = Q;
   c->ldd = ldd;
-  c->last_err = hipSuccess;
-  c->use_graphs = false;
-  c->withhold_release = std::getenv("LST_TEST_WITHHOLD_WOODBURY_RELEASE") != nullptr;
-  c->one_stream = std::getenv("LST_ONE_STREAM") != nullptr;
-  {
-    const char *ok = std::getenv("LST_ONLINE_KERNEL");
-    c->online = loss == LST_LOSS_SQUARED && !(ok && std::strcmp(ok, "0") == 0);
+  st = take_ws(c, workspace, ws_bytes, carve_factored);
+  if (st == LST_OK) {
+    StepBufs &b = c->sb;
+    b.D = D;
+    b.d = d;
+    b.ldd = ldd;
+    b.loss = loss;
+    b.eps = eps;
+    b.V = V;
+    b.ldv = ldv;
+    b.U = U;
+    b.UinvT = UinvT;
+    b.Q = Q;
+    c->plans.reserve(kPlanCap);
+    if (hipStreamCreateWithFlags(&c->cap, hipStreamNonBlocking) != hipSuccess) st = LST_E_HIP;
+    else c->have_cap = true;
   }
-  st = alloc_ws(c, carve_factored);
-  if (st == LST_OK) st = side_create(c);
   if (st != LST_OK) {
     lst_destroy(c);
     return st;
@@ -401,27 +434,19 @@ int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max
 }
 
 int lst_naive_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max,
-                     int32_t loss, float eps, float *W, int64_t ldw, void *stream) {
+                     int32_t loss, float eps, float *W, int64_t ldw, void *workspace,
+                     size_t ws_bytes, void *stream) {
   if (!out) return LST_E_ARG;
   *out = nullptr;
   int st = common_args(D, d, m_max, K_max, loss, eps);
   if (st != LST_OK) return st;
   if (!W) return LST_E_ARG;
   if (ldw < d) return LST_E_SHAPE;
-  lst_ctx *c = new (std::nothrow) lst_ctx{};
+  lst_ctx *c = new_ctx(KIND_NAIVE, D, d, m_max, K_max, loss, eps, stream);
   if (!c) return LST_E_ARG;
-  c->kind = KIND_NAIVE;
-  c->D = D;
-  c->d = d;
-  c->m_max = m_max;
-  c->K_max = K_max;
-  c->loss = loss;
-  c->eps = eps;
-  c->stream = static_cast<hipStream_t>(stream);
   c->W = W;
   c->ldw = ldw;
-  c->last_err = hipSuccess;
-  st = alloc_ws(c, carve_naive);
+  st = take_ws(c, workspace, ws_bytes, carve_naive);
   if (st != LST_OK) {
     lst_destroy(c);
     return st;
@@ -432,15 +457,28 @@ int lst_naive_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t
 
 void lst_destroy(lst_ctx *c) {
   if (!c) return;
-  if (c->ws) {
-    (void)hipStreamSynchronize(c->stream);
-    (void)hipFree(c->ws);
-  }
-  if (c->have_side)
-    for (int i = 0; i < 1; ++i) (void)hipStreamSynchronize(c->side[i]);
-  side_free(c);
+  if (c->ws) (void)hipStreamSynchronize(c->stream);
+  graphs_free(c);
+  if (c->have_cap) (void)hipStreamDestroy(c->cap);
   prof_free(c);
   delete c;
+}
+
+int lst_set_option(lst_ctx *c, int32_t option, int64_t value) {
+  if (!c) return LST_E_ARG;
+  switch (option) {
+    case LST_OPT_ONLINE_KERNEL:
+      if (c->kind != KIND_FACTORED) return LST_E_STATE;
+      if (value != 0 && value != 1) return LST_E_ARG;
+      c->online = value == 1 && c->loss == LST_LOSS_SQUARED;
+      return LST_OK;
+    case LST_OPT_SPIN_LIMIT:
+      if (value < 0 || value > (int64_t)1 << 30) return LST_E_ARG;
+      c->spin_limit = (int)value;
+      return LST_OK;
+    default:
+      return LST_E_ARG;
+  }
 }
 
 int lst_profile_enable(lst_ctx *c, int32_t on) {
@@ -472,9 +510,6 @@ int lst_profile_read(lst_ctx *c, int32_t *counts, double *ms, int32_t n) {
 int lst_sync_status(lst_ctx *c) {
   if (!c) return LST_E_ARG;
   if (hipStreamSynchronize(c->stream) != hipSuccess) return LST_E_HIP;
-  if (c->have_side)
-    for (int i = 0; i < 1; ++i)
-      if (hipStreamSynchronize(c->side[i]) != hipSuccess) return LST_E_HIP;
   if (c->last_err != hipSuccess) {
     c->last_err = hipSuccess;
     return LST_E_HIP;
@@ -490,7 +525,7 @@ int lst_sync_status(lst_ctx *c) {
   if (f & FLAG_NONFINITE) return LST_E_NONFINITE;
   if (f & FLAG_NOT_SPD) return LST_E_NOT_SPD;
   if (f & FLAG_SYNC) {
-    // Both streams are idle: restart the progress counters from a consistent state.
+    // The stream is idle: restart the online step's barrier counter and decision word.
     if (c->cnt && hipMemset(c->cnt, 0, 4 * sizeof(int)) != hipSuccess) return LST_E_HIP;
     return LST_E_SYNC;
   }
@@ -533,14 +568,22 @@ int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0
         record(c, launch_identity(s, c->UinvT, d, c->ldd)))
       return LST_E_HIP;
   }
-  // Q = U^T (V^T V) U  (Q = V^T V when U = I), V^T V split over D.
+  // Q = U^T (V^T V) U  (Q = V^T V when U = I), V^T V split over D into the workspace's
+  // partial sums (as many splits as they hold).
   GemmDesc g = gemm_desc(d, d, (int)c->D, c->V, c->ldv, 1, c->V, c->ldv, 1, nullptr, d);
-  const size_t pf = gemm_plan_split(g, kTargetWGs, nullptr);
-  float *tmp = nullptr;
-  const size_t tmp_floats = pf + 2 * (size_t)d * d + 64;
-  if (record(c, hipMalloc(&tmp, tmp_floats * sizeof(float)))) return LST_E_HIP;
-  float *part = tmp, *Gm = tmp + ((pf + 63) / 64) * 64, *Tm = Gm + (size_t)d * d;
-  gemm_plan_split(g, kTargetWGs, part);
+  if (gemm_plan_split(g, kTargetWGs, c->initpart) > c->initpart_floats) {
+    const int fit = (int)(c->initpart_floats / ((size_t)d * d));
+    if (fit >= 2) {
+      int chunk = (int)((c->D + fit - 1) / fit);
+      chunk = (chunk + 7) / 8 * 8;
+      g.kchunk = chunk;
+      g.splits = (int)((c->D + chunk - 1) / chunk);
+    } else {
+      g.splits = 1;
+      g.kchunk = (int)c->D;
+      g.partial = nullptr;
+    }
+  }
   GemmBatch b{};
   int st = LST_OK;
   if (!U0) {
@@ -550,6 +593,7 @@ int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0
     b.n = 1;
     if (record(c, gemm_launch(b, nullptr, s))) st = LST_E_HIP;
   } else {
+    float *Gm = c->Sd0, *Tm = c->Sd1;
     g.C = Gm;
     g.ldc = d;
     b.d[0] = g;
@@ -566,7 +610,6 @@ int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0
   }
   const int zero = 0;
   if (record(c, hipStreamSynchronize(s))) st = LST_E_HIP;
-  (void)hipFree(tmp);
   if (record(c, hipMemcpy(c->flag, &zero, sizeof(int), hipMemcpyHostToDevice))) st = LST_E_HIP;
   return st;
 }
@@ -575,101 +618,28 @@ int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0
 
 namespace {
 
-// Enqueues one factored step on stream s (and the context's side streams).
-void gemm_run(GemmBatch &b, const int *gate, hipStream_t s, int phase = GEMM_OTHER) {
-  gemm_prepare(b);
-  gemm_enqueue(b, gate, s, phase);
-}
-
-// The step's GEMM batches for minibatch size m, with H and grad_H as placeholders.
-void build_plan(const lst_ctx *c, int m, GemmBatch (&b)[kPlanBatches]) {
-  const int d = c->d, ldd = c->ldd;
-  const float *H = sym_H();
-  float *gH = sym_gradH();
-  for (GemmBatch &x : b) x = GemmBatch{};
-  // N = H^T H (Woodbury branch)
-  b[0].d[0] = gemm_desc(m, m, d, H, d, 0, H, d, 0, c->N, m);
-  b[0].n = 1;
-  // H^ = Q H, H~ = U H, X = U^{-T} H (Algorithm 3 steps 1, 5, 6; Algorithm 4 rows 1, 5)
-  b[1].d[0] = gemm_desc(m, d, d, H, d, 0, c->Q, ldd, 0, c->Hhat, d);
-  b[1].d[1] = gemm_desc(m, d, d, H, d, 0, c->U, ldd, 0, c->Htil, d);
-  b[1].d[2] = gemm_desc(m, d, d, H, d, 0, c->UinvT, ldd, 0, c->X, d);
-  b[1].n = 3;
-  // Z^ = U^T G with grad_H = 2 H^ diag(dl/dq) + Z^; M^ = H^T H^; H^T Z^ = H~^T G
-  GemmDesc z = gemm_desc(m, d, d, c->G, d, 0, c->U, ldd, 1, c->Zhat, d);
-  z.epi = EPI_GRADH;
-  z.rs = c->dq;
-  z.E = c->Hhat;
-  z.lde = d;
-  z.C2 = gH;
-  z.ldc2 = d;
-  b[2].d[0] = z;
-  b[2].d[1] = gemm_desc(m, m, d, H, d, 0, c->Hhat, d, 0, c->Mhat, m);
-  b[2].d[2] = gemm_desc(m, m, d, c->Htil, d, 0, c->G, d, 0, c->HZ, m);
-  b[2].n = 3;
-  // Yw = R X; Zq = (eta^2/2) M H - eta grad_H; U <- U - 2 eta H~ diag(dl/dq) H^T
-  // (eq. updateU / gen-updateU).  Zq's alpha and beta scale with eta at launch.
-  b[3].d[0] = gemm_desc(m, d, m, c->R, m, 0, c->X, d, 1, c->Yw, d);
-  GemmDesc zq = gemm_desc(m, d, m, c->M, m, 0, H, d, 1, c->Zq, d, 0.5f, gH, d, -1.f);
-  zq.lr_scaled = 1;
-  b[3].d[1] = zq;
-  b[3].d[2] = gemm_desc(d, d, m, c->Atil, d, 1, H, d, 1, c->U, ldd, -1.f, c->U, ldd, 1.f);
-  b[3].n = 3;
-  // U^{-T} += (2 eta X S C^{-1} S) H^T (Woodbury); Q += H Zq^T + Zq H^T (eq. updateQ /
-  // gen-Qnew); P = U_new^{-T} H = X + (2 eta X S C^{-1} S)(H^T H).
-  b[4].d[0] = gemm_desc(d, d, m, c->Yw, d, 1, H, d, 1, c->UinvT, ldd, 1.f, c->UinvT, ldd, 1.f);
-  GemmDesc qd = gemm_desc(d, d, m, H, d, 1, c->Zq, d, 1, c->Q, ldd, 1.f, c->Q, ldd, 1.f);
-  qd.A2 = c->Zq;
-  qd.lda2 = d;
-  qd.B2 = H;
-  qd.ldb2 = d;
-  qd.K2 = m;
-  b[4].d[1] = qd;
-  // P is needed for the spherical softmax only: for squared error S = I, and with
-  // 2 eta N = I - C one has I + N R = I + (I - C) C^{-1} = C^{-1}, so P = C^{-1} X
-  // = Yw / (2 eta) and the V update (eq. updateV) uses Yw with the factor 1/2.
-  b[4].d[2] = gemm_desc(m, d, m, c->N, m, 0, c->Yw, d, 1, c->P, d, 1.f, c->X, d, 1.f);
-  b[4].n = c->loss == LST_LOSS_SQUARED ? 2 : 3;
-  // 16 x 16 tiles where the outputs are m x m or m x d with long k (Gram product,
-  // contractions, Z^): four times the workgroups of 32 x 32 tiles.  The d x d
-  // updates (short k = m, read-modify-write of the state) keep 32 x 32 tiles.
-  for (int i = 0; i < kPlanBatches; ++i) {
-    b[i].t16 = i <= 2 ? 1 : 0;
-    gemm_prepare(b[i]);
-  }
-  // The contraction launch also reads the step's target rows of V into the caches
-  // (one workgroup per example, on the XCD of that example's gather workgroup).
-  b[1].pf_V = c->V;
-  b[1].pf_D = c->D;
-  b[1].pf_ldv = c->ldv;
-  b[1].pf_d = d;
-  b[1].pf_m = m;
-  b[1].pf_base = (b[1].total_tiles + 7) / 8 * 8;
-}
-
-// The plan for m, built and copied to its device slot on first use.  Replacing
-// the least recently used plan first drains the streams and drops the recorded
-// graphs that launch it.
+// The plan for m, built and copied to its device slot on first use (an ordered copy
+// on the context's stream).  Replacing the least recently used plan first drains the
+// stream and drops the recorded graphs that launch it.
 PlanEntry *get_plan(lst_ctx *c, int m) {
   for (PlanEntry &e : c->plans)
     if (e.m == m) {
       e.last_use = ++c->plan_tick;
       return &e;
     }
-  GemmBatch *slot;
+  StepPlan *slot;
   if (c->plans.size() < kPlanCap) {
-    slot = c->plan_pool + c->plans.size() * kPlanBatches;
+    slot = c->plan_pool + c->plans.size();
     c->plans.push_back(PlanEntry{});
   } else {
     size_t v = 0;
     for (size_t i = 1; i < c->plans.size(); ++i)
       if (c->plans[i].last_use < c->plans[v].last_use) v = i;
-    if (record(c, hipStreamSynchronize(c->stream)) || record(c, hipStreamSynchronize(c->side[0])))
-      return nullptr;
+    if (record(c, hipStreamSynchronize(c->stream))) return nullptr;
     const int old_m = c->plans[v].m;
     for (size_t i = c->graphs.size(); i-- > 0;)
       if (c->graphs[i].m == old_m) {
-        graph_entry_free(c->graphs[i]);
+        (void)hipGraphExecDestroy(c->graphs[i].exec);
         c->graphs.erase(c->graphs.begin() + i);
       }
     slot = c->plans[v].dev;
@@ -679,8 +649,14 @@ PlanEntry *get_plan(lst_ctx *c, int m) {
   PlanEntry &e = c->plans.back();
   e.m = m;
   e.dev = slot;
-  build_plan(c, m, e.b);
-  if (record(c, hipMemcpy(e.dev, e.b, sizeof(e.b), hipMemcpyHostToDevice))) {
+  e.host.reset(new (std::nothrow) StepPlan);
+  if (!e.host) {
+    c->plans.pop_back();
+    return nullptr;
+  }
+  build_step_plan(c->sb, m, *e.host);
+  if (record(c, hipMemcpyAsync(e.dev, e.host.get(), sizeof(StepPlan), hipMemcpyHostToDevice,
+                               c->stream))) {
     c->plans.pop_back();
     return nullptr;
   }
@@ -688,163 +664,28 @@ PlanEntry *get_plan(lst_ctx *c, int m) {
   return &e;
 }
 
-// A step runs on two streams ordered by the progress counters c->cnt (no host
-// events): the main stream signals when its contraction launch starts (the
-// step's inputs are ready and the previous step has consumed N and R); the side
-// stream then forms N = H^T H and the Woodbury inverse and releases R; the main
-// stream waits for that before the state updates.  Each wait is a kernel of one
-// workgroup (many polling workgroups slow the step down).
-// The parts are launched in the order main (to M), side, main (updates), so that
-// every wait's producer is launched before it even where the two streams share
-// a hardware queue.
+constexpr int kStepPhase[5] = {LST_PHASE_CONTRACT, LST_PHASE_GATHER, LST_PHASE_ZGRAD,
+                               LST_PHASE_MID, LST_PHASE_UPDATE};
 
-// Main stream up to M: contractions, gather and loss epilogue, Z^ and grad_H, M.
-int enqueue_main_a(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *H, int32_t m,
-                   const int32_t *idx, const float *val, int32_t K, float lr, float *loss_dev,
-                   float *gH) {
-  const bool unit_dq = (c->loss == LST_LOSS_SQUARED);
-  auto gemm = [&](int i, int phase, int *sig) {
-    StepSync sy;
-    sy.sig = sig;
-    gemm_enqueue_plan(pl.b[i], pl.dev + i, H, gH, lr, nullptr, s, phase, i == 1 ? idx : nullptr,
-                      K, sy);
-  };
-  prof(c, LST_PHASE_CONTRACT, true);
-  gemm(1, GEMM_CONTRACT, c->cnt + 0);
-  prof(c, LST_PHASE_CONTRACT, false);
-
-  // Sparse gather of the K target rows of the pre-update V and the loss epilogue.
-  prof(c, LST_PHASE_GATHER, true);
-  launch_gather(s, m, K, c->d, c->D, H, c->Hhat, c->Htil, idx, val, c->V, c->ldv, c->loss, c->eps,
-                lr, c->G, c->Atil, c->dq, c->dA, c->lvec, c->flag);
-  prof(c, LST_PHASE_GATHER, false);
-
-  // Z^ and grad_H; its start tells the spherical softmax's Woodbury branch that
-  // dl/dq is ready.
-  prof(c, LST_PHASE_ZGRAD, true);
-  gemm(2, GEMM_ZGRAD, unit_dq ? nullptr : c->cnt + 2);
-  prof(c, LST_PHASE_ZGRAD, false);
-
-  // Loss and M; sets the error flag on a non-finite loss.
-  prof(c, LST_PHASE_MBLOCK, true);
-  launch_mblock(s, m, K, idx, c->lvec, c->dq, c->dA, c->Mhat, c->HZ, c->M, loss_dev, c->flag);
-  prof(c, LST_PHASE_MBLOCK, false);
-  return record(c, hipGetLastError()) ? LST_E_HIP : LST_OK;
-}
-
-// Side stream: N = H^T H, then C = I - 2 eta S N S and R = 2 eta S C^{-1} S (for
-// m > d, through the d x d inverse of I - 2 eta (SH)^T (SH): the m >= d variant the
-// paper suggests after Algorithm 3, here as the same Woodbury R).  For squared error
-// dl/dq = 1; the spherical softmax waits for the gather's dl/dq = T / (q + D eps).
-int enqueue_side(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *H, int32_t m,
-                 float lr, float *gH) {
-  const bool unit_dq = (c->loss == LST_LOSS_SQUARED);
-  StepSync started;  // the main stream has reached this step's contraction
-  started.wx = c->cnt + 0;
-  started.wy = c->cnt + 1;
-  started.wd = 1;
-  started.flag = c->flag;
-  launch_step_sync(s, started, nullptr);
-  prof(c, LST_PHASE_GRAM, true);
-  gemm_enqueue_plan(pl.b[0], pl.dev + 0, H, gH, lr, nullptr, s, GEMM_OTHER);
-  prof(c, LST_PHASE_GRAM, false);
-  StepSync gathered;
-  if (!unit_dq) {
-    gathered.wx = c->cnt + 2;
-    gathered.wy = c->cnt + 1;
-    gathered.wd = 1;
-    gathered.flag = c->flag;
+// The five launches of a factored step on stream s.
+int enqueue_factored_step(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const StepArgs &a) {
+  for (int l = 0; l < 5; ++l) {
+    prof(c, kStepPhase[l], true);
+    enqueue_step_launch(l, c->sb, *pl.host, pl.dev, a, s);
+    prof(c, kStepPhase[l], false);
   }
-  prof(c, LST_PHASE_WOODBURY, true);
-  int *done = c->withhold_release ? nullptr : c->cnt + 1;
-  const int d = c->d;
-  if (m > kWoodburyOneWG && d < m) {
-    // m > d: the d x d inverse of B = I - 2 eta Hs^T Hs instead of the m x m one (see
-    // push_through_r_kernel): R' = 2 eta B^{-1} into Sd0, then R = 2 eta S (I + Hs R' Hs^T) S.
-    const float *Hs = H;
-    if (!unit_dq) {
-      launch_step_sync(s, gathered, nullptr);
-      launch_scale_rows_sqrt(s, m, d, H, c->dq, c->P, c->flag);
-      Hs = c->P;
-    }
-    GemmBatch b{};
-    b.d[0] = gemm_desc(d, d, m, Hs, d, 1, Hs, d, 1, c->Sd1, d);  // Hs^T Hs
-    b.n = 1;
-    gemm_run(b, nullptr, s);
-    launch_woodbury(s, d, lr, 1, c->dq, c->Sd1, c->Sd0, c->Cwork, c->Pbig, c->Cp, c->Rp, c->flag,
-                    StepSync{}, nullptr);
-    b = GemmBatch{};
-    b.d[0] = gemm_desc(m, d, d, Hs, d, 0, c->Sd0, d, 1, c->Zq, d);  // T = Hs R'
-    b.n = 1;
-    gemm_run(b, nullptr, s);
-    b = GemmBatch{};
-    b.d[0] = gemm_desc(m, m, d, c->Zq, d, 0, Hs, d, 0, c->R, m);  // R0 = T Hs^T
-    b.n = 1;
-    gemm_run(b, nullptr, s);
-    launch_push_through_r(s, m, lr, unit_dq ? 1 : 0, c->dq, c->R);
-    if (done) launch_step_sync(s, StepSync{}, done);
-  } else {
-    launch_woodbury(s, m, lr, unit_dq ? 1 : 0, c->dq, c->N, c->R, c->Cwork, c->Pbig, c->Cp, c->Rp,
-                    c->flag, gathered, done);
-  }
-  prof(c, LST_PHASE_WOODBURY, false);
+  // launch errors are not checked one by one: one stays pending and is reported here
   return record(c, hipGetLastError()) ? LST_E_HIP : LST_OK;
-}
-
-// Main stream: the gated state updates (see build_plan) once the side stream has
-// released this step's R (and its error flag), then the scatter into V.
-int enqueue_main_b(lst_ctx *c, hipStream_t s, const PlanEntry &pl, const float *H, int32_t m,
-                   const int32_t *idx, int32_t K, float lr, float *gH) {
-  StepSync joined;
-  joined.wx = c->cnt + 1;
-  joined.wy = c->cnt + 0;
-  joined.wd = 0;
-  joined.flag = c->flag;
-  launch_step_sync(s, joined, nullptr);
-  prof(c, LST_PHASE_MID, true);
-  gemm_enqueue_plan(pl.b[3], pl.dev + 3, H, gH, lr, c->flag, s, GEMM_MID);
-  prof(c, LST_PHASE_MID, false);
-  // V_r -= eta sum dl/dA P_j over the slots of each distinct target row (eq. updateV).
-  // For squared error eta P = Yw / 2 (see build_plan): the scatter needs nothing
-  // from the update launch and runs in it; the spherical softmax's P comes from it.
-  const bool squared = c->loss == LST_LOSS_SQUARED;
-  prof(c, LST_PHASE_UPDATE, true);
-  const bool fused =
-      squared && m * K > 0 &&
-      gemm_enqueue_plan_scatter(pl.b[4], pl.dev + 4, H, gH, lr, c->flag, s, m * K, K, c->d, 0.5f,
-                                idx, c->dA, c->Yw, c->V, c->ldv);
-  if (!fused) gemm_enqueue_plan(pl.b[4], pl.dev + 4, H, gH, lr, c->flag, s, GEMM_UPDATE);
-  prof(c, LST_PHASE_UPDATE, false);
-  if (!fused) {
-    prof(c, LST_PHASE_SCATTER, true);
-    launch_scatter(s, m, K, c->d, squared ? 0.5f : lr, idx, c->dA, squared ? c->Yw : c->P, c->V,
-                   c->ldv, c->flag);
-    prof(c, LST_PHASE_SCATTER, false);
-  }
-  // Kernel launches above are not checked one by one: a launch error stays pending
-  // and is reported here.
-  return record(c, hipGetLastError()) ? LST_E_HIP : LST_OK;
-}
-
-int enqueue_factored_step(lst_ctx *c, const PlanEntry &pl, const float *H, int32_t m,
-                          const int32_t *idx, const float *val, int32_t K, float lr,
-                          float *loss_dev, float *grad_H) {
-  float *gH = grad_H ? grad_H : c->gradH;
-  int st = enqueue_main_a(c, c->stream, pl, H, m, idx, val, K, lr, loss_dev, gH);
-  if (st == LST_OK) st = enqueue_side(c, c->one_stream ? c->stream : c->side[0], pl, H, m, lr, gH);
-  if (st == LST_OK) st = enqueue_main_b(c, c->stream, pl, H, m, idx, K, lr, gH);
-  return st;
 }
 
 // Replays (capturing first if needed) the graph of a step with these arguments.
-int graph_step(lst_ctx *c, const PlanEntry &pl, const float *H, int32_t m, const int32_t *idx,
-               const float *val, int32_t K, float lr, float *loss_dev, float *grad_H) {
+int graph_step(lst_ctx *c, const PlanEntry &pl, const StepArgs &a, const float *grad_arg) {
   uint32_t lr_bits;
-  std::memcpy(&lr_bits, &lr, sizeof(lr_bits));
+  std::memcpy(&lr_bits, &a.lr, sizeof(lr_bits));
   GraphEntry *hit = nullptr;
   for (GraphEntry &g : c->graphs)
-    if (g.H == H && g.idx == idx && g.val == val && g.loss == loss_dev && g.grad == grad_H &&
-        g.m == m && g.K == K && g.lr_bits == lr_bits) {
+    if (g.H == a.H && g.idx == a.idx && g.val == a.val && g.loss == a.loss &&
+        g.grad == grad_arg && g.m == a.m && g.K == a.K && g.lr_bits == lr_bits) {
       hit = &g;
       break;
     }
@@ -853,47 +694,30 @@ int graph_step(lst_ctx *c, const PlanEntry &pl, const float *H, int32_t m, const
       size_t v = 0;
       for (size_t i = 1; i < c->graphs.size(); ++i)
         if (c->graphs[i].last_use < c->graphs[v].last_use) v = i;
-      if (record(c, hipStreamSynchronize(c->stream)) || record(c, hipStreamSynchronize(c->side[0])))
-        return LST_E_HIP;
-      graph_entry_free(c->graphs[v]);
+      if (record(c, hipStreamSynchronize(c->stream))) return LST_E_HIP;
+      (void)hipGraphExecDestroy(c->graphs[v].exec);
       c->graphs.erase(c->graphs.begin() + v);
     }
-    float *gH = grad_H ? grad_H : c->gradH;
-    // The step's three parts are captured one after the other on the capture stream.
-    auto capture = [&](int part, hipGraphExec_t *exec) -> int {
-      if (record(c, hipStreamBeginCapture(c->cap, hipStreamCaptureModeThreadLocal)))
-        return LST_E_HIP;
-      const int st =
-          part == 0   ? enqueue_main_a(c, c->cap, pl, H, m, idx, val, K, lr, loss_dev, gH)
-          : part == 1 ? enqueue_side(c, c->cap, pl, H, m, lr, gH)
-                      : enqueue_main_b(c, c->cap, pl, H, m, idx, K, lr, gH);
-      hipGraph_t graph = nullptr;
-      const hipError_t ec = hipStreamEndCapture(c->cap, &graph);
-      if (st != LST_OK || ec != hipSuccess || !graph) {
-        if (graph) (void)hipGraphDestroy(graph);
-        if (ec != hipSuccess) c->last_err = ec;
-        return st != LST_OK ? st : LST_E_HIP;
-      }
-      const hipError_t ei = hipGraphInstantiate(exec, graph, nullptr, nullptr, 0);
-      (void)hipGraphDestroy(graph);
-      return record(c, ei) ? LST_E_HIP : LST_OK;
-    };
-    GraphEntry e{H, idx, val, loss_dev, grad_H, m, K, lr_bits, nullptr, nullptr, nullptr, 0};
-    int st = capture(0, &e.exec_a);
-    if (st == LST_OK) st = capture(1, &e.exec_side);
-    if (st == LST_OK) st = capture(2, &e.exec_b);
-    if (st != LST_OK) {
-      graph_entry_free(e);
-      return st;
+    if (record(c, hipStreamBeginCapture(c->cap, hipStreamCaptureModeThreadLocal)))
+      return LST_E_HIP;
+    const int st = enqueue_factored_step(c, c->cap, pl, a);
+    hipGraph_t graph = nullptr;
+    const hipError_t ec = hipStreamEndCapture(c->cap, &graph);
+    if (st != LST_OK || ec != hipSuccess || !graph) {
+      if (graph) (void)hipGraphDestroy(graph);
+      if (ec != hipSuccess) c->last_err = ec;
+      return st != LST_OK ? st : LST_E_HIP;
     }
+    GraphEntry e{a.H, a.idx, a.val, a.loss, const_cast<float *>(grad_arg), a.m, a.K, lr_bits,
+                 nullptr, 0};
+    const hipError_t ei = hipGraphInstantiate(&e.exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    if (record(c, ei)) return LST_E_HIP;
     c->graphs.push_back(e);
     hit = &c->graphs.back();
   }
   hit->last_use = ++c->graph_tick;
-  if (record(c, hipGraphLaunch(hit->exec_a, c->stream)) ||
-      record(c, hipGraphLaunch(hit->exec_side, c->one_stream ? c->stream : c->side[0])))
-    return LST_E_HIP;
-  return record(c, hipGraphLaunch(hit->exec_b, c->stream));
+  return record(c, hipGraphLaunch(hit->exec, c->stream));
 }
 
 }  // namespace
@@ -914,14 +738,15 @@ int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const fl
     prof(c, LST_PHASE_ONLINE, true);
     const hipError_t e = launch_online_step(
         c->stream, c->D, c->d, K, H, idx, val, lr, c->V, c->ldv, c->U, c->UinvT, c->Q, c->ldd,
-        loss_dev, grad_H, c->spart, reinterpret_cast<unsigned *>(c->cnt + 3), c->flag);
+        loss_dev, grad_H, c->spart, reinterpret_cast<unsigned *>(c->cnt), c->spin_limit, c->flag);
     prof(c, LST_PHASE_ONLINE, false);
     return record(c, e);
   }
   const PlanEntry *pl = get_plan(c, m);
   if (!pl) return LST_E_HIP;
-  if (graphs) return graph_step(c, *pl, H, m, idx, val, K, lr, loss_dev, grad_H);
-  return enqueue_factored_step(c, *pl, H, m, idx, val, K, lr, loss_dev, grad_H);
+  StepArgs a{H, m, idx, val, K, lr, loss_dev, grad_H ? grad_H : c->gradH};
+  if (graphs) return graph_step(c, *pl, a, grad_H);
+  return enqueue_factored_step(c, c->stream, *pl, a);
 }
 
 int lst_use_graphs(lst_ctx *c, int32_t on) {
@@ -975,10 +800,10 @@ int lst_naive_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, co
   // The loss and dl/dq, dl/da from the explicit O.
   prof(c, LST_PHASE_NAIVE_LOSS, true);
   if (record(c, launch_naive_epilogue(s, m, K, D, nparts, c->colpart, c->O, idx, val, c->loss,
-                                      c->eps, c->dq, c->dA, c->lvec, c->flag)))
+                                      c->eps, c->sb.dq, c->sb.dA, c->sb.lvec, c->flag)))
     return LST_E_HIP;
   // grad_O = 2 O diag(dl/dq) + Yring, in place over O.
-  if (record(c, launch_grad_o(s, c->O, D, m, K, c->dq, idx, c->dA, c->lvec, loss_dev, c->flag)))
+  if (record(c, launch_grad_o(s, c->O, D, m, K, c->sb.dq, idx, c->sb.dA, c->sb.lvec, loss_dev, c->flag)))
     return LST_E_HIP;
   prof(c, LST_PHASE_NAIVE_LOSS, false);
   // grad_H = grad_O^T W (split over D), then W <- W - eta grad_O H.

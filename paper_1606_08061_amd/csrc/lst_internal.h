@@ -35,54 +35,6 @@ extern thread_local ProfHook g_prof;
 enum : int { FLAG_INDEX = 1, FLAG_NOT_SPD = 2, FLAG_NONFINITE = 4, FLAG_SYNC = 8 };
 
 // ---------------------------------------------------------------------------
-// Ordering between the step's two streams without host events: monotone
-// progress counters in device memory.  A kernel given a StepSync adds 1 to
-// *sig from its workgroup 0 on entry ("every kernel before me on my stream has
-// completed") and, if wx is set, waits until *wx - *wy >= wd (thread 0 polls,
-// then the workgroup acquires).  Waits are placed in single-workgroup kernels
-// only.  A producer publishes its results with release_count at its end.
-// The wait is bounded (a few tenths of a second); when it expires it sets
-// FLAG_SYNC, which also closes the gated state updates, and the kernel goes on,
-// so no wave waits forever.
-// ---------------------------------------------------------------------------
-struct StepSync {
-  const int *wx = nullptr, *wy = nullptr;
-  int wd = 0;
-  int *sig = nullptr;
-  int *flag = nullptr;
-};
-
-constexpr int kSyncSpinLimit = 1 << 18;
-
-__device__ inline void step_sync_begin(const StepSync &s) {
-  if (s.sig && blockIdx.x == 0 && threadIdx.x == 0)
-    __hip_atomic_fetch_add(s.sig, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-  if (!s.wx) return;
-  if (threadIdx.x == 0) {
-    // relaxed polls (coherent loads, no cache invalidation per poll), one acquire after
-    for (int it = 0;; ++it) {
-      const int x = __hip_atomic_load(s.wx, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      const int y = __hip_atomic_load(s.wy, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if ((int)((unsigned)x - (unsigned)y) >= s.wd) break;
-      if (it >= kSyncSpinLimit) {
-        atomicOr(s.flag, FLAG_SYNC);
-        break;
-      }
-      __builtin_amdgcn_s_sleep(2);
-    }
-  }
-  __syncthreads();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-}
-
-// Called by every thread of the (single) producing workgroup after its last write.
-__device__ inline void release_count(int *cnt) {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
-
-// ---------------------------------------------------------------------------
 // Batched fp32 MFMA GEMM.
 //
 // One descriptor computes  C[i,j] = alpha * sum_k opA(i,k) opB(k,j) + beta * Cin[i,j]
@@ -123,7 +75,7 @@ struct GemmDesc {
 
 // Operand placeholders of plans kept in device memory: a plan is built once per
 // minibatch size m and refers to the step's H and grad_H through these values,
-// which the kernel replaces by the pointers passed at launch.
+// which the kernels replace by the pointers passed at launch.
 inline const float *sym_H() { return reinterpret_cast<const float *>(uintptr_t{16}); }
 inline float *sym_gradH() { return reinterpret_cast<float *>(uintptr_t{32}); }
 
@@ -134,27 +86,15 @@ struct GemmBatch {
   int n;
   int total_tiles;
   int wide;  // 8 wavefronts per tile (long k) instead of 4
-  int t16;   // 16 x 16 output tiles (plans): set before gemm_prepare
-  // Optional prefetch (16 x 16 plans): pf_m extra workgroups after the tiles
-  // (whose count is padded to pf_base, a multiple of 8, so that workgroup
-  // pf_base + j shares an XCD with workgroup j of the next launch) read the K
-  // target rows of example j of V (D x ldv) into the caches.
-  const float *pf_V;
-  int64_t pf_D, pf_ldv;
-  int pf_m, pf_d, pf_base;
 };
 
 GemmDesc gemm_desc(int M, int N, int K, const float *A, int64_t lda, int tA, const float *B,
                    int64_t ldb, int tB, float *C, int64_t ldc, float alpha = 1.f,
                    const float *Cin = nullptr, int64_t ldcin = 0, float beta = 0.f);
 
-// Kernel instantiations (distinct symbols per step phase for profilers).
+// Kernel instantiations (distinct symbols per phase for profilers).
 enum : int {
   GEMM_OTHER = 0,
-  GEMM_CONTRACT = 1,
-  GEMM_ZGRAD = 2,
-  GEMM_MID = 3,
-  GEMM_UPDATE = 4,
   GEMM_NAIVE_FWD = 5,
   GEMM_NAIVE_GRAD = 6,
   GEMM_NAIVE_UPDATE = 7
@@ -170,23 +110,6 @@ hipError_t gemm_launch(GemmBatch &b, const int *gate, hipStream_t s, int phase =
 int gemm_prepare(GemmBatch &b);
 void gemm_enqueue(const GemmBatch &b, const int *gate, hipStream_t s, int phase);
 
-// Launch of a prepared batch whose identical copy `dev` lives in device memory
-// (no split-k): the kernel reads its descriptors from there and takes H, grad_H
-// and lr for the placeholders, so the launch carries a few dozen bytes of
-// arguments instead of the whole batch.
-void gemm_enqueue_plan(const GemmBatch &host, const GemmBatch *dev, const float *H,
-                       float *gradH, float lr, const int *gate, hipStream_t s, int phase,
-                       const int *pf_idx = nullptr, int pf_K = 0, const StepSync &sync = {});
-
-// The same launch for a plan of 32 x 32 tiles without split-k, with n more
-// workgroups that each run one target slot of the V scatter (V_r -= slr sum
-// dl/dA P_j over the row's slots).  Returns false, launching nothing, if the
-// plan does not qualify.
-bool gemm_enqueue_plan_scatter(const GemmBatch &host, const GemmBatch *dev, const float *H,
-                               float *gradH, float lr, const int *gate, hipStream_t s, int n,
-                               int K, int d, float slr, const int *idx, const float *dA,
-                               const float *P, float *V, int64_t ldv);
-
 // Large single products on 128 x 128 tiles (the naive path).  gemm_big_ok: the
 // operands meet the kernel's alignment needs (else use gemm_launch).  gemm_big_plan
 // fills the tile counts and splits k over workgroups when the tiles are few, with
@@ -201,40 +124,121 @@ hipError_t gemm_big_launch(GemmDesc g, const int *gate, hipStream_t s, int phase
 size_t gemm_plan_split(GemmDesc &g, int target_wgs, float *partial);
 
 // ---------------------------------------------------------------------------
-// Step kernels (step_kernels.hip)
+// The factored step (fused.hip): five launches on one stream.
+//
+// Op16: one product C = post(A opB) on 16 x 16 output tiles, k = K.  A is a plain
+// operand (A(i,k) = A[i lda + k], or A[k lda + i] with tA) or, for the Q update's
+// M, assembled as it is loaded (AM_MASM: 4 dq_i M^_ik dq_k + YY_ik + 2 dq_i HZ_ik +
+// 2 dq_k HZ_ki).  opB(k,j) = sum_t coef_t scale_t(k) B_t(k,j) over up to four terms
+// (tr = 0: B_t[j ld + k]; tr = 1: B_t[k ld + j]).  Epilogue:
+//   v = alpha lr^alpha_lr rs(i) cs(j) (acc + sum_t coef_t scale_t(i) Add_t[i ld + j])
+//       + beta lr^beta_lr Cin_ij,
+// stored to C (if any), C2 = 2 rs2(i) E_ij + v (if any), and the row partial sums
+// (v Rr_ij, or |v|) of the tile's 16 columns to rowout[tile column][i].  The scale
+// modes take dl/dq (SC_DQ) or its square root (SC_SQRT) of the index; coefficient
+// indices select one of the Woodbury polynomial's c_k (-1: 1).
 // ---------------------------------------------------------------------------
-hipError_t launch_gather(hipStream_t s, int m, int K, int d, int64_t D, const float *H,
-                         const float *Hhat, const float *Htil, const int *idx, const float *val,
-                         const float *V, int64_t ldv, int loss, float eps, float lr, float *G,
-                         float *Atil, float *dq, float *dA, float *lvec, int *flag);
+enum : int { SC_NONE = 0, SC_DQ = 1, SC_SQRT = 2 };
+enum : int { RR_NONE = 0, RR_DOT = 1, RR_ABS = 2 };
+enum : int { AM_PLAIN = 0, AM_MASM = 1 };
+constexpr int kMaxTerms = 4;
+constexpr int kMaxOps = 6;
 
-// m <= kWoodburyOneWG: one workgroup.  Larger m: blocked in kBigBlock-row steps
-// through Cwork (m x m), Pbig (2 kBigBlock^2), Cp (m x kBigBlock) and Rp (kBigBlock x m).
-constexpr int kWoodburyOneWG = 128;
-constexpr int kBigBlock = 128;
-// wait: ordering before the first kernel reads dq; done: counter released after
-// R is written (also when the matrix was rejected).
-hipError_t launch_woodbury(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
-                           const float *N, float *R, float *Cwork, float *Pbig, float *Cp,
-                           float *Rp, int *flag, const StepSync &wait, int *done);
+struct OpTerm {
+  const float *p;
+  int64_t ld;
+  int tr;
+  int sc;
+  int coef;
+};
 
-// The m > d form of the branch (push-through identity): Hs = diag(dq)^(1/2) H (m x d,
-// flagging dq < 0), and R = 2 eta S (R0 + I) S in place over R0 = Hs R' Hs^T (m x m).
-hipError_t launch_scale_rows_sqrt(hipStream_t s, int m, int d, const float *H, const float *dq,
-                                  float *Hs, int *flag);
-hipError_t launch_push_through_r(hipStream_t s, int m, float lr, int unit_dq, const float *dq,
-                                 float *R);
+struct Op16 {
+  int M, N, K;
+  int tiles_m, tiles_n, tile_begin;
+  int amode;
+  const float *A;
+  int64_t lda;
+  int tA;
+  const float *Mh, *HZ, *YY;
+  int64_t ldm;
+  int nb;
+  OpTerm b[kMaxTerms];
+  int nadd;
+  OpTerm add[kMaxTerms];
+  float alpha;
+  int alpha_lr;
+  int rs, cs;
+  const float *Cin;
+  int64_t ldcin;
+  float beta;
+  int beta_lr;
+  float *C;
+  int64_t ldc;
+  float *C2;
+  int64_t ldc2;
+  const float *E;
+  int64_t lde;
+  int rs2;
+  int rowred;
+  const float *Rr;
+  int64_t ldrr;
+  float *rowout;
+  int alt;  // >= 0: the descriptor used instead when the Woodbury polynomial is not certified
+};
 
-// One workgroup: waits as `wait` says, then releases *done (if not null).
-hipError_t launch_step_sync(hipStream_t s, const StepSync &wait, int *done);
+struct OpBatch {
+  Op16 op[kMaxOps];
+  int n;       // descriptors (including alternates)
+  int n_main;  // descriptors that own tiles (the first n_main)
+  int total;   // tiles
+};
 
-hipError_t launch_mblock(hipStream_t s, int m, int K, const int *idx, const float *lvec,
-                         const float *dq, const float *dA, const float *Mhat, const float *HZ,
-                         float *M, float *loss_out, int *flag);
+// The products of one step for one minibatch size m (kept in device memory):
+// ob[l] for launches 1..4 (16 x 16 tiles), gb_mid (the U update, launch 4) and
+// gb_update (the Q and U^{-T} updates, launch 5) on 32 x 32 tiles.
+struct StepPlan {
+  OpBatch ob[4];
+  GemmBatch gb_mid, gb_update;
+};
 
-hipError_t launch_scatter(hipStream_t s, int m, int K, int d, float lr, const int *idx,
-                          const float *dA, const float *P, float *V, int64_t ldv, const int *flag);
+// The context's state and workspace pieces the step uses.
+struct StepBufs {
+  int64_t D;
+  int d, ldd, loss;
+  float eps;
+  float *V;
+  int64_t ldv;
+  float *U, *UinvT, *Q;
+  float *Hhat, *Htil, *X, *G, *Atil, *W1, *P2, *P3, *RX, *Zq;  // m x d
+  float *N, *Mhat, *HZ, *YY, *E2, *E4, *R, *Cwork;             // m x m
+  float *qpart, *bpart;  // row partials: [ceil(d/16)][m], [ceil(m/16)][m]
+  float *dq, *lvec;      // m
+  float *dA, *wA, *sval; // m x K
+  int *srow, *scnt;      // m x K, m
+  float *coef;           // 8
+  int *cert;
+  int *flag;
+};
 
+struct StepArgs {
+  const float *H;
+  int m;
+  const int *idx;
+  const float *val;
+  int K;
+  float lr;
+  float *loss;
+  float *gH;
+};
+
+void build_step_plan(const StepBufs &sb, int m, StepPlan &pl);
+// which = 0..4: launch which + 1 of the step.
+void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, const StepPlan *dev,
+                         const StepArgs &a, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Non-step kernels (step_kernels.hip)
+// ---------------------------------------------------------------------------
 hipError_t launch_identity(hipStream_t s, float *A, int d, int64_t ld);
 hipError_t launch_fill(hipStream_t s, float *p, float v);
 
@@ -267,13 +271,15 @@ hipError_t launch_input_update(hipStream_t s, float *W1, int64_t ldw, int64_t D_
 // ---------------------------------------------------------------------------
 // The online step (m = 1, squared error; Algorithm 2) as one launch
 // (online.hip).  work: online_work_floats(d) floats; bar: a grid-barrier counter
-// that starts at 0 and is reset together with the step's progress counters.
+// and its decision word (bar[0], bar[1]) that start at 0; spin_limit bounds the barrier's
+// wait (polls) before the step is abandoned.
 // ---------------------------------------------------------------------------
 size_t online_work_floats(int d);
 hipError_t launch_online_step(hipStream_t s, int64_t D, int d, int K, const float *h,
                               const int *idx, const float *val, float lr, float *V, int64_t ldv,
                               float *U, float *UinvT, float *Q, int ldd, float *loss_out,
-                              float *grad_h, float *work, unsigned *bar, int *flag);
+                              float *grad_h, float *work, unsigned *bar, int spin_limit,
+                              int *flag);
 
 // ---------------------------------------------------------------------------
 // Numerical stabilisation kernels (stabilize.hip), enqueued between steps.

@@ -22,7 +22,6 @@ namespace {
 
 constexpr int kOnlineWGs = 128;   // workgroups: 128 x 256 threads fit on the GPU at once
 constexpr int kOnlineSlices = 8;  // row slices of the y^ = U^T g partial sums
-constexpr int kBarrierSpin = 1 << 20;
 
 __device__ __forceinline__ float wave_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
@@ -41,30 +40,57 @@ __device__ __forceinline__ float get(const float *p) {
   return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Grid-wide barrier on a monotone counter (unsigned, wrapping): each launch adds
-// gridDim.x arrivals, a multiple of which 2^32 is.  The workgroup's handoff stores
-// complete (workgroup-scope release) before its arrival.  Bounded: on expiry
-// FLAG_SYNC is set and the caller writes nothing (lst_sync_status then resets the
-// counter).
-__device__ bool grid_barrier(unsigned *bar, int *flag) {
+// Grid-wide barrier with one go/abort decision per launch.
+//
+// bar[0] counts arrivals (unsigned, wrapping; each launch adds exactly gridDim.x, a
+// divisor of 2^32, since every workgroup arrives once even when late), so launch
+// number gen = ticket / gridDim.x.  bar[1] holds the decision of the latest decided
+// launch as (gen << 2) | state, state 1 = go, 2 = abort; any other content means the
+// current launch is still pending.  The last arriver moves pending to go, a waiter
+// whose bounded spin expires moves pending to abort (both by compare-and-swap, so the
+// first decision stands), and every workgroup then acts on the one decision: either
+// all of them write their part of the step, or none does.
+//
+// Ordering: every thread waits for its own hand-off stores to complete (s_waitcnt
+// vmcnt(0): agent-scope atomic stores are complete once they have reached the
+// memory side, where the other XCDs read them) before the workgroup barrier, and
+// thread 0 arrives after that barrier, so the arrival is ordered after all of the
+// workgroup's phase-A results.  Phase B reads them with agent-scope loads issued
+// after the decision was seen.
+__device__ __forceinline__ unsigned decided(unsigned w, unsigned gen) {
+  return ((w >> 2) == (gen & 0x3FFFFFFFu) && (w & 3u) != 0u) ? (w & 3u) : 0u;
+}
+
+__device__ bool grid_barrier(unsigned *bar, int spin_limit, int *flag) {
   __shared__ int ok;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (threadIdx.x == 0) {
     const unsigned ticket =
         __hip_atomic_fetch_add(bar, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const unsigned target = (ticket / gridDim.x + 1u) * gridDim.x;
-    ok = 1;
-    for (int it = 0;; ++it) {
-      const unsigned x = __hip_atomic_load(bar, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      if ((int)(x - target) >= 0) break;
-      if (it >= kBarrierSpin) {
-        atomicOr(flag, FLAG_SYNC);
-        ok = 0;
-        break;
+    const unsigned gen = ticket / gridDim.x;
+    const unsigned tag = (gen & 0x3FFFFFFFu) << 2;
+    unsigned *dec = bar + 1;
+    unsigned w = __hip_atomic_load(dec, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (ticket % gridDim.x == gridDim.x - 1u) {  // last arriver: pending -> go
+      while (!decided(w, gen) &&
+             !__hip_atomic_compare_exchange_strong(dec, &w, tag | 1u, __ATOMIC_RELAXED,
+                                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+      }
+    }
+    for (int it = 0; !decided(w, gen); ++it) {
+      if (it >= spin_limit) {  // expired: pending -> abort, unless decided meanwhile
+        if (__hip_atomic_compare_exchange_strong(dec, &w, tag | 2u, __ATOMIC_RELAXED,
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+          w = tag | 2u;
+          atomicOr(flag, FLAG_SYNC);
+        }
+        continue;  // w now holds the current word
       }
       __builtin_amdgcn_s_sleep(1);
+      w = __hip_atomic_load(dec, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
+    ok = decided(w, gen) == 1u ? 1 : 0;
   }
   __syncthreads();
   return ok != 0;
@@ -74,7 +100,7 @@ __global__ __launch_bounds__(256) void online_step_kernel(
     int64_t D, int d, int K, const float *__restrict__ h, const int *__restrict__ idx,
     const float *__restrict__ val, float lr, float *V, int64_t ldv, float *U, float *UinvT,
     float *Q, int ldd, float *__restrict__ loss_out, float *__restrict__ grad_h,
-    float *__restrict__ work, unsigned *__restrict__ bar, int *__restrict__ flag) {
+    float *__restrict__ work, unsigned *__restrict__ bar, int spin_limit, int *__restrict__ flag) {
   extern __shared__ float lds[];  // h, y^, h^, g, X (d each)
   __shared__ float red[4][64];
   __shared__ int bad_idx;
@@ -151,7 +177,7 @@ __global__ __launch_bounds__(256) void online_step_kernel(
     __syncthreads();
   }
 
-  const bool met = grid_barrier(bar, flag);
+  const bool met = grid_barrier(bar, spin_limit, flag);
 
   // ---- phase B ----
   for (int j = t; j < d; j += 256) {
@@ -249,9 +275,11 @@ size_t online_work_floats(int d) { return (size_t)(kOnlineSlices + 3) * d; }
 hipError_t launch_online_step(hipStream_t s, int64_t D, int d, int K, const float *h,
                               const int *idx, const float *val, float lr, float *V, int64_t ldv,
                               float *U, float *UinvT, float *Q, int ldd, float *loss_out,
-                              float *grad_h, float *work, unsigned *bar, int *flag) {
+                              float *grad_h, float *work, unsigned *bar, int spin_limit,
+                              int *flag) {
   LST_LAUNCH(online_step_kernel, dim3(kOnlineWGs), dim3(256), (size_t)(5 * d * sizeof(float)), s,
-             D, d, K, h, idx, val, lr, V, ldv, U, UinvT, Q, ldd, loss_out, grad_h, work, bar, flag);
+             D, d, K, h, idx, val, lr, V, ldv, U, UinvT, Q, ldd, loss_out, grad_h, work, bar,
+             spin_limit, flag);
   return hipGetLastError();
 }
 

@@ -54,22 +54,25 @@ def test_status_strings(L):
 def test_host_argument_errors(L):
     # shape and argument checks run before any device call
     P = 0x1000  # a non-null placeholder; never dereferenced on these paths
-    st, ctx = lst.lst_create(0, 8, 4, 2, 0, 1e-3, P, 8, P, P, P, 8, 0)
+    WS = 0x100000  # a 256-byte aligned placeholder workspace
+    nb = lst.lst_workspace_bytes(10, 8, 4, 2, 0)
+    st, ctx = lst.lst_create(0, 8, 4, 2, 0, 1e-3, P, 8, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_SHAPE and ctx == 0
-    st, _ = lst.lst_create(10, 8, 4, 2, 5, 1e-3, P, 8, P, P, P, 8, 0)
+    st, _ = lst.lst_create(10, 8, 4, 2, 5, 1e-3, P, 8, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_ARG
-    st, _ = lst.lst_create(10, 8, 4, 2, 1, 0.0, P, 8, P, P, P, 8, 0)
+    st, _ = lst.lst_create(10, 8, 4, 2, 1, 0.0, P, 8, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_ARG
-    st, _ = lst.lst_create(10, 8, 4, 2, 0, 1e-3, 0, 8, P, P, P, 8, 0)
+    st, _ = lst.lst_create(10, 8, 4, 2, 0, 1e-3, 0, 8, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_ARG
-    st, _ = lst.lst_create(10, 8, 4, 2, 0, 1e-3, P, 7, P, P, P, 8, 0)
+    st, _ = lst.lst_create(10, 8, 4, 2, 0, 1e-3, P, 7, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_SHAPE
-    st, _ = lst.lst_create(10, 8, 2048, 2, 0, 1e-3, P, 8, P, P, P, 8, 0)
+    st, _ = lst.lst_create(10, 8, 2048, 2, 0, 1e-3, P, 8, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_SHAPE
-    st, _ = lst.lst_create(10, 8, 512, 64, 0, 1e-3, P, 8, P, P, P, 8, 0)
+    st, _ = lst.lst_create(10, 8, 512, 64, 0, 1e-3, P, 8, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_SHAPE
-    st, _ = lst.lst_naive_create(10, 0, 4, 2, 0, 1e-3, P, 8, 0)
+    st, _ = lst.lst_naive_create(10, 0, 4, 2, 0, 1e-3, P, 8, WS, nb, 0)
     assert st == lst.LST_E_SHAPE
+    assert lst.lst_set_option(0, lst.LST_OPT_SPIN_LIMIT, 1) == lst.LST_E_ARG
     assert lst.lst_step(0, P, 1, P, P, 1, 0.1, P, P) == lst.LST_E_ARG
     assert lst.lst_sync_status(0) == lst.LST_E_ARG
     assert lst.lst_materialize_W(0, P, 8) == lst.LST_E_ARG
@@ -86,6 +89,28 @@ def test_host_argument_errors(L):
     assert lst.lst_input_update(P, 8, 10, 8, P, P, 1, 65, P, 0.1, P, 0) == lst.LST_E_SHAPE
     assert lst.lst_input_update(P, 8, 10, 8, P, P, 1, 1, P, -1.0, P, 0) == lst.LST_E_ARG
     lst.lst_destroy(0)
+
+
+def test_workspace_is_checked_on_the_host(L):
+    # the workspace is the caller's: a missing, misaligned or too small one is rejected
+    # before anything is enqueued, and its size grows with every dimension it holds
+    P = 0x1000
+    nb = lst.lst_workspace_bytes(1000, 32, 16, 3, 0)
+    assert nb > 0 and nb % 256 == 0
+    assert lst.lst_workspace_bytes(0, 32, 16, 3, 0) == 0
+    assert lst.lst_workspace_bytes(1000, 32, 16, 3, 9) == 0
+    assert lst.lst_workspace_bytes(1000, 32, 32, 3, 0) > nb
+    assert lst.lst_workspace_bytes(1000, 64, 16, 3, 0) > nb
+    assert lst.lst_workspace_bytes(1000, 32, 16, 6, 0) > nb
+    ws = 0x100000
+    for args, want in [((0, nb), lst.LST_E_ARG), ((ws + 4, nb), lst.LST_E_ARG),
+                       ((ws, nb - 256), lst.LST_E_SHAPE)]:
+        st, ctx = lst.lst_create(1000, 32, 16, 3, 0, 1e-3, P, 32, P, P, P, 32, *args, 0)
+        assert st == want and ctx == 0
+    nn = lst.lst_naive_workspace_bytes(1000, 32, 16, 3, 0)
+    assert nn >= 1000 * 16 * 4  # holds the D x m output
+    st, ctx = lst.lst_naive_create(1000, 32, 16, 3, 0, 1e-3, P, 32, ws, nn - 256, 0)
+    assert st == lst.LST_E_SHAPE and ctx == 0
 
 
 def test_product_path_does_not_import_the_oracle():

@@ -147,27 +147,29 @@ def test_naive_index_error_keeps_W():
     n.close()
 
 
-@pytest.mark.parametrize("m", [8, 200])
-def test_woodbury_release_withheld(monkeypatch, m):
-    """The two streams of a step are ordered by device progress counters.  With the
-    Woodbury branch's release withheld (a test hook read at creation), the state
-    updates' bounded wait must expire: the step reports LST_E_SYNC, writes no state,
-    and the kernels all finish (the wait, not the GPU, gives up)."""
-    w = Workload("t", LOSS_SQUARED, 1000, 32, m, 2)
+def test_online_barrier_expiry_is_all_or_nothing():
+    """The one-launch online step (m = 1) meets at a bounded grid barrier.  With its
+    spin limit set to 0 (LST_OPT_SPIN_LIMIT) every waiting workgroup gives up at once:
+    the single go/abort decision must be abort, so no workgroup writes its part of the
+    state (V, U, U^{-T}, Q bit-identical) and the step reports LST_E_SYNC; every kernel
+    still finishes (the wait, not the GPU, gives up).  With the limit restored the next
+    step matches the oracle."""
+    w = Workload("t", LOSS_SQUARED, 2000, 64, 1, 3)
     s = Stream(w)
-    monkeypatch.setenv("LST_TEST_WITHHOLD_WOODBURY_RELEASE", "1")
     f = make_factored(w, s.V0)
-    monkeypatch.delenv("LST_TEST_WITHHOLD_WOODBURY_RELEASE")
+    f.set_option(lst.LST_OPT_SPIN_LIMIT, 0)
     snap = _state(f)
     H, idx, val = s.batch()
+    f.profile(True)
     f.step(*to_dev(H, idx, val), w.lr)
     assert f.sync_status() == lst.LST_E_SYNC
+    assert f.profile_read()["online"][0] == 1  # the one-launch kernel ran
+    f.profile(False)
     assert _same(f, snap)
-    f.close()
-    # a context created without the hook is unaffected
-    g = make_factored(w, s.V0)
+    f.set_option(lst.LST_OPT_SPIN_LIMIT, 1 << 20)
     ref = oracle_step(s.V0.astype(np.float64), H, idx, val, w)
-    loss, grad = g.step(*to_dev(H, idx, val), w.lr)
-    assert g.sync_status() == lst.LST_OK
+    loss, grad = f.step(*to_dev(H, idx, val), w.lr)
+    assert f.sync_status() == lst.LST_OK
     assert abs(loss.item() - ref.loss) <= 1e-4 * abs(ref.loss)
-    g.close()
+    assert rel(f.materialize_W().cpu().numpy(), ref.W_new) <= 1e-4
+    f.close()

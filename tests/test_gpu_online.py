@@ -1,5 +1,6 @@
-"""The online step (m = 1, squared error, Algorithm 2) as one cooperative launch, against the
-fp64 dense oracle, and against the general step path (LST_ONLINE_KERNEL=0) on the same inputs.
+"""The online step (m = 1, squared error, Algorithm 2) as one launch with a bounded grid
+barrier, against the fp64 dense oracle, and against the general step path
+(LST_OPT_ONLINE_KERNEL = 0) on the same inputs.
 
 Tolerances as for every step: relative 1e-4 on the loss and grad_h of the first step, 1e-3
 after; bit-exact untouched rows of V; state bit-identical after a rejected step.
@@ -18,13 +19,11 @@ TOL1 = 1e-4
 TOL100 = 1e-3
 
 
-def _run(w, steps, env_off=False, monkeypatch=None, batches=None):
+def _run(w, steps, general=False, batches=None):
     s = Stream(w)
-    if env_off:
-        monkeypatch.setenv("LST_ONLINE_KERNEL", "0")
     f = make_factored(w, s.V0)
-    if env_off:
-        monkeypatch.delenv("LST_ONLINE_KERNEL")
+    if general:
+        f.set_option(lst.LST_OPT_ONLINE_KERNEL, 0)
     W = s.V0.astype(np.float64)
     f.profile(True)
     for t in range(steps):
@@ -51,12 +50,12 @@ def test_online_kernel_matches_oracle(D, d, K):
     assert prof["online"][0] == 40 and prof["contract"][0] == 0  # the fused launch ran
 
 
-def test_online_kernel_and_general_path_agree(monkeypatch):
+def test_online_kernel_and_general_path_agree():
     w = Workload("t", LOSS_SQUARED, 6000, 128, 1, 4, index_dist="zipf")
     s = Stream(w)
     batches = [s.batch() for _ in range(30)]
     Wa, W, pa = _run(w, 30, batches=batches)
-    Wb, _, pb = _run(w, 30, env_off=True, monkeypatch=monkeypatch, batches=batches)
+    Wb, _, pb = _run(w, 30, general=True, batches=batches)
     assert pa["online"][0] == 30 and pb["online"][0] == 0 and pb["contract"][0] == 30
     assert rel(Wa, W) <= TOL100 and rel(Wb, W) <= TOL100 and rel(Wa, Wb) <= TOL100
 

@@ -226,30 +226,3 @@ def test_graph_replay_matches_eager(loss):
         assert torch.equal(a, b)
     for a, b in zip(s0, s1):
         assert torch.equal(a, b)
-
-
-def test_one_stream_mode_is_bit_identical(monkeypatch):
-    # LST_ONE_STREAM (for profilers that run one dispatch at a time) puts the Woodbury
-    # branch on the caller's stream: same kernels, same arithmetic, so the same bits.
-    for loss in (LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX):
-        w = Workload("t", loss, 3000, 48, 24, 2,
-                     value_dist="normal" if loss == LOSS_SQUARED else "ones")
-        s = Stream(w)
-        batches = [to_dev(*s.batch()) for _ in range(4)]
-        outs = []
-        for one in (False, True):
-            if one:
-                monkeypatch.setenv("LST_ONE_STREAM", "1")
-            f = make_factored(w, s.V0)
-            monkeypatch.delenv("LST_ONE_STREAM", raising=False)
-            res = []
-            for b in batches:
-                loss_v, g = f.step(*b, w.lr)
-                res.append((loss_v.item(), g.clone()))
-            f.check()
-            outs.append((res, [t.clone() for t in (f.V, f.U, f.UinvT, f.Q)]))
-            f.close()
-        (r0, s0), (r1, s1) = outs
-        for (l0, g0), (l1, g1) in zip(r0, r1):
-            assert l0 == l1 and torch.equal(g0, g1)
-        assert all(torch.equal(a, b) for a, b in zip(s0, s1))
