@@ -144,6 +144,9 @@ void carve_factored(lst_ctx *c, Carver &cv) {
   b.Cwork = cv.take<float>(mm);
   b.qpart = cv.take<float>((d + 15) / 16 * m);
   b.bpart = cv.take<float>((m + 15) / 16 * m);
+  b.q = cv.take<float>(m);
+  b.tsum = cv.take<float>(m);
+  b.qcnt = cv.take<int>((m + 15) / 16);
   b.dq = cv.take<float>(m);
   b.lvec = cv.take<float>(m);
   b.dA = cv.take<float>(mk);

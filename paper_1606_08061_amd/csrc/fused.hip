@@ -64,28 +64,10 @@ __device__ __forceinline__ const float *rsv(const float *p, const float *H, floa
   return v == 16 ? H : (v == 32 ? gH : p);
 }
 
-// q_j from the row partials of launch 1's H^ tiles, summed in tile order (every
-// workgroup that needs q_j forms the identical value).
-__device__ __forceinline__ float q_of(const float *__restrict__ qpart, int T, int m, int j) {
-  float q = 0.f;
-  for (int t = 0; t < T; ++t) q += qpart[(int64_t)t * m + j];
-  return q;
-}
-
 // dl/dq_j: 1 for squared error; for the spherical softmax (sum of the example's
 // target weights over its valid slots, in slot order) / (q_j + D eps).
 __device__ __forceinline__ float dq_of(int loss, float q, float tsum, float Deps) {
   return loss == LST_LOSS_SQUARED ? 1.f : tsum / (q + Deps);
-}
-
-__device__ __forceinline__ float tsum_of(const int *__restrict__ idx, const float *__restrict__ val,
-                                         int K, int64_t D, int j) {
-  float s = 0.f;
-  for (int k = 0; k < K; ++k) {
-    const int r = idx[(int64_t)j * K + k];
-    if (r >= 0 && (int64_t)r < D) s += val[(int64_t)j * K + k];
-  }
-  return s;
 }
 
 __device__ __forceinline__ float scale_of(int mode, const float *dq, int i) {
@@ -104,43 +86,6 @@ __device__ __forceinline__ float scale_of(int mode, const float *dq, int i) {
 // ---------------------------------------------------------------------------
 constexpr int kGroup = 8;
 
-// Four consecutive k values of index idx of a source: tr = 0 -> p[idx ld + k]
-// (contiguous, one 16-byte load when aligned), tr = 1 -> p[k ld + idx].  k >= kend
-// reads as zero (address clamped).
-__device__ __forceinline__ void ld4k(const float *__restrict__ p, int64_t ld, int tr, int idx,
-                                     int k0, int kend, float (&o)[4]) {
-  if (k0 + 3 < kend) {
-    if (tr == 0) {
-      const float *q = p + (int64_t)idx * ld + k0;
-      if (((reinterpret_cast<uintptr_t>(q)) & 15) == 0) {
-        const float4 v = *reinterpret_cast<const float4 *>(q);
-        o[0] = v.x;
-        o[1] = v.y;
-        o[2] = v.z;
-        o[3] = v.w;
-      } else {
-        o[0] = q[0];
-        o[1] = q[1];
-        o[2] = q[2];
-        o[3] = q[3];
-      }
-    } else {
-      const float *q = p + (int64_t)k0 * ld + idx;
-      o[0] = q[0];
-      o[1] = q[ld];
-      o[2] = q[2 * ld];
-      o[3] = q[3 * ld];
-    }
-    return;
-  }
-#pragma unroll
-  for (int s = 0; s < 4; ++s) {
-    const int k = min(k0 + s, kend - 1);
-    const float v = tr == 0 ? p[(int64_t)idx * ld + k] : p[(int64_t)k * ld + idx];
-    o[s] = (k0 + s < kend) ? v : 0.f;
-  }
-}
-
 struct TileCtx {
   const float *H;
   float *gH;
@@ -151,6 +96,218 @@ struct TileCtx {
 
 __device__ __forceinline__ float coef_of(const TileCtx &x, int c) { return c < 0 ? 1.f : x.coef[c]; }
 
+// Four consecutive k values (k0 .. k0 + 3, all below the end of k) of index idx of
+// a source, by operand access mode: LV contiguous in k and 16-byte aligned (one
+// vector load), LS contiguous in k, LT k-major (p[k ld + idx]).
+enum : int { LV = 0, LS = 1, LT = 2 };
+
+template <int MODE>
+__device__ __forceinline__ void ld4f(const float *__restrict__ p, int64_t ld, int idx, int k0,
+                                     float (&o)[4]) {
+  if constexpr (MODE == LV) {
+    const float4 v = *reinterpret_cast<const float4 *>(p + (int64_t)idx * ld + k0);
+    o[0] = v.x;
+    o[1] = v.y;
+    o[2] = v.z;
+    o[3] = v.w;
+  } else if constexpr (MODE == LS) {
+    const float *q = p + (int64_t)idx * ld + k0;
+    o[0] = q[0];
+    o[1] = q[1];
+    o[2] = q[2];
+    o[3] = q[3];
+  } else {
+    const float *q = p + (int64_t)k0 * ld + idx;
+    o[0] = q[0];
+    o[1] = q[ld];
+    o[2] = q[2 * ld];
+    o[3] = q[3 * ld];
+  }
+}
+
+template <int MODE>
+__device__ __forceinline__ void ld4m(const float *__restrict__ p, int64_t ld, int idx, int k0,
+                                     int kend, float (&o)[4]) {
+  if (k0 + 3 < kend) {
+    ld4f<MODE>(p, ld, idx, k0, o);
+    return;
+  }
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const int k = min(k0 + s, kend - 1);
+    const float v = MODE == LT ? p[(int64_t)k * ld + idx] : p[(int64_t)idx * ld + k];
+    o[s] = (k0 + s < kend) ? v : 0.f;
+  }
+}
+
+// The operand values of one k-block for one lane: a (A row ia) and b (the B terms
+// combined, column jb) at k = k0 .. k0 + 3; MASKED: the block may pass the end of k.
+template <int AMODE, int NB, bool SC, int AMD, int BMD, bool MASKED>
+__device__ __forceinline__ void op16_block(const Op16 &g, const float *A, const float *const *Bp,
+                                           const float *bco, float dqi, int ia, int jb, int k0,
+                                           const TileCtx &x, float (&a)[4], float (&b)[4]) {
+  const int K = g.K;
+  if constexpr (AMODE == AM_MASM) {
+    // M_ik = 4 dq_i M^_ik dq_k + YY_ik + 2 dq_i HZ_ik + 2 dq_k HZ_ki
+    float mh[4], yy[4], hz[4], hzt[4], dk[4];
+    ld4m<LS>(g.Mh, g.ldm, ia, k0, K, mh);
+    ld4m<LS>(g.YY, g.ldm, ia, k0, K, yy);
+    ld4m<LS>(g.HZ, g.ldm, ia, k0, K, hz);
+    ld4m<LT>(g.HZ, g.ldm, ia, k0, K, hzt);
+    if (x.dq) {
+      ld4m<LS>(x.dq, 0, 0, k0, K, dk);
+    } else {
+      dk[0] = dk[1] = dk[2] = dk[3] = 1.f;
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+      a[s] = 4.f * dqi * mh[s] * dk[s] + yy[s] + 2.f * dqi * hz[s] + 2.f * dk[s] * hzt[s];
+  } else if constexpr (MASKED) {
+    ld4m<AMD>(A, g.lda, ia, k0, K, a);
+  } else {
+    ld4f<AMD>(A, g.lda, ia, k0, a);
+  }
+#pragma unroll
+  for (int t = 0; t < NB; ++t) {
+    float v[4];
+    if constexpr (MASKED)
+      ld4m<BMD>(Bp[t], g.b[t].ld, jb, k0, K, v);
+    else
+      ld4f<BMD>(Bp[t], g.b[t].ld, jb, k0, v);
+    if constexpr (SC) {
+      if (g.b[t].sc != SC_NONE) {
+        float sv[4];
+        if constexpr (MASKED) {
+#pragma unroll
+          for (int s = 0; s < 4; ++s) sv[s] = x.dq[min(k0 + s, K - 1)];
+        } else {
+          ld4f<LV>(x.dq, 0, 0, k0, sv);
+        }
+#pragma unroll
+        for (int s = 0; s < 4; ++s) v[s] *= g.b[t].sc == SC_DQ ? sv[s] : sqrtf(sv[s]);
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) b[s] = t == 0 ? bco[0] * v[s] : fmaf(bco[t], v[s], b[s]);
+  }
+}
+
+// Row partial sums of a tile (v Rr_ij, or |v|) over its 16 columns into
+// rowout[tile column][i]; with qout, the last tile of the row block to finish sums
+// the row's partials into qout[i].
+__device__ __forceinline__ void rowred_epilogue(const Op16 &g, float v, bool ok, float rrv, int oi,
+                                                int c, int tm, int tn, int i0) {
+  if (g.rowred != RR_NONE) {
+    float r = 0.f;
+    if (ok) r = g.rowred == RR_DOT ? v * rrv : fabsf(v);
+    // the 16 lanes of this row (same g, same wavefront), in a fixed order
+    r += __shfl_xor(r, 1);
+    r += __shfl_xor(r, 2);
+    r += __shfl_xor(r, 4);
+    r += __shfl_xor(r, 8);
+    if (c == 0 && oi < g.M) {
+      float *dst = g.rowout + (int64_t)tn * g.M + oi;
+      if (g.qout)  // read by another workgroup of this launch, possibly on another XCD
+        __hip_atomic_store(dst, r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      else
+        *dst = r;
+    }
+    if (g.qout) {
+      // Arrival after this workgroup's partials are complete (each thread waits for
+      // its own stores); the last of the row block's tiles_n arrivals sums them.
+      __shared__ int last;
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (threadIdx.x == 0)
+        last = __hip_atomic_fetch_add(g.qcnt + tm, 1, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT) == g.tiles_n - 1;
+      __syncthreads();
+      if (last) {
+        // row i0 + threadIdx.x / 16: lane l sums the partials l, l + 16, ... in order,
+        // then the 16 lanes are added pairwise in a fixed pattern
+        const int i = i0 + (int)(threadIdx.x >> 4), l = threadIdx.x & 15;
+        float q = 0.f;
+        if (i < g.M)
+          for (int t = l; t < g.tiles_n; t += 16)
+            q += __hip_atomic_load(g.rowout + (int64_t)t * g.M + i, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+        q += __shfl_xor(q, 1);
+        q += __shfl_xor(q, 2);
+        q += __shfl_xor(q, 4);
+        q += __shfl_xor(q, 8);
+        if (l == 0 && i < g.M) g.qout[i] = q;
+      }
+    }
+  }
+}
+
+// The k loop of one tile, specialised at compile time: AMODE (plain or assembled M),
+// NB (B terms: 1 or kMaxTerms), SC (B terms scaled by dl/dq), G (k-blocks whose loads
+// are issued before their products; smaller where a block needs more registers, so
+// that the kernels keep four wavefronts per SIMD without spilling), AMD / BMD (the
+// operands' access modes).  The four wavefronts take the whole k-blocks of 16 in turn;
+// the ragged end of k (K mod 16) is one more masked block, taken by wavefront 3.
+template <int AMODE, int NB, bool SC, int G, int AMD, int BMD>
+__device__ __forceinline__ floatx4 op16_kloop(const Op16 &g, int ia, int jb, const TileCtx &x,
+                                              int wave, int lg) {
+  const int K = g.K;
+  const float *A = rsv(g.A, x.H, x.gH);
+  const float *Bp[NB];
+  float bco[NB];
+#pragma unroll
+  for (int t = 0; t < NB; ++t) {
+    Bp[t] = rsv(g.b[t].p, x.H, x.gH);
+    bco[t] = NB > 1 ? coef_of(x, g.b[t].coef) : 1.f;
+  }
+  const float dqi = (AMODE == AM_MASM && x.dq) ? x.dq[ia] : 1.f;
+  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
+  const int nfull = K >> 4;
+  const int nw = nfull > wave ? (nfull - wave + 3) / 4 : 0;
+  for (int u0 = 0; u0 < nw; u0 += G) {
+    float a[G][4], b[G][4];
+#pragma unroll
+    for (int u = 0; u < G; ++u) {
+      const int k0 = 16 * (wave + 4 * min(u0 + u, nw - 1)) + 4 * lg;
+      op16_block<AMODE, NB, SC, AMD, BMD, false>(g, A, Bp, bco, dqi, ia, jb, k0, x, a[u], b[u]);
+    }
+#pragma unroll
+    for (int u = 0; u < G; ++u)
+      if (u0 + u < nw) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][s], b[u][s], acc, 0, 0, 0);
+      }
+  }
+  if ((K & 15) && wave == 3) {
+    float a[4], b[4];
+    op16_block<AMODE, NB, SC, AMD, BMD, true>(g, A, Bp, bco, dqi, ia, jb, 16 * nfull + 4 * lg,
+                                               x, a, b);
+#pragma unroll
+    for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s], acc, 0, 0, 0);
+  }
+  return acc;
+}
+
+template <int AMODE, int NB, bool SC, int G>
+__device__ __forceinline__ floatx4 op16_dispatch(const Op16 &g, int ia, int jb, const TileCtx &x,
+                                                 int wave, int lg) {
+  if constexpr (AMODE == AM_MASM || NB > 1) {
+    // assembled M or several B terms: every B term k-major (the plan builder's layout)
+    return op16_kloop<AMODE, NB, SC, G, LS, LT>(g, ia, jb, x, wave, lg);
+  } else {
+    const bool av = vec_ok(rsv(g.A, x.H, x.gH), g.lda);
+    const int bm = g.b[0].tr ? LT : (vec_ok(rsv(g.b[0].p, x.H, x.gH), g.b[0].ld) ? LV : LS);
+    if (av) {
+      if (bm == LV) return op16_kloop<AMODE, NB, SC, G, LV, LV>(g, ia, jb, x, wave, lg);
+      if (bm == LS) return op16_kloop<AMODE, NB, SC, G, LV, LS>(g, ia, jb, x, wave, lg);
+      return op16_kloop<AMODE, NB, SC, G, LV, LT>(g, ia, jb, x, wave, lg);
+    }
+    if (bm == LV) return op16_kloop<AMODE, NB, SC, G, LS, LV>(g, ia, jb, x, wave, lg);
+    if (bm == LS) return op16_kloop<AMODE, NB, SC, G, LS, LS>(g, ia, jb, x, wave, lg);
+    return op16_kloop<AMODE, NB, SC, G, LS, LT>(g, ia, jb, x, wave, lg);
+  }
+}
+
 __device__ __forceinline__ void op16_tile(const Op16 &g, int local, const TileCtx &x) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = lane & 15, lg = lane >> 4;
@@ -158,84 +315,40 @@ __device__ __forceinline__ void op16_tile(const Op16 &g, int local, const TileCt
   const int tn = local / g.tiles_m, tm = local - tn * g.tiles_m;
   const int i0 = tm * 16, j0 = tn * 16;
   const int ia = min(i0 + c, g.M - 1), jb = min(j0 + c, g.N - 1);
-  const int K = g.K;
+  // Output of this thread after the reduction: accumulator register `wave` of lane
+  // `lane`.  Its epilogue operands are loaded before the k loop, so that their
+  // latency overlaps it.
+  const int oi = i0 + 4 * lg + wave, oj = j0 + c;
+  const bool ok = oi < g.M && oj < g.N;
+  const int ci = min(oi, g.M - 1), cj = min(oj, g.N - 1);
+  float addv[kMaxTerms];
+#pragma unroll
+  for (int t = 0; t < kMaxTerms; ++t)
+    addv[t] = t < g.nadd ? rsv(g.add[t].p, x.H, x.gH)[(int64_t)ci * g.add[t].ld + cj] : 0.f;
+  const float cinv = g.Cin ? rsv(g.Cin, x.H, x.gH)[(int64_t)ci * g.ldcin + cj] : 0.f;
+  const float ev = g.C2 ? rsv(g.E, x.H, x.gH)[(int64_t)ci * g.lde + cj] : 0.f;
+  const float rrv = g.rowred == RR_DOT ? rsv(g.Rr, x.H, x.gH)[(int64_t)ci * g.ldrr + cj] : 0.f;
 
-  const float *A = rsv(g.A, x.H, x.gH);
-  const float *Bp[kMaxTerms];
-  float bco[kMaxTerms];
-#pragma unroll
-  for (int t = 0; t < kMaxTerms; ++t) {
-    Bp[t] = t < g.nb ? rsv(g.b[t].p, x.H, x.gH) : nullptr;
-    bco[t] = t < g.nb ? coef_of(x, g.b[t].coef) : 0.f;
-  }
-  // MASM: A(i,k) = 4 dq_i M^_ik dq_k + YY_ik + 2 dq_i HZ_ik + 2 dq_k HZ_ki
-  const float dqi = (g.amode == AM_MASM && x.dq) ? x.dq[ia] : 1.f;
-
-  floatx4 acc = {0.f, 0.f, 0.f, 0.f};
-  const int nblk = (K + 15) >> 4;
-  const int nw = nblk > wave ? (nblk - wave + 3) / 4 : 0;
-  for (int u0 = 0; u0 < nw; u0 += kGroup) {
-    float a[kGroup][4], b[kGroup][4];
-#pragma unroll
-    for (int u = 0; u < kGroup; ++u) {
-      const int k0 = 16 * (wave + 4 * min(u0 + u, nw - 1)) + 4 * lg;
-      if (g.amode == AM_MASM) {
-        float mh[4], yy[4], hz[4], hzt[4], dk[4];
-        ld4k(g.Mh, g.ldm, 0, ia, k0, K, mh);
-        ld4k(g.YY, g.ldm, 0, ia, k0, K, yy);
-        ld4k(g.HZ, g.ldm, 0, ia, k0, K, hz);
-        ld4k(g.HZ, g.ldm, 1, ia, k0, K, hzt);
-        if (x.dq) {
-          ld4k(x.dq, 0, 0, 0, k0, K, dk);
-        } else {
-          dk[0] = dk[1] = dk[2] = dk[3] = 1.f;
-        }
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-          a[u][s] = 4.f * dqi * mh[s] * dk[s] + yy[s] + 2.f * dqi * hz[s] + 2.f * dk[s] * hzt[s];
-      } else {
-        ld4k(A, g.lda, g.tA, ia, k0, K, a[u]);
-      }
-#pragma unroll
-      for (int s = 0; s < 4; ++s) b[u][s] = 0.f;
-#pragma unroll
-      for (int t = 0; t < kMaxTerms; ++t) {
-        if (t >= g.nb) break;
-        float v[4];
-        ld4k(Bp[t], g.b[t].ld, g.b[t].tr, jb, k0, K, v);
-        if (g.b[t].sc != SC_NONE) {
-#pragma unroll
-          for (int s = 0; s < 4; ++s) v[s] *= scale_of(g.b[t].sc, x.dq, min(k0 + s, K - 1));
-        }
-#pragma unroll
-        for (int s = 0; s < 4; ++s) b[u][s] = fmaf(bco[t], v[s], b[u][s]);
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kGroup; ++u)
-      if (u0 + u < nw) {
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[u][s], b[u][s], acc, 0, 0, 0);
-      }
-  }
+  floatx4 acc;
+  if (g.amode == AM_MASM)
+    acc = op16_dispatch<AM_MASM, 1, false, 2>(g, ia, jb, x, wave, lg);
+  else if (g.nb > 1)
+    acc = op16_dispatch<AM_PLAIN, kMaxTerms, true, 2>(g, ia, jb, x, wave, lg);
+  else if (g.b[0].sc != SC_NONE)
+    acc = op16_dispatch<AM_PLAIN, 1, true, 4>(g, ia, jb, x, wave, lg);
+  else
+    acc = op16_dispatch<AM_PLAIN, 1, false, 8>(g, ia, jb, x, wave, lg);
 
   __shared__ float red[4][4][64];
 #pragma unroll
   for (int r = 0; r < 4; ++r) red[wave][r][lane] = acc[r];
   __syncthreads();
-  // output of this thread: accumulator register `wave` of lane `lane`
-  const int oi = i0 + 4 * lg + wave, oj = j0 + c;
-  const bool ok = oi < g.M && oj < g.N;
-  const int ci = min(oi, g.M - 1), cj = min(oj, g.N - 1);
   float v = (red[0][wave][lane] + red[1][wave][lane]) + (red[2][wave][lane] + red[3][wave][lane]);
   __syncthreads();  // red is reused by the next tile of this workgroup
 #pragma unroll
   for (int t = 0; t < kMaxTerms; ++t) {
     if (t >= g.nadd) break;
-    const OpTerm &ad = g.add[t];
-    const float *p = rsv(ad.p, x.H, x.gH);
-    v = fmaf(coef_of(x, ad.coef) * scale_of(ad.sc, x.dq, ci), p[(int64_t)ci * ad.ld + cj], v);
+    v = fmaf(coef_of(x, g.add[t].coef) * scale_of(g.add[t].sc, x.dq, ci), addv[t], v);
   }
   float al = g.alpha;
   for (int e = 0; e < g.alpha_lr; ++e) al *= x.lr;
@@ -243,24 +356,15 @@ __device__ __forceinline__ void op16_tile(const Op16 &g, int local, const TileCt
   if (g.Cin) {
     float be = g.beta;
     for (int e = 0; e < g.beta_lr; ++e) be *= x.lr;
-    v = fmaf(be, rsv(g.Cin, x.H, x.gH)[(int64_t)ci * g.ldcin + cj], v);
+    v = fmaf(be, cinv, v);
   }
   if (ok) {
     if (g.C) const_cast<float *>(rsv(g.C, x.H, x.gH))[(int64_t)oi * g.ldc + oj] = v;
     if (g.C2)
       const_cast<float *>(rsv(g.C2, x.H, x.gH))[(int64_t)oi * g.ldc2 + oj] =
-          2.f * scale_of(g.rs2, x.dq, oi) * rsv(g.E, x.H, x.gH)[(int64_t)oi * g.lde + oj] + v;
+          2.f * scale_of(g.rs2, x.dq, oi) * ev + v;
   }
-  if (g.rowred != RR_NONE) {
-    float r = 0.f;
-    if (ok) r = g.rowred == RR_DOT ? v * rsv(g.Rr, x.H, x.gH)[(int64_t)oi * g.ldrr + oj] : fabsf(v);
-    // the 16 lanes of this row (same g, same wavefront), in a fixed order
-    r += __shfl_xor(r, 1);
-    r += __shfl_xor(r, 2);
-    r += __shfl_xor(r, 4);
-    r += __shfl_xor(r, 8);
-    if (c == 0 && oi < g.M) g.rowout[(int64_t)tn * g.M + oi] = r;
-  }
+  rowred_epilogue(g, v, ok, rrv, oi, c, tm, tn, i0);
 }
 
 // Workgroup w of a section of 8 ceil(T / 8) workgroups (the section starting on a
@@ -289,11 +393,10 @@ __device__ __forceinline__ void run_op(const OpBatch &ob, int tile, const TileCt
 // ---------------------------------------------------------------------------
 // Launch 1: contractions, N, prefetch of the target rows.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void step_contract_kernel(const StepPlan *__restrict__ pl,
-                                                            const float *H, float lr,
-                                                            const int *__restrict__ idx, int K,
-                                                            const float *__restrict__ V,
-                                                            int64_t ldv, int64_t D, int d, int m) {
+__global__ __launch_bounds__(256, 5) void step_contract_kernel(
+    const StepPlan *__restrict__ pl, const float *H, float lr, const int *__restrict__ idx,
+    const float *__restrict__ val, int K, const float *__restrict__ V, int64_t ldv, int64_t D,
+    int d, int m, float *__restrict__ tsum) {
   const OpBatch &ob = pl->ob[0];
   const int w = blockIdx.x;
   const int sec = (ob.total + 7) & ~7;
@@ -305,15 +408,24 @@ __global__ __launch_bounds__(256) void step_contract_kernel(const StepPlan *__re
     return;
   }
   // Prefetch workgroup of example j (XCD j % 8, that of its gather workgroup in
-  // launch 2): the indices, then one load per 128-byte line of every target row.
+  // launch 2): the indices, then one load per 128-byte line of every target row;
+  // also the sum of the example's target weights over its valid slots, in slot order.
   const int j = w - sec;
   if (j >= m) return;
   __shared__ int prow[LST_MAX_K];
+  __shared__ float pval[LST_MAX_K];
   for (int k = threadIdx.x; k < K; k += 256) {
     const int r = idx[(int64_t)j * K + k];
     prow[k] = (r < 0 || (int64_t)r >= D) ? -1 : r;
+    pval[k] = val[(int64_t)j * K + k];
   }
   __syncthreads();
+  if (threadIdx.x == 0) {
+    float ts = 0.f;
+    for (int k = 0; k < K; ++k)
+      if (prow[k] >= 0) ts += pval[k];
+    tsum[j] = ts;
+  }
   const int nl = (d + 31) >> 5;
   float sink = 0.f;
   for (int e = threadIdx.x; e < K * nl; e += 256) {
@@ -327,9 +439,11 @@ __global__ __launch_bounds__(256) void step_contract_kernel(const StepPlan *__re
 // Launch 2: the gather and loss epilogue of one example per workgroup.
 // ---------------------------------------------------------------------------
 struct GatherArgs {
-  int K, d, m, T;
+  int K, d, m;
   int64_t D;
-  const float *H, *Htil, *qpart;
+  const float *H, *Hhat, *Htil, *q, *tsum;
+  int *qcnt;
+  int nqcnt;
   const int *idx;
   const float *val;
   const float *V;
@@ -406,6 +520,85 @@ __device__ __forceinline__ void sorted_slots(int j, int K, const int *sr, const 
   }
 }
 
+// The loss epilogue on register arrays (KM slots, fully unrolled): the serial part of
+// a gather workgroup then makes no dependent LDS reads.
+template <int KM>
+__device__ __forceinline__ void epilogue_reg(int loss, float q, int K, const int (&r)[KM],
+                                             const float (&t)[KM], const float (&a)[KM],
+                                             float Deps, float eps, float &l, float (&g)[KM]) {
+  l = 0.f;
+  if (loss == LST_LOSS_SQUARED) {
+    float at = 0.f, yy = 0.f;
+#pragma unroll
+    for (int k = 0; k < KM; ++k) {
+      const bool ok = k < K && r[k] >= 0;
+      g[k] = ok ? -2.f * t[k] : 0.f;
+      if (!ok) continue;
+      at += t[k] * a[k];
+#pragma unroll
+      for (int kk = 0; kk < KM; ++kk)
+        if (kk < K && r[kk] == r[k]) yy += t[k] * t[kk];
+    }
+    l = q - 2.f * at + yy;
+  } else {
+    const float lz = logf(q + Deps);
+#pragma unroll
+    for (int k = 0; k < KM; ++k) {
+      g[k] = 0.f;
+      if (k >= K || r[k] < 0) continue;
+      const float den = a[k] * a[k] + eps;
+      l += t[k] * (lz - logf(den));
+      g[k] = -2.f * t[k] * a[k] / den;
+    }
+  }
+}
+
+// sorted_slots with the example's KM slots in registers (K <= KM).
+template <int KM>
+__device__ __forceinline__ void sorted_slots_reg(int j, int K, const int *sr, const float *sg,
+                                                 int *srow, float *sval, int *scnt) {
+  int rr[KM];
+  float vv[KM];
+#pragma unroll
+  for (int k = 0; k < KM; ++k) {
+    rr[k] = k < K ? sr[k] : -1;
+    vv[k] = k < K ? sg[k] : 0.f;
+  }
+  bool first[KM];
+  int n = 0;
+#pragma unroll
+  for (int k = 0; k < KM; ++k) {
+    bool f = rr[k] >= 0;
+#pragma unroll
+    for (int k2 = 0; k2 < k; ++k2) f &= rr[k2] != rr[k];
+    first[k] = f;
+    n += f ? 1 : 0;
+  }
+  const int k = threadIdx.x;
+  if (k < K) {
+    int me = -1;
+    bool fk = false;
+#pragma unroll
+    for (int u = 0; u < KM; ++u)
+      if (u == k) {
+        me = rr[u];
+        fk = first[u];
+      }
+    if (fk) {
+      float v = 0.f;
+      int pos = 0;
+#pragma unroll
+      for (int u = 0; u < KM; ++u) {
+        if (rr[u] == me) v += vv[u];
+        pos += (first[u] && rr[u] < me) ? 1 : 0;
+      }
+      srow[(int64_t)j * K + pos] = me;
+      sval[(int64_t)j * K + pos] = v;
+    }
+  }
+  if (threadIdx.x == 0) scnt[j] = n;
+}
+
 // Register-resident form for K <= 4 KPW and d <= 64 NV: wavefront w keeps the
 // target rows k = w, w + 4, ... in registers from the dot products a_kj to the G
 // sum, so V is read once and the index loads lead straight into the row loads.
@@ -417,18 +610,39 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
   __shared__ float s_dq;
   __shared__ int s_bad;
   __shared__ float gpart[W][64 * NV];
+  __shared__ float sred[W];
   const int K = ga.K, d = ga.d;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
   if (t == 0) s_bad = 0;
+  // q_j: for squared error h_j . h^_j here (its operands loaded into registers first
+  // and used after the target rows' dot products, so that the loads overlap); for the
+  // spherical softmax reduced in launch 1 (its E products need every q_j).
+  constexpr int NQ = (64 * NV + 255) / 256;
+  float qh[NQ], qhh[NQ];
+  float qv = 0.f, tsv = 0.f;
+  const bool sq = ga.loss == LST_LOSS_SQUARED;
+#pragma unroll
+  for (int u = 0; u < NQ; ++u) {
+    const int c = t + 256 * u;
+    qh[u] = (sq && c < d) ? ga.H[(int64_t)j * d + c] : 0.f;
+    qhh[u] = (sq && c < d) ? ga.Hhat[(int64_t)j * d + c] : 0.f;
+  }
+  if (!sq && t == 0) {
+    qv = ga.q[j];
+    tsv = ga.tsum[j];
+  }
   int r[KPW];
+  float tv[KPW];  // the slots' target values, loaded with the indices
   bool bad = false;
 #pragma unroll
   for (int i = 0; i < KPW; ++i) {
     const int k = wave + W * i;
     int v = -1;
+    tv[i] = 0.f;
     if (k < K) {
       v = ga.idx[(int64_t)j * K + k];
+      tv[i] = ga.val[(int64_t)j * K + k];
       if (v < -1 || (int64_t)v >= ga.D) {
         bad = true;
         v = -1;
@@ -462,6 +676,13 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
     for (int n = 0; n < NV; ++n) sacc += ht[n] * vr[i][n];
     a[i] = wave_sum(sacc);
   }
+  if (sq) {
+    float qs = 0.f;
+#pragma unroll
+    for (int u = 0; u < NQ; ++u) qs += qh[u] * qhh[u];
+    qs = wave_sum(qs);
+    if (lane == 0) sred[wave] = qs;
+  }
   __syncthreads();  // s_bad initialised
   if (lane == 0) {
 #pragma unroll
@@ -470,7 +691,7 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
       if (k < K) {
         sr[k] = r[i];
         sa[k] = a[i];
-        st[k] = ga.val[(int64_t)j * K + k];
+        st[k] = tv[i];
       }
     }
     if (bad) atomicOr(&s_bad, 1);
@@ -478,11 +699,23 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
   __syncthreads();
   if (t == 0) {
     if (s_bad) atomicOr(ga.flag, FLAG_INDEX);
-    const float q = q_of(ga.qpart, ga.T, ga.m, j);
+    const float q = ga.loss == LST_LOSS_SQUARED ? (sred[0] + sred[1]) + (sred[2] + sred[3]) : qv;
     const float Deps = (float)ga.D * ga.eps;
-    const float gq = dq_of(ga.loss, q, tsum_of(ga.idx, ga.val, K, ga.D, j), Deps);
+    const float gq = dq_of(ga.loss, q, tsv, Deps);
+    constexpr int KM = W * KPW;
+    int rr[KM];
+    float tt[KM], aa[KM], gg[KM];
+#pragma unroll
+    for (int k = 0; k < KM; ++k) {
+      rr[k] = k < K ? sr[k] : -1;
+      tt[k] = k < K ? st[k] : 0.f;
+      aa[k] = k < K ? sa[k] : 0.f;
+    }
     float l;
-    epilogue(ga.loss, q, gq, K, sr, st, sa, Deps, ga.eps, l, sg);
+    epilogue_reg<KM>(ga.loss, q, K, rr, tt, aa, Deps, ga.eps, l, gg);
+#pragma unroll
+    for (int k = 0; k < KM; ++k)
+      if (k < K) sg[k] = gg[k];
     ga.dq[j] = gq;
     ga.lvec[j] = l;
     s_dq = gq;
@@ -493,7 +726,7 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
     ga.dA[(int64_t)j * K + k] = sg[k];
     ga.wA[(int64_t)j * K + k] = gq != 0.f ? sg[k] / (2.f * gq) : 0.f;
   }
-  sorted_slots(j, K, sr, sg, ga.srow, ga.sval, ga.scnt);
+  sorted_slots_reg<W * KPW>(j, K, sr, sg, ga.srow, ga.sval, ga.scnt);
 #pragma unroll
   for (int n = 0; n < NV; ++n) {
     float gv = 0.f;
@@ -519,10 +752,21 @@ __device__ __forceinline__ void gather_gen(const GatherArgs &ga, int j) {
   __shared__ float sa[LST_MAX_K], st[LST_MAX_K], sg[LST_MAX_K];
   __shared__ float s_dq;
   __shared__ int s_bad;
+  __shared__ float sred[4];
   const int K = ga.K, d = ga.d;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
   const float *ht = ga.Htil + (int64_t)j * d;
   if (t == 0) s_bad = 0;
+  float qv = 0.f, tsv = 0.f;
+  if (ga.loss == LST_LOSS_SQUARED) {
+    float qs = 0.f;
+    for (int c = t; c < d; c += 256) qs += ga.H[(int64_t)j * d + c] * ga.Hhat[(int64_t)j * d + c];
+    qs = wave_sum(qs);
+    if (lane == 0) sred[wave] = qs;
+  } else if (t == 0) {
+    qv = ga.q[j];
+    tsv = ga.tsum[j];
+  }
   __syncthreads();
   for (int k = t; k < K; k += 256) {
     int r = ga.idx[(int64_t)j * K + k];
@@ -548,9 +792,9 @@ __device__ __forceinline__ void gather_gen(const GatherArgs &ga, int j) {
   __syncthreads();
   if (t == 0) {
     if (s_bad) atomicOr(ga.flag, FLAG_INDEX);
-    const float q = q_of(ga.qpart, ga.T, ga.m, j);
+    const float q = ga.loss == LST_LOSS_SQUARED ? (sred[0] + sred[1]) + (sred[2] + sred[3]) : qv;
     const float Deps = (float)ga.D * ga.eps;
-    const float gq = dq_of(ga.loss, q, tsum_of(ga.idx, ga.val, K, ga.D, j), Deps);
+    const float gq = dq_of(ga.loss, q, tsv, Deps);
     float l;
     epilogue(ga.loss, q, gq, K, sr, st, sa, Deps, ga.eps, l, sg);
     ga.dq[j] = gq;
@@ -579,20 +823,20 @@ __device__ __forceinline__ void gather_gen(const GatherArgs &ga, int j) {
 // dl/dq of every example into LDS (the spherical softmax's E products need all of
 // them before the gather workgroups have written theirs; the same arithmetic).
 __device__ __forceinline__ void dq_all(const GatherArgs &ga, float *sdq) {
-  for (int i = threadIdx.x; i < ga.m; i += 256) {
-    const float q = q_of(ga.qpart, ga.T, ga.m, i);
-    sdq[i] = dq_of(ga.loss, q, tsum_of(ga.idx, ga.val, ga.K, ga.D, i), (float)ga.D * ga.eps);
-  }
+  for (int i = threadIdx.x; i < ga.m; i += 256)
+    sdq[i] = dq_of(ga.loss, ga.q[i], ga.tsum[i], (float)ga.D * ga.eps);
   __syncthreads();
 }
 
 template <int KPW, int NV>
-__global__ __launch_bounds__(256) void step_gather_kernel(const StepPlan *__restrict__ pl,
+__global__ __launch_bounds__(256, 5) void step_gather_kernel(const StepPlan *__restrict__ pl,
                                                           const float *H, float lr,
                                                           const GatherArgs ga) {
   const int w = blockIdx.x;
   const int gsec = (ga.m + 7) & ~7;
   if (w < gsec) {
+    // launch 1 is complete: its q-reduction counters start the next step at zero
+    if (w == 0 && (int)threadIdx.x < ga.nqcnt) ga.qcnt[threadIdx.x] = 0;
     if (w >= ga.m) return;
     if constexpr (NV > 0)
       gather_reg<KPW, NV>(ga, w);
@@ -603,7 +847,7 @@ __global__ __launch_bounds__(256) void step_gather_kernel(const StepPlan *__rest
   const OpBatch &ob = pl->ob[1];
   const int tile = section_tile(w - gsec, ob.total);
   if (tile < 0) return;
-  __shared__ float sdq[LST_MAX_M];
+  __shared__ __align__(16) float sdq[LST_MAX_M];
   const float *dq = nullptr;
   if (ga.loss != LST_LOSS_SQUARED) {
     dq_all(ga, sdq);
@@ -635,11 +879,10 @@ __device__ void cheb_coeffs(double b, float *c) {
     for (int k = 0; k < 8; ++k) c[k] = 1.f;
     return;
   }
-  double y[8], f[8];
-  for (int i = 0; i < 8; ++i) {
-    y[i] = 0.5 * (1.0 + cos((2.0 * i + 1.0) * M_PI / 16.0));
-    f[i] = 1.0 / (1.0 - b * y[i]);
-  }
+  // (1 + cos((2i + 1) pi / 16)) / 2, i = 0..7: the Chebyshev points of [0, 1]
+  const double y[8] = {0.9903926402016152, 0.9157348061512727, 0.7777851165098011, 0.5975451610080642, 0.4024548389919359, 0.22221488349019902, 0.08426519384872733, 0.009607359798384785};
+  double f[8];
+  for (int i = 0; i < 8; ++i) f[i] = 1.0 / (1.0 - b * y[i]);
   for (int k = 1; k < 8; ++k)
     for (int i = 7; i >= k; --i) f[i] = (f[i] - f[i - 1]) / (y[i] - y[i - k]);
   // p(y) = f0 + (y - y0)(f1 + (y - y1)(f2 + ...)): expand from the innermost factor
@@ -765,7 +1008,11 @@ __device__ void cert_task(const CertArgs &ca, float lr) {
   if (!ok) exact_r(ca, lr);
 }
 
-// Yring^T Yring entry (i, j): the merge of the two examples' sorted slot lists.
+// Yring^T Yring entry (i, j) = sum over common rows r of (summed dl/dA of i at r) x
+// (summed dl/dA of j at r), from the two examples' merged slot lists: chunks of 16
+// entries of each list in registers (all loads of a chunk in flight together), every
+// pair compared.  The products of a matching pair meet in the same order for (i, j)
+// and (j, i) (rows ascending), so the matrix is exactly symmetric.
 __device__ __forceinline__ void yy_entry(int e, int m, int K, const int *__restrict__ srow,
                                          const float *__restrict__ sval,
                                          const int *__restrict__ scnt, float *__restrict__ YY) {
@@ -775,17 +1022,29 @@ __device__ __forceinline__ void yy_entry(int e, int m, int K, const int *__restr
   const float *vi = sval + (int64_t)i * K, *vj = sval + (int64_t)j * K;
   const int na = scnt[i], nb = scnt[j];
   float yy = 0.f;
-  int a = 0, b = 0;
-  while (a < na && b < nb) {
-    const int ra = ri[a], rb = rj[b];
-    if (ra == rb) {
-      yy += vi[a] * vj[b];
-      ++a;
-      ++b;
-    } else if (ra < rb) {
-      ++a;
-    } else {
-      ++b;
+  for (int a0 = 0; a0 < na; a0 += 16) {
+    int ra[16];
+    float va[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+      const bool in = a0 + u < na;
+      ra[u] = in ? ri[a0 + u] : -1;
+      va[u] = in ? vi[a0 + u] : 0.f;
+    }
+    for (int b0 = 0; b0 < nb; b0 += 16) {
+      int rb[16];
+      float vb[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const bool in = b0 + u < nb;
+        rb[u] = in ? rj[b0 + u] : -2;
+        vb[u] = in ? vj[b0 + u] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+#pragma unroll
+        for (int v = 0; v < 16; ++v)
+          if (ra[u] == rb[v]) yy = fmaf(va[u], vb[v], yy);
     }
   }
   YY[e] = yy;
@@ -802,7 +1061,7 @@ struct MidArgs {
   int *flag;
 };
 
-__global__ __launch_bounds__(256) void step_zgrad_kernel(const StepPlan *__restrict__ pl,
+__global__ __launch_bounds__(256, 5) void step_zgrad_kernel(const StepPlan *__restrict__ pl,
                                                          const float *H, float *gH, float lr,
                                                          const float *dq, const MidArgs ma,
                                                          const CertArgs ca) {
@@ -849,7 +1108,7 @@ __global__ __launch_bounds__(256) void step_zgrad_kernel(const StepPlan *__restr
 // Launch 4: Zq, R X and the U update.  Launch 5: the Q and U^{-T} updates and the
 // V scatter.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void step_mid_kernel(const StepPlan *__restrict__ pl,
+__global__ __launch_bounds__(256, 5) void step_mid_kernel(const StepPlan *__restrict__ pl,
                                                        const float *H, float *gH, float lr,
                                                        const float *dq,
                                                        const float *__restrict__ coef,
@@ -872,10 +1131,10 @@ __global__ __launch_bounds__(256) void step_mid_kernel(const StepPlan *__restric
   const GemmBatch &gb = pl->gb_mid;
   const int w2 = w - sec;
   if (w2 >= gb.total_tiles) return;
-  gemm_body<4>(gb, H, gH, lr, flag, w2);
+  gemm_body<4, 2>(gb, H, gH, lr, flag, w2);
 }
 
-__global__ __launch_bounds__(256) void step_update_kernel(const StepPlan *__restrict__ pl,
+__global__ __launch_bounds__(256, 5) void step_update_kernel(const StepPlan *__restrict__ pl,
                                                           const float *H, float *gH, float lr,
                                                           const int *__restrict__ flag, int n,
                                                           int K, int d,
@@ -883,18 +1142,17 @@ __global__ __launch_bounds__(256) void step_update_kernel(const StepPlan *__rest
                                                           const float *__restrict__ wA,
                                                           const float *__restrict__ RX, float *V,
                                                           int64_t ldv) {
-  const GemmBatch &gb = pl->gb_update;
   const int w = blockIdx.x;
-  const int sec = (gb.total_tiles + 7) & ~7;
-  if (w < sec) {
-    if (w >= gb.total_tiles) return;
-    gemm_body<4>(gb, H, gH, lr, flag, w);
+  const int ssec = (n + 7) & ~7;  // the scatter first: its workgroups are short
+  if (w >= ssec) {
+    gemm_body<4, 2>(pl->gb_update, H, gH, lr, flag, w - ssec);
     return;
   }
+  if (w >= n) return;
   extern __shared__ int sh[];
   if (*flag != 0) return;
   // V_r -= sum over the row's slots of (dl/dA_kj / (2 dl/dq_j)) (R X)_j
-  scatter_slot<256>(w - sec, n, K, d, 1.f, idx, wA, RX, V, ldv, sh);
+  scatter_slot<256>(w, n, K, d, 1.f, idx, wA, RX, V, ldv, sh);
 }
 
 }  // namespace
@@ -948,16 +1206,18 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
   const bool sq = sb.loss == LST_LOSS_SQUARED;
   const float *H = sym_H();
   float *gH = sym_gradH();
-  const int T = (d + 15) / 16;
-  (void)T;
   // Launch 1: H^ = H Q (row partials h . h^ -> qpart), H~ = H U^T, X = H U^{-T T}, N = H H^T
   {
     OpBatch &ob = pl.ob[0];
     ob.op[0] = op(m, d, d, H, d, 0, sb.Q, ldd, 0, sb.Hhat, d);
-    ob.op[0].rowred = RR_DOT;
-    ob.op[0].Rr = H;
-    ob.op[0].ldrr = d;
-    ob.op[0].rowout = sb.qpart;
+    if (!sq) {  // the spherical softmax's launch 2 needs every q_j at its start
+      ob.op[0].rowred = RR_DOT;
+      ob.op[0].Rr = H;
+      ob.op[0].ldrr = d;
+      ob.op[0].rowout = sb.qpart;
+      ob.op[0].qout = sb.q;
+      ob.op[0].qcnt = sb.qcnt;
+    }
     ob.op[1] = op(m, d, d, H, d, 0, sb.U, ldd, 0, sb.Htil, d);
     ob.op[2] = op(m, d, d, H, d, 0, sb.UinvT, ldd, 0, sb.X, d);
     ob.op[3] = op(m, m, d, H, d, 0, H, d, 0, sb.N, m);
@@ -1071,7 +1331,7 @@ void step_launch_sizes(const StepPlan &pl, int m, int K, int (&grid)[5]) {
   grid[1] = sec(m) + sec(pl.ob[1].total);
   grid[2] = sec(pl.ob[2].total) + (m * m + 255) / 256 + 2;
   grid[3] = sec(pl.ob[3].total) + pl.gb_mid.total_tiles;
-  grid[4] = sec(pl.gb_update.total_tiles) + m * K;
+  grid[4] = sec(m * K) + pl.gb_update.total_tiles;
 }
 
 void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, const StepPlan *dev,
@@ -1081,19 +1341,22 @@ void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, co
   const float *dqp = sb.loss == LST_LOSS_SQUARED ? nullptr : sb.dq;
   switch (which) {
     case 0:
-      LST_LAUNCH(step_contract_kernel, dim3(grid[0]), dim3(256), 0, s, dev, a.H, a.lr, a.idx, a.K,
-                 sb.V, sb.ldv, sb.D, sb.d, a.m);
+      LST_LAUNCH(step_contract_kernel, dim3(grid[0]), dim3(256), 0, s, dev, a.H, a.lr, a.idx,
+                 a.val, a.K, sb.V, sb.ldv, sb.D, sb.d, a.m, sb.tsum);
       break;
     case 1: {
       GatherArgs ga{};
       ga.K = a.K;
       ga.d = sb.d;
       ga.m = a.m;
-      ga.T = (sb.d + 15) / 16;
+      ga.Hhat = sb.Hhat;
+      ga.q = sb.q;
+      ga.tsum = sb.tsum;
+      ga.qcnt = sb.qcnt;
+      ga.nqcnt = (a.m + 15) / 16;
       ga.D = sb.D;
       ga.H = a.H;
       ga.Htil = sb.Htil;
-      ga.qpart = sb.qpart;
       ga.idx = a.idx;
       ga.val = a.val;
       ga.V = sb.V;

@@ -15,8 +15,8 @@
 //
 // Loads are branch free: a lane whose output row (column) lies beyond M (N)
 // reads the last valid row instead, since that output is never stored; only
-// the ragged end of the k range is masked.  Operands are fetched kStage
-// k-blocks ahead of the matrix cores.
+// the ragged end of the k range is masked.  Operands are fetched KS k-blocks
+// ahead of the matrix cores (kStage unless a launch needs fewer registers).
 #pragma once
 
 #include "lst_internal.h"
@@ -67,7 +67,7 @@ __device__ __forceinline__ void ld4_tail(const float *__restrict__ p, int64_t si
 // the first segment (k in [kbeg, kbeg + len1)) followed by the second (k in
 // [0, len2) of A2, B2), so that the loads of both are in flight together.  The
 // last block of a segment may be ragged (masked loads).
-template <int NW, int AM, int BM>
+template <int NW, int AM, int BM, int KS>
 __device__ __forceinline__ void kloop(floatx16 &acc, const float *A, int64_t asi, int64_t ask,
                                       const float *B, int64_t bsi, int64_t bsk, int len1,
                                       const float *A2, int64_t asi2, int64_t ask2, const float *B2,
@@ -99,16 +99,16 @@ __device__ __forceinline__ void kloop(floatx16 &acc, const float *A, int64_t asi
     }
   };
   if (nw == 0) return;
-  float a[kStage][4], b[kStage][4];
+  float a[KS][4], b[KS][4];
 #pragma unroll
-  for (int u = 0; u < kStage; ++u) load(u, a[u], b[u]);
-  for (int s0 = 0; s0 < nw; s0 += kStage) {
-    float an[kStage][4], bn[kStage][4];
+  for (int u = 0; u < KS; ++u) load(u, a[u], b[u]);
+  for (int s0 = 0; s0 < nw; s0 += KS) {
+    float an[KS][4], bn[KS][4];
 #pragma unroll
-    for (int u = 0; u < kStage; ++u)
-      if (s0 + kStage + u < nw) load(s0 + kStage + u, an[u], bn[u]);
+    for (int u = 0; u < KS; ++u)
+      if (s0 + KS + u < nw) load(s0 + KS + u, an[u], bn[u]);
 #pragma unroll
-    for (int u = 0; u < kStage; ++u) {
+    for (int u = 0; u < KS; ++u) {
       if (s0 + u < nw) {
 #pragma unroll
         for (int s = 0; s < 4; ++s)
@@ -116,7 +116,7 @@ __device__ __forceinline__ void kloop(floatx16 &acc, const float *A, int64_t asi
       }
     }
 #pragma unroll
-    for (int u = 0; u < kStage; ++u)
+    for (int u = 0; u < KS; ++u)
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
         a[u][s] = an[u][s];
@@ -132,7 +132,7 @@ __device__ __forceinline__ bool vec_ok(const float *p, int64_t ld) {
 // opA(i,k): tA = 0 -> A[i*lda + k] (index stride lda, k stride 1); tA = 1 -> A[k*lda + i].
 // opB(k,j): tB = 0 -> B[j*ldb + k];                                 tB = 1 -> B[k*ldb + j].
 // k runs over [kbeg, kend) of (A, B) and then over [0, K2) of (A2, B2).
-template <int NW>
+template <int NW, int KS>
 __device__ __forceinline__ void segment(floatx16 &acc, const float *A, int64_t lda, int tA,
                                         const float *B, int64_t ldb, int tB, const float *A2,
                                         int64_t lda2, const float *B2, int64_t ldb2, int K2,
@@ -144,7 +144,7 @@ __device__ __forceinline__ void segment(floatx16 &acc, const float *A, int64_t l
   const bool av = !tA && vec_ok(A, lda) && (K2 == 0 || vec_ok(A2, lda2));
   const bool bv = !tB && vec_ok(B, ldb) && (K2 == 0 || vec_ok(B2, ldb2));
 #define LST_KLOOP(AMODE, BMODE)                                                                    \
-  kloop<NW, AMODE, BMODE>(acc, A, asi, ask, B, bsi, bsk, kend - kbeg, A2, asi2, ask2, B2, bsi2, \
+  kloop<NW, AMODE, BMODE, KS>(acc, A, asi, ask, B, bsi, bsk, kend - kbeg, A2, asi2, ask2, B2, bsi2, \
                           bsk2, K2, ia, jb, kbeg, wave, lh)
   if (av && bv)
     LST_KLOOP(VEC, VEC);
@@ -177,7 +177,7 @@ __device__ __forceinline__ const float *resolve(const float *p, const float *H, 
   return v == 16 ? H : (v == 32 ? gH : p);
 }
 
-template <int NW>
+template <int NW, int KS = kStage>
 __device__ __forceinline__ void gemm_body(const GemmBatch &bt, const float *H, float *gH, float lr,
                                           const int *__restrict__ gate, int wg) {
   // The gate only suppresses writes, so its load is waited for at the end.
@@ -235,10 +235,10 @@ __device__ __forceinline__ void gemm_body(const GemmBatch &bt, const float *H, f
   if (g.splits > 1) {
     const int kbeg = split * g.kchunk;
     const int kend = min(g.K, kbeg + g.kchunk);
-    segment<NW>(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, nullptr, 0, nullptr, 0, 0, ia, jb, kbeg,
+    segment<NW, KS>(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, nullptr, 0, nullptr, 0, 0, ia, jb, kbeg,
                 kend, wave, lh);
   } else {
-    segment<NW>(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, g.A2, g.lda2, g.B2, g.ldb2, g.K2, ia, jb,
+    segment<NW, KS>(acc, g.A, g.lda, g.tA, g.B, g.ldb, g.tB, g.A2, g.lda2, g.B2, g.ldb2, g.K2, ia, jb,
                 0, g.K, wave, lh);
   }
 

@@ -183,6 +183,10 @@ struct Op16 {
   const float *Rr;
   int64_t ldrr;
   float *rowout;
+  // With qout: the last tile of each row block to finish (counted in qcnt[tile row],
+  // which the next launch resets) sums the row partials into qout[i].
+  float *qout;
+  int *qcnt;
   int alt;  // >= 0: the descriptor used instead when the Woodbury polynomial is not certified
 };
 
@@ -212,6 +216,8 @@ struct StepBufs {
   float *Hhat, *Htil, *X, *G, *Atil, *W1, *P2, *P3, *RX, *Zq;  // m x d
   float *N, *Mhat, *HZ, *YY, *E2, *E4, *R, *Cwork;             // m x m
   float *qpart, *bpart;  // row partials: [ceil(d/16)][m], [ceil(m/16)][m]
+  float *q, *tsum;       // m: q_j = h_j . h^_j, the sum of example j's valid target weights
+  int *qcnt;             // ceil(m/16) arrival counters of the q reduction
   float *dq, *lvec;      // m
   float *dA, *wA, *sval; // m x K
   int *srow, *scnt;      // m x K, m
