@@ -6,8 +6,10 @@ the naive O(D d) path and the fp64 CPU oracle as baselines.
 
 A step is one pass of the whole factored step (dense contractions, sparse
 gather, loss and grad_H, the m x m Woodbury block, the U / U^{-T} / Q updates
-and the V scatter) over one minibatch already resident in HBM.  Prints one JSON
-line.
+and the V scatter: five kernel launches) over one minibatch already resident in
+HBM.  Prints one JSON line: the headline workload (squared error, D=200k, d=500,
+m=128, K=5) with its roofline and baselines, and beside it the spherical-softmax
+and D=800k workloads and a compact D x d sweep with the measured crossover.
 """
 from __future__ import annotations
 
@@ -28,35 +30,29 @@ METRIC = "examples/s exact loss+grad+update, D=200k d=500 m=128; speedup vs naiv
 
 
 def phase_work(w, idx_pool):
-    """Algorithmic work per launch of each phase: (bound, amount, unit of amount).
+    """Algorithmic work per launch of each of the step's five launches: (bound, amount,
+    unit of amount).
 
-    bound "mfma": dense contractions, flops against the fp32 matrix peak; "hbm":
-    sparse V traffic, bytes against HBM bandwidth; "serial": the m x m Woodbury
-    inverse, a dependent chain of m pivots on one compute unit, reported by time.
+    bound "mfma": dense contractions, flops against the fp32 matrix peak; "hbm": the
+    sparse V traffic, bytes against HBM bandwidth.  Launch 2 (gather) also carries three
+    small products (H H^^T, E^2, E Xs: 2 (2 m^2 d + m^3) flops) beside the per-example
+    gather; its figure is the gather's bytes only.
     """
     m, d, K = w.m, w.d, w.K
     uniq = float(np.mean([len(np.unique(i[i >= 0])) for i in idx_pool]))
     return {
-        # H^, H~, X = {Q, U, U^-T} H: three m x d x d products
-        "contract": ("mfma", 2.0 * 3 * m * d * d, "flop"),
-        # N = H^T H (m x m x d)
-        "gram": ("mfma", 2.0 * m * m * d, "flop"),
-        # the m x K target rows of V plus H, H^, H~ read; G and the scaled H~ written
-        "gather": ("hbm", 4.0 * (m * K * d + 5 * m * d), "byte"),
-        # Z^ = U^T G (m d^2), H^T H^ and H~^T G (m^2 d each)
-        "zgrad": ("mfma", 2.0 * (m * d * d + 2 * m * m * d), "flop"),
-        # Gauss-Jordan inverse of the m x m Woodbury matrix: m^3 multiply-adds
-        "woodbury": ("serial", 2.0 * m ** 3, "flop"),
-        # loss sum and the m x m entries of M
-        "mblock": ("serial", 8.0 * m * m, "flop"),
-        # R X, M H (m^2 d each) and the U update (m d^2)
-        "mid": ("mfma", 2.0 * (m * d * d + 2 * m * m * d), "flop"),
-        # U^-T update (m d^2), Q update (2 m d^2), and for the spherical softmax P = X + N Yw
-        # (m^2 d); for squared error the same launch also carries the V scatter
-        "update": ("mfma", 2.0 * (3 * m * d * d + (m * m * d if w.loss != "squared" else 0)),
-                   "flop"),
-        # read-modify-write of the distinct target rows and the P rows they use
-        "scatter": ("hbm", 4.0 * (2 * uniq * d + m * d), "byte"),
+        # H^, H~, X = {Q, U, U^-T} H (3 m d^2) and N = H H^T (m^2 d)
+        "contract": ("mfma", 2.0 * (3 * m * d * d + m * m * d), "flop"),
+        # the m x K target rows of V and the m rows of H~ read; G and 2 eta D H~ written
+        "gather": ("hbm", 4.0 * (m * K * d + 3 * m * d), "byte"),
+        # Z^ = G U (m d^2), H~ G^T, E^2 Xs, E^2 W1 (m^2 d each), E^4 (m^3)
+        "zgrad": ("mfma", 2.0 * (m * d * d + 3 * m * m * d + m ** 3), "flop"),
+        # (eta^2/2) M H - eta grad_H and R X (m^2 d each), the U update (m d^2)
+        "mid": ("mfma", 2.0 * (2 * m * m * d + m * d * d), "flop"),
+        # the U^-T update (m d^2) and the Q update (2 m d^2); the V scatter's read-modify-write
+        # of the distinct target rows rides in the same launch
+        "update": ("mfma", 2.0 * 3 * m * d * d, "flop"),
+        "scatter_bytes": ("hbm", 4.0 * (2 * uniq * d + m * K * d), "byte"),
     }
 
 
@@ -64,7 +60,7 @@ def kernel_table(phases, work):
     """Per-phase average duration and, where a roofline applies, its fraction."""
     out = {}
     for name, (bound, amount, unit) in work.items():
-        cnt, ms = phases.get(name, (0, 0.0))
+        cnt, ms = phases.get("update" if name == "scatter_bytes" else name, (0, 0.0))
         if not cnt:
             continue
         avg_s = ms / cnt / 1e3
@@ -80,17 +76,19 @@ def kernel_table(phases, work):
     return out
 
 
-def load_traffic():
-    """Per-launch HBM bytes measured by hardware counters (traffic.json, written by
-    paper_1606_08061_amd.traffic_from_pmc), per phase, kept only while the kernel's
-    source file is unchanged since the counters were taken."""
-    from paper_1606_08061_amd.traffic_from_pmc import source_sha
+TRAFFIC_MD = os.path.join(ROOT, "profiles", "factored_step_sq_D200k_d500_m128_K5_pmc_traffic.md")
 
-    path = os.path.join(ROOT, "paper_1606_08061_amd", "traffic.json")
-    if not os.path.exists(path):
+
+def load_traffic():
+    """Per-launch HBM bytes measured by hardware counters (the JSON block of the traffic
+    summary under profiles/, written by bench_pmc.py), per phase, kept only while the
+    kernel's sources are unchanged since the counters were taken."""
+    from bench_pmc import read_traffic_block, source_sha
+
+    if not os.path.exists(TRAFFIC_MD):
         return {}
     out = {}
-    for phase, r in json.load(open(path)).get("phases", {}).items():
+    for phase, r in read_traffic_block(TRAFFIC_MD).items():
         try:
             same = source_sha(r["source"]) == r["source_sha256"]
         except OSError:
@@ -101,10 +99,8 @@ def load_traffic():
 
 
 def roofline_for(table, traffic=None):
-    """The dominant kernel: the longest of the kernels a roofline applies to (the
-    dense contractions and the sparse V passes).  The serial m x m inverse runs on
-    a side stream and is reported by its time only."""
-    name = max((k for k in table if table[k]["bound"] in ("mfma", "hbm")),
+    """The dominant kernel: the longest of the step's launches."""
+    name = max((k for k in table if k != "scatter_bytes" and table[k]["bound"] in ("mfma", "hbm")),
                key=lambda k: table[k]["avg_us"])
     r = table[name]
     return {"kernel_phase": name, "bound": r["bound"], "achieved": r["achieved"], "peak": r["peak"],
@@ -174,69 +170,120 @@ def cpu_baseline(w, V0, pool, seconds, threads=None):
                       f"affinity={len(os.sched_getaffinity(0))}"}
 
 
-def run_sweep(args):
-    """Factored vs naive ms/step over the D x d sweep (squared error, m=512, K=5), one
-    JSON line per config plus a line with the measured crossover per d."""
+def device_stream(w, dev, n, seed):
+    """V0 and n minibatches of a workload, on the device: V0 and H drawn on the GPU
+    (torch's generator, seeded: these legs are timed, not compared with the oracle),
+    the targets by the workload's own index and value laws (numpy PCG64, seeded)."""
+    import torch
+
+    from workloads import ZipfSampler, make_targets
+
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    V0 = torch.randn((w.D, w.d), device=dev, generator=g).mul_(float(1.0 / np.sqrt(w.d)))
+    rng = np.random.default_rng(seed)
+    zipf = ZipfSampler(w.D, w.zipf_s) if w.index_dist == "zipf" else None
+    batches, idxs = [], []
+    for _ in range(n):
+        H = torch.randn((w.m, w.d), device=dev, generator=g).mul_(float(1.0 / np.sqrt(w.d)))
+        idx, val = make_targets(rng, w, None, zipf)
+        idxs.append(idx)
+        batches.append((H.contiguous(), torch.from_numpy(idx).to(dev), torch.from_numpy(val).to(dev)))
+    return V0, batches, idxs
+
+
+def timed(step, batches, n, warm, lr, grad):
+    """ms per step over n steps (HIP events on the current stream) after warm steps."""
+    import torch
+
+    for t in range(warm):
+        step(*batches[t % len(batches)], lr, grad_H=grad)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for t in range(n):
+        step(*batches[t % len(batches)], lr, grad_H=grad)
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / n
+
+
+def factored_vs_naive(w, dev, seed, steps, naive_steps, profile=False):
+    """Factored and naive ms/step on the same device-drawn batches of workload w."""
     import torch
 
     import paper_1606_08061_amd as lst
+
+    V0, batches, idxs = device_stream(w, dev, 8, seed)
+    grad = torch.empty((w.m, w.d), dtype=torch.float32, device=dev)
+    eps = float(np.float32(w.eps))
+    f = lst.Factored(w.D, w.d, w.m, w.K, w.loss, eps, device=dev)
+    f.init(V0)
+    fms = timed(f.step, batches, steps, 8, w.lr, grad)
+    f.check(f"factored steps of {w.name}")
+    row = {"workload": w.name, "loss": w.loss, "D": w.D, "d": w.d, "m": w.m, "K": w.K,
+           "index_dist": w.index_dist, "factored_ms_per_step": round(fms, 5),
+           "examples_per_s": round(w.m / (fms / 1e3), 1)}
+    if profile:
+        f.profile(True)
+        for t in range(steps):
+            f.step(*batches[t % len(batches)], w.lr, grad_H=grad)
+        table = kernel_table(f.profile_read(), phase_work(w, idxs))
+        f.profile(False)
+        f.check(f"profiled steps of {w.name}")
+        r = roofline_for(table)
+        row["roofline"] = {k: r[k] for k in ("kernel_phase", "bound", "achieved", "peak", "unit",
+                                                 "frac", "avg_launch_us")}
+        row["phases_us"] = {k: v["avg_us"] for k, v in table.items() if k != "scatter_bytes"}
+    f.close()
+    n = lst.Naive(w.D, w.d, w.m, w.K, w.loss, eps, device=dev)
+    n.init(V0)
+    nms = timed(n.step, batches, naive_steps, 2, w.lr, grad)
+    n.check(f"naive steps of {w.name}")
+    n.close()
+    del V0, batches, f, n
+    torch.cuda.empty_cache()
+    row.update(naive_ms_per_step=round(nms, 4), speedup_vs_naive=round(nms / fms, 2),
+               D_over_4d=round(w.D / (4 * w.d), 1))
+    return row
+
+
+def sweep_rows(fsteps, nsteps, emit=None):
+    """Factored vs naive over the D x d sweep (squared error, m = 512, K = 5) and the
+    measured crossover (speedup 1, log-linear between the bracketing D) per d."""
     from workloads import sweep_workloads
+
+    import torch
 
     dev = torch.device("cuda:0")
     res = []
     for w in sweep_workloads():
-        g = torch.Generator(device=dev)
-        g.manual_seed(w.D * 7 + w.d)
-        V0 = torch.randn((w.D, w.d), device=dev, generator=g) * (1.0 / np.sqrt(w.d))
-        batches = []
-        for t in range(4):
-            H = torch.randn((w.m, w.d), device=dev, generator=g) * (1.0 / np.sqrt(w.d))
-            idx = torch.randint(0, w.D, (w.m, w.K), device=dev, generator=g, dtype=torch.int32)
-            val = torch.randn((w.m, w.K), device=dev, generator=g)
-            batches.append((H.contiguous(), idx, val))
-        grad = torch.empty((w.m, w.d), device=dev)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-
-        def timed(step, n):
-            for t in range(3):
-                step(*batches[t % 4], w.lr, grad_H=grad)
-            torch.cuda.synchronize()
-            e0.record()
-            for t in range(n):
-                step(*batches[t % 4], w.lr, grad_H=grad)
-            e1.record()
-            torch.cuda.synchronize()
-            return e0.elapsed_time(e1) / n
-
-        f = lst.Factored(w.D, w.d, w.m, w.K, w.loss, float(np.float32(w.eps)), device=dev)
-        f.init(V0)
-        fms = timed(f.step, args.sweep_steps)
-        f.check("sweep factored")
-        f.close()
-        n = lst.Naive(w.D, w.d, w.m, w.K, w.loss, float(np.float32(w.eps)), device=dev)
-        n.init(V0)
-        nms = timed(n.step, max(2, args.sweep_steps // 4))
-        n.check("sweep naive")
-        n.close()
-        del V0, batches
-        torch.cuda.empty_cache()
-        row = {"sweep": w.name, "D": w.D, "d": w.d, "m": w.m, "K": w.K,
-               "factored_ms_per_step": round(fms, 4), "naive_ms_per_step": round(nms, 4),
-               "speedup": round(nms / fms, 3), "D_over_4d": round(w.D / (4 * w.d), 2)}
+        r = factored_vs_naive(w, dev, w.D * 7 + w.d, fsteps, nsteps)
+        row = {"D": w.D, "d": w.d, "factored_ms": r["factored_ms_per_step"],
+               "naive_ms": r["naive_ms_per_step"], "speedup": r["speedup_vs_naive"],
+               "D_over_4d": r["D_over_4d"]}
         res.append(row)
-        print(json.dumps(row), flush=True)
+        if emit:
+            emit(row)
     cross = {}
     for d in sorted({r["d"] for r in res}):
         pts = sorted((r["D"], r["speedup"]) for r in res if r["d"] == d)
         c = None
         for (D0, s0), (D1, s1) in zip(pts, pts[1:]):
-            if s0 < 1.0 <= s1:  # log-linear interpolation of speedup = 1
+            if s0 < 1.0 <= s1:
                 t = (0.0 - np.log(s0)) / (np.log(s1) - np.log(s0))
                 c = float(np.exp(np.log(D0) + t * (np.log(D1) - np.log(D0))))
                 break
         if c is None and pts and pts[0][1] >= 1.0:
             c = f"below {pts[0][0]}"
         cross[str(d)] = c if not isinstance(c, float) else round(c, 1)
+    return res, cross
+
+
+def run_sweep(args):
+    """The sweep as JSON lines: one per configuration, then the crossover per d."""
+    res, cross = sweep_rows(args.sweep_steps, max(2, args.sweep_steps // 4),
+                            emit=lambda r: print(json.dumps(r), flush=True))
     print(json.dumps({"sweep_crossover_D": cross, "m": 512, "K": 5}), flush=True)
 
 
@@ -321,9 +368,9 @@ def stabilize_leg(f, w, dev, reps=5):
 
 def online_leg(w, dev, V0, gpool, steps=2000, general_steps=300):
     """The online step (m = 1, squared error, Algorithm 2) on the benchmark's V: the first
-    example of each pooled minibatch, through the single cooperative launch and through the
-    general step path (LST_ONLINE_KERNEL=0).  Algorithmic bytes per step: Q, U, U^{-T} read
-    and written once (6 d^2 floats; the K target rows of V add 8 K d)."""
+    example of each pooled minibatch, through the single launch with its bounded grid barrier
+    and through the general step path (LST_OPT_ONLINE_KERNEL = 0).  Algorithmic bytes per
+    step: Q, U, U^{-T} read and written once (6 d^2 floats; the K target rows of V add 8 K d)."""
     import torch
 
     import paper_1606_08061_amd as lst
@@ -331,11 +378,9 @@ def online_leg(w, dev, V0, gpool, steps=2000, general_steps=300):
     ex = [[t[:1].contiguous() for t in b] for b in gpool]
     grad = torch.empty((1, w.d), dtype=torch.float32, device=dev)
     out = {}
-    for name, n, env in (("fused", steps, None), ("general", general_steps, "0")):
-        if env is not None:
-            os.environ["LST_ONLINE_KERNEL"] = env
+    for name, n, online in (("fused", steps, 1), ("general", general_steps, 0)):
         f = lst.Factored(w.D, w.d, 1, w.K, "squared", device=dev)
-        os.environ.pop("LST_ONLINE_KERNEL", None)
+        f.set_option(lst.LST_OPT_ONLINE_KERNEL, online)
         f.init(V0)
         for t in range(64):
             f.step(*ex[t % len(ex)], w.lr, grad_H=grad)
@@ -434,14 +479,11 @@ def main():
     ap.add_argument("--sweep", action="store_true",
                     help="factored vs naive over the D x d sweep instead of the default line")
     ap.add_argument("--sweep-steps", type=int, default=20)
-    ap.add_argument("--one-stream", action="store_true",
-                    help="enqueue the whole step on one stream (for hardware counter "
-                         "collection, which runs one dispatch at a time)")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the spherical-softmax, D=800k and sweep legs")
     ap.add_argument("--copy-calib", type=int, default=0, metavar="MIB",
                     help="also run one plain device copy of MIB MiB (hardware-counter calibration)")
     args = ap.parse_args()
-    if args.one_stream:
-        os.environ["LST_ONE_STREAM"] = "1"  # read by the library when a context is created
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py runs on exactly one GPU: the factored step is measured on one GPU's "
               "share (multi-GPU sharding of V by rows is described but not built)",
@@ -476,8 +518,8 @@ def main():
     f = lst.Factored(w.D, w.d, w.m, w.K, w.loss, float(np.float32(w.eps)), device=dev)
     f.init(V0)
     grad = torch.empty((w.m, w.d), dtype=torch.float32, device=dev)
-    # Warm-up with exactly the timed calls: every (batch, output) argument set is
-    # recorded as a HIP graph here, so the timed region only replays graphs.
+    # Warm-up with exactly the timed calls (the step's descriptors for this m are
+    # built and copied on the first call).
     for t in range(max(args.warmup, len(gpool))):
         f.step(*gpool[t % len(gpool)], w.lr, grad_H=grad)
     f.check("warm-up")
@@ -568,6 +610,17 @@ def main():
 
     del V0, gpool
     torch.cuda.empty_cache()
+    secondary = sweep = None
+    if not args.no_secondary:
+        from workloads import WORKLOADS as WL
+
+        secondary = {}
+        for name in ("sphsm_D200k_d500_m128_zipf", "sq_D800k_d512_m256_K10_zipf"):
+            print(f"[bench] secondary workload {name}", file=sys.stderr, flush=True)
+            secondary[name] = factored_vs_naive(WL[name], dev, 11, 300, 8, profile=True)
+        print("[bench] D x d sweep", file=sys.stderr, flush=True)
+        pts, cross = sweep_rows(10, 3)
+        sweep = {"m": 512, "K": 5, "loss": "squared", "points": pts, "crossover_D": cross}
     att = None
     if not (args.no_peaks or args.copy_calib):  # counter runs take the copy as their scale
         att = attainable_peaks(dev)
@@ -595,11 +648,12 @@ def main():
         "speedup_model_D_over_4d": round(w.D / (4 * w.d), 1),
         "host_enqueue_us_per_step": round(host_us, 2),
         "kernels": table,
-        "serial_inverse_us": table.get("woodbury", {}).get("avg_us"),
         "attainable": att,
         "stabilize": stab,
         "online": online,
         "input_layer": inp,
+        "secondary": secondary,
+        "sweep": sweep,
     }
     print(json.dumps(out), flush=True)
 

@@ -9,6 +9,7 @@ import pytest
 import torch
 
 from gpu_common import DEV, Compare, make_factored, oracle_step, rel, to_dev
+from oracle import dense_step
 from workloads import LOSS_SPHERICAL_SOFTMAX, LOSS_SQUARED, WORKLOADS, Stream, Workload
 
 pytestmark = pytest.mark.gpu
@@ -79,29 +80,108 @@ def test_spherical_softmax_zipf_steps():
     c.close()
 
 
+def _dup_batch(c, t):
+    H, idx, val = c.s.batch()
+    idx[0, 1] = idx[0, 0]
+    idx[1, 2] = -1
+    if t % 3 == 0:
+        idx[2, :] = -1
+    return H, idx, val
+
+
 @pytest.mark.parametrize("loss,D,K", [
     (LOSS_SQUARED, 9, 3), (LOSS_SPHERICAL_SOFTMAX, 9, 3), (LOSS_SQUARED, 40, 16),
     (LOSS_SQUARED, 60, 20),
 ])
 def test_duplicates_and_empty_slots(loss, D, K):
     # small D under Zipf: rows repeat across examples; some examples repeat an index or have
-    # -1.  K <= 16 takes the M kernel's direct K x K compare, K = 20 its sorted-list merge
-    # (the same kernel for both losses).  Not the spherical softmax at K = 16 of D = 40: with
-    # most classes targeted, many a_kj sit near 0 where d/da of a / (a^2 + eps) is 1/eps, and
-    # fp32 rounding of a alone then exceeds the 100-step tolerance (both M paths alike).
+    # -1; Yring^T Yring from the merged slot lists (K = 20: two 16-entry chunks).
     w = Workload("t", loss, D, 8, 24, K, index_dist="zipf",
                  value_dist="normal" if loss == LOSS_SQUARED else "ones")
     c = Compare(w)
     for t in range(10):
-        H, idx, val = c.s.batch()
-        idx[0, 1] = idx[0, 0]
-        idx[1, 2] = -1
-        if t % 3 == 0:
-            idx[2, :] = -1
-        st, l, g, ref = c.step((H, idx, val))
+        st, l, g, ref = c.step(_dup_batch(c, t))
         _check_step(st, l, g, ref, TOL1 if t == 0 else TOL100)
     assert rel(c.W_gpu(), c.W) <= TOL100
     c.close()
+
+
+def test_duplicates_spherical_softmax_most_classes_targeted():
+    # The spherical softmax with K = 16 slots over D = 40 classes (Zipf), the same repeated
+    # and empty slots.  With most classes targeted many a_kj sit near 0, where d/da of
+    # a / (a^2 + eps) is 1 / eps, and this workload's trajectory magnifies any rounding
+    # difference about fourfold per step: the dense definition itself, run in fp32 along its
+    # own trajectory, is 3.5e-3 away from the fp64 one after ten steps.  Parity is therefore
+    # taken one step at a time from the GPU's own state: the oracle steps W = V U formed in
+    # fp64 from the context's fp32 V and U, and the step's loss, grad_H and updated V U must
+    # match it to 1e-4 (the fp32 definition is within 1e-6 of it from the same state).
+    w = Workload("t", LOSS_SPHERICAL_SOFTMAX, 40, 8, 24, 16, index_dist="zipf",
+                 value_dist="ones")
+    c = Compare(w)
+
+    def W_exact():
+        return c.ctx.V.double().cpu().numpy() @ c.ctx.U.double().cpu().numpy()
+
+    for t in range(30):
+        H, idx, val = _dup_batch(c, t)
+        ref = oracle_step(W_exact(), H, idx, val, w)
+        loss, grad = c.ctx.step(*to_dev(H, idx, val), w.lr)
+        assert c.ctx.sync_status() == 0
+        assert abs(loss.item() - ref.loss) <= TOL1 * abs(ref.loss), t
+        assert rel(grad.cpu().numpy(), ref.grad_H) <= TOL1, t
+        assert rel(W_exact(), ref.W_new) <= TOL1, t
+    c.close()
+
+
+@pytest.mark.parametrize("loss,d", [(LOSS_SQUARED, 512), (LOSS_SQUARED, 1024),
+                                    (LOSS_SQUARED, 700), (LOSS_SPHERICAL_SOFTMAX, 700)])
+def test_sweep_minibatch_m512(loss, d):
+    # the sweep's m = 512 (32 tile rows of every m x m product of the Woodbury polynomial;
+    # 512 < d <= 1024 takes the gather with 16 columns per lane; d = 700 is no multiple of
+    # 64), at D = 20000: the whole updated W after one step, and a second step.
+    K = 5 if loss == LOSS_SQUARED else 1
+    w = Workload("t", loss, 20000, d, 512, K,
+                 value_dist="normal" if loss == LOSS_SQUARED else "ones")
+    c = Compare(w, seed=d)
+    st, l, g, ref = c.step()
+    _check_step(st, l, g, ref)
+    assert rel(c.W_gpu(), ref.W_new) <= TOL1
+    st, l, g, ref = c.step()
+    _check_step(st, l, g, ref, TOL100)
+    assert rel(c.W_gpu(), c.W) <= TOL100
+    c.close()
+
+
+def _poly_bound(H, dq, lr):
+    """||E^2||_inf^(1/2) of E = 2 lr S H H^T S (S = diag(dq)^(1/2)), in fp64: the bound on the
+    spectral radius the step's certificate takes."""
+    Hs = np.sqrt(dq)[:, None] * H.astype(np.float64)
+    E = 2.0 * float(lr) * (Hs @ Hs.T)
+    return float(np.sqrt(np.abs(E @ E).sum(1).max()))
+
+
+@pytest.mark.parametrize("m,d", [(64, 32), (200, 48)])
+def test_uncertified_woodbury_takes_exact_elimination(m, d):
+    # Steps large enough (2 eta lambda_max(H H^T) = 0.6) that the degree-7 polynomial cannot
+    # certify C^{-1} = (I - 2 eta H H^T)^{-1} (its bound needs ||E^2||^(1/2) <= 0.3), while C is
+    # still positive definite: one workgroup inverts C by exact elimination (m = 200: beyond
+    # the 128 rows the tiles of one product hold), and the step matches the oracle.
+    w = Workload("t", LOSS_SQUARED, 3000, d, m, 3)
+    s = Stream(w, seed=m)
+    f = make_factored(w, s.V0)
+    W = s.V0.astype(np.float64)
+    for t in range(3):
+        H, idx, val = s.batch()
+        lam = float(np.linalg.eigvalsh(H.astype(np.float64) @ H.astype(np.float64).T).max())
+        lr = float(np.float32(0.3 / lam))
+        assert _poly_bound(H, np.ones(m), lr) > 0.31  # not certifiable
+        ref = dense_step(W, H, idx, val, np.float32(lr), w.loss)
+        loss, grad = f.step(*to_dev(H, idx, val), lr)
+        st = f.sync_status()
+        _check_step(st, loss.item(), grad.cpu().numpy(), ref, TOL1 if t == 0 else TOL100)
+        W = ref.W_new
+    assert rel(f.materialize_W().cpu().numpy(), W) <= TOL100
+    f.close()
 
 
 def test_all_slots_same_row():
