@@ -187,6 +187,38 @@ int lst_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, const fl
 int lst_use_graphs(lst_ctx *c, int32_t on);
 
 /*
+ * lst_step_noalloc -- for callers that cannot allocate device memory (code under
+ * stream capture, tight serving loops, hosts that forbid allocation): lst_step
+ * without a context or workspace, on the same kernels.  The state (V, U, UinvT, Q,
+ * as in lst_create) and the step's arguments (as in lst_step) are passed directly;
+ * the step's descriptors and intermediates live in a device array of 16 MiB that
+ * the library holds on each GPU it runs on until the process ends.  The call
+ * allocates and frees nothing.
+ *   m, K         0 <= m <= LST_MAX_M, 0 <= K <= LST_MAX_K, m K <= 8192, and the
+ *                step must fit the array: 4 (11 m d + 8 m^2) bytes plus about
+ *                4 (m (d + m) / 16 + 4 m K + 7 m) + 16 KiB (m = 128 fits up to
+ *                d = 2863, m = 256 up to d = 1290, m = 512 up to d = 364);
+ *                LST_E_SHAPE beyond it.
+ *   status_dev   device int32, set to 0 by the call, then ORed by the kernels with
+ *                1 (a target index outside [-1, D)), 2 (the Woodbury matrix is not
+ *                positive definite) or 4 (the loss is not finite); a nonzero value
+ *                means the step changed no state.  Read it after the stream is done.
+ *   stream       hipStream_t as void*; it must belong to the current device
+ *                (LST_E_ARG otherwise), as must every buffer.
+ * Every call on one GPU shares that GPU's array, which keeps the last call's
+ * contents: calls that overlap on one GPU (different streams or host threads
+ * without ordering between them) race and give wrong results; calls ordered on
+ * one stream do not.  The first call on a device looks up the array's address
+ * there; a call whose descriptors differ from the previous call's (another m, d,
+ * K, loss or state buffers) rewrites them with a few extra small launches.
+ * Results equal lst_step's on the same state (m = 1 takes the five-launch path).
+ */
+int lst_step_noalloc(int64_t D, int32_t d, int32_t loss, float eps, float *V, int64_t ldv, float *U,
+                     float *UinvT, float *Q, int32_t ldd, const float *H, int32_t m,
+                     const int32_t *idx, const float *val, int32_t K, float lr, float *loss_dev,
+                     float *grad_H, int32_t *status_dev, void *stream);
+
+/*
  * lst_materialize_W -- W = V U into a D x ldw device buffer (section 5.1: the
  * explicit weights, an O(D d^2) product).  For a naive context, copies its W.
  */

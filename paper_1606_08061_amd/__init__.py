@@ -13,6 +13,6 @@ from ._binding import (  # noqa: F401
     lst_use_graphs, lst_restore_pristine, lst_refresh_uinvt, lst_power_iteration,
     lst_fix_singular_value, lst_singular_stabilize, lst_input_forward, lst_input_update,
     SparseInput, LST_OPT_ONLINE_KERNEL, LST_OPT_SPIN_LIMIT, lst_set_option, lst_workspace_bytes,
-    lst_naive_workspace_bytes,
+    lst_naive_workspace_bytes, lst_step_noalloc,
     lst_step, lst_sync_status, status_string, PHASES,
 )

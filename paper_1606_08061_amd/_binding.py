@@ -55,6 +55,8 @@ SIGNATURES = {
     "lst_profile_read": (_I32, [_P, ctypes.POINTER(_I32), ctypes.POINTER(ctypes.c_double), _I32]),
     "lst_input_forward": (_I32, [_P, _I64, _I64, _I32, _P, _P, _I32, _I32, _P, _P, _P]),
     "lst_input_update": (_I32, [_P, _I64, _I64, _I32, _P, _P, _I32, _I32, _P, _F, _P, _P]),
+    "lst_step_noalloc": (_I32, [_I64, _I32, _I32, _F, _P, _I64, _P, _P, _P, _I32, _P, _I32, _P, _P,
+                                _I32, _F, _P, _P, _P, _P]),
     "lst_restore_pristine": (_I32, [_P]),
     "lst_refresh_uinvt": (_I32, [_P, _I32, _I32, _P]),
     "lst_power_iteration": (_I32, [_P, _I32, _I32, _P, _P, _P]),
@@ -193,6 +195,12 @@ def lst_input_forward(W1, ldw, D_in, d, idx, val, m, K, A, status, stream) -> in
 
 def lst_input_update(W1, ldw, D_in, d, idx, val, m, K, grad_A, lr, status, stream) -> int:
     return lib().lst_input_update(W1, ldw, D_in, d, idx, val, m, K, grad_A, lr, status, stream)
+
+
+def lst_step_noalloc(D, d, loss, eps, V, ldv, U, UinvT, Q, ldd, H, m, idx, val, K, lr, loss_dev,
+                     grad_H, status, stream) -> int:
+    return lib().lst_step_noalloc(D, d, loss, eps, V, ldv, U, UinvT, Q, ldd, H, m, idx, val, K, lr,
+                                  loss_dev, grad_H, status, stream)
 
 
 class SparseInput:

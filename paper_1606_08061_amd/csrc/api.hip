@@ -5,6 +5,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <memory>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -118,11 +119,11 @@ size_t init_partial_floats(int64_t D, int d) {
   return std::min(want, kInitPartialCap / ((size_t)d * d) * ((size_t)d * d));
 }
 
-void carve_factored(lst_ctx *c, Carver &cv) {
-  const size_t m = (size_t)c->m_max, d = (size_t)c->d;
-  const size_t md = m * d, mm = m * m;
-  const size_t mk = m * (c->K_max > 0 ? c->K_max : 1);
-  StepBufs &b = c->sb;
+// The step's intermediates for minibatches of up to m examples with up to K slots
+// each (m x d, m x m, per-example and per-slot pieces), and grad_H's stand-in for
+// steps given no grad_H buffer.
+void carve_step(StepBufs &b, float *&gradH, size_t m, size_t d, size_t K, Carver &cv) {
+  const size_t md = m * d, mm = m * m, mk = m * (K > 0 ? K : 1);
   b.Hhat = cv.take<float>(md);
   b.Htil = cv.take<float>(md);
   b.X = cv.take<float>(md);
@@ -133,7 +134,7 @@ void carve_factored(lst_ctx *c, Carver &cv) {
   b.P3 = cv.take<float>(md);
   b.RX = cv.take<float>(md);
   b.Zq = cv.take<float>(md);
-  c->gradH = cv.take<float>(md);
+  gradH = cv.take<float>(md);
   b.N = cv.take<float>(mm);
   b.Mhat = cv.take<float>(mm);
   b.HZ = cv.take<float>(mm);
@@ -156,6 +157,11 @@ void carve_factored(lst_ctx *c, Carver &cv) {
   b.scnt = cv.take<int>(m);
   b.coef = cv.take<float>(8);
   b.cert = cv.take<int>(1);
+}
+
+void carve_factored(lst_ctx *c, Carver &cv) {
+  const size_t d = (size_t)c->d;
+  carve_step(c->sb, c->gradH, (size_t)c->m_max, d, (size_t)c->K_max, cv);
   c->Sd0 = cv.take<float>(d * d);
   c->Sd1 = cv.take<float>(d * d);
   c->svec = cv.take<float>(4 * d);
@@ -166,7 +172,7 @@ void carve_factored(lst_ctx *c, Carver &cv) {
   c->flag = cv.take<int>(1);
   c->cnt = cv.take<int>(4);
   c->plan_pool = cv.take<StepPlan>(kPlanCap);
-  b.flag = c->flag;
+  c->sb.flag = c->flag;
 }
 
 // Upper bound of the split-k partial buffer of grad_H = grad_O^T W for any m <= m_max:
@@ -1046,6 +1052,148 @@ int lst_input_update(float *W1, int64_t ldw, int64_t D_in, int32_t d, const int3
   const hipError_t e = launch_input_update(static_cast<hipStream_t>(stream), W1, ldw, D_in, d, idx,
                                            val, m, K, grad_A, lr, status_dev);
   return e == hipSuccess ? LST_OK : LST_E_HIP;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// lst_step_noalloc: the factored step with its intermediates in a fixed device array
+// ---------------------------------------------------------------------------
+
+namespace {
+
+constexpr size_t kScratchBytes = size_t(16) << 20;
+constexpr int kScratchDevices = 16;
+
+}  // namespace
+
+// The step's descriptors and intermediates of lst_step_noalloc.  Each device holds its
+// own copy at its own address, obtained once per device with hipGetSymbolAddress; host
+// code uses that address only (the symbol's name is not a device address on the host).
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+struct ScratchDev {
+  char *base;        // this device's copy of scratch, null until set up
+  bool plan_valid;   // plan holds the descriptors last written to the array
+  StepPlan plan;
+};
+ScratchDev g_scratch[kScratchDevices];
+std::mutex g_scratch_mu;
+
+constexpr int kChunkWords = 512;  // 2 KiB of kernel arguments per launch
+struct WordChunk {
+  uint32_t w[kChunkWords];
+};
+
+__global__ void __launch_bounds__(256) put_words_kernel(uint32_t *dst, WordChunk c, int n) {
+  for (int i = (int)threadIdx.x; i < n; i += 256) dst[i] = c.w[i];
+}
+
+__global__ void __launch_bounds__(64) clear_words_kernel(int *a, int na, int *b, int nb) {
+  for (int i = (int)threadIdx.x; i < na; i += 64) a[i] = 0;
+  for (int i = (int)threadIdx.x; i < nb; i += 64) b[i] = 0;
+}
+
+// Bytes of the array a step of m examples, K slots and hidden size d takes: the
+// descriptors first, then the intermediates.
+size_t noalloc_bytes(int m, int d, int K) {
+  Carver cv{nullptr};
+  cv.take<StepPlan>(1);
+  StepBufs b{};
+  float *g = nullptr;
+  carve_step(b, g, (size_t)m, (size_t)d, (size_t)K, cv);
+  return cv.off;
+}
+
+// Writes the descriptors into the array with kernel arguments (no host buffer has to
+// outlive the call), unless the array already holds these exact descriptors.
+hipError_t put_plan(ScratchDev &sd, const StepPlan &pl, hipStream_t s) {
+  static_assert(sizeof(StepPlan) % sizeof(uint32_t) == 0, "plan is copied in words");
+  if (sd.plan_valid && std::memcmp(&sd.plan, &pl, sizeof(StepPlan)) == 0) return hipSuccess;
+  sd.plan_valid = false;
+  const uint32_t *src = reinterpret_cast<const uint32_t *>(&pl);
+  uint32_t *dst = reinterpret_cast<uint32_t *>(sd.base);
+  const int words = (int)(sizeof(StepPlan) / sizeof(uint32_t));
+  for (int o = 0; o < words; o += kChunkWords) {
+    WordChunk c;
+    const int n = std::min(kChunkWords, words - o);
+    std::memcpy(c.w, src + o, (size_t)n * sizeof(uint32_t));
+    hipLaunchKernelGGL(put_words_kernel, dim3(1), dim3(256), 0, s, dst + o, c, n);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  std::memcpy(&sd.plan, &pl, sizeof(StepPlan));
+  sd.plan_valid = true;
+  return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+int lst_step_noalloc(int64_t D, int32_t d, int32_t loss, float eps, float *V, int64_t ldv, float *U,
+                     float *UinvT, float *Q, int32_t ldd, const float *H, int32_t m,
+                     const int32_t *idx, const float *val, int32_t K, float lr, float *loss_dev,
+                     float *grad_H, int32_t *status_dev, void *stream) {
+  const int mm = m < 1 ? 1 : m;
+  int st = common_args(D, d, mm, K, loss, eps);
+  if (st != LST_OK) return st;
+  if (!V || !U || !UinvT || !Q || !loss_dev || !status_dev) return LST_E_ARG;
+  if (ldv < d || ldd < d) return LST_E_SHAPE;
+  if (m < 0) return LST_E_SHAPE;
+  if (m > 0 && !H) return LST_E_ARG;
+  if (m > 0 && K > 0 && (!idx || !val)) return LST_E_ARG;
+  if (!finite_pos(lr)) return LST_E_ARG;
+  if (noalloc_bytes(mm, d, K) > kScratchBytes) return LST_E_SHAPE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return LST_E_HIP;
+  if (dev < 0 || dev >= kScratchDevices) return LST_E_ARG;
+  if (s) {
+    int sdev = -1;
+    if (hipStreamGetDevice(s, &sdev) != hipSuccess) return LST_E_HIP;
+    if (sdev != dev) return LST_E_ARG;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  ScratchDev &sd = g_scratch[dev];
+  if (!sd.base) {
+    void *p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return LST_E_HIP;
+    sd.base = static_cast<char *>(p);
+  }
+  if (m == 0) {
+    hipLaunchKernelGGL(clear_words_kernel, dim3(1), dim3(64), 0, s, status_dev, 1, nullptr, 0);
+    if (hipGetLastError() != hipSuccess) return LST_E_HIP;
+    return launch_fill(s, loss_dev, 0.f) == hipSuccess ? LST_OK : LST_E_HIP;
+  }
+  StepBufs b{};
+  float *gradH = nullptr;
+  Carver cv{sd.base};
+  StepPlan *dev_plan = cv.take<StepPlan>(1);
+  carve_step(b, gradH, (size_t)m, (size_t)d, (size_t)K, cv);
+  b.D = D;
+  b.d = d;
+  b.ldd = ldd;
+  b.loss = loss;
+  b.eps = eps;
+  b.V = V;
+  b.ldv = ldv;
+  b.U = U;
+  b.UinvT = UinvT;
+  b.Q = Q;
+  b.flag = status_dev;
+  static StepPlan host;  // built under the lock; copied into the array by put_plan
+  build_step_plan(b, m, host);
+  if (put_plan(sd, host, s) != hipSuccess) return LST_E_HIP;
+  // the error word and the arrival counters of this layout start at zero
+  hipLaunchKernelGGL(clear_words_kernel, dim3(1), dim3(64), 0, s, status_dev, 1, b.qcnt,
+                     (m + 15) / 16);
+  if (hipGetLastError() != hipSuccess) return LST_E_HIP;
+  StepArgs a{H, m, idx, val, K, lr, loss_dev, grad_H ? grad_H : gradH};
+  for (int l = 0; l < 5; ++l) enqueue_step_launch(l, b, host, dev_plan, a, s);
+  return hipGetLastError() == hipSuccess ? LST_OK : LST_E_HIP;
 }
 
 }  // extern "C"

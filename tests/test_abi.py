@@ -113,6 +113,27 @@ def test_workspace_is_checked_on_the_host(L):
     assert st == lst.LST_E_SHAPE and ctx == 0
 
 
+def test_noalloc_step_checks_its_arguments_on_the_host(L):
+    # argument and size checks of the allocation-free step run before any device call
+    P = 0x1000
+    base = [200000, 500, 0, 1e-3, P, 500, P, P, P, 500, P, 128, P, P, 5, 0.1, P, P, P, 0]
+    def call(**kw):
+        a = list(base)
+        for k, v in kw.items():
+            a[int(k[1:])] = v
+        return lst.lst_step_noalloc(*a)
+    assert call(a4=0) == lst.LST_E_ARG         # V
+    assert call(a18=0) == lst.LST_E_ARG        # status
+    assert call(a16=0) == lst.LST_E_ARG        # loss_dev
+    assert call(a15=0.0) == lst.LST_E_ARG      # lr
+    assert call(a5=499) == lst.LST_E_SHAPE     # ldv < d
+    assert call(a11=-1) == lst.LST_E_SHAPE     # m < 0
+    assert call(a2=7) == lst.LST_E_ARG         # loss kind
+    # the 16 MiB array holds m = 128 (K = 5) up to d = 2863 and m = 512 up to d = 364
+    assert call(a1=2864, a5=2864, a9=2864) == lst.LST_E_SHAPE
+    assert call(a1=365, a5=365, a9=365, a11=512, a14=5) == lst.LST_E_SHAPE
+
+
 def test_product_path_does_not_import_the_oracle():
     pkg = os.path.join(ROOT, "paper_1606_08061_amd")
     for dirpath, _, files in os.walk(pkg):
