@@ -19,10 +19,12 @@ oracle shares no code, table or helper with that path.
 
 All inputs are float64 upcasts of the float32 arrays the GPU receives.
 """
-from .dense import dense_targets, dense_step, squared_error_step, spherical_softmax_step
+from .dense import (dense_targets, dense_step, spherical_softmax_step, squared_error_step,
+                    taylor_softmax_step)
 from .factored import FactoredState, factored_init, factored_step
 
 __all__ = [
     "dense_targets", "dense_step", "squared_error_step", "spherical_softmax_step",
+    "taylor_softmax_step",
     "FactoredState", "factored_init", "factored_step",
 ]

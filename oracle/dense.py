@@ -21,6 +21,14 @@ Sources in the paper:
                       (c_k, t_k), l_j = -sum_k t_k log((o_{c_k}^2 + eps) /
                       sum_i (o_i^2 + eps)); the denominator is q_j + D eps and
                       the loss does not depend on s.
+  Taylor softmax   -- also named in section 4 and never defined.  The reading:
+                      the softmax with exp replaced by its second-order Taylor
+                      polynomial f(x) = 1 + x + x^2/2 (positive everywhere, so
+                      every output is a probability),
+                      l_j = -sum_k t_k log(f(o_{c_k}) / sum_i f(o_i)); the
+                      denominator is sum_i f(o_i) = D + s_j + q_j / 2, so the
+                      loss depends on both q and s (dl/dq = T / (2 Z),
+                      dl/ds = T / Z with T = sum_k t_k, Z = D + s + q/2).
 Target representation: (index, value) pairs (section 2.1, section 4.1.4), with
 -1 marking an empty slot; an index repeated inside one example adds its values
 (y = sum_k t_k onehot(c_k)).
@@ -108,9 +116,48 @@ def spherical_softmax_step(W, H, idx, val, lr, eps) -> StepResult:
     return StepResult(float(per.sum()), grad_H, W_new, per)
 
 
+def taylor_softmax_step(W, H, idx, val, lr) -> StepResult:
+    """Taylor softmax through the naive steps of section 4, with dl/ds nonzero:
+    grad_O = 2 O diag(dl/dq) + 1_D (dl/ds)^T + Yring (eq. gen-grad-O)."""
+    W = np.asarray(W, dtype=F64)
+    H = np.asarray(H, dtype=F64)
+    idx = np.asarray(idx)
+    val = np.asarray(val, dtype=F64)
+    lr = F64(lr)
+    D = W.shape[0]
+    _check_idx(D, idx)
+    m, K = idx.shape
+    O = W @ H.T                       # D x m
+    q = np.sum(O * O, axis=0)         # q_j = ||o_j||^2
+    s = np.sum(O, axis=0)             # s_j = sum(o_j)
+    Z = D + s + 0.5 * q               # sum_i f(o_ij)
+    per = np.zeros(m, dtype=F64)
+    dl_dq = np.zeros(m, dtype=F64)
+    dl_ds = np.zeros(m, dtype=F64)
+    y_ring = np.zeros((D, m), dtype=F64)
+    for j in range(m):
+        for k in range(K):
+            c = int(idx[j, k])
+            if c < 0:
+                continue
+            t = val[j, k]
+            a = O[c, j]
+            fa = 1.0 + a + 0.5 * a * a
+            per[j] -= t * (np.log(fa) - np.log(Z[j]))
+            dl_dq[j] += t / (2.0 * Z[j])
+            dl_ds[j] += t / Z[j]
+            y_ring[c, j] -= t * (1.0 + a) / fa
+    grad_O = 2.0 * O * dl_dq[None, :] + dl_ds[None, :] + y_ring
+    grad_H = grad_O.T @ W
+    W_new = W - lr * (grad_O @ H)
+    return StepResult(float(per.sum()), grad_H, W_new, per)
+
+
 def dense_step(W, H, idx, val, lr, loss: str = "squared", eps: float = 1e-3) -> StepResult:
     if loss == "squared":
         return squared_error_step(W, H, idx, val, lr)
     if loss == "spherical_softmax":
         return spherical_softmax_step(W, H, idx, val, lr, eps)
+    if loss == "taylor_softmax":
+        return taylor_softmax_step(W, H, idx, val, lr)
     raise ValueError(loss)

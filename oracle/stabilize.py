@@ -35,12 +35,14 @@ F64 = np.float64
 def restore_pristine(st: FactoredState) -> FactoredState:
     """Section 5.1: move U into V; U and U^{-T} become the identity, Q is unchanged."""
     d = st.U.shape[0]
-    return FactoredState(st.V @ st.U, np.eye(d, dtype=F64), np.eye(d, dtype=F64), st.Q.copy())
+    return FactoredState(st.V @ st.U, np.eye(d, dtype=F64), np.eye(d, dtype=F64), st.Q.copy(),
+                         st.omega.copy(), st.wbar.copy())
 
 
 def reinvert(st: FactoredState) -> FactoredState:
     """Section 5.3: U^{-T} from U by Gaussian elimination (no use of the carried value)."""
-    return FactoredState(st.V.copy(), st.U.copy(), np.linalg.inv(st.U).T, st.Q.copy())
+    return FactoredState(st.V.copy(), st.U.copy(), np.linalg.inv(st.U).T, st.Q.copy(),
+                         st.omega.copy(), st.wbar.copy())
 
 
 def power_iteration(A, u0, iters: int):
@@ -78,7 +80,7 @@ def fix_singular_value(st: FactoredState, sigma: float, u, target: float = 1.0) 
     U = st.U + alpha * np.outer(u, st.U.T @ u)
     V = st.V + beta * np.outer(st.V @ u, u)
     UinvT = st.UinvT + beta * np.outer(u, st.UinvT.T @ u)
-    return FactoredState(V, U, UinvT, st.Q.copy())
+    return FactoredState(V, U, UinvT, st.Q.copy(), st.omega.copy(), st.wbar.copy())
 
 
 def singular_stabilize(st: FactoredState, u0, iters: int, lo: float, hi: float, max_fixes: int):

@@ -12,7 +12,8 @@ import pytest
 
 from oracle import dense_step, factored_init
 from oracle.factored import alg3_step, alg4_step
-from workloads import LOSS_SPHERICAL_SOFTMAX, LOSS_SQUARED, WORKLOADS, Stream, Workload
+from workloads import (LOSS_SPHERICAL_SOFTMAX, LOSS_SQUARED, LOSS_TAYLOR_SOFTMAX, WORKLOADS,
+                       Stream, Workload)
 
 
 def _rel(a, b):
@@ -59,7 +60,32 @@ def test_spherical_softmax_steps_match_dense():
     assert _rel(st.Q, W.T @ W) < 1e-10
 
 
-@pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX])
+@pytest.mark.parametrize("K,index_dist", [(1, "zipf"), (4, "uniform")])
+def test_taylor_softmax_steps_match_dense(K, index_dist):
+    # every row of Algorithm 4: s, h~, grad_s, y_bar, the omega and w_bar updates and the
+    # grad_s terms of Z^ and M; omega leaves 0 after the first step and w_bar tracks W^T 1
+    w = Workload("t", LOSS_TAYLOR_SOFTMAX, 300, 12, 8, K, index_dist=index_dist,
+                 value_dist="ones", lr=0.05, steps=30)
+    s = Stream(w)
+    st = factored_init(s.V0)
+    W = s.V0.astype(np.float64)
+    assert _rel(st.wbar, W.sum(axis=0)) < 1e-14 and not st.omega.any()
+    for _ in range(w.steps):
+        H, idx, val = s.batch()
+        ref = dense_step(W, H, idx, val, w.lr, LOSS_TAYLOR_SOFTMAX)
+        L, g, inter = alg4_step(st, H, idx, val, w.lr, LOSS_TAYLOR_SOFTMAX)
+        W = ref.W_new
+        assert L == pytest.approx(ref.loss, rel=1e-10)
+        assert _rel(g, ref.grad_H) < 1e-10
+        assert np.all(inter["ds"] > 0)
+    assert np.abs(st.omega).max() > 1e-3
+    assert _rel(st.W(), W) < 1e-10
+    assert _rel(st.Q, W.T @ W) < 1e-10
+    assert _rel(st.wbar, W.sum(axis=0)) < 1e-10
+    assert np.abs(st.U @ st.UinvT.T - np.eye(w.d)).max() < 1e-10
+
+
+@pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX, LOSS_TAYLOR_SOFTMAX])
 def test_duplicates_across_and_within_examples(loss):
     # Zipf over a tiny D makes many rows repeat across examples; one example repeats an index.
     w = Workload("t", loss, 7, 5, 6, 3, index_dist="zipf",

@@ -1,8 +1,10 @@
 """Pins of the dense fp64 oracle against things other than itself.
 
 * hand-worked examples (tests/golden/hand_examples.json), exact arithmetic;
-* closed forms: W = 0 for both losses; the spherical softmax normalisation
-  (sum over all D classes of exp(-loss) equals 1);
+* closed forms: W = 0 for every loss; the spherical and Taylor softmax
+  normalisation (sum over all D classes of exp(-loss) equals 1);
+* the Taylor softmax against the softmax cross-entropy of torch (a library
+  routine) for small outputs, where they agree to third order;
 * torch.autograd (fp64, CPU) differentiating the loss written from its
   definition: checks grad_H and the W update (dL/dW);
 * central finite differences of the oracle's own loss;
@@ -17,7 +19,8 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import dense_step, dense_targets, spherical_softmax_step, squared_error_step
+from oracle import (dense_step, dense_targets, spherical_softmax_step, squared_error_step,
+                    taylor_softmax_step)
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "hand_examples.json")
 
@@ -27,7 +30,7 @@ def _rand_case(seed, D=11, d=4, m=3, K=2, loss="squared"):
     W = rng.standard_normal((D, d))
     H = rng.standard_normal((m, d)) / np.sqrt(d)
     idx = np.stack([rng.choice(D, size=K, replace=False) for _ in range(m)]).astype(np.int32)
-    val = np.ones((m, K)) if loss == "spherical_softmax" else rng.standard_normal((m, K))
+    val = rng.standard_normal((m, K)) if loss == "squared" else np.ones((m, K))
     return W, H, idx, val
 
 
@@ -57,6 +60,15 @@ def test_hand_example_spherical_softmax():
     assert res.loss == pytest.approx(L, abs=1e-14)
     np.testing.assert_allclose(res.grad_H, [[grad_o @ W[:, 0]]], atol=1e-14)
     np.testing.assert_allclose(res.W_new, W - lr * grad_o[:, None] * 1.0, atol=1e-14)
+
+
+def test_hand_example_taylor_softmax():
+    case = _golden()["taylor_softmax"][0]
+    res = taylor_softmax_step(np.array(case["W"], float), np.array(case["H"], float),
+                              np.array(case["idx"]), np.array(case["val"], float), case["lr"])
+    assert res.loss == pytest.approx(np.log(7 / 5), abs=1e-15)
+    np.testing.assert_allclose(res.grad_H, [[-8 / 35]], atol=1e-15)
+    np.testing.assert_allclose(res.W_new, np.array(case["W_new"], float), atol=1e-15)
 
 
 def test_squared_zero_W_closed_form():
@@ -95,6 +107,41 @@ def test_spherical_softmax_normalises_over_all_classes():
             assert tot == pytest.approx(1.0, abs=1e-13)
 
 
+def test_taylor_softmax_zero_W_closed_form():
+    _, H, idx, val = _rand_case(4, D=13, K=2, loss="taylor_softmax")
+    W = np.zeros((13, 4))
+    res = taylor_softmax_step(W, H, idx, val, 0.1)
+    # o = 0, f(0) = 1: every class has probability 1/D; grad_O = (T/D) 1_D - Y (dl/da = -t
+    # since f'(0)/f(0) = 1), so grad_H = W^T grad_O = 0 and W_new = -eta grad_O H
+    np.testing.assert_allclose(res.per_example, val.sum(axis=1) * np.log(13.0), rtol=1e-14)
+    assert np.all(res.grad_H == 0)
+    gO = val.sum(axis=1)[None, :] / 13.0 - dense_targets(13, idx, val)
+    np.testing.assert_allclose(res.W_new, -0.1 * gO @ H, atol=1e-16)
+
+
+def test_taylor_softmax_normalises_over_all_classes():
+    W, H, _, _ = _rand_case(8, D=9, d=3, m=2, K=1, loss="taylor_softmax")
+    W *= 3.0  # large outputs, negative ones included: f stays positive
+    for j in range(2):
+        tot = sum(np.exp(-taylor_softmax_step(W, H[j:j + 1], np.array([[c]]), np.ones((1, 1)),
+                                               0.1).loss) for c in range(9))
+        assert tot == pytest.approx(1.0, abs=1e-13)
+
+
+@pytest.mark.parametrize("scale", [1e-2, 3e-2])
+def test_taylor_softmax_agrees_with_softmax_to_third_order(scale):
+    # log f(x) = x - x^3/6 + O(x^4) and log sum f = logsumexp + O(max |o|^3): the two losses
+    # differ by at most about max|o|^3 / 3 per unit of target weight
+    W, H, idx, val = _rand_case(9, D=40, d=6, m=3, K=2, loss="taylor_softmax")
+    W *= scale / np.abs(W @ H.T).max()
+    res = taylor_softmax_step(W, H, idx, val, 0.1)
+    logp = torch.log_softmax(torch.tensor(W @ H.T), dim=0).numpy()
+    for j in range(3):
+        ce = -sum(val[j, k] * logp[idx[j, k], j] for k in range(2))
+        assert abs(res.per_example[j] - ce) <= 2 * 0.5 * scale ** 3
+        assert abs(res.per_example[j] - ce) < 1e-2 * abs(ce)
+
+
 def _torch_loss(Wt, Ht, idx, val, loss, eps):
     D = Wt.shape[0]
     O = Wt @ Ht.T
@@ -102,6 +149,15 @@ def _torch_loss(Wt, Ht, idx, val, loss, eps):
         Y = torch.tensor(dense_targets(D, idx, val))
         return ((O - Y) ** 2).sum()
     tot = 0
+    if loss == "taylor_softmax":  # f over every output, the normaliser summed explicitly
+        F = 1 + O + O * O / 2
+        denom = F.sum(dim=0)
+        for j in range(idx.shape[0]):
+            for k in range(idx.shape[1]):
+                c = int(idx[j, k])
+                if c >= 0:
+                    tot = tot - val[j, k] * torch.log(F[c, j] / denom[j])
+        return tot
     denom = (O * O + eps).sum(dim=0)
     for j in range(idx.shape[0]):
         for k in range(idx.shape[1]):
@@ -111,7 +167,7 @@ def _torch_loss(Wt, Ht, idx, val, loss, eps):
     return tot
 
 
-@pytest.mark.parametrize("loss", ["squared", "spherical_softmax"])
+@pytest.mark.parametrize("loss", ["squared", "spherical_softmax", "taylor_softmax"])
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_autograd(loss, seed):
     W, H, idx, val = _rand_case(seed, D=17, d=5, m=4, K=3, loss=loss)
@@ -126,7 +182,7 @@ def test_autograd(loss, seed):
     np.testing.assert_allclose(res.W_new, W - lr * Wt.grad.numpy(), rtol=1e-11, atol=1e-12)
 
 
-@pytest.mark.parametrize("loss", ["squared", "spherical_softmax"])
+@pytest.mark.parametrize("loss", ["squared", "spherical_softmax", "taylor_softmax"])
 def test_finite_differences(loss):
     W, H, idx, val = _rand_case(7, D=8, d=3, m=2, K=2, loss=loss)
     lr, eps, h = 0.05, 1e-2, 1e-6
@@ -168,7 +224,7 @@ def test_brute_force_loops_squared():
     assert squared_error_step(W, H, idx, val, 0.1).loss == pytest.approx(L, rel=1e-13)
 
 
-@pytest.mark.parametrize("loss", ["squared", "spherical_softmax"])
+@pytest.mark.parametrize("loss", ["squared", "spherical_softmax", "taylor_softmax"])
 def test_minibatch_is_sum_of_examples(loss):
     W, H, idx, val = _rand_case(5, D=10, d=4, m=3, K=2, loss=loss)
     lr = 0.02
@@ -196,13 +252,15 @@ def test_example_and_slot_order_invariance():
     np.testing.assert_allclose(sp.W_new, base.W_new, rtol=1e-12, atol=1e-15)
 
 
-def test_repeated_index_adds_values_spherical():
-    # spherical softmax with two slots of the same class c and weights t1, t2 equals one slot
-    # with weight t1 + t2 (the per-slot sum reading)
-    W, H, _, _ = _rand_case(8, D=6, d=3, m=1, K=1, loss="spherical_softmax")
-    a = spherical_softmax_step(W, H, np.array([[4, 4]]), np.array([[0.25, 0.5]]), 0.1, 1e-3)
-    b = spherical_softmax_step(W, H, np.array([[4]]), np.array([[0.75]]), 0.1, 1e-3)
+@pytest.mark.parametrize("loss", ["spherical_softmax", "taylor_softmax"])
+def test_repeated_index_adds_values_spherical(loss):
+    # a spherical-family loss with two slots of the same class c and weights t1, t2 equals one
+    # slot with weight t1 + t2 (the per-slot sum reading); an empty slot adds nothing
+    W, H, _, _ = _rand_case(8, D=6, d=3, m=1, K=1, loss=loss)
+    a = dense_step(W, H, np.array([[4, 4, -1]]), np.array([[0.25, 0.5, 9.0]]), 0.1, loss, 1e-3)
+    b = dense_step(W, H, np.array([[4]]), np.array([[0.75]]), 0.1, loss, 1e-3)
     assert a.loss == pytest.approx(b.loss, rel=1e-14)
+    np.testing.assert_allclose(a.grad_H, b.grad_H, rtol=1e-13)
     np.testing.assert_allclose(a.W_new, b.W_new, rtol=1e-13)
 
 

@@ -29,6 +29,7 @@ import numpy as np
 
 LOSS_SQUARED = "squared"
 LOSS_SPHERICAL_SOFTMAX = "spherical_softmax"
+LOSS_TAYLOR_SOFTMAX = "taylor_softmax"
 
 
 @dataclasses.dataclass(frozen=True)
@@ -51,7 +52,8 @@ class Workload:
         return dataclasses.asdict(self)
 
 
-# The five workloads the measurements are quoted on.
+# The workloads the measurements are quoted on (with the sweep below), and the Taylor
+# softmax on the spherical softmax's shapes and target recipe.
 WORKLOADS = {
     "sq_D2k_d32_m16_K3": Workload("sq_D2k_d32_m16_K3", LOSS_SQUARED, 2000, 32, 16, 3,
                                   steps=100),
@@ -64,6 +66,10 @@ WORKLOADS = {
     "sq_D800k_d512_m256_K10_zipf": Workload("sq_D800k_d512_m256_K10_zipf", LOSS_SQUARED,
                                             800_000, 512, 256, 10, index_dist="zipf",
                                             steps=500),
+    "taylor_D200k_d500_m128_zipf": Workload("taylor_D200k_d500_m128_zipf",
+                                            LOSS_TAYLOR_SOFTMAX, 200_000, 500, 128, 1,
+                                            index_dist="zipf", value_dist="ones",
+                                            steps=1000),
 }
 
 
