@@ -3,9 +3,10 @@
  *
  * Method: Vincent, de Brebisson, Bouthillier, "Exact gradient updates in time
  * independent of output size for the spherical loss family" (arXiv 1606.08061).
- * The D x d output weights are kept factored as W = V U (section 3.2), with the
- * bookkeeping matrices Q = W^T W (section 3.4) and U^{-T} (eq. updateU-T,
- * Woodbury for minibatches, section 3.6 / 4.7).  One step (Algorithm 3 for
+ * The D x d output weights are kept factored as W = V U (section 3.2), or
+ * W = V U + 1_D omega^T for losses that use s = sum(o) (eq. gen-Wfact), with the
+ * bookkeeping matrices Q = W^T W (section 3.4), U^{-T} (eq. updateU-T, Woodbury
+ * for minibatches, section 3.6 / 4.7) and w_bar = W^T 1_D (section 4.1.2).  One step (Algorithm 3 for
  * squared error, Algorithm 4 for the spherical family) computes the exact
  * minibatch loss, its gradient with respect to the hidden layer H and the full
  * gradient update of the implicit W in O(m d^2 + m^2 d + m^3 + m K d), touching
@@ -23,7 +24,8 @@
  *   - Layout: row-major.  A minibatch H is m x d, one example per row (the same
  *     bytes as the paper's d x m H with one example per column).  V and W are
  *     D x d with row stride ldv / ldw >= d (floats); U, U^{-T} and Q are d x d
- *     with row stride ldd >= d.
+ *     with row stride ldd >= d; WO is 2 x d with row stride ldd, row 0 holding
+ *     w_bar and row 1 omega.
  *   - Targets: idx and val are m x K (row stride K).  idx holds 0-based row
  *     indices in [0, D); -1 marks an empty slot (the paper's "at most K"
  *     non-zeros).  An index repeated inside one example adds its values
@@ -38,8 +40,8 @@
  *     errors found on the device (an index outside [-1, D), a Woodbury matrix
  *     that is not positive definite, a non-finite loss) set a sticky device
  *     flag: all later state writes of that step and of every following step
- *     are skipped, so V, U, U^{-T} and Q keep the values they had before the
- *     failing step.  lst_sync_status reports and clears the flag.
+ *     are skipped, so V, U, U^{-T}, Q and WO keep the values they had before
+ *     the failing step.  lst_sync_status reports and clears the flag.
  */
 #ifndef LST_H
 #define LST_H
@@ -60,7 +62,15 @@ enum lst_loss {
   /* l = -sum_k t_k log((o_{c_k}^2 + eps) / sum_i (o_i^2 + eps)), the spherical
      softmax named in section 4 (no definition is printed there; this is the
      reading used by the library, independent of sum(o)). */
-  LST_LOSS_SPHERICAL_SOFTMAX = 1
+  LST_LOSS_SPHERICAL_SOFTMAX = 1,
+  /* l = -sum_k t_k log(f(o_{c_k}) / sum_i f(o_i)), f(x) = 1 + x + x^2/2: the
+     Taylor softmax, also named in section 4 without a definition; read as the
+     softmax with exp replaced by its second-order Taylor polynomial.  Since
+     sum_i f(o_i) = D + s + q/2 it depends on s = sum(o): the step keeps omega and
+     w_bar (eq. gen-Wfact, gen-update-omega, gen-update-wbar) and needs WO.  The
+     target weights of an example must not sum to a negative value (dl/dq >= 0,
+     which the Woodbury update needs). */
+  LST_LOSS_TAYLOR_SOFTMAX = 2
 };
 
 enum lst_status {
@@ -107,6 +117,9 @@ size_t lst_workspace_bytes(int64_t D, int32_t d, int32_t m_max, int32_t K_max, i
  *   eps          spherical softmax epsilon (> 0); ignored for squared error.
  *   V            D x ldv device buffer holding V (updated in place by lst_step).
  *   U, UinvT, Q  d x ldd device buffers (updated in place by lst_step).
+ *   WO           2 x ldd device buffer: w_bar (row 0) and omega (row 1), updated
+ *                in place by lst_step; needed by LST_LOSS_TAYLOR_SOFTMAX (else
+ *                LST_E_ARG), unused by the other losses (may be NULL).
  *   workspace    device buffer of ws_bytes >= lst_workspace_bytes(D, d, m_max,
  *                K_max, loss) bytes, 256-byte aligned (LST_E_ARG if NULL or
  *                misaligned, LST_E_SHAPE if too small); cleared on the stream here.
@@ -116,8 +129,8 @@ size_t lst_workspace_bytes(int64_t D, int32_t d, int32_t m_max, int32_t K_max, i
  * step.  On success *out receives the context.
  */
 int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss,
-               float eps, float *V, int64_t ldv, float *U, float *UinvT, float *Q, int32_t ldd,
-               void *workspace, size_t ws_bytes, void *stream);
+               float eps, float *V, int64_t ldv, float *U, float *UinvT, float *Q, float *WO,
+               int32_t ldd, void *workspace, size_t ws_bytes, void *stream);
 
 /* Options of a context (lst_set_option). */
 enum lst_option {
@@ -137,8 +150,10 @@ int lst_set_option(lst_ctx *c, int32_t option, int64_t value);
  * lst_init_factored -- Algorithm 1 (and the general initialisation of section 4.8).
  *   V0 (D x ldv0, device) is copied into V when not NULL; NULL keeps V as it is.
  *   U0 (d x ldu0, device) is copied into U when not NULL; NULL sets U = I.
- * Then U^{-T} = inv(U)^T and Q = (V U)^T (V U) are computed (Q = V^T V when
- * U = I), and the sticky error flag is cleared.  With U0 given, U is inverted
+ * Then U^{-T} = inv(U)^T and Q = W^T W are computed (Q = V^T V when U = I), and
+ * the sticky error flag is cleared.  For the Taylor softmax W = V U + 1_D omega^T
+ * with omega read from row 1 of WO as the caller left it (zero for a fresh start,
+ * as section 4.8 initialises it), and w_bar = W^T 1_D is written to row 0.  With U0 given, U is inverted
  * in fp64 on the host (LST_E_NOT_SPD if it is singular).  V^T V is split over D
  * into the workspace's partial sums.  Synchronises the stream.  Passing the current (V, U) re-derives the bookkeeping from scratch,
  * which is also how a run resumes from a (V, U) checkpoint.
@@ -191,13 +206,14 @@ int lst_use_graphs(lst_ctx *c, int32_t on);
  * stream capture, tight serving loops, hosts that forbid allocation): lst_step
  * without a context or workspace, on the same kernels.  The state (V, U, UinvT, Q,
  * as in lst_create) and the step's arguments (as in lst_step) are passed directly;
- * the step's descriptors and intermediates live in a device array of 16 MiB that
+ * WO is needed for the Taylor softmax as in lst_create.  The step's descriptors
+ * and intermediates live in a device array of 16 MiB that
  * the library holds on each GPU it runs on until the process ends.  The call
  * allocates and frees nothing.
  *   m, K         0 <= m <= LST_MAX_M, 0 <= K <= LST_MAX_K, m K <= 8192, and the
  *                step must fit the array: 4 (11 m d + 8 m^2) bytes plus about
- *                4 (m (d + m) / 16 + 4 m K + 7 m) + 16 KiB (m = 128 fits up to
- *                d = 2863, m = 256 up to d = 1290, m = 512 up to d = 364);
+ *                4 (m (d + m) / 16 + 4 m K + 13 m) + 16 KiB (m = 128 fits up to
+ *                d = 2863, m = 256 up to d = 1290, m = 512 up to d = 363);
  *                LST_E_SHAPE beyond it.
  *   status_dev   device int32, set to 0 by the call, then ORed by the kernels with
  *                1 (a target index outside [-1, D)), 2 (the Woodbury matrix is not
@@ -214,13 +230,14 @@ int lst_use_graphs(lst_ctx *c, int32_t on);
  * Results equal lst_step's on the same state (m = 1 takes the five-launch path).
  */
 int lst_step_noalloc(int64_t D, int32_t d, int32_t loss, float eps, float *V, int64_t ldv, float *U,
-                     float *UinvT, float *Q, int32_t ldd, const float *H, int32_t m,
+                     float *UinvT, float *Q, float *WO, int32_t ldd, const float *H, int32_t m,
                      const int32_t *idx, const float *val, int32_t K, float lr, float *loss_dev,
                      float *grad_H, int32_t *status_dev, void *stream);
 
 /*
- * lst_materialize_W -- W = V U into a D x ldw device buffer (section 5.1: the
- * explicit weights, an O(D d^2) product).  For a naive context, copies its W.
+ * lst_materialize_W -- W = V U (+ 1_D omega^T for the Taylor softmax) into a D x ldw
+ * device buffer (section 5.1: the explicit weights, an O(D d^2) product).  For a
+ * naive context, copies its W.
  */
 int lst_materialize_W(lst_ctx *c, float *W, int64_t ldw);
 
@@ -256,7 +273,7 @@ int lst_input_update(float *W1, int64_t ldw, int64_t D_in, int32_t d, const int3
  * beyond fp32 rounding.  Device-side errors surface at lst_sync_status.
  *
  * lst_restore_pristine -- section 5.1: V <- V U (in place, an O(D d^2) product on
- * the matrix cores), then U <- I and U^{-T} <- I.  Needs d <= 1024 (LST_E_SHAPE
+ * the matrix cores), then U <- I and U^{-T} <- I (omega and w_bar unchanged).  Needs d <= 1024 (LST_E_SHAPE
  * otherwise).
  */
 int lst_restore_pristine(lst_ctx *c);

@@ -7,7 +7,8 @@ this package is its ctypes binding.
 """
 from ._binding import (  # noqa: F401
     LIB_PATH, LOSSES, LST_E_ARG, LST_E_HIP, LST_E_INDEX, LST_E_NONFINITE, LST_E_NOT_SPD,
-    LST_E_SHAPE, LST_E_STATE, LST_E_SYNC, LST_LOSS_SPHERICAL_SOFTMAX, LST_LOSS_SQUARED, LST_OK, SIGNATURES,
+    LST_E_SHAPE, LST_E_STATE, LST_E_SYNC, LST_LOSS_SPHERICAL_SOFTMAX, LST_LOSS_SQUARED,
+    LST_LOSS_TAYLOR_SOFTMAX, LST_OK, SIGNATURES,
     Factored, LstError, Naive, lib, library_path, lst_create, lst_destroy, lst_init_factored,
     lst_materialize_W, lst_naive_create, lst_naive_step, lst_profile_enable, lst_profile_read,
     lst_use_graphs, lst_restore_pristine, lst_refresh_uinvt, lst_power_iteration,

@@ -18,7 +18,9 @@ LIB_PATH = os.path.join(_HERE, "liblst.so")
 
 LST_LOSS_SQUARED = 0
 LST_LOSS_SPHERICAL_SOFTMAX = 1
-LOSSES = {"squared": LST_LOSS_SQUARED, "spherical_softmax": LST_LOSS_SPHERICAL_SOFTMAX}
+LST_LOSS_TAYLOR_SOFTMAX = 2
+LOSSES = {"squared": LST_LOSS_SQUARED, "spherical_softmax": LST_LOSS_SPHERICAL_SOFTMAX,
+          "taylor_softmax": LST_LOSS_TAYLOR_SOFTMAX}
 
 LST_OK = 0
 LST_E_ARG = -1
@@ -39,7 +41,7 @@ SIGNATURES = {
     "lst_workspace_bytes": (ctypes.c_size_t, [_I64, _I32, _I32, _I32, _I32]),
     "lst_naive_workspace_bytes": (ctypes.c_size_t, [_I64, _I32, _I32, _I32, _I32]),
     "lst_create": (_I32, [ctypes.POINTER(_P), _I64, _I32, _I32, _I32, _I32, _F, _P, _I64, _P, _P,
-                          _P, _I32, _P, ctypes.c_size_t, _P]),
+                          _P, _P, _I32, _P, ctypes.c_size_t, _P]),
     "lst_set_option": (_I32, [_P, _I32, _I64]),
     "lst_init_factored": (_I32, [_P, _P, _I64, _P, _I32]),
     "lst_step": (_I32, [_P, _P, _I32, _P, _P, _I32, _F, _P, _P]),
@@ -55,8 +57,8 @@ SIGNATURES = {
     "lst_profile_read": (_I32, [_P, ctypes.POINTER(_I32), ctypes.POINTER(ctypes.c_double), _I32]),
     "lst_input_forward": (_I32, [_P, _I64, _I64, _I32, _P, _P, _I32, _I32, _P, _P, _P]),
     "lst_input_update": (_I32, [_P, _I64, _I64, _I32, _P, _P, _I32, _I32, _P, _F, _P, _P]),
-    "lst_step_noalloc": (_I32, [_I64, _I32, _I32, _F, _P, _I64, _P, _P, _P, _I32, _P, _I32, _P, _P,
-                                _I32, _F, _P, _P, _P, _P]),
+    "lst_step_noalloc": (_I32, [_I64, _I32, _I32, _F, _P, _I64, _P, _P, _P, _P, _I32, _P, _I32, _P,
+                                _P, _I32, _F, _P, _P, _P, _P]),
     "lst_restore_pristine": (_I32, [_P]),
     "lst_refresh_uinvt": (_I32, [_P, _I32, _I32, _P]),
     "lst_power_iteration": (_I32, [_P, _I32, _I32, _P, _P, _P]),
@@ -129,11 +131,11 @@ def lst_naive_workspace_bytes(D, d, m_max, K_max, loss) -> int:
     return int(lib().lst_naive_workspace_bytes(D, d, m_max, K_max, loss))
 
 
-def lst_create(D, d, m_max, K_max, loss, eps, V, ldv, U, UinvT, Q, ldd, ws, ws_bytes,
+def lst_create(D, d, m_max, K_max, loss, eps, V, ldv, U, UinvT, Q, WO, ldd, ws, ws_bytes,
                stream) -> tuple[int, int]:
     ctx = _P()
     st = lib().lst_create(ctypes.byref(ctx), D, d, m_max, K_max, loss, eps, V, ldv, U, UinvT, Q,
-                          ldd, ws, ws_bytes, stream)
+                          WO, ldd, ws, ws_bytes, stream)
     return st, (ctx.value or 0)
 
 
@@ -197,10 +199,10 @@ def lst_input_update(W1, ldw, D_in, d, idx, val, m, K, grad_A, lr, status, strea
     return lib().lst_input_update(W1, ldw, D_in, d, idx, val, m, K, grad_A, lr, status, stream)
 
 
-def lst_step_noalloc(D, d, loss, eps, V, ldv, U, UinvT, Q, ldd, H, m, idx, val, K, lr, loss_dev,
-                     grad_H, status, stream) -> int:
-    return lib().lst_step_noalloc(D, d, loss, eps, V, ldv, U, UinvT, Q, ldd, H, m, idx, val, K, lr,
-                                  loss_dev, grad_H, status, stream)
+def lst_step_noalloc(D, d, loss, eps, V, ldv, U, UinvT, Q, WO, ldd, H, m, idx, val, K, lr,
+                     loss_dev, grad_H, status, stream) -> int:
+    return lib().lst_step_noalloc(D, d, loss, eps, V, ldv, U, UinvT, Q, WO, ldd, H, m, idx, val, K,
+                                  lr, loss_dev, grad_H, status, stream)
 
 
 class SparseInput:
@@ -356,18 +358,30 @@ class Factored(_Ctx):
         self.U = torch.zeros((self.d, self.d), **kw)
         self.UinvT = torch.zeros((self.d, self.d), **kw)
         self.Q = torch.zeros((self.d, self.d), **kw)
+        # w_bar (row 0) and omega (row 1) of W = V U + 1_D omega^T; used by the Taylor softmax
+        self.WO = torch.zeros((2, self.d), **kw)
         nb = lst_workspace_bytes(self.D, self.d, self.m_max, self.K_max, self.loss)
         if nb == 0:
             raise LstError(LST_E_SHAPE, "lst_workspace_bytes")
         self.ws = _workspace(nb, self.device)
         st, self.ctx = lst_create(self.D, self.d, self.m_max, self.K_max, self.loss, self.eps,
                                   _ptr(self.V), self.d, _ptr(self.U), _ptr(self.UinvT),
-                                  _ptr(self.Q), self.d, _ptr(self.ws), nb,
+                                  _ptr(self.Q), _ptr(self.WO), self.d, _ptr(self.ws), nb,
                                   _stream_handle(self.stream))
         _check(st, "lst_create")
         self._step_fn = lib().lst_step
 
+    @property
+    def wbar(self):
+        return self.WO[0]
+
+    @property
+    def omega(self):
+        return self.WO[1]
+
     def init(self, V0=None, U0=None) -> None:
+        """Algorithm 1: V = V0, U = U0 (or I), then U^{-T}, Q and w_bar from them (omega as
+        it stands in WO[1]: zero unless the caller set it)."""
         if V0 is not None:
             _need(V0, torch.float32, (self.D, self.d), "V0")
         if U0 is not None:

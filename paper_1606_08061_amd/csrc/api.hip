@@ -23,6 +23,7 @@ enum : int { KIND_FACTORED = 1, KIND_NAIVE = 2 };
 constexpr int kTargetWGs = 1024;  // workgroups a split-k GEMM aims for
 constexpr int kColnormBlocks = 1024;
 constexpr size_t kInitPartialCap = size_t(8) << 20;  // floats of split-k partials for Q = V^T V
+constexpr int kWbarBlocks = 256;                    // row blocks of the column sums V^T 1_D
 constexpr int kDefaultSpin = 1 << 20;               // polls of the online step's barrier
 constexpr size_t kWsAlign = 256;
 
@@ -71,6 +72,7 @@ struct lst_ctx {
   float *V;
   int64_t ldv;
   float *U, *UinvT, *Q;
+  float *WO;  // w_bar, omega (Taylor softmax)
   int ldd;
   // naive state (borrowed)
   float *W;
@@ -86,9 +88,10 @@ struct lst_ctx {
   float *Sd0, *Sd1, *svec, *spart, *sscal;
   float *initpart;  // split-k partial sums of Q = V^T V (lst_init_factored)
   size_t initpart_floats;
+  float *wpart;     // row-block column sums of V for w_bar (Taylor softmax)
   int *flag;
   int *cnt;  // [0] the online step's grid-barrier counter, [1] its decision word
-  float *O, *colpart, *splitpart;
+  float *O, *colpart, *colsum, *splitpart;
   hipError_t last_err;
   hipStream_t cap;  // stream a step is captured on when it is recorded as a HIP graph
   bool have_cap;
@@ -157,6 +160,10 @@ void carve_step(StepBufs &b, float *&gradH, size_t m, size_t d, size_t K, Carver
   b.scnt = cv.take<int>(m);
   b.coef = cv.take<float>(8);
   b.cert = cv.take<int>(1);
+  b.SW = cv.take<float>(2 * m);
+  b.ds = cv.take<float>(m);
+  b.yb = cv.take<float>(m);
+  b.cwo = cv.take<float>(2 * m);
 }
 
 void carve_factored(lst_ctx *c, Carver &cv) {
@@ -169,6 +176,7 @@ void carve_factored(lst_ctx *c, Carver &cv) {
   c->sscal = cv.take<float>(8);
   c->initpart_floats = init_partial_floats(c->D, c->d);
   c->initpart = cv.take<float>(c->initpart_floats);
+  c->wpart = c->loss == LST_LOSS_TAYLOR_SOFTMAX ? cv.take<float>((size_t)kWbarBlocks * d) : nullptr;
   c->flag = cv.take<int>(1);
   c->cnt = cv.take<int>(4);
   c->plan_pool = cv.take<StepPlan>(kPlanCap);
@@ -211,11 +219,17 @@ void carve_naive(lst_ctx *c, Carver &cv) {
   c->sb.dq = cv.take<float>(c->m_max);
   c->sb.lvec = cv.take<float>(c->m_max);
   c->sb.dA = cv.take<float>(mk);
+  if (c->loss == LST_LOSS_TAYLOR_SOFTMAX) {  // column sums of O for s_j, and dl/ds
+    c->colsum = cv.take<float>((size_t)kColnormBlocks * c->m_max);
+    c->sb.ds = cv.take<float>(c->m_max);
+  }
   c->flag = cv.take<int>(1);
 }
 
 int common_args(int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss, float eps) {
-  if (loss != LST_LOSS_SQUARED && loss != LST_LOSS_SPHERICAL_SOFTMAX) return LST_E_ARG;
+  if (loss != LST_LOSS_SQUARED && loss != LST_LOSS_SPHERICAL_SOFTMAX &&
+      loss != LST_LOSS_TAYLOR_SOFTMAX)
+    return LST_E_ARG;
   if (loss == LST_LOSS_SPHERICAL_SOFTMAX && !finite_pos(eps)) return LST_E_ARG;
   if (D < 1 || D > LST_MAX_D || d < 1 || d > LST_MAX_d) return LST_E_SHAPE;
   if (m_max < 1 || m_max > LST_MAX_M || K_max < 0 || K_max > LST_MAX_K) return LST_E_SHAPE;
@@ -401,13 +415,14 @@ size_t lst_naive_workspace_bytes(int64_t D, int32_t d, int32_t m_max, int32_t K_
 }
 
 int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max, int32_t loss,
-               float eps, float *V, int64_t ldv, float *U, float *UinvT, float *Q, int32_t ldd,
-               void *workspace, size_t ws_bytes, void *stream) {
+               float eps, float *V, int64_t ldv, float *U, float *UinvT, float *Q, float *WO,
+               int32_t ldd, void *workspace, size_t ws_bytes, void *stream) {
   if (!out) return LST_E_ARG;
   *out = nullptr;
   int st = common_args(D, d, m_max, K_max, loss, eps);
   if (st != LST_OK) return st;
   if (!V || !U || !UinvT || !Q) return LST_E_ARG;
+  if (loss == LST_LOSS_TAYLOR_SOFTMAX && !WO) return LST_E_ARG;
   if (ldv < d || ldd < d) return LST_E_SHAPE;
   lst_ctx *c = new_ctx(KIND_FACTORED, D, d, m_max, K_max, loss, eps, stream);
   if (!c) return LST_E_ARG;
@@ -416,6 +431,7 @@ int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max
   c->U = U;
   c->UinvT = UinvT;
   c->Q = Q;
+  c->WO = loss == LST_LOSS_TAYLOR_SOFTMAX ? WO : nullptr;
   c->ldd = ldd;
   st = take_ws(c, workspace, ws_bytes, carve_factored);
   if (st == LST_OK) {
@@ -430,6 +446,7 @@ int lst_create(lst_ctx **out, int64_t D, int32_t d, int32_t m_max, int32_t K_max
     b.U = U;
     b.UinvT = UinvT;
     b.Q = Q;
+    b.WO = c->WO;
     c->plans.reserve(kPlanCap);
     if (hipStreamCreateWithFlags(&c->cap, hipStreamNonBlocking) != hipSuccess) st = LST_E_HIP;
     else c->have_cap = true;
@@ -617,6 +634,15 @@ int lst_init_factored(lst_ctx *c, const float *V0, int64_t ldv0, const float *U0
     b3.n = 1;
     if (st == LST_OK && record(c, gemm_launch(b3, nullptr, s))) st = LST_E_HIP;
   }
+  if (st == LST_OK && c->WO) {
+    // W = V U + 1_D omega^T with the caller's omega: w_bar = U^T (V^T 1_D) + D omega,
+    // and Q gains the omega part of W^T W
+    const float *omega = c->WO + c->ldd;
+    if (record(c, launch_wbar(s, c->V, c->ldv, c->D, d, U0 ? c->U : nullptr, c->ldd, omega,
+                              c->wpart, kWbarBlocks, c->WO)) ||
+        record(c, launch_q_omega(s, c->Q, c->ldd, d, c->D, c->WO, omega)))
+      st = LST_E_HIP;
+  }
   const int zero = 0;
   if (record(c, hipStreamSynchronize(s))) st = LST_E_HIP;
   if (record(c, hipMemcpy(c->flag, &zero, sizeof(int), hipMemcpyHostToDevice))) st = LST_E_HIP;
@@ -775,6 +801,11 @@ int lst_materialize_W(lst_ctx *c, float *W, int64_t ldw) {
   }
   GemmBatch b{};
   b.d[0] = gemm_desc((int)c->D, c->d, c->d, c->V, c->ldv, 0, c->U, c->ldd, 1, W, ldw);
+  if (c->WO) {  // + 1_D omega^T: omega as a C input of row stride 0
+    b.d[0].Cin = c->WO + c->ldd;
+    b.d[0].ldcin = 0;
+    b.d[0].beta = 1.f;
+  }
   b.n = 1;
   return record(c, gemm_launch(b, nullptr, c->stream));
 }
@@ -795,24 +826,28 @@ int lst_naive_step(lst_ctx *c, const float *H, int32_t m, const int32_t *idx, co
   prof(c, LST_PHASE_NAIVE_FWD, true);
   GemmDesc fwd = gemm_desc((int)D, m, d, c->W, c->ldw, 0, H, d, 0, c->O, m);
   int nparts = kColnormBlocks;
-  if (gemm_big_ok(fwd)) {
+  const bool tay = c->loss == LST_LOSS_TAYLOR_SOFTMAX;
+  if (gemm_big_ok(fwd) && !tay) {
     fwd.colsq = c->colpart;
     gemm_big_plan(fwd, kTargetWGs, 0, nullptr);
     nparts = kBigColsqRows * fwd.tiles_m;
     if (record(c, gemm_big_launch(fwd, nullptr, s, GEMM_NAIVE_FWD))) return LST_E_HIP;
   } else {
     if (record(c, naive_gemm(c, fwd, false, nullptr, s, GEMM_NAIVE_FWD)) ||
-        record(c, launch_colnorm(s, c->O, D, m, c->colpart, kColnormBlocks)))
+        record(c, launch_colnorm(s, c->O, D, m, c->colpart, tay ? c->colsum : nullptr,
+                                 kColnormBlocks)))
       return LST_E_HIP;
   }
   prof(c, LST_PHASE_NAIVE_FWD, false);
   // The loss and dl/dq, dl/da from the explicit O.
   prof(c, LST_PHASE_NAIVE_LOSS, true);
-  if (record(c, launch_naive_epilogue(s, m, K, D, nparts, c->colpart, c->O, idx, val, c->loss,
-                                      c->eps, c->sb.dq, c->sb.dA, c->sb.lvec, c->flag)))
+  if (record(c, launch_naive_epilogue(s, m, K, D, nparts, c->colpart, tay ? c->colsum : nullptr,
+                                      c->O, idx, val, c->loss, c->eps, c->sb.dq,
+                                      tay ? c->sb.ds : nullptr, c->sb.dA, c->sb.lvec, c->flag)))
     return LST_E_HIP;
-  // grad_O = 2 O diag(dl/dq) + Yring, in place over O.
-  if (record(c, launch_grad_o(s, c->O, D, m, K, c->sb.dq, idx, c->sb.dA, c->sb.lvec, loss_dev, c->flag)))
+  // grad_O = 2 O diag(dl/dq) + 1_D (dl/ds)^T + Yring, in place over O.
+  if (record(c, launch_grad_o(s, c->O, D, m, K, c->sb.dq, tay ? c->sb.ds : nullptr, idx,
+                              c->sb.dA, c->sb.lvec, loss_dev, c->flag)))
     return LST_E_HIP;
   prof(c, LST_PHASE_NAIVE_LOSS, false);
   // grad_H = grad_O^T W (split over D), then W <- W - eta grad_O H.
@@ -1134,13 +1169,14 @@ hipError_t put_plan(ScratchDev &sd, const StepPlan &pl, hipStream_t s) {
 extern "C" {
 
 int lst_step_noalloc(int64_t D, int32_t d, int32_t loss, float eps, float *V, int64_t ldv, float *U,
-                     float *UinvT, float *Q, int32_t ldd, const float *H, int32_t m,
+                     float *UinvT, float *Q, float *WO, int32_t ldd, const float *H, int32_t m,
                      const int32_t *idx, const float *val, int32_t K, float lr, float *loss_dev,
                      float *grad_H, int32_t *status_dev, void *stream) {
   const int mm = m < 1 ? 1 : m;
   int st = common_args(D, d, mm, K, loss, eps);
   if (st != LST_OK) return st;
   if (!V || !U || !UinvT || !Q || !loss_dev || !status_dev) return LST_E_ARG;
+  if (loss == LST_LOSS_TAYLOR_SOFTMAX && !WO) return LST_E_ARG;
   if (ldv < d || ldd < d) return LST_E_SHAPE;
   if (m < 0) return LST_E_SHAPE;
   if (m > 0 && !H) return LST_E_ARG;
@@ -1183,6 +1219,7 @@ int lst_step_noalloc(int64_t D, int32_t d, int32_t loss, float eps, float *V, in
   b.U = U;
   b.UinvT = UinvT;
   b.Q = Q;
+  b.WO = loss == LST_LOSS_TAYLOR_SOFTMAX ? WO : nullptr;
   b.flag = status_dev;
   static StepPlan host;  // built under the lock; copied into the array by put_plan
   build_step_plan(b, m, host);

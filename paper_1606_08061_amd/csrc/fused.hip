@@ -1,5 +1,6 @@
-// The factored minibatch step (Algorithm 3 for squared error, Algorithm 4 with
-// dl/ds = 0 for the spherical softmax) as five launches on one stream.
+// The factored minibatch step (Algorithm 3 for squared error, Algorithm 4 for the
+// spherical family: dl/ds = 0 for the spherical softmax, every row for the Taylor
+// softmax) as five launches on one stream.
 //
 // Notation (rows are examples: H is m x d, the paper's d x m H transposed):
 //   H^ = H Q, H~ = H U^T, X = H U^{-T T}      (Alg. 3 steps 1, 5, 6; Alg. 4 rows 1, 5)
@@ -8,6 +9,11 @@
 //   Z^ = G U, grad_H = 2 diag(dl/dq) H^ + Z^ (eq. gen-grad-H-fact)
 //   M = 4 D M^ D + Yring^T Yring + 2 D HZ + 2 HZ^T D (eq. gen-M; M^ = H H^^T,
 //       HZ = H~ G^T, D = diag(dl/dq))
+// With dl/ds (the Taylor softmax; W = V U + 1 omega^T, eq. gen-Wfact): s_j = h_j . w_bar
+// and h~_j = h_j . omega (eq. svec, gen-htilde; launch 1), a_kj gains h~_j, Z^ gains
+// w_bar ds_j + omega y_bar_j (eq. gen-Zhat-fact; y_bar_j = sum_k dl/dA_kj), HZ gains
+// s ds^T + h~ y_bar^T (HZ = H^T Z^), M gains D ds ds^T + ds y_bar^T + y_bar ds^T, and
+// launch 5 updates omega and w_bar (eq. gen-update-omega, gen-update-wbar).
 //   U <- U - 2 eta H~^T D H (eq. updateU / gen-updateU)
 //   Q <- Q + H^T Zq + Zq^T H, Zq = (eta^2/2) M H - eta grad_H (eq. updateQ / gen-Qnew)
 //   U^{-T} <- U^{-T} + (R X)^T H, R = 2 eta S C^{-1} S, C = I - 2 eta S N S,
@@ -37,9 +43,9 @@
 //   3  Z^ with grad_H; HZ; P2 = E^2 Xs; P3 = E^2 W1; E^4; Yring^T Yring; L = sum l_j;
 //      the certificate, the coefficients c_k, and (uncertified) the exact R
 //   4  Zq; R X; the U update                                 [writes U]
-//   5  the Q and U^{-T} updates; the V scatter                [writes Q, U^{-T}, V]
-// Q, U, U^{-T} and V are read (launches 1-3) before any of them is written
-// (launches 4-5), and every error is raised by launch 3 at the latest; launches 4
+//   5  the Q, U^{-T} (and omega, w_bar) updates; the V scatter [writes Q, U^{-T}, V]
+// Q, U, U^{-T}, V, omega and w_bar are read (launches 1-3) before any of them is
+// written (launches 4-5), and every error is raised by launch 3 at the latest; launches 4
 // and 5 read the error flag first and write nothing if it is set, so a failed step
 // changes no state.
 #include <cmath>
@@ -64,10 +70,14 @@ __device__ __forceinline__ const float *rsv(const float *p, const float *H, floa
   return v == 16 ? H : (v == 32 ? gH : p);
 }
 
-// dl/dq_j: 1 for squared error; for the spherical softmax (sum of the example's
-// target weights over its valid slots, in slot order) / (q_j + D eps).
-__device__ __forceinline__ float dq_of(int loss, float q, float tsum, float Deps) {
-  return loss == LST_LOSS_SQUARED ? 1.f : tsum / (q + Deps);
+// dl/dq_j with T = the sum of the example's target weights over its valid slots (in
+// slot order): 1 for squared error, T / (q_j + D eps) for the spherical softmax,
+// T / (2 D + 2 s_j + q_j) for the Taylor softmax.
+__device__ __forceinline__ float dq_of(int loss, float q, float s, float tsum, float Dn,
+                                       float eps) {
+  if (loss == LST_LOSS_SQUARED) return 1.f;
+  if (loss == LST_LOSS_TAYLOR_SOFTMAX) return tsum / (2.f * Dn + 2.f * s + q);
+  return tsum / (q + Dn * eps);
 }
 
 __device__ __forceinline__ float scale_of(int mode, const float *dq, int i) {
@@ -144,10 +154,11 @@ __device__ __forceinline__ void ld4m(const float *__restrict__ p, int64_t ld, in
 // combined, column jb) at k = k0 .. k0 + 3; MASKED: the block may pass the end of k.
 template <int AMODE, int NB, bool SC, int AMD, int BMD, bool MASKED>
 __device__ __forceinline__ void op16_block(const Op16 &g, const float *A, const float *const *Bp,
-                                           const float *bco, float dqi, int ia, int jb, int k0,
-                                           const TileCtx &x, float (&a)[4], float (&b)[4]) {
+                                           const float *bco, float dqi, float dsi, float ybi,
+                                           int ia, int jb, int k0, const TileCtx &x,
+                                           float (&a)[4], float (&b)[4]) {
   const int K = g.K;
-  if constexpr (AMODE == AM_MASM) {
+  if constexpr (AMODE != AM_PLAIN) {
     // M_ik = 4 dq_i M^_ik dq_k + YY_ik + 2 dq_i HZ_ik + 2 dq_k HZ_ki
     float mh[4], yy[4], hz[4], hzt[4], dk[4];
     ld4m<LS>(g.Mh, g.ldm, ia, k0, K, mh);
@@ -162,6 +173,14 @@ __device__ __forceinline__ void op16_block(const Op16 &g, const float *A, const 
 #pragma unroll
     for (int s = 0; s < 4; ++s)
       a[s] = 4.f * dqi * mh[s] * dk[s] + yy[s] + 2.f * dqi * hz[s] + 2.f * dk[s] * hzt[s];
+    if constexpr (AMODE == AM_MASM_S) {
+      // + D ds_i ds_k + ds_i yb_k + yb_i ds_k
+      float sk[4], yk[4];
+      ld4m<LS>(g.ds, 0, 0, k0, K, sk);
+      ld4m<LS>(g.yb, 0, 0, k0, K, yk);
+#pragma unroll
+      for (int s = 0; s < 4; ++s) a[s] += dsi * fmaf(g.Dn, sk[s], yk[s]) + ybi * sk[s];
+    }
   } else if constexpr (MASKED) {
     ld4m<AMD>(A, g.lda, ia, k0, K, a);
   } else {
@@ -259,7 +278,9 @@ __device__ __forceinline__ floatx4 op16_kloop(const Op16 &g, int ia, int jb, con
     Bp[t] = rsv(g.b[t].p, x.H, x.gH);
     bco[t] = NB > 1 ? coef_of(x, g.b[t].coef) : 1.f;
   }
-  const float dqi = (AMODE == AM_MASM && x.dq) ? x.dq[ia] : 1.f;
+  const float dqi = (AMODE != AM_PLAIN && x.dq) ? x.dq[ia] : 1.f;
+  const float dsi = AMODE == AM_MASM_S ? g.ds[ia] : 0.f;
+  const float ybi = AMODE == AM_MASM_S ? g.yb[ia] : 0.f;
   floatx4 acc = {0.f, 0.f, 0.f, 0.f};
   const int nfull = K >> 4;
   const int nw = nfull > wave ? (nfull - wave + 3) / 4 : 0;
@@ -268,7 +289,8 @@ __device__ __forceinline__ floatx4 op16_kloop(const Op16 &g, int ia, int jb, con
 #pragma unroll
     for (int u = 0; u < G; ++u) {
       const int k0 = 16 * (wave + 4 * min(u0 + u, nw - 1)) + 4 * lg;
-      op16_block<AMODE, NB, SC, AMD, BMD, false>(g, A, Bp, bco, dqi, ia, jb, k0, x, a[u], b[u]);
+      op16_block<AMODE, NB, SC, AMD, BMD, false>(g, A, Bp, bco, dqi, dsi, ybi, ia, jb, k0, x,
+                                                 a[u], b[u]);
     }
 #pragma unroll
     for (int u = 0; u < G; ++u)
@@ -280,8 +302,8 @@ __device__ __forceinline__ floatx4 op16_kloop(const Op16 &g, int ia, int jb, con
   }
   if ((K & 15) && wave == 3) {
     float a[4], b[4];
-    op16_block<AMODE, NB, SC, AMD, BMD, true>(g, A, Bp, bco, dqi, ia, jb, 16 * nfull + 4 * lg,
-                                               x, a, b);
+    op16_block<AMODE, NB, SC, AMD, BMD, true>(g, A, Bp, bco, dqi, dsi, ybi, ia, jb,
+                                               16 * nfull + 4 * lg, x, a, b);
 #pragma unroll
     for (int s = 0; s < 4; ++s) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[s], b[s], acc, 0, 0, 0);
   }
@@ -291,7 +313,7 @@ __device__ __forceinline__ floatx4 op16_kloop(const Op16 &g, int ia, int jb, con
 template <int AMODE, int NB, bool SC, int G>
 __device__ __forceinline__ floatx4 op16_dispatch(const Op16 &g, int ia, int jb, const TileCtx &x,
                                                  int wave, int lg) {
-  if constexpr (AMODE == AM_MASM || NB > 1) {
+  if constexpr (AMODE != AM_PLAIN || NB > 1) {
     // assembled M or several B terms: every B term k-major (the plan builder's layout)
     return op16_kloop<AMODE, NB, SC, G, LS, LT>(g, ia, jb, x, wave, lg);
   } else {
@@ -332,6 +354,8 @@ __device__ __forceinline__ void op16_tile(const Op16 &g, int local, const TileCt
   floatx4 acc;
   if (g.amode == AM_MASM)
     acc = op16_dispatch<AM_MASM, 1, false, 2>(g, ia, jb, x, wave, lg);
+  else if (g.amode == AM_MASM_S)
+    acc = op16_dispatch<AM_MASM_S, 1, false, 1>(g, ia, jb, x, wave, lg);
   else if (g.nb > 1)
     acc = op16_dispatch<AM_PLAIN, kMaxTerms, true, 2>(g, ia, jb, x, wave, lg);
   else if (g.b[0].sc != SC_NONE)
@@ -350,6 +374,10 @@ __device__ __forceinline__ void op16_tile(const Op16 &g, int local, const TileCt
     if (t >= g.nadd) break;
     v = fmaf(coef_of(x, g.add[t].coef) * scale_of(g.add[t].sc, x.dq, ci), addv[t], v);
   }
+  // the rank-nuv addend (only the dl/ds products have one: loaded here, not before the
+  // k loop, to keep the other products' registers)
+  for (int r = 0; r < g.nuv; ++r)
+    v = fmaf(g.ux[r][(int64_t)ci * g.uxi[r]], g.uy[r][(int64_t)cj * g.uyi[r]], v);
   float al = g.alpha;
   for (int e = 0; e < g.alpha_lr; ++e) al *= x.lr;
   v *= al * scale_of(g.rs, x.dq, ci) * scale_of(g.cs, x.dq, cj);
@@ -454,15 +482,32 @@ struct GatherArgs {
   int *srow;
   float *sval;
   int *scnt;
+  const float *SW;         // Taylor softmax: s_j, h~_j (launch 1)
+  float *ds, *yb, *cwo;    // Taylor softmax: dl/ds, y_bar, the omega / w_bar coefficients
   int *flag;
 };
 
-// Loss epilogue of one example (section 4, dl/ds = 0); r[k] < 0 marks an empty slot.
-// l = q - 2 a.t + ||y||^2 (squared error, ||y||^2 by index equality) or
-// l = sum_k t_k [log(q + D eps) - log(a_k^2 + eps)] (spherical softmax).
-__device__ __forceinline__ void epilogue(int loss, float q, float gq, int K, const int *r,
-                                         const float *t, const float *a, float Deps, float eps,
-                                         float &l, float *g) {
+// The Taylor softmax's per-example outputs besides dl/dq and dl/dA: dl/ds_j = 2 dl/dq_j
+// (= T / Z), y_bar_j = sum_k dl/dA_kj, and the coefficients of the launch-5 products
+// w_bar -= H^T c_w, omega -= H^T c_o: c_w = eta (2 dq s + D ds + y_bar) (eq.
+// gen-update-wbar), c_o = eta (2 dq h~ + ds) (eq. gen-update-omega).
+__device__ __forceinline__ void taylor_outputs(const GatherArgs &ga, int j, float gq, float sj,
+                                               float hw, float ybar) {
+  const float gs = 2.f * gq;
+  ga.ds[j] = gs;
+  ga.yb[j] = ybar;
+  ga.cwo[j] = ga.lr * (2.f * gq * sj + (float)ga.D * gs + ybar);
+  ga.cwo[ga.m + j] = ga.lr * (2.f * gq * hw + gs);
+}
+
+// Loss epilogue of one example (section 4); r[k] < 0 marks an empty slot; a holds
+// h~_j . V_r, to which the Taylor softmax adds h~_j = h_j . omega (eq. gen-A-fact).
+// l = q - 2 a.t + ||y||^2 (squared error, ||y||^2 by index equality),
+// l = sum_k t_k [log(q + D eps) - log(a_k^2 + eps)] (spherical softmax) or
+// l = sum_k t_k [log(D + s + q/2) - log(1 + a_k + a_k^2/2)] (Taylor softmax).
+__device__ __forceinline__ void epilogue(int loss, float q, float sj, float hw, int K,
+                                         const int *r, const float *t, const float *a, float Dn,
+                                         float eps, float &l, float *g) {
   l = 0.f;
   if (loss == LST_LOSS_SQUARED) {
     float at = 0.f, yy = 0.f;
@@ -475,8 +520,18 @@ __device__ __forceinline__ void epilogue(int loss, float q, float gq, int K, con
       g[k] = -2.f * t[k];
     }
     l = q - 2.f * at + yy;
+  } else if (loss == LST_LOSS_TAYLOR_SOFTMAX) {
+    const float lz = logf(Dn + sj + 0.5f * q);
+    for (int k = 0; k < K; ++k) {
+      g[k] = 0.f;
+      if (r[k] < 0) continue;
+      const float ak = a[k] + hw;
+      const float f = 1.f + ak + 0.5f * ak * ak;
+      l += t[k] * (lz - logf(f));
+      g[k] = -t[k] * (1.f + ak) / f;
+    }
   } else {
-    const float lz = logf(q + Deps);
+    const float lz = logf(q + Dn * eps);
     for (int k = 0; k < K; ++k) {
       g[k] = 0.f;
       if (r[k] < 0) continue;
@@ -485,7 +540,6 @@ __device__ __forceinline__ void epilogue(int loss, float q, float gq, int K, con
       g[k] = -2.f * t[k] * a[k] / den;
     }
   }
-  (void)gq;
 }
 
 // The sorted list of the example's target rows with their summed dl/dA (rows
@@ -523,9 +577,10 @@ __device__ __forceinline__ void sorted_slots(int j, int K, const int *sr, const 
 // The loss epilogue on register arrays (KM slots, fully unrolled): the serial part of
 // a gather workgroup then makes no dependent LDS reads.
 template <int KM>
-__device__ __forceinline__ void epilogue_reg(int loss, float q, int K, const int (&r)[KM],
-                                             const float (&t)[KM], const float (&a)[KM],
-                                             float Deps, float eps, float &l, float (&g)[KM]) {
+__device__ __forceinline__ void epilogue_reg(int loss, float q, float sj, float hw, int K,
+                                             const int (&r)[KM], const float (&t)[KM],
+                                             const float (&a)[KM], float Dn, float eps, float &l,
+                                             float (&g)[KM]) {
   l = 0.f;
   if (loss == LST_LOSS_SQUARED) {
     float at = 0.f, yy = 0.f;
@@ -540,8 +595,19 @@ __device__ __forceinline__ void epilogue_reg(int loss, float q, int K, const int
         if (kk < K && r[kk] == r[k]) yy += t[k] * t[kk];
     }
     l = q - 2.f * at + yy;
+  } else if (loss == LST_LOSS_TAYLOR_SOFTMAX) {
+    const float lz = logf(Dn + sj + 0.5f * q);
+#pragma unroll
+    for (int k = 0; k < KM; ++k) {
+      g[k] = 0.f;
+      if (k >= K || r[k] < 0) continue;
+      const float ak = a[k] + hw;
+      const float f = 1.f + ak + 0.5f * ak * ak;
+      l += t[k] * (lz - logf(f));
+      g[k] = -t[k] * (1.f + ak) / f;
+    }
   } else {
-    const float lz = logf(q + Deps);
+    const float lz = logf(q + Dn * eps);
 #pragma unroll
     for (int k = 0; k < KM; ++k) {
       g[k] = 0.f;
@@ -700,8 +766,9 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
   if (t == 0) {
     if (s_bad) atomicOr(ga.flag, FLAG_INDEX);
     const float q = ga.loss == LST_LOSS_SQUARED ? (sred[0] + sred[1]) + (sred[2] + sred[3]) : qv;
-    const float Deps = (float)ga.D * ga.eps;
-    const float gq = dq_of(ga.loss, q, tsv, Deps);
+    const bool tay = ga.loss == LST_LOSS_TAYLOR_SOFTMAX;
+    const float sj = tay ? ga.SW[2 * j] : 0.f, hw = tay ? ga.SW[2 * j + 1] : 0.f;
+    const float gq = dq_of(ga.loss, q, sj, tsv, (float)ga.D, ga.eps);
     constexpr int KM = W * KPW;
     int rr[KM];
     float tt[KM], aa[KM], gg[KM];
@@ -712,10 +779,15 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
       aa[k] = k < K ? sa[k] : 0.f;
     }
     float l;
-    epilogue_reg<KM>(ga.loss, q, K, rr, tt, aa, Deps, ga.eps, l, gg);
+    epilogue_reg<KM>(ga.loss, q, sj, hw, K, rr, tt, aa, (float)ga.D, ga.eps, l, gg);
+    float ybar = 0.f;
 #pragma unroll
     for (int k = 0; k < KM; ++k)
-      if (k < K) sg[k] = gg[k];
+      if (k < K) {
+        sg[k] = gg[k];
+        ybar += gg[k];
+      }
+    if (tay) taylor_outputs(ga, j, gq, sj, hw, ybar);
     ga.dq[j] = gq;
     ga.lvec[j] = l;
     s_dq = gq;
@@ -767,6 +839,7 @@ __device__ __forceinline__ void gather_gen(const GatherArgs &ga, int j) {
     qv = ga.q[j];
     tsv = ga.tsum[j];
   }
+  const bool tay = ga.loss == LST_LOSS_TAYLOR_SOFTMAX;
   __syncthreads();
   for (int k = t; k < K; k += 256) {
     int r = ga.idx[(int64_t)j * K + k];
@@ -793,10 +866,15 @@ __device__ __forceinline__ void gather_gen(const GatherArgs &ga, int j) {
   if (t == 0) {
     if (s_bad) atomicOr(ga.flag, FLAG_INDEX);
     const float q = ga.loss == LST_LOSS_SQUARED ? (sred[0] + sred[1]) + (sred[2] + sred[3]) : qv;
-    const float Deps = (float)ga.D * ga.eps;
-    const float gq = dq_of(ga.loss, q, tsv, Deps);
+    const float sj = tay ? ga.SW[2 * j] : 0.f, hw = tay ? ga.SW[2 * j + 1] : 0.f;
+    const float gq = dq_of(ga.loss, q, sj, tsv, (float)ga.D, ga.eps);
     float l;
-    epilogue(ga.loss, q, gq, K, sr, st, sa, Deps, ga.eps, l, sg);
+    epilogue(ga.loss, q, sj, hw, K, sr, st, sa, (float)ga.D, ga.eps, l, sg);
+    if (tay) {
+      float ybar = 0.f;
+      for (int k = 0; k < K; ++k) ybar += sg[k];
+      taylor_outputs(ga, j, gq, sj, hw, ybar);
+    }
     ga.dq[j] = gq;
     ga.lvec[j] = l;
     s_dq = gq;
@@ -823,8 +901,9 @@ __device__ __forceinline__ void gather_gen(const GatherArgs &ga, int j) {
 // dl/dq of every example into LDS (the spherical softmax's E products need all of
 // them before the gather workgroups have written theirs; the same arithmetic).
 __device__ __forceinline__ void dq_all(const GatherArgs &ga, float *sdq) {
+  const bool tay = ga.loss == LST_LOSS_TAYLOR_SOFTMAX;
   for (int i = threadIdx.x; i < ga.m; i += 256)
-    sdq[i] = dq_of(ga.loss, ga.q[i], ga.tsum[i], (float)ga.D * ga.eps);
+    sdq[i] = dq_of(ga.loss, ga.q[i], tay ? ga.SW[2 * i] : 0.f, ga.tsum[i], (float)ga.D, ga.eps);
   __syncthreads();
 }
 
@@ -1204,6 +1283,7 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
   pl = StepPlan{};
   const int d = sb.d, ldd = sb.ldd;
   const bool sq = sb.loss == LST_LOSS_SQUARED;
+  const bool tay = sb.loss == LST_LOSS_TAYLOR_SOFTMAX;
   const float *H = sym_H();
   float *gH = sym_gradH();
   // Launch 1: H^ = H Q (row partials h . h^ -> qpart), H~ = H U^T, X = H U^{-T T}, N = H H^T
@@ -1222,7 +1302,9 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
     ob.op[2] = op(m, d, d, H, d, 0, sb.UinvT, ldd, 0, sb.X, d);
     ob.op[3] = op(m, m, d, H, d, 0, H, d, 0, sb.N, m);
     ob.n = 4;
-    finalize(ob, 4);
+    if (tay)  // [s h~] = H [w_bar omega] (eq. svec, gen-htilde)
+      ob.op[ob.n++] = op(m, 2, d, H, d, 0, sb.WO, ldd, 0, sb.SW, 2);
+    finalize(ob, ob.n);
   }
   // Launch 2: M^ = H H^^T; E^2 = 4 eta^2 S N D N S (|row| partials -> bpart);
   // W1 = E Xs = 2 eta S N D X
@@ -1256,8 +1338,30 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
     z.E = sb.Hhat;
     z.lde = d;
     z.rs2 = sq ? SC_NONE : SC_DQ;
+    Op16 hz = op(m, m, d, sb.Htil, d, 0, sb.G, d, 0, sb.HZ, m);
+    if (tay) {
+      // Z^ += ds w_bar^T + y_bar omega^T; HZ += s ds^T + h~ y_bar^T
+      z.nuv = 2;
+      z.ux[0] = sb.ds;
+      z.uxi[0] = 1;
+      z.uy[0] = sb.WO;
+      z.uyi[0] = 1;
+      z.ux[1] = sb.yb;
+      z.uxi[1] = 1;
+      z.uy[1] = sb.WO + ldd;
+      z.uyi[1] = 1;
+      hz.nuv = 2;
+      hz.ux[0] = sb.SW;
+      hz.uxi[0] = 2;
+      hz.uy[0] = sb.ds;
+      hz.uyi[0] = 1;
+      hz.ux[1] = sb.SW + 1;
+      hz.uxi[1] = 2;
+      hz.uy[1] = sb.yb;
+      hz.uyi[1] = 1;
+    }
     ob.op[0] = z;
-    ob.op[1] = op(m, m, d, sb.Htil, d, 0, sb.G, d, 0, sb.HZ, m);
+    ob.op[1] = hz;
     ob.op[2] = op(m, m, m, sb.E2, m, 0, sb.E2, m, 1, sb.E4, m);
     ob.op[3] = op(m, d, m, sb.E2, m, 0, sb.X, d, 1, sb.P2, d);
     if (!sq) ob.op[3].b[0].sc = SC_SQRT;
@@ -1272,6 +1376,12 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
     OpBatch &ob = pl.ob[3];
     Op16 zq = op(m, d, m, nullptr, 0, 0, H, d, 1, sb.Zq, d);
     zq.amode = AM_MASM;
+    if (tay) {
+      zq.amode = AM_MASM_S;
+      zq.ds = sb.ds;
+      zq.yb = sb.yb;
+      zq.Dn = (float)sb.D;
+    }
     zq.Mh = sb.Mhat;
     zq.HZ = sb.HZ;
     zq.YY = sb.YY;
@@ -1309,7 +1419,7 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
     gb.n = 1;
     gemm_prepare(gb);
   }
-  // Launch 5: Q <- Q + H^T Zq + Zq^T H; U^{-T} <- U^{-T} + (R X)^T H
+  // Launch 5: Q <- Q + H^T Zq + Zq^T H; U^{-T} <- U^{-T} + (R X)^T H; omega, w_bar
   {
     GemmBatch &gb = pl.gb_update;
     GemmDesc qd = gemm_desc(d, d, m, H, d, 1, sb.Zq, d, 1, sb.Q, ldd, 1.f, sb.Q, ldd, 1.f);
@@ -1321,6 +1431,8 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
     gb.d[0] = gemm_desc(d, d, m, sb.RX, d, 1, H, d, 1, sb.UinvT, ldd, 1.f, sb.UinvT, ldd, 1.f);
     gb.d[1] = qd;
     gb.n = 2;
+    if (tay)  // [w_bar; omega] -= [c_w; c_o] H (eta folded into the coefficients)
+      gb.d[gb.n++] = gemm_desc(2, d, m, sb.cwo, m, 0, H, d, 1, sb.WO, ldd, -1.f, sb.WO, ldd, 1.f);
     gemm_prepare(gb);
   }
 }
@@ -1373,6 +1485,10 @@ void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, co
       ga.srow = sb.srow;
       ga.sval = sb.sval;
       ga.scnt = sb.scnt;
+      ga.SW = sb.SW;
+      ga.ds = sb.ds;
+      ga.yb = sb.yb;
+      ga.cwo = sb.cwo;
       ga.flag = sb.flag;
       const int kpw = (a.K + 3) / 4;
       const int d = sb.d;

@@ -129,10 +129,11 @@ size_t gemm_plan_split(GemmDesc &g, int target_wgs, float *partial);
 // Op16: one product C = post(A opB) on 16 x 16 output tiles, k = K.  A is a plain
 // operand (A(i,k) = A[i lda + k], or A[k lda + i] with tA) or, for the Q update's
 // M, assembled as it is loaded (AM_MASM: 4 dq_i M^_ik dq_k + YY_ik + 2 dq_i HZ_ik +
-// 2 dq_k HZ_ki).  opB(k,j) = sum_t coef_t scale_t(k) B_t(k,j) over up to four terms
+// 2 dq_k HZ_ki; AM_MASM_S adds the dl/ds terms D ds_i ds_k + ds_i yb_k + yb_i ds_k).
+// opB(k,j) = sum_t coef_t scale_t(k) B_t(k,j) over up to four terms
 // (tr = 0: B_t[j ld + k]; tr = 1: B_t[k ld + j]).  Epilogue:
-//   v = alpha lr^alpha_lr rs(i) cs(j) (acc + sum_t coef_t scale_t(i) Add_t[i ld + j])
-//       + beta lr^beta_lr Cin_ij,
+//   v = alpha lr^alpha_lr rs(i) cs(j) (acc + sum_t coef_t scale_t(i) Add_t[i ld + j]
+//       + sum_r ux_r[i uxi_r] uy_r[j uyi_r]) + beta lr^beta_lr Cin_ij,
 // stored to C (if any), C2 = 2 rs2(i) E_ij + v (if any), and the row partial sums
 // (v Rr_ij, or |v|) of the tile's 16 columns to rowout[tile column][i].  The scale
 // modes take dl/dq (SC_DQ) or its square root (SC_SQRT) of the index; coefficient
@@ -140,9 +141,10 @@ size_t gemm_plan_split(GemmDesc &g, int target_wgs, float *partial);
 // ---------------------------------------------------------------------------
 enum : int { SC_NONE = 0, SC_DQ = 1, SC_SQRT = 2 };
 enum : int { RR_NONE = 0, RR_DOT = 1, RR_ABS = 2 };
-enum : int { AM_PLAIN = 0, AM_MASM = 1 };
+enum : int { AM_PLAIN = 0, AM_MASM = 1, AM_MASM_S = 2 };
 constexpr int kMaxTerms = 4;
 constexpr int kMaxOps = 6;
+constexpr int kMaxRank = 2;
 
 struct OpTerm {
   const float *p;
@@ -165,6 +167,13 @@ struct Op16 {
   OpTerm b[kMaxTerms];
   int nadd;
   OpTerm add[kMaxTerms];
+  // rank-nuv addend sum_r ux_r[i uxi_r] uy_r[j uyi_r] (the dl/ds terms of Z^ and HZ)
+  int nuv;
+  const float *ux[kMaxRank], *uy[kMaxRank];
+  int uxi[kMaxRank], uyi[kMaxRank];
+  // AM_MASM_S: dl/ds (ds), y_bar (yb) and D of M's dl/ds terms
+  const float *ds, *yb;
+  float Dn;
   float alpha;
   int alpha_lr;
   int rs, cs;
@@ -213,6 +222,7 @@ struct StepBufs {
   float *V;
   int64_t ldv;
   float *U, *UinvT, *Q;
+  float *WO;             // 2 x ldd: w_bar, omega (Taylor softmax; else null)
   float *Hhat, *Htil, *X, *G, *Atil, *W1, *P2, *P3, *RX, *Zq;  // m x d
   float *N, *Mhat, *HZ, *YY, *E2, *E4, *R, *Cwork;             // m x m
   float *qpart, *bpart;  // row partials: [ceil(d/16)][m], [ceil(m/16)][m]
@@ -223,6 +233,9 @@ struct StepBufs {
   int *srow, *scnt;      // m x K, m
   float *coef;           // 8
   int *cert;
+  float *SW;             // m x 2: s_j = h_j . w_bar, h~_j = h_j . omega
+  float *ds, *yb;        // m: dl/ds_j, y_bar_j = sum_k dl/dA_kj
+  float *cwo;            // 2 x m: eta (2 dq s + D ds + y_bar), eta (2 dq h~ + ds)
   int *flag;
 };
 
@@ -249,18 +262,30 @@ hipError_t launch_identity(hipStream_t s, float *A, int d, int64_t ld);
 hipError_t launch_fill(hipStream_t s, float *p, float v);
 
 // Naive-path kernels.  Column norms come as nparts partial sums partial[p][j]
-// (from the forward product's epilogue, or from launch_colnorm).
+// (from the forward product's epilogue, or from launch_colnorm, which also writes the
+// partial column sums to psum when it is not null).
 hipError_t launch_colnorm(hipStream_t s, const float *O, int64_t D, int m, float *partial,
-                          int nblk);
+                          float *psum, int nblk);
+// w_bar = U^T (V^T 1_D) + D omega: nblk row blocks of V summed into part (nblk x d),
+// then reduced and multiplied by U^T (U null: identity).  out must not alias part.
+hipError_t launch_wbar(hipStream_t s, const float *V, int64_t ldv, int64_t D, int d,
+                       const float *U, int ldd, const float *omega, float *part, int nblk,
+                       float *out);
+// Q += u omega^T + omega u^T + D omega omega^T with u = w_bar - D omega (the omega part
+// of W^T W for W = V U + 1_D omega^T, given Q = (V U)^T (V U)).
+hipError_t launch_q_omega(hipStream_t s, float *Q, int ldd, int d, int64_t D, const float *wbar,
+                          const float *omega);
+// psum (Taylor softmax): partial column sums of O (nparts x m, from launch_colnorm),
+// giving s_j; dl/ds_j goes to ds.  Both null for the other losses.
 hipError_t launch_naive_epilogue(hipStream_t s, int m, int K, int64_t D, int nparts,
-                                 const float *partial, const float *O, const int *idx,
-                                 const float *val, int loss, float eps, float *dq, float *dA,
-                                 float *lvec, int *flag);
-// grad_O = 2 O diag(dq) + sum of dA at the targets, in place over O; also
-// loss_out = sum_j lvec[j].
+                                 const float *partial, const float *psum, const float *O,
+                                 const int *idx, const float *val, int loss, float eps, float *dq,
+                                 float *ds, float *dA, float *lvec, int *flag);
+// grad_O = 2 O diag(dq) + 1_D ds^T (ds may be null) + sum of dA at the targets, in place
+// over O; also loss_out = sum_j lvec[j].
 hipError_t launch_grad_o(hipStream_t s, float *O, int64_t D, int m, int K, const float *dq,
-                         const int *idx, const float *dA, const float *lvec, float *loss_out,
-                         int *flag);
+                         const float *ds, const int *idx, const float *dA, const float *lvec,
+                         float *loss_out, int *flag);
 
 // ---------------------------------------------------------------------------
 // The sparse input layer of section 2.2 (input_layer.hip): A = X W1 and

@@ -56,20 +56,26 @@ def test_host_argument_errors(L):
     P = 0x1000  # a non-null placeholder; never dereferenced on these paths
     WS = 0x100000  # a 256-byte aligned placeholder workspace
     nb = lst.lst_workspace_bytes(10, 8, 4, 2, 0)
-    st, ctx = lst.lst_create(0, 8, 4, 2, 0, 1e-3, P, 8, P, P, P, 8, WS, nb, 0)
+    st, ctx = lst.lst_create(0, 8, 4, 2, 0, 1e-3, P, 8, P, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_SHAPE and ctx == 0
-    st, _ = lst.lst_create(10, 8, 4, 2, 5, 1e-3, P, 8, P, P, P, 8, WS, nb, 0)
+    st, _ = lst.lst_create(10, 8, 4, 2, 5, 1e-3, P, 8, P, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_ARG
-    st, _ = lst.lst_create(10, 8, 4, 2, 1, 0.0, P, 8, P, P, P, 8, WS, nb, 0)
+    st, _ = lst.lst_create(10, 8, 4, 2, 1, 0.0, P, 8, P, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_ARG
-    st, _ = lst.lst_create(10, 8, 4, 2, 0, 1e-3, 0, 8, P, P, P, 8, WS, nb, 0)
+    st, _ = lst.lst_create(10, 8, 4, 2, 0, 1e-3, 0, 8, P, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_ARG
-    st, _ = lst.lst_create(10, 8, 4, 2, 0, 1e-3, P, 7, P, P, P, 8, WS, nb, 0)
+    st, _ = lst.lst_create(10, 8, 4, 2, 0, 1e-3, P, 7, P, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_SHAPE
-    st, _ = lst.lst_create(10, 8, 2048, 2, 0, 1e-3, P, 8, P, P, P, 8, WS, nb, 0)
+    st, _ = lst.lst_create(10, 8, 2048, 2, 0, 1e-3, P, 8, P, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_SHAPE
-    st, _ = lst.lst_create(10, 8, 512, 64, 0, 1e-3, P, 8, P, P, P, 8, WS, nb, 0)
+    st, _ = lst.lst_create(10, 8, 512, 64, 0, 1e-3, P, 8, P, P, P, P, 8, WS, nb, 0)
     assert st == lst.LST_E_SHAPE
+    # the Taylor softmax keeps w_bar and omega: WO is required
+    nt = lst.lst_workspace_bytes(10, 8, 4, 2, lst.LST_LOSS_TAYLOR_SOFTMAX)
+    st, _ = lst.lst_create(10, 8, 4, 2, 2, 1e-3, P, 8, P, P, P, 0, 8, WS, nt, 0)
+    assert st == lst.LST_E_ARG
+    st, _ = lst.lst_create(10, 8, 4, 2, 3, 1e-3, P, 8, P, P, P, P, 8, WS, nt, 0)
+    assert st == lst.LST_E_ARG
     st, _ = lst.lst_naive_create(10, 0, 4, 2, 0, 1e-3, P, 8, WS, nb, 0)
     assert st == lst.LST_E_SHAPE
     assert lst.lst_set_option(0, lst.LST_OPT_SPIN_LIMIT, 1) == lst.LST_E_ARG
@@ -105,7 +111,7 @@ def test_workspace_is_checked_on_the_host(L):
     ws = 0x100000
     for args, want in [((0, nb), lst.LST_E_ARG), ((ws + 4, nb), lst.LST_E_ARG),
                        ((ws, nb - 256), lst.LST_E_SHAPE)]:
-        st, ctx = lst.lst_create(1000, 32, 16, 3, 0, 1e-3, P, 32, P, P, P, 32, *args, 0)
+        st, ctx = lst.lst_create(1000, 32, 16, 3, 0, 1e-3, P, 32, P, P, P, P, 32, *args, 0)
         assert st == want and ctx == 0
     nn = lst.lst_naive_workspace_bytes(1000, 32, 16, 3, 0)
     assert nn >= 1000 * 16 * 4  # holds the D x m output
@@ -116,22 +122,23 @@ def test_workspace_is_checked_on_the_host(L):
 def test_noalloc_step_checks_its_arguments_on_the_host(L):
     # argument and size checks of the allocation-free step run before any device call
     P = 0x1000
-    base = [200000, 500, 0, 1e-3, P, 500, P, P, P, 500, P, 128, P, P, 5, 0.1, P, P, P, 0]
+    base = [200000, 500, 0, 1e-3, P, 500, P, P, P, 0, 500, P, 128, P, P, 5, 0.1, P, P, P, 0]
     def call(**kw):
         a = list(base)
         for k, v in kw.items():
             a[int(k[1:])] = v
         return lst.lst_step_noalloc(*a)
     assert call(a4=0) == lst.LST_E_ARG         # V
-    assert call(a18=0) == lst.LST_E_ARG        # status
-    assert call(a16=0) == lst.LST_E_ARG        # loss_dev
-    assert call(a15=0.0) == lst.LST_E_ARG      # lr
+    assert call(a19=0) == lst.LST_E_ARG        # status
+    assert call(a17=0) == lst.LST_E_ARG        # loss_dev
+    assert call(a16=0.0) == lst.LST_E_ARG      # lr
     assert call(a5=499) == lst.LST_E_SHAPE     # ldv < d
-    assert call(a11=-1) == lst.LST_E_SHAPE     # m < 0
+    assert call(a12=-1) == lst.LST_E_SHAPE     # m < 0
     assert call(a2=7) == lst.LST_E_ARG         # loss kind
-    # the 16 MiB array holds m = 128 (K = 5) up to d = 2863 and m = 512 up to d = 364
-    assert call(a1=2864, a5=2864, a9=2864) == lst.LST_E_SHAPE
-    assert call(a1=365, a5=365, a9=365, a11=512, a14=5) == lst.LST_E_SHAPE
+    assert call(a2=2) == lst.LST_E_ARG         # the Taylor softmax without WO
+    # the 16 MiB array holds m = 128 (K = 5) up to d = 2863 and m = 512 up to d = 363
+    assert call(a1=2864, a5=2864, a10=2864) == lst.LST_E_SHAPE
+    assert call(a1=364, a5=364, a10=364, a12=512, a15=5) == lst.LST_E_SHAPE
 
 
 def test_product_path_does_not_import_the_oracle():

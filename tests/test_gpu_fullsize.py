@@ -1,7 +1,8 @@
 """Parity at the full workload sizes (D = 200k / 800k), in the launch configuration the
 benchmark times: one step of the factored and of the naive path against the fp64 oracle
 (loss, grad_H and the whole updated W), rows of V outside the targets bit-identical, and
-100 steps of the D = 200k squared-error workload with the drift of Q and U^{-T} watched."""
+100 steps of the D = 200k squared-error workload with the drift of Q and U^{-T} watched,
+and ten steps of the Taylor softmax at D = 200k (omega and w_bar included)."""
 import numpy as np
 import pytest
 import torch
@@ -11,7 +12,8 @@ from workloads import WORKLOADS, Stream
 
 pytestmark = pytest.mark.gpu
 
-FULL = ["sq_D200k_d500_m128_K5", "sphsm_D200k_d500_m128_zipf", "sq_D800k_d512_m256_K10_zipf"]
+FULL = ["sq_D200k_d500_m128_K5", "sphsm_D200k_d500_m128_zipf", "sq_D800k_d512_m256_K10_zipf",
+        "taylor_D200k_d500_m128_zipf"]
 
 
 @pytest.mark.parametrize("name", FULL)
@@ -154,4 +156,23 @@ def test_full_size_fix_singular_value_sampled_rows():
     assert rel(f.V[rt].cpu().numpy(), want) <= 1e-4
     W_after = (f.V[rt] @ f.U).cpu().numpy().astype(np.float64)
     assert rel(W_after, W_before) <= 1e-4
+    f.close()
+
+
+def test_full_size_taylor_ten_steps():
+    w = WORKLOADS["taylor_D200k_d500_m128_zipf"]
+    s = Stream(w)
+    W = s.V0.astype(np.float64)
+    f = make_factored(w, s.V0)
+    for t in range(10):
+        H, idx, val = s.batch()
+        ref = oracle_step(W, H, idx, val, w)
+        loss, grad = f.step(*to_dev(H, idx, val), w.lr)
+        assert f.sync_status() == 0
+        tol = 1e-4 if t == 0 else 1e-3
+        assert abs(loss.item() - ref.loss) <= tol * abs(ref.loss), t
+        assert rel(grad.cpu().numpy(), ref.grad_H) <= tol, t
+        W = ref.W_new
+    assert rel(f.materialize_W().cpu().numpy(), W) <= 1e-3
+    assert rel(f.wbar.cpu().numpy(), W.sum(axis=0)) <= 1e-3
     f.close()

@@ -10,7 +10,8 @@ import torch
 
 from gpu_common import DEV, Compare, make_factored, oracle_step, rel, to_dev
 from oracle import dense_step
-from workloads import LOSS_SPHERICAL_SOFTMAX, LOSS_SQUARED, WORKLOADS, Stream, Workload
+from workloads import (LOSS_SPHERICAL_SOFTMAX, LOSS_SQUARED, LOSS_TAYLOR_SOFTMAX, WORKLOADS,
+                       Stream, Workload)
 
 pytestmark = pytest.mark.gpu
 
@@ -50,12 +51,11 @@ def test_small_config_100_steps():
     c.close()
 
 
-@pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX])
+@pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX, LOSS_TAYLOR_SOFTMAX])
 @pytest.mark.parametrize("D,d,m,K", [
     (50, 1, 1, 1), (300, 31, 2, 3), (1000, 33, 17, 2), (777, 65, 33, 1), (2000, 40, 70, 3),
     (1500, 47, 130, 2), (3000, 24, 300, 1), (2500, 20, 520, 1), (400, 64, 5, 0),
-    # m > 128 with d >= m: the m x m blocked inverse (the cases above with d < m take the d x d
-    # push-through form); d = 200 < m = 260: the push-through form with a blocked d x d inverse
+    # m above 128, with d above and below m (E = 2 eta S H H^T S of rank min(m, d))
     (2000, 160, 150, 2), (1200, 300, 260, 1), (1800, 200, 260, 2),
 ])
 def test_awkward_shapes(loss, D, d, m, K):
@@ -91,7 +91,7 @@ def _dup_batch(c, t):
 
 @pytest.mark.parametrize("loss,D,K", [
     (LOSS_SQUARED, 9, 3), (LOSS_SPHERICAL_SOFTMAX, 9, 3), (LOSS_SQUARED, 40, 16),
-    (LOSS_SQUARED, 60, 20),
+    (LOSS_SQUARED, 60, 20), (LOSS_TAYLOR_SOFTMAX, 9, 3), (LOSS_TAYLOR_SOFTMAX, 40, 16),
 ])
 def test_duplicates_and_empty_slots(loss, D, K):
     # small D under Zipf: rows repeat across examples; some examples repeat an index or have
@@ -134,7 +134,8 @@ def test_duplicates_spherical_softmax_most_classes_targeted():
 
 
 @pytest.mark.parametrize("loss,d", [(LOSS_SQUARED, 512), (LOSS_SQUARED, 1024),
-                                    (LOSS_SQUARED, 700), (LOSS_SPHERICAL_SOFTMAX, 700)])
+                                    (LOSS_SQUARED, 700), (LOSS_SPHERICAL_SOFTMAX, 700),
+                                    (LOSS_TAYLOR_SOFTMAX, 700)])
 def test_sweep_minibatch_m512(loss, d):
     # the sweep's m = 512 (32 tile rows of every m x m product of the Woodbury polynomial;
     # 512 < d <= 1024 takes the gather with 16 columns per lane; d = 700 is no multiple of
@@ -277,7 +278,7 @@ def test_untouched_rows_bit_identical_and_deterministic():
         assert torch.equal(a, b)
 
 
-@pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX])
+@pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX, LOSS_TAYLOR_SOFTMAX])
 def test_graph_replay_matches_eager(loss):
     # Each step's arguments recur every third step, so the cached graphs are replayed several
     # times, with eager torch work and host synchronisations between the replays; every replay

@@ -8,21 +8,21 @@ import torch
 
 import paper_1606_08061_amd as lst
 from gpu_common import DEV, make_factored, rel, to_dev
-from workloads import LOSS_SPHERICAL_SOFTMAX, LOSS_SQUARED, Stream, Workload
+from workloads import LOSS_SPHERICAL_SOFTMAX, LOSS_SQUARED, LOSS_TAYLOR_SOFTMAX, Stream, Workload
 
 pytestmark = pytest.mark.gpu
 
 TOL = 1e-4
 
 
-@pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX])
+@pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX, LOSS_TAYLOR_SOFTMAX])
 def test_noalloc_step_matches_lst_step(loss):
     sq = loss == LOSS_SQUARED
     w = Workload("t", loss, 20000, 256, 128, 5 if sq else 3,
                  index_dist="uniform" if sq else "zipf", value_dist="normal" if sq else "ones")
     s = Stream(w)
     f = make_factored(w, s.V0)
-    V, U, UinvT, Q = (t.clone() for t in (f.V, f.U, f.UinvT, f.Q))
+    V, U, UinvT, Q, WO = (t.clone() for t in (f.V, f.U, f.UinvT, f.Q, f.WO))
     loss_dev = torch.zeros(1, dtype=torch.float32, device=DEV)
     status = torch.full((1,), 99, dtype=torch.int32, device=DEV)
     stream = torch.cuda.current_stream(DEV).cuda_stream
@@ -36,7 +36,8 @@ def test_noalloc_step_matches_lst_step(loss):
         grad = torch.empty((m, w.d), dtype=torch.float32, device=DEV)
         st = lst.lst_step_noalloc(w.D, w.d, lst.LOSSES[loss], float(np.float32(w.eps)),
                                   V.data_ptr(), w.d, U.data_ptr(), UinvT.data_ptr(),
-                                  Q.data_ptr(), w.d, Hd.data_ptr(), m, idxd.data_ptr(),
+                                  Q.data_ptr(), WO.data_ptr(), w.d, Hd.data_ptr(), m,
+                                  idxd.data_ptr(),
                                   vald.data_ptr(), K, w.lr, loss_dev.data_ptr(),
                                   grad.data_ptr(), status.data_ptr(), stream)
         assert st == lst.LST_OK
@@ -44,6 +45,6 @@ def test_noalloc_step_matches_lst_step(loss):
         assert int(status.item()) == 0
         assert abs(loss_dev.item() - l_ref.item()) <= TOL * abs(l_ref.item())
         assert rel(grad.cpu().numpy(), g_ref.cpu().numpy()) <= TOL
-        for mine, theirs in ((V, f.V), (U, f.U), (UinvT, f.UinvT), (Q, f.Q)):
+        for mine, theirs in ((V, f.V), (U, f.U), (UinvT, f.UinvT), (Q, f.Q), (WO, f.WO)):
             assert rel(mine.cpu().numpy(), theirs.cpu().numpy()) <= TOL
     f.close()
