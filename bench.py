@@ -615,7 +615,8 @@ def main():
         from workloads import WORKLOADS as WL
 
         secondary = {}
-        for name in ("sphsm_D200k_d500_m128_zipf", "sq_D800k_d512_m256_K10_zipf"):
+        for name in ("sphsm_D200k_d500_m128_zipf", "sq_D800k_d512_m256_K10_zipf",
+                     "taylor_D200k_d500_m128_zipf"):
             print(f"[bench] secondary workload {name}", file=sys.stderr, flush=True)
             secondary[name] = factored_vs_naive(WL[name], dev, 11, 300, 8, profile=True)
         print("[bench] D x d sweep", file=sys.stderr, flush=True)
