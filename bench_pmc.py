@@ -5,6 +5,8 @@
     python bench_pmc.py traffic FETCH.csv WRITE.csv --calib-mib 256 --out SUMMARY.md
         per-launch HBM bytes of each phase from a FETCH_SIZE pass and a WRITE_SIZE pass
         over `bench.py --no-cpu --no-naive --no-secondary --copy-calib 256`
+    python bench_pmc.py stats KERNEL_STATS.csv [--kernels PREFIX ...]
+        one markdown row per kernel of a `rocprofv3 --kernel-trace --stats` summary
 
 Both counters read KiB per dispatch; the bench's plain device copy of a known size (the
 largest __amd_rocclr_copyBuffer dispatch) gives the factor that turns each into bytes.
@@ -74,6 +76,19 @@ def table(path: str, prefixes=None) -> str:
     return "\n".join(out)
 
 
+def stats(path: str, prefixes=None) -> str:
+    out = ["| kernel | calls | average us | min us | max us | share of GPU time |",
+           "|---|---|---|---|---|---|"]
+    for r in _rows(path):
+        k = _short(r["Name"])
+        if prefixes and not any(k.startswith(p) for p in prefixes):
+            continue
+        out.append(f"| `{k}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.3f} | "
+                   f"{float(r['MinNs']) / 1e3:.3f} | {float(r['MaxNs']) / 1e3:.3f} | "
+                   f"{float(r['Percentage']):.2f} % |")
+    return "\n".join(out)
+
+
 def _per_kernel(path, counter):
     acc = collections.defaultdict(list)
     for r in _rows(path):
@@ -117,6 +132,9 @@ def main():
     t = sub.add_parser("table")
     t.add_argument("csv")
     t.add_argument("--kernels", nargs="*")
+    st = sub.add_parser("stats")
+    st.add_argument("csv")
+    st.add_argument("--kernels", nargs="*")
     tr = sub.add_parser("traffic")
     tr.add_argument("fetch_csv")
     tr.add_argument("write_csv")
@@ -126,6 +144,9 @@ def main():
     a = ap.parse_args()
     if a.cmd == "table":
         print(table(a.csv, a.kernels))
+        return
+    if a.cmd == "stats":
+        print(stats(a.csv, a.kernels))
         return
     ph, cf, cw = traffic(a.fetch_csv, a.write_csv, a.calib_mib)
     lines = [a.header.rstrip(), "",
