@@ -15,6 +15,50 @@ using namespace lst;
 
 namespace lst {
 thread_local ProfHook g_prof;
+
+// The step's intermediates for minibatches of up to m examples with up to K slots
+// each (m x d, m x m, per-example and per-slot pieces), and grad_H's stand-in for
+// steps given no grad_H buffer.
+void carve_step(StepBufs &b, float *&gradH, size_t m, size_t d, size_t K, Carver &cv) {
+  const size_t md = m * d, mm = m * m, mk = m * (K > 0 ? K : 1);
+  b.Hhat = cv.take<float>(md);
+  b.Htil = cv.take<float>(md);
+  b.X = cv.take<float>(md);
+  b.G = cv.take<float>(md);
+  b.Atil = cv.take<float>(md);
+  b.W1 = cv.take<float>(md);
+  b.P2 = cv.take<float>(md);
+  b.P3 = cv.take<float>(md);
+  b.RX = cv.take<float>(md);
+  b.Zq = cv.take<float>(md);
+  gradH = cv.take<float>(md);
+  b.N = cv.take<float>(mm);
+  b.Mhat = cv.take<float>(mm);
+  b.HZ = cv.take<float>(mm);
+  b.YY = cv.take<float>(mm);
+  b.E2 = cv.take<float>(mm);
+  b.E4 = cv.take<float>(mm);
+  b.R = cv.take<float>(mm);
+  b.Cwork = cv.take<float>(mm);
+  b.qpart = cv.take<float>((d + 15) / 16 * m);
+  b.bpart = cv.take<float>((m + 15) / 16 * m);
+  b.q = cv.take<float>(m);
+  b.tsum = cv.take<float>(m);
+  b.qcnt = cv.take<int>((m + 15) / 16);
+  b.dq = cv.take<float>(m);
+  b.lvec = cv.take<float>(m);
+  b.dA = cv.take<float>(mk);
+  b.wA = cv.take<float>(mk);
+  b.sval = cv.take<float>(mk);
+  b.srow = cv.take<int>(mk);
+  b.scnt = cv.take<int>(m);
+  b.coef = cv.take<float>(8);
+  b.cert = cv.take<int>(1);
+  b.SW = cv.take<float>(2 * m);
+  b.ds = cv.take<float>(m);
+  b.yb = cv.take<float>(m);
+  b.cwo = cv.take<float>(2 * m);
+}
 }  // namespace lst
 
 namespace {
@@ -25,20 +69,7 @@ constexpr int kColnormBlocks = 1024;
 constexpr size_t kInitPartialCap = size_t(8) << 20;  // floats of split-k partials for Q = V^T V
 constexpr int kWbarBlocks = 256;                    // row blocks of the column sums V^T 1_D
 constexpr int kDefaultSpin = 1 << 20;               // polls of the online step's barrier
-constexpr size_t kWsAlign = 256;
 
-// Device workspace carved in 256-byte aligned pieces (a null base only measures).
-struct Carver {
-  char *base;
-  size_t off = 0;
-  template <class T>
-  T *take(size_t n) {
-    off = (off + kWsAlign - 1) & ~(kWsAlign - 1);
-    T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
-    off += n * sizeof(T);
-    return p;
-  }
-};
 
 // A factored step recorded as a HIP graph, replayed when the same arguments recur.
 struct GraphEntry {
@@ -120,50 +151,6 @@ size_t init_partial_floats(int64_t D, int d) {
   GemmDesc g = gemm_desc(d, d, (int)D, nullptr, d, 1, nullptr, d, 1, nullptr, d);
   const size_t want = gemm_plan_split(g, kTargetWGs, nullptr);
   return std::min(want, kInitPartialCap / ((size_t)d * d) * ((size_t)d * d));
-}
-
-// The step's intermediates for minibatches of up to m examples with up to K slots
-// each (m x d, m x m, per-example and per-slot pieces), and grad_H's stand-in for
-// steps given no grad_H buffer.
-void carve_step(StepBufs &b, float *&gradH, size_t m, size_t d, size_t K, Carver &cv) {
-  const size_t md = m * d, mm = m * m, mk = m * (K > 0 ? K : 1);
-  b.Hhat = cv.take<float>(md);
-  b.Htil = cv.take<float>(md);
-  b.X = cv.take<float>(md);
-  b.G = cv.take<float>(md);
-  b.Atil = cv.take<float>(md);
-  b.W1 = cv.take<float>(md);
-  b.P2 = cv.take<float>(md);
-  b.P3 = cv.take<float>(md);
-  b.RX = cv.take<float>(md);
-  b.Zq = cv.take<float>(md);
-  gradH = cv.take<float>(md);
-  b.N = cv.take<float>(mm);
-  b.Mhat = cv.take<float>(mm);
-  b.HZ = cv.take<float>(mm);
-  b.YY = cv.take<float>(mm);
-  b.E2 = cv.take<float>(mm);
-  b.E4 = cv.take<float>(mm);
-  b.R = cv.take<float>(mm);
-  b.Cwork = cv.take<float>(mm);
-  b.qpart = cv.take<float>((d + 15) / 16 * m);
-  b.bpart = cv.take<float>((m + 15) / 16 * m);
-  b.q = cv.take<float>(m);
-  b.tsum = cv.take<float>(m);
-  b.qcnt = cv.take<int>((m + 15) / 16);
-  b.dq = cv.take<float>(m);
-  b.lvec = cv.take<float>(m);
-  b.dA = cv.take<float>(mk);
-  b.wA = cv.take<float>(mk);
-  b.sval = cv.take<float>(mk);
-  b.srow = cv.take<int>(mk);
-  b.scnt = cv.take<int>(m);
-  b.coef = cv.take<float>(8);
-  b.cert = cv.take<int>(1);
-  b.SW = cv.take<float>(2 * m);
-  b.ds = cv.take<float>(m);
-  b.yb = cv.take<float>(m);
-  b.cwo = cv.take<float>(2 * m);
 }
 
 void carve_factored(lst_ctx *c, Carver &cv) {

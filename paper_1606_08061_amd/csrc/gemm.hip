@@ -16,6 +16,7 @@
 // reads the last valid row instead, since that output is never stored; only
 // the ragged end of the k range is masked.  Operands are fetched kStage
 // k-blocks ahead of the matrix cores.
+#include <algorithm>
 #include "gemm_tiles.h"
 
 namespace lst {
@@ -275,16 +276,17 @@ GemmDesc gemm_desc(int M, int N, int K, const float *A, int64_t lda, int tA, con
 size_t gemm_plan_split(GemmDesc &g, int target_wgs, float *partial) {
   const int tiles = ((g.M + 31) / 32) * ((g.N + 31) / 32);
   int splits = (target_wgs + tiles - 1) / tiles;
-  const int max_splits = (g.K + 255) / 256;  // at least 256 k per split
+  // (k arithmetic in 64 bits: K may be D, up to 2^31 - 1)
+  const int max_splits = (int)(((int64_t)g.K + 255) / 256);  // at least 256 k per split
   if (splits > max_splits) splits = max_splits;
   if (splits < 2) {
     g.splits = 1;
     g.kchunk = g.K;
     return 0;
   }
-  int chunk = (g.K + splits - 1) / splits;
+  int chunk = (int)(((int64_t)g.K + splits - 1) / splits);
   chunk = (chunk + 7) / 8 * 8;
-  splits = (g.K + chunk - 1) / chunk;
+  splits = (int)(((int64_t)g.K + chunk - 1) / chunk);
   g.splits = splits;
   g.kchunk = chunk;
   g.partial = partial;
@@ -302,8 +304,8 @@ int gemm_prepare(GemmBatch &b) {
     g.tile_begin = total;
     if (g.M > 0 && g.N > 0) {
       total += g.tiles_m * g.tiles_n * (g.splits > 1 ? g.splits : 1);
-      const int kk = g.splits > 1 ? g.kchunk : g.K + g.K2;
-      if (kk > kmax) kmax = kk;
+      const int64_t kk = g.splits > 1 ? (int64_t)g.kchunk : (int64_t)g.K + g.K2;
+      if (kk > kmax) kmax = (int)std::min<int64_t>(kk, 1 << 30);
     }
   }
   // Empty descriptors (M or N == 0) own no tiles; give them tile_begin past the end.

@@ -251,6 +251,22 @@ struct StepArgs {
 };
 
 void build_step_plan(const StepBufs &sb, int m, StepPlan &pl);
+
+// Device memory carved in 256-byte aligned pieces (a null base only measures).
+constexpr size_t kWsAlign = 256;
+struct Carver {
+  char *base;
+  size_t off = 0;
+  template <class T>
+  T *take(size_t n) {
+    off = (off + kWsAlign - 1) & ~(kWsAlign - 1);
+    T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+    off += n * sizeof(T);
+    return p;
+  }
+};
+// The step's intermediates for up to m examples of up to K slots (api.hip).
+void carve_step(StepBufs &b, float *&gradH, size_t m, size_t d, size_t K, Carver &cv);
 // which = 0..4: launch which + 1 of the step.
 void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, const StepPlan *dev,
                          const StepArgs &a, hipStream_t s);
