@@ -101,7 +101,7 @@ struct TileCtx {
   float *gH;
   float lr;
   const float *dq;    // dl/dq for the scale modes (may be null when no term scales)
-  const float *coef;  // polynomial coefficients (LDS), or null
+  const float *coef;  // polynomial coefficients, or null
 };
 
 __device__ __forceinline__ float coef_of(const TileCtx &x, int c) { return c < 0 ? 1.f : x.coef[c]; }
@@ -409,11 +409,11 @@ __device__ __forceinline__ int section_tile(int w, int T) {
 // descriptors replace theirs when the polynomial is not certified.
 __device__ __forceinline__ void run_op(const OpBatch &ob, int tile, const TileCtx &x, bool cert) {
   int di = 0;
-  for (int q = 1; q < ob.n; ++q)
-    if (tile >= ob.op[q].tile_begin) di = q;
-  if (di >= ob.n_main) return;  // alt descriptors own no tiles of their own
+#pragma unroll
+  for (int q = 1; q < kMaxOps; ++q)
+    if (q < ob.n_main && tile >= ob.begin[q]) di = q;
   const Op16 *g = &ob.op[di];
-  const int local = tile - g->tile_begin;
+  const int local = tile - ob.begin[di];
   if (!cert && g->alt >= 0) g = &ob.op[g->alt];
   op16_tile(*g, local, x);
 }
@@ -574,51 +574,6 @@ __device__ __forceinline__ void sorted_slots(int j, int K, const int *sr, const 
   }
 }
 
-// The loss epilogue on register arrays (KM slots, fully unrolled): the serial part of
-// a gather workgroup then makes no dependent LDS reads.
-template <int KM>
-__device__ __forceinline__ void epilogue_reg(int loss, float q, float sj, float hw, int K,
-                                             const int (&r)[KM], const float (&t)[KM],
-                                             const float (&a)[KM], float Dn, float eps, float &l,
-                                             float (&g)[KM]) {
-  l = 0.f;
-  if (loss == LST_LOSS_SQUARED) {
-    float at = 0.f, yy = 0.f;
-#pragma unroll
-    for (int k = 0; k < KM; ++k) {
-      const bool ok = k < K && r[k] >= 0;
-      g[k] = ok ? -2.f * t[k] : 0.f;
-      if (!ok) continue;
-      at += t[k] * a[k];
-#pragma unroll
-      for (int kk = 0; kk < KM; ++kk)
-        if (kk < K && r[kk] == r[k]) yy += t[k] * t[kk];
-    }
-    l = q - 2.f * at + yy;
-  } else if (loss == LST_LOSS_TAYLOR_SOFTMAX) {
-    const float lz = logf(Dn + sj + 0.5f * q);
-#pragma unroll
-    for (int k = 0; k < KM; ++k) {
-      g[k] = 0.f;
-      if (k >= K || r[k] < 0) continue;
-      const float ak = a[k] + hw;
-      const float f = 1.f + ak + 0.5f * ak * ak;
-      l += t[k] * (lz - logf(f));
-      g[k] = -t[k] * (1.f + ak) / f;
-    }
-  } else {
-    const float lz = logf(q + Dn * eps);
-#pragma unroll
-    for (int k = 0; k < KM; ++k) {
-      g[k] = 0.f;
-      if (k >= K || r[k] < 0) continue;
-      const float den = a[k] * a[k] + eps;
-      l += t[k] * (lz - logf(den));
-      g[k] = -2.f * t[k] * a[k] / den;
-    }
-  }
-}
-
 // sorted_slots with the example's KM slots in registers (K <= KM).
 template <int KM>
 __device__ __forceinline__ void sorted_slots_reg(int j, int K, const int *sr, const float *sg,
@@ -668,35 +623,44 @@ __device__ __forceinline__ void sorted_slots_reg(int j, int K, const int *sr, co
 // Register-resident form for K <= 4 KPW and d <= 64 NV: wavefront w keeps the
 // target rows k = w, w + 4, ... in registers from the dot products a_kj to the G
 // sum, so V is read once and the index loads lead straight into the row loads.
+// A slot's dl/dA depends on its own a_kj only, so every wavefront forms the
+// derivatives of its slots and its share of G_j = sum_k dl/dA_kj V_r without
+// waiting for the others (squared error: dl/dA = -2 t, known with the indices);
+// the loss, dl/dq and the slot lists follow after the one workgroup barrier.
+// The loss is summed per wavefront (slots w, w + 4, ...), then over the wavefronts
+// in a fixed order.
 template <int KPW, int NV>
 __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
-  constexpr int W = 4;
-  __shared__ int sr[W * KPW];
-  __shared__ float sa[W * KPW], st[W * KPW], sg[W * KPW];
-  __shared__ float s_dq;
-  __shared__ int s_bad;
+  constexpr int W = 4, KM = W * KPW;
+  __shared__ int sr[KM];
+  __shared__ float st[KM], sg[KM];
   __shared__ float gpart[W][64 * NV];
-  __shared__ float sred[W];
+  __shared__ float sred[W], slp[W];  // q partials (squared error), loss partials
+  __shared__ int sbad[W];
   const int K = ga.K, d = ga.d;
   const int t = threadIdx.x, lane = t & 63;
   const int wave = __builtin_amdgcn_readfirstlane(t >> 6);
-  if (t == 0) s_bad = 0;
-  // q_j: for squared error h_j . h^_j here (its operands loaded into registers first
-  // and used after the target rows' dot products, so that the loads overlap); for the
-  // spherical softmax reduced in launch 1 (its E products need every q_j).
+  const bool sq = ga.loss == LST_LOSS_SQUARED, tay = ga.loss == LST_LOSS_TAYLOR_SOFTMAX;
+  const float Dn = (float)ga.D;
+  // q_j: for squared error h_j . h^_j here (its operands loaded first, used after the
+  // target rows' dot products); for the spherical family reduced in launch 1 (its E
+  // products need every q_j), loaded with T, s_j and h~_j as uniform values.
   constexpr int NQ = (64 * NV + 255) / 256;
   float qh[NQ], qhh[NQ];
-  float qv = 0.f, tsv = 0.f;
-  const bool sq = ga.loss == LST_LOSS_SQUARED;
 #pragma unroll
   for (int u = 0; u < NQ; ++u) {
     const int c = t + 256 * u;
     qh[u] = (sq && c < d) ? ga.H[(int64_t)j * d + c] : 0.f;
     qhh[u] = (sq && c < d) ? ga.Hhat[(int64_t)j * d + c] : 0.f;
   }
-  if (!sq && t == 0) {
+  float qv = 0.f, tsv = 0.f, sj = 0.f, hw = 0.f;
+  if (!sq) {
     qv = ga.q[j];
     tsv = ga.tsum[j];
+    if (tay) {
+      sj = ga.SW[2 * j];
+      hw = ga.SW[2 * j + 1];
+    }
   }
   int r[KPW];
   float tv[KPW];  // the slots' target values, loaded with the indices
@@ -734,13 +698,45 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
     const int c = lane + 64 * n;
     ht[n] = (c < d) ? htp[c] : 0.f;
   }
-  float a[KPW];
+  // the loss's log of the normaliser (spherical family)
+  float lz = 0.f;
+  if (tay)
+    lz = logf(Dn + sj + 0.5f * qv);
+  else if (!sq)
+    lz = logf(qv + Dn * ga.eps);
+  // a_kj, dl/dA_kj and this wavefront's part of the loss (squared error: of sum t a)
+  float g[KPW];
+  float lpart = 0.f;
 #pragma unroll
   for (int i = 0; i < KPW; ++i) {
     float sacc = 0.f;
 #pragma unroll
     for (int n = 0; n < NV; ++n) sacc += ht[n] * vr[i][n];
-    a[i] = wave_sum(sacc);
+    const float a = wave_sum(sacc) + hw;
+    const bool ok = wave + W * i < K && r[i] >= 0;
+    float gi = 0.f;
+    if (ok) {
+      if (sq) {
+        gi = -2.f * tv[i];
+        lpart += tv[i] * a;
+      } else if (tay) {
+        const float f = 1.f + a + 0.5f * a * a;
+        lpart += tv[i] * (lz - logf(f));
+        gi = -tv[i] * (1.f + a) / f;
+      } else {
+        const float den = a * a + ga.eps;
+        lpart += tv[i] * (lz - logf(den));
+        gi = -2.f * tv[i] * a / den;
+      }
+    }
+    g[i] = gi;
+  }
+#pragma unroll
+  for (int n = 0; n < NV; ++n) {
+    float gv = 0.f;
+#pragma unroll
+    for (int i = 0; i < KPW; ++i) gv += g[i] * vr[i][n];
+    gpart[wave][lane + 64 * n] = gv;
   }
   if (sq) {
     float qs = 0.f;
@@ -749,72 +745,64 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
     qs = wave_sum(qs);
     if (lane == 0) sred[wave] = qs;
   }
-  __syncthreads();  // s_bad initialised
   if (lane == 0) {
 #pragma unroll
     for (int i = 0; i < KPW; ++i) {
       const int k = wave + W * i;
       if (k < K) {
         sr[k] = r[i];
-        sa[k] = a[i];
         st[k] = tv[i];
+        sg[k] = g[i];
       }
     }
-    if (bad) atomicOr(&s_bad, 1);
+    slp[wave] = lpart;
+    sbad[wave] = bad ? 1 : 0;
   }
   __syncthreads();
-  if (t == 0) {
-    if (s_bad) atomicOr(ga.flag, FLAG_INDEX);
-    const float q = ga.loss == LST_LOSS_SQUARED ? (sred[0] + sred[1]) + (sred[2] + sred[3]) : qv;
-    const bool tay = ga.loss == LST_LOSS_TAYLOR_SOFTMAX;
-    const float sj = tay ? ga.SW[2 * j] : 0.f, hw = tay ? ga.SW[2 * j + 1] : 0.f;
-    const float gq = dq_of(ga.loss, q, sj, tsv, (float)ga.D, ga.eps);
-    constexpr int KM = W * KPW;
-    int rr[KM];
-    float tt[KM], aa[KM], gg[KM];
-#pragma unroll
-    for (int k = 0; k < KM; ++k) {
-      rr[k] = k < K ? sr[k] : -1;
-      tt[k] = k < K ? st[k] : 0.f;
-      aa[k] = k < K ? sa[k] : 0.f;
-    }
-    float l;
-    epilogue_reg<KM>(ga.loss, q, sj, hw, K, rr, tt, aa, (float)ga.D, ga.eps, l, gg);
-    float ybar = 0.f;
-#pragma unroll
-    for (int k = 0; k < KM; ++k)
-      if (k < K) {
-        sg[k] = gg[k];
-        ybar += gg[k];
-      }
-    if (tay) taylor_outputs(ga, j, gq, sj, hw, ybar);
-    ga.dq[j] = gq;
-    ga.lvec[j] = l;
-    s_dq = gq;
-  }
-  __syncthreads();
-  const float gq = s_dq;
-  for (int k = t; k < K; k += 256) {
-    ga.dA[(int64_t)j * K + k] = sg[k];
-    ga.wA[(int64_t)j * K + k] = gq != 0.f ? sg[k] / (2.f * gq) : 0.f;
-  }
-  sorted_slots_reg<W * KPW>(j, K, sr, sg, ga.srow, ga.sval, ga.scnt);
-#pragma unroll
-  for (int n = 0; n < NV; ++n) {
-    float gv = 0.f;
-#pragma unroll
-    for (int i = 0; i < KPW; ++i) {
-      const int k = wave + W * i;
-      if (k < K) gv += sg[k] * vr[i][n];
-    }
-    gpart[wave][lane + 64 * n] = gv;
-  }
-  __syncthreads();
+  // G_j and 2 eta dl/dq_j h~_j
+  const float gq = dq_of(ga.loss, qv, sj, tsv, Dn, ga.eps);
   const float s2 = 2.f * ga.lr * gq;
   for (int c = t; c < d; c += 256) {
     ga.G[(int64_t)j * d + c] = (gpart[0][c] + gpart[1][c]) + (gpart[2][c] + gpart[3][c]);
     ga.Atil[(int64_t)j * d + c] = s2 * htp[c];
   }
+  if (t == 0) {
+    if (sbad[0] | sbad[1] | sbad[2] | sbad[3]) atomicOr(ga.flag, FLAG_INDEX);
+    float l = (slp[0] + slp[1]) + (slp[2] + slp[3]);
+    if (sq) {  // l = q - 2 a.t + ||y||^2, ||y||^2 by index equality
+      const float q = (sred[0] + sred[1]) + (sred[2] + sred[3]);
+      int rr[KM];
+      float tt[KM];
+#pragma unroll
+      for (int k = 0; k < KM; ++k) {
+        rr[k] = k < K ? sr[k] : -1;
+        tt[k] = k < K ? st[k] : 0.f;
+      }
+      float yy = 0.f;
+#pragma unroll
+      for (int k = 0; k < KM; ++k) {
+        if (rr[k] < 0) continue;
+#pragma unroll
+        for (int kk = 0; kk < KM; ++kk)
+          if (rr[kk] == rr[k]) yy += tt[k] * tt[kk];
+      }
+      l = q - 2.f * l + yy;
+    }
+    ga.lvec[j] = l;
+    ga.dq[j] = gq;
+    if (tay) {
+      float ybar = 0.f;
+#pragma unroll
+      for (int k = 0; k < KM; ++k)
+        if (k < K) ybar += sg[k];
+      taylor_outputs(ga, j, gq, sj, hw, ybar);
+    }
+  }
+  for (int k = t; k < K; k += 256) {
+    ga.dA[(int64_t)j * K + k] = sg[k];
+    ga.wA[(int64_t)j * K + k] = gq != 0.f ? sg[k] / (2.f * gq) : 0.f;
+  }
+  sorted_slots_reg<KM>(j, K, sr, sg, ga.srow, ga.sval, ga.scnt);
 }
 
 // General form (any K <= LST_MAX_K, any d): the K dot products spread over the
@@ -1199,12 +1187,9 @@ __global__ __launch_bounds__(256, 5) void step_mid_kernel(const StepPlan *__rest
   if (w < sec) {
     const int tile = section_tile(w, ob.total);
     if (tile < 0) return;
-    __shared__ float sc[8];
-    if (threadIdx.x < 8) sc[threadIdx.x] = coef[threadIdx.x];
-    const bool ok = *cert != 0;
-    __syncthreads();
-    const TileCtx x{H, gH, lr, dq, sc};
-    run_op(ob, tile, x, ok);
+    // the coefficients and the certificate are read where they are used (uniform loads)
+    const TileCtx x{H, gH, lr, dq, coef};
+    run_op(ob, tile, x, *cert != 0);
     return;
   }
   const GemmBatch &gb = pl->gb_mid;
@@ -1273,6 +1258,7 @@ void finalize(OpBatch &ob, int n_main) {
   }
   for (int q = 0; q < ob.n; ++q)
     if (q >= n_main || ob.op[q].M <= 0 || ob.op[q].N <= 0) ob.op[q].tile_begin = total;
+  for (int q = 0; q < kMaxOps; ++q) ob.begin[q] = q < ob.n ? ob.op[q].tile_begin : total;
   ob.total = total;
   ob.n_main = n_main;
 }

@@ -199,11 +199,14 @@ struct Op16 {
   int alt;  // >= 0: the descriptor used instead when the Woodbury polynomial is not certified
 };
 
+// The header fields come first and the tile ranges are repeated there, so that a
+// workgroup finds its descriptor from one cache line.
 struct OpBatch {
+  int n;                 // descriptors (including alternates)
+  int n_main;            // descriptors that own tiles (the first n_main)
+  int total;             // tiles
+  int begin[kMaxOps];    // op[q].tile_begin
   Op16 op[kMaxOps];
-  int n;       // descriptors (including alternates)
-  int n_main;  // descriptors that own tiles (the first n_main)
-  int total;   // tiles
 };
 
 // The products of one step for one minibatch size m (kept in device memory):
