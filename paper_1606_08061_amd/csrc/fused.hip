@@ -896,7 +896,7 @@ __device__ __forceinline__ void dq_all(const GatherArgs &ga, float *sdq) {
 }
 
 template <int KPW, int NV>
-__global__ __launch_bounds__(256, 5) void step_gather_kernel(const StepPlan *__restrict__ pl,
+__global__ __launch_bounds__(256, 4) void step_gather_kernel(const StepPlan *__restrict__ pl,
                                                           const float *H, float lr,
                                                           const GatherArgs ga) {
   const int w = blockIdx.x;
@@ -1128,7 +1128,7 @@ struct MidArgs {
   int *flag;
 };
 
-__global__ __launch_bounds__(256, 5) void step_zgrad_kernel(const StepPlan *__restrict__ pl,
+__global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__restrict__ pl,
                                                          const float *H, float *gH, float lr,
                                                          const float *dq, const MidArgs ma,
                                                          const CertArgs ca) {
@@ -1175,7 +1175,7 @@ __global__ __launch_bounds__(256, 5) void step_zgrad_kernel(const StepPlan *__re
 // Launch 4: Zq, R X and the U update.  Launch 5: the Q and U^{-T} updates and the
 // V scatter.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256, 5) void step_mid_kernel(const StepPlan *__restrict__ pl,
+__global__ __launch_bounds__(256, 4) void step_mid_kernel(const StepPlan *__restrict__ pl,
                                                        const float *H, float *gH, float lr,
                                                        const float *dq,
                                                        const float *__restrict__ coef,
@@ -1192,10 +1192,13 @@ __global__ __launch_bounds__(256, 5) void step_mid_kernel(const StepPlan *__rest
     run_op(ob, tile, x, *cert != 0);
     return;
   }
+  // The U update (k = m): four k-blocks of 8 per wavefront at m = 128, all loaded
+  // before the first product (the launch bound of four workgroups per CU leaves the
+  // registers for that).
   const GemmBatch &gb = pl->gb_mid;
   const int w2 = w - sec;
   if (w2 >= gb.total_tiles) return;
-  gemm_body<4, 2>(gb, H, gH, lr, flag, w2);
+  gemm_body<4, 4>(gb, H, gH, lr, flag, w2);
 }
 
 __global__ __launch_bounds__(256, 5) void step_update_kernel(const StepPlan *__restrict__ pl,
@@ -1206,12 +1209,14 @@ __global__ __launch_bounds__(256, 5) void step_update_kernel(const StepPlan *__r
                                                           const float *__restrict__ wA,
                                                           const float *__restrict__ RX, float *V,
                                                           int64_t ldv) {
-  const int w = blockIdx.x;
-  const int ssec = (n + 7) & ~7;  // the scatter first: its workgroups are short
-  if (w >= ssec) {
-    gemm_body<4, 2>(pl->gb_update, H, gH, lr, flag, w - ssec);
+  // the products first (their workgroups are the long ones), then the scatter
+  const int gsec = (pl->gb_update.total_tiles + 7) & ~7;
+  if (blockIdx.x < gsec) {
+    if ((int)blockIdx.x < pl->gb_update.total_tiles)
+      gemm_body<4, 2>(pl->gb_update, H, gH, lr, flag, blockIdx.x);
     return;
   }
+  const int w = blockIdx.x - gsec;
   if (w >= n) return;
   extern __shared__ int sh[];
   if (*flag != 0) return;
@@ -1429,7 +1434,7 @@ void step_launch_sizes(const StepPlan &pl, int m, int K, int (&grid)[5]) {
   grid[1] = sec(m) + sec(pl.ob[1].total);
   grid[2] = sec(pl.ob[2].total) + (m * m + 255) / 256 + 2;
   grid[3] = sec(pl.ob[3].total) + pl.gb_mid.total_tiles;
-  grid[4] = sec(m * K) + pl.gb_update.total_tiles;
+  grid[4] = sec(pl.gb_update.total_tiles) + m * K;
 }
 
 void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, const StepPlan *dev,
