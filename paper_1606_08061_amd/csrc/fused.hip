@@ -405,6 +405,30 @@ __device__ __forceinline__ int section_tile(int w, int T) {
   return x < r ? x * (q + 1) + slot : r * (q + 1) + (x - r) * q + slot;
 }
 
+// The same with each product split over the XCDs on its own: XCD x owns a contiguous
+// eighth of every product's tiles, so that products of different k lengths spread
+// evenly over the chip.  section_by_op: the section's workgroups.
+__host__ __device__ __forceinline__ int section_by_op(const OpBatch &ob) {
+  int n = 0;
+  for (int q = 0; q < kMaxOps; ++q)
+    if (q < ob.n_main) n += (ob.count[q] + 7) >> 3;
+  return 8 * n;
+}
+
+__device__ __forceinline__ int tile_by_op(const OpBatch &ob, int w) {
+  const int x = w & 7;
+  int s = w >> 3;
+#pragma unroll
+  for (int q = 0; q < kMaxOps; ++q) {
+    if (q >= ob.n_main) break;
+    const int T = ob.count[q], c8 = T >> 3, r = T & 7;
+    const int c = x < r ? c8 + 1 : c8;
+    if (s < c) return ob.begin[q] + (x < r ? x * (c8 + 1) : r * (c8 + 1) + (x - r) * c8) + s;
+    s -= c;
+  }
+  return -1;
+}
+
 // Tile `tile` of a batch of Op16 (the descriptor whose range holds it); alt
 // descriptors replace theirs when the polynomial is not certified.
 __device__ __forceinline__ void run_op(const OpBatch &ob, int tile, const TileCtx &x, bool cert) {
@@ -912,7 +936,7 @@ __global__ __launch_bounds__(256, 4) void step_gather_kernel(const StepPlan *__r
     return;
   }
   const OpBatch &ob = pl->ob[1];
-  const int tile = section_tile(w - gsec, ob.total);
+  const int tile = tile_by_op(ob, w - gsec);
   if (tile < 0) return;
   __shared__ __align__(16) float sdq[LST_MAX_M];
   const float *dq = nullptr;
@@ -1134,9 +1158,9 @@ __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__re
                                                          const CertArgs ca) {
   const OpBatch &ob = pl->ob[2];
   const int w = blockIdx.x;
-  const int sec = (ob.total + 7) & ~7;
+  const int sec = section_by_op(ob);
   if (w < sec) {
-    const int tile = section_tile(w, ob.total);
+    const int tile = tile_by_op(ob, w);
     if (tile < 0) return;
     const TileCtx x{H, gH, lr, dq, nullptr};
     run_op(ob, tile, x, true);
@@ -1264,6 +1288,10 @@ void finalize(OpBatch &ob, int n_main) {
   for (int q = 0; q < ob.n; ++q)
     if (q >= n_main || ob.op[q].M <= 0 || ob.op[q].N <= 0) ob.op[q].tile_begin = total;
   for (int q = 0; q < kMaxOps; ++q) ob.begin[q] = q < ob.n ? ob.op[q].tile_begin : total;
+  for (int q = 0; q < kMaxOps; ++q)
+    ob.count[q] = q < n_main && ob.op[q].M > 0 && ob.op[q].N > 0
+                      ? ob.op[q].tiles_m * ob.op[q].tiles_n
+                      : 0;
   ob.total = total;
   ob.n_main = n_main;
 }
@@ -1431,8 +1459,8 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
 void step_launch_sizes(const StepPlan &pl, int m, int K, int (&grid)[5]) {
   auto sec = [](int n) { return (n + 7) & ~7; };
   grid[0] = sec(pl.ob[0].total) + m;
-  grid[1] = sec(m) + sec(pl.ob[1].total);
-  grid[2] = sec(pl.ob[2].total) + (m * m + 255) / 256 + 2;
+  grid[1] = sec(m) + section_by_op(pl.ob[1]);
+  grid[2] = section_by_op(pl.ob[2]) + (m * m + 255) / 256 + 2;
   grid[3] = sec(pl.ob[3].total) + pl.gb_mid.total_tiles;
   grid[4] = sec(pl.gb_update.total_tiles) + m * K;
 }

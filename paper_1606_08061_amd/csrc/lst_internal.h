@@ -206,6 +206,7 @@ struct OpBatch {
   int n_main;            // descriptors that own tiles (the first n_main)
   int total;             // tiles
   int begin[kMaxOps];    // op[q].tile_begin
+  int count[kMaxOps];    // op[q]'s tiles
   Op16 op[kMaxOps];
 };
 

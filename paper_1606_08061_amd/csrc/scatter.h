@@ -51,9 +51,8 @@ __device__ __forceinline__ void scatter_slot(int s, int n, int K, int d, float l
 
   // The row's sum over its `total` slots: columns in groups of four where the
   // layout allows; the slots split into np interleaved parts (np a power of two,
-  // as many as the threads left over by the columns allow), each part's sum
-  // carried in kIlp independent partial sums, the parts then added in a fixed
-  // order through LDS.  Rows with many slots (frequent targets) are so spread
+  // as many as the threads left over by the columns allow), each part summed in
+  // slot order, the parts then added in a fixed order through LDS.  Rows with many slots (frequent targets) are so spread
   // over the workgroup instead of running one slot after another.
   float *vr = V + (int64_t)r * ldv;
   const bool v4 = (d & 3) == 0 && (ldv & 3) == 0 && (reinterpret_cast<uintptr_t>(V) & 15) == 0 &&
@@ -67,51 +66,38 @@ __device__ __forceinline__ void scatter_slot(int s, int n, int K, int d, float l
     const int gl = threadIdx.x % (T / np), part = threadIdx.x / (T / np);
     const int g = g0 + gl;
     const bool active = g < ng;
+    // kIlp slots' rows loaded before any is accumulated (the loads all in flight), then
+    // added in slot order
     constexpr int kIlp = 8;
-    float4 a[kIlp];
-#pragma unroll
-    for (int u = 0; u < kIlp; ++u) a[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 sum = make_float4(0.f, 0.f, 0.f, 0.f);
+    auto row = [&](int q) {
+      const float *pr = P + (int64_t)(q / K) * d + g * width;
+      return v4 ? *reinterpret_cast<const float4 *>(pr) : make_float4(pr[0], 0.f, 0.f, 0.f);
+    };
+    auto add = [&](float w, const float4 &x) {
+      sum.x += w * x.x;
+      sum.y += w * x.y;
+      sum.z += w * x.z;
+      sum.w += w * x.w;
+    };
     if (active) {
       int t = part;
       for (; t + (kIlp - 1) * np < total; t += kIlp * np) {
+        float w[kIlp];
+        float4 x[kIlp];
 #pragma unroll
         for (int u = 0; u < kIlp; ++u) {
           const int q = slist[t + u * np];
-          const float w = dA[q];
-          const float *pr = P + (int64_t)(q / K) * d + g * width;
-          if (v4) {
-            const float4 x = *reinterpret_cast<const float4 *>(pr);
-            a[u].x += w * x.x;
-            a[u].y += w * x.y;
-            a[u].z += w * x.z;
-            a[u].w += w * x.w;
-          } else {
-            a[u].x += w * pr[0];
-          }
+          w[u] = dA[q];
+          x[u] = row(q);
         }
+#pragma unroll
+        for (int u = 0; u < kIlp; ++u) add(w[u], x[u]);
       }
       for (; t < total; t += np) {  // fewer than kIlp left
         const int q = slist[t];
-        const float w = dA[q];
-        const float *pr = P + (int64_t)(q / K) * d + g * width;
-        if (v4) {
-          const float4 x = *reinterpret_cast<const float4 *>(pr);
-          a[0].x += w * x.x;
-          a[0].y += w * x.y;
-          a[0].z += w * x.z;
-          a[0].w += w * x.w;
-        } else {
-          a[0].x += w * pr[0];
-        }
+        add(dA[q], row(q));
       }
-    }
-    float4 sum = a[0];
-#pragma unroll
-    for (int u = 1; u < kIlp; ++u) {
-      sum.x += a[u].x;
-      sum.y += a[u].y;
-      sum.z += a[u].z;
-      sum.w += a[u].w;
     }
     spart[threadIdx.x] = sum;
     __syncthreads();
