@@ -47,13 +47,15 @@ void carve_step(StepBufs &b, float *&gradH, size_t m, size_t d, size_t K, Carver
   b.qcnt = cv.take<int>((m + 15) / 16);
   b.dq = cv.take<float>(m);
   b.lvec = cv.take<float>(m);
-  b.dA = cv.take<float>(mk);
+  b.rcnt = cv.take<int>(mk);
+  b.splan = cv.take<int>(4 * mk);
   b.wA = cv.take<float>(mk);
   b.sval = cv.take<float>(mk);
   b.srow = cv.take<int>(mk);
   b.scnt = cv.take<int>(m);
   b.coef = cv.take<float>(8);
-  b.cert = cv.take<int>(1);
+  b.cert = cv.take<int>(2);  // the certificate, then the scatter's ticket
+  b.ticket = b.cert ? b.cert + 1 : nullptr;
   b.SW = cv.take<float>(2 * m);
   b.ds = cv.take<float>(m);
   b.yb = cv.take<float>(m);
@@ -1113,9 +1115,11 @@ __global__ void __launch_bounds__(256) put_words_kernel(uint32_t *dst, WordChunk
   for (int i = (int)threadIdx.x; i < n; i += 256) dst[i] = c.w[i];
 }
 
-__global__ void __launch_bounds__(64) clear_words_kernel(int *a, int na, int *b, int nb) {
-  for (int i = (int)threadIdx.x; i < na; i += 64) a[i] = 0;
-  for (int i = (int)threadIdx.x; i < nb; i += 64) b[i] = 0;
+__global__ void __launch_bounds__(256) clear_words_kernel(int *a, int na, int *b, int nb, int *c,
+                                                           int nc) {
+  for (int i = (int)threadIdx.x; i < na; i += 256) a[i] = 0;
+  for (int i = (int)threadIdx.x; i < nb; i += 256) b[i] = 0;
+  for (int i = (int)threadIdx.x; i < nc; i += 256) c[i] = 0;
 }
 
 // Bytes of the array a step of m examples, K slots and hidden size d takes: the
@@ -1187,7 +1191,8 @@ int lst_step_noalloc(int64_t D, int32_t d, int32_t loss, float eps, float *V, in
     sd.base = static_cast<char *>(p);
   }
   if (m == 0) {
-    hipLaunchKernelGGL(clear_words_kernel, dim3(1), dim3(64), 0, s, status_dev, 1, nullptr, 0);
+    hipLaunchKernelGGL(clear_words_kernel, dim3(1), dim3(256), 0, s, status_dev, 1, nullptr, 0,
+                       nullptr, 0);
     if (hipGetLastError() != hipSuccess) return LST_E_HIP;
     return launch_fill(s, loss_dev, 0.f) == hipSuccess ? LST_OK : LST_E_HIP;
   }
@@ -1212,8 +1217,8 @@ int lst_step_noalloc(int64_t D, int32_t d, int32_t loss, float eps, float *V, in
   build_step_plan(b, m, host);
   if (put_plan(sd, host, s) != hipSuccess) return LST_E_HIP;
   // the error word and the arrival counters of this layout start at zero
-  hipLaunchKernelGGL(clear_words_kernel, dim3(1), dim3(64), 0, s, status_dev, 1, b.qcnt,
-                     (m + 15) / 16);
+  hipLaunchKernelGGL(clear_words_kernel, dim3(1), dim3(256), 0, s, status_dev, 1, b.qcnt,
+                     (m + 15) / 16, b.rcnt, m * (K > 0 ? K : 1));
   if (hipGetLastError() != hipSuccess) return LST_E_HIP;
   StepArgs a{H, m, idx, val, K, lr, loss_dev, grad_H ? grad_H : gradH};
   for (int l = 0; l < 5; ++l) enqueue_step_launch(l, b, host, dev_plan, a, s);

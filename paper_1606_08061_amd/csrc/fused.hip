@@ -42,7 +42,8 @@
 //      its absolute row sums); W1 = E Xs
 //   3  Z^ with grad_H; HZ; P2 = E^2 Xs; P3 = E^2 W1; E^4; Yring^T Yring; L = sum l_j;
 //      the certificate, the coefficients c_k, and (uncertified) the exact R
-//   4  Zq; R X; the U update                                 [writes U]
+//   4  Zq; R X; the U update; the scatter's plan (each slot's rank in its row, the
+//      slots ordered by row)                                   [writes U]
 //   5  the Q, U^{-T} (and omega, w_bar) updates; the V scatter [writes Q, U^{-T}, V]
 // Q, U, U^{-T}, V, omega and w_bar are read (launches 1-3) before any of them is
 // written (launches 4-5), and every error is raised by launch 3 at the latest; launches 4
@@ -91,10 +92,9 @@ __device__ __forceinline__ float scale_of(int mode, const float *dq, int i) {
 // l = c + 16 g of wavefront w supplies A[i0 + c][k] and B[k][j0 + c] for
 // k = kb + 4 g + s in instruction s of the k-block kb = 16 (w + 4 u); accumulator
 // register r holds C[i0 + 4 g + r][j0 + c].  The four wavefronts' sums are added
-// through LDS in a fixed order.  Loads of up to kGroup k-blocks are issued before
-// their products.
+// through LDS in a fixed order.  Loads of up to eight k-blocks (the G of op16_kloop)
+// are issued before their products.
 // ---------------------------------------------------------------------------
-constexpr int kGroup = 8;
 
 struct TileCtx {
   const float *H;
@@ -502,7 +502,8 @@ struct GatherArgs {
   int64_t ldv;
   int loss;
   float eps, lr;
-  float *G, *Atil, *dq, *dA, *wA, *lvec;
+  float *G, *Atil, *dq, *wA, *lvec;
+  int *ticket;  // the V scatter's partial-sum ticket (launch 5), zeroed here
   int *srow;
   float *sval;
   int *scnt;
@@ -822,10 +823,7 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
       taylor_outputs(ga, j, gq, sj, hw, ybar);
     }
   }
-  for (int k = t; k < K; k += 256) {
-    ga.dA[(int64_t)j * K + k] = sg[k];
-    ga.wA[(int64_t)j * K + k] = gq != 0.f ? sg[k] / (2.f * gq) : 0.f;
-  }
+  for (int k = t; k < K; k += 256) ga.wA[(int64_t)j * K + k] = gq != 0.f ? sg[k] / (2.f * gq) : 0.f;
   sorted_slots_reg<KM>(j, K, sr, sg, ga.srow, ga.sval, ga.scnt);
 }
 
@@ -893,10 +891,7 @@ __device__ __forceinline__ void gather_gen(const GatherArgs &ga, int j) {
   }
   __syncthreads();
   const float gq = s_dq;
-  for (int k = t; k < K; k += 256) {
-    ga.dA[(int64_t)j * K + k] = sg[k];
-    ga.wA[(int64_t)j * K + k] = gq != 0.f ? sg[k] / (2.f * gq) : 0.f;
-  }
+  for (int k = t; k < K; k += 256) ga.wA[(int64_t)j * K + k] = gq != 0.f ? sg[k] / (2.f * gq) : 0.f;
   sorted_slots(j, K, sr, sg, ga.srow, ga.sval, ga.scnt);
   const float s2 = 2.f * ga.lr * gq;
   for (int c = t; c < d; c += 256) {
@@ -926,8 +921,10 @@ __global__ __launch_bounds__(256, 4) void step_gather_kernel(const StepPlan *__r
   const int w = blockIdx.x;
   const int gsec = (ga.m + 7) & ~7;
   if (w < gsec) {
-    // launch 1 is complete: its q-reduction counters start the next step at zero
+    // launch 1 is complete: its q-reduction counters start the next step at zero; the
+    // scatter's ticket starts launch 5 at zero
     if (w == 0 && (int)threadIdx.x < ga.nqcnt) ga.qcnt[threadIdx.x] = 0;
+    if (w == 0 && threadIdx.x == 0) *ga.ticket = 0;
     if (w >= ga.m) return;
     if constexpr (NV > 0)
       gather_reg<KPW, NV>(ga, w);
@@ -1196,15 +1193,16 @@ __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__re
 }
 
 // ---------------------------------------------------------------------------
-// Launch 4: Zq, R X and the U update.  Launch 5: the Q and U^{-T} updates and the
-// V scatter.
+// Launch 4: Zq, R X, the U update and the V scatter's plan.  Launch 5: the Q and U^{-T}
+// updates and the V scatter.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256, 4) void step_mid_kernel(const StepPlan *__restrict__ pl,
                                                        const float *H, float *gH, float lr,
                                                        const float *dq,
                                                        const float *__restrict__ coef,
                                                        const int *__restrict__ cert,
-                                                       const int *__restrict__ flag) {
+                                                       const int *__restrict__ flag, int n,
+                                                       const int *__restrict__ idx, int *splan) {
   const OpBatch &ob = pl->ob[3];
   const int w = blockIdx.x;
   const int sec = (ob.total + 7) & ~7;
@@ -1221,8 +1219,13 @@ __global__ __launch_bounds__(256, 4) void step_mid_kernel(const StepPlan *__rest
   // registers for that).
   const GemmBatch &gb = pl->gb_mid;
   const int w2 = w - sec;
-  if (w2 >= gb.total_tiles) return;
-  gemm_body<4, 4>(gb, H, gH, lr, flag, w2);
+  const int gsec = (gb.total_tiles + 7) & ~7;
+  if (w2 < gsec) {
+    if (w2 < gb.total_tiles) gemm_body<4, 4>(gb, H, gH, lr, flag, w2);
+    return;
+  }
+  // the V scatter's plan for launch 5, 16 slots per workgroup
+  if ((w2 - gsec) * 16 < n) scatter_plan(w2 - gsec, n, idx, splan);
 }
 
 __global__ __launch_bounds__(256, 5) void step_update_kernel(const StepPlan *__restrict__ pl,
@@ -1232,7 +1235,7 @@ __global__ __launch_bounds__(256, 5) void step_update_kernel(const StepPlan *__r
                                                           const int *__restrict__ idx,
                                                           const float *__restrict__ wA,
                                                           const float *__restrict__ RX, float *V,
-                                                          int64_t ldv) {
+                                                          int64_t ldv, const ScatterChunks ch) {
   // the products first (their workgroups are the long ones), then the scatter
   const int gsec = (pl->gb_update.total_tiles + 7) & ~7;
   if (blockIdx.x < gsec) {
@@ -1242,10 +1245,9 @@ __global__ __launch_bounds__(256, 5) void step_update_kernel(const StepPlan *__r
   }
   const int w = blockIdx.x - gsec;
   if (w >= n) return;
-  extern __shared__ int sh[];
   if (*flag != 0) return;
   // V_r -= sum over the row's slots of (dl/dA_kj / (2 dl/dq_j)) (R X)_j
-  scatter_slot<256>(w, n, K, d, 1.f, idx, wA, RX, V, ldv, sh);
+  scatter_planned<256>(w, n, K, d, 1.f, idx, wA, RX, V, ldv, ch);
 }
 
 }  // namespace
@@ -1461,7 +1463,7 @@ void step_launch_sizes(const StepPlan &pl, int m, int K, int (&grid)[5]) {
   grid[0] = sec(pl.ob[0].total) + m;
   grid[1] = sec(m) + section_by_op(pl.ob[1]);
   grid[2] = section_by_op(pl.ob[2]) + (m * m + 255) / 256 + 2;
-  grid[3] = sec(pl.ob[3].total) + pl.gb_mid.total_tiles;
+  grid[3] = sec(pl.ob[3].total) + sec(pl.gb_mid.total_tiles) + (m * K + 15) / 16;
   grid[4] = sec(pl.gb_update.total_tiles) + m * K;
 }
 
@@ -1498,7 +1500,7 @@ void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, co
       ga.G = sb.G;
       ga.Atil = sb.Atil;
       ga.dq = sb.dq;
-      ga.dA = sb.dA;
+      ga.ticket = sb.ticket;
       ga.wA = sb.wA;
       ga.lvec = sb.lvec;
       ga.srow = sb.srow;
@@ -1534,12 +1536,22 @@ void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, co
     }
     case 3:
       LST_LAUNCH(step_mid_kernel, dim3(grid[3]), dim3(256), 0, s, dev, a.H, a.gH, a.lr, dqp,
-                 sb.coef, sb.cert, sb.flag);
+                 sb.coef, sb.cert, sb.flag, a.m * a.K, a.idx, sb.splan);
       break;
-    default:
-      LST_LAUNCH(step_update_kernel, dim3(grid[4]), dim3(256), (size_t)(2 * a.m * a.K) * sizeof(int),
-                 s, dev, a.H, a.gH, a.lr, sb.flag, a.m * a.K, a.K, sb.d, a.idx, sb.wA, sb.RX, sb.V,
-                 sb.ldv);
+    default: {
+      // rows of more than C slots summed in chunks; the partial sums in P2 and P3, which
+      // launch 4 has finished reading
+      ScatterChunks ch{};
+      ch.C = a.K > 32 ? a.K : 32;
+      ch.half = a.m;
+      ch.part0 = sb.P2;
+      ch.part1 = sb.P3;
+      ch.plan = sb.splan;
+      ch.rcnt = sb.rcnt;
+      ch.ticket = sb.ticket;
+      LST_LAUNCH(step_update_kernel, dim3(grid[4]), dim3(256), 0, s, dev, a.H, a.gH, a.lr, sb.flag, a.m * a.K, a.K, sb.d, a.idx, sb.wA, sb.RX, sb.V,
+                 sb.ldv, ch);
+    }
   }
 }
 

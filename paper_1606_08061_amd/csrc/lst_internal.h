@@ -233,10 +233,13 @@ struct StepBufs {
   float *q, *tsum;       // m: q_j = h_j . h^_j, the sum of example j's valid target weights
   int *qcnt;             // ceil(m/16) arrival counters of the q reduction
   float *dq, *lvec;      // m
-  float *dA, *wA, *sval; // m x K
+  float *dA, *wA, *sval; // m x K (dA: the naive path's only)
   int *srow, *scnt;      // m x K, m
+  int *rcnt;             // m x K: the V scatter's per-row arrival counters (zero between steps)
+  int *splan;            // 4 m x K: the V scatter's plan (meta, pos, sorted, tbl; launch 4)
   float *coef;           // 8
   int *cert;
+  int *ticket;           // the V scatter's next partial-sum id (zeroed by launch 2)
   float *SW;             // m x 2: s_j = h_j . w_bar, h~_j = h_j . omega
   float *ds, *yb;        // m: dl/ds_j, y_bar_j = sum_k dl/dA_kj
   float *cwo;            // 2 x m: eta (2 dq s + D ds + y_bar), eta (2 dq h~ + ds)

@@ -10,12 +10,6 @@ namespace lst {
 
 namespace {
 
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
-
 // Loss epilogue of one example (section 4: l(q, s, K, a, t)).  r[k] < 0 marks an
 // empty slot.  Writes the example's loss, dl/dq, dl/ds and dl/da_k.
 __device__ __forceinline__ void loss_epilogue(int loss, float q, float s, int K, const int *r,

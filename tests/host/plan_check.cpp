@@ -189,7 +189,7 @@ void plans() {
                 {(uintptr_t)b.R, "R"}, {(uintptr_t)b.Cwork, "Cwork"}, {(uintptr_t)b.qpart, "qpart"},
                 {(uintptr_t)b.bpart, "bpart"}, {(uintptr_t)b.q, "q"}, {(uintptr_t)b.tsum, "tsum"},
                 {(uintptr_t)b.qcnt, "qcnt"}, {(uintptr_t)b.dq, "dq"}, {(uintptr_t)b.lvec, "lvec"},
-                {(uintptr_t)b.dA, "dA"}, {(uintptr_t)b.wA, "wA"}, {(uintptr_t)b.sval, "sval"},
+                {(uintptr_t)b.rcnt, "rcnt"}, {(uintptr_t)b.splan, "splan"}, {(uintptr_t)b.wA, "wA"}, {(uintptr_t)b.sval, "sval"},
                 {(uintptr_t)b.srow, "srow"}, {(uintptr_t)b.scnt, "scnt"}, {(uintptr_t)b.coef, "coef"},
                 {(uintptr_t)b.cert, "cert"}, {(uintptr_t)b.SW, "SW"}, {(uintptr_t)b.ds, "ds"},
                 {(uintptr_t)b.yb, "yb"}, {(uintptr_t)b.cwo, "cwo"}};

@@ -106,6 +106,21 @@ def test_duplicates_and_empty_slots(loss, D, K):
     c.close()
 
 
+@pytest.mark.parametrize("D,d,m,K", [(8, 40, 128, 8), (3, 37, 96, 3), (48, 24, 120, 48)])
+def test_frequent_rows_summed_in_chunks(D, d, m, K):
+    # A V row with more than max(32, K) slots is summed by several workgroups (chunks of
+    # that many slots, partial sums added in chunk order by the last to arrive): every
+    # example targets every row here, so each row has m slots (3 or 4 chunks); d = 37 takes
+    # the one-column partial sums, K = 48 the chunk size K.
+    w = Workload("t", LOSS_SQUARED, D, d, m, K, index_dist="uniform", lr=1e-3)
+    c = Compare(w, seed=D * 1000 + K)
+    for t in range(5):
+        st, l, g, ref = c.step()
+        _check_step(st, l, g, ref, TOL1 if t == 0 else TOL100)
+    assert rel(c.W_gpu(), c.W) <= TOL100
+    c.close()
+
+
 def test_duplicates_spherical_softmax_most_classes_targeted():
     # The spherical softmax with K = 16 slots over D = 40 classes (Zipf), the same repeated
     # and empty slots.  With most classes targeted many a_kj sit near 0, where d/da of
