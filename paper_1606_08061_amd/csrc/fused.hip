@@ -445,12 +445,12 @@ __device__ __forceinline__ void run_op(const OpBatch &ob, int tile, const TileCt
 // ---------------------------------------------------------------------------
 // Launch 1: contractions, N, prefetch of the target rows.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256, 5) void step_contract_kernel(
+__global__ __launch_bounds__(256, 4) void step_contract_kernel(
     const StepPlan *__restrict__ pl, const float *H, float lr, const int *__restrict__ idx,
     const float *__restrict__ val, int K, const float *__restrict__ V, int64_t ldv, int64_t D,
     int d, int m, float *__restrict__ tsum) {
   const OpBatch &ob = pl->ob[0];
-  const int w = blockIdx.x;
+  int w = blockIdx.x;
   const int sec = (ob.total + 7) & ~7;
   if (w < sec) {
     const int tile = section_tile(w, ob.total);
@@ -459,10 +459,17 @@ __global__ __launch_bounds__(256, 5) void step_contract_kernel(
     run_op(ob, tile, x, true);
     return;
   }
+  w -= sec;
+  const GemmBatch &gb = pl->gb_contract;
+  const int gsec = (gb.total_tiles + 7) & ~7;
+  if (w < gsec) {  // the products on 32 x 32 tiles (large shapes)
+    if (w < gb.total_tiles) gemm_body<4, 4>(gb, H, nullptr, lr, nullptr, w);
+    return;
+  }
   // Prefetch workgroup of example j (XCD j % 8, that of its gather workgroup in
   // launch 2): the indices, then one load per 128-byte line of every target row;
   // also the sum of the example's target weights over its valid slots, in slot order.
-  const int j = w - sec;
+  const int j = w - gsec;
   if (j >= m) return;
   __shared__ int prow[LST_MAX_K];
   __shared__ float pval[LST_MAX_K];
@@ -1276,6 +1283,15 @@ Op16 op(int M, int N, int K, const float *A, int64_t lda, int tA, const float *B
   return g;
 }
 
+constexpr int kContract32MinTiles = 128;  // 32 x 32 tiles of one m x d product
+
+// Launch 1's m x d products on 32 x 32 tiles once a product has 128 of them (measured:
+// slower at m = 128, d = 500, where 16 x 16 tiles fill the chip better; 2-6 % faster
+// per step at m = 256, d = 512 and at m = 512, d = 256 to 1024).
+bool contract_on_32(int m, int d) {
+  return ((m + 31) / 32) * ((d + 31) / 32) >= kContract32MinTiles;
+}
+
 void finalize(OpBatch &ob, int n_main) {
   int total = 0;
   for (int q = 0; q < ob.n; ++q) {
@@ -1307,25 +1323,42 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
   const bool tay = sb.loss == LST_LOSS_TAYLOR_SOFTMAX;
   const float *H = sym_H();
   float *gH = sym_gradH();
-  // Launch 1: H^ = H Q (row partials h . h^ -> qpart), H~ = H U^T, X = H U^{-T T}, N = H H^T
+  // Launch 1: H^ = H Q (row partials h . h^ -> qpart), H~ = H U^T, X = H U^{-T T}, N = H H^T.
+  // At large shapes the m x d products go to 32 x 32 tiles, which read half the operand
+  // bytes per output (H^ stays on 16 x 16 tiles for the spherical family, whose epilogue
+  // reduces q_j).
   {
     OpBatch &ob = pl.ob[0];
-    ob.op[0] = op(m, d, d, H, d, 0, sb.Q, ldd, 0, sb.Hhat, d);
-    if (!sq) {  // the spherical softmax's launch 2 needs every q_j at its start
-      ob.op[0].rowred = RR_DOT;
-      ob.op[0].Rr = H;
-      ob.op[0].ldrr = d;
-      ob.op[0].rowout = sb.qpart;
-      ob.op[0].qout = sb.q;
-      ob.op[0].qcnt = sb.qcnt;
+    GemmBatch &gb = pl.gb_contract;
+    const bool big = contract_on_32(m, d);
+    ob.n = 0;
+    gb.n = 0;
+    if (!sq || !big) {
+      Op16 h = op(m, d, d, H, d, 0, sb.Q, ldd, 0, sb.Hhat, d);
+      if (!sq) {  // the spherical softmax's launch 2 needs every q_j at its start
+        h.rowred = RR_DOT;
+        h.Rr = H;
+        h.ldrr = d;
+        h.rowout = sb.qpart;
+        h.qout = sb.q;
+        h.qcnt = sb.qcnt;
+      }
+      ob.op[ob.n++] = h;
+    } else {
+      gb.d[gb.n++] = gemm_desc(m, d, d, H, d, 0, sb.Q, ldd, 0, sb.Hhat, d);
     }
-    ob.op[1] = op(m, d, d, H, d, 0, sb.U, ldd, 0, sb.Htil, d);
-    ob.op[2] = op(m, d, d, H, d, 0, sb.UinvT, ldd, 0, sb.X, d);
-    ob.op[3] = op(m, m, d, H, d, 0, H, d, 0, sb.N, m);
-    ob.n = 4;
+    if (big) {
+      gb.d[gb.n++] = gemm_desc(m, d, d, H, d, 0, sb.U, ldd, 0, sb.Htil, d);
+      gb.d[gb.n++] = gemm_desc(m, d, d, H, d, 0, sb.UinvT, ldd, 0, sb.X, d);
+    } else {
+      ob.op[ob.n++] = op(m, d, d, H, d, 0, sb.U, ldd, 0, sb.Htil, d);
+      ob.op[ob.n++] = op(m, d, d, H, d, 0, sb.UinvT, ldd, 0, sb.X, d);
+    }
+    ob.op[ob.n++] = op(m, m, d, H, d, 0, H, d, 0, sb.N, m);
     if (tay)  // [s h~] = H [w_bar omega] (eq. svec, gen-htilde)
       ob.op[ob.n++] = op(m, 2, d, H, d, 0, sb.WO, ldd, 0, sb.SW, 2);
     finalize(ob, ob.n);
+    if (gb.n) gemm_prepare(gb);
   }
   // Launch 2: M^ = H H^^T; E^2 = 4 eta^2 S N D N S (|row| partials -> bpart);
   // W1 = E Xs = 2 eta S N D X
@@ -1460,7 +1493,7 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
 
 void step_launch_sizes(const StepPlan &pl, int m, int K, int (&grid)[5]) {
   auto sec = [](int n) { return (n + 7) & ~7; };
-  grid[0] = sec(pl.ob[0].total) + m;
+  grid[0] = sec(pl.ob[0].total) + sec(pl.gb_contract.total_tiles) + m;
   grid[1] = sec(m) + section_by_op(pl.ob[1]);
   grid[2] = section_by_op(pl.ob[2]) + (m * m + 255) / 256 + 2;
   grid[3] = sec(pl.ob[3].total) + sec(pl.gb_mid.total_tiles) + (m * K + 15) / 16;

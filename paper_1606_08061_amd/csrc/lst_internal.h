@@ -215,7 +215,8 @@ struct OpBatch {
 // gb_update (the Q and U^{-T} updates, launch 5) on 32 x 32 tiles.
 struct StepPlan {
   OpBatch ob[4];
-  GemmBatch gb_mid, gb_update;
+  GemmBatch gb_contract, gb_mid, gb_update;  // gb_contract: launch 1's products on 32 x 32
+                                             // tiles at large shapes (else empty)
 };
 
 // The context's state and workspace pieces the step uses.

@@ -226,6 +226,9 @@ void plans() {
                             ldd, l + 1);
               check_batch(sp, pl.ob[l], tag);
             }
+            std::snprintf(tag, sizeof tag, "loss %d m %d d %d K %d ldd %d contraction", loss, m, d,
+                          K, ldd);
+            check_gemm(sp, pl.gb_contract, tag);
             std::snprintf(tag, sizeof tag, "loss %d m %d d %d K %d ldd %d U update", loss, m, d, K, ldd);
             check_gemm(sp, pl.gb_mid, tag);
             std::snprintf(tag, sizeof tag, "loss %d m %d d %d K %d ldd %d Q/U^-T update", loss, m, d,
