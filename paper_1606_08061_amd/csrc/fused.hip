@@ -1156,12 +1156,17 @@ struct MidArgs {
   int *flag;
 };
 
+// BIG: the plan has products on 32 x 32 tiles (a separate instantiation, so that the
+// other shapes keep the smaller kernel: with the 32 x 32 section compiled in, the
+// registers and LDS it takes made the step 5 us slower at m = 128, d = 500, section
+// empty or not).
+template <bool BIG>
 __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__restrict__ pl,
                                                          const float *H, float *gH, float lr,
                                                          const float *dq, const MidArgs ma,
                                                          const CertArgs ca) {
   const OpBatch &ob = pl->ob[2];
-  const int w = blockIdx.x;
+  int w = blockIdx.x;
   const int sec = section_by_op(ob);
   if (w < sec) {
     const int tile = tile_by_op(ob, w);
@@ -1170,8 +1175,18 @@ __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__re
     run_op(ob, tile, x, true);
     return;
   }
+  w -= sec;
+  if constexpr (BIG) {
+    const GemmBatch &gb = pl->gb_zgrad;
+    const int gsec = (gb.total_tiles + 7) & ~7;
+    if (w < gsec) {  // the products on 32 x 32 tiles (large shapes)
+      if (w < gb.total_tiles) gemm_body<4, 4>(gb, H, gH, lr, nullptr, w);
+      return;
+    }
+    w -= gsec;
+  }
   const int nyy = (ma.m * ma.m + 255) / 256;
-  const int u = w - sec;
+  const int u = w;
   if (u < nyy) {
     if (ma.K > 0)
       yy_entry(u * 256 + threadIdx.x, ma.m, ma.K, ma.srow, ma.sval, ma.scnt, ma.YY);
@@ -1414,14 +1429,33 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
       hz.uy[1] = sb.yb;
       hz.uyi[1] = 1;
     }
-    ob.op[0] = z;
-    ob.op[1] = hz;
-    ob.op[2] = op(m, m, m, sb.E2, m, 0, sb.E2, m, 1, sb.E4, m);
-    ob.op[3] = op(m, d, m, sb.E2, m, 0, sb.X, d, 1, sb.P2, d);
-    if (!sq) ob.op[3].b[0].sc = SC_SQRT;
-    ob.op[4] = op(m, d, m, sb.E2, m, 0, sb.W1, d, 1, sb.P3, d);
-    ob.n = 5;
-    finalize(ob, 5);
+    // at large shapes the products without a fused epilogue or operand scaling go to
+    // 32 x 32 tiles (as in launch 1)
+    GemmBatch &gb = pl.gb_zgrad;
+    const bool big = contract_on_32(m, d);
+    ob.n = 0;
+    gb.n = 0;
+    ob.op[ob.n++] = z;
+    if (big && !tay)
+      gb.d[gb.n++] = gemm_desc(m, m, d, sb.Htil, d, 0, sb.G, d, 0, sb.HZ, m);
+    else
+      ob.op[ob.n++] = hz;
+    if (big) {
+      gb.d[gb.n++] = gemm_desc(m, m, m, sb.E2, m, 0, sb.E2, m, 1, sb.E4, m);
+      gb.d[gb.n++] = gemm_desc(m, d, m, sb.E2, m, 0, sb.W1, d, 1, sb.P3, d);
+    } else {
+      ob.op[ob.n++] = op(m, m, m, sb.E2, m, 0, sb.E2, m, 1, sb.E4, m);
+      ob.op[ob.n++] = op(m, d, m, sb.E2, m, 0, sb.W1, d, 1, sb.P3, d);
+    }
+    if (big && sq) {
+      gb.d[gb.n++] = gemm_desc(m, d, m, sb.E2, m, 0, sb.X, d, 1, sb.P2, d);
+    } else {
+      ob.op[ob.n] = op(m, d, m, sb.E2, m, 0, sb.X, d, 1, sb.P2, d);
+      if (!sq) ob.op[ob.n].b[0].sc = SC_SQRT;
+      ++ob.n;
+    }
+    finalize(ob, ob.n);
+    if (gb.n) gemm_prepare(gb);
   }
   // Launch 4: Zq = (eta^2/2) M H - eta grad_H (M assembled as it is loaded);
   // R X = 2 eta S (c0 Xs + c1 W1 + c2 P2 + c3 P3 + E^4 (c4 Xs + c5 W1 + c6 P2 + c7 P3)),
@@ -1495,7 +1529,7 @@ void step_launch_sizes(const StepPlan &pl, int m, int K, int (&grid)[5]) {
   auto sec = [](int n) { return (n + 7) & ~7; };
   grid[0] = sec(pl.ob[0].total) + sec(pl.gb_contract.total_tiles) + m;
   grid[1] = sec(m) + section_by_op(pl.ob[1]);
-  grid[2] = section_by_op(pl.ob[2]) + (m * m + 255) / 256 + 2;
+  grid[2] = section_by_op(pl.ob[2]) + sec(pl.gb_zgrad.total_tiles) + (m * m + 255) / 256 + 2;
   grid[3] = sec(pl.ob[3].total) + sec(pl.gb_mid.total_tiles) + (m * K + 15) / 16;
   grid[4] = sec(pl.gb_update.total_tiles) + m * K;
 }
@@ -1563,8 +1597,12 @@ void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, co
     case 2: {
       MidArgs ma{a.m, a.K, sb.srow, sb.sval, sb.scnt, sb.YY, sb.lvec, a.loss, sb.flag};
       CertArgs ca{a.m, sb.bpart, sb.N, dqp, sb.Cwork, sb.R, sb.coef, sb.cert, sb.flag};
-      LST_LAUNCH(step_zgrad_kernel, dim3(grid[2]), dim3(256), 0, s, dev, a.H, a.gH, a.lr, dqp, ma,
-                 ca);
+      if (host.gb_zgrad.n > 0)
+        LST_LAUNCH(step_zgrad_kernel<true>, dim3(grid[2]), dim3(256), 0, s, dev, a.H, a.gH, a.lr,
+                   dqp, ma, ca);
+      else
+        LST_LAUNCH(step_zgrad_kernel<false>, dim3(grid[2]), dim3(256), 0, s, dev, a.H, a.gH, a.lr,
+                   dqp, ma, ca);
       break;
     }
     case 3:

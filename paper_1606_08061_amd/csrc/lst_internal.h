@@ -215,8 +215,9 @@ struct OpBatch {
 // gb_update (the Q and U^{-T} updates, launch 5) on 32 x 32 tiles.
 struct StepPlan {
   OpBatch ob[4];
-  GemmBatch gb_contract, gb_mid, gb_update;  // gb_contract: launch 1's products on 32 x 32
-                                             // tiles at large shapes (else empty)
+  // gb_contract, gb_zgrad: products of launches 1 and 3 on 32 x 32 tiles at large
+  // shapes (else empty)
+  GemmBatch gb_contract, gb_zgrad, gb_mid, gb_update;
 };
 
 // The context's state and workspace pieces the step uses.

@@ -229,6 +229,9 @@ void plans() {
             std::snprintf(tag, sizeof tag, "loss %d m %d d %d K %d ldd %d contraction", loss, m, d,
                           K, ldd);
             check_gemm(sp, pl.gb_contract, tag);
+            std::snprintf(tag, sizeof tag, "loss %d m %d d %d K %d ldd %d launch 3 32 x 32", loss, m,
+                          d, K, ldd);
+            check_gemm(sp, pl.gb_zgrad, tag);
             std::snprintf(tag, sizeof tag, "loss %d m %d d %d K %d ldd %d U update", loss, m, d, K, ldd);
             check_gemm(sp, pl.gb_mid, tag);
             std::snprintf(tag, sizeof tag, "loss %d m %d d %d K %d ldd %d Q/U^-T update", loss, m, d,
