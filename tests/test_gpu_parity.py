@@ -106,13 +106,19 @@ def test_duplicates_and_empty_slots(loss, D, K):
     c.close()
 
 
-@pytest.mark.parametrize("D,d,m,K", [(8, 40, 128, 8), (3, 37, 96, 3), (48, 24, 120, 48)])
-def test_frequent_rows_summed_in_chunks(D, d, m, K):
+@pytest.mark.parametrize("loss,D,d,m,K", [
+    (LOSS_SQUARED, 8, 40, 128, 8), (LOSS_SQUARED, 3, 37, 96, 3), (LOSS_SQUARED, 48, 24, 120, 48),
+    (LOSS_SPHERICAL_SOFTMAX, 3, 40, 128, 1), (LOSS_TAYLOR_SOFTMAX, 3, 40, 128, 1),
+])
+def test_frequent_rows_summed_in_chunks(loss, D, d, m, K):
     # A V row with more than max(32, K) slots is summed by several workgroups (chunks of
-    # that many slots, partial sums added in chunk order by the last to arrive): every
-    # example targets every row here, so each row has m slots (3 or 4 chunks); d = 37 takes
-    # the one-column partial sums, K = 48 the chunk size K.
-    w = Workload("t", LOSS_SQUARED, D, d, m, K, index_dist="uniform", lr=1e-3)
+    # that many slots, partial sums added in chunk order by the last to arrive): with D <= K
+    # every example targets every row, so each row has m slots (3 or 4 chunks); d = 37 takes
+    # the one-column partial sums, K = 48 the chunk size K; the softmax losses (one-hot
+    # targets over D = 3 classes, about 43 slots a row: two chunks) weight the slots by
+    # their own dl/dA.
+    w = Workload("t", loss, D, d, m, K, index_dist="uniform", lr=1e-3,
+                 value_dist="normal" if loss == LOSS_SQUARED else "ones")
     c = Compare(w, seed=D * 1000 + K)
     for t in range(5):
         st, l, g, ref = c.step()
