@@ -240,12 +240,28 @@ __global__ __launch_bounds__(256) void online_step_kernel(
     float *q = Q + (int64_t)r * ldd, *u = U + (int64_t)r * ldd, *x = UinvT + (int64_t)r * ldd;
     const float hr = sh[r], gr = 2.f * (shh[r] - sy[r]);
     const float ur = -2.f * lr * get(uh + r), xr = cu * sx[r];
-#pragma unroll 4
-    for (int k = lane; k < d; k += 64) {
-      const float hk = sh[k], gk = 2.f * (shh[k] - sy[k]);
-      u[k] = fmaf(ur, hk, u[k]);
-      x[k] = fmaf(xr, hk, x[k]);
-      q[k] = fmaf(c4 * hr, hk, q[k] - lr * (hr * gk + gr * hk));
+    // eight columns per lane of the three rows loaded before any of them is stored (the
+    // rows may not overlap, but the compiler cannot know that)
+    constexpr int kCols = 8;
+    for (int k0 = lane; k0 < d; k0 += 64 * kCols) {
+      float uv[kCols], xv2[kCols], qv[kCols];
+#pragma unroll
+      for (int e = 0; e < kCols; ++e) {
+        const int k = min(k0 + 64 * e, d - 1);
+        uv[e] = u[k];
+        xv2[e] = x[k];
+        qv[e] = q[k];
+      }
+#pragma unroll
+      for (int e = 0; e < kCols; ++e) {
+        const int k = k0 + 64 * e;
+        if (k < d) {
+          const float hk = sh[k], gk = 2.f * (shh[k] - sy[k]);
+          u[k] = fmaf(ur, hk, uv[e]);
+          x[k] = fmaf(xr, hk, xv2[e]);
+          q[k] = fmaf(c4 * hr, hk, qv[e] - lr * (hr * gk + gr * hk));
+        }
+      }
     }
   }
   // step 7: V_c += 2 eta (sum of t over the slots of row c) P, P = U_new^{-T} h =
