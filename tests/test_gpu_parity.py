@@ -109,6 +109,7 @@ def test_duplicates_and_empty_slots(loss, D, K):
 @pytest.mark.parametrize("loss,D,d,m,K", [
     (LOSS_SQUARED, 8, 40, 128, 8), (LOSS_SQUARED, 3, 37, 96, 3), (LOSS_SQUARED, 48, 24, 120, 48),
     (LOSS_SPHERICAL_SOFTMAX, 3, 40, 128, 1), (LOSS_TAYLOR_SOFTMAX, 3, 40, 128, 1),
+    (LOSS_SQUARED, 8, 32, 1024, 8),  # m K = 8192, the largest: 32 chunks a row
 ])
 def test_frequent_rows_summed_in_chunks(loss, D, d, m, K):
     # A V row with more than max(32, K) slots is summed by several workgroups (chunks of
