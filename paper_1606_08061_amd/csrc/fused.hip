@@ -408,14 +408,16 @@ __device__ __forceinline__ int section_tile(int w, int T) {
 // The same with each product split over the XCDs on its own: XCD x owns a contiguous
 // eighth of every product's tiles, so that products of different k lengths spread
 // evenly over the chip.  section_by_op: the section's workgroups.
-__host__ __device__ __forceinline__ int section_by_op(const OpBatch &ob) {
+template <class B>  // OpBatch or OpHdr
+__host__ __device__ __forceinline__ int section_by_op(const B &ob) {
   int n = 0;
   for (int q = 0; q < kMaxOps; ++q)
     if (q < ob.n_main) n += (ob.count[q] + 7) >> 3;
   return 8 * n;
 }
 
-__device__ __forceinline__ int tile_by_op(const OpBatch &ob, int w) {
+template <class B>
+__device__ __forceinline__ int tile_by_op(const B &ob, int w) {
   const int x = w & 7;
   int s = w >> 3;
 #pragma unroll
@@ -431,14 +433,15 @@ __device__ __forceinline__ int tile_by_op(const OpBatch &ob, int w) {
 
 // Tile `tile` of a batch of Op16 (the descriptor whose range holds it); alt
 // descriptors replace theirs when the polynomial is not certified.
-__device__ __forceinline__ void run_op(const OpBatch &ob, int tile, const TileCtx &x, bool cert) {
+__device__ __forceinline__ void run_op(const OpHdr &hd, const Op16 *ops, int tile, const TileCtx &x,
+                                       bool cert) {
   int di = 0;
 #pragma unroll
   for (int q = 1; q < kMaxOps; ++q)
-    if (q < ob.n_main && tile >= ob.begin[q]) di = q;
-  const Op16 *g = &ob.op[di];
-  const int local = tile - ob.begin[di];
-  if (!cert && g->alt >= 0) g = &ob.op[g->alt];
+    if (q < hd.n_main && tile >= hd.begin[q]) di = q;
+  const Op16 *g = &ops[di];
+  const int local = tile - hd.begin[di];
+  if (!cert && g->alt >= 0) g = &ops[g->alt];
   op16_tile(*g, local, x);
 }
 
@@ -446,24 +449,23 @@ __device__ __forceinline__ void run_op(const OpBatch &ob, int tile, const TileCt
 // Launch 1: contractions, N, prefetch of the target rows.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256, 4) void step_contract_kernel(
-    const StepPlan *__restrict__ pl, const float *H, float lr, const int *__restrict__ idx,
+    const StepPlan *__restrict__ pl, const OpHdr hd, const GemmHdr gh, const float *H, float lr,
+    const int *__restrict__ idx,
     const float *__restrict__ val, int K, const float *__restrict__ V, int64_t ldv, int64_t D,
     int d, int m, float *__restrict__ tsum) {
-  const OpBatch &ob = pl->ob[0];
   int w = blockIdx.x;
-  const int sec = (ob.total + 7) & ~7;
+  const int sec = (hd.total + 7) & ~7;
   if (w < sec) {
-    const int tile = section_tile(w, ob.total);
+    const int tile = section_tile(w, hd.total);
     if (tile < 0) return;
     const TileCtx x{H, nullptr, lr, nullptr, nullptr};
-    run_op(ob, tile, x, true);
+    run_op(hd, pl->ob[0].op, tile, x, true);
     return;
   }
   w -= sec;
-  const GemmBatch &gb = pl->gb_contract;
-  const int gsec = (gb.total_tiles + 7) & ~7;
+  const int gsec = (gh.total_tiles + 7) & ~7;
   if (w < gsec) {  // the products on 32 x 32 tiles (large shapes)
-    if (w < gb.total_tiles) gemm_body<4, 4>(gb, H, nullptr, lr, nullptr, w);
+    if (w < gh.total_tiles) gemm_body<4, 4>(pl->gb_contract, gh, H, nullptr, lr, nullptr, w);
     return;
   }
   // Prefetch workgroup of example j (XCD j % 8, that of its gather workgroup in
@@ -923,7 +925,7 @@ __device__ __forceinline__ void dq_all(const GatherArgs &ga, float *sdq) {
 
 template <int KPW, int NV>
 __global__ __launch_bounds__(256, 4) void step_gather_kernel(const StepPlan *__restrict__ pl,
-                                                          const float *H, float lr,
+                                                          const OpHdr hd, const float *H, float lr,
                                                           const GatherArgs ga) {
   const int w = blockIdx.x;
   const int gsec = (ga.m + 7) & ~7;
@@ -939,8 +941,7 @@ __global__ __launch_bounds__(256, 4) void step_gather_kernel(const StepPlan *__r
       gather_gen(ga, w);
     return;
   }
-  const OpBatch &ob = pl->ob[1];
-  const int tile = tile_by_op(ob, w - gsec);
+  const int tile = tile_by_op(hd, w - gsec);
   if (tile < 0) return;
   __shared__ __align__(16) float sdq[LST_MAX_M];
   const float *dq = nullptr;
@@ -949,7 +950,7 @@ __global__ __launch_bounds__(256, 4) void step_gather_kernel(const StepPlan *__r
     dq = sdq;
   }
   const TileCtx x{H, nullptr, lr, dq, nullptr};
-  run_op(ob, tile, x, true);
+  run_op(hd, pl->ob[1].op, tile, x, true);
 }
 
 // ---------------------------------------------------------------------------
@@ -1162,25 +1163,24 @@ struct MidArgs {
 // empty or not).
 template <bool BIG>
 __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__restrict__ pl,
+                                                         const OpHdr hd, const GemmHdr gh,
                                                          const float *H, float *gH, float lr,
                                                          const float *dq, const MidArgs ma,
                                                          const CertArgs ca) {
-  const OpBatch &ob = pl->ob[2];
   int w = blockIdx.x;
-  const int sec = section_by_op(ob);
+  const int sec = section_by_op(hd);
   if (w < sec) {
-    const int tile = tile_by_op(ob, w);
+    const int tile = tile_by_op(hd, w);
     if (tile < 0) return;
     const TileCtx x{H, gH, lr, dq, nullptr};
-    run_op(ob, tile, x, true);
+    run_op(hd, pl->ob[2].op, tile, x, true);
     return;
   }
   w -= sec;
   if constexpr (BIG) {
-    const GemmBatch &gb = pl->gb_zgrad;
-    const int gsec = (gb.total_tiles + 7) & ~7;
+    const int gsec = (gh.total_tiles + 7) & ~7;
     if (w < gsec) {  // the products on 32 x 32 tiles (large shapes)
-      if (w < gb.total_tiles) gemm_body<4, 4>(gb, H, gH, lr, nullptr, w);
+      if (w < gh.total_tiles) gemm_body<4, 4>(pl->gb_zgrad, gh, H, gH, lr, nullptr, w);
       return;
     }
     w -= gsec;
@@ -1219,31 +1219,30 @@ __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__re
 // updates and the V scatter.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256, 4) void step_mid_kernel(const StepPlan *__restrict__ pl,
+                                                       const OpHdr hd, const GemmHdr gh,
                                                        const float *H, float *gH, float lr,
                                                        const float *dq,
                                                        const float *__restrict__ coef,
                                                        const int *__restrict__ cert,
                                                        const int *__restrict__ flag, int n,
                                                        const int *__restrict__ idx, int *splan) {
-  const OpBatch &ob = pl->ob[3];
   const int w = blockIdx.x;
-  const int sec = (ob.total + 7) & ~7;
+  const int sec = (hd.total + 7) & ~7;
   if (w < sec) {
-    const int tile = section_tile(w, ob.total);
+    const int tile = section_tile(w, hd.total);
     if (tile < 0) return;
     // the coefficients and the certificate are read where they are used (uniform loads)
     const TileCtx x{H, gH, lr, dq, coef};
-    run_op(ob, tile, x, *cert != 0);
+    run_op(hd, pl->ob[3].op, tile, x, *cert != 0);
     return;
   }
   // The U update (k = m): four k-blocks of 8 per wavefront at m = 128, all loaded
   // before the first product (the launch bound of four workgroups per CU leaves the
   // registers for that).
-  const GemmBatch &gb = pl->gb_mid;
   const int w2 = w - sec;
-  const int gsec = (gb.total_tiles + 7) & ~7;
+  const int gsec = (gh.total_tiles + 7) & ~7;
   if (w2 < gsec) {
-    if (w2 < gb.total_tiles) gemm_body<4, 4>(gb, H, gH, lr, flag, w2);
+    if (w2 < gh.total_tiles) gemm_body<4, 4>(pl->gb_mid, gh, H, gH, lr, flag, w2);
     return;
   }
   // the V scatter's plan for launch 5, 16 slots per workgroup
@@ -1251,7 +1250,8 @@ __global__ __launch_bounds__(256, 4) void step_mid_kernel(const StepPlan *__rest
 }
 
 __global__ __launch_bounds__(256, 5) void step_update_kernel(const StepPlan *__restrict__ pl,
-                                                          const float *H, float *gH, float lr,
+                                                          const GemmHdr gh, const float *H,
+                                                          float *gH, float lr,
                                                           const int *__restrict__ flag, int n,
                                                           int K, int d,
                                                           const int *__restrict__ idx,
@@ -1259,10 +1259,10 @@ __global__ __launch_bounds__(256, 5) void step_update_kernel(const StepPlan *__r
                                                           const float *__restrict__ RX, float *V,
                                                           int64_t ldv, const ScatterChunks ch) {
   // the products first (their workgroups are the long ones), then the scatter
-  const int gsec = (pl->gb_update.total_tiles + 7) & ~7;
+  const int gsec = (gh.total_tiles + 7) & ~7;
   if (blockIdx.x < gsec) {
-    if ((int)blockIdx.x < pl->gb_update.total_tiles)
-      gemm_body<4, 2>(pl->gb_update, H, gH, lr, flag, blockIdx.x);
+    if ((int)blockIdx.x < gh.total_tiles)
+      gemm_body<4, 2>(pl->gb_update, gh, H, gH, lr, flag, blockIdx.x);
     return;
   }
   const int w = blockIdx.x - gsec;
@@ -1541,8 +1541,8 @@ void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, co
   const float *dqp = sb.loss == LST_LOSS_SQUARED ? nullptr : sb.dq;
   switch (which) {
     case 0:
-      LST_LAUNCH(step_contract_kernel, dim3(grid[0]), dim3(256), 0, s, dev, a.H, a.lr, a.idx,
-                 a.val, a.K, sb.V, sb.ldv, sb.D, sb.d, a.m, sb.tsum);
+      LST_LAUNCH(step_contract_kernel, dim3(grid[0]), dim3(256), 0, s, dev, op_hdr(host.ob[0]),
+                 gemm_hdr(host.gb_contract), a.H, a.lr, a.idx, a.val, a.K, sb.V, sb.ldv, sb.D, sb.d, a.m, sb.tsum);
       break;
     case 1: {
       GatherArgs ga{};
@@ -1580,9 +1580,11 @@ void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, co
       ga.flag = sb.flag;
       const int kpw = (a.K + 3) / 4;
       const int d = sb.d;
+      const OpHdr hd1 = op_hdr(host.ob[1]);
 #define LST_GATHER(KPW, NV)                                                                        \
   if (kpw <= KPW && d <= 64 * NV) {                                                                \
-    LST_LAUNCH((step_gather_kernel<KPW, NV>), dim3(grid[1]), dim3(256), 0, s, dev, a.H, a.lr, ga); \
+    LST_LAUNCH((step_gather_kernel<KPW, NV>), dim3(grid[1]), dim3(256), 0, s, dev, hd1, a.H, a.lr, \
+               ga);                                                                                \
     break;                                                                                         \
   }
       LST_GATHER(1, 8)
@@ -1591,23 +1593,24 @@ void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, co
       LST_GATHER(1, 16)
       LST_GATHER(2, 16)
 #undef LST_GATHER
-      LST_LAUNCH((step_gather_kernel<0, 0>), dim3(grid[1]), dim3(256), 0, s, dev, a.H, a.lr, ga);
+      LST_LAUNCH((step_gather_kernel<0, 0>), dim3(grid[1]), dim3(256), 0, s, dev, hd1, a.H, a.lr,
+                 ga);
       break;
     }
     case 2: {
       MidArgs ma{a.m, a.K, sb.srow, sb.sval, sb.scnt, sb.YY, sb.lvec, a.loss, sb.flag};
       CertArgs ca{a.m, sb.bpart, sb.N, dqp, sb.Cwork, sb.R, sb.coef, sb.cert, sb.flag};
       if (host.gb_zgrad.n > 0)
-        LST_LAUNCH(step_zgrad_kernel<true>, dim3(grid[2]), dim3(256), 0, s, dev, a.H, a.gH, a.lr,
-                   dqp, ma, ca);
+        LST_LAUNCH(step_zgrad_kernel<true>, dim3(grid[2]), dim3(256), 0, s, dev,
+                   op_hdr(host.ob[2]), gemm_hdr(host.gb_zgrad), a.H, a.gH, a.lr, dqp, ma, ca);
       else
-        LST_LAUNCH(step_zgrad_kernel<false>, dim3(grid[2]), dim3(256), 0, s, dev, a.H, a.gH, a.lr,
-                   dqp, ma, ca);
+        LST_LAUNCH(step_zgrad_kernel<false>, dim3(grid[2]), dim3(256), 0, s, dev,
+                   op_hdr(host.ob[2]), gemm_hdr(host.gb_zgrad), a.H, a.gH, a.lr, dqp, ma, ca);
       break;
     }
     case 3:
-      LST_LAUNCH(step_mid_kernel, dim3(grid[3]), dim3(256), 0, s, dev, a.H, a.gH, a.lr, dqp,
-                 sb.coef, sb.cert, sb.flag, a.m * a.K, a.idx, sb.splan);
+      LST_LAUNCH(step_mid_kernel, dim3(grid[3]), dim3(256), 0, s, dev, op_hdr(host.ob[3]),
+                 gemm_hdr(host.gb_mid), a.H, a.gH, a.lr, dqp, sb.coef, sb.cert, sb.flag, a.m * a.K, a.idx, sb.splan);
       break;
     default: {
       // rows of more than C slots summed in chunks; the partial sums in P2 and P3, which
@@ -1620,8 +1623,9 @@ void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, co
       ch.plan = sb.splan;
       ch.rcnt = sb.rcnt;
       ch.ticket = sb.ticket;
-      LST_LAUNCH(step_update_kernel, dim3(grid[4]), dim3(256), 0, s, dev, a.H, a.gH, a.lr, sb.flag, a.m * a.K, a.K, sb.d, a.idx, sb.wA, sb.RX, sb.V,
-                 sb.ldv, ch);
+      LST_LAUNCH(step_update_kernel, dim3(grid[4]), dim3(256), 0, s, dev,
+                 gemm_hdr(host.gb_update), a.H, a.gH, a.lr, sb.flag, a.m * a.K, a.K, sb.d, a.idx,
+                 sb.wA, sb.RX, sb.V, sb.ldv, ch);
     }
   }
 }

@@ -26,7 +26,7 @@ namespace {
 // PHASE only names the instantiation, so profilers report each step phase separately.
 template <int PHASE, int NW>
 __global__ __launch_bounds__(64 * NW, 12 / NW) void gemm_kernel(const GemmBatch bt, const int *__restrict__ gate) {
-  gemm_body<NW>(bt, nullptr, nullptr, 1.f, gate, blockIdx.x);
+  gemm_body<NW>(bt, bt, nullptr, nullptr, 1.f, gate, blockIdx.x);
 }
 
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const GemmDesc g, const int *__restrict__ gate) {

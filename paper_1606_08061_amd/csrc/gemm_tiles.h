@@ -177,16 +177,18 @@ __device__ __forceinline__ const float *resolve(const float *p, const float *H, 
   return v == 16 ? H : (v == 32 ? gH : p);
 }
 
-template <int NW, int KS = kStage>
-__device__ __forceinline__ void gemm_body(const GemmBatch &bt, const float *H, float *gH, float lr,
-                                          const int *__restrict__ gate, int wg) {
+// hd: the batch's tile ranges (the batch itself, or a GemmHdr passed by value).
+template <int NW, int KS = kStage, class Hd>
+__device__ __forceinline__ void gemm_body(const GemmBatch &bt, const Hd &hd, const float *H,
+                                          float *gH, float lr, const int *__restrict__ gate,
+                                          int wg) {
   // The gate only suppresses writes, so its load is waited for at the end.
   const int closed = gate ? *gate : 0;
-  const int tile = xcd_tile(wg, bt.total_tiles);
+  const int tile = xcd_tile(wg, hd.total_tiles);
   int di = 0;
 #pragma unroll
   for (int q = 1; q < kMaxBatch; ++q)
-    if (q < bt.n && tile >= bt.d[q].tile_begin) di = q;
+    if (q < hd.n && tile >= hdr_begin(hd, q)) di = q;
   GemmDesc g = bt.d[di];
   g.A = resolve(g.A, H, gH);
   g.B = resolve(g.B, H, gH);

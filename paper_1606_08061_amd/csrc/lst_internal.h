@@ -88,6 +88,21 @@ struct GemmBatch {
   int wide;  // 8 wavefronts per tile (long k) instead of 4
 };
 
+// A GemmBatch's tile ranges, passed to the step's kernels by value (as OpHdr below).
+struct GemmHdr {
+  int n, total_tiles;
+  int tile_begin[kMaxBatch];
+};
+inline GemmHdr gemm_hdr(const GemmBatch &b) {
+  GemmHdr h{};
+  h.n = b.n;
+  h.total_tiles = b.total_tiles;
+  for (int q = 0; q < kMaxBatch; ++q) h.tile_begin[q] = b.d[q].tile_begin;
+  return h;
+}
+__host__ __device__ inline int hdr_begin(const GemmBatch &b, int q) { return b.d[q].tile_begin; }
+__host__ __device__ inline int hdr_begin(const GemmHdr &h, int q) { return h.tile_begin[q]; }
+
 GemmDesc gemm_desc(int M, int N, int K, const float *A, int64_t lda, int tA, const float *B,
                    int64_t ldb, int tB, float *C, int64_t ldc, float alpha = 1.f,
                    const float *Cin = nullptr, int64_t ldcin = 0, float beta = 0.f);
@@ -209,6 +224,23 @@ struct OpBatch {
   int count[kMaxOps];    // op[q]'s tiles
   Op16 op[kMaxOps];
 };
+
+// An OpBatch's tile ranges, passed to the kernels by value so that a workgroup finds its
+// descriptor with one dependent load (of the descriptor itself) instead of two.
+struct OpHdr {
+  int n_main, total;
+  int begin[kMaxOps], count[kMaxOps];
+};
+inline OpHdr op_hdr(const OpBatch &ob) {
+  OpHdr h{};
+  h.n_main = ob.n_main;
+  h.total = ob.total;
+  for (int q = 0; q < kMaxOps; ++q) {
+    h.begin[q] = ob.begin[q];
+    h.count[q] = ob.count[q];
+  }
+  return h;
+}
 
 // The products of one step for one minibatch size m (kept in device memory):
 // ob[l] for launches 1..4 (16 x 16 tiles), gb_mid (the U update, launch 4) and
