@@ -445,9 +445,22 @@ __device__ __forceinline__ void run_op(const OpHdr &hd, const Op16 *ops, int til
   op16_tile(*g, local, x);
 }
 
+// The step's products on 32 x 32 tiles (GT = 32, KS k-blocks of 8 in flight per wave)
+// or on LDS-staged 64 x 64 tiles (GT = 64, large shapes).
+template <int GT, int KS, class Hd>
+__device__ __forceinline__ void step_gemm(const GemmBatch &bt, const Hd &hd, const float *H,
+                                          float *gH, float lr, const int *gate, int w) {
+  if constexpr (GT == 64)
+    gemm_body64(bt, hd, H, gH, lr, gate, w);
+  else
+    gemm_body<4, KS>(bt, hd, H, gH, lr, gate, w);
+}
+
 // ---------------------------------------------------------------------------
-// Launch 1: contractions, N, prefetch of the target rows.
+// Launch 1: contractions, N, prefetch of the target rows.  GT: the tile edge of the
+// products in gb_contract.
 // ---------------------------------------------------------------------------
+template <int GT>
 __global__ __launch_bounds__(256, 4) void step_contract_kernel(
     const StepPlan *__restrict__ pl, const OpHdr hd, const GemmHdr gh, const float *H, float lr,
     const int *__restrict__ idx,
@@ -464,8 +477,8 @@ __global__ __launch_bounds__(256, 4) void step_contract_kernel(
   }
   w -= sec;
   const int gsec = (gh.total_tiles + 7) & ~7;
-  if (w < gsec) {  // the products on 32 x 32 tiles (large shapes)
-    if (w < gh.total_tiles) gemm_body<4, 4>(pl->gb_contract, gh, H, nullptr, lr, nullptr, w);
+  if (w < gsec) {  // the products on 32 x 32 or 64 x 64 tiles (large shapes)
+    if (w < gh.total_tiles) step_gemm<GT, 4>(pl->gb_contract, gh, H, nullptr, lr, nullptr, w);
     return;
   }
   // Prefetch workgroup of example j (XCD j % 8, that of its gather workgroup in
@@ -1157,11 +1170,11 @@ struct MidArgs {
   int *flag;
 };
 
-// BIG: the plan has products on 32 x 32 tiles (a separate instantiation, so that the
-// other shapes keep the smaller kernel: with the 32 x 32 section compiled in, the
-// registers and LDS it takes made the step 5 us slower at m = 128, d = 500, section
-// empty or not).
-template <bool BIG>
+// GT: the tile edge of the products in gb_zgrad, 0 when it is empty (a separate
+// instantiation, so that the other shapes keep the smaller kernel: with the 32 x 32
+// section compiled in, the registers and LDS it takes made the step 5 us slower at
+// m = 128, d = 500, section empty or not).
+template <int GT>
 __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__restrict__ pl,
                                                          const OpHdr hd, const GemmHdr gh,
                                                          const float *H, float *gH, float lr,
@@ -1177,10 +1190,10 @@ __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__re
     return;
   }
   w -= sec;
-  if constexpr (BIG) {
+  if constexpr (GT != 0) {
     const int gsec = (gh.total_tiles + 7) & ~7;
-    if (w < gsec) {  // the products on 32 x 32 tiles (large shapes)
-      if (w < gh.total_tiles) gemm_body<4, 4>(pl->gb_zgrad, gh, H, gH, lr, nullptr, w);
+    if (w < gsec) {  // the products on 32 x 32 or 64 x 64 tiles (large shapes)
+      if (w < gh.total_tiles) step_gemm<GT, 4>(pl->gb_zgrad, gh, H, gH, lr, nullptr, w);
       return;
     }
     w -= gsec;
@@ -1216,8 +1229,9 @@ __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__re
 
 // ---------------------------------------------------------------------------
 // Launch 4: Zq, R X, the U update and the V scatter's plan.  Launch 5: the Q and U^{-T}
-// updates and the V scatter.
+// updates and the V scatter.  GT: the tile edge of gb_mid's and gb_update's products.
 // ---------------------------------------------------------------------------
+template <int GT>
 __global__ __launch_bounds__(256, 4) void step_mid_kernel(const StepPlan *__restrict__ pl,
                                                        const OpHdr hd, const GemmHdr gh,
                                                        const float *H, float *gH, float lr,
@@ -1242,14 +1256,16 @@ __global__ __launch_bounds__(256, 4) void step_mid_kernel(const StepPlan *__rest
   const int w2 = w - sec;
   const int gsec = (gh.total_tiles + 7) & ~7;
   if (w2 < gsec) {
-    if (w2 < gh.total_tiles) gemm_body<4, 4>(pl->gb_mid, gh, H, gH, lr, flag, w2);
+    if (w2 < gh.total_tiles) step_gemm<GT, 4>(pl->gb_mid, gh, H, gH, lr, flag, w2);
     return;
   }
   // the V scatter's plan for launch 5, 16 slots per workgroup
   if ((w2 - gsec) * 16 < n) scatter_plan(w2 - gsec, n, idx, splan);
 }
 
-__global__ __launch_bounds__(256, 5) void step_update_kernel(const StepPlan *__restrict__ pl,
+// (five workgroups per CU on 32 x 32 tiles; four with the 64 x 64 tiles' LDS)
+template <int GT>
+__global__ __launch_bounds__(256, GT == 64 ? 4 : 5) void step_update_kernel(const StepPlan *__restrict__ pl,
                                                           const GemmHdr gh, const float *H,
                                                           float *gH, float lr,
                                                           const int *__restrict__ flag, int n,
@@ -1262,7 +1278,7 @@ __global__ __launch_bounds__(256, 5) void step_update_kernel(const StepPlan *__r
   const int gsec = (gh.total_tiles + 7) & ~7;
   if (blockIdx.x < gsec) {
     if ((int)blockIdx.x < gh.total_tiles)
-      gemm_body<4, 2>(pl->gb_update, gh, H, gH, lr, flag, blockIdx.x);
+      step_gemm<GT, 2>(pl->gb_update, gh, H, gH, lr, flag, blockIdx.x);
     return;
   }
   const int w = blockIdx.x - gsec;
@@ -1305,6 +1321,21 @@ constexpr int kContract32MinTiles = 128;  // 32 x 32 tiles of one m x d product
 // per step at m = 256, d = 512 and at m = 512, d = 256 to 1024).
 bool contract_on_32(int m, int d) {
   return ((m + 31) / 32) * ((d + 31) / 32) >= kContract32MinTiles;
+}
+
+// The tile edge of the large-shape batches: LDS-staged 64 x 64 tiles where they were
+// measured faster than 32 x 32 tiles (m = 512: launch 3 at d = 256 to 1024, launches 1,
+// 4 and 5 at d = 1024; slower at m = 256, d = 512 and in launches 1, 4 and 5 at
+// d <= 512, where a product has too few 64 x 64 tiles to fill the chip).
+constexpr int kT64Contract = 128, kT64Zgrad = 64, kT64Update = 256, kT64MinK = 256;
+int tiles64(int M, int N) { return ((M + 63) / 64) * ((N + 63) / 64); }
+// launch 1 (m x d outputs, k = d)
+int tile_contract(int m, int d) { return tiles64(m, d) >= kT64Contract ? 64 : 32; }
+// launch 3 (m x m and m x d outputs, k = d or m)
+int tile_zgrad(int m, int d) { return tiles64(m, m) >= kT64Zgrad ? 64 : 32; }
+// launches 4 and 5 (d x d outputs, k = m)
+int tile_update(int m, int d) {
+  return tiles64(d, d) >= kT64Update && m >= kT64MinK ? 64 : 32;
 }
 
 void finalize(OpBatch &ob, int n_main) {
@@ -1373,7 +1404,7 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
     if (tay)  // [s h~] = H [w_bar omega] (eq. svec, gen-htilde)
       ob.op[ob.n++] = op(m, 2, d, H, d, 0, sb.WO, ldd, 0, sb.SW, 2);
     finalize(ob, ob.n);
-    if (gb.n) gemm_prepare(gb);
+    if (gb.n) gemm_prepare(gb, tile_contract(m, d));
   }
   // Launch 2: M^ = H H^^T; E^2 = 4 eta^2 S N D N S (|row| partials -> bpart);
   // W1 = E Xs = 2 eta S N D X
@@ -1455,7 +1486,7 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
       ++ob.n;
     }
     finalize(ob, ob.n);
-    if (gb.n) gemm_prepare(gb);
+    if (gb.n) gemm_prepare(gb, tile_zgrad(m, d));
   }
   // Launch 4: Zq = (eta^2/2) M H - eta grad_H (M assembled as it is loaded);
   // R X = 2 eta S (c0 Xs + c1 W1 + c2 P2 + c3 P3 + E^4 (c4 Xs + c5 W1 + c6 P2 + c7 P3)),
@@ -1505,7 +1536,7 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
     // U <- U - (2 eta D H~)^T H
     gb.d[0] = gemm_desc(d, d, m, sb.Atil, d, 1, H, d, 1, sb.U, ldd, -1.f, sb.U, ldd, 1.f);
     gb.n = 1;
-    gemm_prepare(gb);
+    gemm_prepare(gb, tile_update(m, d));
   }
   // Launch 5: Q <- Q + H^T Zq + Zq^T H; U^{-T} <- U^{-T} + (R X)^T H; omega, w_bar
   {
@@ -1521,7 +1552,7 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
     gb.n = 2;
     if (tay)  // [w_bar; omega] -= [c_w; c_o] H (eta folded into the coefficients)
       gb.d[gb.n++] = gemm_desc(2, d, m, sb.cwo, m, 0, H, d, 1, sb.WO, ldd, -1.f, sb.WO, ldd, 1.f);
-    gemm_prepare(gb);
+    gemm_prepare(gb, tile_update(m, d));
   }
 }
 
@@ -1541,8 +1572,15 @@ void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, co
   const float *dqp = sb.loss == LST_LOSS_SQUARED ? nullptr : sb.dq;
   switch (which) {
     case 0:
-      LST_LAUNCH(step_contract_kernel, dim3(grid[0]), dim3(256), 0, s, dev, op_hdr(host.ob[0]),
-                 gemm_hdr(host.gb_contract), a.H, a.lr, a.idx, a.val, a.K, sb.V, sb.ldv, sb.D, sb.d, a.m, sb.tsum);
+#define LST_CONTRACT(GT)                                                                          \
+  LST_LAUNCH(step_contract_kernel<GT>, dim3(grid[0]), dim3(256), 0, s, dev, op_hdr(host.ob[0]),    \
+             gemm_hdr(host.gb_contract), a.H, a.lr, a.idx, a.val, a.K, sb.V, sb.ldv, sb.D, sb.d, a.m, \
+             sb.tsum)
+      if (host.gb_contract.tile == 64)
+        LST_CONTRACT(64);
+      else
+        LST_CONTRACT(32);
+#undef LST_CONTRACT
       break;
     case 1: {
       GatherArgs ga{};
@@ -1600,17 +1638,28 @@ void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, co
     case 2: {
       MidArgs ma{a.m, a.K, sb.srow, sb.sval, sb.scnt, sb.YY, sb.lvec, a.loss, sb.flag};
       CertArgs ca{a.m, sb.bpart, sb.N, dqp, sb.Cwork, sb.R, sb.coef, sb.cert, sb.flag};
-      if (host.gb_zgrad.n > 0)
-        LST_LAUNCH(step_zgrad_kernel<true>, dim3(grid[2]), dim3(256), 0, s, dev,
-                   op_hdr(host.ob[2]), gemm_hdr(host.gb_zgrad), a.H, a.gH, a.lr, dqp, ma, ca);
+#define LST_ZGRAD(GT)                                                                          \
+  LST_LAUNCH(step_zgrad_kernel<GT>, dim3(grid[2]), dim3(256), 0, s, dev, op_hdr(host.ob[2]), \
+             gemm_hdr(host.gb_zgrad), a.H, a.gH, a.lr, dqp, ma, ca)
+      if (host.gb_zgrad.n == 0)
+        LST_ZGRAD(0);
+      else if (host.gb_zgrad.tile == 64)
+        LST_ZGRAD(64);
       else
-        LST_LAUNCH(step_zgrad_kernel<false>, dim3(grid[2]), dim3(256), 0, s, dev,
-                   op_hdr(host.ob[2]), gemm_hdr(host.gb_zgrad), a.H, a.gH, a.lr, dqp, ma, ca);
+        LST_ZGRAD(32);
+#undef LST_ZGRAD
       break;
     }
     case 3:
-      LST_LAUNCH(step_mid_kernel, dim3(grid[3]), dim3(256), 0, s, dev, op_hdr(host.ob[3]),
-                 gemm_hdr(host.gb_mid), a.H, a.gH, a.lr, dqp, sb.coef, sb.cert, sb.flag, a.m * a.K, a.idx, sb.splan);
+#define LST_MID(GT)                                                                             \
+  LST_LAUNCH(step_mid_kernel<GT>, dim3(grid[3]), dim3(256), 0, s, dev, op_hdr(host.ob[3]),       \
+             gemm_hdr(host.gb_mid), a.H, a.gH, a.lr, dqp, sb.coef, sb.cert, sb.flag, a.m * a.K, \
+             a.idx, sb.splan)
+      if (host.gb_mid.tile == 64)
+        LST_MID(64);
+      else
+        LST_MID(32);
+#undef LST_MID
       break;
     default: {
       // rows of more than C slots summed in chunks; the partial sums in P2 and P3, which
@@ -1623,9 +1672,15 @@ void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, co
       ch.plan = sb.splan;
       ch.rcnt = sb.rcnt;
       ch.ticket = sb.ticket;
-      LST_LAUNCH(step_update_kernel, dim3(grid[4]), dim3(256), 0, s, dev,
-                 gemm_hdr(host.gb_update), a.H, a.gH, a.lr, sb.flag, a.m * a.K, a.K, sb.d, a.idx,
-                 sb.wA, sb.RX, sb.V, sb.ldv, ch);
+#define LST_UPDATE(GT)                                                                          \
+  LST_LAUNCH(step_update_kernel<GT>, dim3(grid[4]), dim3(256), 0, s, dev,                        \
+             gemm_hdr(host.gb_update), a.H, a.gH, a.lr, sb.flag, a.m * a.K, a.K, sb.d, a.idx, sb.wA, \
+             sb.RX, sb.V, sb.ldv, ch)
+      if (host.gb_update.tile == 64)
+        LST_UPDATE(64);
+      else
+        LST_UPDATE(32);
+#undef LST_UPDATE
     }
   }
 }

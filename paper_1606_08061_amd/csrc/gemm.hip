@@ -293,10 +293,10 @@ size_t gemm_plan_split(GemmDesc &g, int target_wgs, float *partial) {
   return (size_t)splits * g.M * g.N;
 }
 
-int gemm_prepare(GemmBatch &b) {
+int gemm_prepare(GemmBatch &b, int ts) {
   int total = 0;
   int kmax = 0;
-  const int ts = 32;
+  b.tile = ts;
   for (int q = 0; q < b.n; ++q) {
     GemmDesc &g = b.d[q];
     g.tiles_m = (g.M + ts - 1) / ts;

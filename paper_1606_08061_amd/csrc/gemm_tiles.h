@@ -270,6 +270,231 @@ __device__ __forceinline__ void gemm_body(const GemmBatch &bt, const Hd &hd, con
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// 64 x 64 tiles staged through LDS (the step's products at large shapes).
+//
+// The workgroup's 256 threads load each 16-wide k step of the two 64-index operand
+// panels once: every row's 64 bytes by 4 consecutive lanes when k is contiguous, every
+// k row's 256 bytes by 16 lanes when the index is.  The panels are stored k-major in
+// LDS ([k][index], padded rows) and wave (wr, wc) runs the 32 x 32 quadrant (wr, wc) of
+// the tile over the whole k range from there, 8 MFMAs a k step into two accumulators
+// (even and odd k pairs).  Against the 32 x 32 tiles above, whose waves read 32-byte
+// pieces of each row straight from memory, an operand element crosses the L2 once per
+// 64 outputs instead of once per 32.
+// LDS is double buffered; the loads of the next kT64P steps are in flight in registers
+// while a step runs on the matrix cores.
+// ---------------------------------------------------------------------------
+constexpr int kT64 = 64, kT64K = 16, kT64Ld = kT64 + 4;
+// per thread and k step: kT64U 16-byte pieces of each operand; k contiguous: kT64Lpr
+// lanes a row, kT64Rpu rows a piece
+constexpr int kT64U = kT64K / 16, kT64Lpr = kT64K / 4, kT64Rpu = 256 / kT64Lpr;
+constexpr int kT64P = 2;  // k steps in flight in registers (even: LDS buffer = step % 2)
+static_assert(kT64P % 2 == 0, "the LDS buffer of a step is its register slot's parity");
+
+// One operand of one k segment: element (index i, k) at p[i * si + k * sk]; n indices,
+// k in [0, kend).
+struct Panel {
+  const float *p;
+  int64_t ld;
+  int n, kend;
+};
+
+// Load modes: KCV: k contiguous, 16-byte loads (aligned p, ld and kend multiples of 4);
+// IXV: index contiguous, 16-byte loads (aligned p, ld and n multiples of 4); GEN: either
+// layout (kc), scalar loads.
+enum : int { KCV = 0, IXV = 1, GEN = 2 };
+
+template <int MODE>
+__device__ __forceinline__ void p64_load(const Panel &q, bool kc, int idx0, int k0,
+                                         float4 (&v)[kT64U]) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int u = 0; u < kT64U; ++u) {
+    if constexpr (MODE == IXV) {  // thread t: k row t / 16 + 16 u, indices 4 (t % 16) ..
+      const int k = k0 + (t >> 4) + 16 * u;
+      const float *row = q.p + (int64_t)min(k, q.kend - 1) * q.ld;
+      const float4 x = *reinterpret_cast<const float4 *>(row + min(idx0 + (t & 15) * 4, q.n - 4));
+      v[u] = k < q.kend ? x : make_float4(0.f, 0.f, 0.f, 0.f);
+    } else {  // thread t: index t / kT64Lpr + kT64Rpu u, k 4 (t % kT64Lpr) ..
+      const int i = min(idx0 + t / kT64Lpr + kT64Rpu * u, q.n - 1);
+      const int k = k0 + (t % kT64Lpr) * 4;
+      if constexpr (MODE == KCV) {
+        const float4 x =
+            *reinterpret_cast<const float4 *>(q.p + (int64_t)i * q.ld + min(k, q.kend - 4));
+        v[u] = k < q.kend ? x : make_float4(0.f, 0.f, 0.f, 0.f);
+      } else {
+        const int64_t si = kc ? q.ld : 1, sk = kc ? 1 : q.ld;
+        float e[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const float x = q.p[(int64_t)i * si + (int64_t)min(k + s, q.kend - 1) * sk];
+          e[s] = k + s < q.kend ? x : 0.f;
+        }
+        v[u] = make_float4(e[0], e[1], e[2], e[3]);
+      }
+    }
+  }
+}
+
+template <int MODE>
+__device__ __forceinline__ void p64_store(float (*lds)[kT64Ld], const float4 (&v)[kT64U]) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int u = 0; u < kT64U; ++u) {
+    if constexpr (MODE == IXV) {
+      *reinterpret_cast<float4 *>(&lds[(t >> 4) + 16 * u][(t & 15) * 4]) = v[u];
+    } else {
+      const int i = t / kT64Lpr + kT64Rpu * u, k = (t % kT64Lpr) * 4;
+      lds[k][i] = v[u].x;
+      lds[k + 1][i] = v[u].y;
+      lds[k + 2][i] = v[u].z;
+      lds[k + 3][i] = v[u].w;
+    }
+  }
+}
+
+__device__ __forceinline__ void p64_mfma(float (*As)[kT64Ld], float (*Bs)[kT64Ld],
+                                         floatx16 (&acc)[2], int ai, int bj, int lh) {
+#pragma unroll
+  for (int kk = 0; kk < kT64K; kk += 2) {
+    const float a = As[kk + lh][ai];
+    const float b = Bs[kk + lh][bj];
+    acc[(kk >> 1) & 1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, acc[(kk >> 1) & 1], 0, 0, 0);
+  }
+}
+
+// k steps 0 .. ns1 - 1 run over segment 0 (pa0, pb0), the rest over segment 1.
+template <int AM, int BM>
+__device__ __forceinline__ void k64(const Panel &pa0, const Panel &pb0, const Panel &pa1,
+                                    const Panel &pb1, bool akc, bool bkc, int ns1, int ns, int i0,
+                                    int j0, float (*As)[kT64K][kT64Ld], float (*Bs)[kT64K][kT64Ld],
+                                    floatx16 (&acc)[2], int ai, int bj, int lh) {
+  auto load = [&](int st, float4(&ra)[kT64U], float4(&rb)[kT64U]) {
+    const bool s1 = st >= ns1;
+    const int k0 = (s1 ? st - ns1 : st) * kT64K;
+    p64_load<AM>(s1 ? pa1 : pa0, akc, i0, k0, ra);
+    p64_load<BM>(s1 ? pb1 : pb0, bkc, j0, k0, rb);
+  };
+  constexpr int AS = AM == IXV ? IXV : KCV, BS = BM == IXV ? IXV : KCV;  // LDS store layout
+  // Register slot u % kT64P holds step u from its load until its store to LDS buffer
+  // u % 2, one step before its products; the slot then takes step u + kT64P.
+  float4 ra[kT64P][kT64U], rb[kT64P][kT64U];
+#pragma unroll
+  for (int u = 0; u < kT64P; ++u)
+    if (u < ns) load(u, ra[u], rb[u]);
+  if (ns > 0) {
+    p64_store<AS>(As[0], ra[0]);
+    p64_store<BS>(Bs[0], rb[0]);
+  }
+  __syncthreads();
+  for (int st = 0; st < ns; st += kT64P) {
+#pragma unroll
+    for (int u = 0; u < kT64P; ++u) {
+      const int s = st + u;
+      if (s < ns) {
+        if (s + kT64P < ns) load(s + kT64P, ra[u], rb[u]);
+        p64_mfma(As[u & 1], Bs[u & 1], acc, ai, bj, lh);
+        if (s + 1 < ns) {
+          p64_store<AS>(As[(u + 1) & 1], ra[(u + 1) % kT64P]);
+          p64_store<BS>(Bs[(u + 1) & 1], rb[(u + 1) % kT64P]);
+        }
+        __syncthreads();
+      }
+    }
+  }
+}
+
+__device__ __forceinline__ bool p64_vec(const float *p, int64_t ld, int ext) {
+  return ((reinterpret_cast<uintptr_t>(p) & 15) == 0) && ((ld & 3) == 0) && ((ext & 3) == 0) &&
+         ext >= 4;
+}
+
+// A batch on 64 x 64 tiles (GemmBatch::tile == 64): C = alpha opA opB + beta C_in, with
+// the second k segment (A2, B2, K2) when K2 > 0.  No split k and no fused epilogue
+// (the host only plans such batches).  Tiles of one product run column by column, so
+// that the tiles one XCD takes share B's panels.
+template <class Hd>
+__device__ __forceinline__ void gemm_body64(const GemmBatch &bt, const Hd &hd, const float *H,
+                                            float *gH, float lr, const int *__restrict__ gate,
+                                            int wg) {
+  const int closed = gate ? *gate : 0;
+  const int tile = xcd_tile(wg, hd.total_tiles);
+  int di = 0;
+#pragma unroll
+  for (int q = 1; q < kMaxBatch; ++q)
+    if (q < hd.n && tile >= hdr_begin(hd, q)) di = q;
+  GemmDesc g = bt.d[di];
+  g.A = resolve(g.A, H, gH);
+  g.B = resolve(g.B, H, gH);
+  g.A2 = resolve(g.A2, H, gH);
+  g.B2 = resolve(g.B2, H, gH);
+  g.Cin = resolve(g.Cin, H, gH);
+  if (g.lr_scaled) {
+    g.alpha *= lr * lr;
+    g.beta *= lr;
+  }
+  const int local = tile - g.tile_begin;
+  const int tn = local / g.tiles_m, tm = local - tn * g.tiles_m;
+  const int i0 = tm * kT64, j0 = tn * kT64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int li = lane & 31, lh = lane >> 5;
+  const int ai = 32 * (wave >> 1) + li, bj = 32 * (wave & 1) + li;
+
+  // C_in before the k loop (its latency overlaps it); lane (li, lh) of the wave holds
+  // rows 8 (r / 4) + 4 lh + r % 4 of the quadrant, column li.
+  const int ib = i0 + 32 * (wave >> 1) + 4 * lh;
+  const int j = j0 + bj;
+  float cin[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int i = min(ib + 8 * (r >> 2) + (r & 3), g.M - 1);
+    cin[r] = g.Cin ? g.Cin[(int64_t)i * g.ldcin + min(j, g.N - 1)] : 0.f;
+  }
+
+  const bool akc = g.tA == 0, bkc = g.tB == 0;
+  const Panel pa0{g.A, g.lda, g.M, g.K}, pb0{g.B, g.ldb, g.N, g.K};
+  const Panel pa1{g.K2 > 0 ? g.A2 : g.A, g.K2 > 0 ? g.lda2 : g.lda, g.M, g.K2};
+  const Panel pb1{g.K2 > 0 ? g.B2 : g.B, g.K2 > 0 ? g.ldb2 : g.ldb, g.N, g.K2};
+  const int ns1 = (g.K + kT64K - 1) / kT64K;
+  const int ns = ns1 + (g.K2 + kT64K - 1) / kT64K;
+  auto vec = [&](const Panel &p0, const Panel &p1, bool kc) {
+    const int e0 = kc ? p0.kend : p0.n, e1 = kc ? p1.kend : p1.n;
+    return p64_vec(p0.p, p0.ld, e0) && (g.K2 == 0 || p64_vec(p1.p, p1.ld, e1));
+  };
+  const bool av = vec(pa0, pa1, akc), bv = vec(pb0, pb1, bkc);
+
+  floatx16 acc[2];
+#pragma unroll
+  for (int x = 0; x < 2; ++x)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[x][r] = 0.f;
+  // one LDS allocation for every load mode (the k loop's instantiations share it)
+  __shared__ float As[2][kT64K][kT64Ld];
+  __shared__ float Bs[2][kT64K][kT64Ld];
+#define LST_K64(AM, BM) \
+  k64<AM, BM>(pa0, pb0, pa1, pb1, akc, bkc, ns1, ns, i0, j0, As, Bs, acc, ai, bj, lh)
+  if (av && bv) {
+    if (akc && bkc)
+      LST_K64(KCV, KCV);
+    else if (akc)
+      LST_K64(KCV, IXV);
+    else if (bkc)
+      LST_K64(IXV, KCV);
+    else
+      LST_K64(IXV, IXV);
+  } else {
+    LST_K64(GEN, GEN);
+  }
+#undef LST_K64
+  if (closed || j >= g.N) return;  // after the k loop's last barrier
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int i = ib + 8 * (r >> 2) + (r & 3);
+    if (i < g.M) g.C[(int64_t)i * g.ldc + j] = g.alpha * (acc[0][r] + acc[1][r]) + g.beta * cin[r];
+  }
+}
+
 }  // namespace
 
 }  // namespace lst

@@ -86,6 +86,8 @@ struct GemmBatch {
   int n;
   int total_tiles;
   int wide;  // 8 wavefronts per tile (long k) instead of 4
+  int tile;  // output tile edge: 32 (the batched launches, the step's default) or 64 (the
+             // step's LDS-staged tiles at large shapes)
 };
 
 // A GemmBatch's tile ranges, passed to the step's kernels by value (as OpHdr below).
@@ -122,7 +124,7 @@ hipError_t gemm_launch(GemmBatch &b, const int *gate, hipStream_t s, int phase =
 
 // Two-part form: gemm_prepare fills the tile bookkeeping (returns the tile
 // count); gemm_enqueue launches without checking for errors.
-int gemm_prepare(GemmBatch &b);
+int gemm_prepare(GemmBatch &b, int tile = 32);
 void gemm_enqueue(const GemmBatch &b, const int *gate, hipStream_t s, int phase);
 
 // Large single products on 128 x 128 tiles (the naive path).  gemm_big_ok: the

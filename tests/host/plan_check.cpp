@@ -157,7 +157,22 @@ void check_gemm(const Space &sp, const GemmBatch &gb, const char *tag) {
     sp.in(w, g.C, (int64_t)(g.M - 1) * g.ldc + (g.N - 1));
     if (g.Cin) sp.in(w, g.Cin, (int64_t)(g.M - 1) * g.ldcin + (g.N - 1));
     CHECK(g.splits == 1, "%s: split descriptors in a step plan", w);
+    // the tile bookkeeping the kernels decode (32 x 32 tiles, or the 64 x 64 tiles,
+    // which have no fused epilogue)
+    CHECK(gb.tile == 32 || gb.tile == 64, "%s: tile edge %d", w, gb.tile);
+    CHECK(g.tiles_m == (g.M + gb.tile - 1) / gb.tile && g.tiles_n == (g.N + gb.tile - 1) / gb.tile,
+          "%s: tile counts", w);
+    CHECK(gb.tile == 32 || (g.epi == 0 && g.colsq == nullptr), "%s: epilogue on 64 x 64 tiles", w);
   }
+  int total = 0;
+  for (int i = 0; i < gb.n; ++i) {
+    const GemmDesc &g = gb.d[i];
+    const int t = (g.M > 0 && g.N > 0) ? g.tiles_m * g.tiles_n : 0;
+    CHECK(t == 0 || g.tile_begin == total, "%s desc %d: tile_begin %d, expected %d", tag, i,
+          g.tile_begin, total);
+    total += t;
+  }
+  CHECK(gb.n == 0 || total == gb.total_tiles, "%s: total %d, tiles %d", tag, gb.total_tiles, total);
 }
 
 void plans() {

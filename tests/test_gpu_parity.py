@@ -175,6 +175,24 @@ def test_sweep_minibatch_m512(loss, d):
     c.close()
 
 
+@pytest.mark.parametrize("loss,d,m", [(LOSS_SQUARED, 514, 258), (LOSS_SPHERICAL_SOFTMAX, 516, 300),
+                                      (LOSS_TAYLOR_SOFTMAX, 514, 258)])
+def test_large_ragged_shapes_on_64_tiles(loss, d, m):
+    # shapes large enough for the LDS-staged 64 x 64 tiles in every launch, with ragged
+    # tile edges; d = 514 and m = 258 are no multiples of 4 (the scalar operand loads)
+    K = 3 if loss == LOSS_SQUARED else 1
+    w = Workload("t", loss, 20000, d, m, K,
+                 value_dist="normal" if loss == LOSS_SQUARED else "ones")
+    c = Compare(w, seed=d + m)
+    st, l, g, ref = c.step()
+    _check_step(st, l, g, ref)
+    assert rel(c.W_gpu(), ref.W_new) <= TOL1
+    st, l, g, ref = c.step()
+    _check_step(st, l, g, ref, TOL100)
+    assert rel(c.W_gpu(), c.W) <= TOL100
+    c.close()
+
+
 def _poly_bound(H, dq, lr):
     """||E^2||_inf^(1/2) of E = 2 lr S H H^T S (S = diag(dq)^(1/2)), in fp64: the bound on the
     spectral radius the step's certificate takes."""
