@@ -476,9 +476,10 @@ __global__ __launch_bounds__(256, 4) void step_contract_kernel(
     return;
   }
   w -= sec;
-  const int gsec = (gh.total_tiles + 7) & ~7;
+  const int gsec = gemm_section(gh, GT);
   if (w < gsec) {  // the products on 32 x 32 or 64 x 64 tiles (large shapes)
-    if (w < gh.total_tiles) step_gemm<GT, 4>(pl->gb_contract, gh, H, nullptr, lr, nullptr, w);
+    if (GT == 64 || w < gh.total_tiles)
+      step_gemm<GT, 4>(pl->gb_contract, gh, H, nullptr, lr, nullptr, w);
     return;
   }
   // Prefetch workgroup of example j (XCD j % 8, that of its gather workgroup in
@@ -1191,9 +1192,10 @@ __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__re
   }
   w -= sec;
   if constexpr (GT != 0) {
-    const int gsec = (gh.total_tiles + 7) & ~7;
+    const int gsec = gemm_section(gh, GT);
     if (w < gsec) {  // the products on 32 x 32 or 64 x 64 tiles (large shapes)
-      if (w < gh.total_tiles) step_gemm<GT, 4>(pl->gb_zgrad, gh, H, gH, lr, nullptr, w);
+      if (GT == 64 || w < gh.total_tiles)
+        step_gemm<GT, 4>(pl->gb_zgrad, gh, H, gH, lr, nullptr, w);
       return;
     }
     w -= gsec;
@@ -1254,9 +1256,9 @@ __global__ __launch_bounds__(256, 4) void step_mid_kernel(const StepPlan *__rest
   // before the first product (the launch bound of four workgroups per CU leaves the
   // registers for that).
   const int w2 = w - sec;
-  const int gsec = (gh.total_tiles + 7) & ~7;
+  const int gsec = gemm_section(gh, GT);
   if (w2 < gsec) {
-    if (w2 < gh.total_tiles) step_gemm<GT, 4>(pl->gb_mid, gh, H, gH, lr, flag, w2);
+    if (GT == 64 || w2 < gh.total_tiles) step_gemm<GT, 4>(pl->gb_mid, gh, H, gH, lr, flag, w2);
     return;
   }
   // the V scatter's plan for launch 5, 16 slots per workgroup
@@ -1275,9 +1277,9 @@ __global__ __launch_bounds__(256, GT == 64 ? 4 : 5) void step_update_kernel(cons
                                                           const float *__restrict__ RX, float *V,
                                                           int64_t ldv, const ScatterChunks ch) {
   // the products first (their workgroups are the long ones), then the scatter
-  const int gsec = (gh.total_tiles + 7) & ~7;
-  if (blockIdx.x < gsec) {
-    if ((int)blockIdx.x < gh.total_tiles)
+  const int gsec = gemm_section(gh, GT);
+  if ((int)blockIdx.x < gsec) {
+    if (GT == 64 || (int)blockIdx.x < gh.total_tiles)
       step_gemm<GT, 2>(pl->gb_update, gh, H, gH, lr, flag, blockIdx.x);
     return;
   }
@@ -1331,7 +1333,8 @@ constexpr int kT64Contract = 128, kT64Zgrad = 64, kT64Update = 256, kT64MinK = 2
 int tiles64(int M, int N) { return ((M + 63) / 64) * ((N + 63) / 64); }
 // launch 1 (m x d outputs, k = d)
 int tile_contract(int m, int d) { return tiles64(m, d) >= kT64Contract ? 64 : 32; }
-// launch 3 (m x m and m x d outputs, k = d or m)
+// launch 3 (m x m and m x d outputs, k = d or m); on 64 x 64 tiles Z^ joins the batch
+// with its grad_H epilogue (d = 1024: the launch 76 -> 50 us)
 int tile_zgrad(int m, int d) { return tiles64(m, m) >= kT64Zgrad ? 64 : 32; }
 // launches 4 and 5 (d x d outputs, k = m)
 int tile_update(int m, int d) {
@@ -1464,9 +1467,22 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
     // 32 x 32 tiles (as in launch 1)
     GemmBatch &gb = pl.gb_zgrad;
     const bool big = contract_on_32(m, d);
+    const int tz = tile_zgrad(m, d);
     ob.n = 0;
     gb.n = 0;
-    ob.op[ob.n++] = z;
+    if (big && tz == 64 && !tay) {
+      // Z^ itself is not stored: its grad_H epilogue writes 2 D H^ + Z^
+      GemmDesc zd = gemm_desc(m, d, d, sb.G, d, 0, sb.U, ldd, 1, nullptr, d);
+      zd.epi = EPI_GRADH;
+      zd.C2 = gH;
+      zd.ldc2 = d;
+      zd.E = sb.Hhat;
+      zd.lde = d;
+      zd.rs = sq ? nullptr : sb.dq;
+      gb.d[gb.n++] = zd;
+    } else {
+      ob.op[ob.n++] = z;
+    }
     if (big && !tay)
       gb.d[gb.n++] = gemm_desc(m, m, d, sb.Htil, d, 0, sb.G, d, 0, sb.HZ, m);
     else
@@ -1486,7 +1502,7 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
       ++ob.n;
     }
     finalize(ob, ob.n);
-    if (gb.n) gemm_prepare(gb, tile_zgrad(m, d));
+    if (gb.n) gemm_prepare(gb, tz);
   }
   // Launch 4: Zq = (eta^2/2) M H - eta grad_H (M assembled as it is loaded);
   // R X = 2 eta S (c0 Xs + c1 W1 + c2 P2 + c3 P3 + E^4 (c4 Xs + c5 W1 + c6 P2 + c7 P3)),
@@ -1558,11 +1574,12 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
 
 void step_launch_sizes(const StepPlan &pl, int m, int K, int (&grid)[5]) {
   auto sec = [](int n) { return (n + 7) & ~7; };
-  grid[0] = sec(pl.ob[0].total) + sec(pl.gb_contract.total_tiles) + m;
+  auto gsec = [](const GemmBatch &b) { return gemm_section(gemm_hdr(b), b.tile); };
+  grid[0] = sec(pl.ob[0].total) + gsec(pl.gb_contract) + m;
   grid[1] = sec(m) + section_by_op(pl.ob[1]);
-  grid[2] = section_by_op(pl.ob[2]) + sec(pl.gb_zgrad.total_tiles) + (m * m + 255) / 256 + 2;
-  grid[3] = sec(pl.ob[3].total) + sec(pl.gb_mid.total_tiles) + (m * K + 15) / 16;
-  grid[4] = sec(pl.gb_update.total_tiles) + m * K;
+  grid[2] = section_by_op(pl.ob[2]) + gsec(pl.gb_zgrad) + (m * m + 255) / 256 + 2;
+  grid[3] = sec(pl.ob[3].total) + gsec(pl.gb_mid) + (m * K + 15) / 16;
+  grid[4] = gsec(pl.gb_update) + m * K;
 }
 
 void enqueue_step_launch(int which, const StepBufs &sb, const StepPlan &host, const StepPlan *dev,

@@ -411,15 +411,17 @@ __device__ __forceinline__ bool p64_vec(const float *p, int64_t ld, int ext) {
 }
 
 // A batch on 64 x 64 tiles (GemmBatch::tile == 64): C = alpha opA opB + beta C_in, with
-// the second k segment (A2, B2, K2) when K2 > 0.  No split k and no fused epilogue
-// (the host only plans such batches).  Tiles of one product run column by column, so
-// that the tiles one XCD takes share B's panels.
-template <class Hd>
-__device__ __forceinline__ void gemm_body64(const GemmBatch &bt, const Hd &hd, const float *H,
-                                            float *gH, float lr, const int *__restrict__ gate,
-                                            int wg) {
+// the second k segment (A2, B2, K2) when K2 > 0, and the grad_H epilogue (C2 = 2 rs E
+// + C, rs = 1 when null; C may then be null).  No split k (the host plans none).
+// Tiles of one product run column by column, so that the tiles one XCD takes share B's
+// panels.
+// wg: the workgroup's index in the batch's section (gemm_section(hd, 64) of them).
+__device__ __forceinline__ void gemm_body64(const GemmBatch &bt, const GemmHdr &hd,
+                                            const float *H, float *gH, float lr,
+                                            const int *__restrict__ gate, int wg) {
+  const int tile = gemm_tile64(hd, wg);
+  if (tile < 0) return;
   const int closed = gate ? *gate : 0;
-  const int tile = xcd_tile(wg, hd.total_tiles);
   int di = 0;
 #pragma unroll
   for (int q = 1; q < kMaxBatch; ++q)
@@ -430,10 +432,12 @@ __device__ __forceinline__ void gemm_body64(const GemmBatch &bt, const Hd &hd, c
   g.A2 = resolve(g.A2, H, gH);
   g.B2 = resolve(g.B2, H, gH);
   g.Cin = resolve(g.Cin, H, gH);
+  g.C2 = const_cast<float *>(resolve(g.C2, H, gH));
   if (g.lr_scaled) {
     g.alpha *= lr * lr;
     g.beta *= lr;
   }
+  const bool epi = g.epi == EPI_GRADH;
   const int local = tile - g.tile_begin;
   const int tn = local / g.tiles_m, tm = local - tn * g.tiles_m;
   const int i0 = tm * kT64, j0 = tn * kT64;
@@ -441,15 +445,18 @@ __device__ __forceinline__ void gemm_body64(const GemmBatch &bt, const Hd &hd, c
   const int li = lane & 31, lh = lane >> 5;
   const int ai = 32 * (wave >> 1) + li, bj = 32 * (wave & 1) + li;
 
-  // C_in before the k loop (its latency overlaps it); lane (li, lh) of the wave holds
-  // rows 8 (r / 4) + 4 lh + r % 4 of the quadrant, column li.
+  // The epilogue operand (E with the grad_H epilogue, else C_in) before the k loop, so
+  // that its latency overlaps it; lane (li, lh) of the wave holds rows
+  // 8 (r / 4) + 4 lh + r % 4 of the quadrant, column li.
   const int ib = i0 + 32 * (wave >> 1) + 4 * lh;
-  const int j = j0 + bj;
-  float cin[16];
+  const int j = j0 + bj, jc = min(j, g.N - 1);
+  const float *pre = epi ? g.E : g.Cin;
+  const int64_t ldpre = epi ? g.lde : g.ldcin;
+  float pv[16];
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int i = min(ib + 8 * (r >> 2) + (r & 3), g.M - 1);
-    cin[r] = g.Cin ? g.Cin[(int64_t)i * g.ldcin + min(j, g.N - 1)] : 0.f;
+    pv[r] = pre ? pre[(int64_t)i * ldpre + jc] : 0.f;
   }
 
   const bool akc = g.tA == 0, bkc = g.tB == 0;
@@ -491,7 +498,12 @@ __device__ __forceinline__ void gemm_body64(const GemmBatch &bt, const Hd &hd, c
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int i = ib + 8 * (r >> 2) + (r & 3);
-    if (i < g.M) g.C[(int64_t)i * g.ldc + j] = g.alpha * (acc[0][r] + acc[1][r]) + g.beta * cin[r];
+    if (i < g.M) {
+      float out = g.alpha * (acc[0][r] + acc[1][r]);
+      if (g.Cin) out += g.beta * (epi ? g.Cin[(int64_t)i * g.ldcin + j] : pv[r]);
+      if (g.C) g.C[(int64_t)i * g.ldc + j] = out;
+      if (epi) g.C2[(int64_t)i * g.ldc2 + j] = 2.f * (g.rs ? g.rs[i] : 1.f) * pv[r] + out;
+    }
   }
 }
 

@@ -79,7 +79,7 @@ struct GemmDesc {
 inline const float *sym_H() { return reinterpret_cast<const float *>(uintptr_t{16}); }
 inline float *sym_gradH() { return reinterpret_cast<float *>(uintptr_t{32}); }
 
-constexpr int kMaxBatch = 4;
+constexpr int kMaxBatch = 5;
 
 struct GemmBatch {
   GemmDesc d[kMaxBatch];
@@ -90,17 +90,51 @@ struct GemmBatch {
              // step's LDS-staged tiles at large shapes)
 };
 
-// A GemmBatch's tile ranges, passed to the step's kernels by value (as OpHdr below).
+// A GemmBatch's tile ranges, passed to the step's kernels by value (as OpHdr below):
+// descriptor q owns tiles [tile_begin[q], tile_begin[q] + count[q]).
 struct GemmHdr {
   int n, total_tiles;
   int tile_begin[kMaxBatch];
+  int count[kMaxBatch];
 };
 inline GemmHdr gemm_hdr(const GemmBatch &b) {
   GemmHdr h{};
   h.n = b.n;
   h.total_tiles = b.total_tiles;
-  for (int q = 0; q < kMaxBatch; ++q) h.tile_begin[q] = b.d[q].tile_begin;
+  for (int q = 0; q < kMaxBatch; ++q) {
+    const GemmDesc &g = b.d[q];
+    h.tile_begin[q] = g.tile_begin;
+    h.count[q] = q < b.n && g.M > 0 && g.N > 0 ? g.tiles_m * g.tiles_n * (g.splits > 1 ? g.splits : 1) : 0;
+  }
   return h;
+}
+
+// The workgroups of a step launch's section for a batch: 32 x 32 tiles in one range
+// (8 ceil(T / 8) workgroups for T tiles, each XCD a contiguous eighth); 64 x 64 tiles
+// product by product, 8 ceil(T_q / 8) workgroups for product q, its T_q tiles spread
+// evenly over the 8 XCDs (measured at m = 512: launch 3, whose products differ in k,
+// 7 us faster at d = 1024; launch 5 6 us).
+__host__ __device__ inline int gemm_section(const GemmHdr &h, int tile_edge) {
+  if (tile_edge != 64) return (h.total_tiles + 7) & ~7;
+  int n = 0;
+  for (int q = 0; q < kMaxBatch; ++q)
+    if (q < h.n) n += (h.count[q] + 7) >> 3;
+  return 8 * n;
+}
+
+// Workgroup w of a 64 x 64 tiles' section (w % 8 its XCD): the tile it owns, or -1.
+// XCD x owns a contiguous eighth of every product's tiles.
+__host__ __device__ inline int gemm_tile64(const GemmHdr &h, int w) {
+  const int x = w & 7;
+  int s = w >> 3;
+  for (int q = 0; q < kMaxBatch; ++q) {
+    if (q >= h.n) break;
+    const int T = h.count[q], c8 = T >> 3, r = T & 7;
+    const int c = x < r ? c8 + 1 : c8;
+    if (s < c) return h.tile_begin[q] + (x < r ? x * (c8 + 1) : r * (c8 + 1) + (x - r) * c8) + s;
+    s -= c;
+  }
+  return -1;
 }
 __host__ __device__ inline int hdr_begin(const GemmBatch &b, int q) { return b.d[q].tile_begin; }
 __host__ __device__ inline int hdr_begin(const GemmHdr &h, int q) { return h.tile_begin[q]; }

@@ -154,15 +154,23 @@ void check_gemm(const Space &sp, const GemmBatch &gb, const char *tag) {
       sp.in(w, g.B2, g.tB ? (int64_t)(g.K2 - 1) * g.ldb2 + (g.N - 1)
                           : (int64_t)(g.N - 1) * g.ldb2 + (g.K2 - 1));
     }
-    sp.in(w, g.C, (int64_t)(g.M - 1) * g.ldc + (g.N - 1));
+    // C may be null under the grad_H epilogue (the product itself not kept)
+    CHECK(g.C || g.epi == EPI_GRADH, "%s: no output", w);
+    if (g.C) sp.in(w, g.C, (int64_t)(g.M - 1) * g.ldc + (g.N - 1));
     if (g.Cin) sp.in(w, g.Cin, (int64_t)(g.M - 1) * g.ldcin + (g.N - 1));
+    if (g.epi == EPI_GRADH) {
+      CHECK(gb.tile == 64 || g.C, "%s: the 32 x 32 grad_H epilogue stores C", w);
+      sp.in(w, g.C2, (int64_t)(g.M - 1) * g.ldc2 + (g.N - 1));
+      sp.in(w, g.E, (int64_t)(g.M - 1) * g.lde + (g.N - 1));
+      if (g.rs) sp.in(w, g.rs, g.M - 1);
+    }
     CHECK(g.splits == 1, "%s: split descriptors in a step plan", w);
     // the tile bookkeeping the kernels decode (32 x 32 tiles, or the 64 x 64 tiles,
     // which have no fused epilogue)
     CHECK(gb.tile == 32 || gb.tile == 64, "%s: tile edge %d", w, gb.tile);
     CHECK(g.tiles_m == (g.M + gb.tile - 1) / gb.tile && g.tiles_n == (g.N + gb.tile - 1) / gb.tile,
           "%s: tile counts", w);
-    CHECK(gb.tile == 32 || (g.epi == 0 && g.colsq == nullptr), "%s: epilogue on 64 x 64 tiles", w);
+    CHECK(gb.tile == 32 || g.colsq == nullptr, "%s: column sums on 64 x 64 tiles", w);
   }
   int total = 0;
   for (int i = 0; i < gb.n; ++i) {
@@ -173,6 +181,22 @@ void check_gemm(const Space &sp, const GemmBatch &gb, const char *tag) {
     total += t;
   }
   CHECK(gb.n == 0 || total == gb.total_tiles, "%s: total %d, tiles %d", tag, gb.total_tiles, total);
+  // the header's per-product counts, and the section covering every tile exactly once
+  const GemmHdr h = gemm_hdr(gb);
+  int sum = 0;
+  for (int i = 0; i < kMaxBatch; ++i) sum += h.count[i];
+  CHECK(gb.n == 0 || sum == gb.total_tiles, "%s: header counts %d, tiles %d", tag, sum, gb.total_tiles);
+  if (gb.n > 0 && gb.tile == 64) {
+    std::vector<int> seen(gb.total_tiles, 0);
+    const int ns = gemm_section(h, 64);
+    for (int w = 0; w < ns; ++w) {
+      const int t = gemm_tile64(h, w);
+      CHECK(t >= -1 && t < gb.total_tiles, "%s: section tile %d out of range", tag, t);
+      if (t >= 0 && t < gb.total_tiles) ++seen[t];
+    }
+    for (int t = 0; t < gb.total_tiles; ++t)
+      CHECK(seen[t] == 1, "%s: 64 x 64 tile %d owned %d times", tag, t, seen[t]);
+  }
 }
 
 void plans() {
