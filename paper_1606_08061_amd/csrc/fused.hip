@@ -1375,7 +1375,7 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
   // Launch 1: H^ = H Q (row partials h . h^ -> qpart), H~ = H U^T, X = H U^{-T T}, N = H H^T.
   // At large shapes the m x d products go to 32 x 32 tiles, which read half the operand
   // bytes per output (H^ stays on 16 x 16 tiles for the spherical family, whose epilogue
-  // reduces q_j).
+  // reduces q_j); on 64 x 64 tiles N joins them.
   {
     OpBatch &ob = pl.ob[0];
     GemmBatch &gb = pl.gb_contract;
@@ -1396,6 +1396,7 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
     } else {
       gb.d[gb.n++] = gemm_desc(m, d, d, H, d, 0, sb.Q, ldd, 0, sb.Hhat, d);
     }
+    const int tc = tile_contract(m, d);
     if (big) {
       gb.d[gb.n++] = gemm_desc(m, d, d, H, d, 0, sb.U, ldd, 0, sb.Htil, d);
       gb.d[gb.n++] = gemm_desc(m, d, d, H, d, 0, sb.UinvT, ldd, 0, sb.X, d);
@@ -1403,11 +1404,14 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
       ob.op[ob.n++] = op(m, d, d, H, d, 0, sb.U, ldd, 0, sb.Htil, d);
       ob.op[ob.n++] = op(m, d, d, H, d, 0, sb.UinvT, ldd, 0, sb.X, d);
     }
-    ob.op[ob.n++] = op(m, m, d, H, d, 0, H, d, 0, sb.N, m);
+    if (big && tc == 64)
+      gb.d[gb.n++] = gemm_desc(m, m, d, H, d, 0, H, d, 0, sb.N, m);
+    else
+      ob.op[ob.n++] = op(m, m, d, H, d, 0, H, d, 0, sb.N, m);
     if (tay)  // [s h~] = H [w_bar omega] (eq. svec, gen-htilde)
       ob.op[ob.n++] = op(m, 2, d, H, d, 0, sb.WO, ldd, 0, sb.SW, 2);
     finalize(ob, ob.n);
-    if (gb.n) gemm_prepare(gb, tile_contract(m, d));
+    if (gb.n) gemm_prepare(gb, tc);
   }
   // Launch 2: M^ = H H^^T; E^2 = 4 eta^2 S N D N S (|row| partials -> bpart);
   // W1 = E Xs = 2 eta S N D X
