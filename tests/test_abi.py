@@ -136,10 +136,10 @@ def test_noalloc_step_checks_its_arguments_on_the_host(L):
     assert call(a12=-1) == lst.LST_E_SHAPE     # m < 0
     assert call(a2=7) == lst.LST_E_ARG         # loss kind
     assert call(a2=2) == lst.LST_E_ARG         # the Taylor softmax without WO
-    # the 16 MiB array holds m = 128 (K = 5) up to d = 2861 and m = 512 up to d = 361 (sizes
+    # the 16 MiB array holds m = 128 (K = 5) up to d = 2860 and m = 512 up to d = 361 (sizes
     # that fit are not called here: with these stand-in pointers the call would go on to
     # the device)
-    assert call(a1=2862, a5=2862, a10=2862) == lst.LST_E_SHAPE
+    assert call(a1=2861, a5=2861, a10=2861) == lst.LST_E_SHAPE
     assert call(a1=362, a5=362, a10=362, a12=512, a15=5) == lst.LST_E_SHAPE
 
 

@@ -201,12 +201,13 @@ def _poly_bound(H, dq, lr):
     return float(np.sqrt(np.abs(E @ E).sum(1).max()))
 
 
-@pytest.mark.parametrize("m,d", [(64, 32), (200, 48)])
+@pytest.mark.parametrize("m,d", [(64, 32), (200, 48), (512, 1024)])
 def test_uncertified_woodbury_takes_exact_elimination(m, d):
     # Steps large enough (2 eta lambda_max(H H^T) = 0.6) that the degree-7 polynomial cannot
     # certify C^{-1} = (I - 2 eta H H^T)^{-1} (its bound needs ||E^2||^(1/2) <= 0.3), while C is
     # still positive definite: one workgroup inverts C by exact elimination (m = 200: beyond
-    # the 128 rows the tiles of one product hold), and the step matches the oracle.
+    # the 128 rows the tiles of one product hold; m = 512, d = 1024: R X on 64 x 64 tiles
+    # takes its alternative), and the step matches the oracle.
     w = Workload("t", LOSS_SQUARED, 3000, d, m, 3)
     s = Stream(w, seed=m)
     f = make_factored(w, s.V0)
