@@ -704,13 +704,26 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
   // q_j: for squared error h_j . h^_j here (its operands loaded first, used after the
   // target rows' dot products); for the spherical family reduced in launch 1 (its E
   // products need every q_j), loaded with T, s_j and h~_j as uniform values.
+  // Also h~_j at the columns this thread writes 2 eta dl/dq_j h~_j to (loaded here: in the
+  // loop of those stores, the compiler could not move a load of h~ above the previous
+  // column's stores, one round trip per 256 columns).
   constexpr int NQ = (64 * NV + 255) / 256;
-  float qh[NQ], qhh[NQ];
+  const float *htp = ga.Htil + (int64_t)j * d;
+  float qh[NQ], qhh[NQ], hv[NQ];
 #pragma unroll
   for (int u = 0; u < NQ; ++u) {
     const int c = t + 256 * u;
     qh[u] = (sq && c < d) ? ga.H[(int64_t)j * d + c] : 0.f;
     qhh[u] = (sq && c < d) ? ga.Hhat[(int64_t)j * d + c] : 0.f;
+    hv[u] = c < d ? htp[c] : 0.f;
+  }
+  // h~_j in the layout of the target rows (lane + 64 n), before the rows' loads, which
+  // wait for the indices
+  float ht[NV];
+#pragma unroll
+  for (int n = 0; n < NV; ++n) {
+    const int c = lane + 64 * n;
+    ht[n] = (c < d) ? htp[c] : 0.f;
   }
   float qv = 0.f, tsv = 0.f, sj = 0.f, hw = 0.f;
   if (!sq) {
@@ -749,13 +762,6 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
       const float xv = row[min(c, d - 1)];
       vr[i][n] = (r[i] >= 0 && c < d) ? xv : 0.f;
     }
-  }
-  float ht[NV];
-  const float *htp = ga.Htil + (int64_t)j * d;
-#pragma unroll
-  for (int n = 0; n < NV; ++n) {
-    const int c = lane + 64 * n;
-    ht[n] = (c < d) ? htp[c] : 0.f;
   }
   // the loss's log of the normaliser (spherical family)
   float lz = 0.f;
@@ -821,9 +827,13 @@ __device__ __forceinline__ void gather_reg(const GatherArgs &ga, int j) {
   // G_j and 2 eta dl/dq_j h~_j
   const float gq = dq_of(ga.loss, qv, sj, tsv, Dn, ga.eps);
   const float s2 = 2.f * ga.lr * gq;
-  for (int c = t; c < d; c += 256) {
-    ga.G[(int64_t)j * d + c] = (gpart[0][c] + gpart[1][c]) + (gpart[2][c] + gpart[3][c]);
-    ga.Atil[(int64_t)j * d + c] = s2 * htp[c];
+#pragma unroll
+  for (int u = 0; u < NQ; ++u) {
+    const int c = t + 256 * u;
+    if (c < d) {
+      ga.G[(int64_t)j * d + c] = (gpart[0][c] + gpart[1][c]) + (gpart[2][c] + gpart[3][c]);
+      ga.Atil[(int64_t)j * d + c] = s2 * hv[u];
+    }
   }
   if (t == 0) {
     if (sbad[0] | sbad[1] | sbad[2] | sbad[3]) atomicOr(ga.flag, FLAG_INDEX);
