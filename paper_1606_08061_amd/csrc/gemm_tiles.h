@@ -292,8 +292,8 @@ constexpr int kT64U = kT64K / 16, kT64Lpr = kT64K / 4, kT64Rpu = 256 / kT64Lpr;
 constexpr int kT64P = 2;  // k steps in flight in registers (even: LDS buffer = step % 2)
 static_assert(kT64P % 2 == 0, "the LDS buffer of a step is its register slot's parity");
 
-// One operand of one k segment: element (index i, k) at p[i * si + k * sk]; n indices,
-// k in [0, kend).
+// One operand of one k segment: element (index i, k) at p[i ld + k] (k contiguous) or
+// p[k ld + i] (index contiguous); n indices, k in [0, kend).
 struct Panel {
   const float *p;
   int64_t ld;
