@@ -1365,14 +1365,15 @@ bool contract_on_32(int m, int d) {
 }
 
 // The tile edge of the large-shape batches: LDS-staged 64 x 64 tiles where they were
-// measured faster than 32 x 32 tiles (m = 512: launch 3 at d = 256 to 1024, launch 1 at
-// d = 512 and 1024, launches 4 and 5 at d = 1024; slower at m = 256, d = 512 and in
-// launches 4 and 5 at d = 512, where the products have too few 64 x 64 tiles to fill
-// the chip).
-constexpr int kT64Contract = 64, kT64Zgrad = 64, kT64Update = 256, kT64MinK = 256;
+// measured faster than 32 x 32 tiles (m = 512: launches 1 and 3 at d = 256 to 1024,
+// launches 4 and 5 at d = 1024; slower at m = 256, d = 512 and in launches 4 and 5 at
+// d = 512, where the products have too few 64 x 64 tiles to fill the chip).
+constexpr int kT64Contract = 32, kT64Zgrad = 64, kT64Update = 256, kT64MinK = 256;
 int tiles64(int M, int N) { return ((M + 63) / 64) * ((N + 63) / 64); }
-// launch 1 (m x d outputs, k = d)
-int tile_contract(int m, int d) { return tiles64(m, d) >= kT64Contract ? 64 : 32; }
+// launch 1 (m x d outputs, k = d; N, m x m, joins them)
+int tile_contract(int m, int d) {
+  return tiles64(m, d) >= kT64Contract && tiles64(m, m) >= kT64Zgrad ? 64 : 32;
+}
 // launch 3 (m x m and m x d outputs, k = d or m); on 64 x 64 tiles Z^ joins the batch
 // with its grad_H epilogue (d = 1024: the launch 76 -> 50 us)
 int tile_zgrad(int m, int d) { return tiles64(m, m) >= kT64Zgrad ? 64 : 32; }
