@@ -447,11 +447,12 @@ __device__ __forceinline__ void run_op(const OpHdr &hd, const Op16 *ops, int til
 
 // The step's products on 32 x 32 tiles (GT = 32, KS k-blocks of 8 in flight per wave)
 // or on LDS-staged 64 x 64 tiles (GT = 64, large shapes).
-template <int GT, int KS, class Hd>
+template <int GT, int KS, bool TERMS = false, class Hd>
 __device__ __forceinline__ void step_gemm(const GemmBatch &bt, const Hd &hd, const float *H,
-                                          float *gH, float lr, const int *gate, int w) {
+                                          float *gH, float lr, const int *gate, int w,
+                                          const int *cert = nullptr) {
   if constexpr (GT == 64)
-    gemm_body64(bt, hd, H, gH, lr, gate, w);
+    gemm_body64<TERMS>(bt, hd, H, gH, lr, gate, w, cert);
   else
     gemm_body<4, KS>(bt, hd, H, gH, lr, gate, w);
 }
@@ -1261,8 +1262,10 @@ __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__re
 // Launch 4: Zq, R X, the U update and the V scatter's plan.  Launch 5: the Q and U^{-T}
 // updates and the V scatter.  GT: the tile edge of gb_mid's and gb_update's products.
 // ---------------------------------------------------------------------------
+// (three workgroups per CU with the 64 x 64 tiles, for the registers of Zq's and R X's
+// operand terms)
 template <int GT>
-__global__ __launch_bounds__(256, 4) void step_mid_kernel(const StepPlan *__restrict__ pl,
+__global__ __launch_bounds__(256, GT == 64 ? 3 : 4) void step_mid_kernel(const StepPlan *__restrict__ pl,
                                                        const OpHdr hd, const GemmHdr gh,
                                                        const float *H, float *gH, float lr,
                                                        const float *dq,
@@ -1278,7 +1281,7 @@ __global__ __launch_bounds__(256, 4) void step_mid_kernel(const StepPlan *__rest
   const int gsec = gemm_section(gh, GT);
   if (GT == 64) {
     if (w < gsec) {
-      step_gemm<GT, 4>(pl->gb_mid, gh, H, gH, lr, flag, w);
+      step_gemm<GT, 4, true>(pl->gb_mid, gh, H, gH, lr, flag, w, cert);
       return;
     }
     w -= gsec;
@@ -1572,7 +1575,11 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
     zq.ldcin = d;
     zq.beta = -1.f;
     zq.beta_lr = 1;
-    ob.op[0] = zq;
+    // On 64 x 64 tiles (d = 1024) the squared error's Zq and R X join the U update: M
+    // and R X's B assembled from their terms as they are staged, R X's addends in the
+    // epilogue, and the exact R X as its alternative.
+    const bool mid64 = sq && tile_update(m, d) == 64;
+    if (!mid64) ob.op[0] = zq;
     const int xsc = sq ? SC_NONE : SC_SQRT;
     Op16 rx = op(m, d, m, sb.E4, m, 0, sb.X, d, 1, sb.RX, d);
     rx.nb = 4;
@@ -1589,15 +1596,55 @@ void build_step_plan(const StepBufs &sb, int m, StepPlan &pl) {
     rx.alpha_lr = 1;
     rx.rs = xsc;
     rx.alt = 2;
-    ob.op[1] = rx;
-    ob.op[2] = op(m, d, m, sb.R, m, 0, sb.X, d, 1, sb.RX, d);  // exact R
-    ob.n = 3;
-    finalize(ob, 2);
     GemmBatch &gb = pl.gb_mid;
     // U <- U - (2 eta D H~)^T H
     gb.d[0] = gemm_desc(d, d, m, sb.Atil, d, 1, H, d, 1, sb.U, ldd, -1.f, sb.U, ldd, 1.f);
     gb.n = 1;
+    if (mid64) {
+      // Zq = (eta^2 / 2) (4 M^ + Yring^T Yring + 2 HZ + 2 HZ^T) H - eta grad_H
+      GemmDesc zd = gemm_desc(m, d, m, sb.Mhat, m, 0, H, d, 1, sb.Zq, d, 0.5f, gH, d, -1.f);
+      zd.lr_scaled = 1;
+      zd.nat = 3;
+      zd.aw[0] = 4.f;
+      zd.At[0] = sb.YY;
+      zd.aw[1] = 1.f;
+      zd.At[1] = sb.HZ;
+      zd.aw[2] = 2.f;
+      zd.Atr = sb.HZ;
+      zd.awt = 2.f;
+      gb.d[gb.n++] = zd;
+      // R X = 2 eta (E^4 (c4 X + c5 W1 + c6 P2 + c7 P3) + c0 X + c1 W1 + c2 P2 + c3 P3)
+      GemmDesc rd = gemm_desc(m, d, m, sb.E4, m, 0, sb.X, d, 1, sb.RX, d, 2.f);
+      rd.lr_scaled = 2;
+      rd.coef = sb.coef;
+      rd.nbt = 4;
+      rd.nadd = 4;
+      rd.ldadd = d;
+      const float *term[4] = {sb.X, sb.W1, sb.P2, sb.P3};
+      for (int t = 0; t < 4; ++t) {
+        rd.bcoef[t] = 4 + t;
+        if (t > 0) rd.Bt[t - 1] = term[t];
+        rd.acoef[t] = t;
+        rd.addp[t] = term[t];
+      }
+      rd.alt1 = 4;  // d[3], below
+      gb.d[gb.n++] = rd;
+      ob.n = 0;
+      finalize(ob, 0);
+    } else {
+      ob.op[1] = rx;
+      ob.op[2] = op(m, d, m, sb.R, m, 0, sb.X, d, 1, sb.RX, d);  // exact R
+      ob.n = 3;
+      finalize(ob, 2);
+    }
     gemm_prepare(gb, tile_update(m, d));
+    if (mid64) {  // R X's alternative with the exact R, outside the batch's tile ranges
+      GemmDesc &alt = gb.d[3];
+      alt = gemm_desc(m, d, m, sb.R, m, 0, sb.X, d, 1, sb.RX, d);
+      alt.tiles_m = gb.d[2].tiles_m;
+      alt.tiles_n = gb.d[2].tiles_n;
+      alt.tile_begin = gb.total_tiles;
+    }
   }
   // Launch 5: Q <- Q + H^T Zq + Zq^T H; U^{-T} <- U^{-T} + (R X)^T H; omega, w_bar
   {

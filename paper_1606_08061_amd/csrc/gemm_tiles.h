@@ -364,41 +364,96 @@ __device__ __forceinline__ void p64_mfma(float (*As)[kT64Ld], float (*Bs)[kT64Ld
   }
 }
 
+// Extra operand terms of a k step (one k segment): NA terms of opA in its layout (the
+// first from the panel, the others from a[]), with ATR one more read transposed
+// (element (i, k) at at[k lda + i], in the k-contiguous thread mapping), and NB terms
+// of opB; each operand's terms are combined with their weights as it is stored to LDS.
+template <int NA, bool ATR, int NB>
+struct Terms {
+  const float *a[NA > 1 ? NA - 1 : 1];
+  const float *b[NB > 1 ? NB - 1 : 1];
+  const float *at;
+  float wa[NA], wb[NB], wt;
+};
+
+template <int MODE, int N, bool TR>
+__device__ __forceinline__ void p64_store_terms(float (*lds)[kT64Ld], const float4 (&v)[N][kT64U],
+                                                const float4 (&vt)[kT64U], const float (&w)[N],
+                                                float wt) {
+  if constexpr (N == 1 && !TR) {
+    p64_store<MODE>(lds, v[0]);
+  } else {
+    float4 c[kT64U];
+#pragma unroll
+    for (int u = 0; u < kT64U; ++u) {
+      c[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int t = 0; t < N + (TR ? 1 : 0); ++t) {
+        const float4 x = t < N ? v[t < N ? t : 0][u] : vt[u];
+        const float y = t < N ? w[t < N ? t : 0] : wt;
+        c[u].x = fmaf(y, x.x, c[u].x);
+        c[u].y = fmaf(y, x.y, c[u].y);
+        c[u].z = fmaf(y, x.z, c[u].z);
+        c[u].w = fmaf(y, x.w, c[u].w);
+      }
+    }
+    p64_store<MODE>(lds, c);
+  }
+}
+
 // k steps 0 .. ns1 - 1 run over segment 0 (pa0, pb0), the rest over segment 1.
-template <int AM, int BM>
+template <int AM, int BM, int NA, bool ATR, int NB>
 __device__ __forceinline__ void k64(const Panel &pa0, const Panel &pb0, const Panel &pa1,
-                                    const Panel &pb1, bool akc, bool bkc, int ns1, int ns, int i0,
-                                    int j0, float (*As)[kT64K][kT64Ld], float (*Bs)[kT64K][kT64Ld],
+                                    const Panel &pb1, const Terms<NA, ATR, NB> &tm, bool akc,
+                                    bool bkc, int ns1, int ns, int i0, int j0,
+                                    float (*As)[kT64K][kT64Ld], float (*Bs)[kT64K][kT64Ld],
                                     floatx16 (&acc)[2], int ai, int bj, int lh) {
-  auto load = [&](int st, float4(&ra)[kT64U], float4(&rb)[kT64U]) {
+  auto load = [&](int st, float4(&ra)[NA][kT64U], float4(&rt)[kT64U], float4(&rb)[NB][kT64U]) {
     const bool s1 = st >= ns1;
     const int k0 = (s1 ? st - ns1 : st) * kT64K;
-    p64_load<AM>(s1 ? pa1 : pa0, akc, i0, k0, ra);
-    p64_load<BM>(s1 ? pb1 : pb0, bkc, j0, k0, rb);
+    const Panel &A = s1 ? pa1 : pa0, &B = s1 ? pb1 : pb0;
+    p64_load<AM>(A, akc, i0, k0, ra[0]);
+#pragma unroll
+    for (int t = 1; t < NA; ++t) {
+      Panel q = A;
+      q.p = tm.a[t - 1];
+      p64_load<AM>(q, akc, i0, k0, ra[t]);
+    }
+    if constexpr (ATR) {
+      Panel q = A;
+      q.p = tm.at;
+      p64_load<GEN>(q, false, i0, k0, rt);
+    }
+    p64_load<BM>(B, bkc, j0, k0, rb[0]);
+#pragma unroll
+    for (int t = 1; t < NB; ++t) {
+      Panel q = B;
+      q.p = tm.b[t - 1];
+      p64_load<BM>(q, bkc, j0, k0, rb[t]);
+    }
   };
   constexpr int AS = AM == IXV ? IXV : KCV, BS = BM == IXV ? IXV : KCV;  // LDS store layout
   // Register slot u % kT64P holds step u from its load until its store to LDS buffer
   // u % 2, one step before its products; the slot then takes step u + kT64P.
-  float4 ra[kT64P][kT64U], rb[kT64P][kT64U];
+  float4 ra[kT64P][NA][kT64U], rt[kT64P][kT64U], rb[kT64P][NB][kT64U];
+  auto store = [&](int buf, int slot) {
+    p64_store_terms<AS, NA, ATR>(As[buf], ra[slot], rt[slot], tm.wa, tm.wt);
+    const float4 none[kT64U] = {};
+    p64_store_terms<BS, NB, false>(Bs[buf], rb[slot], none, tm.wb, 0.f);
+  };
 #pragma unroll
   for (int u = 0; u < kT64P; ++u)
-    if (u < ns) load(u, ra[u], rb[u]);
-  if (ns > 0) {
-    p64_store<AS>(As[0], ra[0]);
-    p64_store<BS>(Bs[0], rb[0]);
-  }
+    if (u < ns) load(u, ra[u], rt[u], rb[u]);
+  if (ns > 0) store(0, 0);
   __syncthreads();
   for (int st = 0; st < ns; st += kT64P) {
 #pragma unroll
     for (int u = 0; u < kT64P; ++u) {
       const int s = st + u;
       if (s < ns) {
-        if (s + kT64P < ns) load(s + kT64P, ra[u], rb[u]);
+        if (s + kT64P < ns) load(s + kT64P, ra[u], rt[u], rb[u]);
         p64_mfma(As[u & 1], Bs[u & 1], acc, ai, bj, lh);
-        if (s + 1 < ns) {
-          p64_store<AS>(As[(u + 1) & 1], ra[(u + 1) % kT64P]);
-          p64_store<BS>(Bs[(u + 1) & 1], rb[(u + 1) % kT64P]);
-        }
+        if (s + 1 < ns) store((u + 1) & 1, (u + 1) % kT64P);
         __syncthreads();
       }
     }
@@ -412,13 +467,17 @@ __device__ __forceinline__ bool p64_vec(const float *p, int64_t ld, int ext) {
 
 // A batch on 64 x 64 tiles (GemmBatch::tile == 64): C = alpha opA opB + beta C_in, with
 // the second k segment (A2, B2, K2) when K2 > 0, and the grad_H epilogue (C2 = 2 rs E
-// + C, rs = 1 when null; C may then be null).  No split k (the host plans none).
-// Tiles of one product run column by column, so that the tiles one XCD takes share B's
-// panels.
-// wg: the workgroup's index in the batch's section (gemm_section(hd, 64) of them).
+// + C, rs = 1 when null; C may then be null).  No split k (the host plans none).  Tiles
+// of one product run column by column, so that the tiles one XCD takes share B's
+// panels.  TERMS: the batch may also hold operand terms, addends and alternatives
+// (GemmDesc::nat ... alt1; a separate instantiation, for the registers they take).
+// wg: the workgroup's index in the batch's section (gemm_section(hd, 64) of them);
+// cert: the certificate flag that selects alternatives (null: certified).
+template <bool TERMS>
 __device__ __forceinline__ void gemm_body64(const GemmBatch &bt, const GemmHdr &hd,
                                             const float *H, float *gH, float lr,
-                                            const int *__restrict__ gate, int wg) {
+                                            const int *__restrict__ gate, int wg,
+                                            const int *__restrict__ cert = nullptr) {
   const int tile = gemm_tile64(hd, wg);
   if (tile < 0) return;
   const int closed = gate ? *gate : 0;
@@ -426,20 +485,23 @@ __device__ __forceinline__ void gemm_body64(const GemmBatch &bt, const GemmHdr &
 #pragma unroll
   for (int q = 1; q < kMaxBatch; ++q)
     if (q < hd.n && tile >= hdr_begin(hd, q)) di = q;
+  const int local = tile - hd.tile_begin[di];
   GemmDesc g = bt.d[di];
+  const int tn = local / g.tiles_m, tm = local - tn * g.tiles_m;
+  if (TERMS && g.alt1 > 0 && cert && *cert == 0) g = bt.d[g.alt1 - 1];  // same shape
   g.A = resolve(g.A, H, gH);
   g.B = resolve(g.B, H, gH);
   g.A2 = resolve(g.A2, H, gH);
   g.B2 = resolve(g.B2, H, gH);
   g.Cin = resolve(g.Cin, H, gH);
   g.C2 = const_cast<float *>(resolve(g.C2, H, gH));
-  if (g.lr_scaled) {
+  if (g.lr_scaled == 1) {
     g.alpha *= lr * lr;
     g.beta *= lr;
+  } else if (g.lr_scaled == 2) {
+    g.alpha *= lr;
   }
   const bool epi = g.epi == EPI_GRADH;
-  const int local = tile - g.tile_begin;
-  const int tn = local / g.tiles_m, tm = local - tn * g.tiles_m;
   const int i0 = tm * kT64, j0 = tn * kT64;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int li = lane & 31, lh = lane >> 5;
@@ -469,7 +531,7 @@ __device__ __forceinline__ void gemm_body64(const GemmBatch &bt, const GemmHdr &
     const int e0 = kc ? p0.kend : p0.n, e1 = kc ? p1.kend : p1.n;
     return p64_vec(p0.p, p0.ld, e0) && (g.K2 == 0 || p64_vec(p1.p, p1.ld, e1));
   };
-  const bool av = vec(pa0, pa1, akc), bv = vec(pb0, pb1, bkc);
+  bool av = vec(pa0, pa1, akc), bv = vec(pb0, pb1, bkc);
 
   floatx16 acc[2];
 #pragma unroll
@@ -479,27 +541,78 @@ __device__ __forceinline__ void gemm_body64(const GemmBatch &bt, const GemmHdr &
   // one LDS allocation for every load mode (the k loop's instantiations share it)
   __shared__ float As[2][kT64K][kT64Ld];
   __shared__ float Bs[2][kT64K][kT64Ld];
-#define LST_K64(AM, BM) \
-  k64<AM, BM>(pa0, pb0, pa1, pb1, akc, bkc, ns1, ns, i0, j0, As, Bs, acc, ai, bj, lh)
-  if (av && bv) {
-    if (akc && bkc)
-      LST_K64(KCV, KCV);
-    else if (akc)
-      LST_K64(KCV, IXV);
-    else if (bkc)
-      LST_K64(IXV, KCV);
-    else
-      LST_K64(IXV, IXV);
-  } else {
-    LST_K64(GEN, GEN);
+#define LST_K64(AM, BM, NA, ATR, NB, TM)                                                       \
+  k64<AM, BM, NA, ATR, NB>(pa0, pb0, pa1, pb1, TM, akc, bkc, ns1, ns, i0, j0, As, Bs, acc, ai, \
+                           bj, lh)
+  int nadd = 0;
+  bool done = false;
+  if constexpr (TERMS) {
+    nadd = g.nadd;
+    if (g.nat > 1 || g.Atr) {  // Zq: M assembled from its terms as it is staged
+      Terms<3, true, 1> t3{};
+#pragma unroll
+      for (int t = 0; t < 3; ++t) {
+        t3.wa[t] = t < g.nat ? g.aw[t] : 0.f;
+        if (t > 0) {
+          t3.a[t - 1] = t < g.nat ? g.At[t - 1] : g.A;
+          av = av && p64_vec(t3.a[t - 1], g.lda, g.K);
+        }
+      }
+      t3.at = g.Atr ? g.Atr : g.A;
+      t3.wt = g.Atr ? g.awt : 0.f;
+      t3.wb[0] = 1.f;
+      if (av && bv && akc && !bkc)
+        LST_K64(KCV, IXV, 3, true, 1, t3);
+      else
+        LST_K64(GEN, GEN, 3, true, 1, t3);
+      done = true;
+    } else if (g.nbt > 1) {  // R X: the B terms combined as they are staged
+      Terms<1, false, 4> t4{};
+      t4.wa[0] = 1.f;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        t4.wb[t] = t < g.nbt ? g.coef[g.bcoef[t]] : 0.f;
+        if (t > 0) {
+          t4.b[t - 1] = t < g.nbt ? g.Bt[t - 1] : g.B;
+          bv = bv && p64_vec(t4.b[t - 1], g.ldb, bkc ? g.K : g.N);
+        }
+      }
+      if (av && bv && akc && !bkc)
+        LST_K64(KCV, IXV, 1, false, 4, t4);
+      else
+        LST_K64(GEN, GEN, 1, false, 4, t4);
+      done = true;
+    }
+  }
+  if (!done) {
+    const Terms<1, false, 1> t1{};
+    if (av && bv) {
+      if (akc && bkc)
+        LST_K64(KCV, KCV, 1, false, 1, t1);
+      else if (akc)
+        LST_K64(KCV, IXV, 1, false, 1, t1);
+      else if (bkc)
+        LST_K64(IXV, KCV, 1, false, 1, t1);
+      else
+        LST_K64(IXV, IXV, 1, false, 1, t1);
+    } else {
+      LST_K64(GEN, GEN, 1, false, 1, t1);
+    }
   }
 #undef LST_K64
   if (closed || j >= g.N) return;  // after the k loop's last barrier
+  float adw[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) adw[t] = t < nadd ? g.coef[g.acoef[t]] : 0.f;
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int i = ib + 8 * (r >> 2) + (r & 3);
     if (i < g.M) {
-      float out = g.alpha * (acc[0][r] + acc[1][r]);
+      float v = acc[0][r] + acc[1][r];
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        if (t < nadd) v = fmaf(adw[t], g.addp[t][(int64_t)i * g.ldadd + j], v);
+      float out = g.alpha * v;
       if (g.Cin) out += g.beta * (epi ? g.Cin[(int64_t)i * g.ldcin + j] : pv[r]);
       if (g.C) g.C[(int64_t)i * g.ldc + j] = out;
       if (epi) g.C2[(int64_t)i * g.ldc2 + j] = 2.f * (g.rs ? g.rs[i] : 1.f) * pv[r] + out;

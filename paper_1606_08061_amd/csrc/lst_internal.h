@@ -66,11 +66,27 @@ struct GemmDesc {
   int kchunk;  // k per split (multiple of 8) when splits > 1
   int tiles_m, tiles_n;
   int tile_begin;
-  int lr_scaled;  // alpha *= lr^2 and beta *= lr at launch (plans shared across lr)
+  int lr_scaled;  // 1: alpha *= lr^2 and beta *= lr at launch; 2: alpha *= lr (plans shared
+                  // across lr)
   // 128 x 128-tile kernel without split: when set, also writes per-column partial
   // sums of squares of the product, colsq[p][j] for p < 4 * tiles_m (each the sum
   // over 32 of the tile's rows of C[i,j]^2 before alpha/beta).
   float *colsq;
+  // Operand terms (64 x 64 tiles of launch 4, one k segment, opA with k contiguous and
+  // opB with the index contiguous):
+  //   opA = sum over t < nat of aw[t] A_t (A_0 = A, the others At[t - 1], same lda)
+  //         + awt opAt, opAt(i,k) = Atr[k lda + i] when Atr is set;
+  //   opB = sum over t < nbt of coef[bcoef[t]] B_t (B_0 = B, the others Bt[t - 1]);
+  //   the product gains sum over t < nadd of coef[acoef[t]] addp[t][i ldadd + j]
+  //   before alpha;
+  //   alt1 > 0: descriptor alt1 - 1 of the batch (same shape, plain) replaces this one
+  //   while *cert == 0.
+  int nat, nbt, nadd, alt1;
+  const float *At[2], *Atr, *Bt[3], *addp[4];
+  float aw[3], awt;
+  int bcoef[4], acoef[4];
+  int64_t ldadd;
+  const float *coef;
 };
 
 // Operand placeholders of plans kept in device memory: a plan is built once per

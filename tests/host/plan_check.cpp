@@ -158,6 +158,40 @@ void check_gemm(const Space &sp, const GemmBatch &gb, const char *tag) {
     CHECK(g.C || g.epi == EPI_GRADH, "%s: no output", w);
     if (g.C) sp.in(w, g.C, (int64_t)(g.M - 1) * g.ldc + (g.N - 1));
     if (g.Cin) sp.in(w, g.Cin, (int64_t)(g.M - 1) * g.ldcin + (g.N - 1));
+    // operand terms, addends, alternatives (64 x 64 tiles, one k segment)
+    if (g.nat > 1 || g.Atr || g.nbt > 1 || g.nadd > 0 || g.alt1 > 0)
+      CHECK(gb.tile == 64 && g.K2 == 0 && g.tA == 0 && g.tB == 1 && g.nat <= 3 && g.nbt <= 4 &&
+                g.nadd <= 4,
+            "%s: operand terms", w);
+    for (int t = 1; t < g.nat && t < 3; ++t)
+      sp.in(w, g.At[t - 1], (int64_t)(g.M - 1) * g.lda + (g.K - 1));
+    if (g.Atr) sp.in(w, g.Atr, (int64_t)(g.K - 1) * g.lda + (g.M - 1));
+    for (int t = 1; t < g.nbt && t < 4; ++t)
+      sp.in(w, g.Bt[t - 1], (int64_t)(g.K - 1) * g.ldb + (g.N - 1));
+    for (int t = 0; t < g.nadd && t < 4; ++t)
+      sp.in(w, g.addp[t], (int64_t)(g.M - 1) * g.ldadd + (g.N - 1));
+    if (g.nbt > 1 || g.nadd > 0) {
+      CHECK(g.coef != nullptr, "%s: coefficients", w);
+      if (g.coef) sp.in(w, g.coef, 7);
+      for (int t = 0; t < 4; ++t)
+        CHECK((t >= g.nbt || (g.bcoef[t] >= 0 && g.bcoef[t] < 8)) &&
+                  (t >= g.nadd || (g.acoef[t] >= 0 && g.acoef[t] < 8)),
+              "%s: coefficient index", w);
+    }
+    if (g.alt1 > 0) {  // outside the batch, same shape, plain, its operands in range
+      CHECK(g.alt1 - 1 >= gb.n && g.alt1 - 1 < kMaxBatch, "%s: alternative index", w);
+      if (g.alt1 - 1 >= gb.n && g.alt1 - 1 < kMaxBatch) {
+        const GemmDesc &a = gb.d[g.alt1 - 1];
+        CHECK(a.M == g.M && a.N == g.N && a.tiles_m == g.tiles_m && a.tiles_n == g.tiles_n &&
+                  a.nat <= 1 && !a.Atr && a.nbt <= 1 && a.nadd == 0 && a.alt1 == 0 && a.K2 == 0,
+              "%s: alternative shape", w);
+        sp.in(w, a.A, a.tA ? (int64_t)(a.K - 1) * a.lda + (a.M - 1)
+                           : (int64_t)(a.M - 1) * a.lda + (a.K - 1));
+        sp.in(w, a.B, a.tB ? (int64_t)(a.K - 1) * a.ldb + (a.N - 1)
+                           : (int64_t)(a.N - 1) * a.ldb + (a.K - 1));
+        sp.in(w, a.C, (int64_t)(a.M - 1) * a.ldc + (a.N - 1));
+      }
+    }
     if (g.epi == EPI_GRADH) {
       CHECK(gb.tile == 64 || g.C, "%s: the 32 x 32 grad_H epilogue stores C", w);
       sp.in(w, g.C2, (int64_t)(g.M - 1) * g.ldc2 + (g.N - 1));
