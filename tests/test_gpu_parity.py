@@ -175,11 +175,14 @@ def test_sweep_minibatch_m512(loss, d):
     c.close()
 
 
-@pytest.mark.parametrize("loss,d,m", [(LOSS_SQUARED, 514, 258), (LOSS_SPHERICAL_SOFTMAX, 516, 300),
-                                      (LOSS_TAYLOR_SOFTMAX, 514, 258)])
+@pytest.mark.parametrize("loss,d,m", [(LOSS_SQUARED, 514, 458), (LOSS_SPHERICAL_SOFTMAX, 516, 460),
+                                      (LOSS_TAYLOR_SOFTMAX, 514, 458), (LOSS_SQUARED, 1022, 258),
+                                      (LOSS_SQUARED, 1000, 300)])
 def test_large_ragged_shapes_on_64_tiles(loss, d, m):
-    # shapes large enough for the LDS-staged 64 x 64 tiles in every launch, with ragged
-    # tile edges; d = 514 and m = 258 are no multiples of 4 (the scalar operand loads)
+    # shapes large enough for the LDS-staged 64 x 64 tiles, with ragged tile edges: m near
+    # 512 puts launches 1 and 3 on them, d near 1024 launches 4 and 5 (with Zq's and R X's
+    # operand terms); d = 514 or 1022 and m = 258 or 458 are no multiples of 4 (the scalar
+    # operand loads)
     K = 3 if loss == LOSS_SQUARED else 1
     w = Workload("t", loss, 20000, d, m, K,
                  value_dist="normal" if loss == LOSS_SQUARED else "ones")
