@@ -212,8 +212,8 @@ int lst_use_graphs(lst_ctx *c, int32_t on);
  * allocates and frees nothing.
  *   m, K         0 <= m <= LST_MAX_M, 0 <= K <= LST_MAX_K, m K <= 8192, and the
  *                step must fit the array: 4 (11 m d + 8 m^2) bytes plus about
- *                4 (m (d + m) / 16 + 8 m K + 13 m) + 19 KiB (with K = 5: m = 128 fits up
- *                to d = 2860, m = 256 up to d = 1288, m = 512 up to d = 361);
+ *                4 (m (d + m) / 16 + 8 m K + 13 m) + 22 KiB (with K = 5: m = 128 fits up
+ *                to d = 2860, m = 256 up to d = 1287, m = 512 up to d = 361);
  *                LST_E_SHAPE beyond it.
  *   status_dev   device int32, set to 0 by the call, then ORed by the kernels with
  *                1 (a target index outside [-1, D)), 2 (the Woodbury matrix is not

@@ -16,13 +16,20 @@ TOL = 1e-4
 
 
 @pytest.mark.parametrize("loss", [LOSS_SQUARED, LOSS_SPHERICAL_SOFTMAX, LOSS_TAYLOR_SOFTMAX,
-                                  "squared_frequent_rows"])
+                                  "squared_frequent_rows", "squared_m512"])
 def test_noalloc_step_matches_lst_step(loss):
+    shapes = None
     if loss == "squared_frequent_rows":
         # six rows targeted by every example: every row is summed in chunks, whose arrival
         # counters sit in the array at another place for each layout
         w = Workload("t", LOSS_SQUARED, 6, 64, 128, 6, lr=1e-3)
         loss = LOSS_SQUARED
+    elif loss == "squared_m512":
+        # m = 512 (the 64 x 64 tiles of launches 1 and 3), then m = 300 (32 x 32 tiles: the
+        # plan and the carve change in the same array), then m = 512 again
+        w = Workload("t", LOSS_SQUARED, 20000, 320, 512, 5)
+        loss = LOSS_SQUARED
+        shapes = [(512, 5), (300, 4), (512, 5)]
     else:
         sq = loss == LOSS_SQUARED
         w = Workload("t", loss, 20000, 256, 128, 5 if sq else 3,
@@ -34,7 +41,7 @@ def test_noalloc_step_matches_lst_step(loss):
     loss_dev = torch.zeros(1, dtype=torch.float32, device=DEV)
     status = torch.full((1,), 99, dtype=torch.int32, device=DEV)
     stream = torch.cuda.current_stream(DEV).cuda_stream
-    for m, K in [(128, w.K), (40, w.K - 1), (128, w.K)]:
+    for m, K in shapes or [(128, w.K), (40, w.K - 1), (128, w.K)]:
         print(f"noalloc step: loss {loss}, m {m}, K {K}", flush=True)
         H, idx, val = s.batch(m)
         idx, val = np.ascontiguousarray(idx[:, :K]), np.ascontiguousarray(val[:, :K])
