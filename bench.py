@@ -250,18 +250,24 @@ def factored_vs_naive(w, dev, seed, steps, naive_steps, profile=False):
 
 def sweep_rows(fsteps, nsteps, emit=None):
     """Factored vs naive over the D x d sweep (squared error, m = 512, K = 5) and the
-    measured crossover (speedup 1, log-linear between the bracketing D) per d."""
+    measured crossover (speedup 1, log-linear between the bracketing D) per d.  The rows
+    of the largest D also carry the per-launch times and the longest launch's roofline."""
     from workloads import sweep_workloads
 
     import torch
 
     dev = torch.device("cuda:0")
     res = []
-    for w in sweep_workloads():
-        r = factored_vs_naive(w, dev, w.D * 7 + w.d, fsteps, nsteps)
+    ws = sweep_workloads()
+    dmax = max(w.D for w in ws)
+    for w in ws:
+        r = factored_vs_naive(w, dev, w.D * 7 + w.d, fsteps, nsteps, profile=w.D == dmax)
         row = {"D": w.D, "d": w.d, "factored_ms": r["factored_ms_per_step"],
                "naive_ms": r["naive_ms_per_step"], "speedup": r["speedup_vs_naive"],
                "D_over_4d": r["D_over_4d"]}
+        if "roofline" in r:
+            row["roofline"] = r["roofline"]
+            row["phases_us"] = r["phases_us"]
         res.append(row)
         if emit:
             emit(row)
