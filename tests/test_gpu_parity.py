@@ -301,8 +301,11 @@ def test_zero_batch_and_no_targets():
     c.close()
 
 
-def test_untouched_rows_bit_identical_and_deterministic():
-    w = Workload("t", LOSS_SQUARED, 20000, 96, 64, 4, index_dist="zipf")
+@pytest.mark.parametrize("d,m", [(96, 64), (1024, 512)])
+def test_untouched_rows_bit_identical_and_deterministic(d, m):
+    # (d = 1024, m = 512: every launch's products on the 64 x 64 tiles, Zq's and R X's
+    # operand terms included)
+    w = Workload("t", LOSS_SQUARED, 20000, d, m, 4, index_dist="zipf")
     s = Stream(w)
     batches = [s.batch() for _ in range(5)]
     outs = []
