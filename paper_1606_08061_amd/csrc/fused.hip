@@ -468,16 +468,16 @@ __global__ __launch_bounds__(256, 4) void step_contract_kernel(
     const float *__restrict__ val, int K, const float *__restrict__ V, int64_t ldv, int64_t D,
     int d, int m, float *__restrict__ tsum) {
   int w = blockIdx.x;
-  // the products on 64 x 64 tiles (large shapes) first: their workgroups are the long
-  // ones, and dispatched after the 16 x 16 tiles they would start only as those end
+  // the products on 32 x 32 or 64 x 64 tiles (large shapes) first: their workgroups are
+  // the long ones, and dispatched after the 16 x 16 tiles they would start only as those
+  // end
   const int gsec = gemm_section(gh, GT);
-  if (GT == 64) {
-    if (w < gsec) {
+  if (w < gsec) {
+    if (GT == 64 || w < gh.total_tiles)
       step_gemm<GT, 4>(pl->gb_contract, gh, H, nullptr, lr, nullptr, w);
-      return;
-    }
-    w -= gsec;
+    return;
   }
+  w -= gsec;
   const int sec = (hd.total + 7) & ~7;
   if (w < sec) {
     const int tile = section_tile(w, hd.total);
@@ -487,13 +487,6 @@ __global__ __launch_bounds__(256, 4) void step_contract_kernel(
     return;
   }
   w -= sec;
-  if (GT != 64) {
-    if (w < gsec) {  // the products on 32 x 32 tiles (large shapes)
-      if (w < gh.total_tiles) step_gemm<GT, 4>(pl->gb_contract, gh, H, nullptr, lr, nullptr, w);
-      return;
-    }
-    w -= gsec;
-  }
   // Prefetch workgroup of example j (XCD j % 8, that of its gather workgroup in
   // launch 2): the indices, then one load per 128-byte line of every target row;
   // also the sum of the example's target weights over its valid slots, in slot order.
@@ -1204,10 +1197,10 @@ __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__re
                                                          const float *dq, const MidArgs ma,
                                                          const CertArgs ca) {
   int w = blockIdx.x;
-  if constexpr (GT == 64) {  // the long workgroups first (as in launch 1)
+  if constexpr (GT != 0) {  // the long workgroups first, as in launch 1
     const int gsec = gemm_section(gh, GT);
     if (w < gsec) {
-      step_gemm<GT, 4>(pl->gb_zgrad, gh, H, gH, lr, nullptr, w);
+      if (GT == 64 || w < gh.total_tiles) step_gemm<GT, 4>(pl->gb_zgrad, gh, H, gH, lr, nullptr, w);
       return;
     }
     w -= gsec;
@@ -1221,14 +1214,6 @@ __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__re
     return;
   }
   w -= sec;
-  if constexpr (GT == 32) {
-    const int gsec = gemm_section(gh, GT);
-    if (w < gsec) {  // the products on 32 x 32 tiles (large shapes)
-      if (w < gh.total_tiles) step_gemm<GT, 4>(pl->gb_zgrad, gh, H, gH, lr, nullptr, w);
-      return;
-    }
-    w -= gsec;
-  }
   const int nyy = (ma.m * ma.m + 255) / 256;
   const int u = w;
   if (u < nyy) {
@@ -1274,18 +1259,17 @@ __global__ __launch_bounds__(256, GT == 64 ? 3 : 4) void step_mid_kernel(const S
                                                        const int *__restrict__ flag, int n,
                                                        const int *__restrict__ idx, int *splan) {
   int w = blockIdx.x;
-  // The U update (k = m): on 64 x 64 tiles first (as in launch 1); on 32 x 32 tiles
-  // after the 16 x 16 tiles, four k-blocks of 8 per wavefront at m = 128, all loaded
-  // before the first product (the launch bound of four workgroups per CU leaves the
-  // registers for that).
+  // The U update (k = m) first, as in launch 1 (on 32 x 32 tiles this saved 0.65 us per
+  // step at m = 128, d = 500 and 3 us at m = 512, d = 256); on 32 x 32 tiles four
+  // k-blocks of 8 per wavefront at m = 128, all loaded before the first product (the
+  // launch bound of four workgroups per CU leaves the registers for that).
   const int gsec = gemm_section(gh, GT);
-  if (GT == 64) {
-    if (w < gsec) {
+  if (w < gsec) {
+    if (GT == 64 || w < gh.total_tiles)
       step_gemm<GT, 4, true>(pl->gb_mid, gh, H, gH, lr, flag, w, cert);
-      return;
-    }
-    w -= gsec;
+    return;
   }
+  w -= gsec;
   const int sec = (hd.total + 7) & ~7;
   if (w < sec) {
     const int tile = section_tile(w, hd.total);
@@ -1296,13 +1280,6 @@ __global__ __launch_bounds__(256, GT == 64 ? 3 : 4) void step_mid_kernel(const S
     return;
   }
   w -= sec;
-  if (GT != 64) {
-    if (w < gsec) {
-      if (w < gh.total_tiles) step_gemm<GT, 4>(pl->gb_mid, gh, H, gH, lr, flag, w);
-      return;
-    }
-    w -= gsec;
-  }
   // the V scatter's plan for launch 5, 16 slots per workgroup
   if (w * 16 < n) scatter_plan(w, n, idx, splan);
 }
