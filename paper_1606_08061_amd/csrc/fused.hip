@@ -1205,16 +1205,18 @@ __global__ __launch_bounds__(256, 4) void step_zgrad_kernel(const StepPlan *__re
     }
     w -= gsec;
   }
-  const int sec = section_by_op(hd);
-  if (w < sec) {
+  // Y^T Y, the loss and the certificate next (a section padded to a multiple of 8, so
+  // that the 16 x 16 tiles' section keeps its XCD alignment)
+  const int nyy = (ma.m * ma.m + 255) / 256;
+  const int nsmall = (nyy + 2 + 7) & ~7;
+  if (w >= nsmall) {
+    w -= nsmall;
     const int tile = tile_by_op(hd, w);
     if (tile < 0) return;
     const TileCtx x{H, gH, lr, dq, nullptr};
     run_op(hd, pl->ob[2].op, tile, x, true);
     return;
   }
-  w -= sec;
-  const int nyy = (ma.m * ma.m + 255) / 256;
   const int u = w;
   if (u < nyy) {
     if (ma.K > 0)
@@ -1646,7 +1648,7 @@ void step_launch_sizes(const StepPlan &pl, int m, int K, int (&grid)[5]) {
   auto gsec = [](const GemmBatch &b) { return gemm_section(gemm_hdr(b), b.tile); };
   grid[0] = sec(pl.ob[0].total) + gsec(pl.gb_contract) + m;
   grid[1] = sec(m) + section_by_op(pl.ob[1]);
-  grid[2] = section_by_op(pl.ob[2]) + gsec(pl.gb_zgrad) + (m * m + 255) / 256 + 2;
+  grid[2] = section_by_op(pl.ob[2]) + gsec(pl.gb_zgrad) + (((m * m + 255) / 256 + 2 + 7) & ~7);
   grid[3] = sec(pl.ob[3].total) + gsec(pl.gb_mid) + (m * K + 15) / 16;
   grid[4] = gsec(pl.gb_update) + m * K;
 }
