@@ -158,6 +158,8 @@ void check_gemm(const Space &sp, const GemmBatch &gb, const char *tag) {
     CHECK(g.C || g.epi == EPI_GRADH, "%s: no output", w);
     if (g.C) sp.in(w, g.C, (int64_t)(g.M - 1) * g.ldc + (g.N - 1));
     if (g.Cin) sp.in(w, g.Cin, (int64_t)(g.M - 1) * g.ldcin + (g.N - 1));
+    // the 32 x 32 body scales by lr only in mode 1
+    CHECK(g.lr_scaled != 2 || gb.tile == 64, "%s: lr scaling mode 2 on 32 x 32 tiles", w);
     // operand terms, addends, alternatives (64 x 64 tiles, one k segment)
     if (g.nat > 1 || g.Atr || g.nbt > 1 || g.nadd > 0 || g.alt1 > 0)
       CHECK(gb.tile == 64 && g.K2 == 0 && g.tA == 0 && g.tB == 1 && g.nat <= 3 && g.nbt <= 4 &&
